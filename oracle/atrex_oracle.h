@@ -1,0 +1,93 @@
+/*
+ * atrex_oracle.h -- plain, slow, single-threaded CPU oracle for the
+ * trace-event -> importance-weight path (paper §3.4 Eq. (2)-(3), §3.6
+ * Eq. (4)-(6)).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may include, link
+ * or call this code: it exists so that the tests, the smoke check and the
+ * benchmark's CPU-baseline leg have an independent answer to compare the GPU
+ * library against.  It shares no header, helper, table or constant generator
+ * with the GPU library; the status values below are restated here on purpose.
+ *
+ * All pointers are HOST pointers.  128-bit integers cross the ABI as two
+ * uint64_t words, low word first ("lohi" arrays hold 2 words per element).
+ *
+ * Fixed-point definition computed here (the paper fixes no numerics; this is
+ * the reading that makes every integer output the floor of an exact rational):
+ *   C        = sum_a c_a                                   (c_a: Q16 card-hours)
+ *   T[a,ph]  = sum of dur over events of app a in phase ph     (Eq. (2), D_a^ph)
+ *   r[a,ph]  = 2^96 * c_a / (C * T[a,ph])                  (p_a / D_a^ph in Q96)
+ *   rho      = floor(log2 r),  m = floor(r * 2^(55 - rho)) in [2^55, 2^56)
+ *              (m = 0, rho = 0 when T = 0 or c_a = 0)
+ *   v_e      = floor(dur_e * m * 2^(rho - 55))   (<= 2^96)
+ *   W[k,ph]  = sum of v_e over events of key k in phase ph (Eq. (3) numerator)
+ *   S[ph]    = sum_k W[k,ph];  weight[k,ph] = RN(W) / RN(S[ph])
+ *   U_i      = (L_P / |Phi_i|) * sum_{ph in Phi_i} sum_{s} W[(i,s),ph],
+ *              L_P = lcm(1..P), Phi_i = phases with >= 1 event of operator i
+ *   w_i      = RN(U_i) / RN(sum_{j retained} U_j)             (Eq. (3))
+ *   S_i      = median of correct S_j of operator i, else 0     (Eq. (5))
+ *   S_agg    = sum_{i retained} w_i * S_i  (Neumaier, ascending op) (Eq. (6))
+ * key = op << 16 | shape; the operator of a key is key >> 16.
+ */
+#ifndef ATREX_ORACLE_H
+#define ATREX_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status values (same numbering as the GPU library's, restated independently). */
+#define ATREX_ORACLE_OK               0
+#define ATREX_ORACLE_E_INVALID_ARG   (-1)
+#define ATREX_ORACLE_E_OUT_OF_RANGE  (-2)
+#define ATREX_ORACLE_E_STATE         (-3)
+
+typedef struct atrex_oracle atrex_oracle;
+
+/* num_phases P in [1,8]; num_apps A >= 1; app_weight_q16[A] with sum > 0. */
+int atrex_oracle_init(uint32_t num_phases, uint32_t num_apps,
+                      const uint32_t *app_weight_q16, atrex_oracle **out);
+
+/* Group-by of n events (n < 2^31).  Exactly once per context.  On error the
+ * context is left as after init.  *num_groups = distinct (key, phase). */
+int atrex_oracle_aggregate_events(atrex_oracle *o, const uint32_t *key,
+                                  const uint32_t *app, const uint8_t *phase,
+                                  const int64_t *dur_ns, uint64_t n,
+                                  uint64_t *num_groups);
+
+/* Groups ascending by (key, phase); arrays sized num_groups (lohi: 2x). */
+int atrex_oracle_phase_normalize(atrex_oracle *o, uint32_t *key, uint8_t *phase,
+                                 uint64_t *count, uint64_t *wsum_lohi,
+                                 uint64_t *raw_ns_lohi /* nullable */,
+                                 double *weight, uint64_t *phase_total_lohi /* [2P] */);
+
+/* Per (app, phase), index a*P + ph: T (lohi), event count, mantissa, exponent. */
+int atrex_oracle_app_totals(const atrex_oracle *o, uint64_t *total_lohi,
+                            uint64_t *count, uint64_t *mant, int32_t *rho);
+
+/* Operators present in the trace, ascending; U (lohi) and w over all of them. */
+int atrex_oracle_num_ops(const atrex_oracle *o, uint64_t *num_ops);
+int atrex_oracle_op_weights(const atrex_oracle *o, uint32_t *op, uint64_t *U_lohi,
+                            double *w);
+
+/* Keys present in the trace, ascending; Eq. (3) at key granularity. */
+int atrex_oracle_num_keys(const atrex_oracle *o, uint64_t *num_keys);
+int atrex_oracle_key_weights(const atrex_oracle *o, uint32_t *key, uint64_t *U_lohi,
+                             double *omega);
+
+/* Eq. (4)-(6).  s[j] is S_j of score_key[j]: NaN = unit not correct,
+ * otherwise it must lie in (0, 1].  Retained operators = those named by
+ * score_key.  Outputs per retained operator (ascending) when non-null. */
+int atrex_oracle_weighted_score(atrex_oracle *o, const uint32_t *score_key,
+                                const double *s, uint64_t n, uint64_t *num_ops,
+                                uint32_t *op, double *op_weight, double *op_score,
+                                double *s_agg);
+
+void atrex_oracle_destroy(atrex_oracle *o);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

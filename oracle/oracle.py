@@ -1,0 +1,177 @@
+"""ctypes binding of the CPU oracle (atrex_oracle.cpp).
+
+TEST INFRASTRUCTURE ONLY: imported by tests/, by the smoke check and by the
+benchmark's CPU-baseline leg.  The product path (the GPU library and its
+binding) never imports it.
+
+``run(...)`` executes the whole path on host arrays -- pass A, scale, pass B,
+per-phase normalisation (§3.4 Eq. (2)-(3)) and, when scores are given, the
+importance-weighted roofline score (§3.6 Eq. (4)-(6)) -- and returns every
+intermediate as numpy arrays.  128-bit integers are returned as (lo, hi)
+uint64 arrays; ``u128_to_int`` turns them into Python ints.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "atrex_oracle.cpp")
+_LIB = os.path.join(_HERE, "libatrex_oracle.so")
+
+OK, E_INVALID_ARG, E_OUT_OF_RANGE, E_STATE = 0, -1, -2, -3
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with g++ (plain C++17, -O2)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", "-Wall",
+                               "-o", tmp, _SRC])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        L = ctypes.CDLL(_LIB)
+        P, U32, U64 = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64
+        L.atrex_oracle_init.argtypes = [U32, U32, P, ctypes.POINTER(P)]
+        L.atrex_oracle_aggregate_events.argtypes = [P, P, P, P, P, U64, P]
+        L.atrex_oracle_phase_normalize.argtypes = [P, P, P, P, P, P, P, P]
+        L.atrex_oracle_app_totals.argtypes = [P, P, P, P, P]
+        L.atrex_oracle_num_ops.argtypes = [P, P]
+        L.atrex_oracle_op_weights.argtypes = [P, P, P, P]
+        L.atrex_oracle_num_keys.argtypes = [P, P]
+        L.atrex_oracle_key_weights.argtypes = [P, P, P, P]
+        L.atrex_oracle_weighted_score.argtypes = [P, P, P, U64, P, P, P, P, P]
+        L.atrex_oracle_destroy.argtypes = [P]
+        for name in ("init", "aggregate_events", "phase_normalize", "app_totals", "num_ops",
+                     "op_weights", "num_keys", "key_weights", "weighted_score"):
+            getattr(L, "atrex_oracle_" + name).restype = ctypes.c_int
+        L.atrex_oracle_destroy.restype = None
+        _lib = L
+    return _lib
+
+
+class OracleError(RuntimeError):
+    def __init__(self, status: int, step: str):
+        super().__init__("oracle %s returned status %d" % (step, status))
+        self.status = status
+        self.step = step
+
+
+def _ptr(a: np.ndarray) -> ctypes.c_void_p:
+    return ctypes.c_void_p(a.ctypes.data) if a.size else ctypes.c_void_p(0)
+
+
+def u128_to_int(lohi: np.ndarray) -> list:
+    """(n, 2) uint64 array of (lo, hi) -> list of Python ints."""
+    a = np.asarray(lohi, dtype=np.uint64).reshape(-1, 2)
+    return [int(lo) | (int(hi) << 64) for lo, hi in a]
+
+
+def run(key, app, phase, dur_ns, app_weight_q16, num_phases, score_key=None, s=None,
+        want_units: bool = True) -> dict:
+    """Run the oracle end to end.  Raises OracleError on a non-OK status."""
+    L = lib()
+    key = np.ascontiguousarray(key, dtype=np.uint32)
+    app = np.ascontiguousarray(app, dtype=np.uint32)
+    phase = np.ascontiguousarray(phase, dtype=np.uint8)
+    dur_ns = np.ascontiguousarray(dur_ns, dtype=np.int64)
+    c = np.ascontiguousarray(app_weight_q16, dtype=np.uint32)
+    n = key.size
+    assert app.size == n and phase.size == n and dur_ns.size == n
+    P, A = int(num_phases), int(c.size)
+    ctx = ctypes.c_void_p()
+    st = L.atrex_oracle_init(P, A, _ptr(c), ctypes.byref(ctx))
+    if st != OK:
+        raise OracleError(st, "init")
+    try:
+        G = ctypes.c_uint64()
+        st = L.atrex_oracle_aggregate_events(ctx, _ptr(key), _ptr(app), _ptr(phase), _ptr(dur_ns),
+                                             n, ctypes.byref(G))
+        if st != OK:
+            raise OracleError(st, "aggregate_events")
+        g = G.value
+        out = {"num_groups": g}
+        out["key"] = np.zeros(g, np.uint32)
+        out["phase"] = np.zeros(g, np.uint8)
+        out["count"] = np.zeros(g, np.uint64)
+        out["wsum"] = np.zeros((g, 2), np.uint64)
+        out["raw_ns"] = np.zeros((g, 2), np.uint64)
+        out["weight"] = np.zeros(g, np.float64)
+        out["phase_total"] = np.zeros((P, 2), np.uint64)
+        AP = A * P
+        out["app_total"] = np.zeros((AP, 2), np.uint64)
+        out["app_count"] = np.zeros(AP, np.uint64)
+        out["mant"] = np.zeros(AP, np.uint64)
+        out["rho"] = np.zeros(AP, np.int32)
+        st = L.atrex_oracle_app_totals(ctx, _ptr(out["app_total"]), _ptr(out["app_count"]),
+                                       _ptr(out["mant"]), _ptr(out["rho"]))
+        if st != OK:
+            raise OracleError(st, "app_totals")
+        st = L.atrex_oracle_phase_normalize(ctx, _ptr(out["key"]), _ptr(out["phase"]),
+                                            _ptr(out["count"]), _ptr(out["wsum"]),
+                                            _ptr(out["raw_ns"]), _ptr(out["weight"]),
+                                            _ptr(out["phase_total"]))
+        if st != OK:
+            raise OracleError(st, "phase_normalize")
+        if want_units:
+            cnt = ctypes.c_uint64()
+            L.atrex_oracle_num_ops(ctx, ctypes.byref(cnt))
+            k = cnt.value
+            out["op"] = np.zeros(k, np.uint32)
+            out["op_U"] = np.zeros((k, 2), np.uint64)
+            out["op_w"] = np.zeros(k, np.float64)
+            if k:
+                L.atrex_oracle_op_weights(ctx, _ptr(out["op"]), _ptr(out["op_U"]), _ptr(out["op_w"]))
+            L.atrex_oracle_num_keys(ctx, ctypes.byref(cnt))
+            k = cnt.value
+            out["ukey"] = np.zeros(k, np.uint32)
+            out["key_U"] = np.zeros((k, 2), np.uint64)
+            out["omega"] = np.zeros(k, np.float64)
+            if k:
+                L.atrex_oracle_key_weights(ctx, _ptr(out["ukey"]), _ptr(out["key_U"]),
+                                           _ptr(out["omega"]))
+        if score_key is not None:
+            sk = np.ascontiguousarray(score_key, dtype=np.uint32)
+            sv = np.ascontiguousarray(s, dtype=np.float64)
+            assert sk.size == sv.size
+            nsc = sk.size
+            nops = ctypes.c_uint64()
+            sc_op = np.zeros(max(nsc, 1), np.uint32)
+            sc_w = np.zeros(max(nsc, 1), np.float64)
+            sc_s = np.zeros(max(nsc, 1), np.float64)
+            sagg = ctypes.c_double()
+            st = L.atrex_oracle_weighted_score(ctx, _ptr(sk), _ptr(sv), nsc, ctypes.byref(nops),
+                                               _ptr(sc_op), _ptr(sc_w), _ptr(sc_s),
+                                               ctypes.byref(sagg))
+            if st != OK:
+                raise OracleError(st, "weighted_score")
+            k = nops.value
+            out["score_op"] = sc_op[:k].copy()
+            out["score_op_weight"] = sc_w[:k].copy()
+            out["score_op_S"] = sc_s[:k].copy()
+            out["s_agg"] = sagg.value
+        return out
+    finally:
+        L.atrex_oracle_destroy(ctx)
+
+
+def status_of(key, app, phase, dur_ns, app_weight_q16, num_phases, score_key=None, s=None) -> int:
+    """Status code of the first failing step (OK when every step succeeds)."""
+    try:
+        run(key, app, phase, dur_ns, app_weight_q16, num_phases, score_key, s, want_units=False)
+    except OracleError as e:
+        return e.status
+    return OK

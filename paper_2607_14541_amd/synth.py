@@ -1,0 +1,224 @@
+"""Seeded synthetic trace generator (inputs only -- no aggregation arithmetic).
+
+The paper's weights come from production inference traces (§3.1, §3.4) that
+are not public; these generators stand in for them with the same structure:
+labelled kernel invocations ``(key = op << 16 | shape, app, phase, dur_ns)``,
+skewed (Zipf) or uniform (operator, shape) popularity, lognormal durations,
+a skewed application card-hour mix (Q16 fixed point), and per-unit roofline
+achievements ``S_j`` for the score.
+
+``CONFIGS`` holds the five workloads: 1M events / 512 keys, 64M / 4096 Zipf(1.1)
+keys, 256M / 1M uniform keys, 1B / 64k Zipf(0.9) keys, and 512M adversarial
+events (99% on one key, durations near 2^40).  Event counts are powers of two.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "csrc", "synth.c")
+_LIB = os.path.join(_HERE, "libatrex_synth.so")
+
+
+class _Cfg(ctypes.Structure):
+    _fields_ = [("seed", ctypes.c_uint64), ("key_mode", ctypes.c_uint32),
+                ("num_ops", ctypes.c_uint32), ("num_shapes", ctypes.c_uint32),
+                ("zipf_n", ctypes.c_uint32), ("shape_bits", ctypes.c_uint32),
+                ("op_base", ctypes.c_uint32), ("tail_n", ctypes.c_uint32),
+                ("hot_p", ctypes.c_double), ("num_phases", ctypes.c_uint32),
+                ("phase0_frac", ctypes.c_double), ("num_apps", ctypes.c_uint32),
+                ("dur_mode", ctypes.c_uint32), ("mu", ctypes.c_double),
+                ("sigma", ctypes.c_double), ("dur_lo", ctypes.c_int64),
+                ("dur_hi", ctypes.c_int64)]
+
+
+CONFIGS = {
+    0: dict(name="1M events, 512 uniform keys, 2 phases, 64 apps", n=1 << 20, seed=0,
+            key_mode=0, num_ops=32, num_shapes=16, num_phases=2, num_apps=64,
+            dur_mode=0, mu=math.log(2e4), sigma=1.5, weights="uniform"),
+    1: dict(name="64M events, 4096 Zipf(1.1) keys, 2 phases 60/40, 1024 apps", n=1 << 26,
+            seed=1, key_mode=1, zipf_n=4096, zipf_s=1.1, shape_bits=6, num_phases=2,
+            phase0_frac=0.6, num_apps=1024, dur_mode=0, mu=math.log(5e4), sigma=2.0,
+            weights="zipf", weights_s=1.1),
+    2: dict(name="256M events, 1M uniform keys, 4 phases, 10k apps", n=1 << 28, seed=2,
+            key_mode=0, num_ops=1024, num_shapes=1024, num_phases=4, num_apps=10000,
+            dur_mode=0, mu=math.log(1e4), sigma=2.5, weights="uniform"),
+    3: dict(name="1B events, 64k Zipf(0.9) keys, 3 phases, 100k apps", n=1 << 30, seed=3,
+            key_mode=1, zipf_n=65536, zipf_s=0.9, shape_bits=8, num_phases=3,
+            num_apps=100000, dur_mode=0, mu=math.log(3e4), sigma=2.0, weights="lognormal"),
+    4: dict(name="512M adversarial events, 99% on one key, durations in [2^39, 2^40]",
+            n=1 << 29, seed=4, key_mode=2, hot_p=0.99, tail_n=1 << 18, shape_bits=10,
+            op_base=1, num_phases=2, num_apps=4, dur_mode=1, dur_lo=1 << 39,
+            dur_hi=1 << 40, weights="uniform"),
+}
+
+
+def build(force: bool = False) -> str:
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-o", tmp, _SRC,
+                               "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _L():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        L = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        L.atrex_synth_events.argtypes = [ctypes.POINTER(_Cfg), P, P, ctypes.c_uint64,
+                                         ctypes.c_uint64, P, P, P, P]
+        L.atrex_synth_events.restype = None
+        L.atrex_synth_u64.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64,
+                                      ctypes.c_uint64, P]
+        L.atrex_synth_u64.restype = None
+        L.atrex_synth_normal.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64, P]
+        L.atrex_synth_normal.restype = None
+        _lib = L
+    return _lib
+
+
+def u64_stream(seed: int, stream: int, n: int, begin: int = 0) -> np.ndarray:
+    out = np.empty(n, np.uint64)
+    if n:
+        _L().atrex_synth_u64(seed, stream, begin, n, out.ctypes.data)
+    return out
+
+
+def normals(seed: int, stream: int, n: int) -> np.ndarray:
+    out = np.empty(n, np.float64)
+    if n:
+        _L().atrex_synth_normal(seed, stream, n, out.ctypes.data)
+    return out
+
+
+def permutation(seed: int, stream: int, n: int) -> np.ndarray:
+    """A fixed pseudo-random permutation of range(n) (sort by random keys)."""
+    return np.argsort(u64_stream(seed, stream, n), kind="stable").astype(np.uint32)
+
+
+def zipf_cdf(n: int, s: float) -> np.ndarray:
+    """Cumulative distribution of P(rank r) proportional to r^-s, r = 1..n."""
+    w = np.arange(1, n + 1, dtype=np.float64) ** (-s)
+    c = np.cumsum(w)
+    c /= c[-1]
+    c[-1] = 1.0
+    return c
+
+
+def _cfg_struct(cfg: dict) -> _Cfg:
+    c = _Cfg()
+    c.seed = cfg["seed"]
+    c.key_mode = cfg["key_mode"]
+    c.num_ops = cfg.get("num_ops", 0)
+    c.num_shapes = cfg.get("num_shapes", 0)
+    c.zipf_n = cfg.get("zipf_n", 0)
+    c.shape_bits = cfg.get("shape_bits", 0)
+    c.op_base = cfg.get("op_base", 0)
+    c.tail_n = cfg.get("tail_n", 0)
+    c.hot_p = cfg.get("hot_p", 0.0)
+    c.num_phases = cfg["num_phases"]
+    c.phase0_frac = cfg.get("phase0_frac", 0.0)
+    c.num_apps = cfg["num_apps"]
+    c.dur_mode = cfg.get("dur_mode", 0)
+    c.mu = cfg.get("mu", 0.0)
+    c.sigma = cfg.get("sigma", 0.0)
+    c.dur_lo = cfg.get("dur_lo", 0)
+    c.dur_hi = cfg.get("dur_hi", 0)
+    return c
+
+
+_tables: dict = {}
+
+
+def _key_tables(cfg: dict):
+    if cfg["key_mode"] != 1:
+        return None, None
+    k = (cfg["seed"], cfg["zipf_n"], cfg["zipf_s"])
+    if k not in _tables:
+        _tables[k] = (zipf_cdf(cfg["zipf_n"], cfg["zipf_s"]),
+                      permutation(cfg["seed"], 100, cfg["zipf_n"]))
+    return _tables[k]
+
+
+def events(cfg: dict, n: int | None = None, begin: int = 0, out: dict | None = None) -> dict:
+    """Events [begin, begin + n) of a workload as numpy arrays.
+
+    ``out`` may supply preallocated arrays (e.g. pinned host buffers) with keys
+    key/app/phase/dur_ns; they are filled in place.
+    """
+    if n is None:
+        n = cfg["n"] - begin
+    if out is None:
+        out = dict(key=np.empty(n, np.uint32), app=np.empty(n, np.uint32),
+                   phase=np.empty(n, np.uint8), dur_ns=np.empty(n, np.int64))
+    for k, dt in (("key", np.uint32), ("app", np.uint32), ("phase", np.uint8),
+                  ("dur_ns", np.int64)):
+        a = out[k]
+        assert a.dtype == dt and a.size >= n and a.flags.c_contiguous
+    cdf, perm = _key_tables(cfg)
+    c = _cfg_struct(cfg)
+    if n:
+        _L().atrex_synth_events(ctypes.byref(c),
+                                cdf.ctypes.data if cdf is not None else None,
+                                perm.ctypes.data if perm is not None else None,
+                                begin, n, out["key"].ctypes.data, out["app"].ctypes.data,
+                                out["phase"].ctypes.data, out["dur_ns"].ctypes.data)
+    return out
+
+
+def app_weights(cfg: dict) -> np.ndarray:
+    """Q16 card-hour weights c_a (uint32), one per application."""
+    A, seed = cfg["num_apps"], cfg["seed"]
+    kind = cfg["weights"]
+    if kind == "uniform":      # round(65536 * U[1, 1000])
+        u = (u64_stream(seed, 200, A) >> np.uint64(11)).astype(np.float64) * 2.0 ** -53
+        c = np.rint(65536.0 * (1.0 + 999.0 * u))
+    elif kind == "zipf":       # max(1, round(65536 * 1000 * rank^-s)), ranks permuted
+        rank = permutation(seed, 201, A).astype(np.float64) + 1.0
+        c = np.maximum(1.0, np.rint(65536.0 * 1000.0 * rank ** (-cfg["weights_s"])))
+    elif kind == "lognormal":  # clamp(round(65536 * exp(N(ln 100, 1))), 1, 2^32 - 1)
+        z = normals(seed, 202, A)
+        c = np.clip(np.rint(65536.0 * np.exp(math.log(100.0) + z)), 1.0, 2.0 ** 32 - 1)
+    else:
+        raise ValueError(kind)
+    return c.astype(np.uint32)
+
+
+def key_space(cfg: dict) -> np.ndarray:
+    """Every (operator, shape) key the workload can emit, ascending."""
+    m = cfg["key_mode"]
+    if m == 0:
+        op = np.repeat(np.arange(cfg["num_ops"], dtype=np.uint32), cfg["num_shapes"])
+        sh = np.tile(np.arange(cfg["num_shapes"], dtype=np.uint32), cfg["num_ops"])
+    elif m == 1:
+        ids = np.arange(cfg["zipf_n"], dtype=np.uint32)
+        op, sh = ids >> np.uint32(cfg["shape_bits"]), ids & np.uint32((1 << cfg["shape_bits"]) - 1)
+    else:
+        ids = np.arange(cfg["tail_n"], dtype=np.uint32)
+        op = np.concatenate([[0], cfg["op_base"] + (ids >> np.uint32(cfg["shape_bits"]))])
+        sh = np.concatenate([[0], ids & np.uint32((1 << cfg["shape_bits"]) - 1)])
+    return np.sort(((op.astype(np.uint32) << np.uint32(16)) | sh.astype(np.uint32)).astype(np.uint32))
+
+
+def scores(cfg: dict, keys: np.ndarray, nan_frac: float = 0.0) -> np.ndarray:
+    """Per-unit roofline achievement S_j ~ U[0.01, 1]; a fraction marked NaN
+    (unit not correct)."""
+    n = keys.size
+    u = (u64_stream(cfg["seed"], 300, n) >> np.uint64(11)).astype(np.float64) * 2.0 ** -53
+    s = 0.01 + 0.99 * u
+    if nan_frac > 0:
+        v = (u64_stream(cfg["seed"], 301, n) >> np.uint64(11)).astype(np.float64) * 2.0 ** -53
+        s[v < nan_frac] = np.nan
+    return s
