@@ -1,0 +1,178 @@
+/*
+ * atrex.h -- C ABI of the MI355X (gfx950) trace-weighting library.
+ *
+ * It turns labelled kernel-invocation events into per-(operator/shape key,
+ * serving phase) importance weights and the importance-weighted roofline
+ * score of the paper:
+ *   - §3.4, Eq. (2): per-(application, phase) device time D_a^phi and per
+ *     (key, phase) device time, summed over every invocation;
+ *   - §3.4, Eq. (3): each invocation's time divided by its application's phase
+ *     total and weighted by the application's card-hour share p_a, averaged
+ *     over the phases the operator runs in, normalised over operators;
+ *   - §3.6, Eq. (4)-(6): per-unit roofline achievement S_j in (0, 1], per
+ *     operator median over correct shapes (0 if none), weighted sum S_agg.
+ *
+ * Numerics (the paper fixes none; every integer output is the floor of an
+ * exact rational, so it is reproducible bit for bit):
+ *   C = sum_a c_a;  T[a,ph] = sum of dur (u128);
+ *   r = 2^96 c_a / (C T),  rho = floor(log2 r),  m = floor(r 2^(55-rho)) in
+ *   [2^55, 2^56)  (m = 0 when T = 0 or c_a = 0);
+ *   v = floor(dur * m * 2^(rho-55)) <= 2^96 per event;  W[k,ph] = sum v (u128);
+ *   S[ph] = sum_k W[k,ph] <= 2^96;  weight = RN(W)/RN(S[ph]) in fp64;
+ *   U_i = (lcm(1..P)/|Phi_i|) sum_{ph in Phi_i} sum_shapes W, Phi_i = phases
+ *   with >= 1 invocation of operator i;  w_i = RN(U_i)/RN(sum_{retained} U).
+ * key = op << 16 | shape; the operator of a key is key >> 16.
+ *
+ * Conventions for every entry point:
+ *   - returns atrex_status (0 = OK, < 0 = error); no exception crosses the ABI;
+ *   - pointers marked DEVICE are HIP device pointers owned by the caller (for
+ *     instance torch tensors); HOST pointers are ordinary host memory;
+ *   - the library allocates no device memory: all scratch space lives in the
+ *     caller's workspace (size from atrex_workspace_bytes);
+ *   - all device work is enqueued on the stream given at init; each call
+ *     synchronises that stream before returning, so device-detected errors
+ *     come back as status codes;
+ *   - a context is not thread-safe; use one context per host thread.
+ * Call order: atrex_aggregate_init -> atrex_aggregate_events (once) ->
+ * atrex_phase_normalize -> atrex_op_weights / atrex_key_weights /
+ * atrex_weighted_score (any number of times) -> atrex_aggregate_destroy.
+ * A call out of order returns ATREX_E_STATE.
+ */
+#ifndef ATREX_H
+#define ATREX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ATREX_OK = 0,
+  ATREX_E_INVALID_ARG = -1,  /* bad parameter, null pointer, P not in [1,8], sum c_a = 0,
+                                duplicate score key, no retained weight */
+  ATREX_E_OUT_OF_RANGE = -2, /* event app >= A, phase >= P or dur < 0; score S not in (0,1] and not NaN */
+  ATREX_E_STATE = -3,        /* call out of order */
+  ATREX_E_CAPACITY = -4,     /* workspace too small, n > max_events, groups > max_groups */
+  ATREX_E_DEVICE = -5        /* a HIP runtime error */
+} atrex_status;
+
+/* Group-by engine for the per-(key, phase) pass.  AUTO picks by capacity;
+ * the others force one engine (all give identical results). */
+typedef enum {
+  ATREX_PATH_AUTO = 0,
+  ATREX_PATH_LDS_HASH = 1,    /* per-workgroup LDS hash table, dense merge */
+  ATREX_PATH_GLOBAL_HASH = 2, /* global hash table with device atomics */
+  ATREX_PATH_RADIX_SORT = 3   /* partition by key digits, then LDS group-by per bucket */
+} atrex_path;
+
+/* Flags for atrex_init_params.flags */
+#define ATREX_FLAG_TIMING 1u /* record per-kernel hipEvent times (atrex_kernel_times) */
+#define ATREX_FLAG_RAW 2u    /* also accumulate the plain device time sum of dur per group */
+
+typedef struct {
+  uint64_t lo, hi; /* value = lo + hi * 2^64 */
+} atrex_u128;
+
+typedef struct atrex_ctx atrex_ctx;
+
+typedef struct {
+  uint32_t num_phases;            /* P in [1, 8] */
+  uint32_t num_apps;              /* A >= 1; event app ids must be < A */
+  const uint32_t *app_weight_q16; /* DEVICE [A]: card-hour weight c_a (Q16); sum must be > 0.
+                                     Read during init only. */
+  uint64_t max_events;            /* largest n passed to aggregate_events; n < 2^31 */
+  uint64_t max_groups;            /* capacity for distinct (key, phase) groups (0: max_events) */
+  uint64_t max_keys;              /* capacity for distinct keys (0: max_groups) */
+  uint64_t max_score;             /* largest n passed to weighted_score (0: max_groups) */
+  atrex_path path;                /* AUTO or a forced engine */
+  void *workspace;                /* DEVICE, caller-owned, 256-byte aligned */
+  size_t workspace_bytes;
+  void *stream;                   /* hipStream_t; NULL = default stream */
+  uint32_t flags;                 /* ATREX_FLAG_* */
+} atrex_init_params;
+
+typedef struct { /* DEVICE struct-of-arrays, caller-owned, read only, borrowed for the call */
+  const uint32_t *key;   /* [n] op << 16 | shape */
+  const uint32_t *app;   /* [n] application id < A */
+  const uint8_t *phase;  /* [n] serving phase < P */
+  const int64_t *dur_ns; /* [n] invocation duration, >= 0 */
+  uint64_t n;            /* n <= max_events, n < 2^31 */
+} atrex_events;
+
+typedef struct {           /* DEVICE outputs, caller-allocated with num_groups rows */
+  uint32_t *key;           /* [G] ascending (key, phase) */
+  uint8_t *phase;          /* [G] */
+  uint64_t *count;         /* [G] invocations */
+  atrex_u128 *wsum;        /* [G] W[k,ph], Q96 */
+  double *weight;          /* [G] RN(W)/RN(S[ph]); each phase sums to 1 */
+  atrex_u128 *phase_total; /* [P] S[ph] */
+  atrex_u128 *raw_ns;      /* [G] or NULL: plain device time sum of dur per group
+                              (requires ATREX_FLAG_RAW at init) */
+} atrex_groups;
+
+/* Workspace size for the given parameters (workspace fields ignored).
+ * HOST: p, bytes.  Fails with ATREX_E_INVALID_ARG on bad parameters. */
+atrex_status atrex_workspace_bytes(const atrex_init_params *p, size_t *bytes);
+
+/* Validates p, computes C = sum c_a on the device and prepares the context.
+ * HOST: p, out.  On error *out is NULL.  Paper: §3.4 (p_a = c_a / C). */
+atrex_status atrex_aggregate_init(const atrex_init_params *p, atrex_ctx **out);
+
+/* Runs the group-by: pass A (Eq. (2), D_a^phi), the per-(app, phase) scale
+ * (Eq. (3), p_a / D_a^phi), pass B (Eq. (2)-(3), per (key, phase) Q96 sums),
+ * and orders the distinct groups.  Exactly once per context; after an error
+ * the context returns to the initialised state.  HOST: ev (struct), num_groups.
+ * Errors: OUT_OF_RANGE for a bad event (no partial results), CAPACITY when
+ * n > max_events or the distinct groups exceed max_groups. */
+atrex_status atrex_aggregate_events(atrex_ctx *ctx, const atrex_events *ev, uint64_t *num_groups);
+
+/* Writes the groups (ascending key, phase) and the per-phase normalised
+ * weights (§3.4, weights normalised within each serving phase), and prepares
+ * Eq. (3) per operator and per key.  HOST: out (struct of DEVICE pointers),
+ * num_ops and num_keys (nullable) receive the number of operators / keys. */
+atrex_status atrex_phase_normalize(atrex_ctx *ctx, const atrex_groups *out, uint64_t *num_ops,
+                                   uint64_t *num_keys);
+
+/* Eq. (3) per operator over every operator in the trace, ascending op:
+ * op [num_ops], U [num_ops] (u128), w [num_ops] (fp64, sums to 1). DEVICE. */
+atrex_status atrex_op_weights(atrex_ctx *ctx, uint32_t *op, atrex_u128 *U, double *w);
+
+/* Eq. (3) at key granularity, ascending key: key, U, omega [num_keys]. DEVICE. */
+atrex_status atrex_key_weights(atrex_ctx *ctx, uint32_t *key, atrex_u128 *U, double *omega);
+
+/* §3.6 Eq. (4)-(6).  score_key [n], s [n] (DEVICE): S_j of each scored
+ * (operator, shape) unit; NaN = not correct, otherwise S_j must be in (0, 1]
+ * (above 1 is an evaluation error, not clipped).  Retained operators = those
+ * named by score_key; w_i is renormalised over them.  Outputs (DEVICE,
+ * nullable, [n] capacity): op, op_weight (w_i), op_score (S_i: median of the
+ * correct S_j, mean of the two middle values for an even count, else 0);
+ * num_ops (HOST, nullable) = retained operators; s_agg (HOST) = sum w_i S_i.
+ * Checks in order: S range (OUT_OF_RANGE), duplicate keys (INVALID_ARG), zero
+ * retained weight (INVALID_ARG).  n <= max_score. */
+atrex_status atrex_weighted_score(atrex_ctx *ctx, const uint32_t *score_key, const double *s,
+                                  uint64_t n, uint32_t *op, double *op_weight, double *op_score,
+                                  uint64_t *num_ops, double *s_agg);
+
+/* Per (app, phase), index a * P + ph (DEVICE, [A*P]): T = D_a^phi (u128);
+ * mant / rho (nullable): the scale m, rho defined above (m = 0: no share). */
+atrex_status atrex_get_app_totals(atrex_ctx *ctx, atrex_u128 *T, uint64_t *mant, int32_t *rho);
+
+/* Per-kernel device times of the last aggregate_events / phase_normalize /
+ * weighted_score call when ATREX_FLAG_TIMING was set (HOST arrays of cap
+ * entries; names point to static strings).  *count = entries written. */
+atrex_status atrex_kernel_times(atrex_ctx *ctx, const char **names, float *ms, uint64_t *items,
+                                int cap, int *count);
+
+/* Name of the engine the last aggregate_events used (static string). */
+const char *atrex_path_used(atrex_ctx *ctx);
+
+atrex_status atrex_aggregate_destroy(atrex_ctx *ctx);
+
+const char *atrex_status_str(atrex_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,275 @@
+"""Python binding of libatrex.so (C ABI in include/atrex.h).
+
+Argument marshalling only: every step of the path runs in the library's gfx950
+kernels.  PyTorch provides device memory (caller-owned tensors, including the
+library's workspace) and the HIP stream.  The library must be built
+(``python -m paper_2607_14541_amd.build``); there is no fallback.
+
+Type mapping: uint32 arrays travel as torch.int32, uint64 and 128-bit (lo, hi)
+pairs as torch.int64 (bit patterns unchanged), fp64 as torch.float64.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libatrex.so")
+
+OK, E_INVALID_ARG, E_OUT_OF_RANGE, E_STATE, E_CAPACITY, E_DEVICE = 0, -1, -2, -3, -4, -5
+PATHS = {"auto": 0, "lds_hash": 1, "global_hash": 2, "radix_sort": 3}
+FLAG_TIMING, FLAG_RAW = 1, 2
+
+
+class AtrexError(RuntimeError):
+    def __init__(self, status: int, call: str):
+        msg = _lib().atrex_status_str(status).decode() if _LIB is not None else str(status)
+        super().__init__("%s failed: %s (%d)" % (call, msg, status))
+        self.status = status
+        self.call = call
+
+
+class _InitParams(ctypes.Structure):
+    _fields_ = [("num_phases", ctypes.c_uint32), ("num_apps", ctypes.c_uint32),
+                ("app_weight_q16", ctypes.c_void_p), ("max_events", ctypes.c_uint64),
+                ("max_groups", ctypes.c_uint64), ("max_keys", ctypes.c_uint64),
+                ("max_score", ctypes.c_uint64), ("path", ctypes.c_int),
+                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+                ("stream", ctypes.c_void_p), ("flags", ctypes.c_uint32)]
+
+
+class _Events(ctypes.Structure):
+    _fields_ = [("key", ctypes.c_void_p), ("app", ctypes.c_void_p), ("phase", ctypes.c_void_p),
+                ("dur_ns", ctypes.c_void_p), ("n", ctypes.c_uint64)]
+
+
+class _Groups(ctypes.Structure):
+    _fields_ = [("key", ctypes.c_void_p), ("phase", ctypes.c_void_p), ("count", ctypes.c_void_p),
+                ("wsum", ctypes.c_void_p), ("weight", ctypes.c_void_p),
+                ("phase_total", ctypes.c_void_p), ("raw_ns", ctypes.c_void_p)]
+
+
+_LIB = None
+
+
+def _lib() -> ctypes.CDLL:
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libatrex.so is not built (%s); run: python -m paper_2607_14541_amd.build"
+                               % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        P, U64, I = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int
+        sigs = {
+            "atrex_workspace_bytes": [ctypes.POINTER(_InitParams), ctypes.POINTER(ctypes.c_size_t)],
+            "atrex_aggregate_init": [ctypes.POINTER(_InitParams), ctypes.POINTER(P)],
+            "atrex_aggregate_events": [P, ctypes.POINTER(_Events), ctypes.POINTER(U64)],
+            "atrex_phase_normalize": [P, ctypes.POINTER(_Groups), ctypes.POINTER(U64), ctypes.POINTER(U64)],
+            "atrex_op_weights": [P, P, P, P],
+            "atrex_key_weights": [P, P, P, P],
+            "atrex_weighted_score": [P, P, P, U64, P, P, P, ctypes.POINTER(U64),
+                                     ctypes.POINTER(ctypes.c_double)],
+            "atrex_get_app_totals": [P, P, P, P],
+            "atrex_kernel_times": [P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float),
+                                   ctypes.POINTER(U64), I, ctypes.POINTER(I)],
+            "atrex_aggregate_destroy": [P],
+        }
+        for name, args in sigs.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = ctypes.c_int
+        L.atrex_status_str.argtypes = [ctypes.c_int]
+        L.atrex_status_str.restype = ctypes.c_char_p
+        L.atrex_path_used.argtypes = [P]
+        L.atrex_path_used.restype = ctypes.c_char_p
+        _LIB = L
+    return _LIB
+
+
+def _ptr(t) -> ctypes.c_void_p:
+    return ctypes.c_void_p(t.data_ptr()) if t is not None and t.numel() else ctypes.c_void_p(0)
+
+
+def _check(st: int, call: str) -> None:
+    if st != OK:
+        raise AtrexError(st, call)
+
+
+def _dev(t: torch.Tensor, dtype: torch.dtype, name: str) -> torch.Tensor:
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    return t.contiguous()
+
+
+def _as_i32(t: torch.Tensor) -> torch.Tensor:
+    """uint32 data as int32 bits."""
+    if t.dtype == torch.int32:
+        return t
+    if t.dtype == getattr(torch, "uint32", None):
+        return t.view(torch.int32)
+    if t.dtype == torch.int64:
+        return t.to(torch.int32)  # callers pass values < 2^31 here
+    raise TypeError("expected 32-bit integer tensor, got %s" % t.dtype)
+
+
+class Aggregator:
+    """One aggregation context: init -> aggregate -> normalize -> weights/score."""
+
+    def __init__(self, num_phases: int, app_weight_q16: torch.Tensor, max_events: int,
+                 max_groups: int = 0, max_keys: int = 0, max_score: int = 0, path: str = "auto",
+                 timing: bool = False, raw: bool = False, stream: torch.cuda.Stream | None = None):
+        L = _lib()
+        c = _dev(_as_i32(app_weight_q16), torch.int32, "app_weight_q16")
+        self.device = c.device
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        self.P, self.A = int(num_phases), int(c.numel())
+        self.raw = raw
+        p = _InitParams()
+        p.num_phases, p.num_apps = self.P, self.A
+        p.app_weight_q16 = c.data_ptr()
+        p.max_events, p.max_groups, p.max_keys, p.max_score = max_events, max_groups, max_keys, max_score
+        p.path = PATHS[path]
+        p.stream = self.stream.cuda_stream
+        p.flags = (FLAG_TIMING if timing else 0) | (FLAG_RAW if raw else 0)
+        nbytes = ctypes.c_size_t()
+        _check(L.atrex_workspace_bytes(ctypes.byref(p), ctypes.byref(nbytes)), "atrex_workspace_bytes")
+        self.workspace = torch.empty(max(int(nbytes.value), 256), dtype=torch.uint8, device=self.device)
+        p.workspace, p.workspace_bytes = self.workspace.data_ptr(), self.workspace.numel()
+        self._app_weight = c
+        ctx = ctypes.c_void_p()
+        _check(L.atrex_aggregate_init(ctypes.byref(p), ctypes.byref(ctx)), "atrex_aggregate_init")
+        self._ctx = ctx
+        self.num_groups = None
+        self.num_ops = self.num_keys = None
+
+    # -- Eq. (2)-(3) group-by ---------------------------------------------------------
+    def aggregate(self, key: torch.Tensor, app: torch.Tensor, phase: torch.Tensor,
+                  dur_ns: torch.Tensor) -> int:
+        key = _dev(_as_i32(key), torch.int32, "key")
+        app = _dev(_as_i32(app), torch.int32, "app")
+        phase = _dev(phase, torch.uint8, "phase")
+        dur_ns = _dev(dur_ns, torch.int64, "dur_ns")
+        n = key.numel()
+        if not (app.numel() == n and phase.numel() == n and dur_ns.numel() == n):
+            raise ValueError("event arrays differ in length")
+        self._events = (key, app, phase, dur_ns)  # keep alive for the call
+        ev = _Events(_ptr(key), _ptr(app), _ptr(phase), _ptr(dur_ns), n)
+        G = ctypes.c_uint64()
+        _check(_lib().atrex_aggregate_events(self._ctx, ctypes.byref(ev), ctypes.byref(G)),
+               "atrex_aggregate_events")
+        self._events = None
+        self.num_groups = G.value
+        return self.num_groups
+
+    def normalize(self) -> dict:
+        G, dev = self.num_groups, self.device
+        out = dict(key=torch.empty(G, dtype=torch.int32, device=dev),
+                   phase=torch.empty(G, dtype=torch.uint8, device=dev),
+                   count=torch.empty(G, dtype=torch.int64, device=dev),
+                   wsum=torch.empty((G, 2), dtype=torch.int64, device=dev),
+                   weight=torch.empty(G, dtype=torch.float64, device=dev),
+                   phase_total=torch.empty((self.P, 2), dtype=torch.int64, device=dev))
+        if self.raw:
+            out["raw_ns"] = torch.empty((G, 2), dtype=torch.int64, device=dev)
+        g = _Groups(_ptr(out["key"]), _ptr(out["phase"]), _ptr(out["count"]), _ptr(out["wsum"]),
+                    _ptr(out["weight"]), _ptr(out["phase_total"]), _ptr(out.get("raw_ns")))
+        nops, nkeys = ctypes.c_uint64(), ctypes.c_uint64()
+        _check(_lib().atrex_phase_normalize(self._ctx, ctypes.byref(g), ctypes.byref(nops),
+                                            ctypes.byref(nkeys)), "atrex_phase_normalize")
+        self.num_ops, self.num_keys = nops.value, nkeys.value
+        return out
+
+    def op_weights(self) -> dict:
+        k, dev = self.num_ops, self.device
+        op = torch.empty(k, dtype=torch.int32, device=dev)
+        U = torch.empty((k, 2), dtype=torch.int64, device=dev)
+        w = torch.empty(k, dtype=torch.float64, device=dev)
+        _check(_lib().atrex_op_weights(self._ctx, _ptr(op), _ptr(U), _ptr(w)), "atrex_op_weights")
+        return dict(op=op, U=U, w=w)
+
+    def key_weights(self) -> dict:
+        k, dev = self.num_keys, self.device
+        key = torch.empty(k, dtype=torch.int32, device=dev)
+        U = torch.empty((k, 2), dtype=torch.int64, device=dev)
+        w = torch.empty(k, dtype=torch.float64, device=dev)
+        _check(_lib().atrex_key_weights(self._ctx, _ptr(key), _ptr(U), _ptr(w)), "atrex_key_weights")
+        return dict(key=key, U=U, omega=w)
+
+    # -- Eq. (4)-(6) ---------------------------------------------------------------------
+    def score(self, score_key: torch.Tensor, s: torch.Tensor) -> dict:
+        score_key = _dev(_as_i32(score_key), torch.int32, "score_key")
+        s = _dev(s, torch.float64, "s")
+        n = score_key.numel()
+        if s.numel() != n:
+            raise ValueError("score_key and s differ in length")
+        dev = self.device
+        op = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
+        ow = torch.empty(max(n, 1), dtype=torch.float64, device=dev)
+        osc = torch.empty(max(n, 1), dtype=torch.float64, device=dev)
+        nops = ctypes.c_uint64()
+        sagg = ctypes.c_double()
+        _check(_lib().atrex_weighted_score(self._ctx, _ptr(score_key), _ptr(s), n, _ptr(op), _ptr(ow),
+                                           _ptr(osc), ctypes.byref(nops), ctypes.byref(sagg)),
+               "atrex_weighted_score")
+        k = nops.value
+        return dict(s_agg=sagg.value, op=op[:k], op_weight=ow[:k], op_score=osc[:k])
+
+    # -- inspection ------------------------------------------------------------------------
+    def app_totals(self) -> dict:
+        GA, dev = self.A * self.P, self.device
+        T = torch.empty((GA, 2), dtype=torch.int64, device=dev)
+        m = torch.empty(GA, dtype=torch.int64, device=dev)
+        r = torch.empty(GA, dtype=torch.int32, device=dev)
+        _check(_lib().atrex_get_app_totals(self._ctx, _ptr(T), _ptr(m), _ptr(r)), "atrex_get_app_totals")
+        return dict(T=T, mant=m, rho=r)
+
+    def kernel_times(self) -> list:
+        cap = 64
+        names = (ctypes.c_char_p * cap)()
+        ms = (ctypes.c_float * cap)()
+        items = (ctypes.c_uint64 * cap)()
+        cnt = ctypes.c_int()
+        _check(_lib().atrex_kernel_times(self._ctx, names, ms, items, cap, ctypes.byref(cnt)),
+               "atrex_kernel_times")
+        return [(names[i].decode(), float(ms[i]), int(items[i])) for i in range(cnt.value)]
+
+    def path_used(self) -> str:
+        return _lib().atrex_path_used(self._ctx).decode()
+
+    def close(self) -> None:
+        if getattr(self, "_ctx", None):
+            _lib().atrex_aggregate_destroy(self._ctx)
+            self._ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def aggregate(key, app, phase, dur_ns, app_weight_q16, num_phases, path="auto", raw=False,
+              score_key=None, s=None, max_groups=0, max_keys=0) -> dict:
+    """Whole path in one call: returns groups, per-op and per-key weights, and
+    the score when (score_key, s) are given."""
+    n = key.numel()
+    nsc = score_key.numel() if score_key is not None else 0
+    ag = Aggregator(num_phases, app_weight_q16, max_events=max(n, 1), max_groups=max_groups,
+                    max_keys=max_keys, max_score=max(nsc, 1) if nsc else 0, path=path, raw=raw)
+    try:
+        ag.aggregate(key, app, phase, dur_ns)
+        out = ag.normalize()
+        out.update({"op_" + k if k != "op" else k: v for k, v in ag.op_weights().items()})
+        kw = ag.key_weights()
+        out.update(ukey=kw["key"], key_U=kw["U"], omega=kw["omega"])
+        out.update({"app_" + k: v for k, v in ag.app_totals().items()})
+        out["path"] = ag.path_used()
+        if score_key is not None:
+            out.update({"score_" + k if k != "s_agg" else k: v for k, v in ag.score(score_key, s).items()})
+        return out
+    finally:
+        ag.close()

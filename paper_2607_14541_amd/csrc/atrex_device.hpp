@@ -1,0 +1,106 @@
+// atrex_device.hpp -- device helpers shared by the gfx950 kernels.
+//
+// Fixed-point conventions (see include/atrex.h):
+//   scale word per (app, phase): 0 = no share, else
+//     bits 56..63 = rho + 64 (rho in [-63, 96]), bits 0..54 = m - 2^55,
+//     m in [2^55, 2^56) the truncated mantissa of r = 2^96 c_a / (C T).
+//   per-event share v = floor(dur * m * 2^(rho - 55)) <= 2^96  (Eq. (3) term
+//   p_a * d / D_a^phi in Q96).
+//   A (key, phase) accumulator is two 64-bit words:
+//     lo = (sum v) mod 2^64,
+//     hi = floor(sum v / 2^64) + count * 2^33   (floor(...) <= 2^32 because the
+//          shares of one phase sum to at most 2^96; count < 2^31).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef unsigned __int128 u128;
+
+#define ATREX_EMPTY_KEY 0xFFFFFFFFu  // LDS tag of a free slot
+#define ATREX_COUNT_SHIFT 33
+#define ATREX_MANT_BITS 56
+
+// --- scale word -----------------------------------------------------------
+__device__ __forceinline__ uint64_t scale_pack(uint64_t m, int rho) {
+  return ((uint64_t)(rho + 64) << 56) | (m - ((uint64_t)1 << (ATREX_MANT_BITS - 1)));
+}
+
+// v = floor(d * m * 2^(rho - 55)); exact because the product fits in 119 bits
+// and the true value is at most 2^96.
+__device__ __forceinline__ u128 event_share(uint64_t d, uint64_t sw) {
+  if (sw == 0) return 0;
+  const uint64_t m = (sw & (((uint64_t)1 << 55) - 1)) | ((uint64_t)1 << 55);
+  const int sh = (int)(sw >> 56) - 64 - (ATREX_MANT_BITS - 1);
+  const u128 p = (u128)d * m;
+  return sh >= 0 ? (p << sh) : (p >> (-sh));
+}
+
+// --- u128 -> fp64, round to nearest, ties to even (IEEE 754 conversion) -----
+__device__ __forceinline__ double u128_to_f64(u128 x) {
+  const uint64_t hi = (uint64_t)(x >> 64);
+  if (hi == 0) {
+    const uint64_t lo = (uint64_t)x;
+    if ((lo >> 53) == 0) return (double)lo;  // exact
+  }
+  // leading one at bit (nb - 1), nb > 53: keep 53 bits, round the rest.
+  const int nb = hi ? 128 - __clzll(hi) : 64 - __clzll((uint64_t)x);
+  const int sh = nb - 53;
+  uint64_t mant = (uint64_t)(x >> sh);
+  const u128 rem = x & (((u128)1 << sh) - 1);
+  const u128 half = (u128)1 << (sh - 1);
+  if (rem > half || (rem == half && (mant & 1))) ++mant;
+  return ldexp((double)mant, sh);  // mant <= 2^53: exact, then exact scaling
+}
+
+// --- hashing ----------------------------------------------------------------
+__device__ __forceinline__ uint32_t hash32(uint32_t k) {
+  k ^= k >> 16;
+  k *= 0x7feb352dU;
+  k ^= k >> 15;
+  k *= 0x846ca68bU;
+  k ^= k >> 16;
+  return k;
+}
+
+// --- wave helpers (wave64) -------------------------------------------------------
+__device__ __forceinline__ uint64_t u128_lo(u128 x) { return (uint64_t)x; }
+__device__ __forceinline__ uint64_t u128_hi(u128 x) { return (uint64_t)(x >> 64); }
+__device__ __forceinline__ u128 make_u128(uint64_t lo, uint64_t hi) {
+  return ((u128)hi << 64) | lo;
+}
+
+__device__ __forceinline__ u128 shfl_down_u128(u128 v, int d) {
+  const uint64_t lo = __shfl_down((unsigned long long)(uint64_t)v, d, 64);
+  const uint64_t hi = __shfl_down((unsigned long long)(uint64_t)(v >> 64), d, 64);
+  return make_u128(lo, hi);
+}
+
+__device__ __forceinline__ u128 wave_sum_u128(u128 v) {
+  for (int d = 32; d >= 1; d >>= 1) v += shfl_down_u128(v, d);
+  return v;  // valid in lane 0
+}
+
+// Accumulate a share into a two-word accumulator (global or LDS) with
+// 64-bit atomics: the low word's carry is detected from the returned value.
+template <typename Ptr>
+__device__ __forceinline__ void acc_add(Ptr lo, Ptr hi, u128 v) {
+  const unsigned long long vlo = (unsigned long long)(uint64_t)v;
+  const unsigned long long old = atomicAdd(lo, vlo);
+  const unsigned long long carry = (old + vlo < old) ? 1ull : 0ull;
+  atomicAdd(hi, (unsigned long long)(uint64_t)(v >> 64) + carry + (1ull << ATREX_COUNT_SHIFT));
+}
+
+// Plain (count-free) 128-bit accumulation, e.g. raw device time.
+template <typename Ptr>
+__device__ __forceinline__ void acc_add_plain(Ptr lo, Ptr hi, u128 v) {
+  const unsigned long long vlo = (unsigned long long)(uint64_t)v;
+  const unsigned long long old = atomicAdd(lo, vlo);
+  const unsigned long long carry = (old + vlo < old) ? 1ull : 0ull;
+  const unsigned long long vhi = (unsigned long long)(uint64_t)(v >> 64) + carry;
+  if (vhi) atomicAdd(hi, vhi);
+}
+
+// Error bits of the device error word.
+#define ATREX_ERRBIT_RANGE 1u
+#define ATREX_ERRBIT_CAPACITY 2u
+#define ATREX_ERRBIT_DUP 4u

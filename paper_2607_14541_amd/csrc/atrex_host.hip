@@ -1,0 +1,586 @@
+// atrex_host.hip -- host side of the C ABI declared in include/atrex.h:
+// parameter checks, workspace layout, kernel sequencing on the caller's
+// stream, device error word readback, optional per-kernel hipEvent timing.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/atrex.h"
+#include "atrex_kernels.h"
+
+#define ATREX_ERRBIT_RANGE 1u
+#define ATREX_ERRBIT_CAPACITY 2u
+#define ATREX_ERRBIT_DUP 4u
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr size_t kLdsBytes = 160 * 1024;
+constexpr uint32_t kPassAThreads = 512;
+constexpr uint64_t kPartialRowsMax = 2048;  // pass-A workgroups with private partial rows
+constexpr uint32_t kMaxTimed = 64;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+uint64_t next_pow2(uint64_t x) {
+  uint64_t p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+// Byte offsets of every workspace region (all 256-byte aligned).
+struct Layout {
+  size_t ctrl, T, carryA, partA, scale, dict, acc, raw;
+  size_t sk[3], sv[3], rs_tmp, scan_tmp;
+  size_t g_key, g_ph, g_cnt, g_w, g_raw, S;
+  size_t flags, scan, starts;
+  size_t op_id, op_U, op_w, key_id, key_U, key_w;
+  size_t r_op, r_U, r_S, partials, total;
+  size_t bytes;
+  uint64_t capD, maxG, maxK, maxS, maxSort, maxOps, partA_rows;
+};
+
+struct Params {
+  uint32_t P, A;
+  uint64_t max_events, max_groups, max_keys, max_score;
+  bool raw;
+};
+
+bool pass_a_fits_lds(uint64_t G_A) { return G_A * 8 <= kLdsBytes - 1024; }
+
+Layout make_layout(const Params& p) {
+  Layout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += align_up(bytes ? bytes : 1);
+    return at;
+  };
+  const uint64_t GA = (uint64_t)p.A * p.P;
+  L.maxG = p.max_groups;
+  L.maxK = p.max_keys;
+  L.maxS = p.max_score;
+  L.maxSort = std::max<uint64_t>(std::max<uint64_t>(L.maxG, L.maxS), 1);
+  L.capD = next_pow2(std::max<uint64_t>(1024, 2 * L.maxK));
+  L.maxOps = std::min<uint64_t>(L.maxG, 65536);
+  L.partA_rows = pass_a_fits_lds(GA) ? kPartialRowsMax : 0;
+  L.ctrl = take(4096);
+  L.T = take(GA * 16);
+  L.carryA = take(GA * 8);
+  L.partA = take(L.partA_rows * GA * 8);
+  L.scale = take(GA * 8);
+  L.dict = take(L.capD * 8);
+  L.acc = take(L.capD * p.P * 16);
+  L.raw = take(p.raw ? L.capD * p.P * 16 : 0);
+  for (int i = 0; i < 3; ++i) {
+    L.sk[i] = take(L.maxSort * 8);
+    L.sv[i] = take(L.maxSort * 4);
+  }
+  L.rs_tmp = take(radix_sort_tmp_bytes(L.maxSort));
+  L.scan_tmp = take(scan_tmp_bytes(L.maxSort + 1));
+  L.g_key = take(L.maxG * 4);
+  L.g_ph = take(L.maxG);
+  L.g_cnt = take(L.maxG * 8);
+  L.g_w = take(L.maxG * 16);
+  L.g_raw = take(p.raw ? L.maxG * 16 : 0);
+  L.S = take(8 * 16);
+  L.flags = take((L.maxSort + 1) * 4);
+  L.scan = take((L.maxSort + 1) * 4);
+  L.starts = take((L.maxSort + 2) * 4);
+  L.op_id = take(L.maxOps * 4);
+  L.op_U = take(L.maxOps * 16);
+  L.op_w = take(L.maxOps * 8);
+  L.key_id = take(L.maxG * 4);
+  L.key_U = take(L.maxG * 16);
+  L.key_w = take(L.maxG * 8);
+  L.r_op = take(L.maxS * 4);
+  L.r_U = take(L.maxS * 16);
+  L.r_S = take(L.maxS * 8);
+  L.partials = take(1024 * 8 * 16);
+  L.total = take(64);
+  L.bytes = off;
+  return L;
+}
+
+atrex_status check_params(const atrex_init_params* ip, Params* out) {
+  if (!ip) return ATREX_E_INVALID_ARG;
+  if (ip->num_phases < 1 || ip->num_phases > 8 || ip->num_apps < 1) return ATREX_E_INVALID_ARG;
+  if (ip->max_events >= (1ull << 31)) return ATREX_E_INVALID_ARG;
+  if ((uint64_t)ip->num_apps * ip->num_phases >= (1ull << 32)) return ATREX_E_INVALID_ARG;
+  if ((unsigned)ip->path > (unsigned)ATREX_PATH_RADIX_SORT) return ATREX_E_INVALID_ARG;
+  Params p;
+  p.P = ip->num_phases;
+  p.A = ip->num_apps;
+  p.max_events = ip->max_events;
+  p.max_groups = ip->max_groups ? ip->max_groups : std::max<uint64_t>(ip->max_events, 1);
+  p.max_keys = ip->max_keys ? ip->max_keys : p.max_groups;
+  p.max_score = ip->max_score ? ip->max_score : p.max_groups;
+  if (p.max_groups >= (1ull << 32) || p.max_score >= (1ull << 31) || p.max_keys >= (1ull << 31))
+    return ATREX_E_INVALID_ARG;
+  p.raw = (ip->flags & ATREX_FLAG_RAW) != 0;
+  *out = p;
+  return ATREX_OK;
+}
+
+struct Timed {
+  const char* name;
+  uint64_t items;
+  hipEvent_t a, b;
+};
+
+uint64_t lcm_1_to(uint32_t P) {
+  uint64_t l = 1;
+  for (uint64_t k = 2; k <= P; ++k) {
+    uint64_t a = l, b = k;
+    while (b) {
+      const uint64_t t = a % b;
+      a = b;
+      b = t;
+    }
+    l = l / a * k;
+  }
+  return l;
+}
+
+}  // namespace
+
+struct atrex_ctx {
+  Params p;
+  Layout L;
+  char* ws;
+  hipStream_t s;
+  atrex_path path;
+  uint32_t flags;
+  const uint32_t* app_weight;
+  int state;  // 0 initialised, 1 aggregated, 2 normalised
+  uint64_t G, nops, nkeys;
+  int cus;
+  const char* path_used;
+  std::vector<Timed> timed;
+  size_t ntimed;
+  std::vector<float> last_ms;
+  std::vector<const char*> last_names;
+  std::vector<uint64_t> last_items;
+
+  template <class T>
+  T* at(size_t off) const {
+    return reinterpret_cast<T*>(ws + off);
+  }
+  uint32_t* err() const { return at<uint32_t>(L.ctrl); }
+  unsigned long long* counter() const { return at<unsigned long long>(L.ctrl + 64); }
+  uint64_t* Csum() const { return at<uint64_t>(L.ctrl + 128); }
+  double* sagg() const { return at<double>(L.ctrl + 192); }
+  GroupTables tables() const {
+    GroupTables gt;
+    gt.dict = at<unsigned long long>(L.dict);
+    gt.dict_mask = (uint32_t)(L.capD - 1);
+    gt.acc = at<unsigned long long>(L.acc);
+    gt.raw = p.raw ? at<unsigned long long>(L.raw) : nullptr;
+    return gt;
+  }
+  SortedGroups groups() const {
+    SortedGroups g;
+    g.key = at<uint32_t>(L.g_key);
+    g.phase = at<uint8_t>(L.g_ph);
+    g.count = at<uint64_t>(L.g_cnt);
+    g.wsum = at<uint64_t>(L.g_w);
+    g.raw = p.raw ? at<uint64_t>(L.g_raw) : nullptr;
+    return g;
+  }
+  // timing helpers
+  void begin_call() { ntimed = 0; }
+  int tstart(const char* name, uint64_t items) {
+    if (!(flags & ATREX_FLAG_TIMING) || ntimed >= timed.size()) return -1;
+    Timed& t = timed[ntimed];
+    t.name = name;
+    t.items = items;
+    (void)hipEventRecord(t.a, s);
+    return (int)ntimed++;
+  }
+  void tstop(int i) {
+    if (i >= 0) (void)hipEventRecord(timed[i].b, s);
+  }
+  void end_call() {
+    if (!(flags & ATREX_FLAG_TIMING)) return;
+    last_ms.clear();
+    last_names.clear();
+    last_items.clear();
+    for (size_t i = 0; i < ntimed; ++i) {
+      float ms = 0.f;
+      (void)hipEventElapsedTime(&ms, timed[i].a, timed[i].b);
+      last_ms.push_back(ms);
+      last_names.push_back(timed[i].name);
+      last_items.push_back(timed[i].items);
+    }
+  }
+};
+
+namespace {
+
+atrex_status sync_status(atrex_ctx* c) {
+  const hipError_t e1 = hipGetLastError();
+  const hipError_t e2 = hipStreamSynchronize(c->s);
+  return (e1 == hipSuccess && e2 == hipSuccess) ? ATREX_OK : ATREX_E_DEVICE;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+#define TIMED(ctx, name, items, stmt) \
+  do {                                \
+    const int t_ = (ctx)->tstart(name, items); \
+    stmt;                             \
+    (ctx)->tstop(t_);                 \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+const char* atrex_status_str(atrex_status s) {
+  switch (s) {
+    case ATREX_OK: return "ok";
+    case ATREX_E_INVALID_ARG: return "invalid argument";
+    case ATREX_E_OUT_OF_RANGE: return "value out of range";
+    case ATREX_E_STATE: return "call out of order";
+    case ATREX_E_CAPACITY: return "capacity exceeded";
+    case ATREX_E_DEVICE: return "HIP device error";
+  }
+  return "unknown status";
+}
+
+atrex_status atrex_workspace_bytes(const atrex_init_params* ip, size_t* bytes) {
+  if (!bytes) return ATREX_E_INVALID_ARG;
+  Params p;
+  const atrex_status st = check_params(ip, &p);
+  if (st != ATREX_OK) return st;
+  *bytes = make_layout(p).bytes;
+  return ATREX_OK;
+}
+
+atrex_status atrex_aggregate_init(const atrex_init_params* ip, atrex_ctx** out) {
+  if (!out) return ATREX_E_INVALID_ARG;
+  *out = nullptr;
+  Params p;
+  atrex_status st = check_params(ip, &p);
+  if (st != ATREX_OK) return st;
+  if (!ip->app_weight_q16 || !ip->workspace || !aligned(ip->workspace, kAlign)) return ATREX_E_INVALID_ARG;
+  const Layout L = make_layout(p);
+  if (ip->workspace_bytes < L.bytes) return ATREX_E_CAPACITY;
+  static bool smem_set = false;
+  if (!smem_set) {
+    if (set_kernel_smem_limits() != hipSuccess) return ATREX_E_DEVICE;
+    smem_set = true;
+  }
+  atrex_ctx* c = new (std::nothrow) atrex_ctx();
+  if (!c) return ATREX_E_INVALID_ARG;
+  c->p = p;
+  c->L = L;
+  c->ws = (char*)ip->workspace;
+  c->s = (hipStream_t)ip->stream;
+  c->path = ip->path;
+  c->flags = ip->flags;
+  c->app_weight = ip->app_weight_q16;
+  c->state = 0;
+  c->G = c->nops = c->nkeys = 0;
+  c->path_used = "none";
+  c->ntimed = 0;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&c->cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+    delete c;
+    return ATREX_E_DEVICE;
+  }
+  if (c->flags & ATREX_FLAG_TIMING) {
+    c->timed.resize(kMaxTimed);
+    for (auto& t : c->timed) {
+      if (hipEventCreate(&t.a) != hipSuccess || hipEventCreate(&t.b) != hipSuccess) {
+        delete c;
+        return ATREX_E_DEVICE;
+      }
+    }
+  }
+  // C = sum_a c_a, checked > 0 (p_a = c_a / C must exist)
+  launch_sum_u32(c->s, c->app_weight, p.A, c->Csum());
+  uint64_t C = 0;
+  (void)hipMemcpyAsync(&C, c->Csum(), 8, hipMemcpyDeviceToHost, c->s);
+  st = sync_status(c);
+  if (st == ATREX_OK && C == 0) st = ATREX_E_INVALID_ARG;
+  if (st != ATREX_OK) {
+    atrex_aggregate_destroy(c);
+    return st;
+  }
+  *out = c;
+  return ATREX_OK;
+}
+
+atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64_t* num_groups) {
+  if (!c || !ev || !num_groups) return ATREX_E_INVALID_ARG;
+  if (c->state != 0) return ATREX_E_STATE;
+  const uint64_t n = ev->n;
+  if (n > c->p.max_events) return ATREX_E_CAPACITY;
+  if (n > 0 && (!ev->key || !ev->app || !ev->phase || !ev->dur_ns)) return ATREX_E_INVALID_ARG;
+  const uint32_t P = c->p.P, A = c->p.A;
+  const uint64_t GA = (uint64_t)A * P;
+  const Layout& L = c->L;
+  hipStream_t s = c->s;
+  c->begin_call();
+  EventsDev d;
+  d.key = ev->key;
+  d.app = ev->app;
+  d.phase = ev->phase;
+  d.dur = ev->dur_ns;
+  d.n = n;
+  const bool vec_ok = aligned(ev->key, 16) && aligned(ev->app, 16) && aligned(ev->phase, 4) &&
+                      aligned(ev->dur_ns, 16);
+  GroupTables gt = c->tables();
+  // clear the control word, the carry table, the dictionary and accumulators
+  launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 16, 0);
+  launch_fill_u64(s, c->at<uint64_t>(L.carryA), GA, 0);
+  launch_fill_u64(s, c->at<uint64_t>(L.dict), L.capD, 0);
+  launch_fill_u64(s, c->at<uint64_t>(L.acc), L.capD * P * 2, 0);
+  if (c->p.raw) launch_fill_u64(s, c->at<uint64_t>(L.raw), L.capD * P * 2, 0);
+  // pass A, Eq. (2)
+  uint64_t* T = c->at<uint64_t>(L.T);
+  if (pass_a_fits_lds(GA) && vec_ok) {
+    const uint64_t per_cu = std::max<uint64_t>(1, std::min<uint64_t>(4, (kLdsBytes - 1024) / (GA * 8)));
+    uint64_t nb = std::min<uint64_t>((uint64_t)c->cus * per_cu, kPartialRowsMax);
+    nb = std::max<uint64_t>(1, std::min<uint64_t>(nb, (n / 4 + kPassAThreads - 1) / kPassAThreads));
+    TIMED(c, "pass_a", n,
+          launch_pass_a_lds(s, d, A, P, (uint32_t)nb, c->at<unsigned long long>(L.partA),
+                            c->at<unsigned long long>(L.carryA), c->err()));
+    TIMED(c, "pass_a_reduce", GA,
+          launch_pass_a_reduce(s, c->at<unsigned long long>(L.partA), (uint32_t)nb, (uint32_t)GA,
+                               c->at<unsigned long long>(L.carryA), T));
+  } else {
+    launch_fill_u64(s, T, GA * 2, 0);
+    TIMED(c, "pass_a_global", n,
+          launch_pass_a_global(s, d, A, P, (uint32_t)std::max<uint64_t>(1, (uint64_t)c->cus * 8), (unsigned long long*)T,
+                               c->err()));
+  }
+  // scale, Eq. (3)
+  uint64_t* scale = c->at<uint64_t>(L.scale);
+  TIMED(c, "scale", GA, launch_scale(s, T, c->app_weight, c->Csum(), A, P, scale));
+  // pass B, Eq. (2)-(3)
+  atrex_path path = c->path;
+  if (path == ATREX_PATH_RADIX_SORT) {
+    c->end_call();
+    return ATREX_E_INVALID_ARG;  // engine not available in this build
+  }
+  if (path == ATREX_PATH_AUTO) path = ATREX_PATH_LDS_HASH;
+  if (path == ATREX_PATH_LDS_HASH && !vec_ok) path = ATREX_PATH_GLOBAL_HASH;
+  if (path == ATREX_PATH_LDS_HASH) {
+    uint32_t sl = 12;
+    while (sl > 1 && pass_b_lds_smem(P, c->p.raw, sl) > kLdsBytes) --sl;
+    c->path_used = "lds_hash";
+    TIMED(c, "pass_b_lds", n,
+          launch_pass_b_lds(s, d, A, P, scale, gt, c->p.raw, sl, (uint32_t)c->cus, c->err()));
+  } else {
+    c->path_used = "global_hash";
+    TIMED(c, "pass_b_global", n,
+          launch_pass_b_global(s, d, A, P, scale, gt, c->p.raw, (uint32_t)c->cus * 8, c->err()));
+  }
+  // compaction and ordering by (key, phase)
+  uint64_t* sk0 = c->at<uint64_t>(L.sk[0]);
+  uint32_t* sv0 = c->at<uint32_t>(L.sv[0]);
+  TIMED(c, "compact", L.capD * P,
+        launch_compact(s, gt, P, L.maxG, sk0, sv0, c->counter(), c->err()));
+  uint64_t hdr[16];
+  (void)hipMemcpyAsync(hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr), hipMemcpyDeviceToHost, s);
+  atrex_status st = sync_status(c);
+  if (st != ATREX_OK) return st;
+  const uint32_t errw = (uint32_t)hdr[0];
+  if (errw & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
+  if (errw & ATREX_ERRBIT_CAPACITY) return ATREX_E_CAPACITY;
+  const uint64_t G = hdr[8];  // compaction counter at byte 64
+  if (G > L.maxG) return ATREX_E_CAPACITY;
+  TIMED(c, "sort_groups", G,
+        radix_sort_pairs(s, sk0, sv0, c->at<uint64_t>(L.sk[1]), c->at<uint32_t>(L.sv[1]), G, 35,
+                         c->at<void>(L.rs_tmp)));
+  TIMED(c, "gather_groups", G, launch_gather_groups(s, sk0, sv0, G, gt, c->p.raw, c->groups()));
+  st = sync_status(c);
+  if (st != ATREX_OK) return st;
+  c->end_call();
+  c->G = G;
+  c->state = 1;
+  *num_groups = G;
+  return ATREX_OK;
+}
+
+atrex_status atrex_phase_normalize(atrex_ctx* c, const atrex_groups* out, uint64_t* num_ops, uint64_t* num_keys) {
+  if (!c || !out) return ATREX_E_INVALID_ARG;
+  if (c->state < 1) return ATREX_E_STATE;
+  const uint64_t G = c->G;
+  const uint32_t P = c->p.P;
+  if (!out->phase_total) return ATREX_E_INVALID_ARG;
+  if (G > 0 && (!out->key || !out->phase || !out->count || !out->wsum || !out->weight)) return ATREX_E_INVALID_ARG;
+  if (out->raw_ns && !c->p.raw) return ATREX_E_INVALID_ARG;
+  const Layout& L = c->L;
+  hipStream_t s = c->s;
+  c->begin_call();
+  const SortedGroups g = c->groups();
+  uint64_t* S = c->at<uint64_t>(L.S);
+  const uint32_t nb = (uint32_t)std::min<uint64_t>(1024, std::max<uint64_t>(1, (G + 255) / 256));
+  TIMED(c, "phase_totals", G, launch_phase_totals(s, g, G, P, c->at<uint64_t>(L.partials), nb, S));
+  TIMED(c, "group_weights", G,
+        launch_group_weights(s, g, G, S, out->key, out->phase, out->count, (uint64_t*)out->wsum, (uint64_t*)out->raw_ns,
+                             out->weight, (uint64_t*)out->phase_total, P));
+  // Eq. (3) units: operators (key >> 16) and keys
+  uint64_t counts[2] = {0, 0};
+  const int shifts[2] = {16, 0};
+  const size_t ids[2] = {L.op_id, L.key_id}, Us[2] = {L.op_U, L.key_U}, ws[2] = {L.op_w, L.key_w};
+  for (int u = 0; u < 2 && G > 0; ++u) {
+    uint32_t* flags = c->at<uint32_t>(L.flags);
+    uint32_t* scan = c->at<uint32_t>(L.scan);
+    uint32_t* starts = c->at<uint32_t>(L.starts);
+    launch_unit_heads(s, g.key, G, shifts[u], flags);
+    exclusive_scan_u32(s, flags, scan, G, c->at<void>(L.scan_tmp));
+    launch_unit_starts(s, flags, scan, G, starts);
+    uint32_t tail[2] = {0, 0};
+    (void)hipMemcpyAsync(&tail[0], scan + (G - 1), 4, hipMemcpyDeviceToHost, s);
+    (void)hipMemcpyAsync(&tail[1], flags + (G - 1), 4, hipMemcpyDeviceToHost, s);
+    atrex_status st = sync_status(c);
+    if (st != ATREX_OK) return st;
+    const uint64_t nu = (uint64_t)tail[0] + tail[1];
+    if (u == 0 && nu > L.maxOps) return ATREX_E_CAPACITY;
+    UnitTable t{c->at<uint32_t>(ids[u]), c->at<uint64_t>(Us[u]), c->at<double>(ws[u])};
+    TIMED(c, u == 0 ? "op_U" : "key_U", nu, launch_unit_U(s, g, G, starts, nu, shifts[u], P, lcm_1_to(P), t));
+    const uint32_t nb2 = (uint32_t)std::min<uint64_t>(1024, std::max<uint64_t>(1, (nu + 255) / 256));
+    uint64_t* tot = c->at<uint64_t>(L.total) + 2 * u;
+    launch_sum_u128(s, t.U, nu, c->at<uint64_t>(L.partials), nb2, tot);
+    launch_unit_weights(s, t, nu, tot);
+    counts[u] = nu;
+  }
+  const atrex_status st = sync_status(c);
+  if (st != ATREX_OK) return st;
+  c->end_call();
+  c->nops = counts[0];
+  c->nkeys = counts[1];
+  if (num_ops) *num_ops = counts[0];
+  if (num_keys) *num_keys = counts[1];
+  c->state = 2;
+  return ATREX_OK;
+}
+
+atrex_status atrex_op_weights(atrex_ctx* c, uint32_t* op, atrex_u128* U, double* w) {
+  if (!c) return ATREX_E_INVALID_ARG;
+  if (c->state < 2) return ATREX_E_STATE;
+  if (c->nops && (!op || !U || !w)) return ATREX_E_INVALID_ARG;
+  if (c->nops) {
+    (void)hipMemcpyAsync(op, c->at<void>(c->L.op_id), c->nops * 4, hipMemcpyDeviceToDevice, c->s);
+    (void)hipMemcpyAsync(U, c->at<void>(c->L.op_U), c->nops * 16, hipMemcpyDeviceToDevice, c->s);
+    (void)hipMemcpyAsync(w, c->at<void>(c->L.op_w), c->nops * 8, hipMemcpyDeviceToDevice, c->s);
+  }
+  return sync_status(c);
+}
+
+atrex_status atrex_key_weights(atrex_ctx* c, uint32_t* key, atrex_u128* U, double* omega) {
+  if (!c) return ATREX_E_INVALID_ARG;
+  if (c->state < 2) return ATREX_E_STATE;
+  if (c->nkeys && (!key || !U || !omega)) return ATREX_E_INVALID_ARG;
+  if (c->nkeys) {
+    (void)hipMemcpyAsync(key, c->at<void>(c->L.key_id), c->nkeys * 4, hipMemcpyDeviceToDevice, c->s);
+    (void)hipMemcpyAsync(U, c->at<void>(c->L.key_U), c->nkeys * 16, hipMemcpyDeviceToDevice, c->s);
+    (void)hipMemcpyAsync(omega, c->at<void>(c->L.key_w), c->nkeys * 8, hipMemcpyDeviceToDevice, c->s);
+  }
+  return sync_status(c);
+}
+
+atrex_status atrex_weighted_score(atrex_ctx* c, const uint32_t* score_key, const double* sv, uint64_t n, uint32_t* op,
+                                  double* op_weight, double* op_score, uint64_t* num_ops, double* s_agg) {
+  if (!c || !s_agg) return ATREX_E_INVALID_ARG;
+  if (c->state < 2) return ATREX_E_STATE;
+  if (n == 0 || !score_key || !sv) return ATREX_E_INVALID_ARG;
+  if (n > c->L.maxS) return ATREX_E_CAPACITY;
+  const Layout& L = c->L;
+  hipStream_t s = c->s;
+  c->begin_call();
+  uint64_t *K0 = c->at<uint64_t>(L.sk[0]), *K1 = c->at<uint64_t>(L.sk[1]), *K2 = c->at<uint64_t>(L.sk[2]);
+  uint32_t *V0 = c->at<uint32_t>(L.sv[0]), *V1 = c->at<uint32_t>(L.sv[1]), *V2 = c->at<uint32_t>(L.sv[2]);
+  void* rtmp = c->at<void>(L.rs_tmp);
+  launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 1, 0);
+  TIMED(c, "score_validate", n, launch_score_validate(s, sv, n, c->err()));
+  // (key) order for the duplicate check; (op, S) order for the medians
+  launch_score_keys(s, score_key, sv, n, K0, K2, V2);
+  (void)hipMemcpyAsync(V0, V2, n * 4, hipMemcpyDeviceToDevice, s);
+  TIMED(c, "score_sort_keys", n, radix_sort_pairs(s, K0, V0, K1, V1, n, 32, rtmp));
+  launch_dup_check(s, K0, n, c->err());
+  TIMED(c, "score_sort_S", n, radix_sort_pairs(s, K2, V2, K1, V1, n, 64, rtmp));
+  launch_score_opkeys(s, score_key, V2, n, K0);
+  TIMED(c, "score_sort_op", n, radix_sort_pairs(s, K0, V2, K1, V1, n, 16, rtmp));
+  uint32_t* flags = c->at<uint32_t>(L.flags);
+  uint32_t* scan = c->at<uint32_t>(L.scan);
+  uint32_t* starts = c->at<uint32_t>(L.starts);
+  launch_heads_u64(s, K0, n, flags);
+  exclusive_scan_u32(s, flags, scan, n, c->at<void>(L.scan_tmp));
+  launch_unit_starts(s, flags, scan, n, starts);
+  uint32_t hdr[4] = {0, 0, 0, 0};
+  (void)hipMemcpyAsync(&hdr[0], c->err(), 4, hipMemcpyDeviceToHost, s);
+  (void)hipMemcpyAsync(&hdr[1], scan + (n - 1), 4, hipMemcpyDeviceToHost, s);
+  (void)hipMemcpyAsync(&hdr[2], flags + (n - 1), 4, hipMemcpyDeviceToHost, s);
+  atrex_status st = sync_status(c);
+  if (st != ATREX_OK) return st;
+  if (hdr[0] & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
+  if (hdr[0] & ATREX_ERRBIT_DUP) return ATREX_E_INVALID_ARG;
+  const uint64_t nr = (uint64_t)hdr[1] + hdr[2];
+  UnitTable opt{c->at<uint32_t>(L.op_id), c->at<uint64_t>(L.op_U), c->at<double>(L.op_w)};
+  uint32_t* r_op = c->at<uint32_t>(L.r_op);
+  uint64_t* r_U = c->at<uint64_t>(L.r_U);
+  double* r_S = c->at<double>(L.r_S);
+  TIMED(c, "score_ops", nr, launch_score_ops(s, score_key, sv, V2, starts, nr, n, opt, c->nops, r_op, r_U, r_S));
+  uint64_t* tot = c->at<uint64_t>(L.total) + 4;
+  const uint32_t nb = (uint32_t)std::min<uint64_t>(1024, std::max<uint64_t>(1, (nr + 255) / 256));
+  launch_sum_u128(s, r_U, nr, c->at<uint64_t>(L.partials), nb, tot);
+  uint64_t totU[2] = {0, 0};
+  (void)hipMemcpyAsync(totU, tot, 16, hipMemcpyDeviceToHost, s);
+  st = sync_status(c);
+  if (st != ATREX_OK) return st;
+  if (totU[0] == 0 && totU[1] == 0) return ATREX_E_INVALID_ARG;  // no retained weight
+  TIMED(c, "score_final", nr,
+        launch_score_final(s, r_op, r_U, r_S, nr, tot, op, op_weight, op_score, c->sagg(), c->err()));
+  double h = 0.0;
+  (void)hipMemcpyAsync(&h, c->sagg(), 8, hipMemcpyDeviceToHost, s);
+  st = sync_status(c);
+  if (st != ATREX_OK) return st;
+  c->end_call();
+  *s_agg = h;
+  if (num_ops) *num_ops = nr;
+  return ATREX_OK;
+}
+
+atrex_status atrex_get_app_totals(atrex_ctx* c, atrex_u128* T, uint64_t* mant, int32_t* rho) {
+  if (!c || !T) return ATREX_E_INVALID_ARG;
+  if (c->state < 1) return ATREX_E_STATE;
+  const uint64_t GA = (uint64_t)c->p.A * c->p.P;
+  (void)hipMemcpyAsync(T, c->at<void>(c->L.T), GA * 16, hipMemcpyDeviceToDevice, c->s);
+  if (mant || rho) launch_unpack_scale(c->s, c->at<uint64_t>(c->L.scale), GA, mant, rho);
+  return sync_status(c);
+}
+
+atrex_status atrex_kernel_times(atrex_ctx* c, const char** names, float* ms, uint64_t* items, int cap, int* count) {
+  if (!c || !count) return ATREX_E_INVALID_ARG;
+  const int n = (int)std::min<size_t>((size_t)std::max(cap, 0), c->last_ms.size());
+  for (int i = 0; i < n; ++i) {
+    if (names) names[i] = c->last_names[i];
+    if (ms) ms[i] = c->last_ms[i];
+    if (items) items[i] = c->last_items[i];
+  }
+  *count = n;
+  return ATREX_OK;
+}
+
+const char* atrex_path_used(atrex_ctx* c) { return c ? c->path_used : "none"; }
+
+atrex_status atrex_aggregate_destroy(atrex_ctx* c) {
+  if (!c) return ATREX_E_INVALID_ARG;
+  for (auto& t : c->timed) {
+    (void)hipEventDestroy(t.a);
+    (void)hipEventDestroy(t.b);
+  }
+  delete c;
+  return ATREX_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,353 @@
+// kernels_normalize.hip -- per-phase normalisation and Eq. (3) per operator /
+// per key (§3.4), and the importance-weighted roofline score (§3.6,
+// Eq. (4)-(6)) on gfx950.
+#include <math.h>
+
+#include "atrex_device.hpp"
+#include "atrex_kernels.h"
+
+namespace {
+
+constexpr int NB = 256;
+
+// ------------------------------------------------------- u128 block reduction
+// Per-phase u128 sums of W over the sorted groups: partials[block][ph].
+__global__ __launch_bounds__(NB) void k_phase_totals_part(SortedGroups g, uint64_t G, uint32_t P,
+                                                          uint64_t* __restrict__ partials) {
+  __shared__ uint64_t s_lo[NB / 64][8], s_hi[NB / 64][8];
+  u128 acc[8];
+#pragma unroll
+  for (int p = 0; p < 8; ++p) acc[p] = 0;
+  for (uint64_t i = (uint64_t)blockIdx.x * NB + threadIdx.x; i < G; i += (uint64_t)gridDim.x * NB) {
+    const u128 w = make_u128(g.wsum[2 * i], g.wsum[2 * i + 1]);
+    const uint32_t ph = g.phase[i];
+#pragma unroll
+    for (int p = 0; p < 8; ++p) acc[p] += (ph == (uint32_t)p) ? w : (u128)0;
+  }
+  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    const u128 t = wave_sum_u128(acc[p]);
+    if (lane == 0) { s_lo[wave][p] = (uint64_t)t; s_hi[wave][p] = (uint64_t)(t >> 64); }
+  }
+  __syncthreads();
+  if (threadIdx.x < P) {
+    u128 t = 0;
+    for (int w = 0; w < NB / 64; ++w) t += make_u128(s_lo[w][threadIdx.x], s_hi[w][threadIdx.x]);
+    partials[((size_t)blockIdx.x * P + threadIdx.x) * 2] = (uint64_t)t;
+    partials[((size_t)blockIdx.x * P + threadIdx.x) * 2 + 1] = (uint64_t)(t >> 64);
+  }
+}
+
+// out[c] = sum over r < rows of x[r][c] for c < cols (u128 entries).
+__global__ __launch_bounds__(NB) void k_colsum_u128(const uint64_t* __restrict__ x, uint32_t rows, uint32_t cols,
+                                                    uint64_t* __restrict__ out) {
+  __shared__ uint64_t s_lo[NB / 64], s_hi[NB / 64];
+  for (uint32_t c = 0; c < cols; ++c) {
+    u128 acc = 0;
+    for (uint32_t r = threadIdx.x; r < rows; r += NB)
+      acc += make_u128(x[((size_t)r * cols + c) * 2], x[((size_t)r * cols + c) * 2 + 1]);
+    const u128 t = wave_sum_u128(acc);
+    if ((threadIdx.x & 63) == 0) { s_lo[threadIdx.x >> 6] = (uint64_t)t; s_hi[threadIdx.x >> 6] = (uint64_t)(t >> 64); }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      u128 s = 0;
+      for (int w = 0; w < NB / 64; ++w) s += make_u128(s_lo[w], s_hi[w]);
+      out[2 * c] = (uint64_t)s;
+      out[2 * c + 1] = (uint64_t)(s >> 64);
+    }
+    __syncthreads();
+  }
+}
+
+// Sum of an array of u128: partials[block].
+__global__ __launch_bounds__(NB) void k_sum_u128_part(const uint64_t* __restrict__ x, uint64_t n,
+                                                      uint64_t* __restrict__ partials) {
+  __shared__ uint64_t s_lo[NB / 64], s_hi[NB / 64];
+  u128 acc = 0;
+  for (uint64_t i = (uint64_t)blockIdx.x * NB + threadIdx.x; i < n; i += (uint64_t)gridDim.x * NB)
+    acc += make_u128(x[2 * i], x[2 * i + 1]);
+  const u128 t = wave_sum_u128(acc);
+  if ((threadIdx.x & 63) == 0) { s_lo[threadIdx.x >> 6] = (uint64_t)t; s_hi[threadIdx.x >> 6] = (uint64_t)(t >> 64); }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    u128 s = 0;
+    for (int w = 0; w < NB / 64; ++w) s += make_u128(s_lo[w], s_hi[w]);
+    partials[2 * blockIdx.x] = (uint64_t)s;
+    partials[2 * blockIdx.x + 1] = (uint64_t)(s >> 64);
+  }
+}
+
+// ------------------------------------------------------- per-phase weights
+// weight = RN(W) / RN(S[ph]): each u128 rounded to nearest-even, one IEEE
+// division.  Also copies the group rows to the caller's output arrays.
+__global__ void k_group_weights(SortedGroups g, uint64_t G, const uint64_t* __restrict__ S, uint32_t P,
+                                uint32_t* __restrict__ okey, uint8_t* __restrict__ oph, uint64_t* __restrict__ ocount,
+                                uint64_t* __restrict__ owsum, uint64_t* __restrict__ oraw, double* __restrict__ oweight,
+                                uint64_t* __restrict__ oS) {
+  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < P && oS) { oS[2 * i] = S[2 * i]; oS[2 * i + 1] = S[2 * i + 1]; }
+  if (i >= G) return;
+  const uint32_t ph = g.phase[i];
+  const u128 w = make_u128(g.wsum[2 * i], g.wsum[2 * i + 1]);
+  const u128 s = make_u128(S[2 * ph], S[2 * ph + 1]);
+  okey[i] = g.key[i];
+  oph[i] = (uint8_t)ph;
+  ocount[i] = g.count[i];
+  owsum[2 * i] = g.wsum[2 * i];
+  owsum[2 * i + 1] = g.wsum[2 * i + 1];
+  if (oraw) { oraw[2 * i] = g.raw[2 * i]; oraw[2 * i + 1] = g.raw[2 * i + 1]; }
+  oweight[i] = s == 0 ? 0.0 : u128_to_f64(w) / u128_to_f64(s);
+}
+
+// ------------------------------------------------------- Eq. (3) units
+__global__ void k_unit_heads(const uint32_t* __restrict__ key, uint64_t G, int shift, uint32_t* __restrict__ flags) {
+  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= G) return;
+  flags[i] = (i == 0 || (key[i] >> shift) != (key[i - 1] >> shift)) ? 1u : 0u;
+}
+
+__global__ void k_unit_starts(const uint32_t* __restrict__ flags, const uint32_t* __restrict__ scan, uint64_t G,
+                              uint32_t* __restrict__ starts) {
+  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < G && flags[i]) starts[scan[i]] = (uint32_t)i;
+  if (i == G - 1) starts[scan[i] + flags[i]] = (uint32_t)G;  // sentinel
+}
+
+// One wave per unit: U = (L / |Phi|) * sum of W over the unit's groups, with
+// Phi the phases in which the unit has at least one invocation.
+__global__ __launch_bounds__(NB) void k_unit_U(SortedGroups g, const uint32_t* __restrict__ starts, uint64_t nunits,
+                                               int shift, uint64_t L, UnitTable t) {
+  const uint64_t u = ((uint64_t)blockIdx.x * NB + threadIdx.x) >> 6;
+  const uint32_t lane = threadIdx.x & 63;
+  if (u >= nunits) return;
+  const uint32_t b = starts[u], e = starts[u + 1];
+  u128 acc = 0;
+  uint32_t present = 0;
+  for (uint32_t i = b + lane; i < e; i += 64) {
+    acc += make_u128(g.wsum[2 * i], g.wsum[2 * i + 1]);
+    if (g.count[i]) present |= 1u << g.phase[i];
+  }
+  acc = wave_sum_u128(acc);
+  for (int d = 32; d >= 1; d >>= 1) present |= __shfl_down(present, d, 64);
+  if (lane == 0) {
+    const uint32_t nph = __popc(present);
+    t.id[u] = g.key[b] >> shift;
+    const u128 U = nph ? (u128)(L / nph) * acc : (u128)0;
+    t.U[2 * u] = (uint64_t)U;
+    t.U[2 * u + 1] = (uint64_t)(U >> 64);
+  }
+}
+
+__global__ void k_unit_weights(UnitTable t, uint64_t nunits, const uint64_t* __restrict__ total) {
+  const uint64_t u = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (u >= nunits) return;
+  const u128 tot = make_u128(total[0], total[1]);
+  const u128 U = make_u128(t.U[2 * u], t.U[2 * u + 1]);
+  t.w[u] = tot == 0 ? 0.0 : u128_to_f64(U) / u128_to_f64(tot);
+}
+
+// ------------------------------------------------------- score, Eq. (4)-(6)
+__global__ void k_score_validate(const double* __restrict__ S, uint64_t n, uint32_t* __restrict__ err) {
+  const uint64_t j = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  bool bad = false;
+  if (j < n) {
+    const double s = S[j];
+    bad = !isnan(s) && !(s > 0.0 && s <= 1.0);  // S_j in (0, 1]; NaN = not correct
+  }
+  if (__any(bad) && (threadIdx.x & 63) == 0) atomicOr(err, ATREX_ERRBIT_RANGE);
+}
+
+// sort keys: (key), (S bit pattern; NaN after every valid value), index
+__global__ void k_score_keys(const uint32_t* __restrict__ score_key, const double* __restrict__ S, uint64_t n,
+                             uint64_t* __restrict__ k_key, uint64_t* __restrict__ k_sval, uint32_t* __restrict__ idx) {
+  const uint64_t j = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  k_key[j] = score_key[j];
+  const double s = S[j];
+  k_sval[j] = isnan(s) ? ~0ull : (uint64_t)__double_as_longlong(s);  // s > 0: bit order = value order
+  idx[j] = (uint32_t)j;
+}
+
+__global__ void k_dup_check(const uint64_t* __restrict__ k, uint64_t n, uint32_t* __restrict__ err) {
+  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const bool dup = i > 0 && i < n && k[i] == k[i - 1];
+  if (__any(dup) && (threadIdx.x & 63) == 0) atomicOr(err, ATREX_ERRBIT_DUP);
+}
+
+__global__ void k_score_opkeys(const uint32_t* __restrict__ score_key, const uint32_t* __restrict__ idx, uint64_t n,
+                               uint64_t* __restrict__ k_op) {
+  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) k_op[i] = score_key[idx[i]] >> 16;
+}
+
+// One thread per retained operator: Eq. (5) median of the correct S_j (they
+// come first in the segment, ascending), 0 if none; U_i looked up in the
+// operator table of the trace (absent: 0).
+__global__ void k_score_ops(const uint32_t* __restrict__ score_key, const double* __restrict__ S,
+                            const uint32_t* __restrict__ order, const uint32_t* __restrict__ starts, uint64_t nops,
+                            UnitTable opt, uint64_t nops_trace, uint32_t* __restrict__ r_op,
+                            uint64_t* __restrict__ r_U, double* __restrict__ r_S) {
+  const uint64_t u = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (u >= nops) return;
+  const uint32_t b = starts[u], e = starts[u + 1];
+  const uint32_t op = score_key[order[b]] >> 16;
+  uint32_t c = 0;
+  while (b + c < e && !isnan(S[order[b + c]])) ++c;
+  double Si = 0.0;
+  if (c) {
+    const uint32_t h = c / 2;
+    Si = (c & 1) ? S[order[b + h]] : (S[order[b + h - 1]] + S[order[b + h]]) / 2.0;
+  }
+  // binary search op in the trace's operator table
+  uint64_t lo = 0, hi = nops_trace;
+  while (lo < hi) {
+    const uint64_t mid = (lo + hi) / 2;
+    if (opt.id[mid] < op) lo = mid + 1; else hi = mid;
+  }
+  uint64_t Ulo = 0, Uhi = 0;
+  if (lo < nops_trace && opt.id[lo] == op) { Ulo = opt.U[2 * lo]; Uhi = opt.U[2 * lo + 1]; }
+  r_op[u] = op;
+  r_U[2 * u] = Ulo;
+  r_U[2 * u + 1] = Uhi;
+  r_S[u] = Si;
+}
+
+struct Comp {
+  double s, c;
+};
+
+__device__ __forceinline__ Comp comp_add(Comp a, double x) {  // Neumaier step
+  const double t = a.s + x;
+  if (fabs(a.s) >= fabs(x)) a.c += (a.s - t) + x; else a.c += (x - t) + a.s;
+  a.s = t;
+  return a;
+}
+
+__device__ __forceinline__ Comp comp_merge(Comp a, Comp b) {  // TwoSum of the sums
+  const double t = a.s + b.s;
+  const double bp = t - a.s;
+  const double e = (a.s - (t - bp)) + (b.s - bp);
+  return Comp{t, a.c + b.c + e};
+}
+
+// Eq. (6): w_i = RN(U_i) / RN(sum over retained U), S_agg = sum w_i S_i with
+// compensated summation (each thread a contiguous run, then a TwoSum tree).
+__global__ __launch_bounds__(1024) void k_score_final(const uint32_t* __restrict__ r_op, const uint64_t* __restrict__ r_U,
+                                                      const double* __restrict__ r_S, uint64_t nops,
+                                                      const uint64_t* __restrict__ totalU, uint32_t* __restrict__ op,
+                                                      double* __restrict__ op_weight, double* __restrict__ op_score,
+                                                      double* __restrict__ s_agg) {
+  __shared__ double s_s[1024], s_c[1024];
+  const u128 tot = make_u128(totalU[0], totalU[1]);
+  const double dt = u128_to_f64(tot);
+  const uint64_t per = (nops + 1023) / 1024;
+  const uint64_t b = threadIdx.x * per, e = (b + per < nops) ? b + per : nops;
+  Comp acc{0.0, 0.0};
+  for (uint64_t u = b; u < e; ++u) {
+    const double w = tot == 0 ? 0.0 : u128_to_f64(make_u128(r_U[2 * u], r_U[2 * u + 1])) / dt;
+    const double x = __dmul_rn(w, r_S[u]);
+    acc = comp_add(acc, x);
+    if (op) op[u] = r_op[u];
+    if (op_weight) op_weight[u] = w;
+    if (op_score) op_score[u] = r_S[u];
+  }
+  s_s[threadIdx.x] = acc.s;
+  s_c[threadIdx.x] = acc.c;
+  __syncthreads();
+  for (int d = 512; d >= 1; d >>= 1) {
+    if (threadIdx.x < (uint32_t)d) {
+      const Comp m = comp_merge(Comp{s_s[threadIdx.x], s_c[threadIdx.x]}, Comp{s_s[threadIdx.x + d], s_c[threadIdx.x + d]});
+      s_s[threadIdx.x] = m.s;
+      s_c[threadIdx.x] = m.c;
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *s_agg = s_s[0] + s_c[0];
+}
+
+__global__ void k_heads_u64(const uint64_t* __restrict__ k, uint64_t n, uint32_t* __restrict__ flags) {
+  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) flags[i] = (i == 0 || k[i] != k[i - 1]) ? 1u : 0u;
+}
+
+uint32_t grid_for(uint64_t n, uint32_t b) { return (uint32_t)((n + b - 1) / b); }
+
+}  // namespace
+
+void launch_phase_totals(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t* partials, uint32_t nb,
+                         uint64_t* S) {
+  hipLaunchKernelGGL(k_phase_totals_part, dim3(nb), dim3(NB), 0, s, g, G, P, partials);
+  hipLaunchKernelGGL(k_colsum_u128, dim3(1), dim3(NB), 0, s, partials, nb, P, S);
+}
+
+void launch_group_weights(hipStream_t s, const SortedGroups& g, uint64_t G, const uint64_t* S, uint32_t* okey,
+                          uint8_t* oph, uint64_t* ocount, uint64_t* owsum, uint64_t* oraw, double* oweight,
+                          uint64_t* oS, uint32_t P) {
+  const uint64_t n = G > P ? G : P;
+  hipLaunchKernelGGL(k_group_weights, dim3(grid_for(n, 256)), dim3(256), 0, s, g, G, S, P, okey, oph, ocount, owsum,
+                     oraw, oweight, oS);
+}
+
+void launch_unit_heads(hipStream_t s, const uint32_t* key, uint64_t G, int shift, uint32_t* flags) {
+  if (G) hipLaunchKernelGGL(k_unit_heads, dim3(grid_for(G, 256)), dim3(256), 0, s, key, G, shift, flags);
+}
+
+void launch_unit_starts(hipStream_t s, const uint32_t* flags, const uint32_t* scan, uint64_t G, uint32_t* starts) {
+  if (G) hipLaunchKernelGGL(k_unit_starts, dim3(grid_for(G, 256)), dim3(256), 0, s, flags, scan, G, starts);
+}
+
+void launch_unit_U(hipStream_t s, const SortedGroups& g, uint64_t G, const uint32_t* starts, uint64_t nunits,
+                   int shift, uint32_t P, uint64_t L, UnitTable t) {
+  (void)G;
+  (void)P;
+  if (nunits)
+    hipLaunchKernelGGL(k_unit_U, dim3(grid_for(nunits * 64, NB)), dim3(NB), 0, s, g, starts, nunits, shift, L, t);
+}
+
+void launch_sum_u128(hipStream_t s, const uint64_t* x, uint64_t n, uint64_t* partials, uint32_t nb, uint64_t* out) {
+  hipLaunchKernelGGL(k_sum_u128_part, dim3(nb), dim3(NB), 0, s, x, n, partials);
+  hipLaunchKernelGGL(k_colsum_u128, dim3(1), dim3(NB), 0, s, partials, nb, 1u, out);
+}
+
+void launch_unit_weights(hipStream_t s, UnitTable t, uint64_t nunits, const uint64_t* total) {
+  if (nunits) hipLaunchKernelGGL(k_unit_weights, dim3(grid_for(nunits, 256)), dim3(256), 0, s, t, nunits, total);
+}
+
+void launch_score_validate(hipStream_t s, const double* S, uint64_t n, uint32_t* err) {
+  hipLaunchKernelGGL(k_score_validate, dim3(grid_for(n, 256)), dim3(256), 0, s, S, n, err);
+}
+
+void launch_score_keys(hipStream_t s, const uint32_t* score_key, const double* S, uint64_t n, uint64_t* k_key,
+                       uint64_t* k_sval, uint32_t* idx) {
+  hipLaunchKernelGGL(k_score_keys, dim3(grid_for(n, 256)), dim3(256), 0, s, score_key, S, n, k_key, k_sval, idx);
+}
+
+void launch_dup_check(hipStream_t s, const uint64_t* sorted_keys, uint64_t n, uint32_t* err) {
+  hipLaunchKernelGGL(k_dup_check, dim3(grid_for(n, 256)), dim3(256), 0, s, sorted_keys, n, err);
+}
+
+void launch_score_opkeys(hipStream_t s, const uint32_t* score_key, const uint32_t* idx, uint64_t n, uint64_t* k_op) {
+  hipLaunchKernelGGL(k_score_opkeys, dim3(grid_for(n, 256)), dim3(256), 0, s, score_key, idx, n, k_op);
+}
+
+void launch_heads_u64(hipStream_t s, const uint64_t* k, uint64_t n, uint32_t* flags) {
+  hipLaunchKernelGGL(k_heads_u64, dim3(grid_for(n, 256)), dim3(256), 0, s, k, n, flags);
+}
+
+void launch_score_ops(hipStream_t s, const uint32_t* score_key, const double* S, const uint32_t* order,
+                      const uint32_t* starts, uint64_t nops, uint64_t n, UnitTable opt, uint64_t nops_trace,
+                      uint32_t* r_op, uint64_t* r_U, double* r_S) {
+  (void)n;
+  if (nops)
+    hipLaunchKernelGGL(k_score_ops, dim3(grid_for(nops, 256)), dim3(256), 0, s, score_key, S, order, starts, nops, opt,
+                       nops_trace, r_op, r_U, r_S);
+}
+
+void launch_score_final(hipStream_t s, const uint32_t* r_op, const uint64_t* r_U, const double* r_S, uint64_t nops,
+                        const uint64_t* totalU, uint32_t* op, double* op_weight, double* op_score, double* s_agg,
+                        uint32_t* err) {
+  (void)err;
+  hipLaunchKernelGGL(k_score_final, dim3(1), dim3(1024), 0, s, r_op, r_U, r_S, nops, totalU, op, op_weight, op_score,
+                     s_agg);
+}

@@ -1,0 +1,97 @@
+"""HIP path vs the CPU oracle, through the C ABI, on the same seeded inputs.
+
+Integers (keys, counts, T, m, rho, W, raw time, S, U) must match bit for bit;
+fp64 outputs (weights, S_agg) within 1e-12 relative, zeros exactly zero.
+Every engine is forced in turn."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import gpu_helpers as H
+from oracle import oracle as O
+from paper_2607_14541_amd import synth
+from test_oracle_bruteforce import random_trace
+
+pytestmark = pytest.mark.gpu
+ENGINES = ["lds_hash", "global_hash"]
+
+
+@pytest.mark.parametrize("path", ENGINES)
+def test_golden_trace(path):
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "tiny_trace.json")))
+    K = g["keys"]
+    ev = g["events"]
+    key, app, ph, dur = ([K[e[0]] for e in ev], [e[1] for e in ev], [e[2] for e in ev], [e[3] for e in ev])
+    sk = [K[k] for k in g["score"]["score_keys"]]
+    s = [math.nan if x is None else x for x in g["score"]["S"]]
+    H.say("golden", path)
+    gr = H.run_gpu(key, app, ph, dur, g["app_weight_q16"], 2, path=path, score_key=sk, s=s)
+    o = O.run(key, app, ph, dur, g["app_weight_q16"], 2, score_key=sk, s=s)
+    H.compare(gr, o, score=True)
+    assert abs(gr["s_agg"] - 363 / 1280) < 1e-15
+
+
+@pytest.mark.parametrize("path", ENGINES)
+@pytest.mark.parametrize("seed", range(0, 48))
+def test_random_small(path, seed):
+    key, app, ph, dur, c, P = random_trace(seed)
+    if key.size == 0:
+        pytest.skip("empty trace covered separately")
+    H.say("random", seed, path, key.size)
+    H.compare(H.run_gpu(key, app, ph, dur, c, P, path=path), O.run(key, app, ph, dur, c, P))
+
+
+@pytest.mark.parametrize("path", ENGINES)
+@pytest.mark.parametrize("n", [1, 3, 5, 64, 4095, 4097, 100003])
+def test_ragged_sizes(path, n):
+    rng = np.random.default_rng(n)
+    P, A = 3, 17
+    key = ((rng.integers(0, 40, n) << 16) | rng.integers(0, 9, n)).astype(np.uint32)
+    app = rng.integers(0, A, n).astype(np.uint32)
+    ph = rng.integers(0, P, n).astype(np.uint8)
+    dur = rng.integers(0, 10 ** 9, n).astype(np.int64)
+    c = rng.integers(1, 2 ** 24, A).astype(np.uint32)
+    H.say("ragged", n, path)
+    H.compare(H.run_gpu(key, app, ph, dur, c, P, path=path), O.run(key, app, ph, dur, c, P))
+
+
+@pytest.mark.parametrize("path", ENGINES)
+def test_empty_trace(path):
+    H.say("empty", path)
+    g = H.run_gpu(np.zeros(0, np.uint32), np.zeros(0, np.uint32), np.zeros(0, np.uint8),
+                  np.zeros(0, np.int64), [5, 6], 3, path=path)
+    assert g["num_groups"] == 0 and not g["phase_total"].any()
+
+
+def _config_case(ci, n):
+    cfg = synth.CONFIGS[ci]
+    ev = synth.events(cfg, n=n)
+    c = synth.app_weights(cfg)
+    return cfg, ev, c
+
+
+@pytest.mark.parametrize("path", ENGINES)
+@pytest.mark.parametrize("ci,n", [(0, 1 << 20), (1, 1 << 21), (2, 1 << 20), (3, 1 << 21), (4, 1 << 21)])
+def test_config_prefix(path, ci, n):
+    cfg, ev, c = _config_case(ci, n)
+    keys = synth.key_space(cfg)
+    if keys.size > 1 << 18:
+        keys = keys[:: keys.size // (1 << 18)]
+    s = synth.scores(cfg, keys, nan_frac=0.1)
+    H.say("config", ci, "n", n, path)
+    g = H.run_gpu(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, cfg["num_phases"], path=path,
+                  score_key=keys, s=s, max_groups=2 * n, max_keys=n)
+    o = O.run(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, cfg["num_phases"], score_key=keys, s=s)
+    H.compare(g, o, score=True)
+
+
+def test_repeat_runs_are_bit_identical():
+    cfg, ev, c = _config_case(1, 1 << 20)
+    H.say("determinism")
+    a = H.run_gpu(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, 2)
+    b = H.run_gpu(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, 2)
+    for k in ("key", "count", "wsum", "weight", "op_U", "omega"):
+        assert np.array_equal(a[k], b[k]), k

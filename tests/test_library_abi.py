@@ -1,0 +1,61 @@
+"""The C-ABI library loads and exports every entry point include/atrex.h
+declares; host-only entry points behave (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "atrex.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(atrex_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2607_14541_amd import atrex
+    return atrex._lib()
+
+
+def test_header_declares_the_four_boundary_calls():
+    names = declared_functions()
+    for n in ("atrex_aggregate_init", "atrex_aggregate_events", "atrex_phase_normalize",
+              "atrex_weighted_score"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    assert lib.atrex_status_str(0) == b"ok"
+    assert lib.atrex_status_str(-4) == b"capacity exceeded"
+
+
+def test_workspace_bytes_validates_parameters(lib):
+    from paper_2607_14541_amd import atrex as X
+    p = X._InitParams()
+    b = ctypes.c_size_t()
+    for P, A, ok in ((2, 1024, True), (0, 4, False), (9, 4, False), (8, 0, False)):
+        p.num_phases, p.num_apps, p.max_events = P, A, 1 << 20
+        st = lib.atrex_workspace_bytes(ctypes.byref(p), ctypes.byref(b))
+        assert (st == 0) == ok
+    p.num_phases, p.num_apps, p.max_events = 2, 4, 1 << 31  # n must stay below 2^31
+    assert lib.atrex_workspace_bytes(ctypes.byref(p), ctypes.byref(b)) == X.E_INVALID_ARG
+
+
+def test_init_rejects_bad_arguments_before_touching_the_device(lib):
+    from paper_2607_14541_amd import atrex as X
+    p = X._InitParams()
+    ctx = ctypes.c_void_p()
+    p.num_phases, p.num_apps, p.max_events = 2, 4, 100
+    assert lib.atrex_aggregate_init(ctypes.byref(p), ctypes.byref(ctx)) == X.E_INVALID_ARG  # no weights
+    assert ctx.value is None
+    assert lib.atrex_aggregate_events(None, None, None) == X.E_INVALID_ARG
