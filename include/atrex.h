@@ -168,6 +168,11 @@ atrex_status atrex_kernel_times(atrex_ctx *ctx, const char **names, float *ms, u
 /* Name of the engine the last aggregate_events used (static string). */
 const char *atrex_path_used(atrex_ctx *ctx);
 
+/* Returns the context to the initialised state so that the next batch of
+ * events can be aggregated with the same workspace (previous results are
+ * discarded).  HOST: ctx. */
+atrex_status atrex_aggregate_reset(atrex_ctx *ctx);
+
 atrex_status atrex_aggregate_destroy(atrex_ctx *ctx);
 
 const char *atrex_status_str(atrex_status s);

@@ -74,6 +74,7 @@ def _lib() -> ctypes.CDLL:
             "atrex_get_app_totals": [P, P, P, P],
             "atrex_kernel_times": [P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float),
                                    ctypes.POINTER(U64), I, ctypes.POINTER(I)],
+            "atrex_aggregate_reset": [P],
             "atrex_aggregate_destroy": [P],
         }
         for name, args in sigs.items():
@@ -165,23 +166,37 @@ class Aggregator:
         self.num_groups = G.value
         return self.num_groups
 
-    def normalize(self) -> dict:
-        G, dev = self.num_groups, self.device
-        out = dict(key=torch.empty(G, dtype=torch.int32, device=dev),
-                   phase=torch.empty(G, dtype=torch.uint8, device=dev),
-                   count=torch.empty(G, dtype=torch.int64, device=dev),
-                   wsum=torch.empty((G, 2), dtype=torch.int64, device=dev),
-                   weight=torch.empty(G, dtype=torch.float64, device=dev),
+    def reset(self) -> None:
+        """Back to the initialised state: the next batch reuses the workspace."""
+        _check(_lib().atrex_aggregate_reset(self._ctx), "atrex_aggregate_reset")
+        self.num_groups = self.num_ops = self.num_keys = None
+
+    def group_buffers(self, capacity: int) -> dict:
+        """Output tensors for normalize() with room for `capacity` groups."""
+        dev = self.device
+        out = dict(key=torch.empty(capacity, dtype=torch.int32, device=dev),
+                   phase=torch.empty(capacity, dtype=torch.uint8, device=dev),
+                   count=torch.empty(capacity, dtype=torch.int64, device=dev),
+                   wsum=torch.empty((capacity, 2), dtype=torch.int64, device=dev),
+                   weight=torch.empty(capacity, dtype=torch.float64, device=dev),
                    phase_total=torch.empty((self.P, 2), dtype=torch.int64, device=dev))
         if self.raw:
-            out["raw_ns"] = torch.empty((G, 2), dtype=torch.int64, device=dev)
+            out["raw_ns"] = torch.empty((capacity, 2), dtype=torch.int64, device=dev)
+        return out
+
+    def normalize(self, out: dict | None = None) -> dict:
+        G = self.num_groups
+        if out is None:
+            out = self.group_buffers(G)
+        elif out["key"].numel() < G:
+            raise ValueError("output buffers hold %d groups, need %d" % (out["key"].numel(), G))
         g = _Groups(_ptr(out["key"]), _ptr(out["phase"]), _ptr(out["count"]), _ptr(out["wsum"]),
                     _ptr(out["weight"]), _ptr(out["phase_total"]), _ptr(out.get("raw_ns")))
         nops, nkeys = ctypes.c_uint64(), ctypes.c_uint64()
         _check(_lib().atrex_phase_normalize(self._ctx, ctypes.byref(g), ctypes.byref(nops),
                                             ctypes.byref(nkeys)), "atrex_phase_normalize")
         self.num_ops, self.num_keys = nops.value, nkeys.value
-        return out
+        return {k: (v if k == "phase_total" else v[:G]) for k, v in out.items()}
 
     def op_weights(self) -> dict:
         k, dev = self.num_ops, self.device
@@ -200,16 +215,20 @@ class Aggregator:
         return dict(key=key, U=U, omega=w)
 
     # -- Eq. (4)-(6) ---------------------------------------------------------------------
-    def score(self, score_key: torch.Tensor, s: torch.Tensor) -> dict:
+    def score(self, score_key: torch.Tensor, s: torch.Tensor, out: dict | None = None) -> dict:
         score_key = _dev(_as_i32(score_key), torch.int32, "score_key")
         s = _dev(s, torch.float64, "s")
         n = score_key.numel()
         if s.numel() != n:
             raise ValueError("score_key and s differ in length")
         dev = self.device
-        op = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
-        ow = torch.empty(max(n, 1), dtype=torch.float64, device=dev)
-        osc = torch.empty(max(n, 1), dtype=torch.float64, device=dev)
+        if out is None:
+            out = dict(op=torch.empty(max(n, 1), dtype=torch.int32, device=dev),
+                       op_weight=torch.empty(max(n, 1), dtype=torch.float64, device=dev),
+                       op_score=torch.empty(max(n, 1), dtype=torch.float64, device=dev))
+        op, ow, osc = out["op"], out["op_weight"], out["op_score"]
+        if op.numel() < n or ow.numel() < n or osc.numel() < n:
+            raise ValueError("score output buffers too small")
         nops = ctypes.c_uint64()
         sagg = ctypes.c_double()
         _check(_lib().atrex_weighted_score(self._ctx, _ptr(score_key), _ptr(s), n, _ptr(op), _ptr(ow),

@@ -573,6 +573,13 @@ atrex_status atrex_kernel_times(atrex_ctx* c, const char** names, float* ms, uin
 
 const char* atrex_path_used(atrex_ctx* c) { return c ? c->path_used : "none"; }
 
+atrex_status atrex_aggregate_reset(atrex_ctx* c) {
+  if (!c) return ATREX_E_INVALID_ARG;
+  c->state = 0;
+  c->G = c->nops = c->nkeys = 0;
+  return ATREX_OK;
+}
+
 atrex_status atrex_aggregate_destroy(atrex_ctx* c) {
   if (!c) return ATREX_E_INVALID_ARG;
   for (auto& t : c->timed) {
