@@ -16,11 +16,12 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libatrex.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 
-HIP_SOURCES = ["atrex_host.hip", "kernels_aggregate.hip", "kernels_util.hip", "kernels_normalize.hip"]
+HIP_SOURCES = ["atrex_host.hip", "kernels_aggregate.hip", "kernels_rows.hip", "kernels_util.hip",
+               "kernels_normalize.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 HIP_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17",
-    # packed fp32 instructions are disabled on purpose
+    # no packed fp32 instructions (v_pk_*_f32) anywhere in the library
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # no contraction: the fp64 score must be the plain product and sum
     "-ffp-contract=off",

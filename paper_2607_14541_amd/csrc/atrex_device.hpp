@@ -35,6 +35,24 @@ __device__ __forceinline__ u128 event_share(uint64_t d, uint64_t sw) {
   return sh >= 0 ? (p << sh) : (p >> (-sh));
 }
 
+// Right-shift amount of the share when rho <= 55 and 55 - rho < 64 (the
+// common case: every (app, phase) whose share of a single invocation is below
+// 2^55 in Q96), else -1.
+__device__ __forceinline__ int share_rshift(uint64_t sw) {
+  const int s = 55 + 64 - (int)(sw >> 56);
+  return (s >= 0 && s < 64) ? s : -1;
+}
+
+// event_share for a scale word with share_rshift(sw) = s in [0, 63]:
+// (d * m) >> s with 64-bit halves (sw = 0 gives 0 since m is then masked to 0).
+__device__ __forceinline__ void event_share_rs(uint64_t d, uint64_t sw, int s, uint64_t& vlo, uint64_t& vhi) {
+  const uint64_t m = sw ? ((sw & (((uint64_t)1 << 55) - 1)) | ((uint64_t)1 << 55)) : 0;
+  const uint64_t lo = d * m;
+  const uint64_t hi = __umul64hi(d, m);
+  vlo = s ? ((lo >> s) | (hi << (64 - s))) : lo;
+  vhi = hi >> s;
+}
+
 // --- u128 -> fp64, round to nearest, ties to even (IEEE 754 conversion) -----
 __device__ __forceinline__ double u128_to_f64(u128 x) {
   const uint64_t hi = (uint64_t)(x >> 64);
@@ -53,6 +71,9 @@ __device__ __forceinline__ double u128_to_f64(u128 x) {
 }
 
 // --- hashing ----------------------------------------------------------------
+// Multiplicative (Fibonacci) hash; the slot is taken from the high bits.
+__device__ __forceinline__ uint32_t hash_mul(uint32_t k) { return k * 0x9E3779B1u; }
+
 __device__ __forceinline__ uint32_t hash32(uint32_t k) {
   k ^= k >> 16;
   k *= 0x7feb352dU;
@@ -90,6 +111,16 @@ __device__ __forceinline__ void acc_add(Ptr lo, Ptr hi, u128 v) {
   atomicAdd(hi, (unsigned long long)(uint64_t)(v >> 64) + carry + (1ull << ATREX_COUNT_SHIFT));
 }
 
+// The same for a pre-summed share of `count` invocations.
+template <typename Ptr>
+__device__ __forceinline__ void acc_add_n(Ptr lo, Ptr hi, u128 v, uint32_t count) {
+  const unsigned long long vlo = (unsigned long long)(uint64_t)v;
+  const unsigned long long old = atomicAdd(lo, vlo);
+  const unsigned long long carry = (old + vlo < old) ? 1ull : 0ull;
+  atomicAdd(hi, (unsigned long long)(uint64_t)(v >> 64) + carry +
+                    ((unsigned long long)count << ATREX_COUNT_SHIFT));
+}
+
 // Plain (count-free) 128-bit accumulation, e.g. raw device time.
 template <typename Ptr>
 __device__ __forceinline__ void acc_add_plain(Ptr lo, Ptr hi, u128 v) {
@@ -104,3 +135,4 @@ __device__ __forceinline__ void acc_add_plain(Ptr lo, Ptr hi, u128 v) {
 #define ATREX_ERRBIT_RANGE 1u
 #define ATREX_ERRBIT_CAPACITY 2u
 #define ATREX_ERRBIT_DUP 4u
+#define ATREX_ERRBIT_SPILL 8u

@@ -15,13 +15,17 @@
 #define ATREX_ERRBIT_RANGE 1u
 #define ATREX_ERRBIT_CAPACITY 2u
 #define ATREX_ERRBIT_DUP 4u
+#define ATREX_ERRBIT_SPILL 8u
 
 namespace {
 
 constexpr size_t kAlign = 256;
 constexpr size_t kLdsBytes = 160 * 1024;
 constexpr uint32_t kPassAThreads = 512;
-constexpr uint64_t kPartialRowsMax = 2048;  // pass-A workgroups with private partial rows
+constexpr uint64_t kPartialRowsMax = 1024;  // pass-A workgroups with private partial rows
+constexpr uint64_t kMaxWG = 256;            // persistent workgroups of the LDS engines
+constexpr uint32_t kMaxBucketBits = 12;     // radix-partition buckets: at most 4096
+constexpr uint32_t kChunk = 1u << 20;       // records per bucket chunk of the partition engine
 constexpr uint32_t kMaxTimed = 64;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -34,13 +38,20 @@ uint64_t next_pow2(uint64_t x) {
 // Byte offsets of every workspace region (all 256-byte aligned).
 struct Layout {
   size_t ctrl, T, carryA, partA, scale, dict, acc, raw;
+  size_t okey, oacc, oraw, ocount, skey, sval, sraw, scount;  // LDS engine outputs
+  size_t H, O, rec, rraw, bstart, istart;                     // partition engine
+  size_t rk, rlo_acc, rhi_acc, rlo_raw, rhi_raw;              // rows
   size_t sk[3], sv[3], rs_tmp, scan_tmp;
   size_t g_key, g_ph, g_cnt, g_w, g_raw, S;
   size_t flags, scan, starts;
   size_t op_id, op_U, op_w, key_id, key_U, key_w;
   size_t r_op, r_U, r_S, partials, total;
   size_t bytes;
-  uint64_t capD, maxG, maxK, maxS, maxSort, maxOps, partA_rows;
+  uint64_t capD, maxG, maxK, maxS, maxSort, maxOps, partA_rows, maxRows;
+  int passA;         // 0: 64-bit LDS table, 1: 32-bit LDS table, 2: global atomics
+  uint32_t ldsSlots; // LDS hash engine slots
+  uint32_t tabSlots; // owner-merge / bucket-aggregate LDS table slots
+  uint32_t capo, scap;
 };
 
 struct Params {
@@ -49,7 +60,11 @@ struct Params {
   bool raw;
 };
 
-bool pass_a_fits_lds(uint64_t G_A) { return G_A * 8 <= kLdsBytes - 1024; }
+int pass_a_mode(uint64_t G_A) {
+  if (G_A * 8 <= kLdsBytes - 1024) return 0;
+  if (G_A * 4 <= kLdsBytes - 512) return 1;
+  return 2;
+}
 
 Layout make_layout(const Params& p) {
   Layout L;
@@ -66,21 +81,52 @@ Layout make_layout(const Params& p) {
   L.maxSort = std::max<uint64_t>(std::max<uint64_t>(L.maxG, L.maxS), 1);
   L.capD = next_pow2(std::max<uint64_t>(1024, 2 * L.maxK));
   L.maxOps = std::min<uint64_t>(L.maxG, 65536);
-  L.partA_rows = pass_a_fits_lds(GA) ? kPartialRowsMax : 0;
+  L.passA = pass_a_mode(GA);
+  L.partA_rows = L.passA == 0 ? kPartialRowsMax : (L.passA == 1 ? kMaxWG : 0);
+  L.ldsSlots = pass_b_lds_slots(p.P, p.raw, kLdsBytes);
+  L.tabSlots = lds_table_slots(p.P, p.raw, kLdsBytes);
+  L.capo = owner_cap(L.ldsSlots);
+  L.scap = spill_cap(p.max_events, kMaxWG);
+  L.maxRows = 2 * L.maxG + (1 << 21);
+  L.maxSort = std::max<uint64_t>(L.maxSort, L.maxRows);
+  const uint64_t accw = (p.raw ? 2 : 1);
   L.ctrl = take(4096);
   L.T = take(GA * 16);
   L.carryA = take(GA * 8);
-  L.partA = take(L.partA_rows * GA * 8);
+  L.partA = take(L.partA_rows * GA * (L.passA == 0 ? 8 : 4));
   L.scale = take(GA * 8);
   L.dict = take(L.capD * 8);
   L.acc = take(L.capD * p.P * 16);
   L.raw = take(p.raw ? L.capD * p.P * 16 : 0);
+  const uint64_t oslots = kMaxWG * ATREX_OWNERS * (uint64_t)L.capo;
+  L.okey = take(oslots * 4);
+  L.oacc = take(oslots * p.P * 16);
+  L.oraw = take(p.raw ? oslots * p.P * 16 : 0);
+  L.ocount = take(kMaxWG * ATREX_OWNERS * 4);
+  const uint64_t sslots = kMaxWG * (uint64_t)L.scap;
+  L.skey = take(sslots * 4);
+  L.sval = take(sslots * 16);
+  L.sraw = take(p.raw ? sslots * 8 : 0);
+  L.scount = take(kMaxWG * 4);
+  const uint64_t hsz = ((uint64_t)1 << kMaxBucketBits) * kMaxWG;
+  L.H = take(hsz * 4);
+  L.O = take(hsz * 4);
+  L.rec = take(p.max_events * 16);
+  L.rraw = take(p.raw ? p.max_events * 8 : 0);
+  L.bstart = take((((uint64_t)1 << kMaxBucketBits) + 1) * 4);
+  L.istart = take((((uint64_t)1 << kMaxBucketBits) + 1) * 4);
+  L.rk = take(L.maxRows * 8);
+  L.rlo_acc = take(L.maxRows * 8);
+  L.rhi_acc = take(L.maxRows * 8);
+  L.rlo_raw = take(p.raw ? L.maxRows * 8 : 0);
+  L.rhi_raw = take(p.raw ? L.maxRows * 8 : 0);
+  (void)accw;
   for (int i = 0; i < 3; ++i) {
     L.sk[i] = take(L.maxSort * 8);
     L.sv[i] = take(L.maxSort * 4);
   }
   L.rs_tmp = take(radix_sort_tmp_bytes(L.maxSort));
-  L.scan_tmp = take(scan_tmp_bytes(L.maxSort + 1));
+  L.scan_tmp = take(std::max(scan_tmp_bytes(L.maxSort + 1), scan_tmp_bytes(hsz)));
   L.g_key = take(L.maxG * 4);
   L.g_ph = take(L.maxG);
   L.g_cnt = take(L.maxG * 8);
@@ -171,8 +217,29 @@ struct atrex_ctx {
   }
   uint32_t* err() const { return at<uint32_t>(L.ctrl); }
   unsigned long long* counter() const { return at<unsigned long long>(L.ctrl + 64); }
-  uint64_t* Csum() const { return at<uint64_t>(L.ctrl + 128); }
-  double* sagg() const { return at<double>(L.ctrl + 192); }
+  unsigned long long* row_count() const { return at<unsigned long long>(L.ctrl + 128); }
+  Rows rows() const {
+    Rows r;
+    r.rk = at<uint64_t>(L.rk);
+    r.lo = at<uint64_t>(L.rlo_acc);
+    r.hi = at<uint64_t>(L.rhi_acc);
+    r.rlo = p.raw ? at<uint64_t>(L.rlo_raw) : nullptr;
+    r.rhi = p.raw ? at<uint64_t>(L.rhi_raw) : nullptr;
+    r.count = row_count();
+    r.cap = L.maxRows;
+    return r;
+  }
+  OwnerRegions owners() const {
+    OwnerRegions o;
+    o.key = at<uint32_t>(L.okey);
+    o.acc = at<uint64_t>(L.oacc);
+    o.raw = p.raw ? at<uint64_t>(L.oraw) : nullptr;
+    o.count = at<uint32_t>(L.ocount);
+    o.capo = L.capo;
+    return o;
+  }
+  uint64_t* Csum() const { return at<uint64_t>(L.ctrl + 1024); }
+  double* sagg() const { return at<double>(L.ctrl + 1088); }
   GroupTables tables() const {
     GroupTables gt;
     gt.dict = at<unsigned long long>(L.dict);
@@ -234,6 +301,47 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
     stmt;                             \
     (ctx)->tstop(t_);                 \
   } while (0)
+
+}  // namespace
+
+namespace {
+
+// The radix-partition engine over all events (spill = false) or over the LDS
+// engine's spill regions: bucket histograms, scan, scatter of 16-byte records,
+// work items, per-bucket-chunk LDS group-by -> rows.
+atrex_status run_partition(atrex_ctx* c, const EventsDev& d, const uint64_t* scale, bool spill, uint32_t nwg,
+                           uint64_t nrec, uint64_t keys_est) {
+  const Layout& L = c->L;
+  hipStream_t s = c->s;
+  const uint32_t P = c->p.P;
+  // buckets: at least 1024 (work for every CU even with one chunk per bucket)
+  // and about half an LDS table of keys per bucket
+  uint32_t BB = 10;
+  while (BB < kMaxBucketBits && ((keys_est + (1ull << BB) - 1) >> BB) > L.tabSlots / 2) ++BB;
+  PartSource src;
+  src.ev = d;
+  src.per = ((d.n + nwg - 1) / nwg + 3) / 4 * 4;
+  src.skey = c->at<uint32_t>(L.skey);
+  src.sval = c->at<uint64_t>(L.sval);
+  src.sraw = c->p.raw ? c->at<uint64_t>(L.sraw) : nullptr;
+  src.scount = c->at<uint32_t>(L.scount);
+  src.scap = spill_cap(d.n, nwg);
+  src.spill = spill;
+  uint32_t* H = c->at<uint32_t>(L.H);
+  uint32_t* O = c->at<uint32_t>(L.O);
+  const uint64_t hn = ((uint64_t)1 << BB) * nwg;
+  TIMED(c, spill ? "part_hist_spill" : "part_hist", nrec, launch_part_hist(s, src, nwg, BB, H));
+  exclusive_scan_u32(s, H, O, hn, c->at<void>(L.scan_tmp));
+  TIMED(c, spill ? "part_scatter_spill" : "part_scatter", nrec,
+        launch_part_scatter(s, src, nwg, c->p.A, P, scale, BB, O, c->at<uint64_t>(L.rec),
+                            c->p.raw ? c->at<uint64_t>(L.rraw) : nullptr, c->err()));
+  launch_part_items(s, O, H, nwg, BB, kChunk, c->at<uint32_t>(L.bstart), c->at<uint32_t>(L.istart));
+  TIMED(c, spill ? "part_aggregate_spill" : "part_aggregate", nrec,
+        launch_part_aggregate(s, c->at<uint64_t>(L.rec), c->p.raw ? c->at<uint64_t>(L.rraw) : nullptr, BB, kChunk,
+                              c->at<uint32_t>(L.bstart), c->at<uint32_t>(L.istart), P, L.tabSlots,
+                              (uint32_t)c->cus, c->rows(), c->err()));
+  return ATREX_OK;
+}
 
 }  // namespace
 
@@ -336,16 +444,13 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
   const bool vec_ok = aligned(ev->key, 16) && aligned(ev->app, 16) && aligned(ev->phase, 4) &&
                       aligned(ev->dur_ns, 16);
   GroupTables gt = c->tables();
-  // clear the control word, the carry table, the dictionary and accumulators
-  launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 16, 0);
+  // clear the control words and the pass-A carry table
+  launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 64, 0);
   launch_fill_u64(s, c->at<uint64_t>(L.carryA), GA, 0);
-  launch_fill_u64(s, c->at<uint64_t>(L.dict), L.capD, 0);
-  launch_fill_u64(s, c->at<uint64_t>(L.acc), L.capD * P * 2, 0);
-  if (c->p.raw) launch_fill_u64(s, c->at<uint64_t>(L.raw), L.capD * P * 2, 0);
   // pass A, Eq. (2)
   uint64_t* T = c->at<uint64_t>(L.T);
-  if (pass_a_fits_lds(GA) && vec_ok) {
-    const uint64_t per_cu = std::max<uint64_t>(1, std::min<uint64_t>(4, (kLdsBytes - 1024) / (GA * 8)));
+  if (L.passA == 0 && vec_ok) {
+    const uint64_t per_cu = std::max<uint64_t>(1, std::min<uint64_t>(2, (kLdsBytes - 1024) / (GA * 8)));
     uint64_t nb = std::min<uint64_t>((uint64_t)c->cus * per_cu, kPartialRowsMax);
     nb = std::max<uint64_t>(1, std::min<uint64_t>(nb, (n / 4 + kPassAThreads - 1) / kPassAThreads));
     TIMED(c, "pass_a", n,
@@ -354,6 +459,14 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
     TIMED(c, "pass_a_reduce", GA,
           launch_pass_a_reduce(s, c->at<unsigned long long>(L.partA), (uint32_t)nb, (uint32_t)GA,
                                c->at<unsigned long long>(L.carryA), T));
+  } else if (L.passA == 1 && vec_ok) {
+    const uint64_t nb = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)c->cus, kMaxWG));
+    TIMED(c, "pass_a", n,
+          launch_pass_a_lds32(s, d, A, P, (uint32_t)nb, c->at<uint32_t>(L.partA), c->at<unsigned long long>(L.carryA),
+                              c->err()));
+    TIMED(c, "pass_a_reduce", GA,
+          launch_pass_a_reduce32(s, c->at<uint32_t>(L.partA), (uint32_t)nb, (uint32_t)GA,
+                                 c->at<unsigned long long>(L.carryA), T));
   } else {
     launch_fill_u64(s, T, GA * 2, 0);
     TIMED(c, "pass_a_global", n,
@@ -363,43 +476,85 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
   // scale, Eq. (3)
   uint64_t* scale = c->at<uint64_t>(L.scale);
   TIMED(c, "scale", GA, launch_scale(s, T, c->app_weight, c->Csum(), A, P, scale));
-  // pass B, Eq. (2)-(3)
+  // pass B, Eq. (2)-(3): every engine emits rows (key << 3 | phase, Q96 sum)
+  const Rows rows = c->rows();
   atrex_path path = c->path;
-  if (path == ATREX_PATH_RADIX_SORT) {
-    c->end_call();
-    return ATREX_E_INVALID_ARG;  // engine not available in this build
-  }
-  if (path == ATREX_PATH_AUTO) path = ATREX_PATH_LDS_HASH;
-  if (path == ATREX_PATH_LDS_HASH && !vec_ok) path = ATREX_PATH_GLOBAL_HASH;
+  if (path == ATREX_PATH_AUTO) path = (c->p.max_keys <= L.ldsSlots) ? ATREX_PATH_LDS_HASH : ATREX_PATH_RADIX_SORT;
+  if (!vec_ok && path != ATREX_PATH_GLOBAL_HASH) path = ATREX_PATH_GLOBAL_HASH;
+  const uint32_t nwg = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)c->cus, kMaxWG));
+  atrex_status st = ATREX_OK;
+  uint64_t hdr[32];  // control words: error at byte 0, row counter at byte 128
   if (path == ATREX_PATH_LDS_HASH) {
-    uint32_t sl = 12;
-    while (sl > 1 && pass_b_lds_smem(P, c->p.raw, sl) > kLdsBytes) --sl;
     c->path_used = "lds_hash";
+    const uint32_t scap = spill_cap(n, nwg);
     TIMED(c, "pass_b_lds", n,
-          launch_pass_b_lds(s, d, A, P, scale, gt, c->p.raw, sl, (uint32_t)c->cus, c->err()));
+          launch_pass_b_lds(s, d, A, P, scale, c->p.raw, L.ldsSlots, nwg, c->owners(), c->at<uint32_t>(L.skey),
+                            c->at<uint64_t>(L.sval), c->p.raw ? c->at<uint64_t>(L.sraw) : nullptr,
+                            c->at<uint32_t>(L.scount), scap, rows, c->err()));
+    TIMED(c, "owner_merge", (uint64_t)nwg * ATREX_OWNERS,
+          launch_owner_merge(s, c->owners(), nwg, P, c->p.raw, L.tabSlots, rows, c->err()));
+    uint32_t scount[kMaxWG];
+    (void)hipMemcpyAsync(hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr), hipMemcpyDeviceToHost, s);
+    (void)hipMemcpyAsync(scount, c->at<uint32_t>(L.scount), nwg * 4, hipMemcpyDeviceToHost, s);
+    st = sync_status(c);
+    if (st != ATREX_OK) return st;
+    if ((uint32_t)hdr[0] & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
+    uint64_t spilled = 0;
+    for (uint32_t w = 0; w < nwg; ++w) spilled += scount[w];
+    if ((uint32_t)hdr[0] & ATREX_ERRBIT_SPILL) {
+      // a spill region overflowed: partition every event instead
+      launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 64, 0);
+      c->path_used = "lds_hash+radix_all";
+      st = run_partition(c, d, scale, false, nwg, n, c->p.max_keys);
+    } else if (spilled) {
+      c->path_used = "lds_hash+radix_spill";
+      st = run_partition(c, d, scale, true, nwg, spilled, std::min<uint64_t>(c->p.max_keys, spilled));
+    }
+    if (st != ATREX_OK) return st;
+  } else if (path == ATREX_PATH_RADIX_SORT) {
+    c->path_used = "radix_sort";
+    st = run_partition(c, d, scale, false, nwg, n, c->p.max_keys);
+    if (st != ATREX_OK) return st;
   } else {
     c->path_used = "global_hash";
+    launch_fill_u64(s, c->at<uint64_t>(L.dict), L.capD, 0);
+    launch_fill_u64(s, c->at<uint64_t>(L.acc), L.capD * P * 2, 0);
+    if (c->p.raw) launch_fill_u64(s, c->at<uint64_t>(L.raw), L.capD * P * 2, 0);
     TIMED(c, "pass_b_global", n,
           launch_pass_b_global(s, d, A, P, scale, gt, c->p.raw, (uint32_t)c->cus * 8, c->err()));
+    TIMED(c, "compact_rows", L.capD * P, launch_compact_rows(s, gt, P, rows, c->err()));
   }
-  // compaction and ordering by (key, phase)
-  uint64_t* sk0 = c->at<uint64_t>(L.sk[0]);
-  uint32_t* sv0 = c->at<uint32_t>(L.sv[0]);
-  TIMED(c, "compact", L.capD * P,
-        launch_compact(s, gt, P, L.maxG, sk0, sv0, c->counter(), c->err()));
-  uint64_t hdr[16];
+  // rows -> groups ordered by (key, phase)
   (void)hipMemcpyAsync(hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr), hipMemcpyDeviceToHost, s);
-  atrex_status st = sync_status(c);
+  st = sync_status(c);
   if (st != ATREX_OK) return st;
-  const uint32_t errw = (uint32_t)hdr[0];
-  if (errw & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
-  if (errw & ATREX_ERRBIT_CAPACITY) return ATREX_E_CAPACITY;
-  const uint64_t G = hdr[8];  // compaction counter at byte 64
-  if (G > L.maxG) return ATREX_E_CAPACITY;
-  TIMED(c, "sort_groups", G,
-        radix_sort_pairs(s, sk0, sv0, c->at<uint64_t>(L.sk[1]), c->at<uint32_t>(L.sv[1]), G, 35,
-                         c->at<void>(L.rs_tmp)));
-  TIMED(c, "gather_groups", G, launch_gather_groups(s, sk0, sv0, G, gt, c->p.raw, c->groups()));
+  if ((uint32_t)hdr[0] & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
+  if ((uint32_t)hdr[0] & ATREX_ERRBIT_CAPACITY) return ATREX_E_CAPACITY;
+  const uint64_t R = hdr[16];  // row counter at byte 128
+  if (R > L.maxRows) return ATREX_E_CAPACITY;
+  uint64_t G = 0;
+  if (R) {
+    uint64_t* K0 = c->at<uint64_t>(L.sk[0]);
+    uint32_t* V0 = c->at<uint32_t>(L.sv[0]);
+    launch_iota_rows(s, rows, R, K0, V0);
+    TIMED(c, "sort_rows", R,
+          radix_sort_pairs(s, K0, V0, c->at<uint64_t>(L.sk[1]), c->at<uint32_t>(L.sv[1]), R, 35,
+                           c->at<void>(L.rs_tmp)));
+    uint32_t* flags = c->at<uint32_t>(L.flags);
+    uint32_t* scan = c->at<uint32_t>(L.scan);
+    uint32_t* starts = c->at<uint32_t>(L.starts);
+    launch_heads_u64(s, K0, R, flags);
+    exclusive_scan_u32(s, flags, scan, R, c->at<void>(L.scan_tmp));
+    launch_unit_starts(s, flags, scan, R, starts);
+    uint32_t tail[2] = {0, 0};
+    (void)hipMemcpyAsync(&tail[0], scan + (R - 1), 4, hipMemcpyDeviceToHost, s);
+    (void)hipMemcpyAsync(&tail[1], flags + (R - 1), 4, hipMemcpyDeviceToHost, s);
+    st = sync_status(c);
+    if (st != ATREX_OK) return st;
+    G = (uint64_t)tail[0] + tail[1];
+    if (G > L.maxG) return ATREX_E_CAPACITY;
+    TIMED(c, "rows_reduce", G, launch_rows_reduce(s, rows, K0, V0, starts, G, c->groups()));
+  }
   st = sync_status(c);
   if (st != ATREX_OK) return st;
   c->end_call();

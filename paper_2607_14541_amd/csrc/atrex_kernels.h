@@ -21,6 +21,42 @@ struct GroupTables {
   unsigned long long* raw;   // [(mask + 1) * P][2] or null
 };
 
+#define ATREX_OWNERS 256  // owner regions of the LDS engine (top byte of the key hash)
+
+// Group rows: sort key = key << 3 | phase, accumulator X = lo + hi * 2^64 with
+// hi = floor(W / 2^64) + count * 2^33, optional raw time (rlo, rhi).
+struct Rows {
+  uint64_t* rk;
+  uint64_t* lo;
+  uint64_t* hi;
+  uint64_t* rlo;
+  uint64_t* rhi;
+  unsigned long long* count;
+  uint64_t cap;
+};
+
+// LDS engine output: per (workgroup, owner) up to capo table rows.
+struct OwnerRegions {
+  uint32_t* key;    // [nwg][ATREX_OWNERS][capo]
+  uint64_t* acc;    // [nwg][ATREX_OWNERS][capo][P][2]
+  uint64_t* raw;    // same shape or null
+  uint32_t* count;  // [nwg][ATREX_OWNERS]
+  uint32_t capo;
+};
+
+// Input of the radix-partition engine: events [w * per, (w + 1) * per) per
+// workgroup, or the LDS engine's spill regions.
+struct PartSource {
+  EventsDev ev;
+  uint64_t per;
+  const uint32_t* skey;
+  const uint64_t* sval;
+  const uint64_t* sraw;
+  const uint32_t* scount;
+  uint32_t scap;
+  bool spill;
+};
+
 // Groups ordered by (key, phase).
 struct SortedGroups {
   uint32_t* key;
@@ -36,6 +72,10 @@ void launch_pass_a_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t 
                        unsigned long long* partial, unsigned long long* carry, uint32_t* err);
 void launch_pass_a_reduce(hipStream_t s, const unsigned long long* partial, uint32_t nb, uint32_t G,
                           const unsigned long long* carry, uint64_t* T);
+void launch_pass_a_lds32(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
+                         uint32_t* partial, unsigned long long* ext, uint32_t* err);
+void launch_pass_a_reduce32(hipStream_t s, const uint32_t* partial, uint32_t nb, uint32_t G,
+                            const unsigned long long* ext, uint64_t* T);
 void launch_pass_a_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
                           unsigned long long* T, uint32_t* err);
 void launch_unpack_scale(hipStream_t s, const uint64_t* sw, uint64_t G, uint64_t* mant, int32_t* rho);
@@ -43,13 +83,35 @@ void launch_scale(hipStream_t s, const uint64_t* T, const uint32_t* c, const uin
                   uint32_t P, uint64_t* scale);
 void launch_pass_b_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, const uint64_t* scale,
                           const GroupTables& gt, bool raw, uint32_t nblocks, uint32_t* err);
-size_t pass_b_lds_smem(uint32_t P, bool raw, uint32_t slots_log2);
-void launch_pass_b_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, const uint64_t* scale,
-                       const GroupTables& gt, bool raw, uint32_t slots_log2, uint32_t nblocks, uint32_t* err);
-void launch_compact(hipStream_t s, const GroupTables& gt, uint32_t P, uint64_t max_groups, uint64_t* sk,
-                    uint32_t* src, unsigned long long* counter, uint32_t* err);
-void launch_gather_groups(hipStream_t s, const uint64_t* sk, const uint32_t* src, uint64_t G, const GroupTables& gt,
-                          bool raw, const SortedGroups& out);
+// LDS hash engine
+uint32_t pass_b_lds_slots(uint32_t P, bool raw, size_t lds_bytes);
+size_t pass_b_lds_smem(uint32_t P, bool raw, uint32_t S);
+uint32_t spill_cap(uint64_t n, uint32_t nwg);
+uint32_t owner_cap(uint32_t S);
+void launch_pass_b_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, const uint64_t* scale, bool raw,
+                       uint32_t S, uint32_t nblocks, const OwnerRegions& orr, uint32_t* spill_key,
+                       uint64_t* spill_val, uint64_t* spill_raw, uint32_t* spill_count, uint32_t scap,
+                       const Rows& rows, uint32_t* err);
+void launch_compact_rows(hipStream_t s, const GroupTables& gt, uint32_t P, const Rows& rows, uint32_t* err);
+
+// kernels_rows.hip
+hipError_t set_rows_smem_limits();
+uint32_t lds_table_slots(uint32_t P, bool raw, size_t lds_bytes);
+size_t lds_table_bytes(uint32_t P, bool raw, uint32_t S);
+void launch_owner_merge(hipStream_t s, const OwnerRegions& orr, uint32_t nwg, uint32_t P, bool raw, uint32_t S,
+                        const Rows& rows, uint32_t* err);
+void launch_part_hist(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t BB, uint32_t* H);
+void launch_part_scatter(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t A, uint32_t P,
+                         const uint64_t* scale, uint32_t BB, const uint32_t* O, uint64_t* rec, uint64_t* rraw,
+                         uint32_t* err);
+void launch_part_items(hipStream_t s, const uint32_t* O, const uint32_t* H, uint32_t nw, uint32_t BB, uint32_t CH,
+                       uint32_t* bstart, uint32_t* item_start);
+void launch_part_aggregate(hipStream_t s, const uint64_t* rec, const uint64_t* rraw, uint32_t BB, uint32_t CH,
+                           const uint32_t* bstart, const uint32_t* item_start, uint32_t P, uint32_t S,
+                           uint32_t nblocks, const Rows& rows, uint32_t* err);
+void launch_iota_rows(hipStream_t s, const Rows& rows, uint64_t R, uint64_t* k, uint32_t* v);
+void launch_rows_reduce(hipStream_t s, const Rows& rows, const uint64_t* rk_sorted, const uint32_t* idx,
+                        const uint32_t* starts, uint64_t G, const SortedGroups& out);
 
 // kernels_util.hip
 void launch_fill_u64(hipStream_t s, uint64_t* p, uint64_t n, uint64_t v);

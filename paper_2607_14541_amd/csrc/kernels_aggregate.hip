@@ -92,15 +92,70 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_lds(EventsDev ev, uint32_t A, 
   for (uint32_t g = threadIdx.x; g < G; g += BLOCK) out[g] = s_lo[g];
 }
 
-// T[g] = sum over blocks of partial[b][g] + carry[g] * 2^64.
-__global__ void k_pass_a_reduce(const unsigned long long* __restrict__ partial, uint32_t nb, uint32_t G,
-                                const unsigned long long* __restrict__ carry, uint64_t* __restrict__ T) {
-  const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
-  if (g >= G) return;
-  u128 s = (u128)carry[g] << 64;
-  for (uint32_t b = 0; b < nb; ++b) s += partial[(size_t)b * G + g];
-  T[2 * g] = (uint64_t)s;
-  T[2 * g + 1] = (uint64_t)(s >> 64);
+// Pass A with 32-bit LDS accumulators (twice the (app, phase) capacity of the
+// 64-bit table).  A wrap of the 32-bit sum and the high half of a duration
+// are both counted in ext[g] in units of 2^32 (global atomics, rare: only
+// when a workgroup's partial sum of one (app, phase) passes 2^32, or for a
+// duration of 2^32 ns or more).
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_pass_a_lds32(EventsDev ev, uint32_t A, uint32_t P, uint32_t G,
+                                                        uint32_t* __restrict__ partial,
+                                                        unsigned long long* __restrict__ ext,
+                                                        uint32_t* __restrict__ err) {
+  extern __shared__ uint32_t s32[];
+  for (uint32_t g = threadIdx.x; g < G; g += BLOCK) s32[g] = 0;
+  __syncthreads();
+  const uint64_t n = ev.n, n4 = n / 4;
+  const uint64_t stride = (uint64_t)gridDim.x * BLOCK;
+  bool bad = false;
+  auto one = [&](uint32_t a, uint32_t ph, int64_t dd) {
+    const bool ok = a < A && ph < P && dd >= 0;
+    bad |= !ok;
+    if (!ok) return;
+    const uint32_t g = a * P + ph;
+    const uint64_t d = (uint64_t)dd;
+    const uint32_t lo = (uint32_t)d;
+    const uint32_t old = atomicAdd(&s32[g], lo);
+    const uint64_t up = (d >> 32) + ((old + lo < old) ? 1u : 0u);
+    if (up) atomicAdd(&ext[g], (unsigned long long)up);
+  };
+  for (uint64_t q = (uint64_t)blockIdx.x * BLOCK + threadIdx.x; q < n4; q += stride) {
+    Ev4 e;
+    load4<false>(ev.key, ev.app, ev.phase, ev.dur, q * 4, e);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) one(e.app[j], e.ph[j], e.dur[j]);
+  }
+  if (blockIdx.x == 0)
+    for (uint64_t i = n4 * 4 + threadIdx.x; i < n; i += BLOCK) one(ev.app[i], ev.phase[i], ev.dur[i]);
+  flag_error(err, bad, ATREX_ERRBIT_RANGE);
+  __syncthreads();
+  uint32_t* out = partial + (size_t)blockIdx.x * G;
+  for (uint32_t g = threadIdx.x; g < G; g += BLOCK) out[g] = s32[g];
+}
+
+// T[g] = sum over blocks of partial[b][g] + ext[g] * 2^ext_shift.
+// Block = 64 consecutive g x 16 strides over the partial rows.
+template <typename PT>
+__global__ __launch_bounds__(1024) void k_pass_a_reduce(const PT* __restrict__ partial, uint32_t nb, uint32_t G,
+                                                        const unsigned long long* __restrict__ ext, int ext_shift,
+                                                        uint64_t* __restrict__ T) {
+  __shared__ uint64_t s_lo[16][64], s_hi[16][64];
+  const uint32_t gl = threadIdx.x & 63, r = threadIdx.x >> 6;
+  const uint32_t g = blockIdx.x * 64 + gl;
+  u128 acc = 0;
+  if (g < G) {
+#pragma unroll 8
+    for (uint32_t b = r; b < nb; b += 16) acc += (uint64_t)partial[(size_t)b * G + g];
+  }
+  s_lo[r][gl] = (uint64_t)acc;
+  s_hi[r][gl] = (uint64_t)(acc >> 64);
+  __syncthreads();
+  if (r == 0 && g < G) {
+    u128 t = (u128)ext[g] << ext_shift;
+    for (int i = 0; i < 16; ++i) t += make_u128(s_lo[i][gl], s_hi[i][gl]);
+    T[2 * g] = (uint64_t)t;
+    T[2 * g + 1] = (uint64_t)(t >> 64);
+  }
 }
 
 // Pass A straight into global 128-bit accumulators (any number of (a, ph)).
@@ -276,152 +331,288 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_global(EventsDev ev, uint32_t 
 }
 
 // ---------------------------------------------------------------------------
-// Pass B with a per-workgroup LDS hash table: slot s holds a key tag and, per
-// phase, a two-word accumulator.  Keys that cannot be placed within MAXPROBE
-// probes (or the reserved tag value) go straight to the global tables.  At the
-// end each workgroup adds its table into the global tables.
+// Pass B with a per-workgroup LDS hash table (the low/medium-cardinality
+// engine).  LDS holds S slots (S sized to the LDS budget, not a power of two):
+// a key tag and, per phase, a two-word accumulator.  Per event: linear probing
+// from mulhi(hash(key), S), at most MAXPROBE slots; an event whose key finds
+// no slot (or the reserved tag value) is appended to a spill list and handled
+// after the kernel, so that no wave waits on device-wide atomics.  Before the
+// LDS atomics, lanes of a wave that hit the same (slot, phase) as the wave's
+// first active lane are summed with shuffles and added once (hot keys).
+// At the end each workgroup writes its table into 256 owner regions (owner =
+// top byte of the key hash); k_owner_merge sums each owner's regions.
+constexpr uint32_t MAXPROBE = 16;
+constexpr uint32_t INVALID_GI = 0xFFFFFFFFu;
+
+
+struct SpillList {
+  uint32_t* key;             // spilled events as records: workgroup w owns [w * cap, (w + 1) * cap)
+  uint64_t* val;             // (share lo, share hi | phase << 40)
+  uint64_t* raw;             // durations (RAW)
+  uint32_t* count;           // [nwg] records written by each workgroup
+  uint32_t cap;
+};
+
+__device__ __forceinline__ uint32_t lane_id() { return threadIdx.x & 63; }
+
+// Wave-aggregated append of this lane's event as a record when `spill` is
+// set, to this workgroup's region of the spill list (counter in LDS).  A
+// region that fills up raises ATREX_ERRBIT_SPILL (the caller then runs the
+// partition engine on all events instead).
+__device__ __forceinline__ void spill_append(const SpillList& sp, uint32_t* s_count, bool spill, uint32_t key,
+                                             u128 v, uint32_t ph, uint64_t d, uint32_t* err) {
+  const uint64_t bm = __ballot(spill);
+  if (bm == 0) return;
+  const uint32_t leader = __ffsll((unsigned long long)bm) - 1;
+  uint32_t base = 0;
+  if (lane_id() == leader) base = atomicAdd(s_count, (uint32_t)__popcll(bm));
+  base = __shfl(base, leader, 64);
+  if (!spill) return;
+  const uint32_t r = base + __popcll(bm & ((1ull << lane_id()) - 1ull));
+  if (r >= sp.cap) {
+    atomicOr(err, ATREX_ERRBIT_SPILL);
+    return;
+  }
+  const size_t i = (size_t)blockIdx.x * sp.cap + r;
+  sp.key[i] = key;
+  sp.val[2 * i] = (uint64_t)v;
+  sp.val[2 * i + 1] = (uint64_t)(v >> 64) | ((uint64_t)ph << 40);
+  if (sp.raw) sp.raw[i] = d;
+}
+
+// Wave-aggregated append of one row per lane with `want` set.
+__device__ __forceinline__ void row_push(const Rows& R, bool want, uint64_t rk, uint64_t lo, uint64_t hi,
+                                         uint64_t rlo, uint64_t rhi, uint32_t* err) {
+  const uint64_t bm = __ballot(want);
+  if (bm == 0) return;
+  const uint32_t leader = __ffsll((unsigned long long)bm) - 1;
+  unsigned long long base = 0;
+  if (lane_id() == leader) base = atomicAdd(R.count, (unsigned long long)__popcll(bm));
+  base = __shfl(base, leader, 64);
+  if (!want) return;
+  const uint64_t pos = base + __popcll(bm & ((1ull << lane_id()) - 1ull));
+  if (pos >= R.cap) {
+    atomicOr(err, ATREX_ERRBIT_CAPACITY);
+    return;
+  }
+  R.rk[pos] = rk;
+  R.lo[pos] = lo;
+  R.hi[pos] = hi;
+  if (R.rlo) {
+    R.rlo[pos] = rlo;
+    R.rhi[pos] = rhi;
+  }
+}
+
 template <int BLOCK, bool RAW>
 __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t A, uint32_t P,
-                                                      const uint64_t* __restrict__ scale, GroupTables gt,
-                                                      uint32_t slots_log2, uint32_t* __restrict__ err) {
+                                                      const uint64_t* __restrict__ scale, uint32_t S,
+                                                      OwnerRegions orr, SpillList sp, Rows rows,
+                                                      uint32_t* __restrict__ err) {
   extern __shared__ unsigned long long smem[];
-  const uint32_t S = 1u << slots_log2, SP = S * P;
+  const uint32_t SP = S * P;
   unsigned long long* s_lo = smem;
   unsigned long long* s_hi = smem + SP;
-  unsigned long long* r_lo = smem + 2 * SP;               // RAW only
-  unsigned long long* r_hi = smem + 3 * SP;               // RAW only
+  unsigned long long* r_lo = smem + 2 * SP;  // RAW only
+  unsigned long long* r_hi = smem + 3 * SP;  // RAW only
   uint32_t* s_tag = (uint32_t*)(smem + (RAW ? 4 : 2) * SP);
+  uint32_t* s_ocnt = s_tag + S;                      // [ATREX_OWNERS]
+  uint32_t& s_spills = s_ocnt[ATREX_OWNERS];         // dynamic LDS: static LDS would not fit beside 160 KB
+  if (threadIdx.x == 0) s_spills = 0;
   for (uint32_t i = threadIdx.x; i < SP; i += BLOCK) {
     s_lo[i] = 0;
     s_hi[i] = 0;
     if (RAW) { r_lo[i] = 0; r_hi[i] = 0; }
   }
   for (uint32_t i = threadIdx.x; i < S; i += BLOCK) s_tag[i] = ATREX_EMPTY_KEY;
+  for (uint32_t i = threadIdx.x; i < ATREX_OWNERS; i += BLOCK) s_ocnt[i] = 0;
   __syncthreads();
-  const uint32_t mask = S - 1;
-  const uint32_t shift = 32 - slots_log2;
-  constexpr uint32_t MAXPROBE = 64;
   const uint64_t n = ev.n, n4 = n / 4;
   const uint64_t stride = (uint64_t)gridDim.x * BLOCK;
+  const uint32_t lane = lane_id();
   bool bad = false;
-  auto one = [&](uint32_t k, uint32_t a, uint32_t ph, int64_t d) {
-    const bool ok = a < A && ph < P && d >= 0;
-    bad |= !ok;
-    if (!ok) return;
-    const u128 v = event_share((uint64_t)d, scale[(size_t)a * P + ph]);
-    int32_t slot = -1;
-    if (k != ATREX_EMPTY_KEY) {
-      uint32_t h = (hash32(k) >> shift) & mask;  // slots_log2 >= 1
-      for (uint32_t probe = 0; probe < MAXPROBE; ++probe) {
-        uint32_t t = s_tag[h];
-        if (t == ATREX_EMPTY_KEY) t = atomicCAS(&s_tag[h], ATREX_EMPTY_KEY, k);
-        if (t == k || t == ATREX_EMPTY_KEY) {
-          slot = (int32_t)h;
-          break;
-        }
-        h = (h + 1) & mask;
-      }
-    }
-    if (slot >= 0) {
-      const uint32_t gi = (uint32_t)slot * P + ph;
-      acc_add(&s_lo[gi], &s_hi[gi], v);
-      if (RAW) acc_add_plain(&r_lo[gi], &r_hi[gi], (u128)(uint64_t)d);
-    } else {
-      global_accumulate<RAW>(gt, P, k, ph, (uint64_t)d, v, err);
+  // Slot of key k (linear probing); INVALID_GI when not placed.  Probing past
+  // the first slot is the rare path and is kept as a plain loop.
+  auto find_slot = [&](uint32_t k, uint32_t h, uint32_t t) -> uint32_t {
+#pragma unroll 1
+    for (uint32_t probe = 0;;) {
+      if (t == ATREX_EMPTY_KEY) t = atomicCAS(&s_tag[h], ATREX_EMPTY_KEY, k);
+      if (t == k || t == ATREX_EMPTY_KEY) return h;
+      if (++probe == MAXPROBE) return INVALID_GI;
+      h = (h + 1 == S) ? 0 : h + 1;
+      t = s_tag[h];
     }
   };
-  for (uint64_t q = (uint64_t)blockIdx.x * BLOCK + threadIdx.x; q < n4; q += stride) {
-    Ev4 e;
-    load4<true>(ev.key, ev.app, ev.phase, ev.dur, q * 4, e);
+  // Four events per lane (all lanes of the wave together): validation, then
+  // four unconditional scale gathers (index clamped to 0 when invalid), the
+  // first-probe LDS reads, the shares, the slots, then accumulation.
+  auto batch = [&](const bool valid[4], const uint32_t k[4], const uint32_t a[4], const uint32_t ph[4],
+                   const int64_t d[4], uint64_t base) {
+    bool ok[4];
+    uint64_t sw[4];
+    uint32_t h[4], t[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) one(e.key[j], e.app[j], e.ph[j], e.dur[j]);
+    for (int j = 0; j < 4; ++j) {
+      ok[j] = valid[j] && a[j] < A && ph[j] < P && d[j] >= 0;
+      bad |= valid[j] && !ok[j];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) sw[j] = scale[ok[j] ? (size_t)a[j] * P + ph[j] : 0];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      h[j] = __umulhi(hash_mul(k[j]), S);
+      t[j] = s_tag[h[j]];
+    }
+    u128 v[4];
+    int rs[4];
+    bool fast = true;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      sw[j] = ok[j] ? sw[j] : 0;
+      rs[j] = share_rshift(sw[j]);
+      fast &= rs[j] >= 0 || sw[j] == 0;
+    }
+    if (__all(fast)) {  // wave-uniform: one 64x64 product and a funnel shift each
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        uint64_t lo, hi;
+        event_share_rs((uint64_t)d[j], sw[j], rs[j] < 0 ? 0 : rs[j], lo, hi);
+        v[j] = make_u128(lo, hi);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[j] = event_share((uint64_t)d[j], sw[j]);
+    }
+    uint32_t gi[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      gi[j] = INVALID_GI;
+      if (ok[j] && k[j] != ATREX_EMPTY_KEY) {
+        const uint32_t slot = (t[j] == k[j]) ? h[j] : find_slot(k[j], h[j], t[j]);
+        if (slot != INVALID_GI) gi[j] = slot * P + ph[j];
+      }
+      spill_append(sp, &s_spills, ok[j] && gi[j] == INVALID_GI, k[j], v[j], ph[j], (uint64_t)d[j], err);
+    }
+    // hot group: when many lanes share the first lane's (slot, phase) in the
+    // first event slot, lanes sharing a group are summed with shuffles first
+    bool hot = false;
+    {
+      const uint64_t act = __ballot(gi[0] != INVALID_GI);
+      if (act) {
+        const uint32_t first = __ffsll((unsigned long long)act) - 1;
+        const uint32_t lead = __shfl(gi[0], first, 64);
+        hot = __popcll(__ballot(gi[0] == lead)) >= 8;
+      }
+    }
+    if (hot) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint64_t act = __ballot(gi[j] != INVALID_GI);
+        if (act == 0) continue;
+        const uint32_t first = __ffsll((unsigned long long)act) - 1;
+        const uint32_t lead = __shfl(gi[j], first, 64);
+        const uint64_t same = __ballot(gi[j] == lead);
+        if (__popcll(same) < 4) continue;
+        const bool mine = gi[j] == lead;
+        const u128 tot = wave_sum_u128(mine ? v[j] : (u128)0);
+        u128 rtot = 0;
+        if (RAW) rtot = wave_sum_u128(mine ? (u128)(uint64_t)d[j] : (u128)0);
+        const uint64_t tlo = __shfl((unsigned long long)(uint64_t)tot, 0, 64);
+        const uint64_t thi = __shfl((unsigned long long)(uint64_t)(tot >> 64), 0, 64);
+        uint64_t rlo = 0, rhi = 0;
+        if (RAW) {
+          rlo = __shfl((unsigned long long)(uint64_t)rtot, 0, 64);
+          rhi = __shfl((unsigned long long)(uint64_t)(rtot >> 64), 0, 64);
+        }
+        if (lane == first) {
+          acc_add_n(&s_lo[lead], &s_hi[lead], make_u128(tlo, thi), __popcll(same));
+          if (RAW) acc_add_plain(&r_lo[lead], &r_hi[lead], make_u128(rlo, rhi));
+        }
+        if (mine) gi[j] = INVALID_GI;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (gi[j] == INVALID_GI) continue;
+      acc_add(&s_lo[gi[j]], &s_hi[gi[j]], v[j]);
+      if (RAW) acc_add_plain(&r_lo[gi[j]], &r_hi[gi[j]], (u128)(uint64_t)d[j]);
+    }
+  };
+  // wave-uniform trip count: a lane past the end processes nothing
+  const uint64_t wave_first = (uint64_t)blockIdx.x * BLOCK + (threadIdx.x & ~63u);
+  for (uint64_t qw = wave_first; qw < n4; qw += stride) {
+    const uint64_t q = qw + lane;
+    const bool v4 = q < n4;
+    Ev4 e;
+    if (v4) load4<true>(ev.key, ev.app, ev.phase, ev.dur, q * 4, e);
+    const bool valid[4] = {v4, v4, v4, v4};
+    batch(valid, e.key, e.app, e.ph, e.dur, q * 4);
   }
-  if (blockIdx.x == 0)
-    for (uint64_t i = n4 * 4 + threadIdx.x; i < n; i += BLOCK) one(ev.key[i], ev.app[i], ev.phase[i], ev.dur[i]);
+  if (blockIdx.x == 0 && threadIdx.x < 64) {  // n % 4 tail events, one wave
+    const uint64_t i = n4 * 4 + lane;
+    bool valid[4] = {i < n, false, false, false};
+    uint32_t k[4] = {0, 0, 0, 0}, a[4] = {0, 0, 0, 0}, ph[4] = {0, 0, 0, 0};
+    int64_t d[4] = {0, 0, 0, 0};
+    if (valid[0]) { k[0] = ev.key[i]; a[0] = ev.app[i]; ph[0] = ev.phase[i]; d[0] = ev.dur[i]; }
+    batch(valid, k, a, ph, d, i);
+  }
   flag_error(err, bad, ATREX_ERRBIT_RANGE);
   __syncthreads();
-  // merge this workgroup's table into the global tables
-  for (uint32_t s = threadIdx.x; s < S; s += BLOCK) {
-    const uint32_t k = s_tag[s];
-    if (k == ATREX_EMPTY_KEY) continue;
-    const int64_t j = dict_slot(gt.dict, gt.dict_mask, k, err);
-    if (j < 0) continue;
+  // this workgroup's table -> owner regions (owner = top byte of the key hash);
+  // a region that is full sends its rows straight to the row list
+  for (uint32_t s0 = 0; s0 < S; s0 += BLOCK) {
+    const uint32_t sl = s0 + threadIdx.x;
+    const uint32_t t = sl < S ? s_tag[sl] : ATREX_EMPTY_KEY;
+    bool spill_rows = false;
+    if (t != ATREX_EMPTY_KEY) {
+      const uint32_t o = hash32(t) >> 24;
+      const uint32_t r = atomicAdd(&s_ocnt[o], 1u);
+      if (r < orr.capo) {
+        const size_t rec = ((size_t)blockIdx.x * ATREX_OWNERS + o) * orr.capo + r;
+        orr.key[rec] = t;
+        for (uint32_t ph = 0; ph < P; ++ph) {
+          orr.acc[(rec * P + ph) * 2] = s_lo[sl * P + ph];
+          orr.acc[(rec * P + ph) * 2 + 1] = s_hi[sl * P + ph];
+          if (RAW) {
+            orr.raw[(rec * P + ph) * 2] = r_lo[sl * P + ph];
+            orr.raw[(rec * P + ph) * 2 + 1] = r_hi[sl * P + ph];
+          }
+        }
+      } else {
+        spill_rows = true;
+      }
+    }
     for (uint32_t ph = 0; ph < P; ++ph) {
-      const uint32_t li = s * P + ph;
-      const unsigned long long hi = s_hi[li], lo = s_lo[li];
-      if ((hi >> ATREX_COUNT_SHIFT) == 0) continue;  // no invocation in this phase
-      const size_t gi = (size_t)j * P + ph;
-      const unsigned long long old = atomicAdd(&gt.acc[2 * gi], lo);
-      atomicAdd(&gt.acc[2 * gi + 1], hi + ((old + lo < old) ? 1ull : 0ull));
-      if (RAW) acc_add_plain(&gt.raw[2 * gi], &gt.raw[2 * gi + 1], make_u128(r_lo[li], r_hi[li]));
+      const uint64_t hi = spill_rows ? s_hi[sl * P + ph] : 0;
+      const bool want = spill_rows && (hi >> ATREX_COUNT_SHIFT) != 0;
+      row_push(rows, want, ((uint64_t)t << 3) | ph, want ? s_lo[sl * P + ph] : 0, hi,
+               (RAW && want) ? r_lo[sl * P + ph] : 0, (RAW && want) ? r_hi[sl * P + ph] : 0, err);
     }
   }
+  __syncthreads();
+  for (uint32_t o = threadIdx.x; o < ATREX_OWNERS; o += BLOCK)
+    orr.count[(size_t)blockIdx.x * ATREX_OWNERS + o] = min(s_ocnt[o], orr.capo);
+  if (threadIdx.x == 0) sp.count[blockIdx.x] = min(s_spills, sp.cap);
 }
 
 // ---------------------------------------------------------------------------
-// Compaction: every (dictionary slot, phase) with at least one invocation
-// becomes a group row (sort key = key << 3 | phase, source index).
-template <int BLOCK>
-__global__ __launch_bounds__(BLOCK) void k_compact(GroupTables gt, uint32_t P, uint64_t max_groups,
-                                                   uint64_t* __restrict__ sk, uint32_t* __restrict__ src,
-                                                   unsigned long long* __restrict__ counter,
-                                                   uint32_t* __restrict__ err) {
-  __shared__ uint32_t s_base;
-  __shared__ uint32_t s_wcnt[BLOCK / 64];
+// Global-hash engine output: every (dictionary slot, phase) with at least one
+// invocation becomes a row.
+__global__ void k_compact_rows(GroupTables gt, uint32_t P, Rows rows, uint32_t* __restrict__ err) {
   const uint64_t total = (uint64_t)(gt.dict_mask + 1) * P;
-  for (uint64_t base = (uint64_t)blockIdx.x * BLOCK; base < total; base += (uint64_t)gridDim.x * BLOCK) {
+  for (uint64_t base = (uint64_t)blockIdx.x * blockDim.x; base < total; base += (uint64_t)gridDim.x * blockDim.x) {
     const uint64_t gi = base + threadIdx.x;
     bool live = false;
-    uint32_t key = 0;
+    uint64_t rk = 0, lo = 0, hi = 0, rl = 0, rh = 0;
     if (gi < total) {
-      const uint64_t j = gi / P;
-      const unsigned long long tag = gt.dict[j];
-      live = tag != 0 && (gt.acc[2 * gi + 1] >> ATREX_COUNT_SHIFT) != 0;
-      key = (uint32_t)(tag - 1);
+      const unsigned long long tag = gt.dict[gi / P];
+      hi = gt.acc[2 * gi + 1];
+      live = tag != 0 && (hi >> ATREX_COUNT_SHIFT) != 0;
+      rk = ((uint64_t)(uint32_t)(tag - 1) << 3) | (gi % P);
+      lo = gt.acc[2 * gi];
+      if (gt.raw) { rl = gt.raw[2 * gi]; rh = gt.raw[2 * gi + 1]; }
     }
-    const uint64_t bal = __ballot(live);
-    const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const uint32_t before = __popcll(bal & ((1ull << lane) - 1));
-    if (lane == 0) s_wcnt[wave] = __popcll(bal);
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      uint32_t tot = 0;
-      for (int w = 0; w < BLOCK / 64; ++w) {
-        const uint32_t c = s_wcnt[w];
-        s_wcnt[w] = tot;
-        tot += c;
-      }
-      s_base = tot ? (uint32_t)atomicAdd(counter, (unsigned long long)tot) : 0;
-    }
-    __syncthreads();
-    if (live) {
-      const uint64_t pos = (uint64_t)s_base + s_wcnt[wave] + before;
-      if (pos < max_groups) {
-        sk[pos] = ((uint64_t)key << 3) | (uint64_t)(gi % P);
-        src[pos] = (uint32_t)gi;
-      } else {
-        atomicOr(err, ATREX_ERRBIT_CAPACITY);
-      }
-    }
-    __syncthreads();
-  }
-}
-
-// Sorted rows -> group arrays.
-__global__ void k_gather_groups(const uint64_t* __restrict__ sk, const uint32_t* __restrict__ src, uint64_t G,
-                                GroupTables gt, bool raw, SortedGroups out) {
-  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= G) return;
-  const uint64_t gi = src[i];
-  const uint64_t hi = gt.acc[2 * gi + 1];
-  out.key[i] = (uint32_t)(sk[i] >> 3);
-  out.phase[i] = (uint8_t)(sk[i] & 7);
-  out.count[i] = hi >> ATREX_COUNT_SHIFT;
-  out.wsum[2 * i] = gt.acc[2 * gi];
-  out.wsum[2 * i + 1] = hi & ((1ull << ATREX_COUNT_SHIFT) - 1);
-  if (raw) {
-    out.raw[2 * i] = gt.raw[2 * gi];
-    out.raw[2 * i + 1] = gt.raw[2 * gi + 1];
+    row_push(rows, live, rk, lo, hi, rl, rh, err);
   }
 }
 
@@ -452,7 +643,20 @@ void launch_pass_a_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t 
 
 void launch_pass_a_reduce(hipStream_t s, const unsigned long long* partial, uint32_t nb, uint32_t G,
                           const unsigned long long* carry, uint64_t* T) {
-  hipLaunchKernelGGL(k_pass_a_reduce, dim3((G + 255) / 256), dim3(256), 0, s, partial, nb, G, carry, T);
+  hipLaunchKernelGGL(k_pass_a_reduce<unsigned long long>, dim3((G + 63) / 64), dim3(1024), 0, s, partial, nb, G, carry,
+                     64, T);
+}
+
+void launch_pass_a_lds32(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
+                         uint32_t* partial, unsigned long long* ext, uint32_t* err) {
+  const uint32_t G = A * P;
+  hipLaunchKernelGGL((k_pass_a_lds32<1024>), dim3(nblocks), dim3(1024), (size_t)G * 4, s, ev, A, P, G, partial, ext,
+                     err);
+}
+
+void launch_pass_a_reduce32(hipStream_t s, const uint32_t* partial, uint32_t nb, uint32_t G,
+                            const unsigned long long* ext, uint64_t* T) {
+  hipLaunchKernelGGL(k_pass_a_reduce<uint32_t>, dim3((G + 63) / 64), dim3(1024), 0, s, partial, nb, G, ext, 32, T);
 }
 
 void launch_pass_a_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
@@ -474,44 +678,56 @@ void launch_pass_b_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32
     hipLaunchKernelGGL((k_pass_b_global<256, false>), dim3(nblocks), dim3(256), 0, s, ev, A, P, scale, gt, err);
 }
 
-size_t pass_b_lds_smem(uint32_t P, bool raw, uint32_t slots_log2) {
-  const size_t S = (size_t)1 << slots_log2;
-  return S * P * 8 * (raw ? 4 : 2) + S * 4;
+uint32_t pass_b_lds_slots(uint32_t P, bool raw, size_t lds_bytes) {
+  const size_t per_slot = 4 + (size_t)16 * P * (raw ? 2 : 1);
+  const size_t fixed = ATREX_OWNERS * 4 + 256;
+  size_t S = (lds_bytes - fixed) / per_slot;
+  if (S > 8 * 1024) S = 8 * 1024;
+  return (uint32_t)S;
 }
 
-void launch_pass_b_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, const uint64_t* scale,
-                       const GroupTables& gt, bool raw, uint32_t slots_log2, uint32_t nblocks, uint32_t* err) {
-  const size_t smem = pass_b_lds_smem(P, raw, slots_log2);
+size_t pass_b_lds_smem(uint32_t P, bool raw, uint32_t S) {
+  return (size_t)S * P * 8 * (raw ? 4 : 2) + (size_t)S * 4 + ATREX_OWNERS * 4 + 4;
+}
+
+// a workgroup of the grid-stride loop sees at most n / nwg + 4 * BLOCK + 3
+// events; its spill region holds half of that
+uint32_t spill_cap(uint64_t n, uint32_t nwg) { return (uint32_t)((n + nwg - 1) / nwg / 2 + 8 * 1024); }
+
+uint32_t owner_cap(uint32_t S) { return 2 * ((S + ATREX_OWNERS - 1) / ATREX_OWNERS) + 32; }
+
+void launch_pass_b_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, const uint64_t* scale, bool raw,
+                       uint32_t S, uint32_t nblocks, const OwnerRegions& orr, uint32_t* spill_key,
+                       uint64_t* spill_val, uint64_t* spill_raw, uint32_t* spill_count, uint32_t scap,
+                       const Rows& rows, uint32_t* err) {
+  const size_t smem = pass_b_lds_smem(P, raw, S);
+  SpillList sp{spill_key, spill_val, spill_raw, spill_count, scap};
   if (raw)
-    hipLaunchKernelGGL((k_pass_b_lds<1024, true>), dim3(nblocks), dim3(1024), smem, s, ev, A, P, scale, gt,
-                       slots_log2, err);
+    hipLaunchKernelGGL((k_pass_b_lds<1024, true>), dim3(nblocks), dim3(1024), smem, s, ev, A, P, scale, S, orr, sp,
+                       rows, err);
   else
-    hipLaunchKernelGGL((k_pass_b_lds<1024, false>), dim3(nblocks), dim3(1024), smem, s, ev, A, P, scale, gt,
-                       slots_log2, err);
+    hipLaunchKernelGGL((k_pass_b_lds<1024, false>), dim3(nblocks), dim3(1024), smem, s, ev, A, P, scale, S, orr, sp,
+                       rows, err);
 }
 
-void launch_compact(hipStream_t s, const GroupTables& gt, uint32_t P, uint64_t max_groups, uint64_t* sk,
-                    uint32_t* src, unsigned long long* counter, uint32_t* err) {
+void launch_compact_rows(hipStream_t s, const GroupTables& gt, uint32_t P, const Rows& rows, uint32_t* err) {
   const uint64_t total = (uint64_t)(gt.dict_mask + 1) * P;
   uint64_t nb = (total + 255) / 256;
   if (nb > 4096) nb = 4096;
-  hipLaunchKernelGGL((k_compact<256>), dim3((uint32_t)nb), dim3(256), 0, s, gt, P, max_groups, sk, src, counter,
-                     err);
-}
-
-void launch_gather_groups(hipStream_t s, const uint64_t* sk, const uint32_t* src, uint64_t G, const GroupTables& gt,
-                          bool raw, const SortedGroups& out) {
-  if (G == 0) return;
-  hipLaunchKernelGGL(k_gather_groups, dim3((uint32_t)((G + 255) / 256)), dim3(256), 0, s, sk, src, G, gt, raw, out);
+  hipLaunchKernelGGL(k_compact_rows, dim3((uint32_t)nb), dim3(256), 0, s, gt, P, rows, err);
 }
 
 hipError_t set_kernel_smem_limits() {
   hipError_t e = hipFuncSetAttribute((const void*)k_pass_a_lds<512>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                      160 * 1024);
   if (e != hipSuccess) return e;
+  e = hipFuncSetAttribute((const void*)k_pass_a_lds32<1024>, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  if (e != hipSuccess) return e;
   e = hipFuncSetAttribute((const void*)k_pass_b_lds<1024, true>, hipFuncAttributeMaxDynamicSharedMemorySize,
                           160 * 1024);
   if (e != hipSuccess) return e;
-  return hipFuncSetAttribute((const void*)k_pass_b_lds<1024, false>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                             160 * 1024);
+  e = hipFuncSetAttribute((const void*)k_pass_b_lds<1024, false>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                          160 * 1024);
+  if (e != hipSuccess) return e;
+  return set_rows_smem_limits();
 }

@@ -16,7 +16,7 @@ from paper_2607_14541_amd import synth
 from test_oracle_bruteforce import random_trace
 
 pytestmark = pytest.mark.gpu
-ENGINES = ["lds_hash", "global_hash"]
+ENGINES = ["lds_hash", "global_hash", "radix_sort"]
 
 
 @pytest.mark.parametrize("path", ENGINES)
@@ -86,6 +86,19 @@ def test_config_prefix(path, ci, n):
                   score_key=keys, s=s, max_groups=2 * n, max_keys=n)
     o = O.run(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, cfg["num_phases"], score_key=keys, s=s)
     H.compare(g, o, score=True)
+
+
+def test_lds_engine_spill_overflow_falls_back_to_partitioning():
+    """1M distinct keys forced through the LDS engine: nearly every event
+    spills; with 8M events the per-workgroup spill regions overflow and the
+    whole pass is redone by the partition engine."""
+    cfg, ev, c = _config_case(2, 1 << 23)
+    H.say("spill overflow")
+    g = H.run_gpu(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, 4, path="lds_hash", raw=False,
+                  max_groups=1 << 23, max_keys=1 << 21)
+    assert g["path"] == "lds_hash+radix_all"
+    o = O.run(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, 4)
+    H.compare(g, o, raw=False)
 
 
 def test_repeat_runs_are_bit_identical():
