@@ -493,23 +493,8 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
                             c->at<uint32_t>(L.scount), scap, rows, c->err()));
     TIMED(c, "owner_merge", (uint64_t)nwg * ATREX_OWNERS,
           launch_owner_merge(s, c->owners(), nwg, P, c->p.raw, L.tabSlots, rows, c->err()));
-    uint32_t scount[kMaxWG];
-    (void)hipMemcpyAsync(hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr), hipMemcpyDeviceToHost, s);
-    (void)hipMemcpyAsync(scount, c->at<uint32_t>(L.scount), nwg * 4, hipMemcpyDeviceToHost, s);
-    st = sync_status(c);
-    if (st != ATREX_OK) return st;
-    if ((uint32_t)hdr[0] & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
-    uint64_t spilled = 0;
-    for (uint32_t w = 0; w < nwg; ++w) spilled += scount[w];
-    if ((uint32_t)hdr[0] & ATREX_ERRBIT_SPILL) {
-      // a spill region overflowed: partition every event instead
-      launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 64, 0);
-      c->path_used = "lds_hash+radix_all";
-      st = run_partition(c, d, scale, false, nwg, n, c->p.max_keys);
-    } else if (spilled) {
-      c->path_used = "lds_hash+radix_spill";
-      st = run_partition(c, d, scale, true, nwg, spilled, std::min<uint64_t>(c->p.max_keys, spilled));
-    }
+    // spilled events (counts stay on the device): partition engine
+    st = run_partition(c, d, scale, true, nwg, 0, c->p.max_keys);
     if (st != ATREX_OK) return st;
   } else if (path == ATREX_PATH_RADIX_SORT) {
     c->path_used = "radix_sort";
@@ -524,16 +509,33 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
           launch_pass_b_global(s, d, A, P, scale, gt, c->p.raw, (uint32_t)c->cus * 8, c->err()));
     TIMED(c, "compact_rows", L.capD * P, launch_compact_rows(s, gt, P, rows, c->err()));
   }
-  // rows -> groups ordered by (key, phase)
+  // rows -> groups ordered by (key, phase): one workgroup when they are few
+  unsigned long long* smallG = c->at<unsigned long long>(L.ctrl + 192);
+  uint32_t* smallDone = c->at<uint32_t>(L.ctrl + 200);
+  TIMED(c, "small_rows", 0, launch_small_rows(s, rows, c->groups(), smallG, smallDone));
   (void)hipMemcpyAsync(hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr), hipMemcpyDeviceToHost, s);
   st = sync_status(c);
   if (st != ATREX_OK) return st;
   if ((uint32_t)hdr[0] & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
+  if (path == ATREX_PATH_LDS_HASH && ((uint32_t)hdr[0] & ATREX_ERRBIT_SPILL)) {
+    // a spill region overflowed: partition every event instead
+    launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 64, 0);
+    c->path_used = "lds_hash+radix_all";
+    st = run_partition(c, d, scale, false, nwg, n, c->p.max_keys);
+    if (st != ATREX_OK) return st;
+    TIMED(c, "small_rows", 0, launch_small_rows(s, rows, c->groups(), smallG, smallDone));
+    (void)hipMemcpyAsync(hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr), hipMemcpyDeviceToHost, s);
+    st = sync_status(c);
+    if (st != ATREX_OK) return st;
+    if ((uint32_t)hdr[0] & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
+  }
   if ((uint32_t)hdr[0] & ATREX_ERRBIT_CAPACITY) return ATREX_E_CAPACITY;
   const uint64_t R = hdr[16];  // row counter at byte 128
   if (R > L.maxRows) return ATREX_E_CAPACITY;
   uint64_t G = 0;
-  if (R) {
+  if ((uint32_t)hdr[25]) {  // done by the one-workgroup kernel (flag at byte 200)
+    G = hdr[24];
+  } else if (R) {
     uint64_t* K0 = c->at<uint64_t>(L.sk[0]);
     uint32_t* V0 = c->at<uint32_t>(L.sv[0]);
     launch_iota_rows(s, rows, R, K0, V0);
@@ -554,9 +556,10 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
     G = (uint64_t)tail[0] + tail[1];
     if (G > L.maxG) return ATREX_E_CAPACITY;
     TIMED(c, "rows_reduce", G, launch_rows_reduce(s, rows, K0, V0, starts, G, c->groups()));
+    st = sync_status(c);
+    if (st != ATREX_OK) return st;
   }
-  st = sync_status(c);
-  if (st != ATREX_OK) return st;
+  if (G > L.maxG) return ATREX_E_CAPACITY;
   c->end_call();
   c->G = G;
   c->state = 1;
@@ -577,6 +580,27 @@ atrex_status atrex_phase_normalize(atrex_ctx* c, const atrex_groups* out, uint64
   c->begin_call();
   const SortedGroups g = c->groups();
   uint64_t* S = c->at<uint64_t>(L.S);
+  if (G <= small_n()) {  // one workgroup: totals, weights and both unit tables
+    unsigned long long* cnt = c->at<unsigned long long>(L.ctrl + 256);
+    uint32_t* done = c->at<uint32_t>(L.ctrl + 272);
+    UnitTable ot{c->at<uint32_t>(L.op_id), c->at<uint64_t>(L.op_U), c->at<double>(L.op_w)};
+    UnitTable kt{c->at<uint32_t>(L.key_id), c->at<uint64_t>(L.key_U), c->at<double>(L.key_w)};
+    TIMED(c, "small_normalize", G,
+          launch_small_normalize(s, g, G, P, lcm_1_to(P), S, out->key, out->phase, out->count, (uint64_t*)out->wsum,
+                                 (uint64_t*)out->raw_ns, out->weight, (uint64_t*)out->phase_total, ot, kt, cnt, done));
+    uint64_t h[4] = {0, 0, 0, 0};
+    (void)hipMemcpyAsync(h, cnt, sizeof(h), hipMemcpyDeviceToHost, s);
+    const atrex_status st = sync_status(c);
+    if (st != ATREX_OK) return st;
+    if ((uint32_t)h[2] != 1) return ATREX_E_DEVICE;
+    c->end_call();
+    c->nops = G ? h[0] : 0;
+    c->nkeys = G ? h[1] : 0;
+    if (num_ops) *num_ops = c->nops;
+    if (num_keys) *num_keys = c->nkeys;
+    c->state = 2;
+    return ATREX_OK;
+  }
   const uint32_t nb = (uint32_t)std::min<uint64_t>(1024, std::max<uint64_t>(1, (G + 255) / 256));
   TIMED(c, "phase_totals", G, launch_phase_totals(s, g, G, P, c->at<uint64_t>(L.partials), nb, S));
   TIMED(c, "group_weights", G,
@@ -652,6 +676,35 @@ atrex_status atrex_weighted_score(atrex_ctx* c, const uint32_t* score_key, const
   const Layout& L = c->L;
   hipStream_t s = c->s;
   c->begin_call();
+  if (n <= small_n()) {  // one workgroup: validation, duplicates, medians, Eq. (6)
+    launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 1, 0);
+    UnitTable opt{c->at<uint32_t>(L.op_id), c->at<uint64_t>(L.op_U), c->at<double>(L.op_w)};
+    uint64_t* tot = c->at<uint64_t>(L.total) + 4;
+    unsigned long long* nret = c->at<unsigned long long>(L.ctrl + 320);
+    // outputs go straight to the caller's arrays when given, else to scratch
+    uint32_t* o_op = op ? op : c->at<uint32_t>(L.r_op);
+    double* o_w = op_weight ? op_weight : c->at<double>(L.sk[0]);
+    double* o_s = op_score ? op_score : c->at<double>(L.sk[1]);
+    TIMED(c, "small_score", n,
+          launch_small_score(s, score_key, sv, n, opt, c->nops, o_op, o_w, o_s, c->sagg(), tot, nret,
+                             c->at<uint64_t>(L.r_U), c->err()));
+    uint64_t h[4] = {0, 0, 0, 0};
+    uint32_t e = 0;
+    double sa = 0.0;
+    (void)hipMemcpyAsync(&e, c->err(), 4, hipMemcpyDeviceToHost, s);
+    (void)hipMemcpyAsync(h, tot, 16, hipMemcpyDeviceToHost, s);
+    (void)hipMemcpyAsync(&h[2], nret, 8, hipMemcpyDeviceToHost, s);
+    (void)hipMemcpyAsync(&sa, c->sagg(), 8, hipMemcpyDeviceToHost, s);
+    const atrex_status st = sync_status(c);
+    if (st != ATREX_OK) return st;
+    if (e & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
+    if (e & ATREX_ERRBIT_DUP) return ATREX_E_INVALID_ARG;
+    if (h[0] == 0 && h[1] == 0) return ATREX_E_INVALID_ARG;  // no retained weight
+    c->end_call();
+    *s_agg = sa;
+    if (num_ops) *num_ops = h[2];
+    return ATREX_OK;
+  }
   uint64_t *K0 = c->at<uint64_t>(L.sk[0]), *K1 = c->at<uint64_t>(L.sk[1]), *K2 = c->at<uint64_t>(L.sk[2]);
   uint32_t *V0 = c->at<uint32_t>(L.sv[0]), *V1 = c->at<uint32_t>(L.sv[1]), *V2 = c->at<uint32_t>(L.sv[2]);
   void* rtmp = c->at<void>(L.rs_tmp);

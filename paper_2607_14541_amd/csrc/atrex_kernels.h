@@ -158,3 +158,16 @@ void launch_score_ops(hipStream_t s, const uint32_t* score_key, const double* S,
 void launch_score_final(hipStream_t s, const uint32_t* r_op, const uint64_t* r_U, const double* r_S,
                         uint64_t nops, const uint64_t* totalU, uint32_t* op, double* op_weight, double* op_score,
                         double* s_agg, uint32_t* err);
+
+// kernels_small.hip (one workgroup, sizes up to small_n(); *done = 0 when larger)
+uint32_t small_n();
+uint32_t small_rows_n();
+void launch_small_rows(hipStream_t s, const Rows& rows, const SortedGroups& out, unsigned long long* G_out,
+                       uint32_t* done);
+void launch_small_normalize(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t L, uint64_t* S_out,
+                            uint32_t* okey, uint8_t* oph, uint64_t* ocount, uint64_t* owsum, uint64_t* oraw,
+                            double* oweight, uint64_t* oS, UnitTable ops, UnitTable keys,
+                            unsigned long long* counts, uint32_t* done);
+void launch_small_score(hipStream_t s, const uint32_t* score_key, const double* S, uint64_t n, UnitTable opt,
+                        uint64_t nops_trace, uint32_t* op_out, double* w_out, double* s_out, double* s_agg,
+                        uint64_t* totU, unsigned long long* nret, uint64_t* rU, uint32_t* err);
