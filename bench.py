@@ -26,9 +26,14 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E peak, GB/s
 BYTES_PASS_A = 13              # app u32 + phase u8 + dur i64 per event
 BYTES_PASS_B = 17              # key u32 + app u32 + phase u8 + dur i64 per event
+# algorithmic HBM bytes per event of the streaming kernels: the event fields
+# each one must read, plus the 16-byte partition records written and re-read
 KERNEL_BYTES = {"pass_a": BYTES_PASS_A, "pass_a_global": BYTES_PASS_A,
-                "pass_b_lds": BYTES_PASS_B, "pass_b_global": BYTES_PASS_B}
+                "pass_b_lds": BYTES_PASS_B, "pass_b_global": BYTES_PASS_B,
+                "part_hist": 4, "part_scatter": BYTES_PASS_B + 16, "part_aggregate": 16}
 KERNEL_SOURCES = ["paper_2607_14541_amd/csrc/kernels_aggregate.hip",
+                  "paper_2607_14541_amd/csrc/kernels_rows.hip",
+                  "paper_2607_14541_amd/csrc/atrex_kernels.h",
                   "paper_2607_14541_amd/csrc/atrex_device.hpp"]
 
 
@@ -44,11 +49,11 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_from_profile(config_id: int, kernel: str, n: int):
+def traffic_from_profile(slug: str, kernel: str, n: int):
     """HBM bytes per launch from committed rocprofv3 counter summaries, or
     None when none exists for this kernel/workload or the kernel source has
     changed since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", "traffic_c%d.json" % config_id)
+    path = os.path.join(ROOT, "profiles", "traffic_%s.json" % slug)
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
@@ -156,7 +161,7 @@ def main() -> int:
     dom = max((k for k in kernels if k in KERNEL_BYTES), key=lambda k: kernels[k]["avg_ms"])
     alg = KERNEL_BYTES[dom] * n
     achieved = alg / (kernels[dom]["avg_ms"] * 1e-3) / 1e9
-    traffic = traffic_from_profile(args.config, dom, n)
+    traffic = traffic_from_profile(cfg["slug"], dom, n)
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "algorithmic_bytes_per_launch": alg, "avg_launch_ms": round(kernels[dom]["avg_ms"], 4)}

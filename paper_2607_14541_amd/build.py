@@ -14,6 +14,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libatrex.so")
+# plain 1 GiB copy, the known-size kernel the HBM byte counters are scaled by
+COPY_CAL = os.path.join(HERE, "copy_calibration")
 BUILD_DIR = os.path.join(HERE, "_build")
 
 HIP_SOURCES = ["atrex_host.hip", "kernels_aggregate.hip", "kernels_rows.hip", "kernels_util.hip",
@@ -50,9 +52,17 @@ def build_lib() -> str:
     return LIB
 
 
+def build_copy_calibration() -> str:
+    tmp = COPY_CAL + ".tmp%d" % os.getpid()
+    subprocess.check_call([HIPCC, *HIP_FLAGS, "-o", tmp, os.path.join(CSRC, "copy_calibration.hip")])
+    os.replace(tmp, COPY_CAL)
+    return COPY_CAL
+
+
 def build_all() -> None:
     from . import synth
     build_lib()
+    build_copy_calibration()
     synth.build(force=True)
 
 

@@ -38,20 +38,20 @@ class _Cfg(ctypes.Structure):
 
 
 CONFIGS = {
-    0: dict(name="1M events, 512 uniform keys, 2 phases, 64 apps", n=1 << 20, seed=0,
+    0: dict(name="1M events, 512 uniform keys, 2 phases, 64 apps", slug="1M_uniform512", n=1 << 20, seed=0,
             key_mode=0, num_ops=32, num_shapes=16, num_phases=2, num_apps=64,
             dur_mode=0, mu=math.log(2e4), sigma=1.5, weights="uniform"),
-    1: dict(name="64M events, 4096 Zipf(1.1) keys, 2 phases 60/40, 1024 apps", n=1 << 26,
+    1: dict(name="64M events, 4096 Zipf(1.1) keys, 2 phases 60/40, 1024 apps", slug="64M_zipf4096", n=1 << 26,
             seed=1, key_mode=1, zipf_n=4096, zipf_s=1.1, shape_bits=6, num_phases=2,
             phase0_frac=0.6, num_apps=1024, dur_mode=0, mu=math.log(5e4), sigma=2.0,
             weights="zipf", weights_s=1.1),
-    2: dict(name="256M events, 1M uniform keys, 4 phases, 10k apps", n=1 << 28, seed=2,
+    2: dict(name="256M events, 1M uniform keys, 4 phases, 10k apps", slug="256M_uniform1M", n=1 << 28, seed=2,
             key_mode=0, num_ops=1024, num_shapes=1024, num_phases=4, num_apps=10000,
             dur_mode=0, mu=math.log(1e4), sigma=2.5, weights="uniform"),
-    3: dict(name="1B events, 64k Zipf(0.9) keys, 3 phases, 100k apps", n=1 << 30, seed=3,
+    3: dict(name="1B events, 64k Zipf(0.9) keys, 3 phases, 100k apps", slug="1B_zipf64k", n=1 << 30, seed=3,
             key_mode=1, zipf_n=65536, zipf_s=0.9, shape_bits=8, num_phases=3,
             num_apps=100000, dur_mode=0, mu=math.log(3e4), sigma=2.0, weights="lognormal"),
-    4: dict(name="512M adversarial events, 99% on one key, durations in [2^39, 2^40]",
+    4: dict(name="512M adversarial events, 99% on one key, durations in [2^39, 2^40]", slug="512M_adversarial",
             n=1 << 29, seed=4, key_mode=2, hot_p=0.99, tail_n=1 << 18, shape_bits=10,
             op_base=1, num_phases=2, num_apps=4, dur_mode=1, dur_lo=1 << 39,
             dur_hi=1 << 40, weights="uniform"),
