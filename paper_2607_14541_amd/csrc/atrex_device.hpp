@@ -53,6 +53,34 @@ __device__ __forceinline__ void event_share_rs(uint64_t d, uint64_t sw, int s, u
   vhi = hi >> s;
 }
 
+// --- pass-B scale word ------------------------------------------------------
+// bits 0..55 = m, bits 56..63 = u = 63 - rho for rho in [-8, 63] (u in [0, 71]),
+// so that v = floor(d * (m * 2^8) / 2^u); u = 255 marks the rare rho outside
+// [-8, 63], which takes the general scale word.  0 = no share.
+#define ATREX_BSCALE_SLOW 255u
+__device__ __forceinline__ uint64_t bscale_pack(uint64_t m, int rho) {
+  const uint64_t u = (rho >= -8 && rho <= 63) ? (uint64_t)(63 - rho) : (uint64_t)ATREX_BSCALE_SLOW;
+  return (u << 56) | m;
+}
+
+// Share of an event with d < 2^32 from a pass-B word (u <= 71), given as its
+// two 32-bit halves: Y = d * (m * 2^8) < 2^96 in three words from two
+// 32 x 32 -> 64-bit products, then v = Y >> u (< 2^96) by selecting words on
+// bits 5 and 6 of u and funnel-shifting by u mod 32.
+__device__ __forceinline__ void bscale_share32(uint32_t d, uint32_t elo, uint32_t ehi, uint64_t& vlo,
+                                               uint32_t& vhi) {
+  const uint32_t u = ehi >> 24;
+  const uint32_t M0 = elo << 8, M1 = __builtin_amdgcn_alignbit(ehi & 0xFFFFFFu, elo, 24u);
+  const uint64_t p0 = (uint64_t)d * M0;
+  const uint64_t p1 = (uint64_t)d * M1 + (p0 >> 32);
+  const uint32_t y0 = (uint32_t)p0, y1 = (uint32_t)p1, y2 = (uint32_t)(p1 >> 32);
+  const bool b1 = (u & 32u) != 0, b2 = (u & 64u) != 0;
+  const uint32_t g0 = b1 ? y1 : y0, g1 = b1 ? y2 : y1, g2 = b1 ? 0u : y2;
+  const uint32_t f0 = b2 ? g2 : g0, f1 = b2 ? 0u : g1, f2 = b2 ? 0u : g2;
+  vlo = ((uint64_t)__builtin_amdgcn_alignbit(f2, f1, u) << 32) | __builtin_amdgcn_alignbit(f1, f0, u);
+  vhi = f2 >> (u & 31u);
+}
+
 // --- u128 -> fp64, round to nearest, ties to even (IEEE 754 conversion) -----
 __device__ __forceinline__ double u128_to_f64(u128 x) {
   const uint64_t hi = (uint64_t)(x >> 64);

@@ -37,7 +37,7 @@ uint64_t next_pow2(uint64_t x) {
 
 // Byte offsets of every workspace region (all 256-byte aligned).
 struct Layout {
-  size_t ctrl, T, carryA, partA, scale, dict, acc, raw;
+  size_t ctrl, T, carryA, partA, scale, bscale, dict, acc, raw;
   size_t okey, oacc, oraw, ocount, skey, sval, sraw, scount;  // LDS engine outputs
   size_t H, O, rec, rraw, bstart, istart;                     // partition engine
   size_t rk, rlo_acc, rhi_acc, rlo_raw, rhi_raw;              // rows
@@ -95,6 +95,7 @@ Layout make_layout(const Params& p) {
   L.carryA = take(GA * 8);
   L.partA = take(L.partA_rows * GA * (L.passA == 0 ? 8 : 4));
   L.scale = take(GA * 8);
+  L.bscale = take(GA * 8);
   L.dict = take(L.capD * 8);
   L.acc = take(L.capD * p.P * 16);
   L.raw = take(p.raw ? L.capD * p.P * 16 : 0);
@@ -475,7 +476,7 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
   }
   // scale, Eq. (3)
   uint64_t* scale = c->at<uint64_t>(L.scale);
-  TIMED(c, "scale", GA, launch_scale(s, T, c->app_weight, c->Csum(), A, P, scale));
+  TIMED(c, "scale", GA, launch_scale(s, T, c->app_weight, c->Csum(), A, P, scale, c->at<void>(L.bscale)));
   // pass B, Eq. (2)-(3): every engine emits rows (key << 3 | phase, Q96 sum)
   const Rows rows = c->rows();
   atrex_path path = c->path;
@@ -488,7 +489,7 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
     c->path_used = "lds_hash";
     const uint32_t scap = spill_cap(n, nwg);
     TIMED(c, "pass_b_lds", n,
-          launch_pass_b_lds(s, d, A, P, scale, c->p.raw, L.ldsSlots, nwg, c->owners(), c->at<uint32_t>(L.skey),
+          launch_pass_b_lds(s, d, A, P, scale, c->at<void>(L.bscale), c->p.raw, L.ldsSlots, nwg, c->owners(), c->at<uint32_t>(L.skey),
                             c->at<uint64_t>(L.sval), c->p.raw ? c->at<uint64_t>(L.sraw) : nullptr,
                             c->at<uint32_t>(L.scount), scap, rows, c->err()));
     TIMED(c, "owner_merge", (uint64_t)nwg * ATREX_OWNERS,

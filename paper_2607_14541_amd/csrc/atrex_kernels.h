@@ -79,8 +79,9 @@ void launch_pass_a_reduce32(hipStream_t s, const uint32_t* partial, uint32_t nb,
 void launch_pass_a_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
                           unsigned long long* T, uint32_t* err);
 void launch_unpack_scale(hipStream_t s, const uint64_t* sw, uint64_t G, uint64_t* mant, int32_t* rho);
+// scale words (general form) and the 16-byte pass-B entries
 void launch_scale(hipStream_t s, const uint64_t* T, const uint32_t* c, const uint64_t* Csum, uint32_t A,
-                  uint32_t P, uint64_t* scale);
+                  uint32_t P, uint64_t* scale, void* bscale);
 void launch_pass_b_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, const uint64_t* scale,
                           const GroupTables& gt, bool raw, uint32_t nblocks, uint32_t* err);
 // LDS hash engine
@@ -88,8 +89,8 @@ uint32_t pass_b_lds_slots(uint32_t P, bool raw, size_t lds_bytes);
 size_t pass_b_lds_smem(uint32_t P, bool raw, uint32_t S);
 uint32_t spill_cap(uint64_t n, uint32_t nwg);
 uint32_t owner_cap(uint32_t S);
-void launch_pass_b_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, const uint64_t* scale, bool raw,
-                       uint32_t S, uint32_t nblocks, const OwnerRegions& orr, uint32_t* spill_key,
+void launch_pass_b_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, const uint64_t* scale,
+                       const void* bscale, bool raw, uint32_t S, uint32_t nblocks, const OwnerRegions& orr, uint32_t* spill_key,
                        uint64_t* spill_val, uint64_t* spill_raw, uint32_t* spill_count, uint32_t scap,
                        const Rows& rows, uint32_t* err);
 void launch_compact_rows(hipStream_t s, const GroupTables& gt, uint32_t P, const Rows& rows, uint32_t* err);

@@ -232,13 +232,14 @@ __device__ __forceinline__ void w256_sub_inplace(W256& a, const W256& b) {
 
 __global__ void k_scale(const uint64_t* __restrict__ T, const uint32_t* __restrict__ c,
                         const uint64_t* __restrict__ Csum, uint32_t A, uint32_t P,
-                        uint64_t* __restrict__ scale) {
+                        uint64_t* __restrict__ scale, uint64_t* __restrict__ bscale) {
   const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
   if (g >= A * P) return;
   const u128 t = make_u128(T[2 * g], T[2 * g + 1]);
   const uint32_t ca = c[g / P];
   if (t == 0 || ca == 0) {
     scale[g] = 0;
+    bscale[g] = 0;
     return;
   }
   const uint64_t C = *Csum;
@@ -279,6 +280,7 @@ __global__ void k_scale(const uint64_t* __restrict__ T, const uint32_t* __restri
     m = q;
   }
   scale[g] = scale_pack(m, rho);
+  bscale[g] = bscale_pack(m, rho);
 }
 
 // ---------------------------------------------------------------------------
@@ -332,16 +334,19 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_global(EventsDev ev, uint32_t 
 
 // ---------------------------------------------------------------------------
 // Pass B with a per-workgroup LDS hash table (the low/medium-cardinality
-// engine).  LDS holds S slots (S sized to the LDS budget, not a power of two):
-// a key tag and, per phase, a two-word accumulator.  Per event: linear probing
-// from mulhi(hash(key), S), at most MAXPROBE slots; an event whose key finds
-// no slot (or the reserved tag value) is appended to a spill list and handled
-// after the kernel, so that no wave waits on device-wide atomics.  Before the
-// LDS atomics, lanes of a wave that hit the same (slot, phase) as the wave's
-// first active lane are summed with shuffles and added once (hot keys).
-// At the end each workgroup writes its table into 256 owner regions (owner =
-// top byte of the key hash); k_owner_merge sums each owner's regions.
-constexpr uint32_t MAXPROBE = 16;
+// engine).  LDS holds S slots in buckets of four (S sized to the LDS budget,
+// not a power of two): a key tag and, per phase, a two-word accumulator.  Per
+// event: the home bucket's four tags are read with one 16-byte LDS load and
+// compared; a key absent from its bucket is looked up in the following
+// buckets and inserted into the first free slot (at most MAXPROBE buckets); an
+// event whose key finds no slot (or the reserved tag value) is appended to a
+// spill list and handled after the kernel, so that no wave waits on
+// device-wide atomics.  Before the LDS atomics, lanes of a wave that hit the
+// same (slot, phase) as the wave's first active lane are summed with shuffles
+// and added once (hot keys).  At the end each workgroup writes its table into
+// 256 owner regions (owner = top byte of the key hash); k_owner_merge sums
+// each owner's regions.
+constexpr uint32_t MAXPROBE = 8;  // buckets
 constexpr uint32_t INVALID_GI = 0xFFFFFFFFu;
 
 
@@ -404,104 +409,154 @@ __device__ __forceinline__ void row_push(const Rows& R, bool want, uint64_t rk, 
   }
 }
 
+// Events of one group of four per lane, once their scale words and first-probe
+// tags have been requested: everything the accumulation step needs.
+struct StagedEv4 {
+  uint32_t key[4], bucket[4];
+  uint32_t ph4;        // the four phases, one byte each
+  int64_t dur[4];
+  uint64_t sw[4];      // pass-B scale words
+};
+
 template <int BLOCK, bool RAW>
-__global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t A, uint32_t P,
-                                                      const uint64_t* __restrict__ scale, uint32_t S,
+__global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, const uint64_t* __restrict__ scale,
+                                                      const uint64_t* __restrict__ bscale, uint32_t S,
                                                       OwnerRegions orr, SpillList sp, Rows rows,
                                                       uint32_t* __restrict__ err) {
   extern __shared__ unsigned long long smem[];
   const uint32_t SP = S * P;
-  unsigned long long* s_lo = smem;
-  unsigned long long* s_hi = smem + SP;
-  unsigned long long* r_lo = smem + 2 * SP;  // RAW only
-  unsigned long long* r_hi = smem + 3 * SP;  // RAW only
-  uint32_t* s_tag = (uint32_t*)(smem + (RAW ? 4 : 2) * SP);
-  uint32_t* s_ocnt = s_tag + S;                      // [ATREX_OWNERS]
-  uint32_t& s_spills = s_ocnt[ATREX_OWNERS];         // dynamic LDS: static LDS would not fit beside 160 KB
-  if (threadIdx.x == 0) s_spills = 0;
-  for (uint32_t i = threadIdx.x; i < SP; i += BLOCK) {
-    s_lo[i] = 0;
-    s_hi[i] = 0;
-    if (RAW) { r_lo[i] = 0; r_hi[i] = 0; }
+  // [S * P] x (lo, hi) interleaved, then 64 per-lane dummy entries that take
+  // the atomics of lanes with nothing to add (never read); RAW: the same again
+  const uint32_t region = 2 * SP + 2 * 64;
+  unsigned long long* s_acc = smem;
+  unsigned long long* s_raw = smem + region;    // RAW only
+  uint32_t* s_tag = (uint32_t*)(smem + (RAW ? 2 : 1) * region);
+  uint32_t* s_ocnt = s_tag + S;                 // [ATREX_OWNERS]
+  uint32_t& s_spills = s_ocnt[ATREX_OWNERS];    // dynamic LDS: static LDS would not fit beside 160 KB
+  // Pass A has validated every event (app < A, phase < P, dur >= 0) and the
+  // call fails on a range error, so the loop below takes the fields as valid;
+  // after a range error this kernel only publishes empty regions.
+  const bool range_error = (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
+                            ATREX_ERRBIT_RANGE) != 0;
+  if (range_error) {
+    for (uint32_t o = threadIdx.x; o < ATREX_OWNERS; o += BLOCK) orr.count[(size_t)blockIdx.x * ATREX_OWNERS + o] = 0;
+    if (threadIdx.x == 0) sp.count[blockIdx.x] = 0;
+    return;
   }
+  if (threadIdx.x == 0) s_spills = 0;
+  for (uint32_t i = threadIdx.x; i < 2 * SP; i += BLOCK) {
+    s_acc[i] = 0;
+    if (RAW) s_raw[i] = 0;
+  }
+  const uint32_t dummy = 2 * SP + 2 * (threadIdx.x & 63);  // this lane's dummy entry
   for (uint32_t i = threadIdx.x; i < S; i += BLOCK) s_tag[i] = ATREX_EMPTY_KEY;
   for (uint32_t i = threadIdx.x; i < ATREX_OWNERS; i += BLOCK) s_ocnt[i] = 0;
   __syncthreads();
   const uint64_t n = ev.n, n4 = n / 4;
   const uint64_t stride = (uint64_t)gridDim.x * BLOCK;
   const uint32_t lane = lane_id();
-  bool bad = false;
-  // Slot of key k (linear probing); INVALID_GI when not placed.  Probing past
-  // the first slot is the rare path and is kept as a plain loop.
-  auto find_slot = [&](uint32_t k, uint32_t h, uint32_t t) -> uint32_t {
+  const uint32_t NB = S / 4;     // buckets; S is a multiple of 4
+  const uint32_t NB8 = NB << 8;  // bucket = mulhi24(hash >> 8, NB << 8) = floor((hash >> 8) * NB / 2^24), NB < 2^16
+  auto bucket_tags = [&](uint32_t b) -> uint4 { return *(const uint4*)&s_tag[4 * b]; };
+  // Slot of key k from its home bucket b (tags tv already read): the key's
+  // slot in this or a following bucket, else the first free slot claimed for
+  // it; INVALID_GI when not placed within MAXPROBE buckets.  Two lanes may
+  // claim two slots for one key in a race; both then accumulate and the owner
+  // merge adds them up.  The rare path: a plain loop, at most 4 retries per
+  // bucket (each failed claim fills a slot).
+  auto find_slot = [&](uint32_t k, uint32_t b, uint4 tv) -> uint32_t {
+    uint32_t probe = 0;
 #pragma unroll 1
-    for (uint32_t probe = 0;;) {
-      if (t == ATREX_EMPTY_KEY) t = atomicCAS(&s_tag[h], ATREX_EMPTY_KEY, k);
-      if (t == k || t == ATREX_EMPTY_KEY) return h;
-      if (++probe == MAXPROBE) return INVALID_GI;
-      h = (h + 1 == S) ? 0 : h + 1;
-      t = s_tag[h];
+    for (uint32_t step = 0; step < 8 * MAXPROBE; ++step) {
+      if (tv.x == k) return 4 * b;
+      if (tv.y == k) return 4 * b + 1;
+      if (tv.z == k) return 4 * b + 2;
+      if (tv.w == k) return 4 * b + 3;
+      const uint32_t e = tv.x == ATREX_EMPTY_KEY ? 0u : tv.y == ATREX_EMPTY_KEY ? 1u
+                       : tv.z == ATREX_EMPTY_KEY ? 2u : tv.w == ATREX_EMPTY_KEY ? 3u : 4u;
+      if (e < 4) {
+        const uint32_t t = atomicCAS(&s_tag[4 * b + e], ATREX_EMPTY_KEY, k);
+        if (t == ATREX_EMPTY_KEY || t == k) return 4 * b + e;
+      } else {
+        if (++probe == MAXPROBE) return INVALID_GI;
+        b = (b + 1 == NB) ? 0 : b + 1;
+      }
+      tv = bucket_tags(b);
     }
+    return INVALID_GI;
   };
-  // Four events per lane (all lanes of the wave together): validation, then
-  // four unconditional scale gathers (index clamped to 0 when invalid), the
-  // first-probe LDS reads, the shares, the slots, then accumulation.
-  auto batch = [&](const bool valid[4], const uint32_t k[4], const uint32_t a[4], const uint32_t ph[4],
-                   const int64_t d[4], uint64_t base) {
-    bool ok[4];
-    uint64_t sw[4];
-    uint32_t h[4], t[4];
+  // stage(): request the scale words of a loaded group, keep what the
+  // accumulation step needs.
+  auto stage = [&](const Ev4& e, StagedEv4& g) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      ok[j] = valid[j] && a[j] < A && ph[j] < P && d[j] >= 0;
-      bad |= valid[j] && !ok[j];
+      g.sw[j] = bscale[e.app[j] * P + e.ph[j]];
+      g.bucket[j] = (uint32_t)(((uint64_t)(hash_mul(e.key[j]) >> 8) * (NB8 & 0xFFFFFFu)) >> 32);
+      g.key[j] = e.key[j];
+      g.dur[j] = e.dur[j];
     }
+    g.ph4 = e.ph[0] | (e.ph[1] << 8) | (e.ph[2] << 16) | (e.ph[3] << 24);
+  };
+  // process(): shares, slots, accumulation of a staged group.  `first` is the
+  // index of event 0 (for the rare paths that re-read an event's fields).
+  auto process = [&](const bool valid[4], const StagedEv4& g, uint64_t first) {
+    uint4 tv[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) sw[j] = scale[ok[j] ? (size_t)a[j] * P + ph[j] : 0];
+    for (int j = 0; j < 4; ++j) tv[j] = bucket_tags(g.bucket[j]);
+    uint32_t ph[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      h[j] = __umulhi(hash_mul(k[j]), S);
-      t[j] = s_tag[h[j]];
-    }
-    u128 v[4];
-    int rs[4];
-    bool fast = true;
+    for (int j = 0; j < 4; ++j) ph[j] = (g.ph4 >> (8 * j)) & 0xFFu;
+    uint64_t vlo[4], vhi[4];
+    uint32_t slow = 0;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      sw[j] = ok[j] ? sw[j] : 0;
-      rs[j] = share_rshift(sw[j]);
-      fast &= rs[j] >= 0 || sw[j] == 0;
-    }
-    if (__all(fast)) {  // wave-uniform: one 64x64 product and a funnel shift each
+    for (int j = 0; j < 4; ++j) slow |= (uint32_t)((uint64_t)g.dur[j] >> 32) | ((uint32_t)(g.sw[j] >> 56) & ~127u);
+    if (__builtin_expect(__any(slow != 0), 0)) {  // a duration >= 2^32 ns, or rho outside [-8, 63]
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        uint64_t lo, hi;
-        event_share_rs((uint64_t)d[j], sw[j], rs[j] < 0 ? 0 : rs[j], lo, hi);
-        v[j] = make_u128(lo, hi);
+        const uint64_t i = valid[j] ? first + j : 0;
+        const u128 v = event_share((uint64_t)g.dur[j], valid[j] ? scale[ev.app[i] * P + ph[j]] : 0);
+        vlo[j] = (uint64_t)v;
+        vhi[j] = (uint64_t)(v >> 64);
       }
     } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) v[j] = event_share((uint64_t)d[j], sw[j]);
+      for (int j = 0; j < 4; ++j) {
+        uint32_t hi32;
+        bscale_share32((uint32_t)g.dur[j], (uint32_t)g.sw[j], (uint32_t)(g.sw[j] >> 32), vlo[j], hi32);
+        vhi[j] = hi32;
+      }
     }
     uint32_t gi[4];
+    bool miss = false;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      gi[j] = INVALID_GI;
-      if (ok[j] && k[j] != ATREX_EMPTY_KEY) {
-        const uint32_t slot = (t[j] == k[j]) ? h[j] : find_slot(k[j], h[j], t[j]);
-        if (slot != INVALID_GI) gi[j] = slot * P + ph[j];
-      }
-      spill_append(sp, &s_spills, ok[j] && gi[j] == INVALID_GI, k[j], v[j], ph[j], (uint64_t)d[j], err);
+      const uint32_t k = g.key[j];
+      const uint32_t w = tv[j].x == k ? 0u : tv[j].y == k ? 1u : tv[j].z == k ? 2u : 3u;
+      const bool hit = (tv[j].w == k || w < 3) && k != ATREX_EMPTY_KEY;
+      gi[j] = (valid[j] && hit) ? __umul24(4 * g.bucket[j] + w, P) + ph[j] : INVALID_GI;
+      miss |= valid[j] && !hit;
     }
-    // hot group: when many lanes share the first lane's (slot, phase) in the
-    // first event slot, lanes sharing a group are summed with shuffles first
+    if (__builtin_expect(__any(miss), 0)) {  // key not in its home bucket: probe on, then spill what is unplaced
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (valid[j] && gi[j] == INVALID_GI && g.key[j] != ATREX_EMPTY_KEY) {
+          const uint32_t sl = find_slot(g.key[j], g.bucket[j], tv[j]);
+          if (sl != INVALID_GI) gi[j] = __umul24(sl, P) + ph[j];
+        }
+        spill_append(sp, &s_spills, valid[j] && gi[j] == INVALID_GI, g.key[j], make_u128(vlo[j], vhi[j]), ph[j],
+                     (uint64_t)g.dur[j], err);
+      }
+    }
+    // hot group: when at least half the lanes share the first lane's (slot,
+    // phase) in the first event slot, lanes sharing a group are summed with
+    // shuffles first (a milder skew costs less as LDS atomic conflicts)
     bool hot = false;
     {
       const uint64_t act = __ballot(gi[0] != INVALID_GI);
       if (act) {
-        const uint32_t first = __ffsll((unsigned long long)act) - 1;
-        const uint32_t lead = __shfl(gi[0], first, 64);
-        hot = __popcll(__ballot(gi[0] == lead)) >= 8;
+        const uint32_t fl = __ffsll((unsigned long long)act) - 1;
+        const uint32_t lead = __builtin_amdgcn_readlane(gi[0], fl);
+        hot = __popcll(__ballot(gi[0] == lead)) >= 32;
       }
     }
     if (hot) {
@@ -509,14 +564,14 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t A, 
       for (int j = 0; j < 4; ++j) {
         const uint64_t act = __ballot(gi[j] != INVALID_GI);
         if (act == 0) continue;
-        const uint32_t first = __ffsll((unsigned long long)act) - 1;
-        const uint32_t lead = __shfl(gi[j], first, 64);
+        const uint32_t fl = __ffsll((unsigned long long)act) - 1;
+        const uint32_t lead = __builtin_amdgcn_readlane(gi[j], fl);
         const uint64_t same = __ballot(gi[j] == lead);
-        if (__popcll(same) < 4) continue;
+        if (__popcll(same) < 16) continue;
         const bool mine = gi[j] == lead;
-        const u128 tot = wave_sum_u128(mine ? v[j] : (u128)0);
+        const u128 tot = wave_sum_u128(mine ? make_u128(vlo[j], vhi[j]) : (u128)0);
         u128 rtot = 0;
-        if (RAW) rtot = wave_sum_u128(mine ? (u128)(uint64_t)d[j] : (u128)0);
+        if (RAW) rtot = wave_sum_u128(mine ? (u128)(uint64_t)g.dur[j] : (u128)0);
         const uint64_t tlo = __shfl((unsigned long long)(uint64_t)tot, 0, 64);
         const uint64_t thi = __shfl((unsigned long long)(uint64_t)(tot >> 64), 0, 64);
         uint64_t rlo = 0, rhi = 0;
@@ -524,39 +579,84 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t A, 
           rlo = __shfl((unsigned long long)(uint64_t)rtot, 0, 64);
           rhi = __shfl((unsigned long long)(uint64_t)(rtot >> 64), 0, 64);
         }
-        if (lane == first) {
-          acc_add_n(&s_lo[lead], &s_hi[lead], make_u128(tlo, thi), __popcll(same));
-          if (RAW) acc_add_plain(&r_lo[lead], &r_hi[lead], make_u128(rlo, rhi));
+        if (lane == fl) {
+          acc_add_n(&s_acc[2 * lead], &s_acc[2 * lead + 1], make_u128(tlo, thi), __popcll(same));
+          if (RAW) acc_add_plain(&s_raw[2 * lead], &s_raw[2 * lead + 1], make_u128(rlo, rhi));
         }
         if (mine) gi[j] = INVALID_GI;
       }
     }
+    // accumulate without branches: a lane with nothing to add for an event
+    // adds into its own dummy entry.  The four low-word atomics go first (their
+    // returned values give the carries), then the high words with the count.
+    uint32_t at[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) at[j] = gi[j] != INVALID_GI ? 2 * gi[j] : dummy;
+    unsigned long long old[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) old[j] = atomicAdd(&s_acc[at[j]], (unsigned long long)vlo[j]);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      if (gi[j] == INVALID_GI) continue;
-      acc_add(&s_lo[gi[j]], &s_hi[gi[j]], v[j]);
-      if (RAW) acc_add_plain(&r_lo[gi[j]], &r_hi[gi[j]], (u128)(uint64_t)d[j]);
+      const unsigned long long carry = (old[j] + vlo[j] < old[j]) ? 1ull : 0ull;
+      atomicAdd(&s_acc[at[j] + 1], (unsigned long long)vhi[j] + carry + (1ull << ATREX_COUNT_SHIFT));
+    }
+    if (RAW) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) old[j] = atomicAdd(&s_raw[at[j]], (unsigned long long)g.dur[j]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (old[j] + (uint64_t)g.dur[j] < old[j]) atomicAdd(&s_raw[at[j] + 1], 1ull);
     }
   };
-  // wave-uniform trip count: a lane past the end processes nothing
+  // Grid-stride over groups of four events with a wave-uniform trip count, as
+  // a three-stage pipeline: while group i is accumulated, the scale words and
+  // tags of group i + 1 and the loads of group i + 2 are in flight.  Indices
+  // are clamped to the last group, so every load is in bounds; `valid` masks
+  // the lanes past the end.
   const uint64_t wave_first = (uint64_t)blockIdx.x * BLOCK + (threadIdx.x & ~63u);
-  for (uint64_t qw = wave_first; qw < n4; qw += stride) {
-    const uint64_t q = qw + lane;
-    const bool v4 = q < n4;
-    Ev4 e;
-    if (v4) load4<true>(ev.key, ev.app, ev.phase, ev.dur, q * 4, e);
-    const bool valid[4] = {v4, v4, v4, v4};
-    batch(valid, e.key, e.app, e.ph, e.dur, q * 4);
+  if (wave_first < n4) {
+    const uint64_t last = n4 - 1;
+    uint64_t q = wave_first + lane, qw = wave_first;
+    Ev4 raw;
+    StagedEv4 gA, gB;
+    load4<true>(ev.key, ev.app, ev.phase, ev.dur, min(q, last) * 4, raw);
+    stage(raw, gA);
+    load4<true>(ev.key, ev.app, ev.phase, ev.dur, min(q + stride, last) * 4, raw);
+    for (;;) {
+      stage(raw, gB);
+      load4<true>(ev.key, ev.app, ev.phase, ev.dur, min(q + 2 * stride, last) * 4, raw);
+      {
+        const bool v = q < n4;
+        const bool valid[4] = {v, v, v, v};
+        process(valid, gA, min(q, last) * 4);
+      }
+      qw += stride;
+      q += stride;
+      if (qw >= n4) break;
+      stage(raw, gA);
+      load4<true>(ev.key, ev.app, ev.phase, ev.dur, min(q + 2 * stride, last) * 4, raw);
+      {
+        const bool v = q < n4;
+        const bool valid[4] = {v, v, v, v};
+        process(valid, gB, min(q, last) * 4);
+      }
+      qw += stride;
+      q += stride;
+      if (qw >= n4) break;
+    }
   }
   if (blockIdx.x == 0 && threadIdx.x < 64) {  // n % 4 tail events, one wave
     const uint64_t i = n4 * 4 + lane;
-    bool valid[4] = {i < n, false, false, false};
-    uint32_t k[4] = {0, 0, 0, 0}, a[4] = {0, 0, 0, 0}, ph[4] = {0, 0, 0, 0};
-    int64_t d[4] = {0, 0, 0, 0};
-    if (valid[0]) { k[0] = ev.key[i]; a[0] = ev.app[i]; ph[0] = ev.phase[i]; d[0] = ev.dur[i]; }
-    batch(valid, k, a, ph, d, i);
+    const bool valid[4] = {i < n, false, false, false};
+    const uint64_t ic = valid[0] ? i : 0;  // n >= 1 here whenever valid[0]
+    Ev4 e;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) { e.key[j] = 0; e.app[j] = 0; e.ph[j] = 0; e.dur[j] = 0; }
+    if (n > 0) { e.key[0] = ev.key[ic]; e.app[0] = ev.app[ic]; e.ph[0] = ev.phase[ic]; e.dur[0] = ev.dur[ic]; }
+    StagedEv4 g;
+    stage(e, g);
+    process(valid, g, ic);
   }
-  flag_error(err, bad, ATREX_ERRBIT_RANGE);
   __syncthreads();
   // this workgroup's table -> owner regions (owner = top byte of the key hash);
   // a region that is full sends its rows straight to the row list
@@ -571,11 +671,11 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t A, 
         const size_t rec = ((size_t)blockIdx.x * ATREX_OWNERS + o) * orr.capo + r;
         orr.key[rec] = t;
         for (uint32_t ph = 0; ph < P; ++ph) {
-          orr.acc[(rec * P + ph) * 2] = s_lo[sl * P + ph];
-          orr.acc[(rec * P + ph) * 2 + 1] = s_hi[sl * P + ph];
+          orr.acc[(rec * P + ph) * 2] = s_acc[2 * (sl * P + ph)];
+          orr.acc[(rec * P + ph) * 2 + 1] = s_acc[2 * (sl * P + ph) + 1];
           if (RAW) {
-            orr.raw[(rec * P + ph) * 2] = r_lo[sl * P + ph];
-            orr.raw[(rec * P + ph) * 2 + 1] = r_hi[sl * P + ph];
+            orr.raw[(rec * P + ph) * 2] = s_raw[2 * (sl * P + ph)];
+            orr.raw[(rec * P + ph) * 2 + 1] = s_raw[2 * (sl * P + ph) + 1];
           }
         }
       } else {
@@ -583,10 +683,11 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t A, 
       }
     }
     for (uint32_t ph = 0; ph < P; ++ph) {
-      const uint64_t hi = spill_rows ? s_hi[sl * P + ph] : 0;
+      const size_t gi = 2 * ((size_t)sl * P + ph);
+      const uint64_t hi = spill_rows ? s_acc[gi + 1] : 0;
       const bool want = spill_rows && (hi >> ATREX_COUNT_SHIFT) != 0;
-      row_push(rows, want, ((uint64_t)t << 3) | ph, want ? s_lo[sl * P + ph] : 0, hi,
-               (RAW && want) ? r_lo[sl * P + ph] : 0, (RAW && want) ? r_hi[sl * P + ph] : 0, err);
+      row_push(rows, want, ((uint64_t)t << 3) | ph, want ? s_acc[gi] : 0, hi,
+               (RAW && want) ? s_raw[gi] : 0, (RAW && want) ? s_raw[gi + 1] : 0, err);
     }
   }
   __syncthreads();
@@ -665,9 +766,9 @@ void launch_pass_a_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32
 }
 
 void launch_scale(hipStream_t s, const uint64_t* T, const uint32_t* c, const uint64_t* Csum, uint32_t A,
-                  uint32_t P, uint64_t* scale) {
+                  uint32_t P, uint64_t* scale, void* bscale) {
   const uint32_t G = A * P;
-  hipLaunchKernelGGL(k_scale, dim3((G + 255) / 256), dim3(256), 0, s, T, c, Csum, A, P, scale);
+  hipLaunchKernelGGL(k_scale, dim3((G + 255) / 256), dim3(256), 0, s, T, c, Csum, A, P, scale, (uint64_t*)bscale);
 }
 
 void launch_pass_b_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, const uint64_t* scale,
@@ -680,14 +781,14 @@ void launch_pass_b_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32
 
 uint32_t pass_b_lds_slots(uint32_t P, bool raw, size_t lds_bytes) {
   const size_t per_slot = 4 + (size_t)16 * P * (raw ? 2 : 1);
-  const size_t fixed = ATREX_OWNERS * 4 + 256;
+  const size_t fixed = ATREX_OWNERS * 4 + 256 + (size_t)64 * 16 * (raw ? 2 : 1);
   size_t S = (lds_bytes - fixed) / per_slot;
-  if (S > 8 * 1024) S = 8 * 1024;
-  return (uint32_t)S;
+  if (S > 8 * 1024) S = 8 * 1024;  // the bucket hash needs S / 4 < 2^16
+  return (uint32_t)(S & ~(size_t)3);  // whole buckets of four
 }
 
 size_t pass_b_lds_smem(uint32_t P, bool raw, uint32_t S) {
-  return (size_t)S * P * 8 * (raw ? 4 : 2) + (size_t)S * 4 + ATREX_OWNERS * 4 + 4;
+  return ((size_t)S * P * 16 + 64 * 16) * (raw ? 2 : 1) + (size_t)S * 4 + ATREX_OWNERS * 4 + 4;
 }
 
 // a workgroup of the grid-stride loop sees at most n / nwg + 4 * BLOCK + 3
@@ -696,18 +797,20 @@ uint32_t spill_cap(uint64_t n, uint32_t nwg) { return (uint32_t)((n + nwg - 1) /
 
 uint32_t owner_cap(uint32_t S) { return 2 * ((S + ATREX_OWNERS - 1) / ATREX_OWNERS) + 32; }
 
-void launch_pass_b_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, const uint64_t* scale, bool raw,
-                       uint32_t S, uint32_t nblocks, const OwnerRegions& orr, uint32_t* spill_key,
+void launch_pass_b_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, const uint64_t* scale,
+                       const void* bscale_v, bool raw, uint32_t S, uint32_t nblocks, const OwnerRegions& orr, uint32_t* spill_key,
                        uint64_t* spill_val, uint64_t* spill_raw, uint32_t* spill_count, uint32_t scap,
                        const Rows& rows, uint32_t* err) {
   const size_t smem = pass_b_lds_smem(P, raw, S);
   SpillList sp{spill_key, spill_val, spill_raw, spill_count, scap};
+  const uint64_t* bscale = (const uint64_t*)bscale_v;
+  (void)A;
   if (raw)
-    hipLaunchKernelGGL((k_pass_b_lds<1024, true>), dim3(nblocks), dim3(1024), smem, s, ev, A, P, scale, S, orr, sp,
-                       rows, err);
+    hipLaunchKernelGGL((k_pass_b_lds<1024, true>), dim3(nblocks), dim3(1024), smem, s, ev, P, scale, bscale, S, orr,
+                       sp, rows, err);
   else
-    hipLaunchKernelGGL((k_pass_b_lds<1024, false>), dim3(nblocks), dim3(1024), smem, s, ev, A, P, scale, S, orr, sp,
-                       rows, err);
+    hipLaunchKernelGGL((k_pass_b_lds<1024, false>), dim3(nblocks), dim3(1024), smem, s, ev, P, scale, bscale, S, orr,
+                       sp, rows, err);
 }
 
 void launch_compact_rows(hipStream_t s, const GroupTables& gt, uint32_t P, const Rows& rows, uint32_t* err) {
