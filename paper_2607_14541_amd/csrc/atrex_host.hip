@@ -27,6 +27,7 @@ constexpr uint64_t kMaxWG = 256;            // persistent workgroups of the LDS 
 constexpr uint32_t kMaxBucketBits = 12;     // radix-partition buckets: at most 4096
 constexpr uint32_t kChunk = 1u << 20;       // records per bucket chunk of the partition engine
 constexpr uint32_t kMaxTimed = 64;
+constexpr uint32_t kSpillInline = 16384;    // spill records the owner merge takes in
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 uint64_t next_pow2(uint64_t x) {
@@ -39,6 +40,7 @@ uint64_t next_pow2(uint64_t x) {
 struct Layout {
   size_t ctrl, T, carryA, partA, scale, bscale, dict, acc, raw;
   size_t okey, oacc, oraw, ocount, skey, sval, sraw, scount;  // LDS engine outputs
+  size_t ol_rk, ol_lo, ol_hi, ol_rlo, ol_rhi, ol_count, ol_part;  // per-owner sorted lists
   size_t H, O, rec, rraw, bstart, istart;                     // partition engine
   size_t rk, rlo_acc, rhi_acc, rlo_raw, rhi_raw;              // rows
   size_t sk[3], sv[3], rs_tmp, scan_tmp;
@@ -52,6 +54,7 @@ struct Layout {
   uint32_t ldsSlots; // LDS hash engine slots
   uint32_t tabSlots; // owner-merge / bucket-aggregate LDS table slots
   uint32_t capo, scap;
+  uint32_t oSlots;   // owner-list LDS table slots
 };
 
 struct Params {
@@ -109,6 +112,15 @@ Layout make_layout(const Params& p) {
   L.sval = take(sslots * 16);
   L.sraw = take(p.raw ? sslots * 8 : 0);
   L.scount = take(kMaxWG * 4);
+  L.oSlots = owner_list_slots(p.P, p.raw);
+  const uint64_t olrows = (uint64_t)ATREX_OWNERS * L.oSlots * p.P;
+  L.ol_rk = take(olrows * 8);
+  L.ol_lo = take(olrows * 8);
+  L.ol_hi = take(olrows * 8);
+  L.ol_rlo = take(p.raw ? olrows * 8 : 0);
+  L.ol_rhi = take(p.raw ? olrows * 8 : 0);
+  L.ol_count = take(ATREX_OWNERS * 4);
+  L.ol_part = take((uint64_t)ATREX_OWNERS * p.P * 16);
   const uint64_t hsz = ((uint64_t)1 << kMaxBucketBits) * kMaxWG;
   L.H = take(hsz * 4);
   L.O = take(hsz * 4);
@@ -248,6 +260,29 @@ struct atrex_ctx {
     gt.acc = at<unsigned long long>(L.acc);
     gt.raw = p.raw ? at<unsigned long long>(L.raw) : nullptr;
     return gt;
+  }
+  OwnerLists lists() const {
+    OwnerLists l;
+    l.rk = at<uint64_t>(L.ol_rk);
+    l.lo = at<uint64_t>(L.ol_lo);
+    l.hi = at<uint64_t>(L.ol_hi);
+    l.rlo = p.raw ? at<uint64_t>(L.ol_rlo) : nullptr;
+    l.rhi = p.raw ? at<uint64_t>(L.ol_rhi) : nullptr;
+    l.count = at<uint32_t>(L.ol_count);
+    l.part = at<uint64_t>(L.ol_part);
+    l.cap = L.oSlots * p.P;
+    return l;
+  }
+  SpillIn spills(uint32_t nwg) const {
+    SpillIn sp;
+    sp.key = at<uint32_t>(L.skey);
+    sp.val = at<uint64_t>(L.sval);
+    sp.raw = p.raw ? at<uint64_t>(L.sraw) : nullptr;
+    sp.count = at<uint32_t>(L.scount);
+    sp.cap = L.scap;
+    sp.nwg = nwg;
+    sp.inline_max = kSpillInline;
+    return sp;
   }
   SortedGroups groups() const {
     SortedGroups g;
@@ -492,11 +527,9 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
           launch_pass_b_lds(s, d, A, P, scale, c->at<void>(L.bscale), c->p.raw, L.ldsSlots, nwg, c->owners(), c->at<uint32_t>(L.skey),
                             c->at<uint64_t>(L.sval), c->p.raw ? c->at<uint64_t>(L.sraw) : nullptr,
                             c->at<uint32_t>(L.scount), scap, rows, c->err()));
-    TIMED(c, "owner_merge", (uint64_t)nwg * ATREX_OWNERS,
-          launch_owner_merge(s, c->owners(), nwg, P, c->p.raw, L.tabSlots, rows, c->err()));
-    // spilled events (counts stay on the device): partition engine
-    st = run_partition(c, d, scale, true, nwg, 0, c->p.max_keys);
-    if (st != ATREX_OK) return st;
+    TIMED(c, "owner_finish", (uint64_t)nwg * ATREX_OWNERS,
+          launch_owner_finish(s, c->owners(), nwg, P, c->p.raw, L.oSlots, c->spills(nwg), c->lists(), rows,
+                              c->err()));
   } else if (path == ATREX_PATH_RADIX_SORT) {
     c->path_used = "radix_sort";
     st = run_partition(c, d, scale, false, nwg, n, c->p.max_keys);
@@ -510,14 +543,33 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
           launch_pass_b_global(s, d, A, P, scale, gt, c->p.raw, (uint32_t)c->cus * 8, c->err()));
     TIMED(c, "compact_rows", L.capD * P, launch_compact_rows(s, gt, P, rows, c->err()));
   }
-  // rows -> groups ordered by (key, phase): one workgroup when they are few
+  // rows -> groups ordered by (key, phase): the owner lists ranked in one
+  // launch (LDS engine), or one workgroup when the rows are few
   unsigned long long* smallG = c->at<unsigned long long>(L.ctrl + 192);
   uint32_t* smallDone = c->at<uint32_t>(L.ctrl + 200);
-  TIMED(c, "small_rows", 0, launch_small_rows(s, rows, c->groups(), smallG, smallDone));
+  if (path == ATREX_PATH_LDS_HASH)
+    TIMED(c, "rank_groups", 0,
+          launch_rank_groups(s, c->lists(), P, c->spills(nwg), rows, c->err(), c->groups(), c->at<uint64_t>(L.S),
+                             smallG, smallDone));
+  else
+    TIMED(c, "small_rows", 0, launch_small_rows(s, rows, c->groups(), smallG, smallDone));
   (void)hipMemcpyAsync(hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr), hipMemcpyDeviceToHost, s);
   st = sync_status(c);
   if (st != ATREX_OK) return st;
   if ((uint32_t)hdr[0] & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
+  if (path == ATREX_PATH_LDS_HASH && !((uint32_t)hdr[0] & ATREX_ERRBIT_SPILL) && !(uint32_t)hdr[25]) {
+    // not ranked in one launch: the lists (and the spill records when too many
+    // for the owner merge) become rows for the general ordering
+    launch_lists_to_rows(s, c->lists(), rows, c->err());
+    if (hdr[26] > kSpillInline) {
+      st = run_partition(c, d, scale, true, nwg, 0, c->p.max_keys);
+      if (st != ATREX_OK) return st;
+    }
+    TIMED(c, "small_rows", 0, launch_small_rows(s, rows, c->groups(), smallG, smallDone));
+    (void)hipMemcpyAsync(hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr), hipMemcpyDeviceToHost, s);
+    st = sync_status(c);
+    if (st != ATREX_OK) return st;
+  }
   if (path == ATREX_PATH_LDS_HASH && ((uint32_t)hdr[0] & ATREX_ERRBIT_SPILL)) {
     // a spill region overflowed: partition every event instead
     launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 64, 0);

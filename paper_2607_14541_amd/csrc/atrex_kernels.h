@@ -58,6 +58,29 @@ struct PartSource {
 };
 
 // Groups ordered by (key, phase).
+// Per-owner sorted group lists written by the owner merge of the LDS engine.
+struct OwnerLists {
+  uint64_t* rk;      // [ATREX_OWNERS][cap] sort keys key << 3 | phase, ascending within an owner
+  uint64_t* lo;      // accumulator low words
+  uint64_t* hi;      // accumulator high words (W >> 64 | count << 33)
+  uint64_t* rlo;     // raw time, nullable
+  uint64_t* rhi;
+  uint32_t* count;   // [ATREX_OWNERS] rows per owner
+  uint64_t* part;    // [ATREX_OWNERS][P][2] per-phase partial sums of W
+  uint32_t cap;      // rows per owner
+};
+
+// Spill records of the LDS engine as read back by the owner merge.
+struct SpillIn {
+  const uint32_t* key;
+  const uint64_t* val;    // (share lo, share hi | phase << 40)
+  const uint64_t* raw;    // nullable
+  const uint32_t* count;  // [nwg]
+  uint32_t cap;           // records per workgroup region
+  uint32_t nwg;
+  uint32_t inline_max;    // merged by the owners when the total is at most this
+};
+
 struct SortedGroups {
   uint32_t* key;
   uint8_t* phase;
@@ -99,8 +122,17 @@ void launch_compact_rows(hipStream_t s, const GroupTables& gt, uint32_t P, const
 hipError_t set_rows_smem_limits();
 uint32_t lds_table_slots(uint32_t P, bool raw, size_t lds_bytes);
 size_t lds_table_bytes(uint32_t P, bool raw, uint32_t S);
-void launch_owner_merge(hipStream_t s, const OwnerRegions& orr, uint32_t nwg, uint32_t P, bool raw, uint32_t S,
-                        const Rows& rows, uint32_t* err);
+// owner merge into sorted per-owner lists (+ the spill records when few), then
+// the global order of the lists' rows by ranking; rows the lists cannot take
+// go to the row list and leave the ranking undone (done = 0)
+uint32_t owner_list_slots(uint32_t P, bool raw);
+constexpr uint32_t kRankMax = 16384;  // rows the one-launch ranking handles
+void launch_owner_finish(hipStream_t s, const OwnerRegions& orr, uint32_t nwg, uint32_t P, bool raw, uint32_t So,
+                         const SpillIn& sp, const OwnerLists& ol, const Rows& rows, uint32_t* err);
+void launch_rank_groups(hipStream_t s, const OwnerLists& ol, uint32_t P, const SpillIn& sp, const Rows& rows,
+                        const uint32_t* err, const SortedGroups& out, uint64_t* S_out, unsigned long long* G_out,
+                        uint32_t* done);
+void launch_lists_to_rows(hipStream_t s, const OwnerLists& ol, const Rows& rows, uint32_t* err);
 void launch_part_hist(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t BB, uint32_t* H);
 void launch_part_scatter(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t A, uint32_t P,
                          const uint64_t* scale, uint32_t BB, const uint32_t* O, uint64_t* rec, uint64_t* rraw,

@@ -344,7 +344,7 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_global(EventsDev ev, uint32_t 
 // device-wide atomics.  Before the LDS atomics, lanes of a wave that hit the
 // same (slot, phase) as the wave's first active lane are summed with shuffles
 // and added once (hot keys).  At the end each workgroup writes its table into
-// 256 owner regions (owner = top byte of the key hash); k_owner_merge sums
+// 256 owner regions (owner = top byte of the key hash); k_owner_finish sums
 // each owner's regions.
 constexpr uint32_t MAXPROBE = 8;  // buckets
 constexpr uint32_t INVALID_GI = 0xFFFFFFFFu;

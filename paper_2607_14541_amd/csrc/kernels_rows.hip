@@ -6,7 +6,9 @@
 //
 //  * owner merge: the LDS engine leaves, per workgroup, its table split into
 //    256 owner regions (owner = top byte of an invertible hash of the key);
-//    one workgroup per owner sums the regions in an LDS table and emits rows.
+//    one workgroup per owner sums the regions in an LDS table and writes a
+//    sorted list; the lists are put in global order by ranking each row in
+//    every list (no sort), or become rows when that cannot be done.
 //  * radix-partition engine (high key cardinality, and the LDS engine's
 //    spilled events): per-workgroup bucket histograms of the top BB bits of the
 //    key hash, one scan, a scatter of 16-byte records (Q96 share, phase, the
@@ -104,49 +106,112 @@ struct LdsTable {
   }
 };
 
-// ---------------------------------------------------------------- owner merge
-template <bool RAW>
-__global__ __launch_bounds__(1024) void k_owner_merge(OwnerRegions orr, uint32_t nwg, uint32_t P, uint32_t S,
-                                                      Rows rows, uint32_t* __restrict__ err) {
-  extern __shared__ unsigned long long smem[];
-  __shared__ uint32_t s_pre[257];
-  LdsTable<RAW> tb;
-  tb.init(smem, S, P);
-  tb.clear();
-  const uint32_t o = blockIdx.x;
-  if (threadIdx.x < 64) {  // prefix over the workgroups' row counts for this owner
+// ---------------------------------------------------------------- owner lists
+// One workgroup per owner: sum the owner's regions (and, when the spill total
+// is at most sp.inline_max, the spill records whose key belongs to this owner)
+// in a small LDS table, then sort the owner's (key, phase) rows in LDS and
+// write them as a list with the per-phase partial sums of W.  Keys the table
+// cannot place go to the row list.
+constexpr uint32_t MAXPROBE_O = 64;
+
+__device__ __forceinline__ uint32_t owner_of(uint32_t key) { return hash32(key) >> 24; }
+
+// exclusive prefix of n <= 256 counts (cnt(i)) into pre[0..n], one wave
+template <class F>
+__device__ __forceinline__ void wave_prefix256(uint32_t n, F cnt, uint32_t* pre) {
+  if (threadIdx.x < 64) {
     uint32_t run = 0;
-    for (uint32_t w0 = 0; w0 < nwg; w0 += 64) {
+    for (uint32_t w0 = 0; w0 < n; w0 += 64) {
       const uint32_t w = w0 + threadIdx.x;
-      const uint32_t c = w < nwg ? orr.count[(size_t)w * ATREX_OWNERS + o] : 0;
+      const uint32_t c = w < n ? cnt(w) : 0;
       uint32_t inc = c;
       for (int d = 1; d < 64; d <<= 1) {
         const uint32_t y = __shfl_up(inc, d, 64);
         if (threadIdx.x >= (uint32_t)d) inc += y;
       }
-      if (w < nwg) s_pre[w] = run + inc - c;
+      if (w < n) pre[w] = run + inc - c;
       run += __shfl(inc, 63, 64);
     }
-    if (threadIdx.x == 0) s_pre[nwg] = run;
+    if (threadIdx.x == 0) pre[n] = run;
+  }
+}
+
+// last w with pre[w] <= idx (pre ascending, pre[0] = 0, idx < pre[n])
+__device__ __forceinline__ uint32_t upper_index(const uint32_t* pre, uint32_t n, uint32_t idx) {
+  uint32_t lo = 0, hi = n;
+  while (hi - lo > 1) {
+    const uint32_t mid = (lo + hi) / 2;
+    if (pre[mid] <= idx) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+template <bool RAW>
+__global__ __launch_bounds__(1024) void k_owner_finish(OwnerRegions orr, uint32_t nwg, uint32_t P, uint32_t So,
+                                                       SpillIn sp, OwnerLists ol, Rows rows,
+                                                       uint32_t* __restrict__ err) {
+  extern __shared__ unsigned long long smem[];
+  __shared__ uint32_t s_pre[257], s_spre[257];
+  __shared__ uint32_t s_cnt;
+  __shared__ unsigned long long s_plo[16], s_phi[16];
+  const uint32_t SoP = So * P;
+  unsigned long long* acc = smem;                    // [So * P] x (lo, hi)
+  unsigned long long* racc = smem + 2 * SoP;         // RAW only
+  uint64_t* skey = (uint64_t*)(smem + (RAW ? 4 : 2) * SoP);  // [pow2 >= So * P] sort keys
+  uint32_t SoP2 = 1;
+  while (SoP2 < SoP) SoP2 <<= 1;
+  uint32_t* tag = (uint32_t*)(skey + SoP2);          // [So]
+  const uint32_t o = blockIdx.x, tid = threadIdx.x;
+  for (uint32_t i = tid; i < 2 * SoP; i += 1024) {
+    acc[i] = 0;
+    if (RAW) racc[i] = 0;
+  }
+  for (uint32_t i = tid; i < So; i += 1024) tag[i] = EMPTY_TAG;
+  if (tid < 16) { s_plo[tid] = 0; s_phi[tid] = 0; }
+  if (tid == 0) s_cnt = 0;
+  wave_prefix256(nwg, [&](uint32_t w) { return orr.count[(size_t)w * ATREX_OWNERS + o]; }, s_pre);
+  if (tid >= 64 && tid < 128) {  // second wave: prefix over the spill regions
+    uint32_t run = 0;
+    const uint32_t l = tid - 64;
+    for (uint32_t w0 = 0; w0 < sp.nwg; w0 += 64) {
+      const uint32_t w = w0 + l;
+      const uint32_t c = w < sp.nwg ? sp.count[w] : 0;
+      uint32_t inc = c;
+      for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t y = __shfl_up(inc, d, 64);
+        if (l >= (uint32_t)d) inc += y;
+      }
+      if (w < sp.nwg) s_spre[w] = run + inc - c;
+      run += __shfl(inc, 63, 64);
+    }
+    if (l == 0) s_spre[sp.nwg] = run;
   }
   __syncthreads();
+  auto slot_of = [&](uint32_t key) -> int32_t {
+    if (key == EMPTY_TAG) return -1;  // the free-slot marker is never a tag
+    uint32_t h = hash32(key) & (So - 1);
+#pragma unroll 1
+    for (uint32_t probe = 0; probe < MAXPROBE_O; ++probe) {
+      uint32_t cur = tag[h];
+      if (cur == EMPTY_TAG) cur = atomicCAS(&tag[h], EMPTY_TAG, key);
+      if (cur == key || cur == EMPTY_TAG) return (int32_t)h;
+      h = (h + 1) & (So - 1);
+    }
+    return -1;
+  };
+  // the owner's regions
   const uint32_t total = s_pre[nwg];
-  for (uint32_t base = 0; base < total; base += blockDim.x) {  // uniform trip count
-    const uint32_t idx = base + threadIdx.x;
+  for (uint32_t base = 0; base < total; base += 1024) {  // uniform trip count (row_append)
+    const uint32_t idx = base + tid;
     const bool valid = idx < total;
-    uint32_t key = 0, w = 0;
+    uint32_t key = 0;
     size_t rec = 0;
     int32_t sl = -1;
     if (valid) {
-      uint32_t lo_w = 0, hi_w = nwg;  // last w with s_pre[w] <= idx
-      while (hi_w - lo_w > 1) {
-        const uint32_t mid = (lo_w + hi_w) / 2;
-        if (s_pre[mid] <= idx) lo_w = mid; else hi_w = mid;
-      }
-      w = lo_w;
+      const uint32_t w = upper_index(s_pre, nwg, idx);
       rec = ((size_t)w * ATREX_OWNERS + o) * orr.capo + (idx - s_pre[w]);
       key = orr.key[rec];
-      sl = tb.slot(key);
+      sl = slot_of(key);
     }
     for (uint32_t ph = 0; ph < P; ++ph) {
       uint64_t lo = 0, hi = 0, rl = 0, rh = 0;
@@ -157,27 +222,186 @@ __global__ __launch_bounds__(1024) void k_owner_merge(OwnerRegions orr, uint32_t
       }
       const bool present = valid && (hi >> ATREX_COUNT_SHIFT) != 0;
       if (present && sl >= 0) {
-        lds_add2(&tb.lo[sl * P + ph], &tb.hi[sl * P + ph], lo, hi);
-        if (RAW) lds_add2(&tb.rlo[sl * P + ph], &tb.rhi[sl * P + ph], rl, rh);
+        lds_add2(&acc[2 * (sl * P + ph)], &acc[2 * (sl * P + ph) + 1], lo, hi);
+        if (RAW) lds_add2(&racc[2 * (sl * P + ph)], &racc[2 * (sl * P + ph) + 1], rl, rh);
       }
       row_append(rows, present && sl < 0, ((uint64_t)key << 3) | ph, lo, hi, rl, rh, err);
     }
   }
-  __syncthreads();
-  for (uint32_t base = 0; base < S * P; base += blockDim.x) {
-    const uint32_t i = base + threadIdx.x;
-    bool want = false;
-    uint64_t rk = 0, lo = 0, hi = 0, rl = 0, rh = 0;
-    if (i < S * P) {
-      const uint32_t s = i / P, ph = i - s * P;
-      const uint32_t t = tb.tag[s];
-      hi = tb.hi[i];
-      want = t != EMPTY_TAG && (hi >> ATREX_COUNT_SHIFT) != 0;
-      rk = ((uint64_t)t << 3) | ph;
-      lo = tb.lo[i];
-      if (RAW) { rl = tb.rlo[i]; rh = tb.rhi[i]; }
+  // the spill records of this owner, when they are few
+  const uint32_t stotal = s_spre[sp.nwg];
+  if (stotal <= sp.inline_max) {
+    for (uint32_t base = 0; base < stotal; base += 1024) {
+      const uint32_t idx = base + tid;
+      bool mine = false;
+      uint32_t key = 0, ph = 0;
+      uint64_t lo = 0, hi = 0, d = 0;
+      int32_t sl = -1;
+      if (idx < stotal) {
+        const uint32_t w = upper_index(s_spre, sp.nwg, idx);
+        const size_t r = (size_t)w * sp.cap + (idx - s_spre[w]);
+        key = sp.key[r];
+        mine = owner_of(key) == o;
+        if (mine) {
+          lo = sp.val[2 * r];
+          const uint64_t w1 = sp.val[2 * r + 1];
+          hi = (w1 & (((uint64_t)1 << 40) - 1)) + ((uint64_t)1 << ATREX_COUNT_SHIFT);
+          ph = (uint32_t)(w1 >> 40);
+          if (RAW) d = sp.raw[r];
+          sl = slot_of(key);
+          if (sl >= 0) {
+            lds_add2(&acc[2 * (sl * P + ph)], &acc[2 * (sl * P + ph) + 1], lo, hi);
+            if (RAW) lds_add2(&racc[2 * (sl * P + ph)], &racc[2 * (sl * P + ph) + 1], d, 0);
+          }
+        }
+      }
+      row_append(rows, mine && sl < 0, ((uint64_t)key << 3) | ph, lo, hi, d, 0, err);
     }
-    row_append(rows, want, rk, lo, hi, rl, rh, err);
+  }
+  __syncthreads();
+  // present (slot, phase) pairs -> sort keys rk << 20 | (slot * P + phase)
+  for (uint32_t i = tid; i < SoP; i += 1024) {
+    const uint32_t t = tag[i / P];
+    if (t != EMPTY_TAG && (acc[2 * i + 1] >> ATREX_COUNT_SHIFT) != 0) {
+      const uint32_t at = atomicAdd(&s_cnt, 1u);
+      skey[at] = ((((uint64_t)t << 3) | (i % P)) << 20) | i;
+    }
+  }
+  __syncthreads();
+  const uint32_t cnt = s_cnt;
+  uint32_t N = 1;
+  while (N < cnt) N <<= 1;
+  for (uint32_t i = cnt + tid; i < N; i += 1024) skey[i] = ~0ull;
+  __syncthreads();
+  for (uint32_t k = 2; k <= N; k <<= 1)  // ascending bitonic sort, N <= So * P
+    for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+      for (uint32_t i = tid; i < N; i += 1024) {
+        const uint32_t q = i ^ j;
+        if (q > i) {
+          const uint64_t x = skey[i], y = skey[q];
+          if ((x > y) == ((i & k) == 0)) { skey[i] = y; skey[q] = x; }
+        }
+      }
+      __syncthreads();
+    }
+  // the list, and the per-phase partial sums of W
+  const size_t base = (size_t)o * ol.cap;
+  for (uint32_t i = tid; i < cnt; i += 1024) {
+    const uint64_t sk = skey[i];
+    const uint32_t e = (uint32_t)(sk & 0xFFFFF);
+    const uint64_t lo = acc[2 * e], hi = acc[2 * e + 1];
+    ol.rk[base + i] = sk >> 20;
+    ol.lo[base + i] = lo;
+    ol.hi[base + i] = hi;
+    if (RAW) { ol.rlo[base + i] = racc[2 * e]; ol.rhi[base + i] = racc[2 * e + 1]; }
+    const uint32_t ph = e % P;
+    const unsigned long long wh = hi & (((uint64_t)1 << ATREX_COUNT_SHIFT) - 1);
+    const unsigned long long old = atomicAdd(&s_plo[ph], (unsigned long long)lo);
+    atomicAdd(&s_phi[ph], wh + ((old + lo < old) ? 1ull : 0ull));
+  }
+  __syncthreads();
+  if (tid < P) {
+    ol.part[((size_t)o * P + tid) * 2] = s_plo[tid];
+    ol.part[((size_t)o * P + tid) * 2 + 1] = s_phi[tid];
+  }
+  if (tid == 0) ol.count[o] = cnt;
+}
+
+// Global order of the owner lists' rows: a row's position is the number of
+// rows below its sort key in every list (keys are distinct across lists), so
+// each owner's workgroup binary-searches its rows in all lists staged in LDS.
+// Done only when no row went to the row list, the spill records were merged
+// and there are at most kRankMax rows; workgroup 0 also writes S[ph].
+__global__ __launch_bounds__(1024) void k_rank_groups(OwnerLists ol, uint32_t P, SpillIn sp, Rows rows,
+                                                      const uint32_t* __restrict__ err, SortedGroups out,
+                                                      uint64_t* __restrict__ S_out, unsigned long long* __restrict__ G_out,
+                                                      uint32_t* __restrict__ done) {
+  extern __shared__ unsigned long long smem[];
+  __shared__ uint32_t s_off[ATREX_OWNERS + 1], s_stot;
+  uint64_t* s_rk = (uint64_t*)smem;               // [kRankMax]
+  uint32_t* s_pos = (uint32_t*)(s_rk + kRankMax); // [ol.cap]
+  const uint32_t o = blockIdx.x, tid = threadIdx.x;
+  wave_prefix256(ATREX_OWNERS, [&](uint32_t w) { return ol.count[w]; }, s_off);
+  if (tid >= 64 && tid < 128) {
+    uint32_t run = 0;
+    const uint32_t l = tid - 64;
+    for (uint32_t w0 = 0; w0 < sp.nwg; w0 += 64) {
+      const uint32_t w = w0 + l;
+      uint32_t inc = w < sp.nwg ? sp.count[w] : 0;
+      for (int d = 1; d < 64; d <<= 1) inc += __shfl_xor(inc, d, 64);
+      run += inc;
+    }
+    if (l == 0) s_stot = run;
+  }
+  __syncthreads();
+  const uint32_t R = s_off[ATREX_OWNERS];
+  const bool ok = *rows.count == 0 && s_stot <= sp.inline_max && R <= kRankMax &&
+                  (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
+                   (ATREX_ERRBIT_RANGE | ATREX_ERRBIT_CAPACITY | ATREX_ERRBIT_SPILL)) == 0;
+  if (o == 0 && tid == 0) G_out[2] = s_stot;  // spill records, for the host's fallback
+  if (!ok) {
+    if (o == 0 && tid == 0) *done = 0;
+    return;
+  }
+  for (uint32_t i = tid; i < R; i += 1024) {
+    const uint32_t l = upper_index(s_off, ATREX_OWNERS, i);
+    s_rk[i] = ol.rk[(size_t)l * ol.cap + (i - s_off[l])];
+  }
+  const uint32_t co = s_off[o + 1] - s_off[o];
+  for (uint32_t i = tid; i < co; i += 1024) s_pos[i] = 0;
+  __syncthreads();
+  // pairs (row i of this owner, list l): a wave covers 64 lists of one row
+  for (uint32_t p = tid; p < co * ATREX_OWNERS; p += 1024) {
+    const uint32_t i = p / ATREX_OWNERS, l = p % ATREX_OWNERS;
+    const uint64_t x = s_rk[s_off[o] + i];
+    uint32_t lo = s_off[l], hi = s_off[l + 1];  // lower bound of x in [lo, hi)
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi) / 2;
+      if (s_rk[mid] < x) lo = mid + 1; else hi = mid;
+    }
+    uint32_t below = lo - s_off[l];
+    for (int d = 32; d >= 1; d >>= 1) below += __shfl_xor(below, d, 64);
+    if ((tid & 63) == 0) atomicAdd(&s_pos[i], below);
+  }
+  __syncthreads();
+  const size_t base = (size_t)o * ol.cap;
+  for (uint32_t i = tid; i < co; i += 1024) {
+    const uint32_t g = s_pos[i];
+    const uint64_t rk = s_rk[s_off[o] + i];
+    const uint64_t hi = ol.hi[base + i];
+    out.key[g] = (uint32_t)(rk >> 3);
+    out.phase[g] = (uint8_t)(rk & 7);
+    out.count[g] = hi >> ATREX_COUNT_SHIFT;
+    out.wsum[2 * g] = ol.lo[base + i];
+    out.wsum[2 * g + 1] = hi & (((uint64_t)1 << ATREX_COUNT_SHIFT) - 1);
+    if (out.raw) {
+      out.raw[2 * g] = ol.rlo[base + i];
+      out.raw[2 * g + 1] = ol.rhi[base + i];
+    }
+  }
+  if (o == 0 && tid < P) {
+    u128 t = 0;
+    for (uint32_t l = 0; l < ATREX_OWNERS; ++l)
+      t += make_u128(ol.part[((size_t)l * P + tid) * 2], ol.part[((size_t)l * P + tid) * 2 + 1]);
+    S_out[2 * tid] = (uint64_t)t;
+    S_out[2 * tid + 1] = (uint64_t)(t >> 64);
+  }
+  if (o == 0 && tid == 0) {
+    *G_out = R;
+    *done = 1;
+  }
+}
+
+// The owner lists appended to the row list (when the ranking is not done).
+__global__ void k_lists_to_rows(OwnerLists ol, Rows rows, uint32_t* __restrict__ err) {
+  const uint32_t o = blockIdx.x;
+  const uint32_t c = ol.count[o];
+  const size_t base = (size_t)o * ol.cap;
+  for (uint32_t i0 = 0; i0 < c; i0 += blockDim.x) {  // uniform trip count (row_append)
+    const uint32_t i = i0 + threadIdx.x;
+    const bool v = i < c;
+    row_append(rows, v, v ? ol.rk[base + i] : 0, v ? ol.lo[base + i] : 0, v ? ol.hi[base + i] : 0,
+               (v && ol.rlo) ? ol.rlo[base + i] : 0, (v && ol.rhi) ? ol.rhi[base + i] : 0, err);
   }
 }
 
@@ -405,14 +629,6 @@ uint32_t lds_table_slots(uint32_t P, bool raw, size_t lds_bytes) {
 
 size_t lds_table_bytes(uint32_t P, bool raw, uint32_t S) { return (size_t)S * (4 + (size_t)16 * P * (raw ? 2 : 1)); }
 
-void launch_owner_merge(hipStream_t s, const OwnerRegions& orr, uint32_t nwg, uint32_t P, bool raw, uint32_t S,
-                        const Rows& rows, uint32_t* err) {
-  const size_t smem = lds_table_bytes(P, raw, S);
-  if (raw)
-    hipLaunchKernelGGL(k_owner_merge<true>, dim3(ATREX_OWNERS), dim3(1024), smem, s, orr, nwg, P, S, rows, err);
-  else
-    hipLaunchKernelGGL(k_owner_merge<false>, dim3(ATREX_OWNERS), dim3(1024), smem, s, orr, nwg, P, S, rows, err);
-}
 
 void launch_part_hist(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t BB, uint32_t* H) {
   hipLaunchKernelGGL(k_part_hist, dim3(nwg), dim3(1024), (size_t)4 << BB, s, src, BB, H);
@@ -455,12 +671,59 @@ void launch_rows_reduce(hipStream_t s, const Rows& rows, const uint64_t* rk_sort
   if (G) hipLaunchKernelGGL(k_rows_reduce, dim3(grid_of(G, 256)), dim3(256), 0, s, rows, rk_sorted, idx, starts, G, out);
 }
 
+static uint32_t pow2_ge(uint32_t x) {
+  uint32_t p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+uint32_t owner_list_slots(uint32_t P, bool raw) {
+  const size_t budget = 160 * 1024 - 4096;
+  uint32_t So = 1024;
+  while (So > 64 && (size_t)So * (4 + 16 * P * (raw ? 2 : 1)) + (size_t)pow2_ge(So * P) * 8 > budget) So >>= 1;
+  return So;
+}
+
+
+static size_t owner_finish_smem(uint32_t P, bool raw, uint32_t So) {
+  return (size_t)So * P * 16 * (raw ? 2 : 1) + (size_t)pow2_ge(So * P) * 8 + (size_t)So * 4;
+}
+
+void launch_owner_finish(hipStream_t s, const OwnerRegions& orr, uint32_t nwg, uint32_t P, bool raw, uint32_t So,
+                         const SpillIn& sp, const OwnerLists& ol, const Rows& rows, uint32_t* err) {
+  const size_t smem = owner_finish_smem(P, raw, So);
+  if (raw)
+    hipLaunchKernelGGL(k_owner_finish<true>, dim3(ATREX_OWNERS), dim3(1024), smem, s, orr, nwg, P, So, sp, ol, rows,
+                       err);
+  else
+    hipLaunchKernelGGL(k_owner_finish<false>, dim3(ATREX_OWNERS), dim3(1024), smem, s, orr, nwg, P, So, sp, ol, rows,
+                       err);
+}
+
+void launch_rank_groups(hipStream_t s, const OwnerLists& ol, uint32_t P, const SpillIn& sp, const Rows& rows,
+                        const uint32_t* err, const SortedGroups& out, uint64_t* S_out, unsigned long long* G_out,
+                        uint32_t* done) {
+  const size_t smem = (size_t)kRankMax * 8 + (size_t)ol.cap * 4;
+  hipLaunchKernelGGL(k_rank_groups, dim3(ATREX_OWNERS), dim3(1024), smem, s, ol, P, sp, rows, err, out, S_out, G_out,
+                     done);
+}
+
+void launch_lists_to_rows(hipStream_t s, const OwnerLists& ol, const Rows& rows, uint32_t* err) {
+  hipLaunchKernelGGL(k_lists_to_rows, dim3(ATREX_OWNERS), dim3(256), 0, s, ol, rows, err);
+}
+
+// Dynamic LDS limits: 160 KB less a margin that covers each kernel's static LDS.
 hipError_t set_rows_smem_limits() {
-  const void* fns[] = {(const void*)k_owner_merge<true>, (const void*)k_owner_merge<false>,
+  const void* fns[] = {(const void*)k_rank_groups,
                        (const void*)k_part_aggregate<true>, (const void*)k_part_aggregate<false>,
                        (const void*)k_part_hist, (const void*)k_part_scatter<true>, (const void*)k_part_scatter<false>};
   for (const void* f : fns) {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 2048);
+    if (e != hipSuccess) return e;
+  }
+  const void* fo[] = {(const void*)k_owner_finish<true>, (const void*)k_owner_finish<false>};
+  for (const void* f : fo) {
+    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 4096);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
