@@ -48,6 +48,8 @@ struct Layout {
   size_t flags, scan, starts;
   size_t op_id, op_U, op_w, key_id, key_U, key_w;
   size_t r_op, r_U, r_S, partials, total;
+  size_t u_keyU, u_tileKeys, u_tileKeyU, u_tileRuns, u_tileCont, u_runOp, u_runW, u_runMask, u_keyOff, u_opBase,
+      u_runOff, u_opMask, u_totals;  // unit launches
   size_t bytes;
   uint64_t capD, maxG, maxK, maxS, maxSort, maxOps, partA_rows, maxRows;
   int passA;         // 0: 64-bit LDS table, 1: 32-bit LDS table, 2: global atomics
@@ -159,6 +161,20 @@ Layout make_layout(const Params& p) {
   L.r_U = take(L.maxS * 16);
   L.r_S = take(L.maxS * 8);
   L.partials = take(1024 * 8 * 16);
+  const uint64_t ut = std::max<uint64_t>(1, units_tiles(L.maxG));
+  L.u_keyU = take(L.maxG * 16);
+  L.u_tileKeys = take(ut * 4);
+  L.u_tileKeyU = take(ut * 16);
+  L.u_tileRuns = take(ut * 4);
+  L.u_tileCont = take(ut * 4);
+  L.u_runOp = take(ut * 1024 * 4);
+  L.u_runW = take(ut * 1024 * 16);
+  L.u_runMask = take(ut * 1024 * 4);
+  L.u_keyOff = take(ut * 4);
+  L.u_opBase = take(ut * 4);
+  L.u_runOff = take(ut * 4);
+  L.u_opMask = take(L.maxOps * 4);
+  L.u_totals = take(64);
   L.total = take(64);
   L.bytes = off;
   return L;
@@ -215,6 +231,7 @@ struct atrex_ctx {
   uint32_t flags;
   const uint32_t* app_weight;
   int state;  // 0 initialised, 1 aggregated, 2 normalised
+  bool S_ready;  // the per-phase totals S were written by the ordering step
   uint64_t G, nops, nkeys;
   int cus;
   const char* path_used;
@@ -283,6 +300,23 @@ struct atrex_ctx {
     sp.nwg = nwg;
     sp.inline_max = kSpillInline;
     return sp;
+  }
+  UnitScratch unit_scratch() const {
+    UnitScratch u;
+    u.keyU = at<uint64_t>(L.u_keyU);
+    u.tileKeys = at<uint32_t>(L.u_tileKeys);
+    u.tileKeyU = at<uint64_t>(L.u_tileKeyU);
+    u.tileRuns = at<uint32_t>(L.u_tileRuns);
+    u.tileCont = at<uint32_t>(L.u_tileCont);
+    u.runOp = at<uint32_t>(L.u_runOp);
+    u.runW = at<uint64_t>(L.u_runW);
+    u.runMask = at<uint32_t>(L.u_runMask);
+    u.keyOff = at<uint32_t>(L.u_keyOff);
+    u.opBase = at<uint32_t>(L.u_opBase);
+    u.runOff = at<uint32_t>(L.u_runOff);
+    u.opMask = at<uint32_t>(L.u_opMask);
+    u.totals = at<uint64_t>(L.u_totals);
+    return u;
   }
   SortedGroups groups() const {
     SortedGroups g;
@@ -428,6 +462,7 @@ atrex_status atrex_aggregate_init(const atrex_init_params* ip, atrex_ctx** out) 
   c->flags = ip->flags;
   c->app_weight = ip->app_weight_q16;
   c->state = 0;
+  c->S_ready = false;
   c->G = c->nops = c->nkeys = 0;
   c->path_used = "none";
   c->ntimed = 0;
@@ -557,6 +592,8 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
   st = sync_status(c);
   if (st != ATREX_OK) return st;
   if ((uint32_t)hdr[0] & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
+  // the ranking also wrote S[ph]
+  bool ranked = path == ATREX_PATH_LDS_HASH && !((uint32_t)hdr[0] & ATREX_ERRBIT_SPILL) && (uint32_t)hdr[25];
   if (path == ATREX_PATH_LDS_HASH && !((uint32_t)hdr[0] & ATREX_ERRBIT_SPILL) && !(uint32_t)hdr[25]) {
     // not ranked in one launch: the lists (and the spill records when too many
     // for the owner merge) become rows for the general ordering
@@ -615,6 +652,7 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
   if (G > L.maxG) return ATREX_E_CAPACITY;
   c->end_call();
   c->G = G;
+  c->S_ready = ranked;
   c->state = 1;
   *num_groups = G;
   return ATREX_OK;
@@ -633,65 +671,31 @@ atrex_status atrex_phase_normalize(atrex_ctx* c, const atrex_groups* out, uint64
   c->begin_call();
   const SortedGroups g = c->groups();
   uint64_t* S = c->at<uint64_t>(L.S);
-  if (G <= small_n()) {  // one workgroup: totals, weights and both unit tables
-    unsigned long long* cnt = c->at<unsigned long long>(L.ctrl + 256);
-    uint32_t* done = c->at<uint32_t>(L.ctrl + 272);
-    UnitTable ot{c->at<uint32_t>(L.op_id), c->at<uint64_t>(L.op_U), c->at<double>(L.op_w)};
-    UnitTable kt{c->at<uint32_t>(L.key_id), c->at<uint64_t>(L.key_U), c->at<double>(L.key_w)};
-    TIMED(c, "small_normalize", G,
-          launch_small_normalize(s, g, G, P, lcm_1_to(P), S, out->key, out->phase, out->count, (uint64_t*)out->wsum,
-                                 (uint64_t*)out->raw_ns, out->weight, (uint64_t*)out->phase_total, ot, kt, cnt, done));
-    uint64_t h[4] = {0, 0, 0, 0};
-    (void)hipMemcpyAsync(h, cnt, sizeof(h), hipMemcpyDeviceToHost, s);
-    const atrex_status st = sync_status(c);
-    if (st != ATREX_OK) return st;
-    if ((uint32_t)h[2] != 1) return ATREX_E_DEVICE;
-    c->end_call();
-    c->nops = G ? h[0] : 0;
-    c->nkeys = G ? h[1] : 0;
-    if (num_ops) *num_ops = c->nops;
-    if (num_keys) *num_keys = c->nkeys;
-    c->state = 2;
-    return ATREX_OK;
+  if (!c->S_ready) {
+    const uint32_t nb = (uint32_t)std::min<uint64_t>(1024, std::max<uint64_t>(1, (G + 255) / 256));
+    TIMED(c, "phase_totals", G, launch_phase_totals(s, g, G, P, c->at<uint64_t>(L.partials), nb, S));
   }
-  const uint32_t nb = (uint32_t)std::min<uint64_t>(1024, std::max<uint64_t>(1, (G + 255) / 256));
-  TIMED(c, "phase_totals", G, launch_phase_totals(s, g, G, P, c->at<uint64_t>(L.partials), nb, S));
-  TIMED(c, "group_weights", G,
-        launch_group_weights(s, g, G, S, out->key, out->phase, out->count, (uint64_t*)out->wsum, (uint64_t*)out->raw_ns,
-                             out->weight, (uint64_t*)out->phase_total, P));
-  // Eq. (3) units: operators (key >> 16) and keys
-  uint64_t counts[2] = {0, 0};
-  const int shifts[2] = {16, 0};
-  const size_t ids[2] = {L.op_id, L.key_id}, Us[2] = {L.op_U, L.key_U}, ws[2] = {L.op_w, L.key_w};
-  for (int u = 0; u < 2 && G > 0; ++u) {
-    uint32_t* flags = c->at<uint32_t>(L.flags);
-    uint32_t* scan = c->at<uint32_t>(L.scan);
-    uint32_t* starts = c->at<uint32_t>(L.starts);
-    launch_unit_heads(s, g.key, G, shifts[u], flags);
-    exclusive_scan_u32(s, flags, scan, G, c->at<void>(L.scan_tmp));
-    launch_unit_starts(s, flags, scan, G, starts);
-    uint32_t tail[2] = {0, 0};
-    (void)hipMemcpyAsync(&tail[0], scan + (G - 1), 4, hipMemcpyDeviceToHost, s);
-    (void)hipMemcpyAsync(&tail[1], flags + (G - 1), 4, hipMemcpyDeviceToHost, s);
-    atrex_status st = sync_status(c);
-    if (st != ATREX_OK) return st;
-    const uint64_t nu = (uint64_t)tail[0] + tail[1];
-    if (u == 0 && nu > L.maxOps) return ATREX_E_CAPACITY;
-    UnitTable t{c->at<uint32_t>(ids[u]), c->at<uint64_t>(Us[u]), c->at<double>(ws[u])};
-    TIMED(c, u == 0 ? "op_U" : "key_U", nu, launch_unit_U(s, g, G, starts, nu, shifts[u], P, lcm_1_to(P), t));
-    const uint32_t nb2 = (uint32_t)std::min<uint64_t>(1024, std::max<uint64_t>(1, (nu + 255) / 256));
-    uint64_t* tot = c->at<uint64_t>(L.total) + 2 * u;
-    launch_sum_u128(s, t.U, nu, c->at<uint64_t>(L.partials), nb2, tot);
-    launch_unit_weights(s, t, nu, tot);
-    counts[u] = nu;
-  }
+  // groups with weights, then Eq. (3) per operator and per key
+  GroupsOut o{out->key, out->phase, out->count, (uint64_t*)out->wsum, (uint64_t*)out->raw_ns, out->weight,
+              (uint64_t*)out->phase_total};
+  UnitTable ot{c->at<uint32_t>(L.op_id), c->at<uint64_t>(L.op_U), c->at<double>(L.op_w)};
+  UnitTable kt{c->at<uint32_t>(L.key_id), c->at<uint64_t>(L.key_U), c->at<double>(L.key_w)};
+  unsigned long long* cnt = c->at<unsigned long long>(L.ctrl + 256);
+  launch_fill_u64(s, (uint64_t*)cnt, 2, 0);
+  TIMED(c, "units", G,
+        launch_units(s, g, G, P, lcm_1_to(P), S, o, c->unit_scratch(), ot, L.maxOps, kt, cnt, c->err()));
+  uint64_t h[2] = {0, 0};
+  uint32_t e = 0;
+  (void)hipMemcpyAsync(h, cnt, sizeof(h), hipMemcpyDeviceToHost, s);
+  (void)hipMemcpyAsync(&e, c->err(), sizeof(e), hipMemcpyDeviceToHost, s);
   const atrex_status st = sync_status(c);
   if (st != ATREX_OK) return st;
+  if (e & ATREX_ERRBIT_CAPACITY) return ATREX_E_CAPACITY;
   c->end_call();
-  c->nops = counts[0];
-  c->nkeys = counts[1];
-  if (num_ops) *num_ops = counts[0];
-  if (num_keys) *num_keys = counts[1];
+  c->nops = h[0];
+  c->nkeys = h[1];
+  if (num_ops) *num_ops = c->nops;
+  if (num_keys) *num_keys = c->nkeys;
   c->state = 2;
   return ATREX_OK;
 }
@@ -729,7 +733,7 @@ atrex_status atrex_weighted_score(atrex_ctx* c, const uint32_t* score_key, const
   const Layout& L = c->L;
   hipStream_t s = c->s;
   c->begin_call();
-  if (n <= small_n()) {  // one workgroup: validation, duplicates, medians, Eq. (6)
+  if (n <= kScoreRankMax) {  // ranking + one workgroup: validation, duplicates, medians, Eq. (6)
     launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 1, 0);
     UnitTable opt{c->at<uint32_t>(L.op_id), c->at<uint64_t>(L.op_U), c->at<double>(L.op_w)};
     uint64_t* tot = c->at<uint64_t>(L.total) + 4;
@@ -738,9 +742,9 @@ atrex_status atrex_weighted_score(atrex_ctx* c, const uint32_t* score_key, const
     uint32_t* o_op = op ? op : c->at<uint32_t>(L.r_op);
     double* o_w = op_weight ? op_weight : c->at<double>(L.sk[0]);
     double* o_s = op_score ? op_score : c->at<double>(L.sk[1]);
-    TIMED(c, "small_score", n,
-          launch_small_score(s, score_key, sv, n, opt, c->nops, o_op, o_w, o_s, c->sagg(), tot, nret,
-                             c->at<uint64_t>(L.r_U), c->err()));
+    TIMED(c, "score", n,
+          launch_score_small(s, score_key, sv, n, c->at<uint32_t>(L.sv[2]), c->at<double>(L.sk[2]), opt, c->nops,
+                             o_op, o_w, o_s, c->sagg(), tot, nret, c->at<uint64_t>(L.r_U), c->err()));
     uint64_t h[4] = {0, 0, 0, 0};
     uint32_t e = 0;
     double sa = 0.0;
@@ -837,6 +841,7 @@ const char* atrex_path_used(atrex_ctx* c) { return c ? c->path_used : "none"; }
 atrex_status atrex_aggregate_reset(atrex_ctx* c) {
   if (!c) return ATREX_E_INVALID_ARG;
   c->state = 0;
+  c->S_ready = false;
   c->G = c->nops = c->nkeys = 0;
   return ATREX_OK;
 }

@@ -164,19 +164,41 @@ struct UnitTable {
   uint64_t* U;         // [num][2]
   double* w;           // [num]
 };
+// caller-side group output arrays of phase_normalize
+struct GroupsOut {
+  uint32_t* key;
+  uint8_t* phase;
+  uint64_t* count;
+  uint64_t* wsum;         // [G][2]
+  uint64_t* raw;          // [G][2] or null
+  double* weight;
+  uint64_t* phase_total;  // [P][2]
+};
+// scratch of the three unit launches (see kernels_units.hip)
+struct UnitScratch {
+  uint64_t* keyU;      // [G][2], at each key's first group
+  uint32_t* tileKeys;  // [tiles]
+  uint64_t* tileKeyU;  // [tiles][2]
+  uint32_t* tileRuns;  // [tiles]
+  uint32_t* tileCont;  // [tiles]
+  uint32_t* runOp;     // [tiles * 1024]
+  uint64_t* runW;      // [tiles * 1024][2]
+  uint32_t* runMask;   // [tiles * 1024]
+  uint32_t* keyOff;    // [tiles]
+  uint32_t* opBase;    // [tiles]
+  uint32_t* runOff;    // [tiles]
+  uint32_t* opMask;    // [max ops]
+  uint64_t* totals;    // [2][2]: sum U over operators, over keys
+};
+uint64_t units_tiles(uint64_t G);
+void launch_units(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t L, const uint64_t* S,
+                  const GroupsOut& out, const UnitScratch& us, const UnitTable& ops, uint64_t maxOps,
+                  const UnitTable& keys, unsigned long long* counts, uint32_t* err);
 void launch_phase_totals(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t* partials,
                          uint32_t nb, uint64_t* S);
-void launch_group_weights(hipStream_t s, const SortedGroups& g, uint64_t G, const uint64_t* S, uint32_t* okey,
-                          uint8_t* oph, uint64_t* ocount, uint64_t* owsum, uint64_t* oraw, double* oweight,
-                          uint64_t* oS, uint32_t P);
 // Segments of equal unit (key >> shift) in sorted groups: flags + scan -> starts.
-void launch_unit_heads(hipStream_t s, const uint32_t* key, uint64_t G, int shift, uint32_t* flags);
 void launch_unit_starts(hipStream_t s, const uint32_t* flags, const uint32_t* scan, uint64_t G, uint32_t* starts);
-void launch_unit_U(hipStream_t s, const SortedGroups& g, uint64_t G, const uint32_t* starts, uint64_t nunits,
-                   int shift, uint32_t P, uint64_t L, UnitTable t);
 void launch_sum_u128(hipStream_t s, const uint64_t* x, uint64_t n, uint64_t* partials, uint32_t nb, uint64_t* out);
-void launch_unit_weights(hipStream_t s, UnitTable t, uint64_t nunits, const uint64_t* total);
-
 // score
 void launch_score_validate(hipStream_t s, const double* S, uint64_t n, uint32_t* err);
 void launch_score_keys(hipStream_t s, const uint32_t* score_key, const double* S, uint64_t n, uint64_t* k_key,
@@ -192,15 +214,14 @@ void launch_score_final(hipStream_t s, const uint32_t* r_op, const uint64_t* r_U
                         uint64_t nops, const uint64_t* totalU, uint32_t* op, double* op_weight, double* op_score,
                         double* s_agg, uint32_t* err);
 
-// kernels_small.hip (one workgroup, sizes up to small_n(); *done = 0 when larger)
-uint32_t small_n();
+// kernels_small.hip (one workgroup, up to small_rows_n() rows; *done = 0 when more)
 uint32_t small_rows_n();
 void launch_small_rows(hipStream_t s, const Rows& rows, const SortedGroups& out, unsigned long long* G_out,
                        uint32_t* done);
-void launch_small_normalize(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t L, uint64_t* S_out,
-                            uint32_t* okey, uint8_t* oph, uint64_t* ocount, uint64_t* owsum, uint64_t* oraw,
-                            double* oweight, uint64_t* oS, UnitTable ops, UnitTable keys,
-                            unsigned long long* counts, uint32_t* done);
-void launch_small_score(hipStream_t s, const uint32_t* score_key, const double* S, uint64_t n, UnitTable opt,
-                        uint64_t nops_trace, uint32_t* op_out, double* w_out, double* s_out, double* s_agg,
-                        uint64_t* totU, unsigned long long* nret, uint64_t* rU, uint32_t* err);
+// score of at most kScoreRankMax units: ranking + one-workgroup finish
+constexpr uint32_t kScoreRankMax = 8192;
+void launch_score_small(hipStream_t s, const uint32_t* score_key, const double* S, uint64_t n, uint32_t* sorted_op,
+                        double* sorted_S, const UnitTable& opt, uint64_t nops_trace, uint32_t* op_out, double* w_out,
+                        double* s_out, double* s_agg, uint64_t* totU, unsigned long long* nret, uint64_t* rU,
+                        uint32_t* err);
+hipError_t set_score_smem_limits();

@@ -832,5 +832,7 @@ hipError_t set_kernel_smem_limits() {
   e = hipFuncSetAttribute((const void*)k_pass_b_lds<1024, false>, hipFuncAttributeMaxDynamicSharedMemorySize,
                           160 * 1024);
   if (e != hipSuccess) return e;
+  e = set_score_smem_limits();
+  if (e != hipSuccess) return e;
   return set_rows_smem_limits();
 }

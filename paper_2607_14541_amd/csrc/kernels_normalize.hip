@@ -1,6 +1,6 @@
-// kernels_normalize.hip -- per-phase normalisation and Eq. (3) per operator /
-// per key (§3.4), and the importance-weighted roofline score (§3.6,
-// Eq. (4)-(6)) on gfx950.
+// kernels_normalize.hip -- per-phase totals of W (§3.4) and the score of
+// Eq. (4)-(6) (§3.6) for many scored units: radix-sorted (key) and (operator,
+// S) orders, run starts, medians, Eq. (6) as a compensated sum; gfx950.
 #include <math.h>
 
 #include "atrex_device.hpp"
@@ -78,34 +78,7 @@ __global__ __launch_bounds__(NB) void k_sum_u128_part(const uint64_t* __restrict
   }
 }
 
-// ------------------------------------------------------- per-phase weights
-// weight = RN(W) / RN(S[ph]): each u128 rounded to nearest-even, one IEEE
-// division.  Also copies the group rows to the caller's output arrays.
-__global__ void k_group_weights(SortedGroups g, uint64_t G, const uint64_t* __restrict__ S, uint32_t P,
-                                uint32_t* __restrict__ okey, uint8_t* __restrict__ oph, uint64_t* __restrict__ ocount,
-                                uint64_t* __restrict__ owsum, uint64_t* __restrict__ oraw, double* __restrict__ oweight,
-                                uint64_t* __restrict__ oS) {
-  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < P && oS) { oS[2 * i] = S[2 * i]; oS[2 * i + 1] = S[2 * i + 1]; }
-  if (i >= G) return;
-  const uint32_t ph = g.phase[i];
-  const u128 w = make_u128(g.wsum[2 * i], g.wsum[2 * i + 1]);
-  const u128 s = make_u128(S[2 * ph], S[2 * ph + 1]);
-  okey[i] = g.key[i];
-  oph[i] = (uint8_t)ph;
-  ocount[i] = g.count[i];
-  owsum[2 * i] = g.wsum[2 * i];
-  owsum[2 * i + 1] = g.wsum[2 * i + 1];
-  if (oraw) { oraw[2 * i] = g.raw[2 * i]; oraw[2 * i + 1] = g.raw[2 * i + 1]; }
-  oweight[i] = s == 0 ? 0.0 : u128_to_f64(w) / u128_to_f64(s);
-}
-
-// ------------------------------------------------------- Eq. (3) units
-__global__ void k_unit_heads(const uint32_t* __restrict__ key, uint64_t G, int shift, uint32_t* __restrict__ flags) {
-  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= G) return;
-  flags[i] = (i == 0 || (key[i] >> shift) != (key[i - 1] >> shift)) ? 1u : 0u;
-}
+// ------------------------------------------------------- run starts
 
 __global__ void k_unit_starts(const uint32_t* __restrict__ flags, const uint32_t* __restrict__ scan, uint64_t G,
                               uint32_t* __restrict__ starts) {
@@ -114,38 +87,7 @@ __global__ void k_unit_starts(const uint32_t* __restrict__ flags, const uint32_t
   if (i == G - 1) starts[scan[i] + flags[i]] = (uint32_t)G;  // sentinel
 }
 
-// One wave per unit: U = (L / |Phi|) * sum of W over the unit's groups, with
-// Phi the phases in which the unit has at least one invocation.
-__global__ __launch_bounds__(NB) void k_unit_U(SortedGroups g, const uint32_t* __restrict__ starts, uint64_t nunits,
-                                               int shift, uint64_t L, UnitTable t) {
-  const uint64_t u = ((uint64_t)blockIdx.x * NB + threadIdx.x) >> 6;
-  const uint32_t lane = threadIdx.x & 63;
-  if (u >= nunits) return;
-  const uint32_t b = starts[u], e = starts[u + 1];
-  u128 acc = 0;
-  uint32_t present = 0;
-  for (uint32_t i = b + lane; i < e; i += 64) {
-    acc += make_u128(g.wsum[2 * i], g.wsum[2 * i + 1]);
-    if (g.count[i]) present |= 1u << g.phase[i];
-  }
-  acc = wave_sum_u128(acc);
-  for (int d = 32; d >= 1; d >>= 1) present |= __shfl_down(present, d, 64);
-  if (lane == 0) {
-    const uint32_t nph = __popc(present);
-    t.id[u] = g.key[b] >> shift;
-    const u128 U = nph ? (u128)(L / nph) * acc : (u128)0;
-    t.U[2 * u] = (uint64_t)U;
-    t.U[2 * u + 1] = (uint64_t)(U >> 64);
-  }
-}
 
-__global__ void k_unit_weights(UnitTable t, uint64_t nunits, const uint64_t* __restrict__ total) {
-  const uint64_t u = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (u >= nunits) return;
-  const u128 tot = make_u128(total[0], total[1]);
-  const u128 U = make_u128(t.U[2 * u], t.U[2 * u + 1]);
-  t.w[u] = tot == 0 ? 0.0 : u128_to_f64(U) / u128_to_f64(tot);
-}
 
 // ------------------------------------------------------- score, Eq. (4)-(6)
 __global__ void k_score_validate(const double* __restrict__ S, uint64_t n, uint32_t* __restrict__ err) {
@@ -281,38 +223,18 @@ void launch_phase_totals(hipStream_t s, const SortedGroups& g, uint64_t G, uint3
   hipLaunchKernelGGL(k_colsum_u128, dim3(1), dim3(NB), 0, s, partials, nb, P, S);
 }
 
-void launch_group_weights(hipStream_t s, const SortedGroups& g, uint64_t G, const uint64_t* S, uint32_t* okey,
-                          uint8_t* oph, uint64_t* ocount, uint64_t* owsum, uint64_t* oraw, double* oweight,
-                          uint64_t* oS, uint32_t P) {
-  const uint64_t n = G > P ? G : P;
-  hipLaunchKernelGGL(k_group_weights, dim3(grid_for(n, 256)), dim3(256), 0, s, g, G, S, P, okey, oph, ocount, owsum,
-                     oraw, oweight, oS);
-}
 
-void launch_unit_heads(hipStream_t s, const uint32_t* key, uint64_t G, int shift, uint32_t* flags) {
-  if (G) hipLaunchKernelGGL(k_unit_heads, dim3(grid_for(G, 256)), dim3(256), 0, s, key, G, shift, flags);
-}
 
 void launch_unit_starts(hipStream_t s, const uint32_t* flags, const uint32_t* scan, uint64_t G, uint32_t* starts) {
   if (G) hipLaunchKernelGGL(k_unit_starts, dim3(grid_for(G, 256)), dim3(256), 0, s, flags, scan, G, starts);
 }
 
-void launch_unit_U(hipStream_t s, const SortedGroups& g, uint64_t G, const uint32_t* starts, uint64_t nunits,
-                   int shift, uint32_t P, uint64_t L, UnitTable t) {
-  (void)G;
-  (void)P;
-  if (nunits)
-    hipLaunchKernelGGL(k_unit_U, dim3(grid_for(nunits * 64, NB)), dim3(NB), 0, s, g, starts, nunits, shift, L, t);
-}
 
 void launch_sum_u128(hipStream_t s, const uint64_t* x, uint64_t n, uint64_t* partials, uint32_t nb, uint64_t* out) {
   hipLaunchKernelGGL(k_sum_u128_part, dim3(nb), dim3(NB), 0, s, x, n, partials);
   hipLaunchKernelGGL(k_colsum_u128, dim3(1), dim3(NB), 0, s, partials, nb, 1u, out);
 }
 
-void launch_unit_weights(hipStream_t s, UnitTable t, uint64_t nunits, const uint64_t* total) {
-  if (nunits) hipLaunchKernelGGL(k_unit_weights, dim3(grid_for(nunits, 256)), dim3(256), 0, s, t, nunits, total);
-}
 
 void launch_score_validate(hipStream_t s, const double* S, uint64_t n, uint32_t* err) {
   hipLaunchKernelGGL(k_score_validate, dim3(grid_for(n, 256)), dim3(256), 0, s, S, n, err);

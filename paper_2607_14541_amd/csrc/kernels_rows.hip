@@ -343,9 +343,9 @@ __global__ __launch_bounds__(1024) void k_rank_groups(OwnerLists ol, uint32_t P,
     if (o == 0 && tid == 0) *done = 0;
     return;
   }
-  for (uint32_t i = tid; i < R; i += 1024) {
-    const uint32_t l = upper_index(s_off, ATREX_OWNERS, i);
-    s_rk[i] = ol.rk[(size_t)l * ol.cap + (i - s_off[l])];
+  for (uint32_t l = tid >> 6; l < ATREX_OWNERS; l += 16) {  // one wave per list
+    const uint32_t c = s_off[l + 1] - s_off[l];
+    for (uint32_t i = tid & 63; i < c; i += 64) s_rk[s_off[l] + i] = ol.rk[(size_t)l * ol.cap + i];
   }
   const uint32_t co = s_off[o + 1] - s_off[o];
   for (uint32_t i = tid; i < co; i += 1024) s_pos[i] = 0;

@@ -1,0 +1,224 @@
+// kernels_score.hip -- the importance-weighted roofline score (§3.6,
+// Eq. (4)-(6)) for up to kScoreRankMax scored units, in two launches:
+//
+//  1. k_score_rank (one wave per unit): Eq. (4) validation (S_j in
+//     (0, 1], NaN = not correct), the duplicate-key check, and each unit's
+//     position in the order (operator, S, index) -- NaN after every value of
+//     its operator -- counted against every unit staged in LDS; the units are
+//     scattered to that order.  No sort.
+//  2. k_score_final (one workgroup): operator runs of the ordered units: the
+//     median of the correct S_j (Eq. (5); mean of the two middle values for an
+//     even count, 0 when none), U_i of the operator from the Eq. (3) table
+//     (0 when the operator is not in the trace), w_i = RN(U_i) / RN(sum U over
+//     the retained operators) and S_agg = sum w_i S_i (Eq. (6)) as a
+//     compensated sum.
+#include <math.h>
+
+#include "atrex_device.hpp"
+#include "atrex_kernels.h"
+
+namespace {
+
+constexpr uint32_t NT = 1024;
+constexpr uint32_t NW = NT / 64;
+constexpr uint32_t MINE = NT / 64;  // units ranked per workgroup: one wave each
+
+__device__ __forceinline__ uint64_t s_order_bits(double v) {
+  return isnan(v) ? ~0ull : (uint64_t)__double_as_longlong(v);  // S > 0: bits order as values
+}
+
+__global__ __launch_bounds__(NT) void k_score_rank(const uint32_t* __restrict__ score_key,
+                                                   const double* __restrict__ S, uint32_t n,
+                                                   uint32_t* __restrict__ sorted_op, double* __restrict__ sorted_S,
+                                                   uint32_t* __restrict__ err) {
+  extern __shared__ uint64_t smem64[];
+  uint64_t* s_sb = smem64;                     // [n]
+  uint32_t* s_key = (uint32_t*)(s_sb + n);     // [n]
+  const uint32_t tid = threadIdx.x, lane = tid & 63;
+  for (uint32_t j = tid; j < n; j += NT) {
+    s_sb[j] = s_order_bits(S[j]);
+    s_key[j] = score_key[j];
+  }
+  __syncthreads();
+  const uint32_t m = blockIdx.x * MINE + (tid >> 6);  // this wave's unit
+  if (m >= n) return;                                 // wave-uniform
+  const uint32_t key_m = s_key[m], op_m = key_m >> 16;
+  const uint64_t sb_m = s_sb[m];
+  uint32_t below = 0;
+  bool dup = false;
+#pragma unroll 4
+  for (uint32_t j = lane; j < n; j += 64) {
+    const uint32_t kj = s_key[j], oj = kj >> 16;
+    const uint64_t sj = s_sb[j];
+    below += (oj < op_m || (oj == op_m && (sj < sb_m || (sj == sb_m && j < m)))) ? 1u : 0u;
+    dup |= kj == key_m && j != m;
+  }
+  for (int d = 32; d >= 1; d >>= 1) below += __shfl_xor(below, d, 64);
+  if (lane == 0) {
+    const double v = S[m];
+    sorted_op[below] = op_m;
+    sorted_S[below] = v;
+    if (!isnan(v) && !(v > 0.0 && v <= 1.0)) atomicOr(err, ATREX_ERRBIT_RANGE);
+  }
+  if (__any(dup) && lane == 0) atomicOr(err, ATREX_ERRBIT_DUP);
+}
+
+struct Comp {
+  double s, c;
+};
+
+__device__ __forceinline__ Comp comp_add(Comp a, double x) {  // Neumaier step
+  const double t = a.s + x;
+  if (fabs(a.s) >= fabs(x)) a.c += (a.s - t) + x; else a.c += (x - t) + a.s;
+  a.s = t;
+  return a;
+}
+
+__device__ __forceinline__ Comp comp_merge(Comp a, Comp b) {  // TwoSum of the sums
+  const double t = a.s + b.s;
+  const double bp = t - a.s;
+  const double e = (a.s - (t - bp)) + (b.s - bp);
+  return Comp{t, a.c + b.c + e};
+}
+
+__device__ uint32_t block_exscan(uint32_t v, uint32_t* s_w, uint32_t& total) {
+  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t inc = v;
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(inc, d, 64);
+    if (lane >= (uint32_t)d) inc += y;
+  }
+  if (lane == 63) s_w[wave] = inc;
+  __syncthreads();
+  uint32_t off = 0;
+  total = 0;
+  for (uint32_t w = 0; w < NW; ++w) {
+    if (w < wave) off += s_w[w];
+    total += s_w[w];
+  }
+  __syncthreads();
+  return off + inc - v;
+}
+
+__global__ __launch_bounds__(NT) void k_score_final(const uint32_t* __restrict__ sorted_op,
+                                                    const double* __restrict__ sorted_S, uint32_t n, UnitTable opt,
+                                                    uint64_t nops_trace, uint32_t* __restrict__ op_out,
+                                                    double* __restrict__ w_out, double* __restrict__ s_out,
+                                                    double* __restrict__ s_agg, uint64_t* __restrict__ totU,
+                                                    unsigned long long* __restrict__ nret,
+                                                    uint64_t* __restrict__ rU) {
+  extern __shared__ uint64_t smem64[];
+  double* s_S = (double*)smem64;             // [n]
+  uint32_t* s_op = (uint32_t*)(s_S + n);     // [n]
+  __shared__ uint32_t s_w[NW];
+  __shared__ uint32_t s_carry;
+  __shared__ uint64_t s_u[2 * NW];
+  __shared__ double s_cs[NT], s_cc[NT];
+  const uint32_t tid = threadIdx.x;
+  for (uint32_t j = tid; j < n; j += NT) {
+    s_S[j] = sorted_S[j];
+    s_op[j] = sorted_op[j];
+  }
+  if (tid == 0) s_carry = 0;
+  __syncthreads();
+  // operator runs: medians (Eq. (5)) and U of the retained operators
+  u128 myU = 0;
+  for (uint32_t c0 = 0; c0 < n; c0 += NT) {
+    const uint32_t i = c0 + tid;
+    const bool head = i < n && (i == 0 || s_op[i - 1] != s_op[i]);
+    uint32_t tot;
+    const uint32_t ob = s_carry + block_exscan(head ? 1u : 0u, s_w, tot);
+    if (head) {
+      const uint32_t op = s_op[i];
+      uint32_t lo = i, hi = n;  // run end: first index with a larger operator
+      while (lo < hi) {
+        const uint32_t mid = (lo + hi) / 2;
+        if (s_op[mid] <= op) lo = mid + 1; else hi = mid;
+      }
+      const uint32_t e = lo;
+      lo = i;
+      hi = e;  // first NaN of the run (NaN sorts last)
+      while (lo < hi) {
+        const uint32_t mid = (lo + hi) / 2;
+        if (!isnan(s_S[mid])) lo = mid + 1; else hi = mid;
+      }
+      const uint32_t c = lo - i;
+      double Si = 0.0;
+      if (c) {
+        const uint32_t h = c / 2;
+        Si = (c & 1) ? s_S[i + h] : (s_S[i + h - 1] + s_S[i + h]) / 2.0;
+      }
+      uint64_t a = 0, b = nops_trace;
+      while (a < b) {
+        const uint64_t mid = (a + b) / 2;
+        if (opt.id[mid] < op) a = mid + 1; else b = mid;
+      }
+      u128 U = 0;
+      if (a < nops_trace && opt.id[a] == op) U = make_u128(opt.U[2 * a], opt.U[2 * a + 1]);
+      myU += U;
+      op_out[ob] = op;
+      s_out[ob] = Si;
+      rU[2 * ob] = (uint64_t)U;
+      rU[2 * ob + 1] = (uint64_t)(U >> 64);
+    }
+    __syncthreads();
+    if (tid == 0) s_carry += tot;
+    __syncthreads();
+  }
+  const uint32_t nops = s_carry;
+  const u128 tu = wave_sum_u128(myU);
+  if ((tid & 63) == 0) { s_u[2 * (tid >> 6)] = (uint64_t)tu; s_u[2 * (tid >> 6) + 1] = (uint64_t)(tu >> 64); }
+  __syncthreads();
+  u128 T = 0;
+  for (uint32_t v = 0; v < NW; ++v) T += make_u128(s_u[2 * v], s_u[2 * v + 1]);
+  if (tid == 0) {
+    totU[0] = (uint64_t)T;
+    totU[1] = (uint64_t)(T >> 64);
+    *nret = nops;
+  }
+  const double dT = u128_to_f64(T);
+  __threadfence_block();
+  __syncthreads();
+  // Eq. (6): compensated sums over contiguous runs of operators, then a TwoSum tree
+  const uint32_t per = (nops + NT - 1) / NT;
+  const uint32_t b = tid * per, e = min(b + per, nops);
+  Comp accs{0.0, 0.0};
+  for (uint32_t k = b; k < e; ++k) {
+    const double wk = T == 0 ? 0.0 : u128_to_f64(make_u128(rU[2 * k], rU[2 * k + 1])) / dT;
+    w_out[k] = wk;
+    accs = comp_add(accs, __dmul_rn(wk, s_out[k]));
+  }
+  s_cs[tid] = accs.s;
+  s_cc[tid] = accs.c;
+  __syncthreads();
+  for (uint32_t d = NT / 2; d >= 1; d >>= 1) {
+    if (tid < d) {
+      const Comp mm = comp_merge(Comp{s_cs[tid], s_cc[tid]}, Comp{s_cs[tid + d], s_cc[tid + d]});
+      s_cs[tid] = mm.s;
+      s_cc[tid] = mm.c;
+    }
+    __syncthreads();
+  }
+  if (tid == 0) *s_agg = s_cs[0] + s_cc[0];
+}
+
+}  // namespace
+
+void launch_score_small(hipStream_t s, const uint32_t* score_key, const double* S, uint64_t n, uint32_t* sorted_op,
+                        double* sorted_S, const UnitTable& opt, uint64_t nops_trace, uint32_t* op_out, double* w_out,
+                        double* s_out, double* s_agg, uint64_t* totU, unsigned long long* nret, uint64_t* rU,
+                        uint32_t* err) {
+  const uint32_t nn = (uint32_t)n;
+  hipLaunchKernelGGL(k_score_rank, dim3((nn + MINE - 1) / MINE), dim3(NT), (size_t)nn * 12, s, score_key, S, nn,
+                     sorted_op, sorted_S, err);
+  hipLaunchKernelGGL(k_score_final, dim3(1), dim3(NT), (size_t)nn * 12, s, sorted_op, sorted_S, nn, opt, nops_trace,
+                     op_out, w_out, s_out, s_agg, totU, nret, rU);
+}
+
+hipError_t set_score_smem_limits() {
+  hipError_t e = hipFuncSetAttribute((const void*)k_score_rank, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)(kScoreRankMax * 12));
+  if (e != hipSuccess) return e;
+  return hipFuncSetAttribute((const void*)k_score_final, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (int)(kScoreRankMax * 12));
+}

@@ -1,0 +1,273 @@
+// kernels_units.hip -- per-phase weights and Eq. (3) per operator and per key
+// (§3.4) over the ordered groups, in three launches for any number of groups:
+//
+//  1. k_units_tiles (one 1024-group tile per workgroup): copies the groups to
+//     the caller's arrays with RN(W) / RN(S[ph]); for each key (its groups are
+//     adjacent, at most P of them) U_k = (L_P / |Phi_k|) * sum W; per tile the
+//     number of keys and sum U_k; and the tile's operator runs (groups of one
+//     operator inside the tile) with their W sums and phase masks.
+//  2. k_units_ops (one workgroup): key offsets of the tiles, the operator
+//     index of every run (a tile's first run continues the previous tile's
+//     operator when the operator spans the boundary), U_i = (L_P / |Phi_i|) *
+//     sum W per operator, sum U and w_i = RN(U_i) / RN(sum U).
+//  3. k_units_keys (tiles): key ids, U_k and omega_k = RN(U_k) / RN(sum U_k).
+//
+// Phi (phases in which the unit runs) is the set of phases with a group,
+// i.e. with at least one invocation.
+#include "atrex_device.hpp"
+#include "atrex_kernels.h"
+
+namespace {
+
+constexpr uint32_t TILE = 1024;
+constexpr uint32_t NW = TILE / 64;
+
+__device__ __forceinline__ u128 load_u128(const uint64_t* p, uint64_t i) { return make_u128(p[2 * i], p[2 * i + 1]); }
+__device__ __forceinline__ void store_u128(uint64_t* p, uint64_t i, u128 v) {
+  p[2 * i] = (uint64_t)v;
+  p[2 * i + 1] = (uint64_t)(v >> 64);
+}
+
+// Exclusive scan of one u32 per thread over the block; total in `total`.
+__device__ uint32_t tile_exscan(uint32_t v, uint32_t* s_w, uint32_t& total) {
+  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t inc = v;
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(inc, d, 64);
+    if (lane >= (uint32_t)d) inc += y;
+  }
+  if (lane == 63) s_w[wave] = inc;
+  __syncthreads();
+  uint32_t off = 0;
+  total = 0;
+  for (uint32_t w = 0; w < NW; ++w) {
+    if (w < wave) off += s_w[w];
+    total += s_w[w];
+  }
+  __syncthreads();
+  return off + inc - v;
+}
+
+// Block sum of a u128 (valid in every thread after the call).
+__device__ u128 tile_sum_u128(u128 v, uint64_t* s_lo, uint64_t* s_hi) {
+  const u128 t = wave_sum_u128(v);
+  if ((threadIdx.x & 63) == 0) {
+    s_lo[threadIdx.x >> 6] = (uint64_t)t;
+    s_hi[threadIdx.x >> 6] = (uint64_t)(t >> 64);
+  }
+  __syncthreads();
+  u128 s = 0;
+  for (uint32_t w = 0; w < NW; ++w) s += make_u128(s_lo[w], s_hi[w]);
+  __syncthreads();
+  return s;
+}
+
+__device__ __forceinline__ double ratio(u128 a, u128 b) { return b == 0 ? 0.0 : u128_to_f64(a) / u128_to_f64(b); }
+
+__global__ __launch_bounds__(TILE) void k_units_tiles(SortedGroups g, uint64_t G, uint32_t P, uint64_t L,
+                                                      const uint64_t* __restrict__ S, GroupsOut out, UnitScratch us) {
+  __shared__ uint32_t s_w[NW];
+  __shared__ uint64_t s_lo[NW], s_hi[NW];
+  __shared__ unsigned long long s_rlo[TILE], s_rhi[TILE];
+  __shared__ uint32_t s_rmask[TILE];
+  const uint32_t t = blockIdx.x, l = threadIdx.x;
+  const uint64_t i = (uint64_t)t * TILE + l;
+  const bool valid = i < G;
+  s_rlo[l] = 0;
+  s_rhi[l] = 0;
+  s_rmask[l] = 0;
+  uint32_t key = 0, ph = 0;
+  u128 W = 0;
+  bool keyHead = false, opHead = false;
+  if (valid) {
+    key = g.key[i];
+    ph = g.phase[i];
+    W = load_u128(g.wsum, i);
+    out.key[i] = key;
+    out.phase[i] = (uint8_t)ph;
+    out.count[i] = g.count[i];
+    store_u128(out.wsum, i, W);
+    if (out.raw) store_u128(out.raw, i, load_u128(g.raw, i));
+    out.weight[i] = ratio(W, load_u128(S, ph));
+    const uint32_t prev = i > 0 ? g.key[i - 1] : 0;
+    keyHead = i == 0 || prev != key;
+    opHead = i == 0 || (prev >> 16) != (key >> 16);
+  }
+  // keys: the head group sums the key's groups (adjacent, at most P)
+  u128 Uk = 0;
+  if (keyHead) {
+    u128 sum = 0;
+    uint32_t mask = 0;
+    for (uint64_t e = i; e < G && g.key[e] == key; ++e) {
+      sum += load_u128(g.wsum, e);
+      mask |= 1u << g.phase[e];
+    }
+    Uk = (u128)(L / __popc(mask)) * sum;
+    store_u128(us.keyU, i, Uk);
+  }
+  uint32_t nkeys;
+  (void)tile_exscan(keyHead ? 1u : 0u, s_w, nkeys);
+  const u128 sumUk = tile_sum_u128(Uk, s_lo, s_hi);
+  // operator runs inside the tile: a run starts at an operator head or at the
+  // tile's first group; its index is the number of run starts before it
+  const bool runStart = valid && (opHead || l == 0);
+  uint32_t nruns;
+  const uint32_t r = tile_exscan(runStart ? 1u : 0u, s_w, nruns) + (runStart ? 1u : 0u) - 1u;  // valid rows only
+  // sum each run's W and phase mask: segmented wave sums, one LDS add per run per wave
+  {
+    const uint32_t lane = l & 63;
+    const uint32_t rr = valid ? r : 0xFFFFFFFFu;
+    u128 v = valid ? W : (u128)0;
+    uint32_t m = valid ? (1u << ph) : 0u;
+    for (int d = 1; d < 64; d <<= 1) {  // suffix sums within runs
+      const u128 y = shfl_down_u128(v, d);
+      const uint32_t ym = __shfl_down(m, d, 64);
+      const uint32_t yr = __shfl_down(rr, d, 64);
+      if (lane + d < 64 && yr == rr) {
+        v += y;
+        m |= ym;
+      }
+    }
+    const uint32_t pr = __shfl_up(rr, 1, 64);
+    const bool segHead = valid && (lane == 0 || pr != rr);
+    if (segHead) {
+      const unsigned long long lo = (unsigned long long)(uint64_t)v;
+      const unsigned long long old = atomicAdd(&s_rlo[r], lo);
+      atomicAdd(&s_rhi[r], (unsigned long long)(uint64_t)(v >> 64) + ((old + lo < old) ? 1ull : 0ull));
+      atomicOr(&s_rmask[r], m);
+    }
+  }
+  __syncthreads();
+  const size_t rb = (size_t)t * TILE;
+  if (runStart) us.runOp[rb + r] = key >> 16;
+  if (l < nruns) {
+    us.runW[2 * (rb + l)] = s_rlo[l];
+    us.runW[2 * (rb + l) + 1] = s_rhi[l];
+    us.runMask[rb + l] = s_rmask[l];
+  }
+  if (l == 0) {
+    us.tileKeys[t] = nkeys;
+    store_u128(us.tileKeyU, t, sumUk);
+    us.tileRuns[t] = nruns;
+    us.tileCont[t] = (valid && !opHead) ? 1u : 0u;
+  }
+}
+
+// One workgroup: key offsets of the tiles, the operator table, counts and totals.
+__global__ __launch_bounds__(TILE) void k_units_ops(uint32_t ntiles, uint32_t P, uint64_t L, UnitScratch us,
+                                                    UnitTable ops, uint64_t maxOps, const uint64_t* __restrict__ S,
+                                                    uint64_t* __restrict__ phase_total,
+                                                    unsigned long long* __restrict__ counts,
+                                                    uint32_t* __restrict__ err) {
+  __shared__ uint32_t s_w[NW];
+  __shared__ uint64_t s_lo[NW], s_hi[NW];
+  __shared__ uint32_t s_carry[3];
+  const uint32_t l = threadIdx.x;
+  if (l < P) {
+    phase_total[2 * l] = S[2 * l];
+    phase_total[2 * l + 1] = S[2 * l + 1];
+  }
+  // exclusive scans over the tiles: keys, operator heads (runs not continuing), runs
+  if (l < 3) s_carry[l] = 0;
+  __syncthreads();
+  u128 sumUk = 0;
+  for (uint32_t t0 = 0; t0 < ntiles; t0 += TILE) {
+    const uint32_t t = t0 + l;
+    const bool v = t < ntiles;
+    const uint32_t nk = v ? us.tileKeys[t] : 0, nr = v ? us.tileRuns[t] : 0;
+    const uint32_t nh = v ? nr - us.tileCont[t] : 0;
+    if (v) sumUk += load_u128(us.tileKeyU, t);
+    uint32_t tk, th, tr;
+    const uint32_t ek = tile_exscan(nk, s_w, tk), eh = tile_exscan(nh, s_w, th), er = tile_exscan(nr, s_w, tr);
+    if (v) {
+      us.keyOff[t] = s_carry[0] + ek;
+      us.opBase[t] = s_carry[1] + eh;
+      us.runOff[t] = s_carry[2] + er;
+    }
+    __syncthreads();
+    if (l == 0) { s_carry[0] += tk; s_carry[1] += th; s_carry[2] += tr; }
+    __syncthreads();
+  }
+  const uint32_t nkeys = s_carry[0], nops = s_carry[1], nruns = s_carry[2];
+  const u128 totUk = tile_sum_u128(sumUk, s_lo, s_hi);
+  if (nops > maxOps) {
+    if (l == 0) atomicOr(err, ATREX_ERRBIT_CAPACITY);
+    return;
+  }
+  // operator accumulators: U (as W sums first) and the phase masks
+  for (uint32_t q = l; q < nops; q += TILE) {
+    ops.U[2 * q] = 0;
+    ops.U[2 * q + 1] = 0;
+    us.opMask[q] = 0;
+  }
+  __threadfence();
+  __syncthreads();
+  for (uint32_t x = l; x < nruns; x += TILE) {
+    uint32_t lo = 0, hi = ntiles;  // tile of run x: last t with runOff[t] <= x
+    while (hi - lo > 1) {
+      const uint32_t mid = (lo + hi) / 2;
+      if (us.runOff[mid] <= x) lo = mid; else hi = mid;
+    }
+    const uint32_t t = lo, rr = x - us.runOff[t];
+    const uint32_t q = us.opBase[t] + rr - us.tileCont[t];  // a continuing first run adds to the previous operator
+    const size_t ri = (size_t)t * TILE + rr;
+    if (rr > 0 || !us.tileCont[t]) ops.id[q] = us.runOp[ri];
+    const unsigned long long wlo = us.runW[2 * ri], whi = us.runW[2 * ri + 1];
+    const unsigned long long old = atomicAdd((unsigned long long*)&ops.U[2 * q], wlo);
+    atomicAdd((unsigned long long*)&ops.U[2 * q + 1], whi + ((old + wlo < old) ? 1ull : 0ull));
+    atomicOr(&us.opMask[q], us.runMask[ri]);
+  }
+  __threadfence();
+  __syncthreads();
+  u128 sumU = 0;
+  for (uint32_t q = l; q < nops; q += TILE) {
+    const uint64_t wlo = __hip_atomic_load(&ops.U[2 * q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t whi = __hip_atomic_load(&ops.U[2 * q + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t mask = __hip_atomic_load(&us.opMask[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const u128 U = (u128)(L / __popc(mask)) * make_u128(wlo, whi);
+    store_u128(ops.U, q, U);
+    sumU += U;
+  }
+  const u128 totU = tile_sum_u128(sumU, s_lo, s_hi);
+  for (uint32_t q = l; q < nops; q += TILE) ops.w[q] = ratio(load_u128(ops.U, q), totU);
+  if (l == 0) {
+    counts[0] = nops;
+    counts[1] = nkeys;
+    store_u128(us.totals, 0, totU);
+    store_u128(us.totals, 1, totUk);
+  }
+}
+
+__global__ __launch_bounds__(TILE) void k_units_keys(SortedGroups g, uint64_t G, UnitScratch us, UnitTable keys) {
+  __shared__ uint32_t s_w[NW];
+  const uint32_t t = blockIdx.x, l = threadIdx.x;
+  const uint64_t i = (uint64_t)t * TILE + l;
+  bool head = false;
+  uint32_t key = 0;
+  if (i < G) {
+    key = g.key[i];
+    head = i == 0 || g.key[i - 1] != key;
+  }
+  uint32_t n;
+  const uint32_t k = us.keyOff[t] + tile_exscan(head ? 1u : 0u, s_w, n);
+  if (head) {
+    const u128 U = load_u128(us.keyU, i);
+    keys.id[k] = key;
+    store_u128(keys.U, k, U);
+    keys.w[k] = ratio(U, load_u128(us.totals, 1));
+  }
+}
+
+}  // namespace
+
+void launch_units(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t L, const uint64_t* S,
+                  const GroupsOut& out, const UnitScratch& us, const UnitTable& ops, uint64_t maxOps,
+                  const UnitTable& keys, unsigned long long* counts, uint32_t* err) {
+  const uint32_t nt = (uint32_t)((G + TILE - 1) / TILE);
+  if (nt) hipLaunchKernelGGL(k_units_tiles, dim3(nt), dim3(TILE), 0, s, g, G, P, L, S, out, us);
+  hipLaunchKernelGGL(k_units_ops, dim3(1), dim3(TILE), 0, s, nt, P, L, us, ops, maxOps, S, out.phase_total, counts,
+                     err);
+  if (nt) hipLaunchKernelGGL(k_units_keys, dim3(nt), dim3(TILE), 0, s, g, G, us, keys);
+}
+
+uint64_t units_tiles(uint64_t G) { return (G + TILE - 1) / TILE; }
