@@ -81,6 +81,24 @@ __device__ __forceinline__ void bscale_share32(uint32_t d, uint32_t elo, uint32_
   vhi = f2 >> (u & 31u);
 }
 
+// The same for any duration d < 2^63 (u <= 71): Y = d * (m * 2^8) < 2^127 in
+// four words from four 32 x 32 -> 64-bit products, v = Y >> u (<= 2^96).
+__device__ __forceinline__ void bscale_share64(uint64_t d, uint32_t elo, uint32_t ehi, uint64_t& vlo, uint64_t& vhi) {
+  const uint32_t u = ehi >> 24;
+  const uint32_t M0 = elo << 8, M1 = __builtin_amdgcn_alignbit(ehi & 0xFFFFFFu, elo, 24u);
+  const uint32_t d0 = (uint32_t)d, d1 = (uint32_t)(d >> 32);
+  const uint64_t p00 = (uint64_t)d0 * M0;
+  const uint64_t t1 = (uint64_t)d0 * M1 + (p00 >> 32);
+  const uint64_t t2 = (uint64_t)d1 * M0 + (uint32_t)t1;
+  const uint64_t t3 = (uint64_t)d1 * M1 + ((t1 >> 32) + (t2 >> 32));
+  const uint32_t y0 = (uint32_t)p00, y1 = (uint32_t)t2, y2 = (uint32_t)t3, y3 = (uint32_t)(t3 >> 32);
+  const bool b1 = (u & 32u) != 0, b2 = (u & 64u) != 0;
+  const uint32_t g0 = b1 ? y1 : y0, g1 = b1 ? y2 : y1, g2 = b1 ? y3 : y2, g3 = b1 ? 0u : y3;
+  const uint32_t f0 = b2 ? g2 : g0, f1 = b2 ? g3 : g1, f2 = b2 ? 0u : g2, f3 = b2 ? 0u : g3;
+  vlo = ((uint64_t)__builtin_amdgcn_alignbit(f2, f1, u) << 32) | __builtin_amdgcn_alignbit(f1, f0, u);
+  vhi = ((uint64_t)(f3 >> (u & 31u)) << 32) | __builtin_amdgcn_alignbit(f3, f2, u);
+}
+
 // --- u128 -> fp64, round to nearest, ties to even (IEEE 754 conversion) -----
 __device__ __forceinline__ double u128_to_f64(u128 x) {
   const uint64_t hi = (uint64_t)(x >> 64);
@@ -157,6 +175,35 @@ __device__ __forceinline__ void acc_add_plain(Ptr lo, Ptr hi, u128 v) {
   const unsigned long long carry = (old + vlo < old) ? 1ull : 0ull;
   const unsigned long long vhi = (unsigned long long)(uint64_t)(v >> 64) + carry;
   if (vhi) atomicAdd(hi, vhi);
+}
+
+// --- streaming event loads ----------------------------------------------------
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+typedef long long v2l __attribute__((ext_vector_type(2)));
+
+// Four consecutive events starting at a multiple of 4 (16-byte aligned SoA),
+// with 16-byte non-temporal vector loads.
+struct Ev4 {
+  uint32_t key[4], app[4];
+  uint32_t ph[4];
+  int64_t dur[4];
+};
+
+template <bool WITH_KEY>
+__device__ __forceinline__ void load4(const uint32_t* __restrict__ key, const uint32_t* __restrict__ app,
+                                      const uint8_t* __restrict__ phase, const int64_t* __restrict__ dur,
+                                      uint64_t i, Ev4& e) {
+  if (WITH_KEY) {
+    const v4u k = __builtin_nontemporal_load((const v4u*)(key + i));
+    e.key[0] = k.x; e.key[1] = k.y; e.key[2] = k.z; e.key[3] = k.w;
+  }
+  const v4u a = __builtin_nontemporal_load((const v4u*)(app + i));
+  const uint32_t p = __builtin_nontemporal_load((const uint32_t*)(phase + i));
+  const v2l d0 = __builtin_nontemporal_load((const v2l*)(dur + i));
+  const v2l d1 = __builtin_nontemporal_load((const v2l*)(dur + i + 2));
+  e.app[0] = a.x; e.app[1] = a.y; e.app[2] = a.z; e.app[3] = a.w;
+  e.ph[0] = p & 0xFF; e.ph[1] = (p >> 8) & 0xFF; e.ph[2] = (p >> 16) & 0xFF; e.ph[3] = p >> 24;
+  e.dur[0] = d0.x; e.dur[1] = d0.y; e.dur[2] = d1.x; e.dur[3] = d1.y;
 }
 
 // Error bits of the device error word.

@@ -65,10 +65,15 @@ struct Params {
   bool raw;
 };
 
+constexpr uint32_t kPassARangeBins = (kLdsBytes - 512) / 4;  // 32-bit LDS counters per range
+constexpr uint32_t kPassARangesMax = 16;
+constexpr uint32_t kPassASlices = 32;
+
 int pass_a_mode(uint64_t G_A) {
-  if (G_A * 8 <= kLdsBytes - 1024) return 0;
-  if (G_A * 4 <= kLdsBytes - 512) return 1;
-  return 2;
+  if (G_A * 8 <= kLdsBytes - 1024) return 0;  // 64-bit LDS table
+  if (G_A * 4 <= kLdsBytes - 512) return 1;   // 32-bit LDS table
+  if ((G_A + kPassARangeBins - 1) / kPassARangeBins <= kPassARangesMax) return 3;  // ranges of the table
+  return 2;                                   // global atomics
 }
 
 Layout make_layout(const Params& p) {
@@ -87,7 +92,7 @@ Layout make_layout(const Params& p) {
   L.capD = next_pow2(std::max<uint64_t>(1024, 2 * L.maxK));
   L.maxOps = std::min<uint64_t>(L.maxG, 65536);
   L.passA = pass_a_mode(GA);
-  L.partA_rows = L.passA == 0 ? kPartialRowsMax : (L.passA == 1 ? kMaxWG : 0);
+  L.partA_rows = L.passA == 0 ? kPartialRowsMax : L.passA == 1 ? kMaxWG : L.passA == 3 ? kPassASlices : 0;
   L.ldsSlots = pass_b_lds_slots(p.P, p.raw, kLdsBytes);
   L.tabSlots = lds_table_slots(p.P, p.raw, kLdsBytes);
   L.capo = owner_cap(L.ldsSlots);
@@ -123,7 +128,7 @@ Layout make_layout(const Params& p) {
   L.ol_rhi = take(p.raw ? olrows * 8 : 0);
   L.ol_count = take(ATREX_OWNERS * 4);
   L.ol_part = take((uint64_t)ATREX_OWNERS * p.P * 16);
-  const uint64_t hsz = ((uint64_t)1 << kMaxBucketBits) * kMaxWG;
+  const uint64_t hsz = ((uint64_t)1 << kMaxBucketBits) * std::max<uint64_t>(kMaxWG, kMaxPartWG);
   L.H = take(hsz * 4);
   L.O = take(hsz * 4);
   L.rec = take(p.max_events * 16);
@@ -237,6 +242,14 @@ struct atrex_ctx {
   const char* path_used;
   std::vector<Timed> timed;
   size_t ntimed;
+  // pinned host staging for device -> host readbacks of status words
+  char* pinned = nullptr;
+  size_t pinned_used = 0;
+  struct Pending {
+    void* dst;
+    size_t off, bytes;
+  };
+  std::vector<Pending> pending;
   std::vector<float> last_ms;
   std::vector<const char*> last_names;
   std::vector<uint64_t> last_items;
@@ -365,6 +378,29 @@ atrex_status sync_status(atrex_ctx* c) {
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
+constexpr size_t kPinnedBytes = 4096;
+
+// Device -> host copy of a few status words through the context's pinned
+// buffer; the host values are filled in by sync_read().
+void d2h(atrex_ctx* c, void* dst, const void* src, size_t bytes) {
+  size_t off = (c->pinned_used + 7) / 8 * 8;
+  if (!c->pinned || off + bytes > kPinnedBytes) {  // no pinned buffer: plain (pageable) copy
+    (void)hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, c->s);
+    return;
+  }
+  (void)hipMemcpyAsync(c->pinned + off, src, bytes, hipMemcpyDeviceToHost, c->s);
+  c->pending.push_back({dst, off, bytes});
+  c->pinned_used = off + bytes;
+}
+
+atrex_status sync_read(atrex_ctx* c) {
+  const atrex_status st = sync_status(c);
+  for (const auto& p : c->pending) memcpy(p.dst, c->pinned + p.off, p.bytes);
+  c->pending.clear();
+  c->pinned_used = 0;
+  return st;
+}
+
 #define TIMED(ctx, name, items, stmt) \
   do {                                \
     const int t_ = (ctx)->tstart(name, items); \
@@ -381,12 +417,14 @@ namespace {
 // work items, per-bucket-chunk LDS group-by -> rows.
 atrex_status run_partition(atrex_ctx* c, const EventsDev& d, const uint64_t* scale, bool spill, uint32_t nwg,
                            uint64_t nrec, uint64_t keys_est) {
+  if (!spill) nwg = part_scatter_wgs((uint32_t)c->cus);  // event ranges: several workgroups per CU
   const Layout& L = c->L;
   hipStream_t s = c->s;
   const uint32_t P = c->p.P;
-  // buckets: at least 1024 (work for every CU even with one chunk per bucket)
-  // and about half an LDS table of keys per bucket
-  uint32_t BB = 10;
+  // buckets: at least 256 (work for every CU even with one chunk per bucket;
+  // few buckets keep the scatter's runs long) and about half an LDS table of
+  // keys per bucket
+  uint32_t BB = 8;
   while (BB < kMaxBucketBits && ((keys_est + (1ull << BB) - 1) >> BB) > L.tabSlots / 2) ++BB;
   PartSource src;
   src.ev = d;
@@ -403,7 +441,7 @@ atrex_status run_partition(atrex_ctx* c, const EventsDev& d, const uint64_t* sca
   TIMED(c, spill ? "part_hist_spill" : "part_hist", nrec, launch_part_hist(s, src, nwg, BB, H));
   exclusive_scan_u32(s, H, O, hn, c->at<void>(L.scan_tmp));
   TIMED(c, spill ? "part_scatter_spill" : "part_scatter", nrec,
-        launch_part_scatter(s, src, nwg, c->p.A, P, scale, BB, O, c->at<uint64_t>(L.rec),
+        launch_part_scatter(s, src, nwg, c->p.A, P, scale, c->at<uint64_t>(L.bscale), BB, O, c->at<uint64_t>(L.rec),
                             c->p.raw ? c->at<uint64_t>(L.rraw) : nullptr, c->err()));
   launch_part_items(s, O, H, nwg, BB, kChunk, c->at<uint32_t>(L.bstart), c->at<uint32_t>(L.istart));
   TIMED(c, spill ? "part_aggregate_spill" : "part_aggregate", nrec,
@@ -466,9 +504,11 @@ atrex_status atrex_aggregate_init(const atrex_init_params* ip, atrex_ctx** out) 
   c->G = c->nops = c->nkeys = 0;
   c->path_used = "none";
   c->ntimed = 0;
+  if (hipHostMalloc((void**)&c->pinned, kPinnedBytes, hipHostMallocDefault) != hipSuccess) c->pinned = nullptr;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&c->cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+    if (c->pinned) (void)hipHostFree(c->pinned);
     delete c;
     return ATREX_E_DEVICE;
   }
@@ -476,6 +516,7 @@ atrex_status atrex_aggregate_init(const atrex_init_params* ip, atrex_ctx** out) 
     c->timed.resize(kMaxTimed);
     for (auto& t : c->timed) {
       if (hipEventCreate(&t.a) != hipSuccess || hipEventCreate(&t.b) != hipSuccess) {
+        if (c->pinned) (void)hipHostFree(c->pinned);
         delete c;
         return ATREX_E_DEVICE;
       }
@@ -484,8 +525,8 @@ atrex_status atrex_aggregate_init(const atrex_init_params* ip, atrex_ctx** out) 
   // C = sum_a c_a, checked > 0 (p_a = c_a / C must exist)
   launch_sum_u32(c->s, c->app_weight, p.A, c->Csum());
   uint64_t C = 0;
-  (void)hipMemcpyAsync(&C, c->Csum(), 8, hipMemcpyDeviceToHost, c->s);
-  st = sync_status(c);
+  d2h(c, &C, c->Csum(), 8);
+  st = sync_read(c);
   if (st == ATREX_OK && C == 0) st = ATREX_E_INVALID_ARG;
   if (st != ATREX_OK) {
     atrex_aggregate_destroy(c);
@@ -530,6 +571,15 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
     TIMED(c, "pass_a_reduce", GA,
           launch_pass_a_reduce(s, c->at<unsigned long long>(L.partA), (uint32_t)nb, (uint32_t)GA,
                                c->at<unsigned long long>(L.carryA), T));
+  } else if (L.passA == 3 && vec_ok) {
+    const uint32_t R = (uint32_t)((GA + kPassARangeBins - 1) / kPassARangeBins);
+    const uint32_t GR = (uint32_t)((GA + R - 1) / R);
+    TIMED(c, "pass_a_range", n,
+          launch_pass_a_range(s, d, A, P, GR, R, kPassASlices, c->at<uint32_t>(L.partA),
+                              c->at<unsigned long long>(L.carryA), c->err()));
+    TIMED(c, "pass_a_reduce", GA,
+          launch_pass_a_reduce32(s, c->at<uint32_t>(L.partA), kPassASlices, (uint32_t)GA,
+                                 c->at<unsigned long long>(L.carryA), T));
   } else if (L.passA == 1 && vec_ok) {
     const uint64_t nb = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)c->cus, kMaxWG));
     TIMED(c, "pass_a", n,
@@ -588,8 +638,8 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
                              smallG, smallDone));
   else
     TIMED(c, "small_rows", 0, launch_small_rows(s, rows, c->groups(), smallG, smallDone));
-  (void)hipMemcpyAsync(hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr), hipMemcpyDeviceToHost, s);
-  st = sync_status(c);
+  d2h(c, hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr));
+  st = sync_read(c);
   if (st != ATREX_OK) return st;
   if ((uint32_t)hdr[0] & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
   // the ranking also wrote S[ph]
@@ -603,8 +653,8 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
       if (st != ATREX_OK) return st;
     }
     TIMED(c, "small_rows", 0, launch_small_rows(s, rows, c->groups(), smallG, smallDone));
-    (void)hipMemcpyAsync(hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr), hipMemcpyDeviceToHost, s);
-    st = sync_status(c);
+    d2h(c, hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr));
+    st = sync_read(c);
     if (st != ATREX_OK) return st;
   }
   if (path == ATREX_PATH_LDS_HASH && ((uint32_t)hdr[0] & ATREX_ERRBIT_SPILL)) {
@@ -614,8 +664,8 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
     st = run_partition(c, d, scale, false, nwg, n, c->p.max_keys);
     if (st != ATREX_OK) return st;
     TIMED(c, "small_rows", 0, launch_small_rows(s, rows, c->groups(), smallG, smallDone));
-    (void)hipMemcpyAsync(hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr), hipMemcpyDeviceToHost, s);
-    st = sync_status(c);
+    d2h(c, hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr));
+    st = sync_read(c);
     if (st != ATREX_OK) return st;
     if ((uint32_t)hdr[0] & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
   }
@@ -639,14 +689,14 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
     exclusive_scan_u32(s, flags, scan, R, c->at<void>(L.scan_tmp));
     launch_unit_starts(s, flags, scan, R, starts);
     uint32_t tail[2] = {0, 0};
-    (void)hipMemcpyAsync(&tail[0], scan + (R - 1), 4, hipMemcpyDeviceToHost, s);
-    (void)hipMemcpyAsync(&tail[1], flags + (R - 1), 4, hipMemcpyDeviceToHost, s);
-    st = sync_status(c);
+    d2h(c, &tail[0], scan + (R - 1), 4);
+    d2h(c, &tail[1], flags + (R - 1), 4);
+    st = sync_read(c);
     if (st != ATREX_OK) return st;
     G = (uint64_t)tail[0] + tail[1];
     if (G > L.maxG) return ATREX_E_CAPACITY;
     TIMED(c, "rows_reduce", G, launch_rows_reduce(s, rows, K0, V0, starts, G, c->groups()));
-    st = sync_status(c);
+    st = sync_read(c);
     if (st != ATREX_OK) return st;
   }
   if (G > L.maxG) return ATREX_E_CAPACITY;
@@ -686,9 +736,9 @@ atrex_status atrex_phase_normalize(atrex_ctx* c, const atrex_groups* out, uint64
         launch_units(s, g, G, P, lcm_1_to(P), S, o, c->unit_scratch(), ot, L.maxOps, kt, cnt, c->err()));
   uint64_t h[2] = {0, 0};
   uint32_t e = 0;
-  (void)hipMemcpyAsync(h, cnt, sizeof(h), hipMemcpyDeviceToHost, s);
-  (void)hipMemcpyAsync(&e, c->err(), sizeof(e), hipMemcpyDeviceToHost, s);
-  const atrex_status st = sync_status(c);
+  d2h(c, h, cnt, sizeof(h));
+  d2h(c, &e, c->err(), sizeof(e));
+  const atrex_status st = sync_read(c);
   if (st != ATREX_OK) return st;
   if (e & ATREX_ERRBIT_CAPACITY) return ATREX_E_CAPACITY;
   c->end_call();
@@ -709,7 +759,7 @@ atrex_status atrex_op_weights(atrex_ctx* c, uint32_t* op, atrex_u128* U, double*
     (void)hipMemcpyAsync(U, c->at<void>(c->L.op_U), c->nops * 16, hipMemcpyDeviceToDevice, c->s);
     (void)hipMemcpyAsync(w, c->at<void>(c->L.op_w), c->nops * 8, hipMemcpyDeviceToDevice, c->s);
   }
-  return sync_status(c);
+  return sync_read(c);
 }
 
 atrex_status atrex_key_weights(atrex_ctx* c, uint32_t* key, atrex_u128* U, double* omega) {
@@ -721,7 +771,7 @@ atrex_status atrex_key_weights(atrex_ctx* c, uint32_t* key, atrex_u128* U, doubl
     (void)hipMemcpyAsync(U, c->at<void>(c->L.key_U), c->nkeys * 16, hipMemcpyDeviceToDevice, c->s);
     (void)hipMemcpyAsync(omega, c->at<void>(c->L.key_w), c->nkeys * 8, hipMemcpyDeviceToDevice, c->s);
   }
-  return sync_status(c);
+  return sync_read(c);
 }
 
 atrex_status atrex_weighted_score(atrex_ctx* c, const uint32_t* score_key, const double* sv, uint64_t n, uint32_t* op,
@@ -748,11 +798,11 @@ atrex_status atrex_weighted_score(atrex_ctx* c, const uint32_t* score_key, const
     uint64_t h[4] = {0, 0, 0, 0};
     uint32_t e = 0;
     double sa = 0.0;
-    (void)hipMemcpyAsync(&e, c->err(), 4, hipMemcpyDeviceToHost, s);
-    (void)hipMemcpyAsync(h, tot, 16, hipMemcpyDeviceToHost, s);
-    (void)hipMemcpyAsync(&h[2], nret, 8, hipMemcpyDeviceToHost, s);
-    (void)hipMemcpyAsync(&sa, c->sagg(), 8, hipMemcpyDeviceToHost, s);
-    const atrex_status st = sync_status(c);
+    d2h(c, &e, c->err(), 4);
+    d2h(c, h, tot, 16);
+    d2h(c, &h[2], nret, 8);
+    d2h(c, &sa, c->sagg(), 8);
+    const atrex_status st = sync_read(c);
     if (st != ATREX_OK) return st;
     if (e & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
     if (e & ATREX_ERRBIT_DUP) return ATREX_E_INVALID_ARG;
@@ -782,10 +832,10 @@ atrex_status atrex_weighted_score(atrex_ctx* c, const uint32_t* score_key, const
   exclusive_scan_u32(s, flags, scan, n, c->at<void>(L.scan_tmp));
   launch_unit_starts(s, flags, scan, n, starts);
   uint32_t hdr[4] = {0, 0, 0, 0};
-  (void)hipMemcpyAsync(&hdr[0], c->err(), 4, hipMemcpyDeviceToHost, s);
-  (void)hipMemcpyAsync(&hdr[1], scan + (n - 1), 4, hipMemcpyDeviceToHost, s);
-  (void)hipMemcpyAsync(&hdr[2], flags + (n - 1), 4, hipMemcpyDeviceToHost, s);
-  atrex_status st = sync_status(c);
+  d2h(c, &hdr[0], c->err(), 4);
+  d2h(c, &hdr[1], scan + (n - 1), 4);
+  d2h(c, &hdr[2], flags + (n - 1), 4);
+  atrex_status st = sync_read(c);
   if (st != ATREX_OK) return st;
   if (hdr[0] & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
   if (hdr[0] & ATREX_ERRBIT_DUP) return ATREX_E_INVALID_ARG;
@@ -799,15 +849,15 @@ atrex_status atrex_weighted_score(atrex_ctx* c, const uint32_t* score_key, const
   const uint32_t nb = (uint32_t)std::min<uint64_t>(1024, std::max<uint64_t>(1, (nr + 255) / 256));
   launch_sum_u128(s, r_U, nr, c->at<uint64_t>(L.partials), nb, tot);
   uint64_t totU[2] = {0, 0};
-  (void)hipMemcpyAsync(totU, tot, 16, hipMemcpyDeviceToHost, s);
-  st = sync_status(c);
+  d2h(c, totU, tot, 16);
+  st = sync_read(c);
   if (st != ATREX_OK) return st;
   if (totU[0] == 0 && totU[1] == 0) return ATREX_E_INVALID_ARG;  // no retained weight
   TIMED(c, "score_final", nr,
         launch_score_final(s, r_op, r_U, r_S, nr, tot, op, op_weight, op_score, c->sagg(), c->err()));
   double h = 0.0;
-  (void)hipMemcpyAsync(&h, c->sagg(), 8, hipMemcpyDeviceToHost, s);
-  st = sync_status(c);
+  d2h(c, &h, c->sagg(), 8);
+  st = sync_read(c);
   if (st != ATREX_OK) return st;
   c->end_call();
   *s_agg = h;
@@ -821,7 +871,7 @@ atrex_status atrex_get_app_totals(atrex_ctx* c, atrex_u128* T, uint64_t* mant, i
   const uint64_t GA = (uint64_t)c->p.A * c->p.P;
   (void)hipMemcpyAsync(T, c->at<void>(c->L.T), GA * 16, hipMemcpyDeviceToDevice, c->s);
   if (mant || rho) launch_unpack_scale(c->s, c->at<uint64_t>(c->L.scale), GA, mant, rho);
-  return sync_status(c);
+  return sync_read(c);
 }
 
 atrex_status atrex_kernel_times(atrex_ctx* c, const char** names, float* ms, uint64_t* items, int cap, int* count) {
@@ -848,6 +898,7 @@ atrex_status atrex_aggregate_reset(atrex_ctx* c) {
 
 atrex_status atrex_aggregate_destroy(atrex_ctx* c) {
   if (!c) return ATREX_E_INVALID_ARG;
+  if (c->pinned) (void)hipHostFree(c->pinned);
   for (auto& t : c->timed) {
     (void)hipEventDestroy(t.a);
     (void)hipEventDestroy(t.b);

@@ -57,7 +57,6 @@ struct PartSource {
   bool spill;
 };
 
-// Groups ordered by (key, phase).
 // Per-owner sorted group lists written by the owner merge of the LDS engine.
 struct OwnerLists {
   uint64_t* rk;      // [ATREX_OWNERS][cap] sort keys key << 3 | phase, ascending within an owner
@@ -81,6 +80,7 @@ struct SpillIn {
   uint32_t inline_max;    // merged by the owners when the total is at most this
 };
 
+// Groups ordered by (key, phase).
 struct SortedGroups {
   uint32_t* key;
   uint8_t* phase;
@@ -99,6 +99,8 @@ void launch_pass_a_lds32(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_
                          uint32_t* partial, unsigned long long* ext, uint32_t* err);
 void launch_pass_a_reduce32(hipStream_t s, const uint32_t* partial, uint32_t nb, uint32_t G,
                             const unsigned long long* ext, uint64_t* T);
+void launch_pass_a_range(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t GR, uint32_t R,
+                         uint32_t slices, uint32_t* partial, unsigned long long* ext, uint32_t* err);
 void launch_pass_a_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
                           unsigned long long* T, uint32_t* err);
 void launch_unpack_scale(hipStream_t s, const uint64_t* sw, uint64_t G, uint64_t* mant, int32_t* rho);
@@ -133,10 +135,12 @@ void launch_rank_groups(hipStream_t s, const OwnerLists& ol, uint32_t P, const S
                         const uint32_t* err, const SortedGroups& out, uint64_t* S_out, unsigned long long* G_out,
                         uint32_t* done);
 void launch_lists_to_rows(hipStream_t s, const OwnerLists& ol, const Rows& rows, uint32_t* err);
+constexpr uint32_t kMaxPartWG = 1024;  // partition workgroups over the events
+uint32_t part_scatter_wgs(uint32_t cus);
 void launch_part_hist(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t BB, uint32_t* H);
 void launch_part_scatter(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t A, uint32_t P,
-                         const uint64_t* scale, uint32_t BB, const uint32_t* O, uint64_t* rec, uint64_t* rraw,
-                         uint32_t* err);
+                         const uint64_t* scale, const uint64_t* bscale, uint32_t BB, const uint32_t* O, uint64_t* rec,
+                         uint64_t* rraw, uint32_t* err);
 void launch_part_items(hipStream_t s, const uint32_t* O, const uint32_t* H, uint32_t nw, uint32_t BB, uint32_t CH,
                        uint32_t* bstart, uint32_t* item_start);
 void launch_part_aggregate(hipStream_t s, const uint64_t* rec, const uint64_t* rraw, uint32_t BB, uint32_t CH,

@@ -8,35 +8,8 @@
 #include "atrex_device.hpp"
 #include "atrex_kernels.h"
 
-typedef unsigned int v4u __attribute__((ext_vector_type(4)));
-typedef long long v2l __attribute__((ext_vector_type(2)));
 
 namespace {
-
-// ---------------------------------------------------------------------------
-// Streaming event loads: four consecutive events starting at a multiple of 4.
-struct Ev4 {
-  uint32_t key[4], app[4];
-  uint32_t ph[4];
-  int64_t dur[4];
-};
-
-template <bool WITH_KEY>
-__device__ __forceinline__ void load4(const uint32_t* __restrict__ key, const uint32_t* __restrict__ app,
-                                      const uint8_t* __restrict__ phase, const int64_t* __restrict__ dur,
-                                      uint64_t i, Ev4& e) {
-  if (WITH_KEY) {
-    const v4u k = __builtin_nontemporal_load((const v4u*)(key + i));
-    e.key[0] = k.x; e.key[1] = k.y; e.key[2] = k.z; e.key[3] = k.w;
-  }
-  const v4u a = __builtin_nontemporal_load((const v4u*)(app + i));
-  const uint32_t p = __builtin_nontemporal_load((const uint32_t*)(phase + i));
-  const v2l d0 = __builtin_nontemporal_load((const v2l*)(dur + i));
-  const v2l d1 = __builtin_nontemporal_load((const v2l*)(dur + i + 2));
-  e.app[0] = a.x; e.app[1] = a.y; e.app[2] = a.z; e.app[3] = a.w;
-  e.ph[0] = p & 0xFF; e.ph[1] = (p >> 8) & 0xFF; e.ph[2] = (p >> 16) & 0xFF; e.ph[3] = p >> 24;
-  e.dur[0] = d0.x; e.dur[1] = d0.y; e.dur[2] = d1.x; e.dur[3] = d1.y;
-}
 
 __device__ __forceinline__ void flag_error(uint32_t* err, bool bad, uint32_t bit) {
   // one atomic per wave that saw a bad event
@@ -131,6 +104,54 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_lds32(EventsDev ev, uint32_t A
   __syncthreads();
   uint32_t* out = partial + (size_t)blockIdx.x * G;
   for (uint32_t g = threadIdx.x; g < G; g += BLOCK) out[g] = s32[g];
+}
+
+// Pass A for more (app, phase) pairs than one LDS holds: the pairs are split
+// into R ranges of at most GR, the events into `slices`; each workgroup sums
+// one (slice, range) in 32-bit LDS counters (wraps and high halves into ext[g]
+// as in k_pass_a_lds32).  The R workgroups of a slice are placed on one XCD
+// (workgroups go round-robin over the 8 XCDs), so the slice is read from HBM
+// about once and from that XCD's L2 by the others.
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A, uint32_t P, uint32_t G,
+                                                        uint32_t GR, uint32_t R, uint32_t slices,
+                                                        uint32_t* __restrict__ partial,
+                                                        unsigned long long* __restrict__ ext,
+                                                        uint32_t* __restrict__ err) {
+  extern __shared__ uint32_t s32[];
+  const uint32_t xcd = blockIdx.x % 8, k = blockIdx.x / 8;
+  const uint32_t slice = (k / R) * 8 + xcd, range = k % R;
+  if (slice >= slices) return;  // whole workgroup
+  const uint32_t g0 = range * GR, g1 = min(G, g0 + GR);
+  for (uint32_t g = threadIdx.x; g < g1 - g0; g += BLOCK) s32[g] = 0;
+  __syncthreads();
+  const uint64_t n = ev.n;
+  const uint64_t per = ((n + slices - 1) / slices + 3) / 4 * 4;
+  const uint64_t b = min(n, (uint64_t)slice * per), e = min(n, b + per);
+  bool bad = false;
+  auto one = [&](uint32_t a, uint32_t ph, int64_t dd) {
+    const bool ok = a < A && ph < P && dd >= 0;
+    bad |= !ok;
+    const uint32_t g = a * P + ph;
+    if (!ok || g < g0 || g >= g1) return;
+    const uint64_t d = (uint64_t)dd;
+    const uint32_t lo = (uint32_t)d;
+    const uint32_t old = atomicAdd(&s32[g - g0], lo);
+    const uint64_t up = (d >> 32) + ((old + lo < old) ? 1u : 0u);
+    if (up) atomicAdd(&ext[g], (unsigned long long)up);
+  };
+  const uint64_t e4 = b + (e - b) / 4 * 4;
+  for (uint64_t q = b + 4 * (uint64_t)threadIdx.x; q < e4; q += 4 * (uint64_t)BLOCK) {
+    Ev4 x;
+    load4<false>(ev.key, ev.app, ev.phase, ev.dur, q, x);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) one(x.app[j], x.ph[j], x.dur[j]);
+  }
+  for (uint64_t i = e4 + threadIdx.x; i < e; i += BLOCK) one(ev.app[i], ev.phase[i], ev.dur[i]);
+  flag_error(err, bad, ATREX_ERRBIT_RANGE);
+  __syncthreads();
+  uint32_t* out = partial + (size_t)slice * G;
+  for (uint32_t g = threadIdx.x; g < g1 - g0; g += BLOCK) out[g0 + g] = s32[g];
 }
 
 // T[g] = sum over blocks of partial[b][g] + ext[g] * 2^ext_shift.
@@ -507,10 +528,13 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
 #pragma unroll
     for (int j = 0; j < 4; ++j) ph[j] = (g.ph4 >> (8 * j)) & 0xFFu;
     uint64_t vlo[4], vhi[4];
-    uint32_t slow = 0;
+    uint32_t slow = 0, wide = 0;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) slow |= (uint32_t)((uint64_t)g.dur[j] >> 32) | ((uint32_t)(g.sw[j] >> 56) & ~127u);
-    if (__builtin_expect(__any(slow != 0), 0)) {  // a duration >= 2^32 ns, or rho outside [-8, 63]
+    for (int j = 0; j < 4; ++j) {
+      slow |= (uint32_t)(g.sw[j] >> 56) & ~127u;
+      wide |= (uint32_t)((uint64_t)g.dur[j] >> 32);
+    }
+    if (__builtin_expect(__any(slow != 0), 0)) {  // rho outside [-8, 63]: the general scale word
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const uint64_t i = valid[j] ? first + j : 0;
@@ -518,6 +542,10 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
         vlo[j] = (uint64_t)v;
         vhi[j] = (uint64_t)(v >> 64);
       }
+    } else if (__builtin_expect(__any(wide != 0), 0)) {  // a duration of 2^32 ns or more
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        bscale_share64((uint64_t)g.dur[j], (uint32_t)g.sw[j], (uint32_t)(g.sw[j] >> 32), vlo[j], vhi[j]);
     } else {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -531,9 +559,10 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const uint32_t k = g.key[j];
-      const uint32_t w = tv[j].x == k ? 0u : tv[j].y == k ? 1u : tv[j].z == k ? 2u : 3u;
-      const bool hit = (tv[j].w == k || w < 3) && k != ATREX_EMPTY_KEY;
-      gi[j] = (valid[j] && hit) ? __umul24(4 * g.bucket[j] + w, P) + ph[j] : INVALID_GI;
+      const uint32_t mask = (tv[j].x == k ? 1u : 0u) | (tv[j].y == k ? 2u : 0u) | (tv[j].z == k ? 4u : 0u) |
+                            (tv[j].w == k ? 8u : 0u);
+      const bool hit = mask != 0 && k != ATREX_EMPTY_KEY;
+      gi[j] = (valid[j] && hit) ? __umul24(4 * g.bucket[j] + (uint32_t)(__ffs(mask) - 1), P) + ph[j] : INVALID_GI;
       miss |= valid[j] && !hit;
     }
     if (__builtin_expect(__any(miss), 0)) {  // key not in its home bucket: probe on, then spill what is unplaced
@@ -760,6 +789,14 @@ void launch_pass_a_reduce32(hipStream_t s, const uint32_t* partial, uint32_t nb,
   hipLaunchKernelGGL(k_pass_a_reduce<uint32_t>, dim3((G + 63) / 64), dim3(1024), 0, s, partial, nb, G, ext, 32, T);
 }
 
+void launch_pass_a_range(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t GR, uint32_t R,
+                         uint32_t slices, uint32_t* partial, unsigned long long* ext, uint32_t* err) {
+  const uint32_t G = A * P;
+  const uint32_t nblocks = ((slices + 7) / 8) * 8 * R;
+  hipLaunchKernelGGL((k_pass_a_range<1024>), dim3(nblocks), dim3(1024), (size_t)GR * 4, s, ev, A, P, G, GR, R, slices,
+                     partial, ext, err);
+}
+
 void launch_pass_a_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
                           unsigned long long* T, uint32_t* err) {
   hipLaunchKernelGGL((k_pass_a_global<256>), dim3(nblocks), dim3(256), 0, s, ev, A, P, T, err);
@@ -825,6 +862,8 @@ hipError_t set_kernel_smem_limits() {
                                      160 * 1024);
   if (e != hipSuccess) return e;
   e = hipFuncSetAttribute((const void*)k_pass_a_lds32<1024>, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  if (e != hipSuccess) return e;
+  e = hipFuncSetAttribute((const void*)k_pass_a_range<1024>, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
   if (e != hipSuccess) return e;
   e = hipFuncSetAttribute((const void*)k_pass_b_lds<1024, true>, hipFuncAttributeMaxDynamicSharedMemorySize,
                           160 * 1024);

@@ -14,6 +14,8 @@
 //    key hash, one scan, a scatter of 16-byte records (Q96 share, phase, the
 //    low 32 - BB hash bits), then per bucket chunk an LDS group-by that emits
 //    rows; the key is recovered by inverting the hash.
+#include <algorithm>
+
 #include "atrex_device.hpp"
 #include "atrex_kernels.h"
 
@@ -418,63 +420,217 @@ __device__ __forceinline__ void part_range(const PartSource& src, uint32_t w, ui
   }
 }
 
+// Wave-aggregated LDS counter increment: lanes whose bucket equals the first
+// active lane's add once together (a hot bucket costs one atomic per wave);
+// returns each lane's rank among the increments of its counter.
+__device__ __forceinline__ uint32_t count_in(uint32_t* cnt, uint32_t b, bool active) {
+  const uint64_t act = __ballot(active);
+  if (act == 0) return 0;
+  const uint32_t lane = lane_of();
+  const uint32_t lead = __builtin_amdgcn_readlane(b, __ffsll((unsigned long long)act) - 1);
+  const uint64_t same = __ballot(active && b == lead);
+  uint32_t base = 0;
+  if (lane == (uint32_t)(__ffsll((unsigned long long)act) - 1)) base = atomicAdd(&cnt[lead], (uint32_t)__popcll(same));
+  base = __builtin_amdgcn_readlane(base, __ffsll((unsigned long long)act) - 1);
+  if (active && b == lead) return base + (uint32_t)__popcll(same & ((1ull << lane) - 1ull));
+  return active ? atomicAdd(&cnt[b], 1u) : 0u;
+}
+
 __global__ __launch_bounds__(1024) void k_part_hist(PartSource src, uint32_t BB, uint32_t* __restrict__ H) {
   extern __shared__ uint32_t s_h[];
-  const uint32_t NB = 1u << BB, w = blockIdx.x, nw = gridDim.x;
+  const uint32_t NB = 1u << BB, w = blockIdx.x, nw = gridDim.x, sh = 32 - BB;
   for (uint32_t i = threadIdx.x; i < NB; i += blockDim.x) s_h[i] = 0;
   __syncthreads();
   uint64_t b, e;
   part_range(src, w, b, e);
-  const uint32_t* keys = src.spill ? src.skey : src.ev.key;
-  for (uint64_t i = b + threadIdx.x; i < e; i += blockDim.x) atomicAdd(&s_h[hash32(keys[i]) >> (32 - BB)], 1u);
+  if (src.spill) {
+    for (uint64_t i0 = b; i0 < e; i0 += blockDim.x) {  // uniform trip count
+      const uint64_t i = i0 + threadIdx.x;
+      const bool v = i < e;
+      (void)count_in(s_h, v ? hash32(src.skey[i]) >> sh : 0, v);
+    }
+  } else {  // b is a multiple of 4: four keys per lane with one 16-byte load
+    const uint64_t e4 = b + (e - b) / 4 * 4;
+    for (uint64_t q0 = b; q0 < e4; q0 += 4 * (uint64_t)blockDim.x) {
+      const uint64_t q = q0 + 4 * (uint64_t)threadIdx.x;
+      const bool v = q < e4;
+      v4u k = {0, 0, 0, 0};
+      if (v) k = __builtin_nontemporal_load((const v4u*)(src.ev.key + q));
+      (void)count_in(s_h, hash32(k.x) >> sh, v);
+      (void)count_in(s_h, hash32(k.y) >> sh, v);
+      (void)count_in(s_h, hash32(k.z) >> sh, v);
+      (void)count_in(s_h, hash32(k.w) >> sh, v);
+    }
+    for (uint64_t i = e4 + threadIdx.x; i < e; i += blockDim.x) atomicAdd(&s_h[hash32(src.ev.key[i]) >> sh], 1u);
+  }
   __syncthreads();
   for (uint32_t i = threadIdx.x; i < NB; i += blockDim.x) H[(size_t)i * nw + w] = s_h[i];
 }
 
-template <bool RAW>
-__global__ __launch_bounds__(1024) void k_part_scatter(PartSource src, uint32_t A, uint32_t P,
-                                                       const uint64_t* __restrict__ scale, uint32_t BB,
-                                                       const uint32_t* __restrict__ O, uint64_t* __restrict__ rec,
-                                                       uint64_t* __restrict__ rraw, uint32_t* __restrict__ err) {
-  extern __shared__ uint32_t s_pos[];
-  const uint32_t NB = 1u << BB, w = blockIdx.x, nw = gridDim.x;
-  for (uint32_t i = threadIdx.x; i < NB; i += blockDim.x) s_pos[i] = O[(size_t)i * nw + w];
-  __syncthreads();
+// Records: (share lo, share hi | phase << 33 | low hash bits << 36).  Each
+// workgroup (SC_BLOCK threads, several per CU) walks its event range in tiles
+// of SC_TILE events, the next tile's events loaded while the current one is
+// placed: records and buckets are formed in registers, counted per bucket in
+// LDS, placed in LDS in bucket order and written out as runs, so that
+// consecutive lanes write consecutive records of a bucket.
+constexpr uint32_t SC_BLOCK = 1024;  // tiles of EPT * SC_BLOCK events, EPT = 8 or 4 (LDS budget)
+
+__device__ __forceinline__ void load_group(const EventsDev& ev, uint64_t q, uint64_t e, Ev4& x) {
+  if (q + 3 < e) {  // q is a multiple of 4: a whole, 16-byte aligned group
+    load4<true>(ev.key, ev.app, ev.phase, ev.dur, q, x);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bool in = q + j < e;
+      x.key[j] = in ? ev.key[q + j] : 0;
+      x.app[j] = in ? ev.app[q + j] : 0;
+      x.ph[j] = in ? ev.phase[q + j] : 0;
+      x.dur[j] = in ? ev.dur[q + j] : 0;
+    }
+  }
+}
+
+template <bool RAW, uint32_t SC_EPT>
+__global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint32_t A, uint32_t P,
+                                                           const uint64_t* __restrict__ scale,
+                                                           const uint64_t* __restrict__ bscale, uint32_t BB,
+                                                           const uint32_t* __restrict__ O,
+                                                           uint64_t* __restrict__ rec, uint64_t* __restrict__ rraw,
+                                                           uint32_t* __restrict__ err) {
+  extern __shared__ uint64_t sm64[];
+  constexpr uint32_t NWV = SC_BLOCK / 64;
+  constexpr uint32_t SC_TILE = SC_EPT * SC_BLOCK;
+  const uint32_t NB = 1u << BB, w = blockIdx.x, nw = gridDim.x, tid = threadIdx.x;
+  uint64_t* s_rec = sm64;                                  // [SC_TILE][2]
+  uint64_t* s_raw = s_rec + 2 * SC_TILE;                   // [SC_TILE] RAW only
+  uint16_t* s_bkt = (uint16_t*)(s_raw + (RAW ? SC_TILE : 0));  // [SC_TILE]
+  uint32_t* s_cur = (uint32_t*)(s_bkt + SC_TILE);          // [NB] this workgroup's next record per bucket
+  uint32_t* s_cnt = s_cur + NB;                            // [NB] records of the tile per bucket
+  uint32_t* s_off = s_cnt + NB;                            // [NB] tile offsets
+  __shared__ uint32_t s_w[NWV];
+  for (uint32_t i = tid; i < NB; i += SC_BLOCK) s_cur[i] = O[(size_t)i * nw + w];
   uint64_t b, e;
   part_range(src, w, b, e);
   const uint32_t lowbits = 32 - BB;
   const uint64_t lowmask = ((uint64_t)1 << lowbits) - 1;
   bool bad = false;
-  for (uint64_t i = b + threadIdx.x; i < e; i += blockDim.x) {
-    uint32_t key, ph;
-    uint64_t vlo, vhi, d = 0;
-    if (src.spill) {
-      key = src.skey[i];
-      vlo = src.sval[2 * i];
-      vhi = src.sval[2 * i + 1] & (((uint64_t)1 << 40) - 1);
-      ph = (uint32_t)(src.sval[2 * i + 1] >> 40);
-      if (RAW) d = src.sraw[i];
-    } else {
-      key = src.ev.key[i];
-      const uint32_t a = src.ev.app[i];
-      ph = src.ev.phase[i];
-      const int64_t dd = src.ev.dur[i];
-      const bool ok = a < A && ph < P && dd >= 0;
-      bad |= !ok;
-      const uint64_t sw = ok ? scale[(size_t)a * P + ph] : 0;
-      const u128 v = event_share(ok ? (uint64_t)dd : 0, sw);
-      vlo = (uint64_t)v;
-      vhi = (uint64_t)(v >> 64);
-      ph &= 7;
-      d = ok ? (uint64_t)dd : 0;
+  constexpr uint32_t G4 = SC_EPT / 4;  // groups of four events per thread, SC_BLOCK groups apart
+  constexpr bool PREFETCH = G4 == 1;   // the next tile's events in registers (when they fit)
+  Ev4 nxt[PREFETCH ? 1 : 0 + 1];
+  if (PREFETCH && !src.spill) load_group(src.ev, b + 4 * (uint64_t)tid, e, nxt[0]);
+  for (uint64_t t0 = b; t0 < e; t0 += SC_TILE) {  // uniform trip count
+    Ev4 evg[G4];
+    if (PREFETCH) {
+      evg[0] = nxt[0];
+      if (!src.spill && t0 + SC_TILE < e) load_group(src.ev, t0 + SC_TILE + 4 * (uint64_t)tid, e, nxt[0]);
+    } else if (!src.spill) {
+#pragma unroll
+      for (uint32_t g = 0; g < G4; ++g) load_group(src.ev, t0 + 4 * ((uint64_t)g * SC_BLOCK + tid), e, evg[g]);
     }
-    const uint32_t h = hash32(key);
-    const uint32_t pos = atomicAdd(&s_pos[h >> lowbits], 1u);
-    rec[2 * (size_t)pos] = vlo;
-    rec[2 * (size_t)pos + 1] = vhi | ((uint64_t)ph << 33) | (((uint64_t)h & lowmask) << 36);
-    if (RAW) rraw[pos] = d;
+    for (uint32_t i = tid; i < NB; i += SC_BLOCK) s_cnt[i] = 0;
+    __syncthreads();
+    uint64_t vlo[SC_EPT], w1[SC_EPT], d[SC_EPT];
+    uint32_t bk[SC_EPT], rank[SC_EPT];
+    bool v[SC_EPT];
+    if (src.spill) {
+#pragma unroll
+      for (uint32_t j = 0; j < SC_EPT; ++j) {
+        const uint64_t i = t0 + 4 * ((uint64_t)(j / 4) * SC_BLOCK + tid) + (j % 4);
+        v[j] = i < e;
+        uint32_t key = 0, ph = 0;
+        vlo[j] = 0; d[j] = 0;
+        uint64_t vhi = 0;
+        if (v[j]) {
+          key = src.skey[i];
+          vlo[j] = src.sval[2 * i];
+          vhi = src.sval[2 * i + 1] & (((uint64_t)1 << 40) - 1);
+          ph = (uint32_t)(src.sval[2 * i + 1] >> 40);
+          if (RAW) d[j] = src.sraw[i];
+        }
+        const uint32_t h = hash32(key);
+        bk[j] = h >> lowbits;
+        w1[j] = vhi | ((uint64_t)ph << 33) | (((uint64_t)h & lowmask) << 36);
+      }
+    } else {
+#pragma unroll
+      for (uint32_t j = 0; j < SC_EPT; ++j) {
+        const Ev4& ev = evg[j / 4];
+        const uint32_t jj = j % 4;
+        v[j] = t0 + 4 * ((uint64_t)(j / 4) * SC_BLOCK + tid) + jj < e;
+        const uint32_t a = ev.app[jj], ph = ev.ph[jj];
+        const int64_t dd = ev.dur[jj];
+        const bool ok = a < A && ph < P && dd >= 0;
+        bad |= v[j] && !ok;
+        const uint32_t g = ok ? a * P + ph : 0;
+        const uint64_t sw = ok ? bscale[g] : 0;
+        uint64_t vl, vh;
+        if (ok && (uint32_t)(sw >> 56) <= 127u) {
+          if (((uint64_t)dd >> 32) == 0) {
+            uint32_t h32;
+            bscale_share32((uint32_t)dd, (uint32_t)sw, (uint32_t)(sw >> 32), vl, h32);
+            vh = h32;
+          } else {
+            bscale_share64((uint64_t)dd, (uint32_t)sw, (uint32_t)(sw >> 32), vl, vh);
+          }
+        } else {
+          const u128 x = event_share(ok ? (uint64_t)dd : 0, ok ? scale[g] : 0);
+          vl = (uint64_t)x;
+          vh = (uint64_t)(x >> 64);
+        }
+        vlo[j] = vl;
+        d[j] = ok ? (uint64_t)dd : 0;
+        const uint32_t h = hash32(ev.key[jj]);
+        bk[j] = h >> lowbits;
+        w1[j] = vh | ((uint64_t)(ok ? ph : 0) << 33) | (((uint64_t)h & lowmask) << 36);
+      }
+    }
+#pragma unroll
+    for (uint32_t j = 0; j < SC_EPT; ++j) rank[j] = count_in(s_cnt, bk[j], v[j]);
+    __syncthreads();
+    // exclusive scan of the tile's bucket counts
+    {
+      const uint32_t per = (NB + SC_BLOCK - 1) / SC_BLOCK, b0 = tid * per;
+      uint32_t sum = 0;
+      for (uint32_t k = 0; k < per; ++k) sum += (b0 + k < NB) ? s_cnt[b0 + k] : 0;
+      const uint32_t lane = tid & 63, wave = tid >> 6;
+      uint32_t inc = sum;
+      for (int dd = 1; dd < 64; dd <<= 1) {
+        const uint32_t y = __shfl_up(inc, dd, 64);
+        if (lane >= (uint32_t)dd) inc += y;
+      }
+      if (lane == 63) s_w[wave] = inc;
+      __syncthreads();
+      uint32_t off = 0;
+      for (uint32_t x = 0; x < wave; ++x) off += s_w[x];
+      uint32_t run = off + inc - sum;
+      for (uint32_t k = 0; k < per; ++k)
+        if (b0 + k < NB) { s_off[b0 + k] = run; run += s_cnt[b0 + k]; }
+    }
+    __syncthreads();
+#pragma unroll
+    for (uint32_t j = 0; j < SC_EPT; ++j) {
+      if (!v[j]) continue;
+      const uint32_t at = s_off[bk[j]] + rank[j];
+      s_rec[2 * at] = vlo[j];
+      s_rec[2 * at + 1] = w1[j];
+      if (RAW) s_raw[at] = d[j];
+      s_bkt[at] = (uint16_t)bk[j];
+    }
+    __syncthreads();
+    const uint32_t nt = (uint32_t)min((uint64_t)SC_TILE, e - t0);
+    for (uint32_t k = tid; k < nt; k += SC_BLOCK) {
+      const uint32_t bb = s_bkt[k];
+      const size_t pos = (size_t)s_cur[bb] + (k - s_off[bb]);
+      v2l r;
+      r.x = (long long)s_rec[2 * k];
+      r.y = (long long)s_rec[2 * k + 1];
+      __builtin_nontemporal_store(r, (v2l*)(rec + 2 * pos));
+      if (RAW) rraw[pos] = s_raw[k];
+    }
+    __syncthreads();
+    for (uint32_t i = tid; i < NB; i += SC_BLOCK) s_cur[i] += s_cnt[i];
   }
-  if (__any(bad) && (threadIdx.x & 63) == 0) atomicOr(err, ATREX_ERRBIT_RANGE);
+  if (__any(bad) && (tid & 63) == 0) atomicOr(err, ATREX_ERRBIT_RANGE);
 }
 
 // Work items = (bucket, chunk of at most CH records); item_start[b] = first
@@ -522,6 +678,11 @@ __global__ __launch_bounds__(1024) void k_part_items(const uint32_t* __restrict_
   if (threadIdx.x == 0) item_start[NB] = total;
 }
 
+// Per work item (bucket, chunk): an LDS table of S slots in buckets of four
+// tags (the record's low hash bits; with the bucket they give the key back
+// through the inverse mix) and per phase a two-word accumulator, plus 64
+// per-lane dummy entries for lanes with nothing to add; four records per lane
+// per step; a wave whose lanes mostly hit one (slot, phase) sums them first.
 template <bool RAW>
 __global__ __launch_bounds__(1024) void k_part_aggregate(const uint64_t* __restrict__ rec,
                                                          const uint64_t* __restrict__ rraw, uint32_t BB, uint32_t CH,
@@ -529,10 +690,37 @@ __global__ __launch_bounds__(1024) void k_part_aggregate(const uint64_t* __restr
                                                          const uint32_t* __restrict__ item_start, uint32_t P,
                                                          uint32_t S, Rows rows, uint32_t* __restrict__ err) {
   extern __shared__ unsigned long long smem[];
-  LdsTable<RAW> tb;
-  tb.init(smem, S, P);
-  const uint32_t NB = 1u << BB, lowbits = 32 - BB;
+  __shared__ uint32_t s_wsum[16];
+  __shared__ unsigned long long s_base;
+  const uint32_t SP = S * P, region = 2 * SP + 128;
+  unsigned long long* acc = smem;                        // [S * P] x (lo, hi), then 64 dummies
+  unsigned long long* racc = smem + region;              // RAW only
+  uint32_t* tag = (uint32_t*)(smem + (RAW ? 2 : 1) * region);  // [S], 16-byte aligned
+  const uint32_t NB = 1u << BB, lowbits = 32 - BB, NBK = S / 4;
+  const uint32_t lane = lane_of(), dummy = 2 * SP + 2 * lane;
   const uint32_t items = item_start[NB];
+  auto bucket_tags = [&](uint32_t bq) -> uint4 { return *(const uint4*)&tag[4 * bq]; };
+  auto find_slot = [&](uint32_t k, uint32_t bq, uint4 tv) -> int32_t {
+    uint32_t probe = 0;
+#pragma unroll 1
+    for (uint32_t step = 0; step < 256; ++step) {
+      if (tv.x == k) return (int32_t)(4 * bq);
+      if (tv.y == k) return (int32_t)(4 * bq + 1);
+      if (tv.z == k) return (int32_t)(4 * bq + 2);
+      if (tv.w == k) return (int32_t)(4 * bq + 3);
+      const uint32_t x = tv.x == EMPTY_TAG ? 0u : tv.y == EMPTY_TAG ? 1u : tv.z == EMPTY_TAG ? 2u
+                       : tv.w == EMPTY_TAG ? 3u : 4u;
+      if (x < 4) {
+        const uint32_t t = atomicCAS(&tag[4 * bq + x], EMPTY_TAG, k);
+        if (t == EMPTY_TAG || t == k) return (int32_t)(4 * bq + x);
+      } else {
+        if (++probe == 32) return -1;
+        bq = (bq + 1 == NBK) ? 0 : bq + 1;
+      }
+      tv = bucket_tags(bq);
+    }
+    return -1;
+  };
   for (uint32_t it = blockIdx.x; it < items; it += gridDim.x) {
     uint32_t lo_b = 0, hi_b = NB;  // bucket: last b with item_start[b] <= it
     while (hi_b - lo_b > 1) {
@@ -543,43 +731,167 @@ __global__ __launch_bounds__(1024) void k_part_aggregate(const uint64_t* __restr
     const uint32_t c = it - item_start[bkt];
     const uint32_t r0 = bstart[bkt] + c * CH;
     const uint32_t r1 = min(bstart[bkt + 1], r0 + CH);
-    tb.clear();
+    for (uint32_t i = threadIdx.x; i < 2 * SP; i += blockDim.x) {
+      acc[i] = 0;
+      if (RAW) racc[i] = 0;
+    }
+    for (uint32_t i = threadIdx.x; i < S; i += blockDim.x) tag[i] = EMPTY_TAG;
     __syncthreads();
-    for (uint32_t base = r0; base < r1; base += blockDim.x) {  // uniform trip count
-      const uint32_t i = base + threadIdx.x;
-      const bool valid = i < r1;
-      uint64_t vlo = 0, w1 = 0, d = 0;
-      if (valid) {
-        vlo = rec[2 * (size_t)i];
-        w1 = rec[2 * (size_t)i + 1];
-        if (RAW) d = rraw[i];
+    // four records per lane per step; the next step's records are loaded
+    // while this step accumulates (indices clamped into the item)
+    v2l nr[4];
+    uint64_t nd[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t ic = min(r0 + j * blockDim.x + threadIdx.x, r1 - 1);
+      nr[j] = __builtin_nontemporal_load((const v2l*)(rec + 2 * (size_t)ic));
+      nd[j] = RAW ? rraw[ic] : 0;
+    }
+    for (uint32_t base = r0; base < r1; base += 4 * blockDim.x) {  // uniform trip count
+      uint64_t vlo[4], vhi[4], d[4];
+      uint32_t low[4], ph[4], gi[4];
+      bool valid[4];
+      uint4 tv[4];
+      v2l cr[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        cr[j] = nr[j];
+        d[j] = nd[j];
       }
-      const uint32_t low = (uint32_t)(w1 >> 36), ph = (uint32_t)(w1 >> 33) & 7u;
-      const uint64_t vhi = w1 & (((uint64_t)1 << 33) - 1);
-      const int32_t sl = valid ? tb.slot(low) : -1;
-      if (valid && sl >= 0) {
-        const uint32_t gi = (uint32_t)sl * P + ph;
-        lds_add2(&tb.lo[gi], &tb.hi[gi], vlo, vhi + (1ull << ATREX_COUNT_SHIFT));
-        if (RAW) lds_add2(&tb.rlo[gi], &tb.rhi[gi], d, 0);
+      if (base + 4 * blockDim.x < r1) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t ic = min(base + 4 * blockDim.x + j * blockDim.x + threadIdx.x, r1 - 1);
+          nr[j] = __builtin_nontemporal_load((const v2l*)(rec + 2 * (size_t)ic));
+          nd[j] = RAW ? rraw[ic] : 0;
+        }
       }
-      const uint32_t key = unmix32((bkt << lowbits) | low);
-      row_append(rows, valid && sl < 0, ((uint64_t)key << 3) | ph, vlo, vhi + (1ull << ATREX_COUNT_SHIFT), d, 0, err);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t i = base + j * blockDim.x + threadIdx.x;
+        valid[j] = i < r1;
+        vlo[j] = (uint64_t)cr[j].x;
+        const uint64_t w1 = (uint64_t)cr[j].y;
+        low[j] = (uint32_t)(w1 >> 36);
+        ph[j] = (uint32_t)(w1 >> 33) & 7u;
+        vhi[j] = w1 & (((uint64_t)1 << 33) - 1);
+        tv[j] = bucket_tags((uint32_t)(((uint64_t)hash_mul(low[j]) * NBK) >> 32));
+      }
+      bool miss = false;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {  // branch-free match of the four tags
+        const uint32_t k = low[j];
+        const uint32_t bq = (uint32_t)(((uint64_t)hash_mul(k) * NBK) >> 32);
+        const uint32_t mask = (tv[j].x == k ? 1u : 0u) | (tv[j].y == k ? 2u : 0u) | (tv[j].z == k ? 4u : 0u) |
+                              (tv[j].w == k ? 8u : 0u);
+        const bool hit = valid[j] && mask != 0;
+        gi[j] = hit ? (4 * bq + (uint32_t)(__ffs(mask) - 1)) * P + ph[j] : 0xFFFFFFFFu;
+        miss |= valid[j] && !hit;
+      }
+      if (__any(miss)) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          int32_t sl = -2;
+          if (valid[j] && gi[j] == 0xFFFFFFFFu) {
+            sl = find_slot(low[j], (uint32_t)(((uint64_t)hash_mul(low[j]) * NBK) >> 32), tv[j]);
+            if (sl >= 0) gi[j] = (uint32_t)sl * P + ph[j];
+          }
+          const uint32_t key = unmix32((bkt << lowbits) | low[j]);
+          row_append(rows, sl == -1, ((uint64_t)key << 3) | ph[j], vlo[j], vhi[j] + (1ull << ATREX_COUNT_SHIFT),
+                     d[j], 0, err);
+        }
+      }
+      // one (slot, phase) for most of the wave: sum those lanes first
+      {
+        const uint64_t act = __ballot(gi[0] != 0xFFFFFFFFu);
+        if (act) {
+          const uint32_t fl = __ffsll((unsigned long long)act) - 1;
+          const uint32_t lead0 = __builtin_amdgcn_readlane(gi[0], fl);
+          if (__popcll(__ballot(gi[0] == lead0)) >= 32) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const uint64_t a2 = __ballot(gi[j] != 0xFFFFFFFFu);
+              if (a2 == 0) continue;
+              const uint32_t f2 = __ffsll((unsigned long long)a2) - 1;
+              const uint32_t lead = __builtin_amdgcn_readlane(gi[j], f2);
+              const uint64_t same = __ballot(gi[j] == lead);
+              if (__popcll(same) < 16) continue;
+              const bool mine = gi[j] == lead;
+              const u128 tot = wave_sum_u128(mine ? make_u128(vlo[j], vhi[j]) : (u128)0);
+              u128 rtot = 0;
+              if (RAW) rtot = wave_sum_u128(mine ? (u128)d[j] : (u128)0);
+              const uint64_t tlo = __shfl((unsigned long long)(uint64_t)tot, 0, 64);
+              const uint64_t thi = __shfl((unsigned long long)(uint64_t)(tot >> 64), 0, 64);
+              uint64_t rl = 0, rh = 0;
+              if (RAW) {
+                rl = __shfl((unsigned long long)(uint64_t)rtot, 0, 64);
+                rh = __shfl((unsigned long long)(uint64_t)(rtot >> 64), 0, 64);
+              }
+              if (lane == f2) {
+                acc_add_n(&acc[2 * lead], &acc[2 * lead + 1], make_u128(tlo, thi), (uint32_t)__popcll(same));
+                if (RAW) acc_add_plain(&racc[2 * lead], &racc[2 * lead + 1], make_u128(rl, rh));
+              }
+              if (mine) gi[j] = 0xFFFFFFFFu;
+            }
+          }
+        }
+      }
+      uint32_t at[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) at[j] = gi[j] != 0xFFFFFFFFu ? 2 * gi[j] : dummy;
+      unsigned long long old[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) old[j] = atomicAdd(&acc[at[j]], (unsigned long long)vlo[j]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        atomicAdd(&acc[at[j] + 1],
+                  (unsigned long long)vhi[j] + ((old[j] + vlo[j] < old[j]) ? 1ull : 0ull) + (1ull << ATREX_COUNT_SHIFT));
+      if (RAW) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) old[j] = atomicAdd(&racc[at[j]], (unsigned long long)d[j]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (old[j] + d[j] < old[j]) atomicAdd(&racc[at[j] + 1], 1ull);
+      }
     }
     __syncthreads();
-    for (uint32_t base = 0; base < S * P; base += blockDim.x) {
-      const uint32_t i = base + threadIdx.x;
-      bool want = false;
-      uint64_t rk = 0, lo = 0, hi = 0, rl = 0, rh = 0;
-      if (i < S * P) {
-        const uint32_t s = i / P, ph = i - s * P;
-        const uint32_t t = tb.tag[s];
-        hi = tb.hi[i];
-        want = t != EMPTY_TAG && (hi >> ATREX_COUNT_SHIFT) != 0;
-        if (want) rk = ((uint64_t)unmix32((bkt << lowbits) | t) << 3) | ph;
-        lo = tb.lo[i];
-        if (RAW) { rl = tb.rlo[i]; rh = tb.rhi[i]; }
+    // the item's rows: each thread takes a contiguous run of (slot, phase)
+    // entries; one row-list reservation per workgroup
+    const uint32_t per = (SP + blockDim.x - 1) / blockDim.x, e0 = threadIdx.x * per;
+    auto present = [&](uint32_t i) {
+      return i < SP && tag[i / P] != EMPTY_TAG && (acc[2 * i + 1] >> ATREX_COUNT_SHIFT) != 0;
+    };
+    uint32_t mine = 0;
+    for (uint32_t k = 0; k < per; ++k) mine += present(e0 + k) ? 1u : 0u;
+    uint32_t inc = mine;
+    const uint32_t wl = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    for (int dd = 1; dd < 64; dd <<= 1) {
+      const uint32_t y = __shfl_up(inc, dd, 64);
+      if (wl >= (uint32_t)dd) inc += y;
+    }
+    if (wl == 63) s_wsum[wv] = inc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t tot = 0;
+      for (uint32_t x = 0; x < blockDim.x / 64; ++x) tot += s_wsum[x];
+      s_base = atomicAdd(rows.count, (unsigned long long)tot);
+    }
+    __syncthreads();
+    uint64_t pos = s_base + inc - mine;
+    for (uint32_t x = 0; x < wv; ++x) pos += s_wsum[x];
+    for (uint32_t k = 0; k < per; ++k) {
+      const uint32_t i = e0 + k;
+      if (!present(i)) continue;
+      if (pos >= rows.cap) {
+        atomicOr(err, ATREX_ERRBIT_CAPACITY);
+        break;
       }
-      row_append(rows, want, rk, lo, hi, rl, rh, err);
+      const uint32_t sl = i / P, ph = i - sl * P;
+      rows.rk[pos] = ((uint64_t)unmix32((bkt << lowbits) | tag[sl]) << 3) | ph;
+      rows.lo[pos] = acc[2 * i];
+      rows.hi[pos] = acc[2 * i + 1];
+      if (RAW) { rows.rlo[pos] = racc[2 * i]; rows.rhi[pos] = racc[2 * i + 1]; }
+      ++pos;
     }
     __syncthreads();
   }
@@ -624,10 +936,21 @@ uint32_t grid_of(uint64_t n, uint32_t b) { return (uint32_t)((n + b - 1) / b); }
 
 uint32_t lds_table_slots(uint32_t P, bool raw, size_t lds_bytes) {
   const size_t per = 4 + (size_t)16 * P * (raw ? 2 : 1);
-  return (uint32_t)((lds_bytes - 2048) / per);
+  const size_t fixed = 2048 + (size_t)64 * 16 * (raw ? 2 : 1);
+  return (uint32_t)(((lds_bytes - fixed) / per) & ~(size_t)3);  // whole buckets of four
 }
 
-size_t lds_table_bytes(uint32_t P, bool raw, uint32_t S) { return (size_t)S * (4 + (size_t)16 * P * (raw ? 2 : 1)); }
+size_t lds_table_bytes(uint32_t P, bool raw, uint32_t S) {
+  return ((size_t)S * P * 16 + 64 * 16) * (raw ? 2 : 1) + (size_t)S * 4;
+}
+
+static uint32_t scatter_ept(uint32_t BB, bool raw) { return (!raw && BB <= 10) ? 8 : 4; }
+
+static size_t scatter_smem(uint32_t BB, bool raw) {
+  return (size_t)scatter_ept(BB, raw) * SC_BLOCK * (16 + (raw ? 8 : 0) + 2) + ((size_t)3 << BB) * 4;
+}
+
+uint32_t part_scatter_wgs(uint32_t cus) { return std::min<uint32_t>(kMaxPartWG, cus); }
 
 
 void launch_part_hist(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t BB, uint32_t* H) {
@@ -635,14 +958,18 @@ void launch_part_hist(hipStream_t s, const PartSource& src, uint32_t nwg, uint32
 }
 
 void launch_part_scatter(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t A, uint32_t P,
-                         const uint64_t* scale, uint32_t BB, const uint32_t* O, uint64_t* rec, uint64_t* rraw,
-                         uint32_t* err) {
+                         const uint64_t* scale, const uint64_t* bscale, uint32_t BB, const uint32_t* O, uint64_t* rec,
+                         uint64_t* rraw, uint32_t* err) {
+  const size_t smem = scatter_smem(BB, rraw != nullptr);
   if (rraw)
-    hipLaunchKernelGGL(k_part_scatter<true>, dim3(nwg), dim3(1024), (size_t)4 << BB, s, src, A, P, scale, BB, O, rec,
-                       rraw, err);
+    hipLaunchKernelGGL((k_part_scatter<true, 4>), dim3(nwg), dim3(SC_BLOCK), smem, s, src, A, P, scale, bscale, BB,
+                       O, rec, rraw, err);
+  else if (scatter_ept(BB, false) == 8)
+    hipLaunchKernelGGL((k_part_scatter<false, 8>), dim3(nwg), dim3(SC_BLOCK), smem, s, src, A, P, scale, bscale, BB,
+                       O, rec, rraw, err);
   else
-    hipLaunchKernelGGL(k_part_scatter<false>, dim3(nwg), dim3(1024), (size_t)4 << BB, s, src, A, P, scale, BB, O,
-                       rec, rraw, err);
+    hipLaunchKernelGGL((k_part_scatter<false, 4>), dim3(nwg), dim3(SC_BLOCK), smem, s, src, A, P, scale, bscale, BB,
+                       O, rec, rraw, err);
 }
 
 void launch_part_items(hipStream_t s, const uint32_t* O, const uint32_t* H, uint32_t nw, uint32_t BB, uint32_t CH,
@@ -716,7 +1043,8 @@ void launch_lists_to_rows(hipStream_t s, const OwnerLists& ol, const Rows& rows,
 hipError_t set_rows_smem_limits() {
   const void* fns[] = {(const void*)k_rank_groups,
                        (const void*)k_part_aggregate<true>, (const void*)k_part_aggregate<false>,
-                       (const void*)k_part_hist, (const void*)k_part_scatter<true>, (const void*)k_part_scatter<false>};
+                       (const void*)k_part_hist, (const void*)k_part_scatter<true, 4>, (const void*)k_part_scatter<false, 4>,
+                       (const void*)k_part_scatter<false, 8>};
   for (const void* f : fns) {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 2048);
     if (e != hipSuccess) return e;
