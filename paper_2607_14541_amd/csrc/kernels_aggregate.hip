@@ -446,12 +446,16 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
                                                       uint32_t* __restrict__ err) {
   extern __shared__ unsigned long long smem[];
   const uint32_t SP = S * P;
-  // [S * P] x (lo, hi) interleaved, then 64 per-lane dummy entries that take
-  // the atomics of lanes with nothing to add (never read); RAW: the same again
-  const uint32_t region = 2 * SP + 2 * 64;
-  unsigned long long* s_acc = smem;
-  unsigned long long* s_raw = smem + region;    // RAW only
-  uint32_t* s_tag = (uint32_t*)(smem + (RAW ? 2 : 1) * region);
+  // low and high words of the [S * P] accumulators as two arrays (8-byte
+  // stride: twice the LDS banks of interleaved pairs for the random 64-bit
+  // atomics), each followed by 64 per-lane dummy entries that take the atomics
+  // of lanes with nothing to add (never read); RAW: the same again
+  const uint32_t NE = SP + 64;
+  unsigned long long* s_lo = smem;
+  unsigned long long* s_hi = smem + NE;
+  unsigned long long* s_rlo = smem + 2 * NE;  // RAW only
+  unsigned long long* s_rhi = smem + 3 * NE;
+  uint32_t* s_tag = (uint32_t*)(smem + (RAW ? 4 : 2) * NE);
   uint32_t* s_ocnt = s_tag + S;                 // [ATREX_OWNERS]
   uint32_t& s_spills = s_ocnt[ATREX_OWNERS];    // dynamic LDS: static LDS would not fit beside 160 KB
   // Pass A has validated every event (app < A, phase < P, dur >= 0) and the
@@ -465,11 +469,12 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
     return;
   }
   if (threadIdx.x == 0) s_spills = 0;
-  for (uint32_t i = threadIdx.x; i < 2 * SP; i += BLOCK) {
-    s_acc[i] = 0;
-    if (RAW) s_raw[i] = 0;
+  for (uint32_t i = threadIdx.x; i < SP; i += BLOCK) {
+    s_lo[i] = 0;
+    s_hi[i] = 0;
+    if (RAW) { s_rlo[i] = 0; s_rhi[i] = 0; }
   }
-  const uint32_t dummy = 2 * SP + 2 * (threadIdx.x & 63);  // this lane's dummy entry
+  const uint32_t dummy = SP + (threadIdx.x & 63);  // this lane's dummy entry
   for (uint32_t i = threadIdx.x; i < S; i += BLOCK) s_tag[i] = ATREX_EMPTY_KEY;
   for (uint32_t i = threadIdx.x; i < ATREX_OWNERS; i += BLOCK) s_ocnt[i] = 0;
   __syncthreads();
@@ -565,15 +570,31 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
       gi[j] = (valid[j] && hit) ? __umul24(4 * g.bucket[j] + (uint32_t)(__ffs(mask) - 1), P) + ph[j] : INVALID_GI;
       miss |= valid[j] && !hit;
     }
-    if (__builtin_expect(__any(miss), 0)) {  // key not in its home bucket: probe on, then spill what is unplaced
+    if (__builtin_expect(__any(miss), 0)) {
+      // not in the home bucket: most such keys sit in the next bucket
+      miss = false;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        if (valid[j] && gi[j] == INVALID_GI && g.key[j] != ATREX_EMPTY_KEY) {
-          const uint32_t sl = find_slot(g.key[j], g.bucket[j], tv[j]);
-          if (sl != INVALID_GI) gi[j] = __umul24(sl, P) + ph[j];
+        const uint32_t k = g.key[j];
+        if (valid[j] && gi[j] == INVALID_GI && k != ATREX_EMPTY_KEY) {
+          const uint32_t b2 = (g.bucket[j] + 1 == NB) ? 0 : g.bucket[j] + 1;
+          const uint4 t2 = bucket_tags(b2);
+          const uint32_t mask = (t2.x == k ? 1u : 0u) | (t2.y == k ? 2u : 0u) | (t2.z == k ? 4u : 0u) |
+                                (t2.w == k ? 8u : 0u);
+          if (mask) gi[j] = __umul24(4 * b2 + (uint32_t)(__ffs(mask) - 1), P) + ph[j];
         }
-        spill_append(sp, &s_spills, valid[j] && gi[j] == INVALID_GI, g.key[j], make_u128(vlo[j], vhi[j]), ph[j],
-                     (uint64_t)g.dur[j], err);
+        miss |= valid[j] && gi[j] == INVALID_GI;
+      }
+      if (__any(miss)) {  // first occurrence, or farther away: probe on, then spill what is unplaced
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (valid[j] && gi[j] == INVALID_GI && g.key[j] != ATREX_EMPTY_KEY) {
+            const uint32_t sl = find_slot(g.key[j], g.bucket[j], tv[j]);
+            if (sl != INVALID_GI) gi[j] = __umul24(sl, P) + ph[j];
+          }
+          spill_append(sp, &s_spills, valid[j] && gi[j] == INVALID_GI, g.key[j], make_u128(vlo[j], vhi[j]), ph[j],
+                       (uint64_t)g.dur[j], err);
+        }
       }
     }
     // hot group: when at least half the lanes share the first lane's (slot,
@@ -609,8 +630,8 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
           rhi = __shfl((unsigned long long)(uint64_t)(rtot >> 64), 0, 64);
         }
         if (lane == fl) {
-          acc_add_n(&s_acc[2 * lead], &s_acc[2 * lead + 1], make_u128(tlo, thi), __popcll(same));
-          if (RAW) acc_add_plain(&s_raw[2 * lead], &s_raw[2 * lead + 1], make_u128(rlo, rhi));
+          acc_add_n(&s_lo[lead], &s_hi[lead], make_u128(tlo, thi), __popcll(same));
+          if (RAW) acc_add_plain(&s_rlo[lead], &s_rhi[lead], make_u128(rlo, rhi));
         }
         if (mine) gi[j] = INVALID_GI;
       }
@@ -620,21 +641,21 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
     // returned values give the carries), then the high words with the count.
     uint32_t at[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) at[j] = gi[j] != INVALID_GI ? 2 * gi[j] : dummy;
+    for (int j = 0; j < 4; ++j) at[j] = gi[j] != INVALID_GI ? gi[j] : dummy;
     unsigned long long old[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) old[j] = atomicAdd(&s_acc[at[j]], (unsigned long long)vlo[j]);
+    for (int j = 0; j < 4; ++j) old[j] = atomicAdd(&s_lo[at[j]], (unsigned long long)vlo[j]);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const unsigned long long carry = (old[j] + vlo[j] < old[j]) ? 1ull : 0ull;
-      atomicAdd(&s_acc[at[j] + 1], (unsigned long long)vhi[j] + carry + (1ull << ATREX_COUNT_SHIFT));
+      atomicAdd(&s_hi[at[j]], (unsigned long long)vhi[j] + carry + (1ull << ATREX_COUNT_SHIFT));
     }
     if (RAW) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) old[j] = atomicAdd(&s_raw[at[j]], (unsigned long long)g.dur[j]);
+      for (int j = 0; j < 4; ++j) old[j] = atomicAdd(&s_rlo[at[j]], (unsigned long long)g.dur[j]);
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        if (old[j] + (uint64_t)g.dur[j] < old[j]) atomicAdd(&s_raw[at[j] + 1], 1ull);
+        if (old[j] + (uint64_t)g.dur[j] < old[j]) atomicAdd(&s_rhi[at[j]], 1ull);
     }
   };
   // Grid-stride over groups of four events with a wave-uniform trip count, as
@@ -700,11 +721,11 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
         const size_t rec = ((size_t)blockIdx.x * ATREX_OWNERS + o) * orr.capo + r;
         orr.key[rec] = t;
         for (uint32_t ph = 0; ph < P; ++ph) {
-          orr.acc[(rec * P + ph) * 2] = s_acc[2 * (sl * P + ph)];
-          orr.acc[(rec * P + ph) * 2 + 1] = s_acc[2 * (sl * P + ph) + 1];
+          orr.acc[(rec * P + ph) * 2] = s_lo[sl * P + ph];
+          orr.acc[(rec * P + ph) * 2 + 1] = s_hi[sl * P + ph];
           if (RAW) {
-            orr.raw[(rec * P + ph) * 2] = s_raw[2 * (sl * P + ph)];
-            orr.raw[(rec * P + ph) * 2 + 1] = s_raw[2 * (sl * P + ph) + 1];
+            orr.raw[(rec * P + ph) * 2] = s_rlo[sl * P + ph];
+            orr.raw[(rec * P + ph) * 2 + 1] = s_rhi[sl * P + ph];
           }
         }
       } else {
@@ -712,11 +733,11 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
       }
     }
     for (uint32_t ph = 0; ph < P; ++ph) {
-      const size_t gi = 2 * ((size_t)sl * P + ph);
-      const uint64_t hi = spill_rows ? s_acc[gi + 1] : 0;
+      const size_t gi = (size_t)sl * P + ph;
+      const uint64_t hi = spill_rows ? s_hi[gi] : 0;
       const bool want = spill_rows && (hi >> ATREX_COUNT_SHIFT) != 0;
-      row_push(rows, want, ((uint64_t)t << 3) | ph, want ? s_acc[gi] : 0, hi,
-               (RAW && want) ? s_raw[gi] : 0, (RAW && want) ? s_raw[gi + 1] : 0, err);
+      row_push(rows, want, ((uint64_t)t << 3) | ph, want ? s_lo[gi] : 0, hi,
+               (RAW && want) ? s_rlo[gi] : 0, (RAW && want) ? s_rhi[gi] : 0, err);
     }
   }
   __syncthreads();
