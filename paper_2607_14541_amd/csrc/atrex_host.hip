@@ -601,6 +601,8 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
   const Rows rows = c->rows();
   atrex_path path = c->path;
   if (path == ATREX_PATH_AUTO) path = (c->p.max_keys <= L.ldsSlots) ? ATREX_PATH_LDS_HASH : ATREX_PATH_RADIX_SORT;
+  // the LDS engine indexes its scale words with 24-bit multiplies
+  if (path == ATREX_PATH_LDS_HASH && (uint64_t)A * P >= (1u << 24)) path = ATREX_PATH_RADIX_SORT;
   if (!vec_ok && path != ATREX_PATH_GLOBAL_HASH) path = ATREX_PATH_GLOBAL_HASH;
   const uint32_t nwg = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)c->cus, kMaxWG));
   atrex_status st = ATREX_OK;

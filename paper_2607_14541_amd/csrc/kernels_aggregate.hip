@@ -356,13 +356,14 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_global(EventsDev ev, uint32_t 
 // ---------------------------------------------------------------------------
 // Pass B with a per-workgroup LDS hash table (the low/medium-cardinality
 // engine).  LDS holds S slots in buckets of four (S sized to the LDS budget,
-// not a power of two): a key tag and, per phase, a two-word accumulator.  Per
-// event: the home bucket's four tags are read with one 16-byte LDS load and
-// compared; a key absent from its bucket is looked up in the following
-// buckets and inserted into the first free slot (at most MAXPROBE buckets); an
-// event whose key finds no slot (or the reserved tag value) is appended to a
-// spill list and handled after the kernel, so that no wave waits on
-// device-wide atomics.  Before the LDS atomics, lanes of a wave that hit the
+// not a power of two): a key tag and, per phase, a two-word accumulator.  A
+// key's home bucket is one of the first S / 4 - 1 buckets; its window is the
+// home bucket and the next one.  Per event the window's eight tags are read
+// with two 16-byte LDS loads and matched without branches.  A key outside its
+// window is looked up by probing on from the home bucket and inserted into the
+// first free slot (at most MAXPROBE buckets); an event whose key finds no slot
+// (or the reserved tag value) is appended to a spill list and handled after
+// the kernel, so that no wave waits on device-wide atomics.  Before the LDS atomics, lanes of a wave that hit the
 // same (slot, phase) as the wave's first active lane are summed with shuffles
 // and added once (hot keys).  At the end each workgroup writes its table into
 // 256 owner regions (owner = top byte of the key hash); k_owner_finish sums
@@ -430,10 +431,10 @@ __device__ __forceinline__ void row_push(const Rows& R, bool want, uint64_t rk, 
   }
 }
 
-// Events of one group of four per lane, once their scale words and first-probe
-// tags have been requested: everything the accumulation step needs.
+// Events of one group of four per lane, once their scale words have been
+// requested: everything the accumulation step needs.
 struct StagedEv4 {
-  uint32_t key[4], bucket[4];
+  uint32_t key[4], gi[4];  // keys, LDS entries found in the windows (or INVALID_GI)
   uint32_t ph4;        // the four phases, one byte each
   int64_t dur[4];
   uint64_t sw[4];      // pass-B scale words
@@ -481,8 +482,8 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
   const uint64_t n = ev.n, n4 = n / 4;
   const uint64_t stride = (uint64_t)gridDim.x * BLOCK;
   const uint32_t lane = lane_id();
-  const uint32_t NB = S / 4;     // buckets; S is a multiple of 4
-  const uint32_t NB8 = NB << 8;  // bucket = mulhi24(hash >> 8, NB << 8) = floor((hash >> 8) * NB / 2^24), NB < 2^16
+  const uint32_t NB = S / 4;         // buckets; S is a multiple of 4, S >= 8
+  const uint32_t NH8 = (NB - 1) << 8;  // home bucket = floor((hash >> 8) * (NB - 1) / 2^24), NB < 2^16
   auto bucket_tags = [&](uint32_t b) -> uint4 { return *(const uint4*)&s_tag[4 * b]; };
   // Slot of key k from its home bucket b (tags tv already read): the key's
   // slot in this or a following bucket, else the first free slot claimed for
@@ -511,24 +512,59 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
     }
     return INVALID_GI;
   };
-  // stage(): request the scale words of a loaded group, keep what the
-  // accumulation step needs.
+  // stage(): request the scale words of a loaded group and find its events'
+  // slots in their windows (a chain of selects over the eight tags, last slot
+  // first, gives the first slot holding the key).  The host takes this engine
+  // only when A * P < 2^24, so the scale word index is one 24-bit multiply-add.
+  auto home_bucket = [&](uint32_t k) -> uint32_t {
+    return (uint32_t)(((uint64_t)(hash_mul(k) >> 8) * (NH8 & 0xFFFFFFu)) >> 32);
+  };
   auto stage = [&](const Ev4& e, StagedEv4& g) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      g.sw[j] = bscale[e.app[j] * P + e.ph[j]];
-      g.bucket[j] = (uint32_t)(((uint64_t)(hash_mul(e.key[j]) >> 8) * (NB8 & 0xFFFFFFu)) >> 32);
+      g.sw[j] = bscale[__umul24(e.app[j], P) + e.ph[j]];
       g.key[j] = e.key[j];
       g.dur[j] = e.dur[j];
     }
     g.ph4 = e.ph[0] | (e.ph[1] << 8) | (e.ph[2] << 16) | (e.ph[3] << 24);
-  };
-  // process(): shares, slots, accumulation of a staged group.  `first` is the
-  // index of event 0 (for the rare paths that re-read an event's fields).
-  auto process = [&](const bool valid[4], const StagedEv4& g, uint64_t first) {
-    uint4 tv[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) tv[j] = bucket_tags(g.bucket[j]);
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t k = e.key[j], b = home_bucket(k);
+      const uint4 t0 = bucket_tags(b), t1 = bucket_tags(b + 1);
+      uint32_t w = INVALID_GI;
+      w = t1.w == k ? 7u : w;
+      w = t1.z == k ? 6u : w;
+      w = t1.y == k ? 5u : w;
+      w = t1.x == k ? 4u : w;
+      w = t0.w == k ? 3u : w;
+      w = t0.z == k ? 2u : w;
+      w = t0.y == k ? 1u : w;
+      w = t0.x == k ? 0u : w;
+      const bool hit = w != INVALID_GI && k != ATREX_EMPTY_KEY;
+      g.gi[j] = hit ? __umul24(4 * b + w, P) + e.ph[j] : INVALID_GI;
+    }
+  };
+  // Grid-stride over groups of four events: iteration `it` of a wave covers
+  // groups wave_first + it * stride + [0, 64); the wave index goes through a
+  // lane read so that the compiler keeps the loop control and the load bases
+  // in scalar registers.
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint64_t wave_first = (uint64_t)blockIdx.x * BLOCK + 64 * wave;
+  const uint64_t iters = wave_first < n4 ? (n4 - 1 - wave_first) / stride + 1 : 0;
+  const uint64_t full = wave_first + 64 <= n4 ? (n4 - 64 - wave_first) / stride + 1 : 0;
+  constexpr uint64_t TAIL = ~0ull;  // `it` of the n % 4 tail events (one per lane, first wave)
+  // events of this lane's group that exist, and the index of its event 0:
+  // wanted only on the rare paths
+  auto nvalid_of = [&](uint64_t it) -> uint32_t {
+    if (it == TAIL) return n4 * 4 + lane < n ? 1u : 0u;
+    return (it < full || wave_first + it * stride + lane < n4) ? 4u : 0u;
+  };
+  auto first_of = [&](uint64_t it) -> uint64_t {
+    return it == TAIL ? n4 * 4 + lane : (wave_first + it * stride + lane) * 4;
+  };
+  // process(): shares, slots, accumulation of a staged group.  Events past
+  // the end carry the reserved key, so they miss the window.
+  auto process = [&](const StagedEv4& g, uint64_t it) {
     uint32_t ph[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) ph[j] = (g.ph4 >> (8 * j)) & 0xFFu;
@@ -536,14 +572,17 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
     uint32_t slow = 0, wide = 0;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      slow |= (uint32_t)(g.sw[j] >> 56) & ~127u;
+      slow |= (uint32_t)(g.sw[j] >> 32);
       wide |= (uint32_t)((uint64_t)g.dur[j] >> 32);
     }
-    if (__builtin_expect(__any(slow != 0), 0)) {  // rho outside [-8, 63]: the general scale word
+    if (__builtin_expect(__any((slow >> 31) != 0), 0)) {  // rho outside [-8, 63]: the general scale word
+      const uint32_t nvalid = nvalid_of(it);
+      const uint64_t first = first_of(it);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const uint64_t i = valid[j] ? first + j : 0;
-        const u128 v = event_share((uint64_t)g.dur[j], valid[j] ? scale[ev.app[i] * P + ph[j]] : 0);
+        const bool valid = (uint32_t)j < nvalid;
+        const uint64_t i = valid ? first + j : 0;
+        const u128 v = event_share((uint64_t)g.dur[j], valid ? scale[ev.app[i] * P + ph[j]] : 0);
         vlo[j] = (uint64_t)v;
         vhi[j] = (uint64_t)(v >> 64);
       }
@@ -563,38 +602,23 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
     bool miss = false;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const uint32_t k = g.key[j];
-      const uint32_t mask = (tv[j].x == k ? 1u : 0u) | (tv[j].y == k ? 2u : 0u) | (tv[j].z == k ? 4u : 0u) |
-                            (tv[j].w == k ? 8u : 0u);
-      const bool hit = mask != 0 && k != ATREX_EMPTY_KEY;
-      gi[j] = (valid[j] && hit) ? __umul24(4 * g.bucket[j] + (uint32_t)(__ffs(mask) - 1), P) + ph[j] : INVALID_GI;
-      miss |= valid[j] && !hit;
+      gi[j] = g.gi[j];
+      miss |= gi[j] == INVALID_GI;
     }
     if (__builtin_expect(__any(miss), 0)) {
-      // not in the home bucket: most such keys sit in the next bucket
-      miss = false;
+      // first occurrence of a key, a key placed past its window, the reserved
+      // key, or events past the end: probe on, then spill what is unplaced
+      const uint32_t nvalid = nvalid_of(it);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const uint32_t k = g.key[j];
-        if (valid[j] && gi[j] == INVALID_GI && k != ATREX_EMPTY_KEY) {
-          const uint32_t b2 = (g.bucket[j] + 1 == NB) ? 0 : g.bucket[j] + 1;
-          const uint4 t2 = bucket_tags(b2);
-          const uint32_t mask = (t2.x == k ? 1u : 0u) | (t2.y == k ? 2u : 0u) | (t2.z == k ? 4u : 0u) |
-                                (t2.w == k ? 8u : 0u);
-          if (mask) gi[j] = __umul24(4 * b2 + (uint32_t)(__ffs(mask) - 1), P) + ph[j];
+        const bool valid = (uint32_t)j < nvalid;
+        if (valid && gi[j] == INVALID_GI && g.key[j] != ATREX_EMPTY_KEY) {
+          const uint32_t b = home_bucket(g.key[j]);
+          const uint32_t sl = find_slot(g.key[j], b, bucket_tags(b));
+          if (sl != INVALID_GI) gi[j] = __umul24(sl, P) + ph[j];
         }
-        miss |= valid[j] && gi[j] == INVALID_GI;
-      }
-      if (__any(miss)) {  // first occurrence, or farther away: probe on, then spill what is unplaced
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          if (valid[j] && gi[j] == INVALID_GI && g.key[j] != ATREX_EMPTY_KEY) {
-            const uint32_t sl = find_slot(g.key[j], g.bucket[j], tv[j]);
-            if (sl != INVALID_GI) gi[j] = __umul24(sl, P) + ph[j];
-          }
-          spill_append(sp, &s_spills, valid[j] && gi[j] == INVALID_GI, g.key[j], make_u128(vlo[j], vhi[j]), ph[j],
-                       (uint64_t)g.dur[j], err);
-        }
+        spill_append(sp, &s_spills, valid && gi[j] == INVALID_GI, g.key[j], make_u128(vlo[j], vhi[j]), ph[j],
+                     (uint64_t)g.dur[j], err);
       }
     }
     // hot group: when at least half the lanes share the first lane's (slot,
@@ -658,54 +682,50 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
         if (old[j] + (uint64_t)g.dur[j] < old[j]) atomicAdd(&s_rhi[at[j]], 1ull);
     }
   };
-  // Grid-stride over groups of four events with a wave-uniform trip count, as
-  // a three-stage pipeline: while group i is accumulated, the scale words and
-  // tags of group i + 1 and the loads of group i + 2 are in flight.  Indices
-  // are clamped to the last group, so every load is in bounds; `valid` masks
-  // the lanes past the end.
-  const uint64_t wave_first = (uint64_t)blockIdx.x * BLOCK + (threadIdx.x & ~63u);
-  if (wave_first < n4) {
-    const uint64_t last = n4 - 1;
-    uint64_t q = wave_first + lane, qw = wave_first;
+  // A three-stage pipeline: while iteration it is accumulated, the scale
+  // words of it + 1 and the loads of it + 2 are in flight.  Iterations whose
+  // 64 groups all exist load through the wave's scalar base address; the one
+  // partial iteration (at most one per grid) clamps its indices and gives the
+  // events past the end the reserved key.
+  if (iters > 0) {
+    auto load_it = [&](uint64_t it, Ev4& e) {
+      const uint64_t g0 = wave_first + it * stride;
+      if (it < full) {
+        load4_lane(ev.key, ev.app, ev.phase, ev.dur, g0 * 4, lane, e);
+      } else {
+        const uint64_t q = g0 + lane;
+        load4<true>(ev.key, ev.app, ev.phase, ev.dur, min(q, n4 - 1) * 4, e);
+        if (q >= n4) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) e.key[j] = ATREX_EMPTY_KEY;
+        }
+      }
+    };
     Ev4 raw;
     StagedEv4 gA, gB;
-    load4<true>(ev.key, ev.app, ev.phase, ev.dur, min(q, last) * 4, raw);
+    load_it(0, raw);
     stage(raw, gA);
-    load4<true>(ev.key, ev.app, ev.phase, ev.dur, min(q + stride, last) * 4, raw);
-    for (;;) {
-      stage(raw, gB);
-      load4<true>(ev.key, ev.app, ev.phase, ev.dur, min(q + 2 * stride, last) * 4, raw);
-      {
-        const bool v = q < n4;
-        const bool valid[4] = {v, v, v, v};
-        process(valid, gA, min(q, last) * 4);
-      }
-      qw += stride;
-      q += stride;
-      if (qw >= n4) break;
-      stage(raw, gA);
-      load4<true>(ev.key, ev.app, ev.phase, ev.dur, min(q + 2 * stride, last) * 4, raw);
-      {
-        const bool v = q < n4;
-        const bool valid[4] = {v, v, v, v};
-        process(valid, gB, min(q, last) * 4);
-      }
-      qw += stride;
-      q += stride;
-      if (qw >= n4) break;
+    if (1 < iters) load_it(1, raw);
+    for (uint64_t it = 0;;) {
+      if (it + 1 < iters) stage(raw, gB);
+      if (it + 2 < iters) load_it(it + 2, raw);
+      process(gA, it);
+      if (++it >= iters) break;
+      if (it + 1 < iters) stage(raw, gA);
+      if (it + 2 < iters) load_it(it + 2, raw);
+      process(gB, it);
+      if (++it >= iters) break;
     }
   }
   if (blockIdx.x == 0 && threadIdx.x < 64) {  // n % 4 tail events, one wave
     const uint64_t i = n4 * 4 + lane;
-    const bool valid[4] = {i < n, false, false, false};
-    const uint64_t ic = valid[0] ? i : 0;  // n >= 1 here whenever valid[0]
     Ev4 e;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) { e.key[j] = 0; e.app[j] = 0; e.ph[j] = 0; e.dur[j] = 0; }
-    if (n > 0) { e.key[0] = ev.key[ic]; e.app[0] = ev.app[ic]; e.ph[0] = ev.phase[ic]; e.dur[0] = ev.dur[ic]; }
+    for (int j = 0; j < 4; ++j) { e.key[j] = ATREX_EMPTY_KEY; e.app[j] = 0; e.ph[j] = 0; e.dur[j] = 0; }
+    if (i < n) { e.key[0] = ev.key[i]; e.app[0] = ev.app[i]; e.ph[0] = ev.phase[i]; e.dur[0] = ev.dur[i]; }
     StagedEv4 g;
     stage(e, g);
-    process(valid, g, ic);
+    process(g, TAIL);
   }
   __syncthreads();
   // this workgroup's table -> owner regions (owner = top byte of the key hash);
