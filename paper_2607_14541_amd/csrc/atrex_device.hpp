@@ -142,6 +142,12 @@ __device__ __forceinline__ u128 shfl_down_u128(u128 v, int d) {
   return make_u128(lo, hi);
 }
 
+__device__ __forceinline__ u128 shfl_up_u128(u128 v, int d) {
+  const uint64_t lo = __shfl_up((unsigned long long)(uint64_t)v, d, 64);
+  const uint64_t hi = __shfl_up((unsigned long long)(uint64_t)(v >> 64), d, 64);
+  return make_u128(lo, hi);
+}
+
 __device__ __forceinline__ u128 wave_sum_u128(u128 v) {
   for (int d = 32; d >= 1; d >>= 1) v += shfl_down_u128(v, d);
   return v;  // valid in lane 0

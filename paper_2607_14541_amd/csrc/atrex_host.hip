@@ -40,7 +40,7 @@ uint64_t next_pow2(uint64_t x) {
 struct Layout {
   size_t ctrl, T, carryA, partA, scale, bscale, dict, acc, raw;
   size_t okey, oacc, oraw, ocount, skey, sval, sraw, scount;  // LDS engine outputs
-  size_t ol_rk, ol_lo, ol_hi, ol_rlo, ol_rhi, ol_count, ol_part;  // per-owner sorted lists
+  size_t ol_rk, ol_key, ol_lo, ol_hi, ol_rlo, ol_rhi, ol_count, ol_part;  // per-owner sorted lists
   size_t H, O, rec, rraw, bstart, istart;                     // partition engine
   size_t rk, rlo_acc, rhi_acc, rlo_raw, rhi_raw;              // rows
   size_t sk[3], sv[3], rs_tmp, scan_tmp;
@@ -122,6 +122,7 @@ Layout make_layout(const Params& p) {
   L.oSlots = owner_list_slots(p.P, p.raw);
   const uint64_t olrows = (uint64_t)ATREX_OWNERS * L.oSlots * p.P;
   L.ol_rk = take(olrows * 8);
+  L.ol_key = take(olrows * 4);
   L.ol_lo = take(olrows * 8);
   L.ol_hi = take(olrows * 8);
   L.ol_rlo = take(p.raw ? olrows * 8 : 0);
@@ -294,6 +295,8 @@ struct atrex_ctx {
   OwnerLists lists() const {
     OwnerLists l;
     l.rk = at<uint64_t>(L.ol_rk);
+    l.dkey = at<uint32_t>(L.ol_key);
+    l.dcount = at<unsigned long long>(L.ctrl + 224);
     l.lo = at<uint64_t>(L.ol_lo);
     l.hi = at<uint64_t>(L.ol_hi);
     l.rlo = p.raw ? at<uint64_t>(L.ol_rlo) : nullptr;
@@ -733,7 +736,6 @@ atrex_status atrex_phase_normalize(atrex_ctx* c, const atrex_groups* out, uint64
   UnitTable ot{c->at<uint32_t>(L.op_id), c->at<uint64_t>(L.op_U), c->at<double>(L.op_w)};
   UnitTable kt{c->at<uint32_t>(L.key_id), c->at<uint64_t>(L.key_U), c->at<double>(L.key_w)};
   unsigned long long* cnt = c->at<unsigned long long>(L.ctrl + 256);
-  launch_fill_u64(s, (uint64_t*)cnt, 2, 0);
   TIMED(c, "units", G,
         launch_units(s, g, G, P, lcm_1_to(P), S, o, c->unit_scratch(), ot, L.maxOps, kt, cnt, c->err()));
   uint64_t h[2] = {0, 0};

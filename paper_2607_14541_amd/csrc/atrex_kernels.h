@@ -60,6 +60,8 @@ struct PartSource {
 // Per-owner sorted group lists written by the owner merge of the LDS engine.
 struct OwnerLists {
   uint64_t* rk;      // [ATREX_OWNERS][cap] sort keys key << 3 | phase, ascending within an owner
+  uint32_t* dkey;    // every list's row keys (rk >> 3), densely and in no particular order
+  unsigned long long* dcount;  // entries of dkey (zero before the owner merge)
   uint64_t* lo;      // accumulator low words
   uint64_t* hi;      // accumulator high words (W >> 64 | count << 33)
   uint64_t* rlo;     // raw time, nullable
@@ -195,6 +197,7 @@ struct UnitScratch {
   uint64_t* totals;    // [2][2]: sum U over operators, over keys
 };
 uint64_t units_tiles(uint64_t G);
+constexpr uint64_t kUnitsSmallMax = 8192;  // groups the one-workgroup unit kernel handles
 void launch_units(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t L, const uint64_t* S,
                   const GroupsOut& out, const UnitScratch& us, const UnitTable& ops, uint64_t maxOps,
                   const UnitTable& keys, unsigned long long* counts, uint32_t* err);

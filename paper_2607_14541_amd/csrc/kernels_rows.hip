@@ -115,27 +115,30 @@ struct LdsTable {
 // write them as a list with the per-phase partial sums of W.  Keys the table
 // cannot place go to the row list.
 constexpr uint32_t MAXPROBE_O = 64;
+constexpr uint32_t kRegionMap = 24 * 1024;  // records per owner mapped to their region by a byte table
 
 __device__ __forceinline__ uint32_t owner_of(uint32_t key) { return hash32(key) >> 24; }
 
-// exclusive prefix of n <= 256 counts (cnt(i)) into pre[0..n], one wave
-template <class F>
-__device__ __forceinline__ void wave_prefix256(uint32_t n, F cnt, uint32_t* pre) {
-  if (threadIdx.x < 64) {
-    uint32_t run = 0;
-    for (uint32_t w0 = 0; w0 < n; w0 += 64) {
-      const uint32_t w = w0 + threadIdx.x;
-      const uint32_t c = w < n ? cnt(w) : 0;
-      uint32_t inc = c;
-      for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t y = __shfl_up(inc, d, 64);
-        if (threadIdx.x >= (uint32_t)d) inc += y;
-      }
-      if (w < n) pre[w] = run + inc - c;
-      run += __shfl(inc, 63, 64);
-    }
-    if (threadIdx.x == 0) pre[n] = run;
+// Exclusive prefix of n <= 256 values into pre[0..n] (pre[n] = total): thread
+// t < n passes its value v (its own load, so all loads are in flight at
+// once), every thread of the workgroup calls; ends with a barrier.
+__device__ __forceinline__ void prefix256(uint32_t n, uint32_t v, uint32_t* pre, uint32_t* s_w4) {
+  const uint32_t t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const uint32_t x = t < n ? v : 0u;
+  uint32_t inc = x;
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(inc, d, 64);
+    if (lane >= (uint32_t)d) inc += y;
   }
+  if (w < 4 && lane == 63) s_w4[w] = inc;
+  __syncthreads();
+  if (t < 256) {
+    uint32_t off = 0;
+    for (uint32_t q = 0; q < w; ++q) off += s_w4[q];
+    if (t < n) pre[t] = off + inc - x;
+    if (t == 255) pre[n] = off + inc;
+  }
+  __syncthreads();
 }
 
 // last w with pre[w] <= idx (pre ascending, pre[0] = 0, idx < pre[n])
@@ -153,8 +156,8 @@ __global__ __launch_bounds__(1024) void k_owner_finish(OwnerRegions orr, uint32_
                                                        SpillIn sp, OwnerLists ol, Rows rows,
                                                        uint32_t* __restrict__ err) {
   extern __shared__ unsigned long long smem[];
-  __shared__ uint32_t s_pre[257], s_spre[257];
-  __shared__ uint32_t s_cnt;
+  __shared__ uint32_t s_pre[257], s_spre[257], s_w4[4];
+  __shared__ uint32_t s_cnt, s_dbase;
   __shared__ unsigned long long s_plo[16], s_phi[16];
   const uint32_t SoP = So * P;
   unsigned long long* acc = smem;                    // [So * P] x (lo, hi)
@@ -163,7 +166,12 @@ __global__ __launch_bounds__(1024) void k_owner_finish(OwnerRegions orr, uint32_
   uint32_t SoP2 = 1;
   while (SoP2 < SoP) SoP2 <<= 1;
   uint32_t* tag = (uint32_t*)(skey + SoP2);          // [So]
+  uint8_t* s_wid = (uint8_t*)(tag + So);             // [kRegionMap] region (workgroup) of each record
   const uint32_t o = blockIdx.x, tid = threadIdx.x;
+  // region sizes and spill-region sizes, loaded together (nwg, sp.nwg <= 256)
+  // while the table is cleared
+  const uint32_t rc = tid < nwg ? orr.count[(size_t)tid * ATREX_OWNERS + o] : 0u;
+  const uint32_t sc = tid < sp.nwg ? sp.count[tid] : 0u;
   for (uint32_t i = tid; i < 2 * SoP; i += 1024) {
     acc[i] = 0;
     if (RAW) racc[i] = 0;
@@ -171,23 +179,12 @@ __global__ __launch_bounds__(1024) void k_owner_finish(OwnerRegions orr, uint32_
   for (uint32_t i = tid; i < So; i += 1024) tag[i] = EMPTY_TAG;
   if (tid < 16) { s_plo[tid] = 0; s_phi[tid] = 0; }
   if (tid == 0) s_cnt = 0;
-  wave_prefix256(nwg, [&](uint32_t w) { return orr.count[(size_t)w * ATREX_OWNERS + o]; }, s_pre);
-  if (tid >= 64 && tid < 128) {  // second wave: prefix over the spill regions
-    uint32_t run = 0;
-    const uint32_t l = tid - 64;
-    for (uint32_t w0 = 0; w0 < sp.nwg; w0 += 64) {
-      const uint32_t w = w0 + l;
-      const uint32_t c = w < sp.nwg ? sp.count[w] : 0;
-      uint32_t inc = c;
-      for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t y = __shfl_up(inc, d, 64);
-        if (l >= (uint32_t)d) inc += y;
-      }
-      if (w < sp.nwg) s_spre[w] = run + inc - c;
-      run += __shfl(inc, 63, 64);
-    }
-    if (l == 0) s_spre[sp.nwg] = run;
-  }
+  prefix256(nwg, rc, s_pre, s_w4);
+  prefix256(sp.nwg, sc, s_spre, s_w4);
+  const uint32_t total = s_pre[nwg];
+  const bool mapped = total <= kRegionMap;  // record -> region by table, else by binary search
+  if (mapped && tid < nwg)
+    for (uint32_t r = s_pre[tid]; r < s_pre[tid + 1]; ++r) s_wid[r] = (uint8_t)tid;
   __syncthreads();
   auto slot_of = [&](uint32_t key) -> int32_t {
     if (key == EMPTY_TAG) return -1;  // the free-slot marker is never a tag
@@ -201,33 +198,39 @@ __global__ __launch_bounds__(1024) void k_owner_finish(OwnerRegions orr, uint32_
     }
     return -1;
   };
-  // the owner's regions
-  const uint32_t total = s_pre[nwg];
-  for (uint32_t base = 0; base < total; base += 1024) {  // uniform trip count (row_append)
-    const uint32_t idx = base + tid;
-    const bool valid = idx < total;
-    uint32_t key = 0;
-    size_t rec = 0;
-    int32_t sl = -1;
-    if (valid) {
-      const uint32_t w = upper_index(s_pre, nwg, idx);
-      rec = ((size_t)w * ATREX_OWNERS + o) * orr.capo + (idx - s_pre[w]);
-      key = orr.key[rec];
-      sl = slot_of(key);
+  // the owner's regions, one (record, phase) item per thread and round: the
+  // loads of a round's K items are issued before any is used
+  constexpr int K = RAW ? 8 : 16;
+  const uint32_t items = total * P;
+  for (uint32_t base = 0; base < items; base += K * 1024) {  // uniform trip count (row_append)
+    uint32_t key[K];
+    uint64_t lo[K], hi[K], rl[K], rh[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const uint32_t it = base + (uint32_t)k * 1024 + tid;
+      key[k] = EMPTY_TAG;
+      lo[k] = hi[k] = rl[k] = rh[k] = 0;
+      if (it < items) {
+        const uint32_t idx = it / P, ph = it - idx * P;
+        const uint32_t w = mapped ? s_wid[idx] : upper_index(s_pre, nwg, idx);
+        const size_t rec = ((size_t)w * ATREX_OWNERS + o) * orr.capo + (idx - s_pre[w]);
+        key[k] = orr.key[rec];
+        lo[k] = orr.acc[(rec * P + ph) * 2];
+        hi[k] = orr.acc[(rec * P + ph) * 2 + 1];
+        if (RAW) { rl[k] = orr.raw[(rec * P + ph) * 2]; rh[k] = orr.raw[(rec * P + ph) * 2 + 1]; }
+      }
     }
-    for (uint32_t ph = 0; ph < P; ++ph) {
-      uint64_t lo = 0, hi = 0, rl = 0, rh = 0;
-      if (valid) {
-        lo = orr.acc[(rec * P + ph) * 2];
-        hi = orr.acc[(rec * P + ph) * 2 + 1];
-        if (RAW) { rl = orr.raw[(rec * P + ph) * 2]; rh = orr.raw[(rec * P + ph) * 2 + 1]; }
-      }
-      const bool present = valid && (hi >> ATREX_COUNT_SHIFT) != 0;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const uint32_t it = base + (uint32_t)k * 1024 + tid;
+      const uint32_t ph = it % P;
+      const bool present = it < items && (hi[k] >> ATREX_COUNT_SHIFT) != 0;
+      const int32_t sl = present ? slot_of(key[k]) : -1;
       if (present && sl >= 0) {
-        lds_add2(&acc[2 * (sl * P + ph)], &acc[2 * (sl * P + ph) + 1], lo, hi);
-        if (RAW) lds_add2(&racc[2 * (sl * P + ph)], &racc[2 * (sl * P + ph) + 1], rl, rh);
+        lds_add2(&acc[2 * (sl * P + ph)], &acc[2 * (sl * P + ph) + 1], lo[k], hi[k]);
+        if (RAW) lds_add2(&racc[2 * (sl * P + ph)], &racc[2 * (sl * P + ph) + 1], rl[k], rh[k]);
       }
-      row_append(rows, present && sl < 0, ((uint64_t)key << 3) | ph, lo, hi, rl, rh, err);
+      row_append(rows, present && sl < 0, ((uint64_t)key[k] << 3) | ph, lo[k], hi[k], rl[k], rh[k], err);
     }
   }
   // the spill records of this owner, when they are few
@@ -271,28 +274,45 @@ __global__ __launch_bounds__(1024) void k_owner_finish(OwnerRegions orr, uint32_
   }
   __syncthreads();
   const uint32_t cnt = s_cnt;
-  uint32_t N = 1;
-  while (N < cnt) N <<= 1;
-  for (uint32_t i = cnt + tid; i < N; i += 1024) skey[i] = ~0ull;
-  __syncthreads();
-  for (uint32_t k = 2; k <= N; k <<= 1)  // ascending bitonic sort, N <= So * P
-    for (uint32_t j = k >> 1; j > 0; j >>= 1) {
-      for (uint32_t i = tid; i < N; i += 1024) {
-        const uint32_t q = i ^ j;
-        if (q > i) {
-          const uint64_t x = skey[i], y = skey[q];
-          if ((x > y) == ((i & k) == 0)) { skey[i] = y; skey[q] = x; }
+  if (cnt <= 64) {  // ascending bitonic sort in one wave's registers
+    if (tid < 64) {
+      uint64_t v = tid < cnt ? skey[tid] : ~0ull;
+      for (uint32_t k = 2; k <= 64; k <<= 1)
+        for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+          const uint64_t w = __shfl_xor((unsigned long long)v, (int)j, 64);
+          const bool up = (tid & k) == 0, lower = (tid & j) == 0;
+          v = (lower == up) ? (v < w ? v : w) : (v < w ? w : v);
         }
-      }
-      __syncthreads();
+      if (tid < cnt) skey[tid] = v;
     }
-  // the list, and the per-phase partial sums of W
-  const size_t base = (size_t)o * ol.cap;
+    __syncthreads();
+  } else {
+    uint32_t N = 1;
+    while (N < cnt) N <<= 1;
+    for (uint32_t i = cnt + tid; i < N; i += 1024) skey[i] = ~0ull;
+    __syncthreads();
+    for (uint32_t k = 2; k <= N; k <<= 1)  // ascending bitonic sort in LDS, N <= So * P
+      for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+        for (uint32_t i = tid; i < N; i += 1024) {
+          const uint32_t q = i ^ j;
+          if (q > i) {
+            const uint64_t x = skey[i], y = skey[q];
+            if ((x > y) == ((i & k) == 0)) { skey[i] = y; skey[q] = x; }
+          }
+        }
+        __syncthreads();
+      }
+  }
+  // the list, its keys in the dense key array, and the per-phase partial sums of W
+  if (tid == 0) s_dbase = cnt ? (uint32_t)atomicAdd(ol.dcount, (unsigned long long)cnt) : 0u;
+  __syncthreads();
+  const size_t base = (size_t)o * ol.cap, dbase = s_dbase;
   for (uint32_t i = tid; i < cnt; i += 1024) {
     const uint64_t sk = skey[i];
     const uint32_t e = (uint32_t)(sk & 0xFFFFF);
     const uint64_t lo = acc[2 * e], hi = acc[2 * e + 1];
     ol.rk[base + i] = sk >> 20;
+    ol.dkey[dbase + i] = (uint32_t)(sk >> 23);
     ol.lo[base + i] = lo;
     ol.hi[base + i] = hi;
     if (RAW) { ol.rlo[base + i] = racc[2 * e]; ol.rhi[base + i] = racc[2 * e + 1]; }
@@ -309,67 +329,122 @@ __global__ __launch_bounds__(1024) void k_owner_finish(OwnerRegions orr, uint32_
   if (tid == 0) ol.count[o] = cnt;
 }
 
-// Global order of the owner lists' rows: a row's position is the number of
-// rows below its sort key in every list (keys are distinct across lists), so
-// each owner's workgroup binary-searches its rows in all lists staged in LDS.
-// Done only when no row went to the row list, the spill records were merged
-// and there are at most kRankMax rows; workgroup 0 also writes S[ph].
+// Global order of the owner lists' rows.  A key's rows all sit in one list,
+// adjacent and ordered by phase, so a row's position is the number of rows
+// with a smaller key (over all lists) plus its place among its key's rows.
+// Each owner's workgroup stages every row key (the dense key array the owner
+// merge appends to) in LDS and counts, for each of its distinct keys, the
+// smaller ones: wave ballots, no search.  Done only when no row went to the
+// row list, the spill records were merged and the rows fit in LDS (kRankMax,
+// fewer when the owner lists are long); workgroup 0 also writes S[ph].
 __global__ __launch_bounds__(1024) void k_rank_groups(OwnerLists ol, uint32_t P, SpillIn sp, Rows rows,
                                                       const uint32_t* __restrict__ err, SortedGroups out,
                                                       uint64_t* __restrict__ S_out, unsigned long long* __restrict__ G_out,
-                                                      uint32_t* __restrict__ done) {
+                                                      uint32_t* __restrict__ done, uint32_t rmax) {
   extern __shared__ unsigned long long smem[];
-  __shared__ uint32_t s_off[ATREX_OWNERS + 1], s_stot;
-  uint64_t* s_rk = (uint64_t*)smem;               // [kRankMax]
-  uint32_t* s_pos = (uint32_t*)(s_rk + kRankMax); // [ol.cap]
-  const uint32_t o = blockIdx.x, tid = threadIdx.x;
-  wave_prefix256(ATREX_OWNERS, [&](uint32_t w) { return ol.count[w]; }, s_off);
-  if (tid >= 64 && tid < 128) {
-    uint32_t run = 0;
-    const uint32_t l = tid - 64;
-    for (uint32_t w0 = 0; w0 < sp.nwg; w0 += 64) {
-      const uint32_t w = w0 + l;
-      uint32_t inc = w < sp.nwg ? sp.count[w] : 0;
-      for (int d = 1; d < 64; d <<= 1) inc += __shfl_xor(inc, d, 64);
-      run += inc;
-    }
-    if (l == 0) s_stot = run;
+  __shared__ uint32_t s_w4[4], s_nh, s_stot, s_wc[16 * 16];
+  __shared__ unsigned long long s_plo[8], s_phi[8];
+  uint32_t* s_key = (uint32_t*)smem;              // [rmax <= kRankMax] every row key
+  uint32_t* s_own = s_key + rmax;                 // [ol.cap] this owner's row keys
+  uint32_t* s_pos = s_own + ol.cap;               // [ol.cap] positions of this owner's key heads (by row)
+  uint32_t* s_head = s_pos + ol.cap;              // [ol.cap] this owner's key heads (rows)
+  uint32_t* s_hkey = s_head + ol.cap;             // [ol.cap] their keys
+  const uint32_t o = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+  // sizes and status words, loaded together
+  const uint32_t co = ol.count[o];
+  const uint32_t R = (uint32_t)*ol.dcount;
+  const uint32_t sc = tid < sp.nwg ? sp.count[tid] : 0u;
+  const unsigned long long nrows = *rows.count;
+  const uint32_t e0 = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (tid < 8) { s_plo[tid] = 0; s_phi[tid] = 0; }
+  if (tid == 0) { s_nh = 0; s_stot = 0; }
+  __syncthreads();
+  {
+    uint32_t t = sc;
+    for (int d = 32; d >= 1; d >>= 1) t += __shfl_xor(t, d, 64);
+    if (lane == 0 && t) atomicAdd(&s_stot, t);
   }
   __syncthreads();
-  const uint32_t R = s_off[ATREX_OWNERS];
-  const bool ok = *rows.count == 0 && s_stot <= sp.inline_max && R <= kRankMax &&
-                  (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
-                   (ATREX_ERRBIT_RANGE | ATREX_ERRBIT_CAPACITY | ATREX_ERRBIT_SPILL)) == 0;
-  if (o == 0 && tid == 0) G_out[2] = s_stot;  // spill records, for the host's fallback
+  const uint32_t stot = s_stot;
+  const bool ok = nrows == 0 && stot <= sp.inline_max && R <= rmax &&
+                  (e0 & (ATREX_ERRBIT_RANGE | ATREX_ERRBIT_CAPACITY | ATREX_ERRBIT_SPILL)) == 0;
+  if (o == 0 && tid == 0) G_out[2] = stot;  // spill records, for the host's fallback
   if (!ok) {
     if (o == 0 && tid == 0) *done = 0;
     return;
   }
-  for (uint32_t l = tid >> 6; l < ATREX_OWNERS; l += 16) {  // one wave per list
-    const uint32_t c = s_off[l + 1] - s_off[l];
-    for (uint32_t i = tid & 63; i < c; i += 64) s_rk[s_off[l] + i] = ol.rk[(size_t)l * ol.cap + i];
+  // every row key and this owner's row keys into LDS: loads first
+  constexpr int K = kRankMax / 1024;
+  uint32_t v[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const uint32_t idx = (uint32_t)k * 1024 + tid;
+    v[k] = idx < R ? ol.dkey[idx] : 0u;
   }
-  const uint32_t co = s_off[o + 1] - s_off[o];
-  for (uint32_t i = tid; i < co; i += 1024) s_pos[i] = 0;
-  __syncthreads();
-  // pairs (row i of this owner, list l): a wave covers 64 lists of one row
-  for (uint32_t p = tid; p < co * ATREX_OWNERS; p += 1024) {
-    const uint32_t i = p / ATREX_OWNERS, l = p % ATREX_OWNERS;
-    const uint64_t x = s_rk[s_off[o] + i];
-    uint32_t lo = s_off[l], hi = s_off[l + 1];  // lower bound of x in [lo, hi)
-    while (lo < hi) {
-      const uint32_t mid = (lo + hi) / 2;
-      if (s_rk[mid] < x) lo = mid + 1; else hi = mid;
-    }
-    uint32_t below = lo - s_off[l];
-    for (int d = 32; d >= 1; d >>= 1) below += __shfl_xor(below, d, 64);
-    if ((tid & 63) == 0) atomicAdd(&s_pos[i], below);
-  }
-  __syncthreads();
   const size_t base = (size_t)o * ol.cap;
+  for (uint32_t i = tid; i < co; i += 1024) s_own[i] = (uint32_t)(ol.rk[base + i] >> 3);
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const uint32_t idx = (uint32_t)k * 1024 + tid;
+    if (idx < R) s_key[idx] = v[k];
+  }
+  // workgroup 0: S[ph] from the owners' partial sums, one (owner, phase) per thread
+  if (o == 0) {
+    for (uint32_t q = tid; q < ATREX_OWNERS * P; q += 1024) {
+      const uint64_t lo = ol.part[2 * (size_t)q], hi = ol.part[2 * (size_t)q + 1];
+      const uint32_t ph = q % P;
+      const unsigned long long old = atomicAdd(&s_plo[ph], (unsigned long long)lo);
+      atomicAdd(&s_phi[ph], (unsigned long long)hi + ((old + lo < old) ? 1ull : 0ull));
+    }
+  }
+  __syncthreads();
+  // this owner's distinct keys (first row of each key) and each row's head
   for (uint32_t i = tid; i < co; i += 1024) {
-    const uint32_t g = s_pos[i];
-    const uint64_t rk = s_rk[s_off[o] + i];
+    const uint32_t k = s_own[i];
+    if (i == 0 || s_own[i - 1] != k) {
+      const uint32_t h = atomicAdd(&s_nh, 1u);
+      s_hkey[h] = k;
+      s_head[h] = i;
+    }
+  }
+  // this wave's share of the staged keys, in registers
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  uint32_t y[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const uint32_t idx = (uint32_t)k * 1024 + wave * 64 + lane;
+    y[k] = idx < R ? s_key[idx] : 0xFFFFFFFFu;
+  }
+  __syncthreads();
+  // rows with a smaller key, HB heads at a time: each wave counts its keys
+  // below each head's key with ballots; the 16 waves' counts are summed
+  constexpr int HB = 16;
+  const uint32_t nh = s_nh;
+  for (uint32_t h0 = 0; h0 < nh; h0 += HB) {
+    uint32_t xk[HB];
+#pragma unroll
+    for (int j = 0; j < HB; ++j) xk[j] = s_hkey[min(h0 + (uint32_t)j, nh - 1)];
+#pragma unroll
+    for (int j = 0; j < HB; ++j) {
+      uint32_t c = 0;
+#pragma unroll
+      for (int k = 0; k < K; ++k) c += (uint32_t)__popcll(__ballot(y[k] < xk[j]));
+      if (lane == 0) s_wc[wave * HB + j] = c;
+    }
+    __syncthreads();
+    if (tid < HB && h0 + tid < nh) {
+      uint32_t c = 0;
+      for (uint32_t w = 0; w < 16; ++w) c += s_wc[w * HB + tid];
+      s_pos[s_head[h0 + tid]] = c;
+    }
+    __syncthreads();
+  }
+  // a row's position: its key's count plus its place among its key's rows
+  for (uint32_t i = tid; i < co; i += 1024) {
+    uint32_t hb = i;  // the key's first row: at most P - 1 rows back
+    while (hb > 0 && s_own[hb - 1] == s_own[i]) --hb;
+    const uint32_t g = s_pos[hb] + (i - hb);
+    const uint64_t rk = ol.rk[base + i];
     const uint64_t hi = ol.hi[base + i];
     out.key[g] = (uint32_t)(rk >> 3);
     out.phase[g] = (uint8_t)(rk & 7);
@@ -382,11 +457,8 @@ __global__ __launch_bounds__(1024) void k_rank_groups(OwnerLists ol, uint32_t P,
     }
   }
   if (o == 0 && tid < P) {
-    u128 t = 0;
-    for (uint32_t l = 0; l < ATREX_OWNERS; ++l)
-      t += make_u128(ol.part[((size_t)l * P + tid) * 2], ol.part[((size_t)l * P + tid) * 2 + 1]);
-    S_out[2 * tid] = (uint64_t)t;
-    S_out[2 * tid + 1] = (uint64_t)(t >> 64);
+    S_out[2 * tid] = s_plo[tid];
+    S_out[2 * tid + 1] = s_phi[tid];
   }
   if (o == 0 && tid == 0) {
     *G_out = R;
@@ -1005,7 +1077,7 @@ static uint32_t pow2_ge(uint32_t x) {
 }
 
 uint32_t owner_list_slots(uint32_t P, bool raw) {
-  const size_t budget = 160 * 1024 - 4096;
+  const size_t budget = 160 * 1024 - 4096 - kRegionMap;
   uint32_t So = 1024;
   while (So > 64 && (size_t)So * (4 + 16 * P * (raw ? 2 : 1)) + (size_t)pow2_ge(So * P) * 8 > budget) So >>= 1;
   return So;
@@ -1013,7 +1085,7 @@ uint32_t owner_list_slots(uint32_t P, bool raw) {
 
 
 static size_t owner_finish_smem(uint32_t P, bool raw, uint32_t So) {
-  return (size_t)So * P * 16 * (raw ? 2 : 1) + (size_t)pow2_ge(So * P) * 8 + (size_t)So * 4;
+  return (size_t)So * P * 16 * (raw ? 2 : 1) + (size_t)pow2_ge(So * P) * 8 + (size_t)So * 4 + kRegionMap;
 }
 
 void launch_owner_finish(hipStream_t s, const OwnerRegions& orr, uint32_t nwg, uint32_t P, bool raw, uint32_t So,
@@ -1030,9 +1102,12 @@ void launch_owner_finish(hipStream_t s, const OwnerRegions& orr, uint32_t nwg, u
 void launch_rank_groups(hipStream_t s, const OwnerLists& ol, uint32_t P, const SpillIn& sp, const Rows& rows,
                         const uint32_t* err, const SortedGroups& out, uint64_t* S_out, unsigned long long* G_out,
                         uint32_t* done) {
-  const size_t smem = (size_t)kRankMax * 8 + (size_t)ol.cap * 4;
+  // rows staged: kRankMax, or fewer when the owner lists are long
+  const size_t budget = 160 * 1024 - 4096 - (size_t)ol.cap * 16;
+  const uint32_t rmax = (uint32_t)std::min<size_t>(kRankMax, budget / 4) & ~7u;
+  const size_t smem = (size_t)rmax * 4 + (size_t)ol.cap * 16;
   hipLaunchKernelGGL(k_rank_groups, dim3(ATREX_OWNERS), dim3(1024), smem, s, ol, P, sp, rows, err, out, S_out, G_out,
-                     done);
+                     done, rmax);
 }
 
 void launch_lists_to_rows(hipStream_t s, const OwnerLists& ol, const Rows& rows, uint32_t* err) {
@@ -1041,15 +1116,15 @@ void launch_lists_to_rows(hipStream_t s, const OwnerLists& ol, const Rows& rows,
 
 // Dynamic LDS limits: 160 KB less a margin that covers each kernel's static LDS.
 hipError_t set_rows_smem_limits() {
-  const void* fns[] = {(const void*)k_rank_groups,
-                       (const void*)k_part_aggregate<true>, (const void*)k_part_aggregate<false>,
+  const void* fns[] = {(const void*)k_part_aggregate<true>, (const void*)k_part_aggregate<false>,
                        (const void*)k_part_hist, (const void*)k_part_scatter<true, 4>, (const void*)k_part_scatter<false, 4>,
                        (const void*)k_part_scatter<false, 8>};
   for (const void* f : fns) {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 2048);
     if (e != hipSuccess) return e;
   }
-  const void* fo[] = {(const void*)k_owner_finish<true>, (const void*)k_owner_finish<false>};
+  const void* fo[] = {(const void*)k_owner_finish<true>, (const void*)k_owner_finish<false>,
+                      (const void*)k_rank_groups};
   for (const void* f : fo) {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 4096);
     if (e != hipSuccess) return e;

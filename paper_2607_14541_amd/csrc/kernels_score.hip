@@ -22,6 +22,7 @@ namespace {
 constexpr uint32_t NT = 1024;
 constexpr uint32_t NW = NT / 64;
 constexpr uint32_t MINE = NT / 64;  // units ranked per workgroup: one wave each
+constexpr uint64_t kScoreOpsLds = 8192;  // operator table ids staged in LDS up to this size
 
 __device__ __forceinline__ uint64_t s_order_bits(double v) {
   return isnan(v) ? ~0ull : (uint64_t)__double_as_longlong(v);  // S > 0: bits order as values
@@ -110,6 +111,8 @@ __global__ __launch_bounds__(NT) void k_score_final(const uint32_t* __restrict__
   extern __shared__ uint64_t smem64[];
   double* s_S = (double*)smem64;             // [n]
   uint32_t* s_op = (uint32_t*)(s_S + n);     // [n]
+  uint32_t* s_opid = s_op + n;               // [nops_trace] when it fits (kScoreOpsLds)
+  const bool opid_lds = nops_trace <= kScoreOpsLds;
   __shared__ uint32_t s_w[NW];
   __shared__ uint32_t s_carry;
   __shared__ uint64_t s_u[2 * NW];
@@ -119,6 +122,8 @@ __global__ __launch_bounds__(NT) void k_score_final(const uint32_t* __restrict__
     s_S[j] = sorted_S[j];
     s_op[j] = sorted_op[j];
   }
+  if (opid_lds)
+    for (uint32_t j = tid; j < (uint32_t)nops_trace; j += NT) s_opid[j] = opt.id[j];
   if (tid == 0) s_carry = 0;
   __syncthreads();
   // operator runs: medians (Eq. (5)) and U of the retained operators
@@ -148,13 +153,13 @@ __global__ __launch_bounds__(NT) void k_score_final(const uint32_t* __restrict__
         const uint32_t h = c / 2;
         Si = (c & 1) ? s_S[i + h] : (s_S[i + h - 1] + s_S[i + h]) / 2.0;
       }
-      uint64_t a = 0, b = nops_trace;
+      uint64_t a = 0, b = nops_trace;  // the operator's row of the Eq. (3) table
       while (a < b) {
         const uint64_t mid = (a + b) / 2;
-        if (opt.id[mid] < op) a = mid + 1; else b = mid;
+        if ((opid_lds ? s_opid[mid] : opt.id[mid]) < op) a = mid + 1; else b = mid;
       }
       u128 U = 0;
-      if (a < nops_trace && opt.id[a] == op) U = make_u128(opt.U[2 * a], opt.U[2 * a + 1]);
+      if (a < nops_trace && (opid_lds ? s_opid[a] : opt.id[a]) == op) U = make_u128(opt.U[2 * a], opt.U[2 * a + 1]);
       myU += U;
       op_out[ob] = op;
       s_out[ob] = Si;
@@ -211,7 +216,9 @@ void launch_score_small(hipStream_t s, const uint32_t* score_key, const double* 
   const uint32_t nn = (uint32_t)n;
   hipLaunchKernelGGL(k_score_rank, dim3((nn + MINE - 1) / MINE), dim3(NT), (size_t)nn * 12, s, score_key, S, nn,
                      sorted_op, sorted_S, err);
-  hipLaunchKernelGGL(k_score_final, dim3(1), dim3(NT), (size_t)nn * 12, s, sorted_op, sorted_S, nn, opt, nops_trace,
+  const size_t opid_bytes = nops_trace <= kScoreOpsLds ? (size_t)nops_trace * 4 : 0;
+  hipLaunchKernelGGL(k_score_final, dim3(1), dim3(NT), (size_t)nn * 12 + opid_bytes, s, sorted_op, sorted_S, nn, opt,
+                     nops_trace,
                      op_out, w_out, s_out, s_agg, totU, nret, rU);
 }
 
@@ -220,5 +227,5 @@ hipError_t set_score_smem_limits() {
                                      (int)(kScoreRankMax * 12));
   if (e != hipSuccess) return e;
   return hipFuncSetAttribute((const void*)k_score_final, hipFuncAttributeMaxDynamicSharedMemorySize,
-                             (int)(kScoreRankMax * 12));
+                             (int)(kScoreRankMax * 12 + kScoreOpsLds * 4));
 }

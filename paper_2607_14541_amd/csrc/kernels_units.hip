@@ -1,5 +1,6 @@
 // kernels_units.hip -- per-phase weights and Eq. (3) per operator and per key
-// (§3.4) over the ordered groups, in three launches for any number of groups:
+// (§3.4) over the ordered groups: one workgroup (k_units_small) for up to
+// kUnitsSmallMax groups, else three launches for any number of groups:
 //
 //  1. k_units_tiles (one 1024-group tile per workgroup): copies the groups to
 //     the caller's arrays with RN(W) / RN(S[ph]); for each key (its groups are
@@ -258,12 +259,210 @@ __global__ __launch_bounds__(TILE) void k_units_keys(SortedGroups g, uint64_t G,
   }
 }
 
+// ---------------------------------------------------------------------------
+// One workgroup for up to kUnitsSmallMax groups: thread t holds groups
+// [8t, 8t + 8) in registers; the key runs and operator runs are summed with
+// one block-wide segmented scan (operator: a run head restarts the sum), and
+// every run's total is taken at its last group.  Same outputs as the three
+// launches above.
+constexpr uint32_t SM_PER = 8;
+
+struct Seg {
+  uint32_t f;  // a run head inside
+  u128 v;      // sum of W since the last head
+  uint32_t m;  // phase mask since the last head
+};
+
+__device__ __forceinline__ Seg seg_cat(const Seg& a, const Seg& b) {  // a, then b
+  return b.f ? b : Seg{a.f, a.v + b.v, a.m | b.m};
+}
+
+__device__ __forceinline__ Seg seg_shfl_up(const Seg& x, int d) {
+  Seg y;
+  y.f = __shfl_up(x.f, d, 64);
+  y.v = shfl_up_u128(x.v, d);
+  y.m = __shfl_up(x.m, d, 64);
+  return y;
+}
+
+__global__ __launch_bounds__(TILE) void k_units_small(SortedGroups g, uint32_t G, uint32_t P, uint64_t L,
+                                                      const uint64_t* __restrict__ S, GroupsOut out, UnitTable ops,
+                                                      uint64_t maxOps, UnitTable keys,
+                                                      unsigned long long* __restrict__ counts,
+                                                      uint32_t* __restrict__ err) {
+  __shared__ Seg s_kw[NW], s_ow[NW];
+  __shared__ uint32_t s_nk[NW], s_no[NW];
+  __shared__ uint64_t s_lo[NW], s_hi[NW];
+  __shared__ uint64_t s_S[16];
+  const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint32_t i0 = tid * SM_PER;
+  if (tid < 2 * P) s_S[tid] = S[tid];
+  // this thread's groups, the key before them and the key after them
+  uint32_t key[SM_PER], ph[SM_PER];
+  u128 W[SM_PER];
+#pragma unroll
+  for (int j = 0; j < SM_PER; ++j) {
+    const uint32_t i = i0 + j;
+    key[j] = i < G ? g.key[i] : 0u;
+    ph[j] = i < G ? g.phase[i] : 0u;
+    W[j] = i < G ? load_u128(g.wsum, i) : (u128)0;
+  }
+  const uint32_t kprev = (i0 > 0 && i0 <= G) ? g.key[i0 - 1] : 0u;
+  const bool has_next = i0 + SM_PER < G;
+  const uint32_t knext = has_next ? g.key[i0 + SM_PER] : 0u;
+  __syncthreads();
+  // the groups, with RN(W) / RN(S[ph])
+#pragma unroll
+  for (int j = 0; j < SM_PER; ++j) {
+    const uint32_t i = i0 + j;
+    if (i < G) {
+      out.key[i] = key[j];
+      out.phase[i] = (uint8_t)ph[j];
+      out.count[i] = g.count[i];
+      store_u128(out.wsum, i, W[j]);
+      if (out.raw) store_u128(out.raw, i, load_u128(g.raw, i));
+      out.weight[i] = ratio(W[j], make_u128(s_S[2 * ph[j]], s_S[2 * ph[j] + 1]));
+    }
+  }
+  if (tid < P) {
+    out.phase_total[2 * tid] = s_S[2 * tid];
+    out.phase_total[2 * tid + 1] = s_S[2 * tid + 1];
+  }
+  // heads of key runs and operator runs
+  uint32_t kh = 0, oh = 0;  // bit j: group j heads a run
+#pragma unroll
+  for (int j = 0; j < SM_PER; ++j) {
+    const uint32_t i = i0 + j;
+    const uint32_t prev = j == 0 ? kprev : key[j - 1];
+    if (i < G && (i == 0 || prev != key[j])) kh |= 1u << j;
+    if (i < G && (i == 0 || (prev >> 16) != (key[j] >> 16))) oh |= 1u << j;
+  }
+  // this thread's aggregates, then the block-wide exclusive scan
+  Seg ka{0, 0, 0}, oa{0, 0, 0};
+#pragma unroll
+  for (int j = 0; j < SM_PER; ++j) {
+    if (i0 + j < G) {
+      const Seg e{1u, W[j], 1u << ph[j]};
+      const Seg c{0u, W[j], 1u << ph[j]};
+      ka = seg_cat(ka, (kh >> j) & 1 ? e : c);
+      oa = seg_cat(oa, (oh >> j) & 1 ? e : c);
+    }
+  }
+  uint32_t nk = __popc(kh), no = __popc(oh);
+  Seg ki = ka, oi = oa;
+  uint32_t nki = nk, noi = no;
+  for (int d = 1; d < 64; d <<= 1) {
+    const Seg ky = seg_shfl_up(ki, d), oy = seg_shfl_up(oi, d);
+    const uint32_t nky = __shfl_up(nki, d, 64), noy = __shfl_up(noi, d, 64);
+    if (lane >= (uint32_t)d) {
+      ki = seg_cat(ky, ki);
+      oi = seg_cat(oy, oi);
+      nki += nky;
+      noi += noy;
+    }
+  }
+  if (lane == 63) {
+    s_kw[wave] = ki;
+    s_ow[wave] = oi;
+    s_nk[wave] = nki;
+    s_no[wave] = noi;
+  }
+  __syncthreads();
+  Seg kc{0, 0, 0}, oc{0, 0, 0};  // carry into this wave
+  uint32_t nkc = 0, noc = 0, nkeys = 0, nops = 0;
+  for (uint32_t w = 0; w < NW; ++w) {
+    if (w < wave) {
+      kc = seg_cat(kc, s_kw[w]);
+      oc = seg_cat(oc, s_ow[w]);
+      nkc += s_nk[w];
+      noc += s_no[w];
+    }
+    nkeys += s_nk[w];
+    nops += s_no[w];
+  }
+  {  // exclusive within the wave
+    const Seg ke = seg_shfl_up(ki, 1), oe = seg_shfl_up(oi, 1);
+    const uint32_t nke = __shfl_up(nki, 1, 64), noe = __shfl_up(noi, 1, 64);
+    if (lane > 0) {
+      kc = seg_cat(kc, ke);
+      oc = seg_cat(oc, oe);
+      nkc += nke;
+      noc += noe;
+    }
+  }
+  const bool ops_fit = nops <= maxOps;
+  // runs ending in this thread: totals, U = (L / |Phi|) * sum W (Eq. (3))
+  u128 sumUk = 0, sumU = 0;
+  {
+    Seg kr = kc, orr = oc;
+    uint32_t kidx = nkc, oidx = noc;  // heads so far
+#pragma unroll
+    for (int j = 0; j < SM_PER; ++j) {
+      const uint32_t i = i0 + j;
+      if (i < G) {
+        const Seg e{1u, W[j], 1u << ph[j]};
+        const Seg c{0u, W[j], 1u << ph[j]};
+        kr = seg_cat(kr, (kh >> j) & 1 ? e : c);
+        orr = seg_cat(orr, (oh >> j) & 1 ? e : c);
+        kidx += (kh >> j) & 1;
+        oidx += (oh >> j) & 1;
+        const bool last = i + 1 == G;
+        const uint32_t nx = j + 1 < SM_PER ? key[j + 1] : knext;
+        if (last || nx != key[j]) {
+          const u128 U = (u128)(L / __popc(kr.m)) * kr.v;
+          keys.id[kidx - 1] = key[j];
+          store_u128(keys.U, kidx - 1, U);
+          sumUk += U;
+        }
+        if (last || (nx >> 16) != (key[j] >> 16)) {
+          const u128 U = (u128)(L / __popc(orr.m)) * orr.v;
+          if (ops_fit) {
+            ops.id[oidx - 1] = key[j] >> 16;
+            store_u128(ops.U, oidx - 1, U);
+          }
+          sumU += U;
+        }
+      }
+    }
+  }
+  const u128 totU = tile_sum_u128(sumU, s_lo, s_hi);
+  const u128 totUk = tile_sum_u128(sumUk, s_lo, s_hi);
+  // w_i = RN(U_i) / RN(sum U), omega_k = RN(U_k) / RN(sum U_k): this thread's own runs
+  {
+    uint32_t kidx = nkc, oidx = noc;
+#pragma unroll
+    for (int j = 0; j < SM_PER; ++j) {
+      const uint32_t i = i0 + j;
+      if (i < G) {
+        kidx += (kh >> j) & 1;
+        oidx += (oh >> j) & 1;
+        const bool last = i + 1 == G;
+        const uint32_t nx = j + 1 < SM_PER ? key[j + 1] : knext;
+        if (last || nx != key[j]) keys.w[kidx - 1] = ratio(load_u128(keys.U, kidx - 1), totUk);
+        if (ops_fit && (last || (nx >> 16) != (key[j] >> 16)))
+          ops.w[oidx - 1] = ratio(load_u128(ops.U, oidx - 1), totU);
+      }
+    }
+  }
+  if (tid == 0) {
+    counts[0] = nops;
+    counts[1] = nkeys;
+    if (!ops_fit) atomicOr(err, ATREX_ERRBIT_CAPACITY);
+  }
+}
+
 }  // namespace
 
 void launch_units(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t L, const uint64_t* S,
                   const GroupsOut& out, const UnitScratch& us, const UnitTable& ops, uint64_t maxOps,
                   const UnitTable& keys, unsigned long long* counts, uint32_t* err) {
+  if (G <= kUnitsSmallMax) {
+    hipLaunchKernelGGL(k_units_small, dim3(1), dim3(TILE), 0, s, g, (uint32_t)G, P, L, S, out, ops, maxOps, keys,
+                       counts, err);
+    return;
+  }
   const uint32_t nt = (uint32_t)((G + TILE - 1) / TILE);
+  launch_fill_u64(s, (uint64_t*)counts, 2, 0);
   if (nt) hipLaunchKernelGGL(k_units_tiles, dim3(nt), dim3(TILE), 0, s, g, G, P, L, S, out, us);
   hipLaunchKernelGGL(k_units_ops, dim3(1), dim3(TILE), 0, s, nt, P, L, us, ops, maxOps, S, out.phase_total, counts,
                      err);

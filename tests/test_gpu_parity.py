@@ -108,3 +108,30 @@ def test_repeat_runs_are_bit_identical():
     b = H.run_gpu(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, 2)
     for k in ("key", "count", "wsum", "weight", "op_U", "omega"):
         assert np.array_equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("path", ENGINES)
+@pytest.mark.parametrize("G", [1023, 1024, 1025, 8191, 8192, 8193, 20000])
+def test_group_count_boundaries(path, G):
+    """Exactly G (key, phase) groups around the one-workgroup unit kernel's
+    limit and the 1024-group tiles; operators of 7 shapes, so that operator
+    runs and key runs cross thread and tile boundaries."""
+    rng = np.random.default_rng(G)
+    P = 2
+    nk = (G + 1) // 2
+    keys = np.array([((k // 7) << 16) | (k % 7) for k in range(nk)], np.uint32)
+    gk = np.repeat(keys, 2)[:G]
+    gp = np.tile(np.array([0, 1], np.uint8), nk)[:G]
+    reps = rng.integers(1, 4, G)
+    key = np.repeat(gk, reps)
+    ph = np.repeat(gp, reps)
+    order = rng.permutation(key.size)
+    key, ph = key[order], ph[order]
+    A = 5
+    app = rng.integers(0, A, key.size).astype(np.uint32)
+    dur = rng.integers(1, 10 ** 7, key.size).astype(np.int64)
+    c = rng.integers(1, 2 ** 20, A).astype(np.uint32)
+    H.say("groups", G, path)
+    g = H.run_gpu(key, app, ph, dur, c, P, path=path, max_groups=G, max_keys=nk)
+    assert g["num_groups"] == G
+    H.compare(g, O.run(key, app, ph, dur, c, P))
