@@ -31,9 +31,13 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_lds(EventsDev ev, uint32_t A, 
   const uint64_t n = ev.n, n4 = n / 4;
   const uint64_t stride = (uint64_t)gridDim.x * BLOCK;
   bool bad = false;
-  for (uint64_t q = (uint64_t)blockIdx.x * BLOCK + threadIdx.x; q < n4; q += stride) {
-    Ev4 e;
-    load4<false>(ev.key, ev.app, ev.phase, ev.dur, q * 4, e);
+  // the next group's loads are issued before the current group is added
+  uint64_t q = (uint64_t)blockIdx.x * BLOCK + threadIdx.x;
+  Ev4 nxt;
+  if (q < n4) load4<false>(ev.key, ev.app, ev.phase, ev.dur, q * 4, nxt);
+  for (; q < n4; q += stride) {
+    const Ev4 e = nxt;
+    if (q + stride < n4) load4<false>(ev.key, ev.app, ev.phase, ev.dur, (q + stride) * 4, nxt);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const bool ok = e.app[j] < A && e.ph[j] < P && e.dur[j] >= 0;
@@ -92,9 +96,12 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_lds32(EventsDev ev, uint32_t A
     const uint64_t up = (d >> 32) + ((old + lo < old) ? 1u : 0u);
     if (up) atomicAdd(&ext[g], (unsigned long long)up);
   };
-  for (uint64_t q = (uint64_t)blockIdx.x * BLOCK + threadIdx.x; q < n4; q += stride) {
-    Ev4 e;
-    load4<false>(ev.key, ev.app, ev.phase, ev.dur, q * 4, e);
+  uint64_t q = (uint64_t)blockIdx.x * BLOCK + threadIdx.x;
+  Ev4 nxt;
+  if (q < n4) load4<false>(ev.key, ev.app, ev.phase, ev.dur, q * 4, nxt);
+  for (; q < n4; q += stride) {
+    const Ev4 e = nxt;
+    if (q + stride < n4) load4<false>(ev.key, ev.app, ev.phase, ev.dur, (q + stride) * 4, nxt);
 #pragma unroll
     for (int j = 0; j < 4; ++j) one(e.app[j], e.ph[j], e.dur[j]);
   }
@@ -110,8 +117,10 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_lds32(EventsDev ev, uint32_t A
 // into R ranges of at most GR, the events into `slices`; each workgroup sums
 // one (slice, range) in 32-bit LDS counters (wraps and high halves into ext[g]
 // as in k_pass_a_lds32).  The R workgroups of a slice are placed on one XCD
-// (workgroups go round-robin over the 8 XCDs), so the slice is read from HBM
-// about once and from that XCD's L2 by the others.
+// (workgroups go round-robin over the 8 XCDs) and walk the slice in the same
+// order with ordinary (L2-allocating) loads, so the slice comes from HBM about
+// once and from that XCD's L2 for the others.  Each lane keeps three groups of
+// four events in flight (loads issued two iterations ahead).
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A, uint32_t P, uint32_t G,
                                                         uint32_t GR, uint32_t R, uint32_t slices,
@@ -140,14 +149,47 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A
     const uint64_t up = (d >> 32) + ((old + lo < old) ? 1u : 0u);
     if (up) atomicAdd(&ext[g], (unsigned long long)up);
   };
-  const uint64_t e4 = b + (e - b) / 4 * 4;
-  for (uint64_t q = b + 4 * (uint64_t)threadIdx.x; q < e4; q += 4 * (uint64_t)BLOCK) {
-    Ev4 x;
-    load4<false>(ev.key, ev.app, ev.phase, ev.dur, q, x);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) one(x.app[j], x.ph[j], x.dur[j]);
+  // groups of four events of the slice: iteration `it` covers groups
+  // it * BLOCK + [0, BLOCK); the trip count is uniform over the workgroup
+  const uint64_t ng = (e - b) / 4;
+  const uint64_t iters = (ng + BLOCK - 1) / BLOCK;
+  struct G4 {
+    v4u a;
+    uint32_t p;
+    v2l d0, d1;
+  };
+  auto load = [&](uint64_t it, G4& x) {
+    const uint64_t gi = it * BLOCK + threadIdx.x;
+    if (gi < ng) {
+      const uint64_t i = b + 4 * gi;
+      x.a = *(const v4u*)(ev.app + i);
+      x.p = *(const uint32_t*)(ev.phase + i);
+      x.d0 = *(const v2l*)(ev.dur + i);
+      x.d1 = *(const v2l*)(ev.dur + i + 2);
+    }
+  };
+  auto process = [&](uint64_t it, const G4& x) {
+    if (it * BLOCK + threadIdx.x >= ng) return;
+    one(x.a.x, x.p & 0xFFu, x.d0.x);
+    one(x.a.y, (x.p >> 8) & 0xFFu, x.d0.y);
+    one(x.a.z, (x.p >> 16) & 0xFFu, x.d1.x);
+    one(x.a.w, x.p >> 24, x.d1.y);
+  };
+  G4 x0, x1, x2;
+  if (0 < iters) load(0, x0);
+  if (1 < iters) load(1, x1);
+  if (2 < iters) load(2, x2);
+  for (uint64_t it = 0; it < iters; it += 3) {
+    process(it, x0);
+    if (it + 3 < iters) load(it + 3, x0);
+    if (it + 1 >= iters) break;
+    process(it + 1, x1);
+    if (it + 4 < iters) load(it + 4, x1);
+    if (it + 2 >= iters) break;
+    process(it + 2, x2);
+    if (it + 5 < iters) load(it + 5, x2);
   }
-  for (uint64_t i = e4 + threadIdx.x; i < e; i += BLOCK) one(ev.app[i], ev.phase[i], ev.dur[i]);
+  for (uint64_t i = b + 4 * ng + threadIdx.x; i < e; i += BLOCK) one(ev.app[i], ev.phase[i], ev.dur[i]);
   flag_error(err, bad, ATREX_ERRBIT_RANGE);
   __syncthreads();
   uint32_t* out = partial + (size_t)slice * G;
