@@ -243,11 +243,14 @@ struct atrex_ctx {
   const char* path_used;
   std::vector<Timed> timed;
   size_t ntimed;
-  // pinned host staging for device -> host readbacks of status words
+  // pinned, device-mapped host staging for device -> host readbacks of
+  // status words: written by one k_publish launch per synchronisation
   char* pinned = nullptr;
+  uint32_t* pinned_dev = nullptr;  // the same buffer as the device sees it
   size_t pinned_used = 0;
   struct Pending {
     void* dst;
+    const void* src;
     size_t off, bytes;
   };
   std::vector<Pending> pending;
@@ -383,20 +386,30 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 constexpr size_t kPinnedBytes = 4096;
 
-// Device -> host copy of a few status words through the context's pinned
-// buffer; the host values are filled in by sync_read().
+// Device -> host readback of a few status words (a multiple of 4 bytes)
+// through the context's mapped pinned buffer; sync_read() launches the copy
+// and fills in the host values after the stream synchronisation.
 void d2h(atrex_ctx* c, void* dst, const void* src, size_t bytes) {
   size_t off = (c->pinned_used + 7) / 8 * 8;
-  if (!c->pinned || off + bytes > kPinnedBytes) {  // no pinned buffer: plain (pageable) copy
-    (void)hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, c->s);
+  if (!c->pinned_dev || off + bytes > kPinnedBytes || bytes % 4 != 0 || c->pending.size() >= kPublishMax) {
+    (void)hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, c->s);  // plain (pageable) copy
     return;
   }
-  (void)hipMemcpyAsync(c->pinned + off, src, bytes, hipMemcpyDeviceToHost, c->s);
-  c->pending.push_back({dst, off, bytes});
+  c->pending.push_back({dst, src, off, bytes});
   c->pinned_used = off + bytes;
 }
 
 atrex_status sync_read(atrex_ctx* c) {
+  if (!c->pending.empty()) {
+    PublishList pl{};
+    for (const auto& p : c->pending) {
+      pl.src[pl.count] = (const uint32_t*)p.src;
+      pl.off32[pl.count] = (uint32_t)(p.off / 4);
+      pl.n32[pl.count] = (uint32_t)(p.bytes / 4);
+      ++pl.count;
+    }
+    launch_publish(c->s, pl, c->pinned_dev);
+  }
   const atrex_status st = sync_status(c);
   for (const auto& p : c->pending) memcpy(p.dst, c->pinned + p.off, p.bytes);
   c->pending.clear();
@@ -507,7 +520,11 @@ atrex_status atrex_aggregate_init(const atrex_init_params* ip, atrex_ctx** out) 
   c->G = c->nops = c->nkeys = 0;
   c->path_used = "none";
   c->ntimed = 0;
-  if (hipHostMalloc((void**)&c->pinned, kPinnedBytes, hipHostMallocDefault) != hipSuccess) c->pinned = nullptr;
+  if (hipHostMalloc((void**)&c->pinned, kPinnedBytes, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) {
+    c->pinned = nullptr;
+  } else if (hipHostGetDevicePointer((void**)&c->pinned_dev, c->pinned, 0) != hipSuccess) {
+    c->pinned_dev = nullptr;  // readbacks fall back to plain copies
+  }
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&c->cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
@@ -562,8 +579,9 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
   // clear the control words and the pass-A carry table
   launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 64, 0);
   launch_fill_u64(s, c->at<uint64_t>(L.carryA), GA, 0);
-  // pass A, Eq. (2)
+  // pass A, Eq. (2), and the Eq. (3) scale words of every (app, phase)
   uint64_t* T = c->at<uint64_t>(L.T);
+  uint64_t* scale = c->at<uint64_t>(L.scale);
   if (L.passA == 0 && vec_ok) {
     const uint64_t per_cu = std::max<uint64_t>(1, std::min<uint64_t>(2, (kLdsBytes - 1024) / (GA * 8)));
     uint64_t nb = std::min<uint64_t>((uint64_t)c->cus * per_cu, kPartialRowsMax);
@@ -573,7 +591,8 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
                             c->at<unsigned long long>(L.carryA), c->err()));
     TIMED(c, "pass_a_reduce", GA,
           launch_pass_a_reduce(s, c->at<unsigned long long>(L.partA), (uint32_t)nb, (uint32_t)GA,
-                               c->at<unsigned long long>(L.carryA), T));
+                               c->at<unsigned long long>(L.carryA), T, c->app_weight, c->Csum(), P, scale,
+                               c->at<void>(L.bscale)));
   } else if (L.passA == 3 && vec_ok) {
     const uint32_t R = (uint32_t)((GA + kPassARangeBins - 1) / kPassARangeBins);
     const uint32_t GR = (uint32_t)((GA + R - 1) / R);
@@ -582,7 +601,8 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
                               c->at<unsigned long long>(L.carryA), c->err()));
     TIMED(c, "pass_a_reduce", GA,
           launch_pass_a_reduce32(s, c->at<uint32_t>(L.partA), kPassASlices, (uint32_t)GA,
-                                 c->at<unsigned long long>(L.carryA), T));
+                                 c->at<unsigned long long>(L.carryA), T, c->app_weight, c->Csum(), P, scale,
+                                 c->at<void>(L.bscale)));
   } else if (L.passA == 1 && vec_ok) {
     const uint64_t nb = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)c->cus, kMaxWG));
     TIMED(c, "pass_a", n,
@@ -590,16 +610,16 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
                               c->err()));
     TIMED(c, "pass_a_reduce", GA,
           launch_pass_a_reduce32(s, c->at<uint32_t>(L.partA), (uint32_t)nb, (uint32_t)GA,
-                                 c->at<unsigned long long>(L.carryA), T));
+                                 c->at<unsigned long long>(L.carryA), T, c->app_weight, c->Csum(), P, scale,
+                                 c->at<void>(L.bscale)));
   } else {
     launch_fill_u64(s, T, GA * 2, 0);
     TIMED(c, "pass_a_global", n,
           launch_pass_a_global(s, d, A, P, (uint32_t)std::max<uint64_t>(1, (uint64_t)c->cus * 8), (unsigned long long*)T,
                                c->err()));
+    // scale, Eq. (3) (the column-sum kernels of the other modes compute it with T)
+    TIMED(c, "scale", GA, launch_scale(s, T, c->app_weight, c->Csum(), A, P, scale, c->at<void>(L.bscale)));
   }
-  // scale, Eq. (3)
-  uint64_t* scale = c->at<uint64_t>(L.scale);
-  TIMED(c, "scale", GA, launch_scale(s, T, c->app_weight, c->Csum(), A, P, scale, c->at<void>(L.bscale)));
   // pass B, Eq. (2)-(3): every engine emits rows (key << 3 | phase, Q96 sum)
   const Rows rows = c->rows();
   atrex_path path = c->path;

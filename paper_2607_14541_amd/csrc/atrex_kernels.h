@@ -96,11 +96,13 @@ hipError_t set_kernel_smem_limits();
 void launch_pass_a_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
                        unsigned long long* partial, unsigned long long* carry, uint32_t* err);
 void launch_pass_a_reduce(hipStream_t s, const unsigned long long* partial, uint32_t nb, uint32_t G,
-                          const unsigned long long* carry, uint64_t* T);
+                          const unsigned long long* carry, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
+                          uint32_t P, uint64_t* scale, void* bscale);
 void launch_pass_a_lds32(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
                          uint32_t* partial, unsigned long long* ext, uint32_t* err);
 void launch_pass_a_reduce32(hipStream_t s, const uint32_t* partial, uint32_t nb, uint32_t G,
-                            const unsigned long long* ext, uint64_t* T);
+                            const unsigned long long* ext, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
+                            uint32_t P, uint64_t* scale, void* bscale);
 void launch_pass_a_range(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t GR, uint32_t R,
                          uint32_t slices, uint32_t* partial, unsigned long long* ext, uint32_t* err);
 void launch_pass_a_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
@@ -154,6 +156,14 @@ void launch_rows_reduce(hipStream_t s, const Rows& rows, const uint64_t* rk_sort
 
 // kernels_util.hip
 void launch_fill_u64(hipStream_t s, uint64_t* p, uint64_t n, uint64_t v);
+// Up to kPublishMax device word ranges copied to a host-mapped buffer (32-bit words).
+constexpr uint32_t kPublishMax = 16;
+struct PublishList {
+  const uint32_t* src[kPublishMax];
+  uint32_t off32[kPublishMax], n32[kPublishMax];
+  uint32_t count;
+};
+void launch_publish(hipStream_t s, const PublishList& pl, uint32_t* dst);
 void launch_sum_u32(hipStream_t s, const uint32_t* x, uint64_t n, uint64_t* out);
 // LSD radix sort of (u64 key, u32 value) pairs on key bits [0, bits).  Stable.
 // tmp must hold radix_sort_tmp_bytes(n); results end in (k0, v0).

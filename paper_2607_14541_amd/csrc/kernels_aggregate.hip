@@ -196,31 +196,6 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A
   for (uint32_t g = threadIdx.x; g < g1 - g0; g += BLOCK) out[g0 + g] = s32[g];
 }
 
-// T[g] = sum over blocks of partial[b][g] + ext[g] * 2^ext_shift.
-// Block = 64 consecutive g x 16 strides over the partial rows.
-template <typename PT>
-__global__ __launch_bounds__(1024) void k_pass_a_reduce(const PT* __restrict__ partial, uint32_t nb, uint32_t G,
-                                                        const unsigned long long* __restrict__ ext, int ext_shift,
-                                                        uint64_t* __restrict__ T) {
-  __shared__ uint64_t s_lo[16][64], s_hi[16][64];
-  const uint32_t gl = threadIdx.x & 63, r = threadIdx.x >> 6;
-  const uint32_t g = blockIdx.x * 64 + gl;
-  u128 acc = 0;
-  if (g < G) {
-#pragma unroll 8
-    for (uint32_t b = r; b < nb; b += 16) acc += (uint64_t)partial[(size_t)b * G + g];
-  }
-  s_lo[r][gl] = (uint64_t)acc;
-  s_hi[r][gl] = (uint64_t)(acc >> 64);
-  __syncthreads();
-  if (r == 0 && g < G) {
-    u128 t = (u128)ext[g] << ext_shift;
-    for (int i = 0; i < 16; ++i) t += make_u128(s_lo[i][gl], s_hi[i][gl]);
-    T[2 * g] = (uint64_t)t;
-    T[2 * g + 1] = (uint64_t)(t >> 64);
-  }
-}
-
 // Pass A straight into global 128-bit accumulators (any number of (a, ph)).
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void k_pass_a_global(EventsDev ev, uint32_t A, uint32_t P,
@@ -244,53 +219,102 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_global(EventsDev ev, uint32_t 
 // ---------------------------------------------------------------------------
 // Scale, Eq. (3): for each (a, ph) with T > 0 and c_a > 0,
 //   r = 2^96 c_a / (C T), rho = floor(log2 r), m = floor(r 2^(55 - rho)).
-// With r0 = bitlen(2^96 c_a) - bitlen(C T), r lies in (2^(r0-1), 2^(r0+1)), so
-// q = floor(2^96 c_a 2^(56 - r0) / (C T)) lies in [2^55, 2^57): if q >= 2^56
-// then rho = r0 and m = floor(q / 2), else rho = r0 - 1 and m = q.  q is found
-// by 57 steps of shift-and-subtract long division on 4 x 64-bit limbs.
-struct W256 {
-  uint64_t w[4];
-};
+// With Y = C T, bc = bitlen(c_a), by = bitlen(Y) and r0 = 96 + bc - by, r lies
+// in (2^(r0-1), 2^(r0+1)), so q = floor(c_a 2^e / Y) with e = 56 - bc + by
+// lies in [2^55, 2^57): if q >= 2^56 then rho = r0 and m = floor(q / 2), else
+// rho = r0 - 1 and m = q.  q comes from an fp64 estimate (off by at most a few
+// tens), an exact 256-bit remainder R = c_a 2^e - q Y, a second fp64 step
+// q += rint(R / Y) that leaves |R| < Y, and a final -1 when R < 0.
 
-__device__ __forceinline__ int w256_bitlen(const W256& a) {
+// value of a signed 256-bit two's-complement number (4 little-endian limbs),
+// rounded to fp64 (exactness is not needed: it feeds an estimate)
+__device__ __forceinline__ double s256_to_f64(const uint64_t w[4]) {
+  const bool neg = (int64_t)w[3] < 0;
+  uint64_t a[4];
+  uint64_t br = neg ? 1 : 0;
 #pragma unroll
-  for (int i = 3; i >= 0; --i)
-    if (a.w[i]) return 64 * i + 64 - __clzll(a.w[i]);
-  return 0;
-}
-
-__device__ __forceinline__ W256 w256_shl(const W256& a, int s) {  // 0 <= s < 256
-  W256 r;
-  const int L = s >> 6, b = s & 63;
-#pragma unroll
-  for (int i = 3; i >= 0; --i) {
-    const int j = i - L;
-    uint64_t v = 0;
-    if (j >= 0) {
-      v = a.w[j] << b;
-      if (b && j >= 1) v |= a.w[j - 1] >> (64 - b);
-    }
-    r.w[i] = v;
+  for (int i = 0; i < 4; ++i) {  // |x| = ~x + 1 when negative
+    const uint64_t x = neg ? ~w[i] : w[i];
+    a[i] = x + br;
+    br = (br && a[i] == 0) ? 1 : 0;
   }
-  return r;
+  const double v = ldexp((double)a[3], 192) + ldexp((double)a[2], 128) + ldexp((double)a[1], 64) + (double)a[0];
+  return neg ? -v : v;
 }
 
-__device__ __forceinline__ bool w256_ge(const W256& a, const W256& b) {
-#pragma unroll
-  for (int i = 3; i >= 0; --i)
-    if (a.w[i] != b.w[i]) return a.w[i] > b.w[i];
-  return true;
-}
-
-__device__ __forceinline__ void w256_sub_inplace(W256& a, const W256& b) {
-  uint64_t br = 0;
+// w -= s * Y (s >= 0 or s < 0, |s| < 2^63), Y = (y0, y1, y2), 256-bit wrap-around
+__device__ __forceinline__ void s256_sub_mul(uint64_t w[4], int64_t s, uint64_t y0, uint64_t y1, uint64_t y2) {
+  const bool neg = s < 0;
+  const uint64_t q = neg ? (uint64_t)(-s) : (uint64_t)s;
+  const u128 p0 = (u128)q * y0;
+  const u128 p1 = (u128)q * y1 + (uint64_t)(p0 >> 64);
+  const u128 p2 = (u128)q * y2 + (uint64_t)(p1 >> 64);
+  const uint64_t m[4] = {(uint64_t)p0, (uint64_t)p1, (uint64_t)p2, (uint64_t)(p2 >> 64)};
+  uint64_t c = 0;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const uint64_t x = a.w[i], y = b.w[i];
-    const uint64_t d = x - y - br;
-    br = (x < y) || (x - y < br) ? 1 : 0;
-    a.w[i] = d;
+    if (neg) {  // w += q * Y
+      const u128 t = (u128)w[i] + m[i] + c;
+      w[i] = (uint64_t)t;
+      c = (uint64_t)(t >> 64);
+    } else {    // w -= q * Y
+      const uint64_t x = w[i];
+      const uint64_t d = x - m[i] - c;
+      c = (x < m[i] || (x - m[i]) < c) ? 1 : 0;
+      w[i] = d;
+    }
   }
+}
+
+// Scale words of one (app, phase): T > 0 (< 2^94), c_a > 0, C = sum of c (< 2^64).
+__device__ __forceinline__ void scale_words(u128 t, uint32_t ca, uint64_t C, uint64_t& sw, uint64_t& bsw) {
+  // Y = C * T < 2^158
+  const u128 p0 = (u128)C * (uint64_t)t;
+  const u128 p1 = (u128)C * (uint64_t)(t >> 64) + (uint64_t)(p0 >> 64);
+  const uint64_t y0 = (uint64_t)p0, y1 = (uint64_t)p1, y2 = (uint64_t)(p1 >> 64);
+  const int by = y2 ? 192 - __clzll(y2) : y1 ? 128 - __clzll(y1) : 64 - __clzll(y0);
+  const int bc = 32 - __clz(ca);
+  const int r0 = 96 + bc - by;
+  const int e = 56 - bc + by;  // in [25, 213]
+  const double yd = ldexp((double)y2, 128) + ldexp((double)y1, 64) + (double)y0;
+  double qd = floor(ldexp((double)ca, e) / yd);
+  qd = fmin(fmax(qd, 0.0), 0x1p58);
+  int64_t q = (int64_t)qd;
+  // R = c_a 2^e - q Y
+  uint64_t R[4] = {0, 0, 0, 0};
+  {
+    const int L = e >> 6, b = e & 63;
+    const uint64_t lo = (uint64_t)ca << b;
+    const uint64_t hi = b ? ((uint64_t)ca >> (64 - b)) : 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) R[i] = (i == L) ? lo : (i == L + 1) ? hi : 0;
+  }
+  s256_sub_mul(R, q, y0, y1, y2);
+  const int64_t dq = (int64_t)rint(s256_to_f64(R) / yd);
+  q += dq;
+  s256_sub_mul(R, dq, y0, y1, y2);
+  if ((int64_t)R[3] < 0) q -= 1;
+  const uint64_t uq = (uint64_t)q;
+  int rho;
+  uint64_t m;
+  if (uq >> 56) {
+    rho = r0;
+    m = uq >> 1;
+  } else {
+    rho = r0 - 1;
+    m = uq;
+  }
+  sw = scale_pack(m, rho);
+  bsw = bscale_pack(m, rho);
+}
+
+__device__ __forceinline__ void write_scale(uint32_t g, u128 t, const uint32_t* __restrict__ c, uint64_t C,
+                                            uint32_t P, uint64_t* __restrict__ scale, uint64_t* __restrict__ bscale) {
+  const uint32_t ca = c[g / P];
+  uint64_t sw = 0, bsw = 0;
+  if (t != 0 && ca != 0) scale_words(t, ca, C, sw, bsw);
+  scale[g] = sw;
+  bscale[g] = bsw;
 }
 
 __global__ void k_scale(const uint64_t* __restrict__ T, const uint32_t* __restrict__ c,
@@ -298,52 +322,36 @@ __global__ void k_scale(const uint64_t* __restrict__ T, const uint32_t* __restri
                         uint64_t* __restrict__ scale, uint64_t* __restrict__ bscale) {
   const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
   if (g >= A * P) return;
-  const u128 t = make_u128(T[2 * g], T[2 * g + 1]);
-  const uint32_t ca = c[g / P];
-  if (t == 0 || ca == 0) {
-    scale[g] = 0;
-    bscale[g] = 0;
-    return;
+  write_scale(g, make_u128(T[2 * g], T[2 * g + 1]), c, *Csum, P, scale, bscale);
+}
+
+// T[g] = sum over blocks of partial[b][g] + ext[g] * 2^ext_shift, and the
+// scale words of g (Eq. (3)) from it.  Block = 64 consecutive g x 16 strides
+// over the partial rows.
+template <typename PT>
+__global__ __launch_bounds__(1024) void k_pass_a_reduce(const PT* __restrict__ partial, uint32_t nb, uint32_t G,
+                                                        const unsigned long long* __restrict__ ext, int ext_shift,
+                                                        uint64_t* __restrict__ T, const uint32_t* __restrict__ c,
+                                                        const uint64_t* __restrict__ Csum, uint32_t P,
+                                                        uint64_t* __restrict__ scale, uint64_t* __restrict__ bscale) {
+  __shared__ uint64_t s_lo[16][64], s_hi[16][64];
+  const uint32_t gl = threadIdx.x & 63, r = threadIdx.x >> 6;
+  const uint32_t g = blockIdx.x * 64 + gl;
+  u128 acc = 0;
+  if (g < G) {
+#pragma unroll 8
+    for (uint32_t b = r; b < nb; b += 16) acc += (uint64_t)partial[(size_t)b * G + g];
   }
-  const uint64_t C = *Csum;
-  // Y = C * T (at most 159 bits)
-  const u128 p0 = (u128)C * (uint64_t)t;
-  const u128 p1 = (u128)C * (uint64_t)(t >> 64);
-  W256 Y;
-  Y.w[0] = (uint64_t)p0;
-  const u128 mid = (p0 >> 64) + (uint64_t)p1;
-  Y.w[1] = (uint64_t)mid;
-  Y.w[2] = (uint64_t)((p1 >> 64) + (mid >> 64));
-  Y.w[3] = 0;
-  const int bx = 96 + 32 - __clz(ca);  // bitlen(2^96 c_a)
-  const int r0 = bx - w256_bitlen(Y);
-  // numerator 2^(96 + s1) c_a, denominator Y 2^s2, quotient < 2^57
-  const int s1 = r0 < 56 ? 56 - r0 : 0;
-  const int s2 = r0 > 56 ? r0 - 56 : 0;
-  const W256 den = w256_shl(Y, s2);
-  W256 rem;  // numerator >> 57; the numerator's low 57 bits are zero
-  rem.w[0] = ca; rem.w[1] = rem.w[2] = rem.w[3] = 0;
-  rem = w256_shl(rem, 96 + s1 - 57);
-  uint64_t q = 0;
-  for (int i = 56; i >= 0; --i) {
-    rem = w256_shl(rem, 1);
-    q <<= 1;
-    if (w256_ge(rem, den)) {
-      w256_sub_inplace(rem, den);
-      q |= 1;
-    }
+  s_lo[r][gl] = (uint64_t)acc;
+  s_hi[r][gl] = (uint64_t)(acc >> 64);
+  __syncthreads();
+  if (r == 0 && g < G) {
+    u128 t = (u128)ext[g] << ext_shift;
+    for (int i = 0; i < 16; ++i) t += make_u128(s_lo[i][gl], s_hi[i][gl]);
+    T[2 * g] = (uint64_t)t;
+    T[2 * g + 1] = (uint64_t)(t >> 64);
+    write_scale(g, t, c, *Csum, P, scale, bscale);  // Eq. (3) scale of this (app, phase)
   }
-  int rho;
-  uint64_t m;
-  if (q >> 56) {
-    rho = r0;
-    m = q >> 1;
-  } else {
-    rho = r0 - 1;
-    m = q;
-  }
-  scale[g] = scale_pack(m, rho);
-  bscale[g] = bscale_pack(m, rho);
 }
 
 // ---------------------------------------------------------------------------
@@ -855,9 +863,10 @@ void launch_pass_a_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t 
 }
 
 void launch_pass_a_reduce(hipStream_t s, const unsigned long long* partial, uint32_t nb, uint32_t G,
-                          const unsigned long long* carry, uint64_t* T) {
+                          const unsigned long long* carry, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
+                          uint32_t P, uint64_t* scale, void* bscale) {
   hipLaunchKernelGGL(k_pass_a_reduce<unsigned long long>, dim3((G + 63) / 64), dim3(1024), 0, s, partial, nb, G, carry,
-                     64, T);
+                     64, T, c, Csum, P, scale, (uint64_t*)bscale);
 }
 
 void launch_pass_a_lds32(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
@@ -868,8 +877,10 @@ void launch_pass_a_lds32(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_
 }
 
 void launch_pass_a_reduce32(hipStream_t s, const uint32_t* partial, uint32_t nb, uint32_t G,
-                            const unsigned long long* ext, uint64_t* T) {
-  hipLaunchKernelGGL(k_pass_a_reduce<uint32_t>, dim3((G + 63) / 64), dim3(1024), 0, s, partial, nb, G, ext, 32, T);
+                            const unsigned long long* ext, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
+                            uint32_t P, uint64_t* scale, void* bscale) {
+  hipLaunchKernelGGL(k_pass_a_reduce<uint32_t>, dim3((G + 63) / 64), dim3(1024), 0, s, partial, nb, G, ext, 32, T, c,
+                     Csum, P, scale, (uint64_t*)bscale);
 }
 
 void launch_pass_a_range(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t GR, uint32_t R,

@@ -101,110 +101,123 @@ __device__ uint32_t block_exscan(uint32_t v, uint32_t* s_w, uint32_t& total) {
   return off + inc - v;
 }
 
+// Each thread owns at most SC_PER consecutive ranked units and keeps the
+// operators that start among them (U_i, S_i) in registers: one block scan
+// numbers the operators, one block sum gives sum U, and the compensated sums
+// of w_i S_i are merged in operator order (thread order, then wave order).
+constexpr uint32_t SC_PER = kScoreRankMax / NT;
+
+__device__ __forceinline__ Comp comp_shfl_down(Comp a, int d) {
+  return Comp{__shfl_down(a.s, d, 64), __shfl_down(a.c, d, 64)};
+}
+
 __global__ __launch_bounds__(NT) void k_score_final(const uint32_t* __restrict__ sorted_op,
                                                     const double* __restrict__ sorted_S, uint32_t n, UnitTable opt,
                                                     uint64_t nops_trace, uint32_t* __restrict__ op_out,
                                                     double* __restrict__ w_out, double* __restrict__ s_out,
                                                     double* __restrict__ s_agg, uint64_t* __restrict__ totU,
-                                                    unsigned long long* __restrict__ nret,
-                                                    uint64_t* __restrict__ rU) {
+                                                    unsigned long long* __restrict__ nret) {
   extern __shared__ uint64_t smem64[];
   double* s_S = (double*)smem64;             // [n]
   uint32_t* s_op = (uint32_t*)(s_S + n);     // [n]
   uint32_t* s_opid = s_op + n;               // [nops_trace] when it fits (kScoreOpsLds)
   const bool opid_lds = nops_trace <= kScoreOpsLds;
   __shared__ uint32_t s_w[NW];
-  __shared__ uint32_t s_carry;
   __shared__ uint64_t s_u[2 * NW];
-  __shared__ double s_cs[NT], s_cc[NT];
-  const uint32_t tid = threadIdx.x;
+  __shared__ double s_cs[NW], s_cc[NW];
+  const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   for (uint32_t j = tid; j < n; j += NT) {
     s_S[j] = sorted_S[j];
     s_op[j] = sorted_op[j];
   }
   if (opid_lds)
     for (uint32_t j = tid; j < (uint32_t)nops_trace; j += NT) s_opid[j] = opt.id[j];
-  if (tid == 0) s_carry = 0;
   __syncthreads();
-  // operator runs: medians (Eq. (5)) and U of the retained operators
-  u128 myU = 0;
-  for (uint32_t c0 = 0; c0 < n; c0 += NT) {
-    const uint32_t i = c0 + tid;
-    const bool head = i < n && (i == 0 || s_op[i - 1] != s_op[i]);
-    uint32_t tot;
-    const uint32_t ob = s_carry + block_exscan(head ? 1u : 0u, s_w, tot);
-    if (head) {
-      const uint32_t op = s_op[i];
-      uint32_t lo = i, hi = n;  // run end: first index with a larger operator
-      while (lo < hi) {
-        const uint32_t mid = (lo + hi) / 2;
-        if (s_op[mid] <= op) lo = mid + 1; else hi = mid;
-      }
-      const uint32_t e = lo;
-      lo = i;
-      hi = e;  // first NaN of the run (NaN sorts last)
-      while (lo < hi) {
-        const uint32_t mid = (lo + hi) / 2;
-        if (!isnan(s_S[mid])) lo = mid + 1; else hi = mid;
-      }
-      const uint32_t c = lo - i;
-      double Si = 0.0;
-      if (c) {
-        const uint32_t h = c / 2;
-        Si = (c & 1) ? s_S[i + h] : (s_S[i + h - 1] + s_S[i + h]) / 2.0;
-      }
-      uint64_t a = 0, b = nops_trace;  // the operator's row of the Eq. (3) table
-      while (a < b) {
-        const uint64_t mid = (a + b) / 2;
-        if ((opid_lds ? s_opid[mid] : opt.id[mid]) < op) a = mid + 1; else b = mid;
-      }
-      u128 U = 0;
-      if (a < nops_trace && (opid_lds ? s_opid[a] : opt.id[a]) == op) U = make_u128(opt.U[2 * a], opt.U[2 * a + 1]);
-      myU += U;
-      op_out[ob] = op;
-      s_out[ob] = Si;
-      rU[2 * ob] = (uint64_t)U;
-      rU[2 * ob + 1] = (uint64_t)(U >> 64);
-    }
-    __syncthreads();
-    if (tid == 0) s_carry += tot;
-    __syncthreads();
+  const uint32_t per = (n + NT - 1) / NT;  // <= SC_PER
+  const uint32_t b = min(n, tid * per), e = min(n, b + per);
+  uint32_t hmask = 0;  // bit j: unit b + j starts an operator run
+#pragma unroll
+  for (uint32_t j = 0; j < SC_PER; ++j) {
+    const uint32_t i = b + j;
+    if (i < e && (i == 0 || s_op[i - 1] != s_op[i])) hmask |= 1u << j;
   }
-  const uint32_t nops = s_carry;
+  uint32_t nops;
+  const uint32_t ob = block_exscan(__popc(hmask), s_w, nops);
+  // operator runs starting here: median of the correct S_j (Eq. (5)) and U_i
+  u128 U[SC_PER];
+  double Si[SC_PER];
+  u128 myU = 0;
+#pragma unroll
+  for (uint32_t j = 0; j < SC_PER; ++j) {
+    U[j] = 0;
+    Si[j] = 0.0;
+    if (!((hmask >> j) & 1u)) continue;
+    const uint32_t i = b + j, op = s_op[i];
+    uint32_t lo = i, hi = n;  // run end: first index with a larger operator
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi) / 2;
+      if (s_op[mid] <= op) lo = mid + 1; else hi = mid;
+    }
+    const uint32_t re = lo;
+    lo = i;
+    hi = re;  // first NaN of the run (NaN sorts last)
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi) / 2;
+      if (!isnan(s_S[mid])) lo = mid + 1; else hi = mid;
+    }
+    const uint32_t c = lo - i;
+    if (c) {
+      const uint32_t h = c / 2;
+      Si[j] = (c & 1) ? s_S[i + h] : (s_S[i + h - 1] + s_S[i + h]) / 2.0;
+    }
+    uint64_t x = 0, y = nops_trace;  // the operator's row of the Eq. (3) table
+    while (x < y) {
+      const uint64_t mid = (x + y) / 2;
+      if ((opid_lds ? s_opid[mid] : opt.id[mid]) < op) x = mid + 1; else y = mid;
+    }
+    if (x < nops_trace && (opid_lds ? s_opid[x] : opt.id[x]) == op) U[j] = make_u128(opt.U[2 * x], opt.U[2 * x + 1]);
+    myU += U[j];
+  }
+  // sum U over the retained operators
   const u128 tu = wave_sum_u128(myU);
-  if ((tid & 63) == 0) { s_u[2 * (tid >> 6)] = (uint64_t)tu; s_u[2 * (tid >> 6) + 1] = (uint64_t)(tu >> 64); }
+  if (lane == 0) {
+    s_u[2 * wave] = (uint64_t)tu;
+    s_u[2 * wave + 1] = (uint64_t)(tu >> 64);
+  }
   __syncthreads();
   u128 T = 0;
   for (uint32_t v = 0; v < NW; ++v) T += make_u128(s_u[2 * v], s_u[2 * v + 1]);
+  const double dT = u128_to_f64(T);
+  // w_i = RN(U_i) / RN(sum U); Eq. (6) as compensated sums in operator order
+  Comp acc{0.0, 0.0};
+  uint32_t k = ob;
+#pragma unroll
+  for (uint32_t j = 0; j < SC_PER; ++j) {
+    if (!((hmask >> j) & 1u)) continue;
+    const double wk = T == 0 ? 0.0 : u128_to_f64(U[j]) / dT;
+    op_out[k] = s_op[b + j];
+    s_out[k] = Si[j];
+    w_out[k] = wk;
+    acc = comp_add(acc, __dmul_rn(wk, Si[j]));
+    ++k;
+  }
+  for (int d = 1; d < 64; d <<= 1) {  // lanes in order: lane l takes l + d when l is a multiple of 2d
+    const Comp o = comp_shfl_down(acc, d);
+    if ((lane & (2 * d - 1)) == 0) acc = comp_merge(acc, o);
+  }
+  if (lane == 0) {
+    s_cs[wave] = acc.s;
+    s_cc[wave] = acc.c;
+  }
+  __syncthreads();
   if (tid == 0) {
+    Comp t{s_cs[0], s_cc[0]};
+    for (uint32_t v = 1; v < NW; ++v) t = comp_merge(t, Comp{s_cs[v], s_cc[v]});
+    *s_agg = t.s + t.c;
     totU[0] = (uint64_t)T;
     totU[1] = (uint64_t)(T >> 64);
     *nret = nops;
   }
-  const double dT = u128_to_f64(T);
-  __threadfence_block();
-  __syncthreads();
-  // Eq. (6): compensated sums over contiguous runs of operators, then a TwoSum tree
-  const uint32_t per = (nops + NT - 1) / NT;
-  const uint32_t b = tid * per, e = min(b + per, nops);
-  Comp accs{0.0, 0.0};
-  for (uint32_t k = b; k < e; ++k) {
-    const double wk = T == 0 ? 0.0 : u128_to_f64(make_u128(rU[2 * k], rU[2 * k + 1])) / dT;
-    w_out[k] = wk;
-    accs = comp_add(accs, __dmul_rn(wk, s_out[k]));
-  }
-  s_cs[tid] = accs.s;
-  s_cc[tid] = accs.c;
-  __syncthreads();
-  for (uint32_t d = NT / 2; d >= 1; d >>= 1) {
-    if (tid < d) {
-      const Comp mm = comp_merge(Comp{s_cs[tid], s_cc[tid]}, Comp{s_cs[tid + d], s_cc[tid + d]});
-      s_cs[tid] = mm.s;
-      s_cc[tid] = mm.c;
-    }
-    __syncthreads();
-  }
-  if (tid == 0) *s_agg = s_cs[0] + s_cc[0];
 }
 
 }  // namespace
@@ -217,9 +230,9 @@ void launch_score_small(hipStream_t s, const uint32_t* score_key, const double* 
   hipLaunchKernelGGL(k_score_rank, dim3((nn + MINE - 1) / MINE), dim3(NT), (size_t)nn * 12, s, score_key, S, nn,
                      sorted_op, sorted_S, err);
   const size_t opid_bytes = nops_trace <= kScoreOpsLds ? (size_t)nops_trace * 4 : 0;
+  (void)rU;
   hipLaunchKernelGGL(k_score_final, dim3(1), dim3(NT), (size_t)nn * 12 + opid_bytes, s, sorted_op, sorted_S, nn, opt,
-                     nops_trace,
-                     op_out, w_out, s_out, s_agg, totU, nret, rU);
+                     nops_trace, op_out, w_out, s_out, s_agg, totU, nret);
 }
 
 hipError_t set_score_smem_limits() {

@@ -15,6 +15,8 @@
 //
 // Phi (phases in which the unit runs) is the set of phases with a group,
 // i.e. with at least one invocation.
+#include <algorithm>
+
 #include "atrex_device.hpp"
 #include "atrex_kernels.h"
 
@@ -103,7 +105,7 @@ __global__ __launch_bounds__(TILE) void k_units_tiles(SortedGroups g, uint64_t G
       sum += load_u128(g.wsum, e);
       mask |= 1u << g.phase[e];
     }
-    Uk = (u128)(L / __popc(mask)) * sum;
+    Uk = (u128)((uint32_t)L / (uint32_t)__popc(mask)) * sum;
     store_u128(us.keyU, i, Uk);
   }
   uint32_t nkeys;
@@ -225,7 +227,7 @@ __global__ __launch_bounds__(TILE) void k_units_ops(uint32_t ntiles, uint32_t P,
     const uint64_t wlo = __hip_atomic_load(&ops.U[2 * q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint64_t whi = __hip_atomic_load(&ops.U[2 * q + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint32_t mask = __hip_atomic_load(&us.opMask[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const u128 U = (u128)(L / __popc(mask)) * make_u128(wlo, whi);
+    const u128 U = (u128)((uint32_t)L / (uint32_t)__popc(mask)) * make_u128(wlo, whi);
     store_u128(ops.U, q, U);
     sumU += U;
   }
@@ -260,6 +262,28 @@ __global__ __launch_bounds__(TILE) void k_units_keys(SortedGroups g, uint64_t G,
 }
 
 // ---------------------------------------------------------------------------
+// The groups copied to the caller's arrays with RN(W) / RN(S[ph]), one thread
+// per group (the per-phase totals by the first threads), for the one-workgroup
+// unit kernel below.
+__global__ __launch_bounds__(256) void k_group_weights(SortedGroups g, uint32_t G, uint32_t P,
+                                                        const uint64_t* __restrict__ S, GroupsOut out) {
+  const uint32_t i = blockIdx.x * 256 + threadIdx.x;
+  if (i < P) {
+    out.phase_total[2 * i] = S[2 * i];
+    out.phase_total[2 * i + 1] = S[2 * i + 1];
+  }
+  if (i >= G) return;
+  const uint32_t ph = g.phase[i];
+  const u128 W = load_u128(g.wsum, i);
+  out.key[i] = g.key[i];
+  out.phase[i] = (uint8_t)ph;
+  out.count[i] = g.count[i];
+  store_u128(out.wsum, i, W);
+  if (out.raw) store_u128(out.raw, i, load_u128(g.raw, i));
+  out.weight[i] = ratio(W, load_u128(S, ph));
+}
+
+// ---------------------------------------------------------------------------
 // One workgroup for up to kUnitsSmallMax groups: thread t holds groups
 // [8t, 8t + 8) in registers; the key runs and operator runs are summed with
 // one block-wide segmented scan (operator: a run head restarts the sum), and
@@ -285,18 +309,15 @@ __device__ __forceinline__ Seg seg_shfl_up(const Seg& x, int d) {
   return y;
 }
 
-__global__ __launch_bounds__(TILE) void k_units_small(SortedGroups g, uint32_t G, uint32_t P, uint64_t L,
-                                                      const uint64_t* __restrict__ S, GroupsOut out, UnitTable ops,
+__global__ __launch_bounds__(TILE) void k_units_small(SortedGroups g, uint32_t G, uint32_t L, UnitTable ops,
                                                       uint64_t maxOps, UnitTable keys,
                                                       unsigned long long* __restrict__ counts,
                                                       uint32_t* __restrict__ err) {
   __shared__ Seg s_kw[NW], s_ow[NW];
   __shared__ uint32_t s_nk[NW], s_no[NW];
   __shared__ uint64_t s_lo[NW], s_hi[NW];
-  __shared__ uint64_t s_S[16];
   const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const uint32_t i0 = tid * SM_PER;
-  if (tid < 2 * P) s_S[tid] = S[tid];
   // this thread's groups, the key before them and the key after them
   uint32_t key[SM_PER], ph[SM_PER];
   u128 W[SM_PER];
@@ -311,23 +332,6 @@ __global__ __launch_bounds__(TILE) void k_units_small(SortedGroups g, uint32_t G
   const bool has_next = i0 + SM_PER < G;
   const uint32_t knext = has_next ? g.key[i0 + SM_PER] : 0u;
   __syncthreads();
-  // the groups, with RN(W) / RN(S[ph])
-#pragma unroll
-  for (int j = 0; j < SM_PER; ++j) {
-    const uint32_t i = i0 + j;
-    if (i < G) {
-      out.key[i] = key[j];
-      out.phase[i] = (uint8_t)ph[j];
-      out.count[i] = g.count[i];
-      store_u128(out.wsum, i, W[j]);
-      if (out.raw) store_u128(out.raw, i, load_u128(g.raw, i));
-      out.weight[i] = ratio(W[j], make_u128(s_S[2 * ph[j]], s_S[2 * ph[j] + 1]));
-    }
-  }
-  if (tid < P) {
-    out.phase_total[2 * tid] = s_S[2 * tid];
-    out.phase_total[2 * tid + 1] = s_S[2 * tid + 1];
-  }
   // heads of key runs and operator runs
   uint32_t kh = 0, oh = 0;  // bit j: group j heads a run
 #pragma unroll
@@ -409,13 +413,13 @@ __global__ __launch_bounds__(TILE) void k_units_small(SortedGroups g, uint32_t G
         const bool last = i + 1 == G;
         const uint32_t nx = j + 1 < SM_PER ? key[j + 1] : knext;
         if (last || nx != key[j]) {
-          const u128 U = (u128)(L / __popc(kr.m)) * kr.v;
+          const u128 U = (u128)(L / (uint32_t)__popc(kr.m)) * kr.v;
           keys.id[kidx - 1] = key[j];
           store_u128(keys.U, kidx - 1, U);
           sumUk += U;
         }
         if (last || (nx >> 16) != (key[j] >> 16)) {
-          const u128 U = (u128)(L / __popc(orr.m)) * orr.v;
+          const u128 U = (u128)(L / (uint32_t)__popc(orr.m)) * orr.v;
           if (ops_fit) {
             ops.id[oidx - 1] = key[j] >> 16;
             store_u128(ops.U, oidx - 1, U);
@@ -457,7 +461,9 @@ void launch_units(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, 
                   const GroupsOut& out, const UnitScratch& us, const UnitTable& ops, uint64_t maxOps,
                   const UnitTable& keys, unsigned long long* counts, uint32_t* err) {
   if (G <= kUnitsSmallMax) {
-    hipLaunchKernelGGL(k_units_small, dim3(1), dim3(TILE), 0, s, g, (uint32_t)G, P, L, S, out, ops, maxOps, keys,
+    hipLaunchKernelGGL(k_group_weights, dim3((uint32_t)std::max<uint64_t>(1, (G + 255) / 256)), dim3(256), 0, s, g,
+                       (uint32_t)G, P, S, out);
+    hipLaunchKernelGGL(k_units_small, dim3(1), dim3(TILE), 0, s, g, (uint32_t)G, (uint32_t)L, ops, maxOps, keys,
                        counts, err);
     return;
   }
