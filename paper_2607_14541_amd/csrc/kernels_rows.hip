@@ -540,12 +540,14 @@ __global__ __launch_bounds__(1024) void k_part_hist(PartSource src, uint32_t BB,
 }
 
 // Records: (share lo, share hi | phase << 33 | low hash bits << 36).  Each
-// workgroup (SC_BLOCK threads, several per CU) walks its event range in tiles
-// of SC_TILE events, the next tile's events loaded while the current one is
-// placed: records and buckets are formed in registers, counted per bucket in
-// LDS, placed in LDS in bucket order and written out as runs, so that
-// consecutive lanes write consecutive records of a bucket.
-constexpr uint32_t SC_BLOCK = 1024;  // tiles of EPT * SC_BLOCK events, EPT = 8 or 4 (LDS budget)
+// workgroup walks its event range in tiles of SC_TILE = 4 x 1024 events
+// (eight events per thread need more than the 128 registers a 1024-thread
+// workgroup allows).  Phase 1 takes every record's bucket and its rank among
+// the tile's records of that bucket (an LDS counter) and requests its scale
+// word; after a scan of the tile's bucket counts, phase 2 forms the Q96 share
+// and places the record in LDS in bucket order; the tile is then written out
+// as runs, consecutive lanes writing consecutive records of a bucket, while
+// the next tile's events are loaded.
 
 __device__ __forceinline__ void load_group(const EventsDev& ev, uint64_t q, uint64_t e, Ev4& x) {
   if (q + 3 < e) {  // q is a multiple of 4: a whole, 16-byte aligned group
@@ -562,7 +564,7 @@ __device__ __forceinline__ void load_group(const EventsDev& ev, uint64_t q, uint
   }
 }
 
-template <bool RAW, uint32_t SC_EPT>
+template <bool RAW, bool SPILL, uint32_t SC_EPT, uint32_t SC_BLOCK>
 __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint32_t A, uint32_t P,
                                                            const uint64_t* __restrict__ scale,
                                                            const uint64_t* __restrict__ bscale, uint32_t BB,
@@ -587,77 +589,50 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint3
   const uint64_t lowmask = ((uint64_t)1 << lowbits) - 1;
   bool bad = false;
   constexpr uint32_t G4 = SC_EPT / 4;  // groups of four events per thread, SC_BLOCK groups apart
-  constexpr bool PREFETCH = G4 == 1;   // the next tile's events in registers (when they fit)
-  Ev4 nxt[PREFETCH ? 1 : 0 + 1];
-  if (PREFETCH && !src.spill) load_group(src.ev, b + 4 * (uint64_t)tid, e, nxt[0]);
+  // the next tile's events are requested once the current tile's records are
+  // placed in LDS, so that they arrive during its write-out
+  Ev4 nxt[G4];
+  if (!SPILL) {
+#pragma unroll
+    for (uint32_t g = 0; g < G4; ++g) load_group(src.ev, b + 4 * ((uint64_t)g * SC_BLOCK + tid), e, nxt[g]);
+  }
   for (uint64_t t0 = b; t0 < e; t0 += SC_TILE) {  // uniform trip count
     Ev4 evg[G4];
-    if (PREFETCH) {
-      evg[0] = nxt[0];
-      if (!src.spill && t0 + SC_TILE < e) load_group(src.ev, t0 + SC_TILE + 4 * (uint64_t)tid, e, nxt[0]);
-    } else if (!src.spill) {
 #pragma unroll
-      for (uint32_t g = 0; g < G4; ++g) load_group(src.ev, t0 + 4 * ((uint64_t)g * SC_BLOCK + tid), e, evg[g]);
-    }
+    for (uint32_t g = 0; g < G4; ++g) evg[g] = nxt[g];
     for (uint32_t i = tid; i < NB; i += SC_BLOCK) s_cnt[i] = 0;
     __syncthreads();
-    uint64_t vlo[SC_EPT], w1[SC_EPT], d[SC_EPT];
-    uint32_t bk[SC_EPT], rank[SC_EPT];
-    bool v[SC_EPT];
-    if (src.spill) {
+    // phase 1: validity, bucket and rank of every record; the scale words
+    // are requested here and used after the scan
+    uint32_t hh[SC_EPT], rk[SC_EPT];  // hash; rank << 4 | exists << 3 | phase
+    uint64_t dv[SC_EPT], sw[SC_EPT];
 #pragma unroll
-      for (uint32_t j = 0; j < SC_EPT; ++j) {
-        const uint64_t i = t0 + 4 * ((uint64_t)(j / 4) * SC_BLOCK + tid) + (j % 4);
-        v[j] = i < e;
-        uint32_t key = 0, ph = 0;
-        vlo[j] = 0; d[j] = 0;
-        uint64_t vhi = 0;
-        if (v[j]) {
-          key = src.skey[i];
-          vlo[j] = src.sval[2 * i];
-          vhi = src.sval[2 * i + 1] & (((uint64_t)1 << 40) - 1);
-          ph = (uint32_t)(src.sval[2 * i + 1] >> 40);
-          if (RAW) d[j] = src.sraw[i];
-        }
-        const uint32_t h = hash32(key);
-        bk[j] = h >> lowbits;
-        w1[j] = vhi | ((uint64_t)ph << 33) | (((uint64_t)h & lowmask) << 36);
-      }
-    } else {
-#pragma unroll
-      for (uint32_t j = 0; j < SC_EPT; ++j) {
+    for (uint32_t j = 0; j < SC_EPT; ++j) {
+      const uint64_t i = t0 + 4 * ((uint64_t)(j / 4) * SC_BLOCK + tid) + (j % 4);
+      const bool vj = i < e;
+      uint32_t key = 0;
+      dv[j] = 0;
+      sw[j] = 0;
+      rk[j] = 0;
+      if (SPILL) {
+        key = vj ? src.skey[i] : 0;
+      } else {
         const Ev4& ev = evg[j / 4];
         const uint32_t jj = j % 4;
-        v[j] = t0 + 4 * ((uint64_t)(j / 4) * SC_BLOCK + tid) + jj < e;
         const uint32_t a = ev.app[jj], ph = ev.ph[jj];
         const int64_t dd = ev.dur[jj];
         const bool ok = a < A && ph < P && dd >= 0;
-        bad |= v[j] && !ok;
-        const uint32_t g = ok ? a * P + ph : 0;
-        const uint64_t sw = ok ? bscale[g] : 0;
-        uint64_t vl, vh;
-        if (ok && (uint32_t)(sw >> 56) <= 127u) {
-          if (((uint64_t)dd >> 32) == 0) {
-            uint32_t h32;
-            bscale_share32((uint32_t)dd, (uint32_t)sw, (uint32_t)(sw >> 32), vl, h32);
-            vh = h32;
-          } else {
-            bscale_share64((uint64_t)dd, (uint32_t)sw, (uint32_t)(sw >> 32), vl, vh);
-          }
-        } else {
-          const u128 x = event_share(ok ? (uint64_t)dd : 0, ok ? scale[g] : 0);
-          vl = (uint64_t)x;
-          vh = (uint64_t)(x >> 64);
-        }
-        vlo[j] = vl;
-        d[j] = ok ? (uint64_t)dd : 0;
-        const uint32_t h = hash32(ev.key[jj]);
-        bk[j] = h >> lowbits;
-        w1[j] = vh | ((uint64_t)(ok ? ph : 0) << 33) | (((uint64_t)h & lowmask) << 36);
+        bad |= vj && !ok;
+        sw[j] = ok ? bscale[a * P + ph] : 0;
+        dv[j] = ok ? (uint64_t)dd : 0;
+        rk[j] = ok ? ph : 0u;
+        key = ev.key[jj];
       }
+      if (vj) rk[j] |= 8u;
+      hh[j] = hash32(key);
     }
 #pragma unroll
-    for (uint32_t j = 0; j < SC_EPT; ++j) rank[j] = count_in(s_cnt, bk[j], v[j]);
+    for (uint32_t j = 0; j < SC_EPT; ++j) rk[j] |= count_in(s_cnt, hh[j] >> lowbits, (rk[j] >> 3) & 1u) << 4;
     __syncthreads();
     // exclusive scan of the tile's bucket counts
     {
@@ -679,14 +654,47 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint3
         if (b0 + k < NB) { s_off[b0 + k] = run; run += s_cnt[b0 + k]; }
     }
     __syncthreads();
+    // phase 2: the Q96 share of every record, placed in LDS in bucket order
 #pragma unroll
     for (uint32_t j = 0; j < SC_EPT; ++j) {
-      if (!v[j]) continue;
-      const uint32_t at = s_off[bk[j]] + rank[j];
-      s_rec[2 * at] = vlo[j];
-      s_rec[2 * at + 1] = w1[j];
-      if (RAW) s_raw[at] = d[j];
-      s_bkt[at] = (uint16_t)bk[j];
+      if (!((rk[j] >> 3) & 1u)) continue;
+      const uint32_t bk = hh[j] >> lowbits;
+      uint64_t vl, vh, d = dv[j];
+      uint32_t ph;
+      if (SPILL) {
+        const uint64_t i = t0 + 4 * ((uint64_t)(j / 4) * SC_BLOCK + tid) + (j % 4);
+        vl = src.sval[2 * i];
+        vh = src.sval[2 * i + 1] & (((uint64_t)1 << 40) - 1);
+        ph = (uint32_t)(src.sval[2 * i + 1] >> 40);
+        if (RAW) d = src.sraw[i];
+      } else {
+        ph = rk[j] & 7u;
+        const uint64_t w = sw[j];
+        if ((uint32_t)(w >> 56) <= 127u) {
+          if ((d >> 32) == 0) {
+            uint32_t h32;
+            bscale_share32((uint32_t)d, (uint32_t)w, (uint32_t)(w >> 32), vl, h32);
+            vh = h32;
+          } else {
+            bscale_share64(d, (uint32_t)w, (uint32_t)(w >> 32), vl, vh);
+          }
+        } else {  // rho outside [-8, 63] (rare): the general scale word, found again from the event
+          const uint64_t i = t0 + 4 * ((uint64_t)(j / 4) * SC_BLOCK + tid) + (j % 4);
+          const u128 x = event_share(d, scale[src.ev.app[i] * P + ph]);
+          vl = (uint64_t)x;
+          vh = (uint64_t)(x >> 64);
+        }
+      }
+      const uint32_t at = s_off[bk] + (rk[j] >> 4);
+      s_rec[2 * at] = vl;
+      s_rec[2 * at + 1] = vh | ((uint64_t)ph << 33) | (((uint64_t)hh[j] & lowmask) << 36);
+      if (RAW) s_raw[at] = d;
+      s_bkt[at] = (uint16_t)bk;
+    }
+    if (!SPILL && t0 + SC_TILE < e) {
+#pragma unroll
+      for (uint32_t g = 0; g < G4; ++g)
+        load_group(src.ev, t0 + SC_TILE + 4 * ((uint64_t)g * SC_BLOCK + tid), e, nxt[g]);
     }
     __syncthreads();
     const uint32_t nt = (uint32_t)min((uint64_t)SC_TILE, e - t0);
@@ -1016,10 +1024,10 @@ size_t lds_table_bytes(uint32_t P, bool raw, uint32_t S) {
   return ((size_t)S * P * 16 + 64 * 16) * (raw ? 2 : 1) + (size_t)S * 4;
 }
 
-static uint32_t scatter_ept(uint32_t BB, bool raw) { return (!raw && BB <= 10) ? 8 : 4; }
+constexpr uint32_t kScatterEpt = 4, kScatterBlock = 1024;
 
 static size_t scatter_smem(uint32_t BB, bool raw) {
-  return (size_t)scatter_ept(BB, raw) * SC_BLOCK * (16 + (raw ? 8 : 0) + 2) + ((size_t)3 << BB) * 4;
+  return (size_t)kScatterEpt * kScatterBlock * (16 + (raw ? 8 : 0) + 2) + ((size_t)3 << BB) * 4;
 }
 
 uint32_t part_scatter_wgs(uint32_t cus) { return std::min<uint32_t>(kMaxPartWG, cus); }
@@ -1033,15 +1041,15 @@ void launch_part_scatter(hipStream_t s, const PartSource& src, uint32_t nwg, uin
                          const uint64_t* scale, const uint64_t* bscale, uint32_t BB, const uint32_t* O, uint64_t* rec,
                          uint64_t* rraw, uint32_t* err) {
   const size_t smem = scatter_smem(BB, rraw != nullptr);
-  if (rraw)
-    hipLaunchKernelGGL((k_part_scatter<true, 4>), dim3(nwg), dim3(SC_BLOCK), smem, s, src, A, P, scale, bscale, BB,
-                       O, rec, rraw, err);
-  else if (scatter_ept(BB, false) == 8)
-    hipLaunchKernelGGL((k_part_scatter<false, 8>), dim3(nwg), dim3(SC_BLOCK), smem, s, src, A, P, scale, bscale, BB,
-                       O, rec, rraw, err);
-  else
-    hipLaunchKernelGGL((k_part_scatter<false, 4>), dim3(nwg), dim3(SC_BLOCK), smem, s, src, A, P, scale, bscale, BB,
-                       O, rec, rraw, err);
+#define ATREX_SCATTER(R, S)                                                                                     \
+  hipLaunchKernelGGL((k_part_scatter<R, S, kScatterEpt, kScatterBlock>), dim3(nwg), dim3(kScatterBlock), smem, s, \
+                     src, A, P, scale, bscale, BB, O, rec, rraw, err)
+  if (rraw) {
+    if (src.spill) ATREX_SCATTER(true, true); else ATREX_SCATTER(true, false);
+  } else {
+    if (src.spill) ATREX_SCATTER(false, true); else ATREX_SCATTER(false, false);
+  }
+#undef ATREX_SCATTER
 }
 
 void launch_part_items(hipStream_t s, const uint32_t* O, const uint32_t* H, uint32_t nw, uint32_t BB, uint32_t CH,
@@ -1117,8 +1125,11 @@ void launch_lists_to_rows(hipStream_t s, const OwnerLists& ol, const Rows& rows,
 // Dynamic LDS limits: 160 KB less a margin that covers each kernel's static LDS.
 hipError_t set_rows_smem_limits() {
   const void* fns[] = {(const void*)k_part_aggregate<true>, (const void*)k_part_aggregate<false>,
-                       (const void*)k_part_hist, (const void*)k_part_scatter<true, 4>, (const void*)k_part_scatter<false, 4>,
-                       (const void*)k_part_scatter<false, 8>};
+                       (const void*)k_part_hist,
+                       (const void*)k_part_scatter<true, false, kScatterEpt, kScatterBlock>,
+                       (const void*)k_part_scatter<true, true, kScatterEpt, kScatterBlock>,
+                       (const void*)k_part_scatter<false, false, kScatterEpt, kScatterBlock>,
+                       (const void*)k_part_scatter<false, true, kScatterEpt, kScatterBlock>};
   for (const void* f : fns) {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 2048);
     if (e != hipSuccess) return e;
