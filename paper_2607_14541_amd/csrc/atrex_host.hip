@@ -21,7 +21,7 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr size_t kLdsBytes = 160 * 1024;
-constexpr uint32_t kPassAThreads = 512;
+constexpr uint32_t kPassAThreads = 1024;  // two workgroups per CU (32 waves) when the table allows
 constexpr uint64_t kPartialRowsMax = 1024;  // pass-A workgroups with private partial rows
 constexpr uint64_t kMaxWG = 256;            // persistent workgroups of the LDS engines
 constexpr uint32_t kMaxBucketBits = 12;     // radix-partition buckets: at most 4096

@@ -859,7 +859,7 @@ void launch_pass_a_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t 
                        unsigned long long* partial, unsigned long long* carry, uint32_t* err) {
   const uint32_t G = A * P;
   const size_t smem = (size_t)G * 8;
-  hipLaunchKernelGGL((k_pass_a_lds<512>), dim3(nblocks), dim3(512), smem, s, ev, A, P, G, partial, carry, err);
+  hipLaunchKernelGGL((k_pass_a_lds<1024>), dim3(nblocks), dim3(1024), smem, s, ev, A, P, G, partial, carry, err);
 }
 
 void launch_pass_a_reduce(hipStream_t s, const unsigned long long* partial, uint32_t nb, uint32_t G,
@@ -952,7 +952,7 @@ void launch_compact_rows(hipStream_t s, const GroupTables& gt, uint32_t P, const
 }
 
 hipError_t set_kernel_smem_limits() {
-  hipError_t e = hipFuncSetAttribute((const void*)k_pass_a_lds<512>, hipFuncAttributeMaxDynamicSharedMemorySize,
+  hipError_t e = hipFuncSetAttribute((const void*)k_pass_a_lds<1024>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                      160 * 1024);
   if (e != hipSuccess) return e;
   e = hipFuncSetAttribute((const void*)k_pass_a_lds32<1024>, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
