@@ -839,43 +839,62 @@ atrex_status atrex_weighted_score(atrex_ctx* c, const uint32_t* score_key, const
   uint64_t *K0 = c->at<uint64_t>(L.sk[0]), *K1 = c->at<uint64_t>(L.sk[1]), *K2 = c->at<uint64_t>(L.sk[2]);
   uint32_t *V0 = c->at<uint32_t>(L.sv[0]), *V1 = c->at<uint32_t>(L.sv[1]), *V2 = c->at<uint32_t>(L.sv[2]);
   void* rtmp = c->at<void>(L.rs_tmp);
-  launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 1, 0);
-  TIMED(c, "score_validate", n, launch_score_validate(s, sv, n, c->err()));
-  // (key) order for the duplicate check; (op, S) order for the medians
-  launch_score_keys(s, score_key, sv, n, K0, K2, V2);
-  (void)hipMemcpyAsync(V0, V2, n * 4, hipMemcpyDeviceToDevice, s);
-  TIMED(c, "score_sort_keys", n, radix_sort_pairs(s, K0, V0, K1, V1, n, 32, rtmp));
-  launch_dup_check(s, K0, n, c->err());
-  TIMED(c, "score_sort_S", n, radix_sort_pairs(s, K2, V2, K1, V1, n, 64, rtmp));
-  launch_score_opkeys(s, score_key, V2, n, K0);
-  TIMED(c, "score_sort_op", n, radix_sort_pairs(s, K0, V2, K1, V1, n, 16, rtmp));
   uint32_t* flags = c->at<uint32_t>(L.flags);
   uint32_t* scan = c->at<uint32_t>(L.scan);
   uint32_t* starts = c->at<uint32_t>(L.starts);
+  uint32_t* maxlen = c->at<uint32_t>(L.ctrl + 336);
+  launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 1, 0);
+  launch_fill_u64(s, c->at<uint64_t>(L.ctrl + 336), 1, 0);
+  TIMED(c, "score_validate", n, launch_score_validate(s, sv, n, c->err()));
+  // operator segments (stable sort of the units by operator)
+  launch_score_opiota(s, score_key, n, K0, V0);
+  TIMED(c, "score_sort_op", n, radix_sort_pairs(s, K0, V0, K1, V1, n, 16, rtmp));
   launch_heads_u64(s, K0, n, flags);
   exclusive_scan_u32(s, flags, scan, n, c->at<void>(L.scan_tmp));
   launch_unit_starts(s, flags, scan, n, starts);
+  launch_seg_maxlen(s, flags, scan, n, starts, maxlen);
   uint32_t hdr[4] = {0, 0, 0, 0};
   d2h(c, &hdr[0], c->err(), 4);
   d2h(c, &hdr[1], scan + (n - 1), 4);
   d2h(c, &hdr[2], flags + (n - 1), 4);
+  d2h(c, &hdr[3], maxlen, 4);
   atrex_status st = sync_read(c);
   if (st != ATREX_OK) return st;
   if (hdr[0] & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
-  if (hdr[0] & ATREX_ERRBIT_DUP) return ATREX_E_INVALID_ARG;
-  const uint64_t nr = (uint64_t)hdr[1] + hdr[2];
+  uint64_t nr = (uint64_t)hdr[1] + hdr[2];
   UnitTable opt{c->at<uint32_t>(L.op_id), c->at<uint64_t>(L.op_U), c->at<double>(L.op_w)};
   uint32_t* r_op = c->at<uint32_t>(L.r_op);
   uint64_t* r_U = c->at<uint64_t>(L.r_U);
   double* r_S = c->at<double>(L.r_S);
-  TIMED(c, "score_ops", nr, launch_score_ops(s, score_key, sv, V2, starts, nr, n, opt, c->nops, r_op, r_U, r_S));
+  if (hdr[3] <= kScoreSegMax) {
+    // per operator in LDS: duplicate check, median, U
+    TIMED(c, "score_seg", nr,
+          launch_score_seg(s, score_key, sv, V0, starts, nr, hdr[3], opt, c->nops, r_op, r_U, r_S, c->err()));
+  } else {
+    // an operator with more than kScoreSegMax units: (key) order for the
+    // duplicate check, (op, S) order for the medians, by global sorts
+    launch_score_keys(s, score_key, sv, n, K0, K2, V2);
+    (void)hipMemcpyAsync(V0, V2, n * 4, hipMemcpyDeviceToDevice, s);
+    TIMED(c, "score_sort_keys", n, radix_sort_pairs(s, K0, V0, K1, V1, n, 32, rtmp));
+    launch_dup_check(s, K0, n, c->err());
+    TIMED(c, "score_sort_S", n, radix_sort_pairs(s, K2, V2, K1, V1, n, 64, rtmp));
+    launch_score_opkeys(s, score_key, V2, n, K0);
+    TIMED(c, "score_sort_op_S", n, radix_sort_pairs(s, K0, V2, K1, V1, n, 16, rtmp));
+    launch_heads_u64(s, K0, n, flags);
+    exclusive_scan_u32(s, flags, scan, n, c->at<void>(L.scan_tmp));
+    launch_unit_starts(s, flags, scan, n, starts);
+    TIMED(c, "score_ops", nr, launch_score_ops(s, score_key, sv, V2, starts, nr, n, opt, c->nops, r_op, r_U, r_S));
+  }
   uint64_t* tot = c->at<uint64_t>(L.total) + 4;
   const uint32_t nb = (uint32_t)std::min<uint64_t>(1024, std::max<uint64_t>(1, (nr + 255) / 256));
   launch_sum_u128(s, r_U, nr, c->at<uint64_t>(L.partials), nb, tot);
   uint64_t totU[2] = {0, 0};
+  uint32_t e2 = 0;
+  d2h(c, &e2, c->err(), 4);
   d2h(c, totU, tot, 16);
   st = sync_read(c);
   if (st != ATREX_OK) return st;
+  if (e2 & ATREX_ERRBIT_DUP) return ATREX_E_INVALID_ARG;          // a key scored twice
   if (totU[0] == 0 && totU[1] == 0) return ATREX_E_INVALID_ARG;  // no retained weight
   TIMED(c, "score_final", nr,
         launch_score_final(s, r_op, r_U, r_S, nr, tot, op, op_weight, op_score, c->sagg(), c->err()));

@@ -227,6 +227,16 @@ void launch_score_opkeys(hipStream_t s, const uint32_t* score_key, const uint32_
 void launch_score_ops(hipStream_t s, const uint32_t* score_key, const double* S, const uint32_t* order,
                       const uint32_t* starts, uint64_t nops, uint64_t n, UnitTable opt, uint64_t nops_trace,
                       uint32_t* r_op, uint64_t* r_U, double* r_S);
+// Large-n score by operator segments: operator keys + identity order, the
+// longest segment, and one workgroup per segment (segments <= kScoreSegMax).
+constexpr uint32_t kScoreSegMax = 8192;
+void launch_score_opiota(hipStream_t s, const uint32_t* score_key, uint64_t n, uint64_t* k_op, uint32_t* idx);
+void launch_seg_maxlen(hipStream_t s, const uint32_t* flags, const uint32_t* scan, uint64_t n, const uint32_t* starts,
+                       uint32_t* out);
+void launch_score_seg(hipStream_t s, const uint32_t* score_key, const double* S, const uint32_t* order,
+                      const uint32_t* starts, uint64_t nseg, uint32_t maxlen, const UnitTable& opt, uint64_t nops_trace,
+                      uint32_t* r_op, uint64_t* r_U, double* r_S, uint32_t* err);
+hipError_t set_normalize_smem_limits();
 void launch_score_final(hipStream_t s, const uint32_t* r_op, const uint64_t* r_U, const double* r_S,
                         uint64_t nops, const uint64_t* totalU, uint32_t* op, double* op_weight, double* op_score,
                         double* s_agg, uint32_t* err);

@@ -124,8 +124,9 @@ __global__ void k_score_opkeys(const uint32_t* __restrict__ score_key, const uin
 }
 
 // One thread per retained operator: Eq. (5) median of the correct S_j (they
-// come first in the segment, ascending), 0 if none; U_i looked up in the
-// operator table of the trace (absent: 0).
+// come first in the segment, ascending; the first NaN is found by binary
+// search), 0 if none; U_i looked up in the operator table of the trace
+// (absent: 0).
 __global__ void k_score_ops(const uint32_t* __restrict__ score_key, const double* __restrict__ S,
                             const uint32_t* __restrict__ order, const uint32_t* __restrict__ starts, uint64_t nops,
                             UnitTable opt, uint64_t nops_trace, uint32_t* __restrict__ r_op,
@@ -134,8 +135,12 @@ __global__ void k_score_ops(const uint32_t* __restrict__ score_key, const double
   if (u >= nops) return;
   const uint32_t b = starts[u], e = starts[u + 1];
   const uint32_t op = score_key[order[b]] >> 16;
-  uint32_t c = 0;
-  while (b + c < e && !isnan(S[order[b + c]])) ++c;
+  uint32_t lo_n = b, hi_n = e;  // first NaN of the segment (NaN sorts after every value)
+  while (lo_n < hi_n) {
+    const uint32_t mid = (lo_n + hi_n) / 2;
+    if (!isnan(S[order[mid]])) lo_n = mid + 1; else hi_n = mid;
+  }
+  const uint32_t c = lo_n - b;
   double Si = 0.0;
   if (c) {
     const uint32_t h = c / 2;
@@ -149,6 +154,106 @@ __global__ void k_score_ops(const uint32_t* __restrict__ score_key, const double
   }
   uint64_t Ulo = 0, Uhi = 0;
   if (lo < nops_trace && opt.id[lo] == op) { Ulo = opt.U[2 * lo]; Uhi = opt.U[2 * lo + 1]; }
+  r_op[u] = op;
+  r_U[2 * u] = Ulo;
+  r_U[2 * u + 1] = Uhi;
+  r_S[u] = Si;
+}
+
+// Operator keys of the scored units in input order, and the identity order.
+__global__ void k_score_opiota(const uint32_t* __restrict__ score_key, uint64_t n, uint64_t* __restrict__ k_op,
+                               uint32_t* __restrict__ idx) {
+  const uint64_t j = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  k_op[j] = score_key[j] >> 16;
+  idx[j] = (uint32_t)j;
+}
+
+// Longest operator segment (starts[0..nseg], nseg = scan[n-1] + flags[n-1]).
+__global__ void k_seg_maxlen(const uint32_t* __restrict__ flags, const uint32_t* __restrict__ scan, uint64_t n,
+                             const uint32_t* __restrict__ starts, uint32_t* __restrict__ out) {
+  const uint32_t nseg = scan[n - 1] + flags[n - 1];
+  uint32_t mx = 0;
+  for (uint64_t u = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; u < nseg; u += (uint64_t)gridDim.x * blockDim.x)
+    mx = max(mx, starts[u + 1] - starts[u]);
+  for (int d = 32; d >= 1; d >>= 1) mx = max(mx, (uint32_t)__shfl_xor(mx, d, 64));
+  if ((threadIdx.x & 63) == 0 && mx) atomicMax(out, mx);
+}
+
+// One workgroup per operator segment of at most kScoreSegMax units (N2 = a
+// power of two at least the longest segment): the segment's keys and S bit
+// patterns (NaN last) are sorted in LDS; equal neighbouring keys are a
+// duplicate; the Eq. (5) median of the correct S_j (mean of the two middle
+// values for an even count, 0 when none) and U_i from the operator table of
+// the trace (absent: 0).
+__device__ __forceinline__ void lds_bitonic(uint64_t* v, uint32_t N2) {
+  for (uint32_t k = 2; k <= N2; k <<= 1)
+    for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+      for (uint32_t i = threadIdx.x; i < N2; i += blockDim.x) {
+        const uint32_t l = i ^ j;
+        if (l > i) {
+          const uint64_t x = v[i], y = v[l];
+          if ((x > y) == ((i & k) == 0)) {
+            v[i] = y;
+            v[l] = x;
+          }
+        }
+      }
+      __syncthreads();
+    }
+}
+
+__global__ __launch_bounds__(256) void k_score_seg(const uint32_t* __restrict__ score_key, const double* __restrict__ S,
+                                                   const uint32_t* __restrict__ order,
+                                                   const uint32_t* __restrict__ starts, uint32_t N2, UnitTable opt,
+                                                   uint64_t nops_trace, uint32_t* __restrict__ r_op,
+                                                   uint64_t* __restrict__ r_U, double* __restrict__ r_S,
+                                                   uint32_t* __restrict__ err) {
+  extern __shared__ uint64_t sm64[];
+  uint64_t* sk = sm64;       // [N2] keys, padding ~0
+  uint64_t* sv = sm64 + N2;  // [N2] S bit patterns (S > 0: bit order = value order), NaN and padding ~0
+  __shared__ uint32_t s_dup;
+  const uint32_t u = blockIdx.x, tid = threadIdx.x;
+  const uint32_t b = starts[u], m = starts[u + 1] - b;
+  if (tid == 0) s_dup = 0;
+  for (uint32_t i = tid; i < N2; i += blockDim.x) {
+    uint64_t kk = ~0ull, vv = ~0ull;
+    if (i < m) {
+      const uint32_t j = order[b + i];
+      kk = score_key[j];
+      const double x = S[j];
+      vv = isnan(x) ? ~0ull : (uint64_t)__double_as_longlong(x);
+    }
+    sk[i] = kk;
+    sv[i] = vv;
+  }
+  __syncthreads();
+  lds_bitonic(sk, N2);
+  lds_bitonic(sv, N2);
+  bool dup = false;
+  for (uint32_t i = tid; i + 1 < m; i += blockDim.x) dup |= sk[i] == sk[i + 1];
+  if (dup) s_dup = 1u;
+  __syncthreads();
+  if (tid != 0) return;
+  if (s_dup) atomicOr(err, ATREX_ERRBIT_DUP);
+  uint32_t lo = 0, hi = m;  // correct S_j: the entries before the first ~0
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi) / 2;
+    if (sv[mid] != ~0ull) lo = mid + 1; else hi = mid;
+  }
+  const uint32_t c = lo, h = c / 2;
+  double Si = 0.0;
+  if (c)
+    Si = (c & 1) ? __longlong_as_double((long long)sv[h])
+                 : (__longlong_as_double((long long)sv[h - 1]) + __longlong_as_double((long long)sv[h])) / 2.0;
+  const uint32_t op = (uint32_t)(sk[0] >> 16);
+  uint64_t x = 0, y = nops_trace;  // the operator's row of the Eq. (3) table
+  while (x < y) {
+    const uint64_t mid = (x + y) / 2;
+    if (opt.id[mid] < op) x = mid + 1; else y = mid;
+  }
+  uint64_t Ulo = 0, Uhi = 0;
+  if (x < nops_trace && opt.id[x] == op) { Ulo = opt.U[2 * x]; Uhi = opt.U[2 * x + 1]; }
   r_op[u] = op;
   r_U[2 * u] = Ulo;
   r_U[2 * u + 1] = Uhi;
@@ -266,10 +371,34 @@ void launch_score_ops(hipStream_t s, const uint32_t* score_key, const double* S,
                        nops_trace, r_op, r_U, r_S);
 }
 
+void launch_score_opiota(hipStream_t s, const uint32_t* score_key, uint64_t n, uint64_t* k_op, uint32_t* idx) {
+  hipLaunchKernelGGL(k_score_opiota, dim3(grid_for(n, 256)), dim3(256), 0, s, score_key, n, k_op, idx);
+}
+
+void launch_seg_maxlen(hipStream_t s, const uint32_t* flags, const uint32_t* scan, uint64_t n, const uint32_t* starts,
+                       uint32_t* out) {
+  hipLaunchKernelGGL(k_seg_maxlen, dim3(256), dim3(256), 0, s, flags, scan, n, starts, out);
+}
+
+void launch_score_seg(hipStream_t s, const uint32_t* score_key, const double* S, const uint32_t* order,
+                      const uint32_t* starts, uint64_t nseg, uint32_t maxlen, const UnitTable& opt, uint64_t nops_trace,
+                      uint32_t* r_op, uint64_t* r_U, double* r_S, uint32_t* err) {
+  uint32_t N2 = 1;
+  while (N2 < maxlen) N2 <<= 1;
+  if (nseg)
+    hipLaunchKernelGGL(k_score_seg, dim3((uint32_t)nseg), dim3(256), (size_t)N2 * 16, s, score_key, S, order, starts,
+                       N2, opt, nops_trace, r_op, r_U, r_S, err);
+}
+
 void launch_score_final(hipStream_t s, const uint32_t* r_op, const uint64_t* r_U, const double* r_S, uint64_t nops,
                         const uint64_t* totalU, uint32_t* op, double* op_weight, double* op_score, double* s_agg,
                         uint32_t* err) {
   (void)err;
   hipLaunchKernelGGL(k_score_final, dim3(1), dim3(1024), 0, s, r_op, r_U, r_S, nops, totalU, op, op_weight, op_score,
                      s_agg);
+}
+
+hipError_t set_normalize_smem_limits() {
+  return hipFuncSetAttribute((const void*)k_score_seg, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (int)(kScoreSegMax * 16));
 }
