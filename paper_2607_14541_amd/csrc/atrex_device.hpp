@@ -183,6 +183,72 @@ __device__ __forceinline__ void acc_add_plain(Ptr lo, Ptr hi, u128 v) {
   if (vhi) atomicAdd(hi, vhi);
 }
 
+// --- hot entries in registers --------------------------------------------------
+// Up to two accumulator entries (a slot and phase of an LDS table) that most
+// lanes of a wave hit, chosen once from the wave's first step (at least
+// `min_lanes` of its 64 lanes on one entry).  A record of a hot entry is added
+// to per-lane registers instead of by two LDS atomics; flush() sums the lanes
+// once and hands each entry's total to the caller in lane 0.
+template <bool RAW>
+struct HotPair {
+  static constexpr uint32_t NONE = 0xFFFFFFFFu;
+  uint32_t ga, gb;  // wave-uniform entries (NONE: unused)
+  u128 va, vb;      // share sums
+  u128 ra, rb;      // raw time sums (RAW)
+  uint32_t ca, cb;  // invocation counts
+  __device__ __forceinline__ void reset() {
+    ga = gb = NONE;
+    va = vb = ra = rb = 0;
+    ca = cb = 0;
+  }
+  __device__ __forceinline__ void choose(uint32_t gi, uint32_t min_lanes) {
+    const uint64_t act = __ballot(gi != NONE);
+    if (act == 0) return;
+    const uint32_t l1 = __builtin_amdgcn_readlane(gi, __ffsll((unsigned long long)act) - 1);
+    const uint64_t s1 = __ballot(gi == l1);
+    uint32_t a = NONE, b = NONE;
+    if ((uint32_t)__popcll(s1) >= min_lanes) a = l1;
+    const uint64_t rest = act & ~s1;
+    if (rest) {
+      const uint32_t l2 = __builtin_amdgcn_readlane(gi, __ffsll((unsigned long long)rest) - 1);
+      if ((uint32_t)__popcll(__ballot(gi == l2)) >= min_lanes) {
+        if (a == NONE) a = l2; else b = l2;
+      }
+    }
+    ga = __builtin_amdgcn_readfirstlane(a);
+    gb = __builtin_amdgcn_readfirstlane(b);
+  }
+  // adds the record and returns true when gi is a hot entry
+  __device__ __forceinline__ bool take(uint32_t gi, uint64_t lo, uint64_t hi, uint64_t d) {
+    if (ga == NONE) return false;  // wave-uniform
+    const bool a = gi == ga, b = gb != NONE && gi == gb;
+    const u128 v = make_u128(lo, hi);
+    va += a ? v : (u128)0;
+    vb += b ? v : (u128)0;
+    ca += a ? 1u : 0u;
+    cb += b ? 1u : 0u;
+    if (RAW) {
+      ra += a ? (u128)d : (u128)0;
+      rb += b ? (u128)d : (u128)0;
+    }
+    return a || b;
+  }
+  // add(entry, share total, count, raw total) is called in lane 0 per used entry
+  template <class F>
+  __device__ __forceinline__ void flush(F add) {
+    if (ga == NONE) return;  // wave-uniform
+    for (int e = 0; e < 2; ++e) {
+      const uint32_t g = e ? gb : ga;
+      if (g == NONE) continue;
+      const u128 tv = wave_sum_u128(e ? vb : va);
+      const u128 tr = RAW ? wave_sum_u128(e ? rb : ra) : (u128)0;
+      uint32_t c = e ? cb : ca;
+      for (int d = 32; d >= 1; d >>= 1) c += __shfl_down(c, d, 64);
+      if ((threadIdx.x & 63) == 0 && c) add(g, tv, c, tr);
+    }
+  }
+};
+
 // --- streaming event loads ----------------------------------------------------
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 typedef long long v2l __attribute__((ext_vector_type(2)));

@@ -762,7 +762,8 @@ __global__ __launch_bounds__(1024) void k_part_items(const uint32_t* __restrict_
 // tags (the record's low hash bits; with the bucket they give the key back
 // through the inverse mix) and per phase a two-word accumulator, plus 64
 // per-lane dummy entries for lanes with nothing to add; four records per lane
-// per step; a wave whose lanes mostly hit one (slot, phase) sums them first.
+// per step; the (at most two) entries most of a wave hits are summed in
+// registers (HotPair) and added once at the end of the item.
 template <bool RAW>
 __global__ __launch_bounds__(1024) void k_part_aggregate(const uint64_t* __restrict__ rec,
                                                          const uint64_t* __restrict__ rraw, uint32_t BB, uint32_t CH,
@@ -819,6 +820,9 @@ __global__ __launch_bounds__(1024) void k_part_aggregate(const uint64_t* __restr
     __syncthreads();
     // four records per lane per step; the next step's records are loaded
     // while this step accumulates (indices clamped into the item)
+    HotPair<RAW> hot;
+    hot.reset();
+    bool first = true;
     v2l nr[4];
     uint64_t nd[4];
 #pragma unroll
@@ -881,41 +885,14 @@ __global__ __launch_bounds__(1024) void k_part_aggregate(const uint64_t* __restr
                      d[j], 0, err);
         }
       }
-      // one (slot, phase) for most of the wave: sum those lanes first
-      {
-        const uint64_t act = __ballot(gi[0] != 0xFFFFFFFFu);
-        if (act) {
-          const uint32_t fl = __ffsll((unsigned long long)act) - 1;
-          const uint32_t lead0 = __builtin_amdgcn_readlane(gi[0], fl);
-          if (__popcll(__ballot(gi[0] == lead0)) >= 32) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const uint64_t a2 = __ballot(gi[j] != 0xFFFFFFFFu);
-              if (a2 == 0) continue;
-              const uint32_t f2 = __ffsll((unsigned long long)a2) - 1;
-              const uint32_t lead = __builtin_amdgcn_readlane(gi[j], f2);
-              const uint64_t same = __ballot(gi[j] == lead);
-              if (__popcll(same) < 16) continue;
-              const bool mine = gi[j] == lead;
-              const u128 tot = wave_sum_u128(mine ? make_u128(vlo[j], vhi[j]) : (u128)0);
-              u128 rtot = 0;
-              if (RAW) rtot = wave_sum_u128(mine ? (u128)d[j] : (u128)0);
-              const uint64_t tlo = __shfl((unsigned long long)(uint64_t)tot, 0, 64);
-              const uint64_t thi = __shfl((unsigned long long)(uint64_t)(tot >> 64), 0, 64);
-              uint64_t rl = 0, rh = 0;
-              if (RAW) {
-                rl = __shfl((unsigned long long)(uint64_t)rtot, 0, 64);
-                rh = __shfl((unsigned long long)(uint64_t)(rtot >> 64), 0, 64);
-              }
-              if (lane == f2) {
-                acc_add_n(&acc[2 * lead], &acc[2 * lead + 1], make_u128(tlo, thi), (uint32_t)__popcll(same));
-                if (RAW) acc_add_plain(&racc[2 * lead], &racc[2 * lead + 1], make_u128(rl, rh));
-              }
-              if (mine) gi[j] = 0xFFFFFFFFu;
-            }
-          }
-        }
+      // entries most of the wave hits are summed in registers
+      if (first) {
+        hot.choose(gi[0], 16);
+        first = false;
       }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (hot.take(gi[j], vlo[j], vhi[j], d[j])) gi[j] = 0xFFFFFFFFu;
       uint32_t at[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) at[j] = gi[j] != 0xFFFFFFFFu ? 2 * gi[j] : dummy;
@@ -934,6 +911,10 @@ __global__ __launch_bounds__(1024) void k_part_aggregate(const uint64_t* __restr
           if (old[j] + d[j] < old[j]) atomicAdd(&racc[at[j] + 1], 1ull);
       }
     }
+    hot.flush([&](uint32_t g, u128 tv, uint32_t c, u128 tr) {
+      acc_add_n(&acc[2 * g], &acc[2 * g + 1], tv, c);
+      if (RAW) acc_add_plain(&racc[2 * g], &racc[2 * g + 1], tr);
+    });
     __syncthreads();
     // the item's rows: each thread takes a contiguous run of (slot, phase)
     // entries; one row-list reservation per workgroup
