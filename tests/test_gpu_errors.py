@@ -89,3 +89,30 @@ def test_capacity_error():
         ag.aggregate(k, z, torch.zeros(n, dtype=torch.uint8, device="cuda"), torch.ones(n, dtype=torch.int64, device="cuda"))
     assert e.value.status == X.E_CAPACITY
     ag.close()
+
+
+@pytest.mark.parametrize("bad", ["app", "phase", "duration"])
+@pytest.mark.parametrize("where", [0, 77777, 199999])
+def test_event_range_errors_range_split_pass_a(bad, where):
+    """30000 apps x 2 phases do not fit one LDS table: pass A is split into
+    ranges of the (app, phase) table, and the first range's workgroups
+    validate every event."""
+    rng = np.random.default_rng(where)
+    n, A, P = 200000, 30000, 2
+    key = rng.integers(0, 50, n).astype(np.uint32)
+    app = rng.integers(0, A, n).astype(np.uint32)
+    ph = rng.integers(0, P, n).astype(np.uint8)
+    dur = rng.integers(1, 10 ** 6, n).astype(np.int64)
+    c = rng.integers(1, 1000, A).astype(np.uint32)
+    if bad == "app":
+        app[where] = A + 3
+    elif bad == "phase":
+        ph[where] = P
+    else:
+        dur[where] = -1
+    H.say("range error, range-split pass A", bad, where)
+    o = O.status_of(key, app, ph, dur, c, P)
+    assert o == O.E_OUT_OF_RANGE
+    assert status(key, app, ph, dur, c, P) == o
+    app[where], ph[where], dur[where] = 1, 0, 5  # the repaired trace aggregates
+    assert status(key, app, ph, dur, c, P) == X.OK
