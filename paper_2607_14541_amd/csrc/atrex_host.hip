@@ -440,8 +440,10 @@ atrex_status run_partition(atrex_ctx* c, const EventsDev& d, const uint64_t* sca
   // buckets: at least 256 (work for every CU even with one chunk per bucket;
   // few buckets keep the scatter's runs long) and about half an LDS table of
   // keys per bucket
+  // (with raw time the scatter's LDS tile leaves room for 2^11 buckets)
+  const uint32_t maxBB = c->p.raw ? kMaxBucketBits - 1 : kMaxBucketBits;
   uint32_t BB = 8;
-  while (BB < kMaxBucketBits && ((keys_est + (1ull << BB) - 1) >> BB) > L.tabSlots / 2) ++BB;
+  while (BB < maxBB && ((keys_est + (1ull << BB) - 1) >> BB) > L.tabSlots / 2) ++BB;
   PartSource src;
   src.ev = d;
   src.per = ((d.n + nwg - 1) / nwg + 3) / 4 * 4;

@@ -579,10 +579,14 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint3
   uint64_t* s_raw = s_rec + 2 * SC_TILE;                   // [SC_TILE] RAW only
   uint16_t* s_bkt = (uint16_t*)(s_raw + (RAW ? SC_TILE : 0));  // [SC_TILE]
   uint32_t* s_cur = (uint32_t*)(s_bkt + SC_TILE);          // [NB] this workgroup's next record per bucket
-  uint32_t* s_cnt = s_cur + NB;                            // [NB] records of the tile per bucket
-  uint32_t* s_off = s_cnt + NB;                            // [NB] tile offsets
+  uint32_t* s_cnt = s_cur + NB;                            // [2][NB] records of the tile per bucket (by tile parity)
+  uint32_t* s_off = s_cnt + 2 * NB;                        // [NB] tile offsets
   __shared__ uint32_t s_w[NWV];
-  for (uint32_t i = tid; i < NB; i += SC_BLOCK) s_cur[i] = O[(size_t)i * nw + w];
+  for (uint32_t i = tid; i < NB; i += SC_BLOCK) {
+    s_cur[i] = O[(size_t)i * nw + w];
+    s_cnt[i] = 0;
+    s_cnt[NB + i] = 0;
+  }
   uint64_t b, e;
   part_range(src, w, b, e);
   const uint32_t lowbits = 32 - BB;
@@ -596,12 +600,21 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint3
 #pragma unroll
     for (uint32_t g = 0; g < G4; ++g) load_group(src.ev, b + 4 * ((uint64_t)g * SC_BLOCK + tid), e, nxt[g]);
   }
-  for (uint64_t t0 = b; t0 < e; t0 += SC_TILE) {  // uniform trip count
+  // Four barriers per tile: the counters are double-buffered (the next
+  // tile's are cleared during this tile's scan) and each bucket's position
+  // moves on by the previous tile's count during the scan, so nothing follows
+  // the write-out.
+  constexpr uint32_t PERMAX = 4;  // buckets per thread in the scan (NB <= 4 * SC_BLOCK)
+  const uint32_t per = (NB + SC_BLOCK - 1) / SC_BLOCK, b0 = tid * per;
+  uint32_t prevcnt[PERMAX] = {0, 0, 0, 0};
+  uint32_t parity = 0;
+  __syncthreads();
+  for (uint64_t t0 = b; t0 < e; t0 += SC_TILE, parity ^= 1u) {  // uniform trip count
     Ev4 evg[G4];
 #pragma unroll
     for (uint32_t g = 0; g < G4; ++g) evg[g] = nxt[g];
-    for (uint32_t i = tid; i < NB; i += SC_BLOCK) s_cnt[i] = 0;
-    __syncthreads();
+    uint32_t* cnt = s_cnt + parity * NB;
+    uint32_t* cnt_next = s_cnt + (parity ^ 1u) * NB;
     // phase 1: validity, bucket and rank of every record; the scale words
     // are requested here and used after the scan
     uint32_t hh[SC_EPT], rk[SC_EPT];  // hash; rank << 4 | exists << 3 | phase
@@ -632,13 +645,22 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint3
       hh[j] = hash32(key);
     }
 #pragma unroll
-    for (uint32_t j = 0; j < SC_EPT; ++j) rk[j] |= count_in(s_cnt, hh[j] >> lowbits, (rk[j] >> 3) & 1u) << 4;
+    for (uint32_t j = 0; j < SC_EPT; ++j) rk[j] |= count_in(cnt, hh[j] >> lowbits, (rk[j] >> 3) & 1u) << 4;
     __syncthreads();
-    // exclusive scan of the tile's bucket counts
+    // exclusive scan of the tile's bucket counts; the previous tile's counts
+    // advance the positions, and the next tile's counters are cleared
     {
-      const uint32_t per = (NB + SC_BLOCK - 1) / SC_BLOCK, b0 = tid * per;
       uint32_t sum = 0;
-      for (uint32_t k = 0; k < per; ++k) sum += (b0 + k < NB) ? s_cnt[b0 + k] : 0;
+#pragma unroll
+      for (uint32_t k = 0; k < PERMAX; ++k) {
+        if (k < per && b0 + k < NB) {
+          const uint32_t c = cnt[b0 + k];
+          s_cur[b0 + k] += prevcnt[k];
+          prevcnt[k] = c;
+          cnt_next[b0 + k] = 0;
+          sum += c;
+        }
+      }
       const uint32_t lane = tid & 63, wave = tid >> 6;
       uint32_t inc = sum;
       for (int dd = 1; dd < 64; dd <<= 1) {
@@ -650,8 +672,9 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint3
       uint32_t off = 0;
       for (uint32_t x = 0; x < wave; ++x) off += s_w[x];
       uint32_t run = off + inc - sum;
-      for (uint32_t k = 0; k < per; ++k)
-        if (b0 + k < NB) { s_off[b0 + k] = run; run += s_cnt[b0 + k]; }
+#pragma unroll
+      for (uint32_t k = 0; k < PERMAX; ++k)
+        if (k < per && b0 + k < NB) { s_off[b0 + k] = run; run += prevcnt[k]; }
     }
     __syncthreads();
     // phase 2: the Q96 share of every record, placed in LDS in bucket order
@@ -707,8 +730,6 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint3
       __builtin_nontemporal_store(r, (v2l*)(rec + 2 * pos));
       if (RAW) rraw[pos] = s_raw[k];
     }
-    __syncthreads();
-    for (uint32_t i = tid; i < NB; i += SC_BLOCK) s_cur[i] += s_cnt[i];
   }
   if (__any(bad) && (tid & 63) == 0) atomicOr(err, ATREX_ERRBIT_RANGE);
 }
@@ -1008,7 +1029,7 @@ size_t lds_table_bytes(uint32_t P, bool raw, uint32_t S) {
 constexpr uint32_t kScatterEpt = 4, kScatterBlock = 1024;
 
 static size_t scatter_smem(uint32_t BB, bool raw) {
-  return (size_t)kScatterEpt * kScatterBlock * (16 + (raw ? 8 : 0) + 2) + ((size_t)3 << BB) * 4;
+  return (size_t)kScatterEpt * kScatterBlock * (16 + (raw ? 8 : 0) + 2) + ((size_t)4 << BB) * 4;
 }
 
 uint32_t part_scatter_wgs(uint32_t cus) { return std::min<uint32_t>(kMaxPartWG, cus); }
