@@ -727,7 +727,7 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint3
       v2l r;
       r.x = (long long)s_rec[2 * k];
       r.y = (long long)s_rec[2 * k + 1];
-      __builtin_nontemporal_store(r, (v2l*)(rec + 2 * pos));
+      *(v2l*)(rec + 2 * pos) = r;  // ordinary store: non-temporal ones ran ~1.5x slower on short runs
       if (RAW) rraw[pos] = s_raw[k];
     }
   }
