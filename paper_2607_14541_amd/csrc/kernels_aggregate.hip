@@ -168,12 +168,69 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A
       x.d1 = *(const v2l*)(ev.dur + i + 2);
     }
   };
+  // Four events without branches.  An event outside the range adds to a
+  // per-lane spare counter past the range, so the four LDS atomics issue back
+  // to back and are waited for once.  When every lane's four events are valid
+  // (the usual case, checked for the group at once: largest app, the phase
+  // bytes, the sign of the durations) the counter's byte offset and the range
+  // test need no per-event validity; otherwise the wave takes the per-event
+  // checks.  The high words and wrap-arounds go to ext[g] only when present.
+  const uint32_t gn = g1 - g0, lane = threadIdx.x & 63;
+  const uint32_t spare = GR + lane, spare4 = 4 * spare, gn4 = 4 * gn, P4 = 4 * P, g04 = 4 * g0;
+  const uint32_t pbytes = P * 0x01010101u;  // P in every byte (P <= 128)
   auto process = [&](uint64_t it, const G4& x) {
     if (it * BLOCK + threadIdx.x >= ng) return;
-    one(x.a.x, x.p & 0xFFu, x.d0.x);
-    one(x.a.y, (x.p >> 8) & 0xFFu, x.d0.y);
-    one(x.a.z, (x.p >> 16) & 0xFFu, x.d1.x);
-    one(x.a.w, x.p >> 24, x.d1.y);
+    const uint32_t av[4] = {x.a.x, x.a.y, x.a.z, x.a.w};
+    const int64_t dv[4] = {x.d0.x, x.d0.y, x.d1.x, x.d1.y};
+    uint32_t dhi[4], old[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dhi[j] = (uint32_t)((uint64_t)dv[j] >> 32);
+    // byte b of `pbad` has its top bit set iff phase byte b >= P (or >= 128)
+    const uint32_t pbad = (x.p | ((x.p | 0x80808080u) - pbytes)) & 0x80808080u;
+    const uint32_t amax = max(max(av[0], av[1]), max(av[2], av[3]));
+    const uint32_t hor = dhi[0] | dhi[1] | dhi[2] | dhi[3];
+    const bool valid = (amax < A) & (pbad == 0) & ((int32_t)hor >= 0);
+    if (__all(valid)) {
+      uint32_t rb[4];
+      bool in[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        // 4 (a P + ph - g0): a < A < 2^24 and 4 A P < 2^32
+        rb[j] = __umul24(av[j], P4) + ((((x.p >> (8 * j)) & 0xFFu) << 2) - g04);
+        in[j] = rb[j] < gn4;
+        rb[j] = in[j] ? rb[j] : spare4;
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) old[j] = atomicAdd((uint32_t*)((char*)s32 + rb[j]), (uint32_t)dv[j]);
+      bool cy = false;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) cy |= old[j] + (uint32_t)dv[j] < old[j];
+      if (__any(cy | (hor != 0)))
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t up = dhi[j] + ((old[j] + (uint32_t)dv[j] < old[j]) ? 1u : 0u);  // < 2^31 + 1
+          if (in[j] && up) atomicAdd(&ext[g0 + rb[j] / 4], (unsigned long long)up);
+        }
+      return;
+    }
+    uint32_t r[4], lo[4];
+    bool in[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t ph = (x.p >> (8 * j)) & 0xFFu;
+      const bool ok = (av[j] < A) & (ph < P) & ((int32_t)dhi[j] >= 0);  // bitwise: no branches
+      bad |= !ok;
+      r[j] = av[j] * P + ph - g0;  // position in the range when in[j]
+      in[j] = ok & (r[j] < gn);
+      lo[j] = in[j] ? (uint32_t)dv[j] : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) old[j] = atomicAdd(&s32[in[j] ? r[j] : spare], lo[j]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t up = dhi[j] + ((old[j] + lo[j] < old[j]) ? 1u : 0u);  // d >= 0: high word < 2^31
+      if (in[j] && up) atomicAdd(&ext[g0 + r[j]], (unsigned long long)up);
+    }
   };
   G4 x0, x1, x2;
   if (0 < iters) load(0, x0);
@@ -887,7 +944,7 @@ void launch_pass_a_range(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_
                          uint32_t slices, uint32_t* partial, unsigned long long* ext, uint32_t* err) {
   const uint32_t G = A * P;
   const uint32_t nblocks = ((slices + 7) / 8) * 8 * R;
-  hipLaunchKernelGGL((k_pass_a_range<1024>), dim3(nblocks), dim3(1024), (size_t)GR * 4, s, ev, A, P, G, GR, R, slices,
+  hipLaunchKernelGGL((k_pass_a_range<1024>), dim3(nblocks), dim3(1024), ((size_t)GR + 64) * 4, s, ev, A, P, G, GR, R, slices,
                      partial, ext, err);
 }
 

@@ -95,8 +95,8 @@ def test_capacity_error():
 @pytest.mark.parametrize("where", [0, 77777, 199999])
 def test_event_range_errors_range_split_pass_a(bad, where):
     """30000 apps x 2 phases do not fit one LDS table: pass A is split into
-    ranges of the (app, phase) table, and the first range's workgroups
-    validate every event."""
+    ranges of the (app, phase) table; a wave that meets an invalid event
+    checks its events one by one, in every range's workgroups."""
     rng = np.random.default_rng(where)
     n, A, P = 200000, 30000, 2
     key = rng.integers(0, 50, n).astype(np.uint32)

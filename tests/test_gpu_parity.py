@@ -135,3 +135,28 @@ def test_group_count_boundaries(path, G):
     g = H.run_gpu(key, app, ph, dur, c, P, path=path, max_groups=G, max_keys=nk)
     assert g["num_groups"] == G
     H.compare(g, O.run(key, app, ph, dur, c, P))
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_range_split_pass_a_wraps_and_high_words(seed):
+    """100000 apps x 3 phases: pass A runs in ranges of the (app, phase)
+    table with 32-bit LDS counters.  A third of the events land on one
+    (app, phase) with durations near 2^31 (the 32-bit counter wraps every
+    few events) and a tenth carry durations up to 2^40 (high words), spread
+    over every range; the tail of the trace is ragged (n not a multiple of 4)."""
+    rng = np.random.default_rng(100 + seed)
+    n, A, P = (1 << 20) + 3, 100000, 3
+    key = rng.integers(0, 4096, n).astype(np.uint32)
+    app = rng.integers(0, A, n).astype(np.uint32)
+    ph = rng.integers(0, P, n).astype(np.uint8)
+    dur = rng.lognormal(math.log(3e4), 2.0, n).astype(np.int64)
+    hot = rng.random(n) < 1 / 3
+    app[hot], ph[hot] = 77777, 1
+    dur[hot] = rng.integers(1 << 30, 1 << 31, int(hot.sum()))
+    big = rng.random(n) < 0.1
+    dur[big] = rng.integers(1 << 32, 1 << 40, int(big.sum()))
+    c = rng.integers(1, 1000, A).astype(np.uint32)
+    H.say("range-split pass A, wraps and high words, seed", seed)
+    g = H.run_gpu(key, app, ph, dur, c, P, max_groups=2 * n, max_keys=n)
+    o = O.run(key, app, ph, dur, c, P)
+    H.compare(g, o)
