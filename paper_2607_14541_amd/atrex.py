@@ -106,6 +106,11 @@ def _dev(t: torch.Tensor, dtype: torch.dtype, name: str) -> torch.Tensor:
     return t.contiguous()
 
 
+def _same_items(d: dict, items: tuple) -> bool:
+    """d still maps the same keys to the same objects as `items`."""
+    return len(d) == len(items) and all(d.get(k) is v for k, v in items)
+
+
 def _as_i32(t: torch.Tensor) -> torch.Tensor:
     """uint32 data as int32 bits."""
     if t.dtype == torch.int32:
@@ -146,6 +151,10 @@ class Aggregator:
         self._ctx = ctx
         self.num_groups = None
         self.num_ops = self.num_keys = None
+        # marshalled arguments of the last normalize()/score() call, reused
+        # while the caller passes the same output tensors (and sizes) again
+        self._gcache = None
+        self._scache = None
 
     # -- Eq. (2)-(3) group-by ---------------------------------------------------------
     def aggregate(self, key: torch.Tensor, app: torch.Tensor, phase: torch.Tensor,
@@ -188,15 +197,19 @@ class Aggregator:
         G = self.num_groups
         if out is None:
             out = self.group_buffers(G)
-        elif out["key"].numel() < G:
-            raise ValueError("output buffers hold %d groups, need %d" % (out["key"].numel(), G))
-        g = _Groups(_ptr(out["key"]), _ptr(out["phase"]), _ptr(out["count"]), _ptr(out["wsum"]),
-                    _ptr(out["weight"]), _ptr(out["phase_total"]), _ptr(out.get("raw_ns")))
+        c = self._gcache
+        if c is None or c[0] is not out or c[1] != G or not _same_items(out, c[2]):
+            if out["key"].numel() < G:
+                raise ValueError("output buffers hold %d groups, need %d" % (out["key"].numel(), G))
+            g = _Groups(_ptr(out["key"]), _ptr(out["phase"]), _ptr(out["count"]), _ptr(out["wsum"]),
+                        _ptr(out["weight"]), _ptr(out["phase_total"]), _ptr(out.get("raw_ns")))
+            views = {k: (v if k == "phase_total" else v[:G]) for k, v in out.items()}
+            c = self._gcache = (out, G, tuple(out.items()), g, views)
         nops, nkeys = ctypes.c_uint64(), ctypes.c_uint64()
-        _check(_lib().atrex_phase_normalize(self._ctx, ctypes.byref(g), ctypes.byref(nops),
+        _check(_lib().atrex_phase_normalize(self._ctx, ctypes.byref(c[3]), ctypes.byref(nops),
                                             ctypes.byref(nkeys)), "atrex_phase_normalize")
         self.num_ops, self.num_keys = nops.value, nkeys.value
-        return {k: (v if k == "phase_total" else v[:G]) for k, v in out.items()}
+        return dict(c[4])
 
     def op_weights(self) -> dict:
         k, dev = self.num_ops, self.device
@@ -226,16 +239,20 @@ class Aggregator:
             out = dict(op=torch.empty(max(n, 1), dtype=torch.int32, device=dev),
                        op_weight=torch.empty(max(n, 1), dtype=torch.float64, device=dev),
                        op_score=torch.empty(max(n, 1), dtype=torch.float64, device=dev))
-        op, ow, osc = out["op"], out["op_weight"], out["op_score"]
-        if op.numel() < n or ow.numel() < n or osc.numel() < n:
-            raise ValueError("score output buffers too small")
+        c = self._scache
+        if c is None or c[0] is not out or c[1] != n or not _same_items(out, c[2]):
+            op, ow, osc = out["op"], out["op_weight"], out["op_score"]
+            if op.numel() < n or ow.numel() < n or osc.numel() < n:
+                raise ValueError("score output buffers too small")
+            c = self._scache = [out, n, tuple(out.items()), (_ptr(op), _ptr(ow), _ptr(osc)), None]
         nops = ctypes.c_uint64()
         sagg = ctypes.c_double()
-        _check(_lib().atrex_weighted_score(self._ctx, _ptr(score_key), _ptr(s), n, _ptr(op), _ptr(ow),
-                                           _ptr(osc), ctypes.byref(nops), ctypes.byref(sagg)),
-               "atrex_weighted_score")
+        _check(_lib().atrex_weighted_score(self._ctx, _ptr(score_key), _ptr(s), n, *c[3], ctypes.byref(nops),
+                                           ctypes.byref(sagg)), "atrex_weighted_score")
         k = nops.value
-        return dict(s_agg=sagg.value, op=op[:k], op_weight=ow[:k], op_score=osc[:k])
+        if c[4] is None or c[4][0] != k:  # views of the first k entries
+            c[4] = (k, out["op"][:k], out["op_weight"][:k], out["op_score"][:k])
+        return dict(s_agg=sagg.value, op=c[4][1], op_weight=c[4][2], op_score=c[4][3])
 
     # -- inspection ------------------------------------------------------------------------
     def app_totals(self) -> dict:

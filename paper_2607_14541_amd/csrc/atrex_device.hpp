@@ -100,20 +100,18 @@ __device__ __forceinline__ void bscale_share64(uint64_t d, uint32_t elo, uint32_
 }
 
 // --- u128 -> fp64, round to nearest, ties to even (IEEE 754 conversion) -----
+// The top 64 bits from the leading one on, with a sticky bit for any nonzero
+// bit below them, round to the same double as x; that u64 is converted as
+// (high word) 2^32 + (low word): both terms are exact, so the one addition is
+// the only rounding.  The power-of-two scaling is exact.
 __device__ __forceinline__ double u128_to_f64(u128 x) {
-  const uint64_t hi = (uint64_t)(x >> 64);
-  if (hi == 0) {
-    const uint64_t lo = (uint64_t)x;
-    if ((lo >> 53) == 0) return (double)lo;  // exact
-  }
-  // leading one at bit (nb - 1), nb > 53: keep 53 bits, round the rest.
-  const int nb = hi ? 128 - __clzll(hi) : 64 - __clzll((uint64_t)x);
-  const int sh = nb - 53;
-  uint64_t mant = (uint64_t)(x >> sh);
-  const u128 rem = x & (((u128)1 << sh) - 1);
-  const u128 half = (u128)1 << (sh - 1);
-  if (rem > half || (rem == half && (mant & 1))) ++mant;
-  return ldexp((double)mant, sh);  // mant <= 2^53: exact, then exact scaling
+  const uint64_t hi = (uint64_t)(x >> 64), lo = (uint64_t)x;
+  const int s = hi ? __clzll(hi) : 0;
+  const uint64_t top = s ? (hi << s) | (lo >> (64 - s)) : hi;
+  const uint64_t below = s ? lo << s : lo;
+  const uint64_t t = hi ? top | (below != 0 ? 1u : 0u) : lo;
+  const double r = ldexp((double)(uint32_t)(t >> 32), 32) + (double)(uint32_t)t;
+  return hi ? ldexp(r, 64 - s) : r;
 }
 
 // --- hashing ----------------------------------------------------------------

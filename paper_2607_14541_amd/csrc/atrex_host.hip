@@ -248,6 +248,8 @@ struct atrex_ctx {
   char* pinned = nullptr;
   uint32_t* pinned_dev = nullptr;  // the same buffer as the device sees it
   size_t pinned_used = 0;
+  uint32_t publish_seq = 0;  // last value k_publish wrote to the completion word
+  bool plain_copies = false;  // a readback went through hipMemcpyAsync instead
   struct Pending {
     void* dst;
     const void* src;
@@ -385,22 +387,46 @@ atrex_status sync_status(atrex_ctx* c) {
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 constexpr size_t kPinnedBytes = 4096;
+constexpr size_t kDoneOff = kPinnedBytes - 64;  // completion word, on a line of its own
 
 // Device -> host readback of a few status words (a multiple of 4 bytes)
 // through the context's mapped pinned buffer; sync_read() launches the copy
-// and fills in the host values after the stream synchronisation.
+// and fills in the host values once it has completed.
 void d2h(atrex_ctx* c, void* dst, const void* src, size_t bytes) {
   size_t off = (c->pinned_used + 7) / 8 * 8;
-  if (!c->pinned_dev || off + bytes > kPinnedBytes || bytes % 4 != 0 || c->pending.size() >= kPublishMax) {
+  if (!c->pinned_dev || off + bytes > kDoneOff || bytes % 4 != 0 || c->pending.size() >= kPublishMax) {
     (void)hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, c->s);  // plain (pageable) copy
+    c->plain_copies = true;
     return;
   }
   c->pending.push_back({dst, src, off, bytes});
   c->pinned_used = off + bytes;
 }
 
+// Wait for k_publish's completion word to read `seq`: the stream's work up to
+// and including the copies is then done (a stream runs its launches in order).
+// The stream is queried every few hundred polls, so a device error or a
+// publish that never wrote ends the wait with ATREX_E_DEVICE.
+atrex_status wait_published(atrex_ctx* c, uint32_t seq) {
+  const uint32_t* done = (const uint32_t*)(c->pinned + kDoneOff);
+  for (uint32_t spin = 1;; ++spin) {
+    if (__atomic_load_n(done, __ATOMIC_ACQUIRE) == seq) return ATREX_OK;
+    if (spin % 256 == 0) {
+      const hipError_t q = hipStreamQuery(c->s);
+      if (q == hipSuccess) return __atomic_load_n(done, __ATOMIC_ACQUIRE) == seq ? ATREX_OK : ATREX_E_DEVICE;
+      if (q != hipErrorNotReady) return ATREX_E_DEVICE;
+    }
+    __builtin_ia32_pause();
+  }
+}
+
+// Ends a call's device work: copies the pending readbacks through one
+// k_publish launch and waits for it by polling its completion word (a stream
+// synchronisation wakes the host later); with timing on, or after a plain
+// copy, by a stream synchronisation.
 atrex_status sync_read(atrex_ctx* c) {
-  if (!c->pending.empty()) {
+  atrex_status st = ATREX_OK;
+  if (c->pinned_dev) {
     PublishList pl{};
     for (const auto& p : c->pending) {
       pl.src[pl.count] = (const uint32_t*)p.src;
@@ -408,12 +434,22 @@ atrex_status sync_read(atrex_ctx* c) {
       pl.n32[pl.count] = (uint32_t)(p.bytes / 4);
       ++pl.count;
     }
-    launch_publish(c->s, pl, c->pinned_dev);
+    if (++c->publish_seq == 0) c->publish_seq = 1;  // 0 is the buffer's initial value
+    launch_publish(c->s, pl, c->pinned_dev, c->pinned_dev + kDoneOff / 4, c->publish_seq);
+    const bool poll = !c->plain_copies && !(c->flags & ATREX_FLAG_TIMING);
+    if (hipGetLastError() != hipSuccess) {
+      (void)hipStreamSynchronize(c->s);
+      st = ATREX_E_DEVICE;
+    } else {
+      st = poll ? wait_published(c, c->publish_seq) : sync_status(c);
+    }
+  } else {
+    st = sync_status(c);
   }
-  const atrex_status st = sync_status(c);
   for (const auto& p : c->pending) memcpy(p.dst, c->pinned + p.off, p.bytes);
   c->pending.clear();
   c->pinned_used = 0;
+  c->plain_copies = false;
   return st;
 }
 
@@ -524,8 +560,10 @@ atrex_status atrex_aggregate_init(const atrex_init_params* ip, atrex_ctx** out) 
   c->ntimed = 0;
   if (hipHostMalloc((void**)&c->pinned, kPinnedBytes, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) {
     c->pinned = nullptr;
-  } else if (hipHostGetDevicePointer((void**)&c->pinned_dev, c->pinned, 0) != hipSuccess) {
-    c->pinned_dev = nullptr;  // readbacks fall back to plain copies
+  } else {
+    memset(c->pinned, 0, kPinnedBytes);  // the completion word starts at 0
+    if (hipHostGetDevicePointer((void**)&c->pinned_dev, c->pinned, 0) != hipSuccess)
+      c->pinned_dev = nullptr;  // readbacks fall back to plain copies
   }
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess ||

@@ -163,7 +163,9 @@ struct PublishList {
   uint32_t off32[kPublishMax], n32[kPublishMax];
   uint32_t count;
 };
-void launch_publish(hipStream_t s, const PublishList& pl, uint32_t* dst);
+// After the copies, `done` (host-mapped) receives `seq` with a system-scope
+// release, so a host that reads `seq` there (acquire) sees the copied words.
+void launch_publish(hipStream_t s, const PublishList& pl, uint32_t* dst, uint32_t* done, uint32_t seq);
 void launch_sum_u32(hipStream_t s, const uint32_t* x, uint64_t n, uint64_t* out);
 // LSD radix sort of (u64 key, u32 value) pairs on key bits [0, bits).  Stable.
 // tmp must hold radix_sort_tmp_bytes(n); results end in (k0, v0).

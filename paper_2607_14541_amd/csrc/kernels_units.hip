@@ -65,6 +65,13 @@ __device__ u128 tile_sum_u128(u128 v, uint64_t* s_lo, uint64_t* s_hi) {
   return s;
 }
 
+// L / k where k divides L (k = |Phi| in [1, P], L = lcm(1..P) <= 840): the
+// quotient is an integer below 2^10 and the fp32 product L * rcp(k) is within
+// 2^-21 relative of it, so rounding it to the nearest integer is exact.
+__device__ __forceinline__ uint32_t lcm_over(uint32_t L, uint32_t k) {
+  return (uint32_t)rintf((float)L * __builtin_amdgcn_rcpf((float)k));
+}
+
 __device__ __forceinline__ double ratio(u128 a, u128 b) { return b == 0 ? 0.0 : u128_to_f64(a) / u128_to_f64(b); }
 
 __global__ __launch_bounds__(TILE) void k_units_tiles(SortedGroups g, uint64_t G, uint32_t P, uint64_t L,
@@ -105,7 +112,7 @@ __global__ __launch_bounds__(TILE) void k_units_tiles(SortedGroups g, uint64_t G
       sum += load_u128(g.wsum, e);
       mask |= 1u << g.phase[e];
     }
-    Uk = (u128)((uint32_t)L / (uint32_t)__popc(mask)) * sum;
+    Uk = (u128)lcm_over((uint32_t)L, (uint32_t)__popc(mask)) * sum;
     store_u128(us.keyU, i, Uk);
   }
   uint32_t nkeys;
@@ -227,7 +234,7 @@ __global__ __launch_bounds__(TILE) void k_units_ops(uint32_t ntiles, uint32_t P,
     const uint64_t wlo = __hip_atomic_load(&ops.U[2 * q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint64_t whi = __hip_atomic_load(&ops.U[2 * q + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint32_t mask = __hip_atomic_load(&us.opMask[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const u128 U = (u128)((uint32_t)L / (uint32_t)__popc(mask)) * make_u128(wlo, whi);
+    const u128 U = (u128)lcm_over((uint32_t)L, (uint32_t)__popc(mask)) * make_u128(wlo, whi);
     store_u128(ops.U, q, U);
     sumU += U;
   }
@@ -285,9 +292,12 @@ __global__ __launch_bounds__(256) void k_group_weights(SortedGroups g, uint32_t 
 
 // ---------------------------------------------------------------------------
 // One workgroup for up to kUnitsSmallMax groups: thread t holds groups
-// [8t, 8t + 8) in registers; the key runs and operator runs are summed with
-// one block-wide segmented scan (operator: a run head restarts the sum), and
-// every run's total is taken at its last group.  Same outputs as the three
+// [8t, 8t + 8) in registers.  A key run has at most P <= 8 groups, so it
+// spans at most two threads: the run's part in the previous thread (that
+// thread's tail after its last key head) comes by one shuffle.  Operator runs
+// are summed with one block-wide segmented scan (a run head restarts the sum).
+// Each run's total is taken at its last group; the run indices come from one
+// block-wide count of the key and operator heads.  Same outputs as the three
 // launches above.
 constexpr uint32_t SM_PER = 8;
 
@@ -313,8 +323,9 @@ __global__ __launch_bounds__(TILE) void k_units_small(SortedGroups g, uint32_t G
                                                       uint64_t maxOps, UnitTable keys,
                                                       unsigned long long* __restrict__ counts,
                                                       uint32_t* __restrict__ err) {
-  __shared__ Seg s_kw[NW], s_ow[NW];
-  __shared__ uint32_t s_nk[NW], s_no[NW];
+  __shared__ Seg s_ow[NW];
+  __shared__ uint32_t s_n[NW];
+  __shared__ uint64_t s_kt[3 * NW];  // each wave's last key tail: sum (lo, hi), phase mask
   __shared__ uint64_t s_lo[NW], s_hi[NW];
   const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const uint32_t i0 = tid * SM_PER;
@@ -329,103 +340,111 @@ __global__ __launch_bounds__(TILE) void k_units_small(SortedGroups g, uint32_t G
     W[j] = i < G ? load_u128(g.wsum, i) : (u128)0;
   }
   const uint32_t kprev = (i0 > 0 && i0 <= G) ? g.key[i0 - 1] : 0u;
-  const bool has_next = i0 + SM_PER < G;
-  const uint32_t knext = has_next ? g.key[i0 + SM_PER] : 0u;
-  __syncthreads();
-  // heads of key runs and operator runs
-  uint32_t kh = 0, oh = 0;  // bit j: group j heads a run
+  const uint32_t knext = i0 + SM_PER < G ? g.key[i0 + SM_PER] : 0u;
+  // heads of key runs and operator runs (bit j: group j heads a run), and
+  // ends (bit j: group j is the last of its run)
+  uint32_t kh = 0, oh = 0, ke = 0, oe = 0;
 #pragma unroll
   for (int j = 0; j < SM_PER; ++j) {
     const uint32_t i = i0 + j;
+    if (i >= G) continue;
     const uint32_t prev = j == 0 ? kprev : key[j - 1];
-    if (i < G && (i == 0 || prev != key[j])) kh |= 1u << j;
-    if (i < G && (i == 0 || (prev >> 16) != (key[j] >> 16))) oh |= 1u << j;
+    const uint32_t nx = j + 1 < SM_PER ? key[j + 1] : knext;
+    const bool last = i + 1 == G;
+    if (i == 0 || prev != key[j]) kh |= 1u << j;
+    if (i == 0 || (prev >> 16) != (key[j] >> 16)) oh |= 1u << j;
+    if (last || nx != key[j]) ke |= 1u << j;
+    if (last || (nx >> 16) != (key[j] >> 16)) oe |= 1u << j;
   }
-  // this thread's aggregates, then the block-wide exclusive scan
-  Seg ka{0, 0, 0}, oa{0, 0, 0};
+  // key tail: W and phases after this thread's last key head (all its groups
+  // when it has none)
+  u128 ktv = 0;
+  uint32_t ktm = 0;
+  // operator aggregate of this thread, for the block-wide scan
+  Seg oa{0, 0, 0};
 #pragma unroll
   for (int j = 0; j < SM_PER; ++j) {
-    if (i0 + j < G) {
-      const Seg e{1u, W[j], 1u << ph[j]};
-      const Seg c{0u, W[j], 1u << ph[j]};
-      ka = seg_cat(ka, (kh >> j) & 1 ? e : c);
-      oa = seg_cat(oa, (oh >> j) & 1 ? e : c);
-    }
+    if (i0 + j >= G) continue;
+    const bool kf = (kh >> j) & 1, of = (oh >> j) & 1;
+    ktv = (kf ? (u128)0 : ktv) + W[j];
+    ktm = (kf ? 0u : ktm) | (1u << ph[j]);
+    oa = Seg{oa.f | (of ? 1u : 0u), (of ? (u128)0 : oa.v) + W[j], (of ? 0u : oa.m) | (1u << ph[j])};
   }
-  uint32_t nk = __popc(kh), no = __popc(oh);
-  Seg ki = ka, oi = oa;
-  uint32_t nki = nk, noi = no;
+  // counts of key heads (low 16 bits) and operator heads (high 16 bits)
+  const uint32_t cnt = __popc(kh) | (__popc(oh) << 16);
+  Seg oi = oa;
+  uint32_t ci = cnt;
   for (int d = 1; d < 64; d <<= 1) {
-    const Seg ky = seg_shfl_up(ki, d), oy = seg_shfl_up(oi, d);
-    const uint32_t nky = __shfl_up(nki, d, 64), noy = __shfl_up(noi, d, 64);
+    const Seg oy = seg_shfl_up(oi, d);
+    const uint32_t cy = __shfl_up(ci, d, 64);
     if (lane >= (uint32_t)d) {
-      ki = seg_cat(ky, ki);
       oi = seg_cat(oy, oi);
-      nki += nky;
-      noi += noy;
+      ci += cy;
     }
   }
+  // the previous thread's key tail (the previous wave's last lane through LDS)
+  u128 kin_v = shfl_up_u128(ktv, 1);
+  uint32_t kin_m = __shfl_up(ktm, 1, 64);
   if (lane == 63) {
-    s_kw[wave] = ki;
     s_ow[wave] = oi;
-    s_nk[wave] = nki;
-    s_no[wave] = noi;
+    s_n[wave] = ci;
+    s_kt[3 * wave] = (uint64_t)ktv;
+    s_kt[3 * wave + 1] = (uint64_t)(ktv >> 64);
+    s_kt[3 * wave + 2] = ktm;
   }
   __syncthreads();
-  Seg kc{0, 0, 0}, oc{0, 0, 0};  // carry into this wave
-  uint32_t nkc = 0, noc = 0, nkeys = 0, nops = 0;
+  if (lane == 0 && wave > 0) {
+    kin_v = make_u128(s_kt[3 * (wave - 1)], s_kt[3 * (wave - 1) + 1]);
+    kin_m = (uint32_t)s_kt[3 * (wave - 1) + 2];
+  }
+  Seg oc{0, 0, 0};  // operator carry into this thread
+  uint32_t cc = 0, ctot = 0;
   for (uint32_t w = 0; w < NW; ++w) {
     if (w < wave) {
-      kc = seg_cat(kc, s_kw[w]);
       oc = seg_cat(oc, s_ow[w]);
-      nkc += s_nk[w];
-      noc += s_no[w];
+      cc += s_n[w];
     }
-    nkeys += s_nk[w];
-    nops += s_no[w];
+    ctot += s_n[w];
   }
   {  // exclusive within the wave
-    const Seg ke = seg_shfl_up(ki, 1), oe = seg_shfl_up(oi, 1);
-    const uint32_t nke = __shfl_up(nki, 1, 64), noe = __shfl_up(noi, 1, 64);
+    const Seg oy = seg_shfl_up(oi, 1);
+    const uint32_t cy = __shfl_up(ci, 1, 64);
     if (lane > 0) {
-      kc = seg_cat(kc, ke);
-      oc = seg_cat(oc, oe);
-      nkc += nke;
-      noc += noe;
+      oc = seg_cat(oc, oy);
+      cc += cy;
     }
   }
+  const uint32_t nkeys = ctot & 0xFFFFu, nops = ctot >> 16;
   const bool ops_fit = nops <= maxOps;
   // runs ending in this thread: totals, U = (L / |Phi|) * sum W (Eq. (3))
   u128 sumUk = 0, sumU = 0;
   {
-    Seg kr = kc, orr = oc;
-    uint32_t kidx = nkc, oidx = noc;  // heads so far
+    u128 kv = kin_v;  // a run continued from the previous thread starts with its tail
+    uint32_t km = kin_m;
+    Seg orr = oc;
+    uint32_t kidx = cc & 0xFFFFu, oidx = cc >> 16;  // heads so far
 #pragma unroll
     for (int j = 0; j < SM_PER; ++j) {
-      const uint32_t i = i0 + j;
-      if (i < G) {
-        const Seg e{1u, W[j], 1u << ph[j]};
-        const Seg c{0u, W[j], 1u << ph[j]};
-        kr = seg_cat(kr, (kh >> j) & 1 ? e : c);
-        orr = seg_cat(orr, (oh >> j) & 1 ? e : c);
-        kidx += (kh >> j) & 1;
-        oidx += (oh >> j) & 1;
-        const bool last = i + 1 == G;
-        const uint32_t nx = j + 1 < SM_PER ? key[j + 1] : knext;
-        if (last || nx != key[j]) {
-          const u128 U = (u128)(L / (uint32_t)__popc(kr.m)) * kr.v;
-          keys.id[kidx - 1] = key[j];
-          store_u128(keys.U, kidx - 1, U);
-          sumUk += U;
+      if (i0 + j >= G) continue;
+      const bool kf = (kh >> j) & 1, of = (oh >> j) & 1;
+      kv = (kf ? (u128)0 : kv) + W[j];
+      km = (kf ? 0u : km) | (1u << ph[j]);
+      orr = Seg{1u, (of ? (u128)0 : orr.v) + W[j], (of ? 0u : orr.m) | (1u << ph[j])};
+      kidx += kf;
+      oidx += of;
+      if ((ke >> j) & 1) {
+        const u128 U = (u128)lcm_over(L, (uint32_t)__popc(km)) * kv;
+        keys.id[kidx - 1] = key[j];
+        store_u128(keys.U, kidx - 1, U);
+        sumUk += U;
+      }
+      if ((oe >> j) & 1) {
+        const u128 U = (u128)lcm_over(L, (uint32_t)__popc(orr.m)) * orr.v;
+        if (ops_fit) {
+          ops.id[oidx - 1] = key[j] >> 16;
+          store_u128(ops.U, oidx - 1, U);
         }
-        if (last || (nx >> 16) != (key[j] >> 16)) {
-          const u128 U = (u128)(L / (uint32_t)__popc(orr.m)) * orr.v;
-          if (ops_fit) {
-            ops.id[oidx - 1] = key[j] >> 16;
-            store_u128(ops.U, oidx - 1, U);
-          }
-          sumU += U;
-        }
+        sumU += U;
       }
     }
   }
@@ -433,19 +452,14 @@ __global__ __launch_bounds__(TILE) void k_units_small(SortedGroups g, uint32_t G
   const u128 totUk = tile_sum_u128(sumUk, s_lo, s_hi);
   // w_i = RN(U_i) / RN(sum U), omega_k = RN(U_k) / RN(sum U_k): this thread's own runs
   {
-    uint32_t kidx = nkc, oidx = noc;
+    uint32_t kidx = cc & 0xFFFFu, oidx = cc >> 16;
 #pragma unroll
     for (int j = 0; j < SM_PER; ++j) {
-      const uint32_t i = i0 + j;
-      if (i < G) {
-        kidx += (kh >> j) & 1;
-        oidx += (oh >> j) & 1;
-        const bool last = i + 1 == G;
-        const uint32_t nx = j + 1 < SM_PER ? key[j + 1] : knext;
-        if (last || nx != key[j]) keys.w[kidx - 1] = ratio(load_u128(keys.U, kidx - 1), totUk);
-        if (ops_fit && (last || (nx >> 16) != (key[j] >> 16)))
-          ops.w[oidx - 1] = ratio(load_u128(ops.U, oidx - 1), totU);
-      }
+      if (i0 + j >= G) continue;
+      kidx += (kh >> j) & 1;
+      oidx += (oh >> j) & 1;
+      if ((ke >> j) & 1) keys.w[kidx - 1] = ratio(load_u128(keys.U, kidx - 1), totUk);
+      if (ops_fit && ((oe >> j) & 1)) ops.w[oidx - 1] = ratio(load_u128(ops.U, oidx - 1), totU);
     }
   }
   if (tid == 0) {

@@ -28,9 +28,14 @@ __global__ void k_fill_u64(uint64_t* __restrict__ p, uint64_t n, uint64_t v) {
 
 // Copies of device status words into the context's host-mapped pinned buffer
 // (one launch for every readback of a call, in place of one copy each).
-__global__ void k_publish(PublishList pl, uint32_t* __restrict__ dst) {
+__global__ void k_publish(PublishList pl, uint32_t* __restrict__ dst, uint32_t* done, uint32_t seq) {
   for (uint32_t e = 0; e < pl.count; ++e)
     for (uint32_t i = threadIdx.x; i < pl.n32[e]; i += blockDim.x) dst[pl.off32[e] + i] = pl.src[e][i];
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence_system();
+    __hip_atomic_store(done, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+  }
 }
 
 __global__ void k_sum_u32(const uint32_t* __restrict__ x, uint64_t n, uint64_t* __restrict__ out) {
@@ -170,8 +175,8 @@ void launch_fill_u64(hipStream_t s, uint64_t* p, uint64_t n, uint64_t v) {
   hipLaunchKernelGGL(k_fill_u64, dim3((uint32_t)nb), dim3(256), 0, s, p, n, v);
 }
 
-void launch_publish(hipStream_t s, const PublishList& pl, uint32_t* dst) {
-  if (pl.count) hipLaunchKernelGGL(k_publish, dim3(1), dim3(64), 0, s, pl, dst);
+void launch_publish(hipStream_t s, const PublishList& pl, uint32_t* dst, uint32_t* done, uint32_t seq) {
+  hipLaunchKernelGGL(k_publish, dim3(1), dim3(64), 0, s, pl, dst, done, seq);
 }
 
 void launch_sum_u32(hipStream_t s, const uint32_t* x, uint64_t n, uint64_t* out) {

@@ -160,3 +160,27 @@ def test_range_split_pass_a_wraps_and_high_words(seed):
     g = H.run_gpu(key, app, ph, dur, c, P, max_groups=2 * n, max_keys=n)
     o = O.run(key, app, ph, dur, c, P)
     H.compare(g, o)
+
+
+def _u(pairs):
+    return [int(lo) | (int(hi) << 64) for lo, hi in np.asarray(pairs, np.uint64).reshape(-1, 2)]
+
+
+@pytest.mark.parametrize("ci,n", [(1, 1 << 20), (3, 1 << 20), (4, 1 << 20)])
+def test_weights_are_correctly_rounded_ratios(ci, n):
+    """Every fp64 weight the kernels produce is RN(numerator) / RN(denominator)
+    of the exact integers they also return (group W over the phase total S,
+    U_i over sum U, U_k over sum U_k): Python's int -> float conversion rounds
+    to nearest even, so this pins the device's 128-bit -> fp64 conversion and
+    its division bit for bit, not only within the parity tolerance."""
+    cfg, ev, c = _config_case(ci, n)
+    H.say("correctly rounded weights, config", ci, "n", n)
+    g = H.run_gpu(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, cfg["num_phases"],
+                  max_groups=2 * n, max_keys=n)
+    S = _u(g["phase_total"])
+    W = _u(g["wsum"])
+    want = [float(w) / float(S[p]) if S[p] else 0.0 for w, p in zip(W, g["phase"])]
+    assert np.array_equal(g["weight"], np.array(want)), "group weight"
+    for U, w in ((_u(g["op_U"]), g["op_w"]), (_u(g["key_U"]), g["omega"])):
+        tot = float(sum(U))
+        assert np.array_equal(w, np.array([float(u) / tot for u in U])), "unit weight"
