@@ -117,6 +117,11 @@ def main() -> int:
     result = {}
 
     def step(a, times=None):
+        if times is None:  # the whole path in one library call (atrex_run)
+            r = a.run(d_key, d_app, d_ph, d_dur, gbuf, d_sk, d_s, sbuf)
+            result["groups"], result["score"] = r["groups"], r["score"]
+            return
+        # per-kernel times: the calls one by one (times are kept per call)
         a.reset()
         a.aggregate(d_key, d_app, d_ph, d_dur)
         if times is not None:
@@ -194,7 +199,7 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": cfg["name"], "events": n, "keys": int(keys.size), "phases": P,
                    "apps": cfg["num_apps"], "seed": cfg["seed"], "path": ag.path_used(),
-                   "parallelism": "none"},
+                   "parallelism": "none", "entry": "atrex_run"},
         "hbm_frac_30B": round(30 * value * 1e9 / (HBM_PEAK_GBS * 1e9), 4),
         "hbm_frac_17B": round(17 * value * 1e9 / (HBM_PEAK_GBS * 1e9), 4),
         "kernels_ms": {k: round(v["avg_ms"], 4) for k, v in kernels.items()},

@@ -155,6 +155,31 @@ atrex_status atrex_weighted_score(atrex_ctx *ctx, const uint32_t *score_key, con
                                   uint64_t n, uint32_t *op, double *op_weight, double *op_score,
                                   uint64_t *num_ops, double *s_agg);
 
+typedef struct {
+  uint64_t num_groups;     /* as atrex_aggregate_events returns it */
+  uint64_t num_ops;        /* as atrex_phase_normalize returns them */
+  uint64_t num_keys;
+  uint64_t num_scored_ops; /* atrex_weighted_score's num_ops (0 without a score) */
+  double s_agg;            /* atrex_weighted_score's s_agg (0 without a score) */
+} atrex_run_result;
+
+/* One batch through the whole path in one call: atrex_aggregate_reset,
+ * atrex_aggregate_events, atrex_phase_normalize and, when n_score > 0,
+ * atrex_weighted_score, with the same outputs and the same errors in the same
+ * order (§3.4 Eq. (2)-(3), §3.6 Eq. (4)-(6)).  out (DEVICE arrays as for
+ * atrex_phase_normalize) holds out_capacity groups: CAPACITY when the trace
+ * has more.  score_key, s, op, op_weight, op_score as for
+ * atrex_weighted_score (n_score = 0: no score).  The host waits for the
+ * device after the group-by (the group count sizes what follows) and once at
+ * the end; with n_score <= 8192 and timing off, the normalisation and the
+ * score run back to back without a wait between them.  After an error the
+ * results of the stages before it stay valid as with the separate calls.
+ * HOST: ev (struct), out (struct), r. */
+atrex_status atrex_run(atrex_ctx *ctx, const atrex_events *ev, const atrex_groups *out,
+                       uint64_t out_capacity, const uint32_t *score_key, const double *s,
+                       uint64_t n_score, uint32_t *op, double *op_weight, double *op_score,
+                       atrex_run_result *r);
+
 /* Per (app, phase), index a * P + ph (DEVICE, [A*P]): T = D_a^phi (u128);
  * mant / rho (nullable): the scale m, rho defined above (m = 0: no share). */
 atrex_status atrex_get_app_totals(atrex_ctx *ctx, atrex_u128 *T, uint64_t *mant, int32_t *rho);

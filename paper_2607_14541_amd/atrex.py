@@ -51,6 +51,11 @@ class _Groups(ctypes.Structure):
                 ("phase_total", ctypes.c_void_p), ("raw_ns", ctypes.c_void_p)]
 
 
+class _RunResult(ctypes.Structure):
+    _fields_ = [("num_groups", ctypes.c_uint64), ("num_ops", ctypes.c_uint64), ("num_keys", ctypes.c_uint64),
+                ("num_scored_ops", ctypes.c_uint64), ("s_agg", ctypes.c_double)]
+
+
 _LIB = None
 
 
@@ -71,6 +76,8 @@ def _lib() -> ctypes.CDLL:
             "atrex_key_weights": [P, P, P, P],
             "atrex_weighted_score": [P, P, P, U64, P, P, P, ctypes.POINTER(U64),
                                      ctypes.POINTER(ctypes.c_double)],
+            "atrex_run": [P, ctypes.POINTER(_Events), ctypes.POINTER(_Groups), U64, P, P, U64, P, P, P,
+                          ctypes.POINTER(_RunResult)],
             "atrex_get_app_totals": [P, P, P, P],
             "atrex_kernel_times": [P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float),
                                    ctypes.POINTER(U64), I, ctypes.POINTER(I)],
@@ -155,6 +162,7 @@ class Aggregator:
         # while the caller passes the same output tensors (and sizes) again
         self._gcache = None
         self._scache = None
+        self._rviews = self._sviews = None
 
     # -- Eq. (2)-(3) group-by ---------------------------------------------------------
     def aggregate(self, key: torch.Tensor, app: torch.Tensor, phase: torch.Tensor,
@@ -210,6 +218,55 @@ class Aggregator:
                                             ctypes.byref(nkeys)), "atrex_phase_normalize")
         self.num_ops, self.num_keys = nops.value, nkeys.value
         return dict(c[4])
+
+    def run(self, key: torch.Tensor, app: torch.Tensor, phase: torch.Tensor, dur_ns: torch.Tensor,
+            out: dict, score_key: torch.Tensor | None = None, s: torch.Tensor | None = None,
+            score_out: dict | None = None) -> dict:
+        """reset + aggregate + normalize (+ score when score_key, s are given) in
+        one library call (atrex_run): the same results as the calls one by one.
+        `out` comes from group_buffers(); `score_out` holds op / op_weight /
+        op_score tensors of at least len(score_key) entries."""
+        key = _dev(_as_i32(key), torch.int32, "key")
+        app = _dev(_as_i32(app), torch.int32, "app")
+        phase = _dev(phase, torch.uint8, "phase")
+        dur_ns = _dev(dur_ns, torch.int64, "dur_ns")
+        n = key.numel()
+        if not (app.numel() == n and phase.numel() == n and dur_ns.numel() == n):
+            raise ValueError("event arrays differ in length")
+        ev = _Events(_ptr(key), _ptr(app), _ptr(phase), _ptr(dur_ns), n)
+        c = self._gcache
+        if c is None or c[0] is not out or c[1] != -1 or not _same_items(out, c[2]):
+            g = _Groups(_ptr(out["key"]), _ptr(out["phase"]), _ptr(out["count"]), _ptr(out["wsum"]),
+                        _ptr(out["weight"]), _ptr(out["phase_total"]), _ptr(out.get("raw_ns")))
+            c = self._gcache = (out, -1, tuple(out.items()), g, None)
+        nsc, sp = 0, (ctypes.c_void_p(0),) * 5
+        if score_key is not None:
+            score_key = _dev(_as_i32(score_key), torch.int32, "score_key")
+            s = _dev(s, torch.float64, "s")
+            nsc = score_key.numel()
+            if s.numel() != nsc:
+                raise ValueError("score_key and s differ in length")
+            if any(score_out[k].numel() < nsc for k in ("op", "op_weight", "op_score")):
+                raise ValueError("score output buffers too small")
+            sp = (_ptr(score_key), _ptr(s), _ptr(score_out["op"]), _ptr(score_out["op_weight"]),
+                  _ptr(score_out["op_score"]))
+        r = _RunResult()
+        st = _lib().atrex_run(self._ctx, ctypes.byref(ev), ctypes.byref(c[3]), out["key"].numel(), sp[0], sp[1],
+                              nsc, sp[2], sp[3], sp[4], ctypes.byref(r))
+        # counts of the stages that completed (as after the separate calls)
+        self.num_groups, self.num_ops, self.num_keys = r.num_groups, r.num_ops, r.num_keys
+        _check(st, "atrex_run")
+        G, k = r.num_groups, r.num_scored_ops
+        v = self._rviews  # views of the first G groups / k operators, kept while they stay the same
+        if v is None or v[0] is not out or v[1] != G:
+            v = self._rviews = (out, G, {kk: (t if kk == "phase_total" else t[:G]) for kk, t in out.items()})
+        res = {"groups": dict(v[2])}
+        if score_key is not None:
+            w = self._sviews
+            if w is None or w[0] is not score_out or w[1] != k:
+                w = self._sviews = (score_out, k, {kk: score_out[kk][:k] for kk in ("op", "op_weight", "op_score")})
+            res["score"] = dict(w[2], s_agg=r.s_agg)
+        return res
 
     def op_weights(self) -> dict:
         k, dev = self.num_ops, self.device

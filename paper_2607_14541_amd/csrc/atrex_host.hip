@@ -289,6 +289,7 @@ struct atrex_ctx {
   }
   uint64_t* Csum() const { return at<uint64_t>(L.ctrl + 1024); }
   double* sagg() const { return at<double>(L.ctrl + 1088); }
+  unsigned long long* unit_counts() const { return at<unsigned long long>(L.ctrl + 256); }  // operators, keys
   GroupTables tables() const {
     GroupTables gt;
     gt.dict = at<unsigned long long>(L.dict);
@@ -773,45 +774,65 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
   return ATREX_OK;
 }
 
-atrex_status atrex_phase_normalize(atrex_ctx* c, const atrex_groups* out, uint64_t* num_ops, uint64_t* num_keys) {
+namespace {
+
+atrex_status normalize_check(atrex_ctx* c, const atrex_groups* out) {
   if (!c || !out) return ATREX_E_INVALID_ARG;
   if (c->state < 1) return ATREX_E_STATE;
+  if (!out->phase_total) return ATREX_E_INVALID_ARG;
+  if (c->G > 0 && (!out->key || !out->phase || !out->count || !out->wsum || !out->weight)) return ATREX_E_INVALID_ARG;
+  if (out->raw_ns && !c->p.raw) return ATREX_E_INVALID_ARG;
+  return ATREX_OK;
+}
+
+// Enqueues the per-phase totals (when the ordering step did not write them),
+// the group weights and Eq. (3) per operator and per key; the counts of
+// operators and keys go to the control words at byte 256.
+void normalize_enqueue(atrex_ctx* c, const atrex_groups* out) {
   const uint64_t G = c->G;
   const uint32_t P = c->p.P;
-  if (!out->phase_total) return ATREX_E_INVALID_ARG;
-  if (G > 0 && (!out->key || !out->phase || !out->count || !out->wsum || !out->weight)) return ATREX_E_INVALID_ARG;
-  if (out->raw_ns && !c->p.raw) return ATREX_E_INVALID_ARG;
   const Layout& L = c->L;
   hipStream_t s = c->s;
-  c->begin_call();
   const SortedGroups g = c->groups();
   uint64_t* S = c->at<uint64_t>(L.S);
   if (!c->S_ready) {
     const uint32_t nb = (uint32_t)std::min<uint64_t>(1024, std::max<uint64_t>(1, (G + 255) / 256));
     TIMED(c, "phase_totals", G, launch_phase_totals(s, g, G, P, c->at<uint64_t>(L.partials), nb, S));
   }
-  // groups with weights, then Eq. (3) per operator and per key
   GroupsOut o{out->key, out->phase, out->count, (uint64_t*)out->wsum, (uint64_t*)out->raw_ns, out->weight,
               (uint64_t*)out->phase_total};
   UnitTable ot{c->at<uint32_t>(L.op_id), c->at<uint64_t>(L.op_U), c->at<double>(L.op_w)};
   UnitTable kt{c->at<uint32_t>(L.key_id), c->at<uint64_t>(L.key_U), c->at<double>(L.key_w)};
-  unsigned long long* cnt = c->at<unsigned long long>(L.ctrl + 256);
   TIMED(c, "units", G,
-        launch_units(s, g, G, P, lcm_1_to(P), S, o, c->unit_scratch(), ot, L.maxOps, kt, cnt, c->err()));
-  uint64_t h[2] = {0, 0};
-  uint32_t e = 0;
-  d2h(c, h, cnt, sizeof(h));
-  d2h(c, &e, c->err(), sizeof(e));
-  const atrex_status st = sync_read(c);
-  if (st != ATREX_OK) return st;
+        launch_units(s, g, G, P, lcm_1_to(P), S, o, c->unit_scratch(), ot, L.maxOps, kt, c->unit_counts(), c->err()));
+}
+
+// After the readback of the counts (h) and the error word (e).
+atrex_status normalize_finish(atrex_ctx* c, const uint64_t h[2], uint32_t e, uint64_t* num_ops, uint64_t* num_keys) {
   if (e & ATREX_ERRBIT_CAPACITY) return ATREX_E_CAPACITY;
-  c->end_call();
   c->nops = h[0];
   c->nkeys = h[1];
   if (num_ops) *num_ops = c->nops;
   if (num_keys) *num_keys = c->nkeys;
   c->state = 2;
   return ATREX_OK;
+}
+
+}  // namespace
+
+atrex_status atrex_phase_normalize(atrex_ctx* c, const atrex_groups* out, uint64_t* num_ops, uint64_t* num_keys) {
+  atrex_status st = normalize_check(c, out);
+  if (st != ATREX_OK) return st;
+  c->begin_call();
+  normalize_enqueue(c, out);
+  uint64_t h[2] = {0, 0};
+  uint32_t e = 0;
+  d2h(c, h, c->unit_counts(), sizeof(h));
+  d2h(c, &e, c->err(), sizeof(e));
+  st = sync_read(c);
+  if (st != ATREX_OK) return st;
+  c->end_call();
+  return normalize_finish(c, h, e, num_ops, num_keys);
 }
 
 atrex_status atrex_op_weights(atrex_ctx* c, uint32_t* op, atrex_u128* U, double* w) {
@@ -838,43 +859,74 @@ atrex_status atrex_key_weights(atrex_ctx* c, uint32_t* key, atrex_u128* U, doubl
   return sync_read(c);
 }
 
-atrex_status atrex_weighted_score(atrex_ctx* c, const uint32_t* score_key, const double* sv, uint64_t n, uint32_t* op,
-                                  double* op_weight, double* op_score, uint64_t* num_ops, double* s_agg) {
+namespace {
+
+atrex_status score_check(atrex_ctx* c, const uint32_t* score_key, const double* sv, uint64_t n, const double* s_agg) {
   if (!c || !s_agg) return ATREX_E_INVALID_ARG;
   if (c->state < 2) return ATREX_E_STATE;
   if (n == 0 || !score_key || !sv) return ATREX_E_INVALID_ARG;
   if (n > c->L.maxS) return ATREX_E_CAPACITY;
+  return ATREX_OK;
+}
+
+// Readback words of the ranking score path.
+struct ScoreWords {
+  uint64_t tot[2], nret;
+  uint32_t err;
+  double sagg;
+};
+
+// n <= kScoreRankMax: ranking + one workgroup (validation, duplicates,
+// medians, Eq. (6)).  The operator count comes from the control words the
+// normalisation wrote, so nothing waits for the host in between.
+// clear_err: start from a clear error word (a call of its own); the one-call
+// path keeps the normalisation's bits, which the score's checks do not read.
+void score_small_enqueue(atrex_ctx* c, const uint32_t* score_key, const double* sv, uint64_t n, uint32_t* op,
+                         double* op_weight, double* op_score, bool clear_err, ScoreWords* w) {
+  const Layout& L = c->L;
+  hipStream_t s = c->s;
+  if (clear_err) launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 1, 0);
+  UnitTable opt{c->at<uint32_t>(L.op_id), c->at<uint64_t>(L.op_U), c->at<double>(L.op_w)};
+  uint64_t* tot = c->at<uint64_t>(L.total) + 4;
+  unsigned long long* nret = c->at<unsigned long long>(L.ctrl + 320);
+  // outputs go straight to the caller's arrays when given, else to scratch
+  uint32_t* o_op = op ? op : c->at<uint32_t>(L.r_op);
+  double* o_w = op_weight ? op_weight : c->at<double>(L.sk[0]);
+  double* o_s = op_score ? op_score : c->at<double>(L.sk[1]);
+  TIMED(c, "score", n,
+        launch_score_small(s, score_key, sv, n, c->at<uint32_t>(L.sv[2]), c->at<double>(L.sk[2]), opt,
+                           c->unit_counts(), L.maxOps, o_op, o_w, o_s, c->sagg(), tot, nret, c->err()));
+  d2h(c, &w->err, c->err(), 4);
+  d2h(c, w->tot, tot, 16);
+  d2h(c, &w->nret, nret, 8);
+  d2h(c, &w->sagg, c->sagg(), 8);
+}
+
+atrex_status score_small_finish(const ScoreWords& w, uint64_t* num_ops, double* s_agg) {
+  if (w.err & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
+  if (w.err & ATREX_ERRBIT_DUP) return ATREX_E_INVALID_ARG;
+  if (w.tot[0] == 0 && w.tot[1] == 0) return ATREX_E_INVALID_ARG;  // no retained weight
+  *s_agg = w.sagg;
+  if (num_ops) *num_ops = w.nret;
+  return ATREX_OK;
+}
+
+}  // namespace
+
+atrex_status atrex_weighted_score(atrex_ctx* c, const uint32_t* score_key, const double* sv, uint64_t n, uint32_t* op,
+                                  double* op_weight, double* op_score, uint64_t* num_ops, double* s_agg) {
+  atrex_status st = score_check(c, score_key, sv, n, s_agg);
+  if (st != ATREX_OK) return st;
   const Layout& L = c->L;
   hipStream_t s = c->s;
   c->begin_call();
-  if (n <= kScoreRankMax) {  // ranking + one workgroup: validation, duplicates, medians, Eq. (6)
-    launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 1, 0);
-    UnitTable opt{c->at<uint32_t>(L.op_id), c->at<uint64_t>(L.op_U), c->at<double>(L.op_w)};
-    uint64_t* tot = c->at<uint64_t>(L.total) + 4;
-    unsigned long long* nret = c->at<unsigned long long>(L.ctrl + 320);
-    // outputs go straight to the caller's arrays when given, else to scratch
-    uint32_t* o_op = op ? op : c->at<uint32_t>(L.r_op);
-    double* o_w = op_weight ? op_weight : c->at<double>(L.sk[0]);
-    double* o_s = op_score ? op_score : c->at<double>(L.sk[1]);
-    TIMED(c, "score", n,
-          launch_score_small(s, score_key, sv, n, c->at<uint32_t>(L.sv[2]), c->at<double>(L.sk[2]), opt, c->nops,
-                             o_op, o_w, o_s, c->sagg(), tot, nret, c->at<uint64_t>(L.r_U), c->err()));
-    uint64_t h[4] = {0, 0, 0, 0};
-    uint32_t e = 0;
-    double sa = 0.0;
-    d2h(c, &e, c->err(), 4);
-    d2h(c, h, tot, 16);
-    d2h(c, &h[2], nret, 8);
-    d2h(c, &sa, c->sagg(), 8);
-    const atrex_status st = sync_read(c);
+  if (n <= kScoreRankMax) {
+    ScoreWords w{};
+    score_small_enqueue(c, score_key, sv, n, op, op_weight, op_score, true, &w);
+    st = sync_read(c);
     if (st != ATREX_OK) return st;
-    if (e & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
-    if (e & ATREX_ERRBIT_DUP) return ATREX_E_INVALID_ARG;
-    if (h[0] == 0 && h[1] == 0) return ATREX_E_INVALID_ARG;  // no retained weight
     c->end_call();
-    *s_agg = sa;
-    if (num_ops) *num_ops = h[2];
-    return ATREX_OK;
+    return score_small_finish(w, num_ops, s_agg);
   }
   uint64_t *K0 = c->at<uint64_t>(L.sk[0]), *K1 = c->at<uint64_t>(L.sk[1]), *K2 = c->at<uint64_t>(L.sk[2]);
   uint32_t *V0 = c->at<uint32_t>(L.sv[0]), *V1 = c->at<uint32_t>(L.sv[1]), *V2 = c->at<uint32_t>(L.sv[2]);
@@ -898,7 +950,7 @@ atrex_status atrex_weighted_score(atrex_ctx* c, const uint32_t* score_key, const
   d2h(c, &hdr[1], scan + (n - 1), 4);
   d2h(c, &hdr[2], flags + (n - 1), 4);
   d2h(c, &hdr[3], maxlen, 4);
-  atrex_status st = sync_read(c);
+  st = sync_read(c);
   if (st != ATREX_OK) return st;
   if (hdr[0] & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
   uint64_t nr = (uint64_t)hdr[1] + hdr[2];
@@ -946,6 +998,43 @@ atrex_status atrex_weighted_score(atrex_ctx* c, const uint32_t* score_key, const
   *s_agg = h;
   if (num_ops) *num_ops = nr;
   return ATREX_OK;
+}
+
+atrex_status atrex_run(atrex_ctx* c, const atrex_events* ev, const atrex_groups* out, uint64_t out_capacity,
+                       const uint32_t* score_key, const double* sv, uint64_t n_score, uint32_t* op, double* op_weight,
+                       double* op_score, atrex_run_result* r) {
+  if (!c || !ev || !out || !r) return ATREX_E_INVALID_ARG;
+  *r = atrex_run_result{};
+  atrex_status st = atrex_aggregate_reset(c);
+  if (st != ATREX_OK) return st;
+  uint64_t G = 0;
+  st = atrex_aggregate_events(c, ev, &G);
+  if (st != ATREX_OK) return st;
+  r->num_groups = G;
+  if (G > out_capacity) return ATREX_E_CAPACITY;
+  st = normalize_check(c, out);
+  if (st != ATREX_OK) return st;
+  // back to back only where the score call could not fail its argument checks
+  const bool fused = n_score > 0 && n_score <= kScoreRankMax && n_score <= c->L.maxS && score_key && sv &&
+                     !(c->flags & ATREX_FLAG_TIMING);
+  if (!fused) {  // the calls one by one (timing on, no score, the large score path, or an argument error)
+    st = atrex_phase_normalize(c, out, &r->num_ops, &r->num_keys);
+    if (st != ATREX_OK || n_score == 0) return st;
+    return atrex_weighted_score(c, score_key, sv, n_score, op, op_weight, op_score, &r->num_scored_ops, &r->s_agg);
+  }
+  // normalisation and score enqueued back to back, one readback for both
+  c->begin_call();
+  normalize_enqueue(c, out);
+  uint64_t h[2] = {0, 0};
+  d2h(c, h, c->unit_counts(), sizeof(h));
+  ScoreWords w{};
+  score_small_enqueue(c, score_key, sv, n_score, op, op_weight, op_score, false, &w);
+  st = sync_read(c);
+  if (st != ATREX_OK) return st;
+  // the normalisation's error bits are still in the word the score read back
+  st = normalize_finish(c, h, w.err, &r->num_ops, &r->num_keys);
+  if (st != ATREX_OK) return st;
+  return score_small_finish(w, &r->num_scored_ops, &r->s_agg);
 }
 
 atrex_status atrex_get_app_totals(atrex_ctx* c, atrex_u128* T, uint64_t* mant, int32_t* rho) {

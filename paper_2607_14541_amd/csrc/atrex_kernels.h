@@ -249,8 +249,10 @@ void launch_small_rows(hipStream_t s, const Rows& rows, const SortedGroups& out,
                        uint32_t* done);
 // score of at most kScoreRankMax units: ranking + one-workgroup finish
 constexpr uint32_t kScoreRankMax = 8192;
+// The operator table holds min(*nops_trace, maxOps) rows (the count the
+// normalisation wrote on the device).
 void launch_score_small(hipStream_t s, const uint32_t* score_key, const double* S, uint64_t n, uint32_t* sorted_op,
-                        double* sorted_S, const UnitTable& opt, uint64_t nops_trace, uint32_t* op_out, double* w_out,
-                        double* s_out, double* s_agg, uint64_t* totU, unsigned long long* nret, uint64_t* rU,
-                        uint32_t* err);
+                        double* sorted_S, const UnitTable& opt, const unsigned long long* nops_trace, uint64_t maxOps,
+                        uint32_t* op_out, double* w_out, double* s_out, double* s_agg, uint64_t* totU,
+                        unsigned long long* nret, uint32_t* err);
 hipError_t set_score_smem_limits();

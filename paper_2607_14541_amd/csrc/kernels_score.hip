@@ -113,7 +113,8 @@ __device__ __forceinline__ Comp comp_shfl_down(Comp a, int d) {
 
 __global__ __launch_bounds__(NT) void k_score_final(const uint32_t* __restrict__ sorted_op,
                                                     const double* __restrict__ sorted_S, uint32_t n, UnitTable opt,
-                                                    uint64_t nops_trace, uint32_t* __restrict__ op_out,
+                                                    const unsigned long long* __restrict__ nops_ptr, uint64_t maxOps,
+                                                    uint32_t* __restrict__ op_out,
                                                     double* __restrict__ w_out, double* __restrict__ s_out,
                                                     double* __restrict__ s_agg, uint64_t* __restrict__ totU,
                                                     unsigned long long* __restrict__ nret) {
@@ -121,6 +122,7 @@ __global__ __launch_bounds__(NT) void k_score_final(const uint32_t* __restrict__
   double* s_S = (double*)smem64;             // [n]
   uint32_t* s_op = (uint32_t*)(s_S + n);     // [n]
   uint32_t* s_opid = s_op + n;               // [nops_trace] when it fits (kScoreOpsLds)
+  const uint64_t nops_trace = min((uint64_t)*nops_ptr, maxOps);
   const bool opid_lds = nops_trace <= kScoreOpsLds;
   __shared__ uint32_t s_w[NW];
   __shared__ uint64_t s_u[2 * NW];
@@ -223,16 +225,14 @@ __global__ __launch_bounds__(NT) void k_score_final(const uint32_t* __restrict__
 }  // namespace
 
 void launch_score_small(hipStream_t s, const uint32_t* score_key, const double* S, uint64_t n, uint32_t* sorted_op,
-                        double* sorted_S, const UnitTable& opt, uint64_t nops_trace, uint32_t* op_out, double* w_out,
-                        double* s_out, double* s_agg, uint64_t* totU, unsigned long long* nret, uint64_t* rU,
-                        uint32_t* err) {
+                        double* sorted_S, const UnitTable& opt, const unsigned long long* nops_trace, uint64_t maxOps,
+                        uint32_t* op_out, double* w_out, double* s_out, double* s_agg, uint64_t* totU,
+                        unsigned long long* nret, uint32_t* err) {
   const uint32_t nn = (uint32_t)n;
   hipLaunchKernelGGL(k_score_rank, dim3((nn + MINE - 1) / MINE), dim3(NT), (size_t)nn * 12, s, score_key, S, nn,
                      sorted_op, sorted_S, err);
-  const size_t opid_bytes = nops_trace <= kScoreOpsLds ? (size_t)nops_trace * 4 : 0;
-  (void)rU;
-  hipLaunchKernelGGL(k_score_final, dim3(1), dim3(NT), (size_t)nn * 12 + opid_bytes, s, sorted_op, sorted_S, nn, opt,
-                     nops_trace, op_out, w_out, s_out, s_agg, totU, nret);
+  hipLaunchKernelGGL(k_score_final, dim3(1), dim3(NT), (size_t)nn * 12 + kScoreOpsLds * 4, s, sorted_op, sorted_S, nn,
+                     opt, nops_trace, maxOps, op_out, w_out, s_out, s_agg, totU, nret);
 }
 
 hipError_t set_score_smem_limits() {

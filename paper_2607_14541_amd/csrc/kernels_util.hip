@@ -28,9 +28,31 @@ __global__ void k_fill_u64(uint64_t* __restrict__ p, uint64_t n, uint64_t v) {
 
 // Copies of device status words into the context's host-mapped pinned buffer
 // (one launch for every readback of a call, in place of one copy each).
+// Lane l copies words l, l + 64, ... of the concatenated ranges; each lane's
+// loads are all issued before its stores, so the copy costs one load latency.
+constexpr uint32_t kPublishWordsPerLane = 8;
+
 __global__ void k_publish(PublishList pl, uint32_t* __restrict__ dst, uint32_t* done, uint32_t seq) {
-  for (uint32_t e = 0; e < pl.count; ++e)
-    for (uint32_t i = threadIdx.x; i < pl.n32[e]; i += blockDim.x) dst[pl.off32[e] + i] = pl.src[e][i];
+  uint32_t v[kPublishWordsPerLane], at[kPublishWordsPerLane];
+  uint32_t e = 0, before = 0;  // range of word w, and the words of the ranges before it
+#pragma unroll
+  for (uint32_t k = 0; k < kPublishWordsPerLane; ++k) {
+    const uint32_t w = threadIdx.x + 64 * k;
+    while (e < pl.count && w >= before + pl.n32[e]) before += pl.n32[e++];
+    at[k] = ~0u;
+    if (e < pl.count) {
+      v[k] = pl.src[e][w - before];
+      at[k] = pl.off32[e] + (w - before);
+    }
+  }
+#pragma unroll
+  for (uint32_t k = 0; k < kPublishWordsPerLane; ++k)
+    if (at[k] != ~0u) dst[at[k]] = v[k];
+  for (uint32_t w = threadIdx.x + 64 * kPublishWordsPerLane;; w += 64) {  // more than 512 words
+    while (e < pl.count && w >= before + pl.n32[e]) before += pl.n32[e++];
+    if (e >= pl.count) break;
+    dst[pl.off32[e] + (w - before)] = pl.src[e][w - before];
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
     __threadfence_system();

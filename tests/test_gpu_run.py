@@ -1,0 +1,142 @@
+"""atrex_run (one call for the whole path) against the calls one by one, on
+the same context type and inputs: every output bit for bit, every count, and
+the same error statuses in the same order."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import gpu_helpers as H
+from paper_2607_14541_amd import atrex as X
+from paper_2607_14541_amd import synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _dev(a, dt):
+    return torch.from_numpy(np.ascontiguousarray(a).view(dt)).to(DEV)
+
+
+def _case(ci, n, nscore=None, seed_s=0):
+    cfg = synth.CONFIGS[ci]
+    ev = synth.events(cfg, n=n)
+    c = synth.app_weights(cfg)
+    keys = synth.key_space(cfg)
+    if nscore is not None:
+        keys = keys[:nscore]
+    s = synth.scores(cfg, keys, nan_frac=0.1)
+    return cfg, ev, c, keys, s
+
+
+def _tensors(ev, c, keys, s):
+    return (_dev(ev["key"], np.int32), _dev(ev["app"], np.int32), _dev(ev["phase"], np.uint8),
+            _dev(ev["dur_ns"], np.int64), _dev(c, np.int32), _dev(keys, np.int32), _dev(s, np.float64))
+
+
+def _score_bufs(n):
+    return dict(op=torch.empty(n, dtype=torch.int32, device=DEV),
+                op_weight=torch.empty(n, dtype=torch.float64, device=DEV),
+                op_score=torch.empty(n, dtype=torch.float64, device=DEV))
+
+
+def _same(a, b, what):
+    assert a.dtype == b.dtype and a.shape == b.shape, what
+    assert torch.equal(a.cpu().view(torch.uint8) if a.dtype == torch.float64 else a.cpu(),
+                       b.cpu().view(torch.uint8) if b.dtype == torch.float64 else b.cpu()), what
+
+
+@pytest.mark.parametrize("ci,n,nscore", [(0, 1 << 20, None), (1, 1 << 21, None), (2, 1 << 20, 1 << 14),
+                                         (1, (1 << 20) + 3, 100)])
+def test_run_matches_the_separate_calls(ci, n, nscore):
+    """nscore above 8192 takes the large score path (its own waits); up to
+    8192 the normalisation and the score run back to back."""
+    cfg, ev, c, keys, s = _case(ci, n, nscore)
+    P = cfg["num_phases"]
+    k, a, p, d, dc, sk, sv = _tensors(ev, c, keys, s)
+    H.say("atrex_run vs separate calls, config", ci, "n", n, "scored", keys.size)
+    mg = 2 * n
+    ag = X.Aggregator(P, dc, max_events=n, max_groups=mg, max_keys=n, max_score=keys.size)
+    try:
+        gb = ag.group_buffers(mg)
+        res = ag.run(k, a, p, d, gb, sk, sv, _score_bufs(keys.size))
+        run_g = {kk: v.clone() for kk, v in res["groups"].items()}
+        run_s = {kk: (v.clone() if torch.is_tensor(v) else v) for kk, v in res["score"].items()}
+        run_ops, run_keys = ag.num_ops, ag.num_keys
+        opw = {kk: v.clone() for kk, v in ag.op_weights().items()}
+        kw = {kk: v.clone() for kk, v in ag.key_weights().items()}
+        ag.reset()
+        G = ag.aggregate(k, a, p, d)
+        sep_g = ag.normalize(out=ag.group_buffers(mg))
+        sep_s = ag.score(sk, sv)
+        assert G == run_g["key"].numel()
+        assert (ag.num_ops, ag.num_keys) == (run_ops, run_keys)
+        for kk in sep_g:
+            _same(run_g[kk], sep_g[kk], kk)
+        for kk in ("op", "op_weight", "op_score"):
+            _same(run_s[kk], sep_s[kk], "score " + kk)
+        assert run_s["s_agg"] == sep_s["s_agg"]
+        for kk, v in ag.op_weights().items():
+            _same(opw[kk], v, "op " + kk)
+        for kk, v in ag.key_weights().items():
+            _same(kw[kk], v, "key " + kk)
+    finally:
+        ag.close()
+
+
+def test_run_without_score_and_repeated():
+    cfg, ev, c, keys, s = _case(0, 1 << 18)
+    k, a, p, d, dc, sk, sv = _tensors(ev, c, keys, s)
+    H.say("atrex_run without score, three times")
+    ag = X.Aggregator(cfg["num_phases"], dc, max_events=1 << 18, max_groups=1 << 19, max_keys=1 << 18)
+    try:
+        gb = ag.group_buffers(1 << 19)
+        first = {kk: v.clone() for kk, v in ag.run(k, a, p, d, gb)["groups"].items()}
+        for _ in range(2):
+            again = ag.run(k, a, p, d, gb)
+            assert "score" not in again
+            for kk in first:
+                _same(first[kk], again["groups"][kk], kk)
+    finally:
+        ag.close()
+
+
+def _status(fn):
+    try:
+        fn()
+    except X.AtrexError as e:
+        return e.status
+    return X.OK
+
+
+def test_run_errors_in_call_order():
+    cfg, ev, c, keys, s = _case(0, 1 << 16)
+    P = cfg["num_phases"]
+    k, a, p, d, dc, sk, sv = _tensors(ev, c, keys, s)
+    H.say("atrex_run errors")
+    ag = X.Aggregator(P, dc, max_events=1 << 16, max_groups=1 << 17, max_keys=1 << 16, max_score=keys.size)
+    try:
+        gb = ag.group_buffers(1 << 17)
+        sb = _score_bufs(keys.size)
+        # fewer output rows than groups
+        small = {kk: (v if kk == "phase_total" else v[:10]) for kk, v in gb.items()}
+        assert _status(lambda: ag.run(k, a, p, d, small, sk, sv, sb)) == X.E_CAPACITY
+        # a bad event: the group-by fails first, the score is not reached
+        bad = d.clone()
+        bad[12345] = -1
+        assert _status(lambda: ag.run(k, a, p, bad, gb, sk, sv, sb)) == X.E_OUT_OF_RANGE
+        # a score above 1: the normalisation results stand, the score fails
+        s2 = sv.clone()
+        s2[3] = 1.5
+        assert _status(lambda: ag.run(k, a, p, d, gb, sk, s2, sb)) == X.E_OUT_OF_RANGE
+        assert ag.num_ops > 0 and ag.op_weights()["w"].numel() == ag.num_ops
+        # a duplicate score key
+        sk2 = sk.clone()
+        sk2[5] = sk2[6]
+        assert _status(lambda: ag.run(k, a, p, d, gb, sk2, sv, sb)) == X.E_INVALID_ARG
+        # and a clean run afterwards
+        r = ag.run(k, a, p, d, gb, sk, sv, sb)
+        assert math.isfinite(r["score"]["s_agg"])
+    finally:
+        ag.close()
