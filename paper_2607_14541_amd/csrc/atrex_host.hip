@@ -583,6 +583,8 @@ atrex_status atrex_aggregate_init(const atrex_init_params* ip, atrex_ctx** out) 
       }
     }
   }
+  // the pass-A carry table starts clear (each pass-A reduce clears it again)
+  launch_fill_u64(c->s, c->at<uint64_t>(c->L.carryA), (uint64_t)p.A * p.P, 0);
   // C = sum_a c_a, checked > 0 (p_a = c_a / C must exist)
   launch_sum_u32(c->s, c->app_weight, p.A, c->Csum());
   uint64_t C = 0;
@@ -617,9 +619,9 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
   const bool vec_ok = aligned(ev->key, 16) && aligned(ev->app, 16) && aligned(ev->phase, 4) &&
                       aligned(ev->dur_ns, 16);
   GroupTables gt = c->tables();
-  // clear the control words and the pass-A carry table
+  // clear the control words (the pass-A carry table is clear: init clears
+  // it and every pass-A reduce leaves it so)
   launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 64, 0);
-  launch_fill_u64(s, c->at<uint64_t>(L.carryA), GA, 0);
   // pass A, Eq. (2), and the Eq. (3) scale words of every (app, phase)
   uint64_t* T = c->at<uint64_t>(L.T);
   uint64_t* scale = c->at<uint64_t>(L.scale);

@@ -95,13 +95,15 @@ struct SortedGroups {
 hipError_t set_kernel_smem_limits();
 void launch_pass_a_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
                        unsigned long long* partial, unsigned long long* carry, uint32_t* err);
+// The reduce reads the carry (extension) table and leaves it zero for the
+// next pass A.
 void launch_pass_a_reduce(hipStream_t s, const unsigned long long* partial, uint32_t nb, uint32_t G,
-                          const unsigned long long* carry, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
+                          unsigned long long* carry, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
                           uint32_t P, uint64_t* scale, void* bscale);
 void launch_pass_a_lds32(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
                          uint32_t* partial, unsigned long long* ext, uint32_t* err);
 void launch_pass_a_reduce32(hipStream_t s, const uint32_t* partial, uint32_t nb, uint32_t G,
-                            const unsigned long long* ext, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
+                            unsigned long long* ext, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
                             uint32_t P, uint64_t* scale, void* bscale);
 void launch_pass_a_range(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t GR, uint32_t R,
                          uint32_t slices, uint32_t* partial, unsigned long long* ext, uint32_t* err);

@@ -387,7 +387,7 @@ __global__ void k_scale(const uint64_t* __restrict__ T, const uint32_t* __restri
 // over the partial rows.
 template <typename PT>
 __global__ __launch_bounds__(1024) void k_pass_a_reduce(const PT* __restrict__ partial, uint32_t nb, uint32_t G,
-                                                        const unsigned long long* __restrict__ ext, int ext_shift,
+                                                        unsigned long long* __restrict__ ext, int ext_shift,
                                                         uint64_t* __restrict__ T, const uint32_t* __restrict__ c,
                                                         const uint64_t* __restrict__ Csum, uint32_t P,
                                                         uint64_t* __restrict__ scale, uint64_t* __restrict__ bscale) {
@@ -404,6 +404,7 @@ __global__ __launch_bounds__(1024) void k_pass_a_reduce(const PT* __restrict__ p
   __syncthreads();
   if (r == 0 && g < G) {
     u128 t = (u128)ext[g] << ext_shift;
+    ext[g] = 0;  // left clear for the next pass A (the only reader of ext is this kernel)
     for (int i = 0; i < 16; ++i) t += make_u128(s_lo[i][gl], s_hi[i][gl]);
     T[2 * g] = (uint64_t)t;
     T[2 * g + 1] = (uint64_t)(t >> 64);
@@ -920,7 +921,7 @@ void launch_pass_a_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t 
 }
 
 void launch_pass_a_reduce(hipStream_t s, const unsigned long long* partial, uint32_t nb, uint32_t G,
-                          const unsigned long long* carry, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
+                          unsigned long long* carry, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
                           uint32_t P, uint64_t* scale, void* bscale) {
   hipLaunchKernelGGL(k_pass_a_reduce<unsigned long long>, dim3((G + 63) / 64), dim3(1024), 0, s, partial, nb, G, carry,
                      64, T, c, Csum, P, scale, (uint64_t*)bscale);
@@ -934,7 +935,7 @@ void launch_pass_a_lds32(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_
 }
 
 void launch_pass_a_reduce32(hipStream_t s, const uint32_t* partial, uint32_t nb, uint32_t G,
-                            const unsigned long long* ext, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
+                            unsigned long long* ext, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
                             uint32_t P, uint64_t* scale, void* bscale) {
   hipLaunchKernelGGL(k_pass_a_reduce<uint32_t>, dim3((G + 63) / 64), dim3(1024), 0, s, partial, nb, G, ext, 32, T, c,
                      Csum, P, scale, (uint64_t*)bscale);

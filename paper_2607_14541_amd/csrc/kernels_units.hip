@@ -475,10 +475,12 @@ void launch_units(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, 
                   const GroupsOut& out, const UnitScratch& us, const UnitTable& ops, uint64_t maxOps,
                   const UnitTable& keys, unsigned long long* counts, uint32_t* err) {
   if (G <= kUnitsSmallMax) {
-    hipLaunchKernelGGL(k_group_weights, dim3((uint32_t)std::max<uint64_t>(1, (G + 255) / 256)), dim3(256), 0, s, g,
-                       (uint32_t)G, P, S, out);
+    // independent launches; the one-workgroup kernel first, so that the host
+    // enqueues the short one while it runs
     hipLaunchKernelGGL(k_units_small, dim3(1), dim3(TILE), 0, s, g, (uint32_t)G, (uint32_t)L, ops, maxOps, keys,
                        counts, err);
+    hipLaunchKernelGGL(k_group_weights, dim3((uint32_t)std::max<uint64_t>(1, (G + 255) / 256)), dim3(256), 0, s, g,
+                       (uint32_t)G, P, S, out);
     return;
   }
   const uint32_t nt = (uint32_t)((G + TILE - 1) / TILE);

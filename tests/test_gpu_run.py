@@ -140,3 +140,34 @@ def test_run_errors_in_call_order():
         assert math.isfinite(r["score"]["s_agg"])
     finally:
         ag.close()
+
+
+@pytest.mark.parametrize("A,P", [(3, 2), (100000, 3)])
+def test_repeated_runs_with_pass_a_carries(A, P):
+    """Pass A's carry / high-word table is cleared once at init and then by
+    every pass-A reduce after reading it: three runs on one context, with
+    per-(app, phase) sums far above 2^64 (64-bit LDS partials wrap; with
+    100000 apps the range engine's 32-bit counters send every high word to
+    the table), each give the oracle's totals and groups."""
+    from oracle import oracle as O
+    rng = np.random.default_rng(A)
+    n = 5000
+    key = (rng.integers(1, 9, n) << 16 | rng.integers(0, 5, n)).astype(np.uint32)
+    app = rng.integers(0, min(A, 7), n).astype(np.uint32)
+    ph = rng.integers(0, P, n).astype(np.uint8)
+    dur = rng.integers(1 << 61, 1 << 62, n).astype(np.int64)
+    c = rng.integers(1, 1000, A).astype(np.uint32)
+    o = O.run(key, app, ph, dur, c, P)
+    H.say("repeated runs with pass-A carries, A", A, "P", P)
+    ag = X.Aggregator(P, _dev(c, np.int32), max_events=n, max_groups=2 * n, max_keys=n)
+    try:
+        gb = ag.group_buffers(2 * n)
+        for _ in range(3):
+            r = ag.run(_dev(key, np.int32), _dev(app, np.int32), _dev(ph, np.uint8), _dev(dur, np.int64), gb)
+            T = ag.app_totals()["T"].cpu().numpy().view(np.uint64)
+            assert np.array_equal(T, o["app_total"]), "app totals"
+            g = r["groups"]
+            assert np.array_equal(g["wsum"].cpu().numpy().view(np.uint64), o["wsum"]), "wsum"
+            assert np.array_equal(g["count"].cpu().numpy().view(np.uint64), o["count"]), "count"
+    finally:
+        ag.close()
