@@ -567,6 +567,7 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
   uint32_t* s_tag = (uint32_t*)(smem + (RAW ? 4 : 2) * NE);
   uint32_t* s_ocnt = s_tag + S;                 // [ATREX_OWNERS]
   uint32_t& s_spills = s_ocnt[ATREX_OWNERS];    // dynamic LDS: static LDS would not fit beside 160 KB
+  uint32_t& s_next = s_ocnt[ATREX_OWNERS + 1];  // next unclaimed block of this workgroup's range
   // Pass A has validated every event (app < A, phase < P, dur >= 0) and the
   // call fails on a range error, so the loop below takes the fields as valid;
   // after a range error this kernel only publishes empty regions.
@@ -577,7 +578,16 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
     if (threadIdx.x == 0) sp.count[blockIdx.x] = 0;
     return;
   }
-  if (threadIdx.x == 0) s_spills = 0;
+  const uint64_t n = ev.n, n4 = n / 4;
+  // blocks of 64 groups of four events (one group per lane): this
+  // workgroup's contiguous share [blk_lo, blk_hi)
+  const uint32_t NBLK = (uint32_t)((n4 + 63) / 64), FULLBLK = (uint32_t)(n4 / 64);
+  const uint32_t blk_lo = (uint32_t)((uint64_t)blockIdx.x * NBLK / gridDim.x);
+  const uint32_t blk_hi = (uint32_t)((uint64_t)(blockIdx.x + 1) * NBLK / gridDim.x);
+  if (threadIdx.x == 0) {
+    s_spills = 0;
+    s_next = blk_lo;
+  }
   for (uint32_t i = threadIdx.x; i < SP; i += BLOCK) {
     s_lo[i] = 0;
     s_hi[i] = 0;
@@ -587,8 +597,6 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
   for (uint32_t i = threadIdx.x; i < S; i += BLOCK) s_tag[i] = ATREX_EMPTY_KEY;
   for (uint32_t i = threadIdx.x; i < ATREX_OWNERS; i += BLOCK) s_ocnt[i] = 0;
   __syncthreads();
-  const uint64_t n = ev.n, n4 = n / 4;
-  const uint64_t stride = (uint64_t)gridDim.x * BLOCK;
   const uint32_t lane = lane_id();
   const uint32_t NB = S / 4;         // buckets; S is a multiple of 4, S >= 8
   const uint32_t NH8 = (NB - 1) << 8;  // home bucket = floor((hash >> 8) * (NB - 1) / 2^24), NB < 2^16
@@ -652,27 +660,29 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
       g.gi[j] = hit ? __umul24(4 * b + w, P) + e.ph[j] : INVALID_GI;
     }
   };
-  // Grid-stride over groups of four events: iteration `it` of a wave covers
-  // groups wave_first + it * stride + [0, 64); the wave index goes through a
-  // lane read so that the compiler keeps the loop control and the load bases
-  // in scalar registers.
-  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const uint64_t wave_first = (uint64_t)blockIdx.x * BLOCK + 64 * wave;
-  const uint64_t iters = wave_first < n4 ? (n4 - 1 - wave_first) / stride + 1 : 0;
-  const uint64_t full = wave_first + 64 <= n4 ? (n4 - 64 - wave_first) / stride + 1 : 0;
-  constexpr uint64_t TAIL = ~0ull;  // `it` of the n % 4 tail events (one per lane, first wave)
+  // The waves of the workgroup claim the blocks of its share one at a time
+  // from a counter in LDS, so that waves the SIMD favours take more blocks and
+  // all finish together (with a fixed split the last ones would run with ever
+  // fewer waves beside them).
+  constexpr uint32_t END = ~0u, TAIL = ~0u - 1;  // TAIL: the n % 4 tail events (one per lane, first wave)
+  auto next_blk = [&]() -> uint32_t {
+    uint32_t bk = 0;
+    if (lane == 0) bk = atomicAdd(&s_next, 1u);
+    bk = __builtin_amdgcn_readfirstlane(bk);
+    return bk < blk_hi ? bk : END;
+  };
   // events of this lane's group that exist, and the index of its event 0:
   // wanted only on the rare paths
-  auto nvalid_of = [&](uint64_t it) -> uint32_t {
-    if (it == TAIL) return n4 * 4 + lane < n ? 1u : 0u;
-    return (it < full || wave_first + it * stride + lane < n4) ? 4u : 0u;
+  auto nvalid_of = [&](uint32_t bk) -> uint32_t {
+    if (bk == TAIL) return n4 * 4 + lane < n ? 1u : 0u;
+    return (bk < FULLBLK || 64 * (uint64_t)bk + lane < n4) ? 4u : 0u;
   };
-  auto first_of = [&](uint64_t it) -> uint64_t {
-    return it == TAIL ? n4 * 4 + lane : (wave_first + it * stride + lane) * 4;
+  auto first_of = [&](uint32_t bk) -> uint64_t {
+    return bk == TAIL ? n4 * 4 + lane : (64 * (uint64_t)bk + lane) * 4;
   };
   // process(): shares, slots, accumulation of a staged group.  Events past
   // the end carry the reserved key, so they miss the window.
-  auto process = [&](const StagedEv4& g, uint64_t it) {
+  auto process = [&](const StagedEv4& g, uint32_t bk) {
     uint32_t ph[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) ph[j] = (g.ph4 >> (8 * j)) & 0xFFu;
@@ -684,8 +694,8 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
       wide |= (uint32_t)((uint64_t)g.dur[j] >> 32);
     }
     if (__builtin_expect(__any((slow >> 31) != 0), 0)) {  // rho outside [-8, 63]: the general scale word
-      const uint32_t nvalid = nvalid_of(it);
-      const uint64_t first = first_of(it);
+      const uint32_t nvalid = nvalid_of(bk);
+      const uint64_t first = first_of(bk);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const bool valid = (uint32_t)j < nvalid;
@@ -716,7 +726,7 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
     if (__builtin_expect(__any(miss), 0)) {
       // first occurrence of a key, a key placed past its window, the reserved
       // key, or events past the end: probe on, then spill what is unplaced
-      const uint32_t nvalid = nvalid_of(it);
+      const uint32_t nvalid = nvalid_of(bk);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const bool valid = (uint32_t)j < nvalid;
@@ -790,15 +800,14 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
         if (old[j] + (uint64_t)g.dur[j] < old[j]) atomicAdd(&s_rhi[at[j]], 1ull);
     }
   };
-  // A three-stage pipeline: while iteration it is accumulated, the scale
-  // words of it + 1 and the loads of it + 2 are in flight.  Iterations whose
-  // 64 groups all exist load through the wave's scalar base address; the one
-  // partial iteration (at most one per grid) clamps its indices and gives the
-  // events past the end the reserved key.
-  if (iters > 0) {
-    auto load_it = [&](uint64_t it, Ev4& e) {
-      const uint64_t g0 = wave_first + it * stride;
-      if (it < full) {
+  // A three-stage pipeline: while one block is accumulated, the scale words
+  // of the next and the loads of the one after are in flight.  Full blocks
+  // load through the wave's scalar base address; the one partial block clamps
+  // its indices and gives the events past the end the reserved key.
+  {
+    auto load_blk = [&](uint32_t bk, Ev4& e) {
+      const uint64_t g0 = 64 * (uint64_t)bk;
+      if (bk < FULLBLK) {
         load4_lane(ev.key, ev.app, ev.phase, ev.dur, g0 * 4, lane, e);
       } else {
         const uint64_t q = g0 + lane;
@@ -809,20 +818,34 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
         }
       }
     };
-    Ev4 raw;
-    StagedEv4 gA, gB;
-    load_it(0, raw);
-    stage(raw, gA);
-    if (1 < iters) load_it(1, raw);
-    for (uint64_t it = 0;;) {
-      if (it + 1 < iters) stage(raw, gB);
-      if (it + 2 < iters) load_it(it + 2, raw);
-      process(gA, it);
-      if (++it >= iters) break;
-      if (it + 1 < iters) stage(raw, gA);
-      if (it + 2 < iters) load_it(it + 2, raw);
-      process(gB, it);
-      if (++it >= iters) break;
+    uint32_t bA = next_blk();
+    if (bA != END) {
+      Ev4 raw;
+      StagedEv4 gA, gB;
+      load_blk(bA, raw);
+      stage(raw, gA);
+      uint32_t bB = next_blk();
+      if (bB != END) load_blk(bB, raw);
+      for (;;) {  // gA holds block bA, raw block bB (when it exists)
+        uint32_t bC = END;
+        if (bB != END) {
+          stage(raw, gB);
+          bC = next_blk();
+          if (bC != END) load_blk(bC, raw);
+        }
+        process(gA, bA);
+        if (bB == END) break;
+        uint32_t bD = END;
+        if (bC != END) {
+          stage(raw, gA);
+          bD = next_blk();
+          if (bD != END) load_blk(bD, raw);
+        }
+        process(gB, bB);
+        if (bC == END) break;
+        bA = bC;
+        bB = bD;
+      }
     }
   }
   if (blockIdx.x == 0 && threadIdx.x < 64) {  // n % 4 tail events, one wave
@@ -977,11 +1000,11 @@ uint32_t pass_b_lds_slots(uint32_t P, bool raw, size_t lds_bytes) {
 }
 
 size_t pass_b_lds_smem(uint32_t P, bool raw, uint32_t S) {
-  return ((size_t)S * P * 16 + 64 * 16) * (raw ? 2 : 1) + (size_t)S * 4 + ATREX_OWNERS * 4 + 4;
+  return ((size_t)S * P * 16 + 64 * 16) * (raw ? 2 : 1) + (size_t)S * 4 + ATREX_OWNERS * 4 + 8;
 }
 
-// a workgroup of the grid-stride loop sees at most n / nwg + 4 * BLOCK + 3
-// events; its spill region holds half of that
+// a workgroup sees at most n / nwg + 4 * 64 + 3 events (its share of the
+// 64-group blocks, and the tail); its spill region holds half of that
 uint32_t spill_cap(uint64_t n, uint32_t nwg) { return (uint32_t)((n + nwg - 1) / nwg / 2 + 8 * 1024); }
 
 uint32_t owner_cap(uint32_t S) { return 2 * ((S + ATREX_OWNERS - 1) / ATREX_OWNERS) + 32; }
