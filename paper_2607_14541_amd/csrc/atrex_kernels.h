@@ -212,6 +212,20 @@ struct UnitScratch {
 };
 uint64_t units_tiles(uint64_t G);
 constexpr uint64_t kUnitsSmallMax = 8192;  // groups the one-workgroup unit kernel handles
+// The score ranking's inputs and outputs (n <= kScoreRankMax units).
+struct ScoreRankArgs {
+  const uint32_t* score_key;
+  const double* S;
+  uint32_t n;
+  uint32_t* sorted_op;
+  double* sorted_S;
+  uint32_t* err;
+};
+// G <= kUnitsSmallMax: the one-workgroup unit kernel, the score ranking and the
+// group weights in one launch (they are independent).
+void launch_units_rank(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t L, const uint64_t* S,
+                       const GroupsOut& out, const UnitTable& ops, uint64_t maxOps, const UnitTable& keys,
+                       unsigned long long* counts, uint32_t* err, const ScoreRankArgs& sr);
 void launch_units(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t L, const uint64_t* S,
                   const GroupsOut& out, const UnitScratch& us, const UnitTable& ops, uint64_t maxOps,
                   const UnitTable& keys, unsigned long long* counts, uint32_t* err);
@@ -241,6 +255,7 @@ void launch_score_seg(hipStream_t s, const uint32_t* score_key, const double* S,
                       const uint32_t* starts, uint64_t nseg, uint32_t maxlen, const UnitTable& opt, uint64_t nops_trace,
                       uint32_t* r_op, uint64_t* r_U, double* r_S, uint32_t* err);
 hipError_t set_normalize_smem_limits();
+hipError_t set_units_smem_limits();
 void launch_score_final(hipStream_t s, const uint32_t* r_op, const uint64_t* r_U, const double* r_S,
                         uint64_t nops, const uint64_t* totalU, uint32_t* op, double* op_weight, double* op_score,
                         double* s_agg, uint32_t* err);
@@ -257,4 +272,8 @@ void launch_score_small(hipStream_t s, const uint32_t* score_key, const double* 
                         double* sorted_S, const UnitTable& opt, const unsigned long long* nops_trace, uint64_t maxOps,
                         uint32_t* op_out, double* w_out, double* s_out, double* s_agg, uint64_t* totU,
                         unsigned long long* nret, uint32_t* err);
+// The second step of the above alone (after the ranking ran elsewhere).
+void launch_score_final(hipStream_t s, uint64_t n, const uint32_t* sorted_op, const double* sorted_S,
+                        const UnitTable& opt, const unsigned long long* nops_trace, uint64_t maxOps, uint32_t* op_out,
+                        double* w_out, double* s_out, double* s_agg, uint64_t* totU, unsigned long long* nret);
 hipError_t set_score_smem_limits();

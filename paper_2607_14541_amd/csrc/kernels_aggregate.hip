@@ -1048,6 +1048,8 @@ hipError_t set_kernel_smem_limits() {
   if (e != hipSuccess) return e;
   e = set_score_smem_limits();
   if (e != hipSuccess) return e;
+  e = set_units_smem_limits();
+  if (e != hipSuccess) return e;
   e = set_normalize_smem_limits();
   if (e != hipSuccess) return e;
   return set_rows_smem_limits();

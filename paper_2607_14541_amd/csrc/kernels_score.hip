@@ -16,52 +16,21 @@
 
 #include "atrex_device.hpp"
 #include "atrex_kernels.h"
+#include "score_rank.hpp"
 
 namespace {
 
 constexpr uint32_t NT = 1024;
 constexpr uint32_t NW = NT / 64;
-constexpr uint32_t MINE = NT / 64;  // units ranked per workgroup: one wave each
+constexpr uint32_t MINE = kRankPerBlock;  // units ranked per workgroup: one wave each
 constexpr uint64_t kScoreOpsLds = 8192;  // operator table ids staged in LDS up to this size
-
-__device__ __forceinline__ uint64_t s_order_bits(double v) {
-  return isnan(v) ? ~0ull : (uint64_t)__double_as_longlong(v);  // S > 0: bits order as values
-}
 
 __global__ __launch_bounds__(NT) void k_score_rank(const uint32_t* __restrict__ score_key,
                                                    const double* __restrict__ S, uint32_t n,
                                                    uint32_t* __restrict__ sorted_op, double* __restrict__ sorted_S,
                                                    uint32_t* __restrict__ err) {
   extern __shared__ uint64_t smem64[];
-  uint64_t* s_sb = smem64;                     // [n]
-  uint32_t* s_key = (uint32_t*)(s_sb + n);     // [n]
-  const uint32_t tid = threadIdx.x, lane = tid & 63;
-  for (uint32_t j = tid; j < n; j += NT) {
-    s_sb[j] = s_order_bits(S[j]);
-    s_key[j] = score_key[j];
-  }
-  __syncthreads();
-  const uint32_t m = blockIdx.x * MINE + (tid >> 6);  // this wave's unit
-  if (m >= n) return;                                 // wave-uniform
-  const uint32_t key_m = s_key[m], op_m = key_m >> 16;
-  const uint64_t sb_m = s_sb[m];
-  uint32_t below = 0;
-  bool dup = false;
-#pragma unroll 4
-  for (uint32_t j = lane; j < n; j += 64) {
-    const uint32_t kj = s_key[j], oj = kj >> 16;
-    const uint64_t sj = s_sb[j];
-    below += (oj < op_m || (oj == op_m && (sj < sb_m || (sj == sb_m && j < m)))) ? 1u : 0u;
-    dup |= kj == key_m && j != m;
-  }
-  for (int d = 32; d >= 1; d >>= 1) below += __shfl_xor(below, d, 64);
-  if (lane == 0) {
-    const double v = S[m];
-    sorted_op[below] = op_m;
-    sorted_S[below] = v;
-    if (!isnan(v) && !(v > 0.0 && v <= 1.0)) atomicOr(err, ATREX_ERRBIT_RANGE);
-  }
-  if (__any(dup) && lane == 0) atomicOr(err, ATREX_ERRBIT_DUP);
+  score_rank_block(blockIdx.x, score_key, S, n, sorted_op, sorted_S, err, smem64);
 }
 
 struct Comp {
@@ -231,6 +200,13 @@ void launch_score_small(hipStream_t s, const uint32_t* score_key, const double* 
   const uint32_t nn = (uint32_t)n;
   hipLaunchKernelGGL(k_score_rank, dim3((nn + MINE - 1) / MINE), dim3(NT), (size_t)nn * 12, s, score_key, S, nn,
                      sorted_op, sorted_S, err);
+  launch_score_final(s, n, sorted_op, sorted_S, opt, nops_trace, maxOps, op_out, w_out, s_out, s_agg, totU, nret);
+}
+
+void launch_score_final(hipStream_t s, uint64_t n, const uint32_t* sorted_op, const double* sorted_S,
+                        const UnitTable& opt, const unsigned long long* nops_trace, uint64_t maxOps, uint32_t* op_out,
+                        double* w_out, double* s_out, double* s_agg, uint64_t* totU, unsigned long long* nret) {
+  const uint32_t nn = (uint32_t)n;
   hipLaunchKernelGGL(k_score_final, dim3(1), dim3(NT), (size_t)nn * 12 + kScoreOpsLds * 4, s, sorted_op, sorted_S, nn,
                      opt, nops_trace, maxOps, op_out, w_out, s_out, s_agg, totU, nret);
 }

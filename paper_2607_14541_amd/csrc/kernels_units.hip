@@ -19,6 +19,7 @@
 
 #include "atrex_device.hpp"
 #include "atrex_kernels.h"
+#include "score_rank.hpp"
 
 namespace {
 
@@ -272,9 +273,8 @@ __global__ __launch_bounds__(TILE) void k_units_keys(SortedGroups g, uint64_t G,
 // The groups copied to the caller's arrays with RN(W) / RN(S[ph]), one thread
 // per group (the per-phase totals by the first threads), for the one-workgroup
 // unit kernel below.
-__global__ __launch_bounds__(256) void k_group_weights(SortedGroups g, uint32_t G, uint32_t P,
-                                                        const uint64_t* __restrict__ S, GroupsOut out) {
-  const uint32_t i = blockIdx.x * 256 + threadIdx.x;
+__device__ __forceinline__ void group_weights_at(uint32_t i, const SortedGroups& g, uint32_t G, uint32_t P,
+                                                 const uint64_t* __restrict__ S, const GroupsOut& out) {
   if (i < P) {
     out.phase_total[2 * i] = S[2 * i];
     out.phase_total[2 * i + 1] = S[2 * i + 1];
@@ -288,6 +288,11 @@ __global__ __launch_bounds__(256) void k_group_weights(SortedGroups g, uint32_t 
   store_u128(out.wsum, i, W);
   if (out.raw) store_u128(out.raw, i, load_u128(g.raw, i));
   out.weight[i] = ratio(W, load_u128(S, ph));
+}
+
+__global__ __launch_bounds__(256) void k_group_weights(SortedGroups g, uint32_t G, uint32_t P,
+                                                        const uint64_t* __restrict__ S, GroupsOut out) {
+  group_weights_at(blockIdx.x * 256 + threadIdx.x, g, G, P, S, out);
 }
 
 // ---------------------------------------------------------------------------
@@ -319,10 +324,10 @@ __device__ __forceinline__ Seg seg_shfl_up(const Seg& x, int d) {
   return y;
 }
 
-__global__ __launch_bounds__(TILE) void k_units_small(SortedGroups g, uint32_t G, uint32_t L, UnitTable ops,
-                                                      uint64_t maxOps, UnitTable keys,
-                                                      unsigned long long* __restrict__ counts,
-                                                      uint32_t* __restrict__ err) {
+__device__ __forceinline__ void units_small_body(const SortedGroups& g, uint32_t G, uint32_t L, const UnitTable& ops,
+                                                 uint64_t maxOps, const UnitTable& keys,
+                                                 unsigned long long* __restrict__ counts,
+                                                 uint32_t* __restrict__ err) {
   __shared__ Seg s_ow[NW];
   __shared__ uint32_t s_n[NW];
   __shared__ uint64_t s_kt[3 * NW];  // each wave's last key tail: sum (lo, hi), phase mask
@@ -469,7 +474,42 @@ __global__ __launch_bounds__(TILE) void k_units_small(SortedGroups g, uint32_t G
   }
 }
 
+__global__ __launch_bounds__(TILE) void k_units_small(SortedGroups g, uint32_t G, uint32_t L, UnitTable ops,
+                                                      uint64_t maxOps, UnitTable keys,
+                                                      unsigned long long* __restrict__ counts,
+                                                      uint32_t* __restrict__ err) {
+  units_small_body(g, G, L, ops, maxOps, keys, counts, err);
+}
+
+// One launch for three independent steps of the one-call path: workgroup 0
+// runs the one-workgroup unit kernel (the longest), the next nrank the score
+// ranking, the rest the group weights, so that the short ones run beside the
+// long one on other CUs.
+__global__ __launch_bounds__(TILE) void k_units_rank(SortedGroups g, uint32_t G, uint32_t P, uint32_t L,
+                                                     const uint64_t* __restrict__ S, GroupsOut out, UnitTable ops,
+                                                     uint64_t maxOps, UnitTable keys,
+                                                     unsigned long long* __restrict__ counts,
+                                                     uint32_t* __restrict__ err, ScoreRankArgs sr, uint32_t nrank) {
+  extern __shared__ uint64_t smem64[];
+  if (blockIdx.x == 0) {
+    units_small_body(g, G, L, ops, maxOps, keys, counts, err);
+  } else if (blockIdx.x <= nrank) {
+    score_rank_block(blockIdx.x - 1, sr.score_key, sr.S, sr.n, sr.sorted_op, sr.sorted_S, sr.err, smem64);
+  } else {
+    group_weights_at((blockIdx.x - 1 - nrank) * TILE + threadIdx.x, g, G, P, S, out);
+  }
+}
+
 }  // namespace
+
+void launch_units_rank(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t L, const uint64_t* S,
+                       const GroupsOut& out, const UnitTable& ops, uint64_t maxOps, const UnitTable& keys,
+                       unsigned long long* counts, uint32_t* err, const ScoreRankArgs& sr) {
+  const uint32_t nrank = (sr.n + kRankPerBlock - 1) / kRankPerBlock;
+  const uint32_t ngw = (uint32_t)std::max<uint64_t>(1, (G + TILE - 1) / TILE);
+  hipLaunchKernelGGL(k_units_rank, dim3(1 + nrank + ngw), dim3(TILE), (size_t)sr.n * 12, s, g, (uint32_t)G, P,
+                     (uint32_t)L, S, out, ops, maxOps, keys, counts, err, sr, nrank);
+}
 
 void launch_units(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t L, const uint64_t* S,
                   const GroupsOut& out, const UnitScratch& us, const UnitTable& ops, uint64_t maxOps,
@@ -492,3 +532,8 @@ void launch_units(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, 
 }
 
 uint64_t units_tiles(uint64_t G) { return (G + TILE - 1) / TILE; }
+
+hipError_t set_units_smem_limits() {
+  return hipFuncSetAttribute((const void*)k_units_rank, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (int)(kScoreRankMax * 12));
+}
