@@ -169,11 +169,13 @@ typedef struct {
  * order (§3.4 Eq. (2)-(3), §3.6 Eq. (4)-(6)).  out (DEVICE arrays as for
  * atrex_phase_normalize) holds out_capacity groups: CAPACITY when the trace
  * has more.  score_key, s, op, op_weight, op_score as for
- * atrex_weighted_score (n_score = 0: no score).  The host waits for the
- * device after the group-by (the group count sizes what follows) and once at
- * the end; with n_score <= 8192 and timing off, the normalisation and the
- * score run back to back without a wait between them.  After an error the
- * results of the stages before it stay valid as with the separate calls.
+ * atrex_weighted_score (n_score = 0: no score).  With n_score <= 8192 and
+ * timing off, the normalisation and the score run back to back; when the
+ * LDS engine orders the groups in one launch (the usual case for it) they
+ * are enqueued right behind the group-by and the host waits once, at the
+ * end; otherwise it also waits after the group-by, whose count sizes what
+ * follows.  After an error the results of the stages before it stay valid as
+ * with the separate calls.
  * HOST: ev (struct), out (struct), r. */
 atrex_status atrex_run(atrex_ctx *ctx, const atrex_events *ev, const atrex_groups *out,
                        uint64_t out_capacity, const uint32_t *score_key, const double *s,

@@ -599,8 +599,22 @@ atrex_status atrex_aggregate_init(const atrex_init_params* ip, atrex_ctx** out) 
   return ATREX_OK;
 }
 
-atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64_t* num_groups) {
-  if (!c || !ev || !num_groups) return ATREX_E_INVALID_ARG;
+namespace {
+
+// State of one group-by between its enqueue and its completion.
+struct AggRun {
+  EventsDev d;
+  atrex_path path;
+  uint32_t nwg;
+  const uint64_t* scale;
+  uint64_t hdr[32];  // control words: error at byte 0, row counter at byte 128
+};
+
+// The group-by up to the ordering of the groups, enqueued; the control words
+// are queued for readback into a->hdr (the caller synchronises, then calls
+// aggregate_complete).
+atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) {
+  if (!c || !ev) return ATREX_E_INVALID_ARG;
   if (c->state != 0) return ATREX_E_STATE;
   const uint64_t n = ev->n;
   if (n > c->p.max_events) return ATREX_E_CAPACITY;
@@ -672,7 +686,6 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
   if (!vec_ok && path != ATREX_PATH_GLOBAL_HASH) path = ATREX_PATH_GLOBAL_HASH;
   const uint32_t nwg = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)c->cus, kMaxWG));
   atrex_status st = ATREX_OK;
-  uint64_t hdr[32];  // control words: error at byte 0, row counter at byte 128
   if (path == ATREX_PATH_LDS_HASH) {
     c->path_used = "lds_hash";
     const uint32_t scap = spill_cap(n, nwg);
@@ -706,9 +719,31 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
                              smallG, smallDone));
   else
     TIMED(c, "small_rows", 0, launch_small_rows(s, rows, c->groups(), smallG, smallDone));
-  d2h(c, hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr));
-  st = sync_read(c);
-  if (st != ATREX_OK) return st;
+  a->d = d;
+  a->path = path;
+  a->nwg = nwg;
+  a->scale = scale;
+  d2h(c, a->hdr, c->at<uint64_t>(L.ctrl), sizeof(a->hdr));
+  return ATREX_OK;
+}
+
+// The rest of the group-by once a->hdr has been read back: the fallbacks the
+// control words ask for (each with its own waits) and the group count.
+// *fast: the ordering finished in one launch and nothing more was enqueued.
+atrex_status aggregate_complete(atrex_ctx* c, AggRun* a, uint64_t* num_groups, bool* fast) {
+  *fast = false;
+  const Layout& L = c->L;
+  hipStream_t s = c->s;
+  const Rows rows = c->rows();
+  const atrex_path path = a->path;
+  const EventsDev& d = a->d;
+  const uint64_t n = d.n;
+  const uint32_t nwg = a->nwg;
+  const uint64_t* scale = a->scale;
+  uint64_t* hdr = a->hdr;
+  unsigned long long* smallG = c->at<unsigned long long>(L.ctrl + 192);
+  uint32_t* smallDone = c->at<uint32_t>(L.ctrl + 200);
+  atrex_status st = ATREX_OK;
   if ((uint32_t)hdr[0] & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
   // the ranking also wrote S[ph]
   bool ranked = path == ATREX_PATH_LDS_HASH && !((uint32_t)hdr[0] & ATREX_ERRBIT_SPILL) && (uint32_t)hdr[25];
@@ -721,7 +756,7 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
       if (st != ATREX_OK) return st;
     }
     TIMED(c, "small_rows", 0, launch_small_rows(s, rows, c->groups(), smallG, smallDone));
-    d2h(c, hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr));
+    d2h(c, hdr, c->at<uint64_t>(L.ctrl), sizeof(a->hdr));
     st = sync_read(c);
     if (st != ATREX_OK) return st;
   }
@@ -732,7 +767,7 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
     st = run_partition(c, d, scale, false, nwg, n, c->p.max_keys);
     if (st != ATREX_OK) return st;
     TIMED(c, "small_rows", 0, launch_small_rows(s, rows, c->groups(), smallG, smallDone));
-    d2h(c, hdr, c->at<uint64_t>(L.ctrl), sizeof(hdr));
+    d2h(c, hdr, c->at<uint64_t>(L.ctrl), sizeof(a->hdr));
     st = sync_read(c);
     if (st != ATREX_OK) return st;
     if ((uint32_t)hdr[0] & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
@@ -743,6 +778,7 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
   uint64_t G = 0;
   if ((uint32_t)hdr[25]) {  // done by the one-workgroup kernel (flag at byte 200)
     G = hdr[24];
+    *fast = ranked;  // ranked in one launch, nothing enqueued since
   } else if (R) {
     uint64_t* K0 = c->at<uint64_t>(L.sk[0]);
     uint32_t* V0 = c->at<uint32_t>(L.sv[0]);
@@ -774,6 +810,19 @@ atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64
   c->state = 1;
   *num_groups = G;
   return ATREX_OK;
+}
+
+}  // namespace
+
+atrex_status atrex_aggregate_events(atrex_ctx* c, const atrex_events* ev, uint64_t* num_groups) {
+  if (!c || !ev || !num_groups) return ATREX_E_INVALID_ARG;
+  AggRun a;
+  atrex_status st = aggregate_enqueue(c, ev, &a);
+  if (st != ATREX_OK) return st;
+  st = sync_read(c);
+  if (st != ATREX_OK) return st;
+  bool fast = false;
+  return aggregate_complete(c, &a, num_groups, &fast);
 }
 
 namespace {
@@ -926,7 +975,8 @@ void units_score_enqueue(atrex_ctx* c, const atrex_groups* out, const uint32_t* 
   uint32_t* sorted_op = c->at<uint32_t>(L.sv[2]);
   double* sorted_S = c->at<double>(L.sk[2]);
   const ScoreRankArgs sr{score_key, sv, (uint32_t)n, sorted_op, sorted_S, c->err()};
-  launch_units_rank(s, g, G, P, lcm_1_to(P), S, o, ot, L.maxOps, kt, c->unit_counts(), c->err(), sr);
+  launch_units_rank(s, g, G, P, lcm_1_to(P), S, o, ot, L.maxOps, kt, c->unit_counts(), c->err(), sr,
+                    UnitsGuard{nullptr, nullptr, nullptr, 0});
   uint64_t* tot = c->at<uint64_t>(L.total) + 4;
   unsigned long long* nret = c->at<unsigned long long>(L.ctrl + 320);
   uint32_t* o_op = op ? op : c->at<uint32_t>(L.r_op);
@@ -1037,6 +1087,50 @@ atrex_status atrex_weighted_score(atrex_ctx* c, const uint32_t* score_key, const
   return ATREX_OK;
 }
 
+namespace {
+
+// The one-call path's speculation: with the LDS engine the groups are usually
+// ordered in one launch, so the unit kernel, the group weights and the score
+// are enqueued right behind the group-by, before its readback.  The unit and
+// weight parts check the ordering's flags on the device (k_units_rank's
+// guard); their error bits and the score's go to words of their own, so that
+// the group-by's words read back unchanged.
+void speculate_enqueue(atrex_ctx* c, const atrex_groups* out, uint64_t out_capacity, const uint32_t* score_key,
+                       const double* sv, uint64_t n, uint32_t* op, double* op_weight, double* op_score,
+                       uint64_t h[2], uint32_t* units_err_host, ScoreWords* w) {
+  const uint32_t P = c->p.P;
+  const Layout& L = c->L;
+  hipStream_t s = c->s;
+  const SortedGroups g = c->groups();
+  uint64_t* S = c->at<uint64_t>(L.S);
+  GroupsOut o{out->key, out->phase, out->count, (uint64_t*)out->wsum, (uint64_t*)out->raw_ns, out->weight,
+              (uint64_t*)out->phase_total};
+  UnitTable ot{c->at<uint32_t>(L.op_id), c->at<uint64_t>(L.op_U), c->at<double>(L.op_w)};
+  UnitTable kt{c->at<uint32_t>(L.key_id), c->at<uint64_t>(L.key_U), c->at<double>(L.key_w)};
+  uint32_t* units_err = c->at<uint32_t>(L.ctrl + 480);
+  uint32_t* score_err = c->at<uint32_t>(L.ctrl + 484);
+  uint32_t* sorted_op = c->at<uint32_t>(L.sv[2]);
+  double* sorted_S = c->at<double>(L.sk[2]);
+  const ScoreRankArgs sr{score_key, sv, (uint32_t)n, sorted_op, sorted_S, score_err};
+  const uint32_t gmax = (uint32_t)std::min<uint64_t>(std::min<uint64_t>(kUnitsSmallMax, out_capacity), L.maxG);
+  const UnitsGuard guard{c->at<unsigned long long>(L.ctrl + 192), c->at<uint32_t>(L.ctrl + 200), c->err(), gmax};
+  launch_units_rank(s, g, 0, P, lcm_1_to(P), S, o, ot, L.maxOps, kt, c->unit_counts(), units_err, sr, guard);
+  uint64_t* tot = c->at<uint64_t>(L.total) + 4;
+  unsigned long long* nret = c->at<unsigned long long>(L.ctrl + 320);
+  uint32_t* o_op = op ? op : c->at<uint32_t>(L.r_op);
+  double* o_w = op_weight ? op_weight : c->at<double>(L.sk[0]);
+  double* o_s = op_score ? op_score : c->at<double>(L.sk[1]);
+  launch_score_final(s, n, sorted_op, sorted_S, ot, c->unit_counts(), L.maxOps, o_op, o_w, o_s, c->sagg(), tot, nret);
+  d2h(c, h, c->unit_counts(), 16);
+  d2h(c, units_err_host, units_err, 4);
+  d2h(c, &w->err, score_err, 4);
+  d2h(c, w->tot, tot, 16);
+  d2h(c, &w->nret, nret, 8);
+  d2h(c, &w->sagg, c->sagg(), 8);
+}
+
+}  // namespace
+
 atrex_status atrex_run(atrex_ctx* c, const atrex_events* ev, const atrex_groups* out, uint64_t out_capacity,
                        const uint32_t* score_key, const double* sv, uint64_t n_score, uint32_t* op, double* op_weight,
                        double* op_score, atrex_run_result* r) {
@@ -1044,16 +1138,34 @@ atrex_status atrex_run(atrex_ctx* c, const atrex_events* ev, const atrex_groups*
   *r = atrex_run_result{};
   atrex_status st = atrex_aggregate_reset(c);
   if (st != ATREX_OK) return st;
-  uint64_t G = 0;
-  st = atrex_aggregate_events(c, ev, &G);
-  if (st != ATREX_OK) return st;
-  r->num_groups = G;
-  if (G > out_capacity) return ATREX_E_CAPACITY;
-  st = normalize_check(c, out);
-  if (st != ATREX_OK) return st;
   // back to back only where the score call could not fail its argument checks
   const bool fused = n_score > 0 && n_score <= kScoreRankMax && n_score <= c->L.maxS && score_key && sv &&
                      !(c->flags & ATREX_FLAG_TIMING);
+  const bool out_ok = out->phase_total && out->key && out->phase && out->count && out->wsum && out->weight &&
+                      (!out->raw_ns || c->p.raw);
+  AggRun a;
+  st = aggregate_enqueue(c, ev, &a);
+  if (st != ATREX_OK) return st;
+  const bool spec = fused && out_ok && out_capacity > 0 && a.path == ATREX_PATH_LDS_HASH;
+  uint64_t h[2] = {0, 0};
+  uint32_t units_err = 0;
+  ScoreWords w{};
+  if (spec) speculate_enqueue(c, out, out_capacity, score_key, sv, n_score, op, op_weight, op_score, h, &units_err, &w);
+  st = sync_read(c);
+  if (st != ATREX_OK) return st;
+  uint64_t G = 0;
+  bool fast = false;
+  st = aggregate_complete(c, &a, &G, &fast);
+  if (st != ATREX_OK) return st;
+  r->num_groups = G;
+  if (G > out_capacity) return ATREX_E_CAPACITY;
+  if (spec && fast && G <= kUnitsSmallMax) {  // the speculation stands (the device took the same decision)
+    st = normalize_finish(c, h, units_err, &r->num_ops, &r->num_keys);
+    if (st != ATREX_OK) return st;
+    return score_small_finish(w, &r->num_scored_ops, &r->s_agg);
+  }
+  st = normalize_check(c, out);
+  if (st != ATREX_OK) return st;
   if (!fused) {  // the calls one by one (timing on, no score, the large score path, or an argument error)
     st = atrex_phase_normalize(c, out, &r->num_ops, &r->num_keys);
     if (st != ATREX_OK || n_score == 0) return st;
@@ -1061,8 +1173,7 @@ atrex_status atrex_run(atrex_ctx* c, const atrex_events* ev, const atrex_groups*
   }
   // normalisation and score enqueued back to back, one readback for both
   c->begin_call();
-  uint64_t h[2] = {0, 0};
-  ScoreWords w{};
+  w = ScoreWords{};
   if (c->G <= kUnitsSmallMax) {
     // the one-workgroup unit kernel, the score ranking and the group weights
     // in one launch, then the score's one-workgroup finish

@@ -221,11 +221,20 @@ struct ScoreRankArgs {
   double* sorted_S;
   uint32_t* err;
 };
+// Device-side group count for launch_units_rank: G (null: the host's G), the
+// ordering's done flag, the group-by's error word, and the largest count
+// taken (at most kUnitsSmallMax).
+struct UnitsGuard {
+  const unsigned long long* G;
+  const uint32_t* done;
+  const uint32_t* err;
+  uint32_t gmax;
+};
 // G <= kUnitsSmallMax: the one-workgroup unit kernel, the score ranking and the
 // group weights in one launch (they are independent).
 void launch_units_rank(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t L, const uint64_t* S,
                        const GroupsOut& out, const UnitTable& ops, uint64_t maxOps, const UnitTable& keys,
-                       unsigned long long* counts, uint32_t* err, const ScoreRankArgs& sr);
+                       unsigned long long* counts, uint32_t* err, const ScoreRankArgs& sr, const UnitsGuard& guard);
 void launch_units(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t L, const uint64_t* S,
                   const GroupsOut& out, const UnitScratch& us, const UnitTable& ops, uint64_t maxOps,
                   const UnitTable& keys, unsigned long long* counts, uint32_t* err);

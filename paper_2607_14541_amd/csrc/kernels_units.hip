@@ -485,17 +485,30 @@ __global__ __launch_bounds__(TILE) void k_units_small(SortedGroups g, uint32_t G
 // runs the one-workgroup unit kernel (the longest), the next nrank the score
 // ranking, the rest the group weights, so that the short ones run beside the
 // long one on other CUs.
+// With guard.G set, the group count comes from the device and the unit and
+// group-weight parts run only when the ordering finished in one launch with a
+// clean error word and at most guard.gmax groups (the caller decides
+// afterwards, from the same words, whether their results stand).
 __global__ __launch_bounds__(TILE) void k_units_rank(SortedGroups g, uint32_t G, uint32_t P, uint32_t L,
                                                      const uint64_t* __restrict__ S, GroupsOut out, UnitTable ops,
                                                      uint64_t maxOps, UnitTable keys,
                                                      unsigned long long* __restrict__ counts,
-                                                     uint32_t* __restrict__ err, ScoreRankArgs sr, uint32_t nrank) {
+                                                     uint32_t* __restrict__ err, ScoreRankArgs sr, uint32_t nrank,
+                                                     UnitsGuard guard) {
   extern __shared__ uint64_t smem64[];
+  bool units_ok = true;
+  if (guard.G) {
+    const unsigned long long gd = *guard.G;
+    units_ok = *guard.done == 1u &&
+               (*guard.err & (ATREX_ERRBIT_RANGE | ATREX_ERRBIT_CAPACITY | ATREX_ERRBIT_SPILL)) == 0 &&
+               gd <= guard.gmax;
+    G = units_ok ? (uint32_t)gd : 0u;
+  }
   if (blockIdx.x == 0) {
-    units_small_body(g, G, L, ops, maxOps, keys, counts, err);
+    if (units_ok) units_small_body(g, G, L, ops, maxOps, keys, counts, err);
   } else if (blockIdx.x <= nrank) {
     score_rank_block(blockIdx.x - 1, sr.score_key, sr.S, sr.n, sr.sorted_op, sr.sorted_S, sr.err, smem64);
-  } else {
+  } else if (units_ok) {
     group_weights_at((blockIdx.x - 1 - nrank) * TILE + threadIdx.x, g, G, P, S, out);
   }
 }
@@ -504,11 +517,12 @@ __global__ __launch_bounds__(TILE) void k_units_rank(SortedGroups g, uint32_t G,
 
 void launch_units_rank(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t L, const uint64_t* S,
                        const GroupsOut& out, const UnitTable& ops, uint64_t maxOps, const UnitTable& keys,
-                       unsigned long long* counts, uint32_t* err, const ScoreRankArgs& sr) {
+                       unsigned long long* counts, uint32_t* err, const ScoreRankArgs& sr, const UnitsGuard& guard) {
   const uint32_t nrank = (sr.n + kRankPerBlock - 1) / kRankPerBlock;
-  const uint32_t ngw = (uint32_t)std::max<uint64_t>(1, (G + TILE - 1) / TILE);
+  const uint64_t gcap = guard.G ? guard.gmax : G;  // groups the weight part covers
+  const uint32_t ngw = (uint32_t)std::max<uint64_t>(1, (gcap + TILE - 1) / TILE);
   hipLaunchKernelGGL(k_units_rank, dim3(1 + nrank + ngw), dim3(TILE), (size_t)sr.n * 12, s, g, (uint32_t)G, P,
-                     (uint32_t)L, S, out, ops, maxOps, keys, counts, err, sr, nrank);
+                     (uint32_t)L, S, out, ops, maxOps, keys, counts, err, sr, nrank, guard);
 }
 
 void launch_units(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t P, uint64_t L, const uint64_t* S,

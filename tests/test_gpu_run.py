@@ -171,3 +171,65 @@ def test_repeated_runs_with_pass_a_carries(A, P):
             assert np.array_equal(g["count"].cpu().numpy().view(np.uint64), o["count"]), "count"
     finally:
         ag.close()
+
+
+def _run_vs_separate(key, app, ph, dur, c, P, sk, s, path="auto", label=""):
+    n = key.size
+    k, a, p, d = _dev(key, np.int32), _dev(app, np.int32), _dev(ph, np.uint8), _dev(dur, np.int64)
+    dc, dsk, dsv = _dev(c, np.int32), _dev(sk, np.int32), _dev(s, np.float64)
+    mg = 2 * n
+    ag = X.Aggregator(P, dc, max_events=n, max_groups=mg, max_keys=n, max_score=sk.size, path=path)
+    try:
+        res = ag.run(k, a, p, d, ag.group_buffers(mg), dsk, dsv, _score_bufs(sk.size))
+        run_g = {kk: v.clone() for kk, v in res["groups"].items()}
+        run_s = {kk: (v.clone() if torch.is_tensor(v) else v) for kk, v in res["score"].items()}
+        counts = (ag.num_ops, ag.num_keys, ag.path_used())
+        ag.reset()
+        ag.aggregate(k, a, p, d)
+        sep_g = ag.normalize(out=ag.group_buffers(mg))
+        sep_s = ag.score(dsk, dsv)
+        assert counts == (ag.num_ops, ag.num_keys, ag.path_used()), label
+        for kk in sep_g:
+            _same(run_g[kk], sep_g[kk], label + " " + kk)
+        for kk in ("op", "op_weight", "op_score"):
+            _same(run_s[kk], sep_s[kk], label + " score " + kk)
+        assert run_s["s_agg"] == sep_s["s_agg"], label
+        return run_g["key"].numel(), counts[2]
+    finally:
+        ag.close()
+
+
+def test_run_more_groups_than_the_one_workgroup_unit_kernel():
+    """4300 keys x 2 phases: the LDS engine orders 8600 groups in one launch,
+    more than the one-workgroup unit kernel takes, so the normalisation the
+    one-call path starts before the group-by's readback is dropped and
+    redone by the general one."""
+    rng = np.random.default_rng(7)
+    n, P, A = 1 << 20, 2, 64
+    keys = np.array([(1 + i // 50) << 16 | (i % 50) for i in range(4300)], np.uint32)
+    key = keys[rng.integers(0, keys.size, n)]
+    key[: keys.size] = keys  # every key at least once
+    app = rng.integers(0, A, n).astype(np.uint32)
+    ph = np.tile(np.array([0, 1], np.uint8), n // 2)
+    dur = rng.integers(1, 10 ** 6, n).astype(np.int64)
+    c = rng.integers(1, 1000, A).astype(np.uint32)
+    s = rng.random(keys.size) * 0.9 + 0.05
+    H.say("atrex_run, 8600 groups through the LDS engine")
+    G, path = _run_vs_separate(key, app, ph, dur, c, P, keys, s, path="lds_hash", label="8600 groups")
+    assert G == 8600 and path == "lds_hash"
+
+
+def test_run_when_the_lds_engine_falls_back():
+    """1M distinct keys forced through the LDS engine: the spill regions
+    overflow and the group-by falls back to partitioning every event, so the
+    started normalisation is dropped; atrex_run still matches the separate
+    calls."""
+    cfg = synth.CONFIGS[2]
+    ev = synth.events(cfg, n=1 << 23)
+    c = synth.app_weights(cfg)
+    keys = synth.key_space(cfg)[:4096]
+    s = synth.scores(cfg, keys, nan_frac=0.1)
+    H.say("atrex_run, LDS engine fallback")
+    G, path = _run_vs_separate(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, cfg["num_phases"], keys, s,
+                               path="lds_hash", label="fallback")
+    assert path == "lds_hash+radix_all"
