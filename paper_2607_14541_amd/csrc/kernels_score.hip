@@ -94,6 +94,7 @@ __global__ __launch_bounds__(NT) void k_score_final(const uint32_t* __restrict__
   const uint64_t nops_trace = min((uint64_t)*nops_ptr, maxOps);
   const bool opid_lds = nops_trace <= kScoreOpsLds;
   __shared__ uint32_t s_w[NW];
+  __shared__ uint32_t s_hbits[kScoreRankMax / 32];  // bit i: unit i starts an operator run
   __shared__ uint64_t s_u[2 * NW];
   __shared__ double s_cs[NW], s_cc[NW];
   const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -101,6 +102,7 @@ __global__ __launch_bounds__(NT) void k_score_final(const uint32_t* __restrict__
     s_S[j] = sorted_S[j];
     s_op[j] = sorted_op[j];
   }
+  for (uint32_t j = tid; j < kScoreRankMax / 32; j += NT) s_hbits[j] = 0;
   if (opid_lds)
     for (uint32_t j = tid; j < (uint32_t)nops_trace; j += NT) s_opid[j] = opt.id[j];
   __syncthreads();
@@ -112,8 +114,12 @@ __global__ __launch_bounds__(NT) void k_score_final(const uint32_t* __restrict__
     const uint32_t i = b + j;
     if (i < e && (i == 0 || s_op[i - 1] != s_op[i])) hmask |= 1u << j;
   }
+  if (hmask) {  // this thread's run heads into the bitmap (its units may span two words)
+    atomicOr(&s_hbits[b >> 5], hmask << (b & 31));
+    if ((b & 31) + per > 32) atomicOr(&s_hbits[(b >> 5) + 1], hmask >> (32 - (b & 31)));
+  }
   uint32_t nops;
-  const uint32_t ob = block_exscan(__popc(hmask), s_w, nops);
+  const uint32_t ob = block_exscan(__popc(hmask), s_w, nops);  // its barriers also publish the bitmap
   // operator runs starting here: median of the correct S_j (Eq. (5)) and U_i
   u128 U[SC_PER];
   double Si[SC_PER];
@@ -124,12 +130,25 @@ __global__ __launch_bounds__(NT) void k_score_final(const uint32_t* __restrict__
     Si[j] = 0.0;
     if (!((hmask >> j) & 1u)) continue;
     const uint32_t i = b + j, op = s_op[i];
-    uint32_t lo = i, hi = n;  // run end: first index with a larger operator
-    while (lo < hi) {
-      const uint32_t mid = (lo + hi) / 2;
-      if (s_op[mid] <= op) lo = mid + 1; else hi = mid;
+    // run end: the next run head (the bitmap's next set bit, looked for in
+    // four words), else a binary search for the first larger operator
+    uint32_t re = n, lo, hi;
+    {
+      uint32_t wi = (i + 1) >> 5;
+      uint32_t bits = i + 1 < n ? s_hbits[wi] & (~0u << ((i + 1) & 31)) : 0u;
+      for (int t = 0; t < 3 && !bits && (wi + 1) * 32 < n; ++t) bits = s_hbits[++wi];
+      if (bits) {
+        re = min(n, wi * 32 + (uint32_t)__builtin_ctz(bits));
+      } else if ((wi + 1) * 32 < n) {
+        lo = (wi + 1) * 32;
+        hi = n;
+        while (lo < hi) {
+          const uint32_t mid = (lo + hi) / 2;
+          if (s_op[mid] <= op) lo = mid + 1; else hi = mid;
+        }
+        re = lo;
+      }
     }
-    const uint32_t re = lo;
     lo = i;
     hi = re;  // first NaN of the run (NaN sorts last)
     while (lo < hi) {

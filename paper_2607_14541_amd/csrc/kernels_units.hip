@@ -421,8 +421,10 @@ __device__ __forceinline__ void units_small_body(const SortedGroups& g, uint32_t
   }
   const uint32_t nkeys = ctot & 0xFFFFu, nops = ctot >> 16;
   const bool ops_fit = nops <= maxOps;
-  // runs ending in this thread: totals, U = (L / |Phi|) * sum W (Eq. (3))
+  // runs ending in this thread: totals, U = (L / |Phi|) * sum W (Eq. (3));
+  // RN(U_k) of the key runs is kept for the weights
   u128 sumUk = 0, sumU = 0;
+  double dUk[SM_PER];
   {
     u128 kv = kin_v;  // a run continued from the previous thread starts with its tail
     uint32_t km = kin_m;
@@ -430,6 +432,7 @@ __device__ __forceinline__ void units_small_body(const SortedGroups& g, uint32_t
     uint32_t kidx = cc & 0xFFFFu, oidx = cc >> 16;  // heads so far
 #pragma unroll
     for (int j = 0; j < SM_PER; ++j) {
+      dUk[j] = 0.0;
       if (i0 + j >= G) continue;
       const bool kf = (kh >> j) & 1, of = (oh >> j) & 1;
       kv = (kf ? (u128)0 : kv) + W[j];
@@ -442,6 +445,7 @@ __device__ __forceinline__ void units_small_body(const SortedGroups& g, uint32_t
         keys.id[kidx - 1] = key[j];
         store_u128(keys.U, kidx - 1, U);
         sumUk += U;
+        dUk[j] = u128_to_f64(U);
       }
       if ((oe >> j) & 1) {
         const u128 U = (u128)lcm_over(L, (uint32_t)__popc(orr.m)) * orr.v;
@@ -457,13 +461,14 @@ __device__ __forceinline__ void units_small_body(const SortedGroups& g, uint32_t
   const u128 totUk = tile_sum_u128(sumUk, s_lo, s_hi);
   // w_i = RN(U_i) / RN(sum U), omega_k = RN(U_k) / RN(sum U_k): this thread's own runs
   {
+    const double dTk = u128_to_f64(totUk);
     uint32_t kidx = cc & 0xFFFFu, oidx = cc >> 16;
 #pragma unroll
     for (int j = 0; j < SM_PER; ++j) {
       if (i0 + j >= G) continue;
       kidx += (kh >> j) & 1;
       oidx += (oh >> j) & 1;
-      if ((ke >> j) & 1) keys.w[kidx - 1] = ratio(load_u128(keys.U, kidx - 1), totUk);
+      if ((ke >> j) & 1) keys.w[kidx - 1] = totUk == 0 ? 0.0 : dUk[j] / dTk;
       if (ops_fit && ((oe >> j) & 1)) ops.w[oidx - 1] = ratio(load_u128(ops.U, oidx - 1), totU);
     }
   }
