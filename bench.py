@@ -70,7 +70,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=1, help="workload index (0..4)")
     ap.add_argument("--path", default="auto", choices=["auto", "lds_hash", "global_hash", "radix_sort"])
-    ap.add_argument("--cpu-sample-log2", type=int, default=24,
+    ap.add_argument("--cpu-sample-log2", type=int, default=26,
                     help="events of the workload the CPU oracle is timed on (2^k)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
