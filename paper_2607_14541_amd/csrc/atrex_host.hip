@@ -640,8 +640,10 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
   uint64_t* T = c->at<uint64_t>(L.T);
   uint64_t* scale = c->at<uint64_t>(L.scale);
   if (L.passA == 0 && vec_ok) {
-    const uint64_t per_cu = std::max<uint64_t>(1, std::min<uint64_t>(2, (kLdsBytes - 1024) / (GA * 8)));
-    uint64_t nb = std::min<uint64_t>((uint64_t)c->cus * per_cu, kPartialRowsMax);
+    // one workgroup per CU (two groups of loads in flight per lane): two per
+    // CU ran as one after the other (the SIMDs favour the older one) and
+    // doubled the partial rows for the reduce
+    uint64_t nb = std::min<uint64_t>((uint64_t)c->cus, kPartialRowsMax);
     nb = std::max<uint64_t>(1, std::min<uint64_t>(nb, (n / 4 + kPassAThreads - 1) / kPassAThreads));
     TIMED(c, "pass_a", n,
           launch_pass_a_lds(s, d, A, P, (uint32_t)nb, c->at<unsigned long long>(L.partA),

@@ -31,13 +31,15 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_lds(EventsDev ev, uint32_t A, 
   const uint64_t n = ev.n, n4 = n / 4;
   const uint64_t stride = (uint64_t)gridDim.x * BLOCK;
   bool bad = false;
-  // the next group's loads are issued before the current group is added
+  // the next two groups' loads are issued before the current group is added
   uint64_t q = (uint64_t)blockIdx.x * BLOCK + threadIdx.x;
-  Ev4 nxt;
+  Ev4 nxt, nxt2;
   if (q < n4) load4<false>(ev.key, ev.app, ev.phase, ev.dur, q * 4, nxt);
+  if (q + stride < n4) load4<false>(ev.key, ev.app, ev.phase, ev.dur, (q + stride) * 4, nxt2);
   for (; q < n4; q += stride) {
     const Ev4 e = nxt;
-    if (q + stride < n4) load4<false>(ev.key, ev.app, ev.phase, ev.dur, (q + stride) * 4, nxt);
+    nxt = nxt2;
+    if (q + 2 * stride < n4) load4<false>(ev.key, ev.app, ev.phase, ev.dur, (q + 2 * stride) * 4, nxt2);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const bool ok = e.app[j] < A && e.ph[j] < P && e.dur[j] >= 0;
