@@ -324,10 +324,14 @@ __device__ __forceinline__ Seg seg_shfl_up(const Seg& x, int d) {
   return y;
 }
 
+// MODE: 1 = the key level only (U_k, omega_k, the key count), 2 = the
+// operator level only (U_i, w_i, the operator count), 3 = both.
+template <int MODE>
 __device__ __forceinline__ void units_small_body(const SortedGroups& g, uint32_t G, uint32_t L, const UnitTable& ops,
                                                  uint64_t maxOps, const UnitTable& keys,
                                                  unsigned long long* __restrict__ counts,
                                                  uint32_t* __restrict__ err) {
+  constexpr bool KEYS = (MODE & 1) != 0, OPS = (MODE & 2) != 0;
   __shared__ Seg s_ow[NW];
   __shared__ uint32_t s_n[NW];
   __shared__ uint64_t s_kt[3 * NW];  // each wave's last key tail: sum (lo, hi), phase mask
@@ -356,10 +360,10 @@ __device__ __forceinline__ void units_small_body(const SortedGroups& g, uint32_t
     const uint32_t prev = j == 0 ? kprev : key[j - 1];
     const uint32_t nx = j + 1 < SM_PER ? key[j + 1] : knext;
     const bool last = i + 1 == G;
-    if (i == 0 || prev != key[j]) kh |= 1u << j;
-    if (i == 0 || (prev >> 16) != (key[j] >> 16)) oh |= 1u << j;
-    if (last || nx != key[j]) ke |= 1u << j;
-    if (last || (nx >> 16) != (key[j] >> 16)) oe |= 1u << j;
+    if (KEYS && (i == 0 || prev != key[j])) kh |= 1u << j;
+    if (OPS && (i == 0 || (prev >> 16) != (key[j] >> 16))) oh |= 1u << j;
+    if (KEYS && (last || nx != key[j])) ke |= 1u << j;
+    if (OPS && (last || (nx >> 16) != (key[j] >> 16))) oe |= 1u << j;
   }
   // key tail: W and phases after this thread's last key head (all its groups
   // when it has none)
@@ -371,34 +375,43 @@ __device__ __forceinline__ void units_small_body(const SortedGroups& g, uint32_t
   for (int j = 0; j < SM_PER; ++j) {
     if (i0 + j >= G) continue;
     const bool kf = (kh >> j) & 1, of = (oh >> j) & 1;
-    ktv = (kf ? (u128)0 : ktv) + W[j];
-    ktm = (kf ? 0u : ktm) | (1u << ph[j]);
-    oa = Seg{oa.f | (of ? 1u : 0u), (of ? (u128)0 : oa.v) + W[j], (of ? 0u : oa.m) | (1u << ph[j])};
+    if (KEYS) {
+      ktv = (kf ? (u128)0 : ktv) + W[j];
+      ktm = (kf ? 0u : ktm) | (1u << ph[j]);
+    }
+    if (OPS) oa = Seg{oa.f | (of ? 1u : 0u), (of ? (u128)0 : oa.v) + W[j], (of ? 0u : oa.m) | (1u << ph[j])};
   }
   // counts of key heads (low 16 bits) and operator heads (high 16 bits)
   const uint32_t cnt = __popc(kh) | (__popc(oh) << 16);
   Seg oi = oa;
   uint32_t ci = cnt;
   for (int d = 1; d < 64; d <<= 1) {
-    const Seg oy = seg_shfl_up(oi, d);
+    Seg oy{0, 0, 0};
+    if (OPS) oy = seg_shfl_up(oi, d);
     const uint32_t cy = __shfl_up(ci, d, 64);
     if (lane >= (uint32_t)d) {
-      oi = seg_cat(oy, oi);
+      if (OPS) oi = seg_cat(oy, oi);
       ci += cy;
     }
   }
   // the previous thread's key tail (the previous wave's last lane through LDS)
-  u128 kin_v = shfl_up_u128(ktv, 1);
-  uint32_t kin_m = __shfl_up(ktm, 1, 64);
+  u128 kin_v = 0;
+  uint32_t kin_m = 0;
+  if (KEYS) {
+    kin_v = shfl_up_u128(ktv, 1);
+    kin_m = __shfl_up(ktm, 1, 64);
+  }
   if (lane == 63) {
-    s_ow[wave] = oi;
+    if (OPS) s_ow[wave] = oi;
     s_n[wave] = ci;
-    s_kt[3 * wave] = (uint64_t)ktv;
-    s_kt[3 * wave + 1] = (uint64_t)(ktv >> 64);
-    s_kt[3 * wave + 2] = ktm;
+    if (KEYS) {
+      s_kt[3 * wave] = (uint64_t)ktv;
+      s_kt[3 * wave + 1] = (uint64_t)(ktv >> 64);
+      s_kt[3 * wave + 2] = ktm;
+    }
   }
   __syncthreads();
-  if (lane == 0 && wave > 0) {
+  if (KEYS && lane == 0 && wave > 0) {
     kin_v = make_u128(s_kt[3 * (wave - 1)], s_kt[3 * (wave - 1) + 1]);
     kin_m = (uint32_t)s_kt[3 * (wave - 1) + 2];
   }
@@ -406,16 +419,17 @@ __device__ __forceinline__ void units_small_body(const SortedGroups& g, uint32_t
   uint32_t cc = 0, ctot = 0;
   for (uint32_t w = 0; w < NW; ++w) {
     if (w < wave) {
-      oc = seg_cat(oc, s_ow[w]);
+      if (OPS) oc = seg_cat(oc, s_ow[w]);
       cc += s_n[w];
     }
     ctot += s_n[w];
   }
   {  // exclusive within the wave
-    const Seg oy = seg_shfl_up(oi, 1);
+    Seg oy{0, 0, 0};
+    if (OPS) oy = seg_shfl_up(oi, 1);
     const uint32_t cy = __shfl_up(ci, 1, 64);
     if (lane > 0) {
-      oc = seg_cat(oc, oy);
+      if (OPS) oc = seg_cat(oc, oy);
       cc += cy;
     }
   }
@@ -435,30 +449,35 @@ __device__ __forceinline__ void units_small_body(const SortedGroups& g, uint32_t
       dUk[j] = 0.0;
       if (i0 + j >= G) continue;
       const bool kf = (kh >> j) & 1, of = (oh >> j) & 1;
-      kv = (kf ? (u128)0 : kv) + W[j];
-      km = (kf ? 0u : km) | (1u << ph[j]);
-      orr = Seg{1u, (of ? (u128)0 : orr.v) + W[j], (of ? 0u : orr.m) | (1u << ph[j])};
-      kidx += kf;
-      oidx += of;
-      if ((ke >> j) & 1) {
-        const u128 U = (u128)lcm_over(L, (uint32_t)__popc(km)) * kv;
-        keys.id[kidx - 1] = key[j];
-        store_u128(keys.U, kidx - 1, U);
-        sumUk += U;
-        dUk[j] = u128_to_f64(U);
-      }
-      if ((oe >> j) & 1) {
-        const u128 U = (u128)lcm_over(L, (uint32_t)__popc(orr.m)) * orr.v;
-        if (ops_fit) {
-          ops.id[oidx - 1] = key[j] >> 16;
-          store_u128(ops.U, oidx - 1, U);
+      if (KEYS) {
+        kv = (kf ? (u128)0 : kv) + W[j];
+        km = (kf ? 0u : km) | (1u << ph[j]);
+        kidx += kf;
+        if ((ke >> j) & 1) {
+          const u128 U = (u128)lcm_over(L, (uint32_t)__popc(km)) * kv;
+          keys.id[kidx - 1] = key[j];
+          store_u128(keys.U, kidx - 1, U);
+          sumUk += U;
+          dUk[j] = u128_to_f64(U);
         }
-        sumU += U;
+      }
+      if (OPS) {
+        orr = Seg{1u, (of ? (u128)0 : orr.v) + W[j], (of ? 0u : orr.m) | (1u << ph[j])};
+        oidx += of;
+        if ((oe >> j) & 1) {
+          const u128 U = (u128)lcm_over(L, (uint32_t)__popc(orr.m)) * orr.v;
+          if (ops_fit) {
+            ops.id[oidx - 1] = key[j] >> 16;
+            store_u128(ops.U, oidx - 1, U);
+          }
+          sumU += U;
+        }
       }
     }
   }
-  const u128 totU = tile_sum_u128(sumU, s_lo, s_hi);
-  const u128 totUk = tile_sum_u128(sumUk, s_lo, s_hi);
+  u128 totU = 0, totUk = 0;
+  if (OPS) totU = tile_sum_u128(sumU, s_lo, s_hi);
+  if (KEYS) totUk = tile_sum_u128(sumUk, s_lo, s_hi);
   // w_i = RN(U_i) / RN(sum U), omega_k = RN(U_k) / RN(sum U_k): this thread's own runs
   {
     const double dTk = u128_to_f64(totUk);
@@ -468,14 +487,16 @@ __device__ __forceinline__ void units_small_body(const SortedGroups& g, uint32_t
       if (i0 + j >= G) continue;
       kidx += (kh >> j) & 1;
       oidx += (oh >> j) & 1;
-      if ((ke >> j) & 1) keys.w[kidx - 1] = totUk == 0 ? 0.0 : dUk[j] / dTk;
-      if (ops_fit && ((oe >> j) & 1)) ops.w[oidx - 1] = ratio(load_u128(ops.U, oidx - 1), totU);
+      if (KEYS && ((ke >> j) & 1)) keys.w[kidx - 1] = totUk == 0 ? 0.0 : dUk[j] / dTk;
+      if (OPS && ops_fit && ((oe >> j) & 1)) ops.w[oidx - 1] = ratio(load_u128(ops.U, oidx - 1), totU);
     }
   }
   if (tid == 0) {
-    counts[0] = nops;
-    counts[1] = nkeys;
-    if (!ops_fit) atomicOr(err, ATREX_ERRBIT_CAPACITY);
+    if (OPS) {
+      counts[0] = nops;
+      if (!ops_fit) atomicOr(err, ATREX_ERRBIT_CAPACITY);
+    }
+    if (KEYS) counts[1] = nkeys;
   }
 }
 
@@ -483,13 +504,13 @@ __global__ __launch_bounds__(TILE) void k_units_small(SortedGroups g, uint32_t G
                                                       uint64_t maxOps, UnitTable keys,
                                                       unsigned long long* __restrict__ counts,
                                                       uint32_t* __restrict__ err) {
-  units_small_body(g, G, L, ops, maxOps, keys, counts, err);
+  units_small_body<3>(g, G, L, ops, maxOps, keys, counts, err);
 }
 
-// One launch for three independent steps of the one-call path: workgroup 0
-// runs the one-workgroup unit kernel (the longest), the next nrank the score
-// ranking, the rest the group weights, so that the short ones run beside the
-// long one on other CUs.
+// One launch for three independent steps of the one-call path: workgroups 0
+// and 1 run the one-workgroup unit kernel's key level and operator level (the
+// longest parts), the next nrank the score ranking, the rest the group
+// weights, so that all of them run side by side on different CUs.
 // With guard.G set, the group count comes from the device and the unit and
 // group-weight parts run only when the ordering finished in one launch with a
 // clean error word and at most guard.gmax groups (the caller decides
@@ -509,12 +530,14 @@ __global__ __launch_bounds__(TILE) void k_units_rank(SortedGroups g, uint32_t G,
                gd <= guard.gmax;
     G = units_ok ? (uint32_t)gd : 0u;
   }
-  if (blockIdx.x == 0) {
-    if (units_ok) units_small_body(g, G, L, ops, maxOps, keys, counts, err);
-  } else if (blockIdx.x <= nrank) {
-    score_rank_block(blockIdx.x - 1, sr.score_key, sr.S, sr.n, sr.sorted_op, sr.sorted_S, sr.err, smem64);
+  if (blockIdx.x == 0) {  // the key level
+    if (units_ok) units_small_body<1>(g, G, L, ops, maxOps, keys, counts, err);
+  } else if (blockIdx.x == 1) {  // the operator level
+    if (units_ok) units_small_body<2>(g, G, L, ops, maxOps, keys, counts, err);
+  } else if (blockIdx.x <= nrank + 1) {
+    score_rank_block(blockIdx.x - 2, sr.score_key, sr.S, sr.n, sr.sorted_op, sr.sorted_S, sr.err, smem64);
   } else if (units_ok) {
-    group_weights_at((blockIdx.x - 1 - nrank) * TILE + threadIdx.x, g, G, P, S, out);
+    group_weights_at((blockIdx.x - 2 - nrank) * TILE + threadIdx.x, g, G, P, S, out);
   }
 }
 
@@ -526,7 +549,7 @@ void launch_units_rank(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_
   const uint32_t nrank = (sr.n + kRankPerBlock - 1) / kRankPerBlock;
   const uint64_t gcap = guard.G ? guard.gmax : G;  // groups the weight part covers
   const uint32_t ngw = (uint32_t)std::max<uint64_t>(1, (gcap + TILE - 1) / TILE);
-  hipLaunchKernelGGL(k_units_rank, dim3(1 + nrank + ngw), dim3(TILE), (size_t)sr.n * 12, s, g, (uint32_t)G, P,
+  hipLaunchKernelGGL(k_units_rank, dim3(2 + nrank + ngw), dim3(TILE), (size_t)sr.n * 12, s, g, (uint32_t)G, P,
                      (uint32_t)L, S, out, ops, maxOps, keys, counts, err, sr, nrank, guard);
 }
 
