@@ -114,6 +114,27 @@ __device__ __forceinline__ double u128_to_f64(u128 x) {
   return hi ? ldexp(r, 64 - s) : r;
 }
 
+// --- global -> LDS staging by one workgroup -------------------------------------
+// dst[j] = f(src[j]) for j < n, by the NT threads of the workgroup; each
+// thread issues its KL loads of a round before the first store, so a round
+// costs one memory latency instead of KL.
+template <uint32_t NT, int KL, typename D, typename T, typename F>
+__device__ __forceinline__ void lds_stage(D* dst, const T* __restrict__ src, uint32_t n, F f) {
+  for (uint32_t j0 = 0; j0 < n; j0 += KL * NT) {
+    T v[KL];
+#pragma unroll
+    for (int k = 0; k < KL; ++k) {
+      const uint32_t j = j0 + (uint32_t)k * NT + threadIdx.x;
+      v[k] = j < n ? src[j] : T();
+    }
+#pragma unroll
+    for (int k = 0; k < KL; ++k) {
+      const uint32_t j = j0 + (uint32_t)k * NT + threadIdx.x;
+      if (j < n) dst[j] = f(v[k]);
+    }
+  }
+}
+
 // --- hashing ----------------------------------------------------------------
 // Multiplicative (Fibonacci) hash; the slot is taken from the high bits.
 __device__ __forceinline__ uint32_t hash_mul(uint32_t k) { return k * 0x9E3779B1u; }

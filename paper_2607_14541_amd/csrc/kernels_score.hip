@@ -98,13 +98,10 @@ __global__ __launch_bounds__(NT) void k_score_final(const uint32_t* __restrict__
   __shared__ uint64_t s_u[2 * NW];
   __shared__ double s_cs[NW], s_cc[NW];
   const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (uint32_t j = tid; j < n; j += NT) {
-    s_S[j] = sorted_S[j];
-    s_op[j] = sorted_op[j];
-  }
+  lds_stage<NT, 8>(s_S, sorted_S, n, [](double v) { return v; });
+  lds_stage<NT, 8>(s_op, sorted_op, n, [](uint32_t v) { return v; });
   for (uint32_t j = tid; j < kScoreRankMax / 32; j += NT) s_hbits[j] = 0;
-  if (opid_lds)
-    for (uint32_t j = tid; j < (uint32_t)nops_trace; j += NT) s_opid[j] = opt.id[j];
+  if (opid_lds) lds_stage<NT, 8>(s_opid, opt.id, (uint32_t)nops_trace, [](uint32_t v) { return v; });
   __syncthreads();
   const uint32_t per = (n + NT - 1) / NT;  // <= SC_PER
   const uint32_t b = min(n, tid * per), e = min(n, b + per);

@@ -26,10 +26,8 @@ __device__ __forceinline__ void score_rank_block(uint32_t blk, const uint32_t* _
   uint64_t* s_sb = smem64;                  // [n]
   uint32_t* s_key = (uint32_t*)(s_sb + n);  // [n]
   const uint32_t tid = threadIdx.x, lane = tid & 63;
-  for (uint32_t j = tid; j < n; j += kRankThreads) {
-    s_sb[j] = score_order_bits(S[j]);
-    s_key[j] = score_key[j];
-  }
+  lds_stage<kRankThreads, 8>(s_sb, S, n, [](double v) { return score_order_bits(v); });
+  lds_stage<kRankThreads, 8>(s_key, score_key, n, [](uint32_t k) { return k; });
   __syncthreads();
   const uint32_t m = blk * kRankPerBlock + (tid >> 6);  // this wave's unit
   if (m >= n) return;                                 // wave-uniform
