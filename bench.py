@@ -66,8 +66,8 @@ def traffic_from_profile(slug: str, kernel: str, n: int):
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=1, help="workload index (0..4)")
     ap.add_argument("--path", default="auto", choices=["auto", "lds_hash", "global_hash", "radix_sort"])
     ap.add_argument("--cpu-sample-log2", type=int, default=26,
