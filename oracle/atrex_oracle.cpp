@@ -21,6 +21,7 @@
 #include <cstring>
 #include <map>
 #include <new>
+#include <thread>
 #include <utility>
 #include <vector>
 
@@ -284,6 +285,84 @@ int atrex_oracle_aggregate_events(atrex_oracle *o, const uint32_t *key,
     g.raw += (u128)(uint64_t)dur_ns[e];
   }
   /* S_phi = sum_k W[k, phi]. */
+  o->phase_total.assign(o->P, 0);
+  for (const auto &kv : o->group) o->phase_total[kv.first.second] += kv.second.wsum;
+  o->state = ST_AGGREGATED;
+  *num_groups = o->group.size();
+  return ATREX_ORACLE_OK;
+}
+
+/* The same group-by with the events split into `threads` contiguous ranges,
+ * one thread each.  Every thread fills private maps for its range (pass A,
+ * then, once the scale exists, pass B) and the maps are merged by exact
+ * integer addition, so the result is the single-threaded one bit for bit:
+ * every output is a sum over events, and integer addition is exact and
+ * order-free. */
+int atrex_oracle_aggregate_events_sharded(atrex_oracle *o, const uint32_t *key,
+                                          const uint32_t *app, const uint8_t *phase,
+                                          const int64_t *dur_ns, uint64_t n,
+                                          uint32_t threads, uint64_t *num_groups) {
+  if (!o || !num_groups || threads < 1) return ATREX_ORACLE_E_INVALID_ARG;
+  if (o->state != ST_INIT) return ATREX_ORACLE_E_STATE;
+  if (n >= ((uint64_t)1 << 31)) return ATREX_ORACLE_E_INVALID_ARG;
+  if (n > 0 && (!key || !app || !phase || !dur_ns)) return ATREX_ORACLE_E_INVALID_ARG;
+  typedef std::pair<uint32_t, uint32_t> Key;
+  const uint64_t T = threads;
+  auto lo_of = [&](uint64_t t) { return n * t / T; };
+  std::vector<int> bad(T, 0);
+  std::vector<std::map<Key, AppAcc> > apps(T);
+  std::vector<std::thread> pool;
+  /* O0 and pass A (Eq. (2)) per range. */
+  for (uint64_t t = 0; t < T; ++t)
+    pool.emplace_back([&, t]() {
+      for (uint64_t e = lo_of(t); e < lo_of(t + 1); ++e) {
+        if (app[e] >= o->A || phase[e] >= o->P || dur_ns[e] < 0) { bad[t] = 1; return; }
+        AppAcc &acc = apps[t][Key(app[e], (uint32_t)phase[e])];
+        acc.total += (u128)(uint64_t)dur_ns[e];
+        acc.count += 1;
+      }
+    });
+  for (auto &th : pool) th.join();
+  pool.clear();
+  for (uint64_t t = 0; t < T; ++t)
+    if (bad[t]) { o->app.clear(); return ATREX_ORACLE_E_OUT_OF_RANGE; }
+  for (uint64_t t = 0; t < T; ++t)
+    for (const auto &kv : apps[t]) {
+      AppAcc &acc = o->app[kv.first];
+      acc.total += kv.second.total;
+      acc.count += kv.second.count;
+    }
+  apps.clear();
+  /* Scale, Eq. (3), as in the single-threaded group-by. */
+  for (const auto &kv : o->app) {
+    uint64_t m;
+    int32_t r;
+    scale_entry(o->c[kv.first.first], o->C, kv.second.total, &m, &r);
+    o->mant[kv.first] = m;
+    o->rho[kv.first] = r;
+  }
+  /* Pass B, Eq. (2)-(3), per range (the scale maps are only read). */
+  std::vector<std::map<Key, GroupAcc> > groups(T);
+  for (uint64_t t = 0; t < T; ++t)
+    pool.emplace_back([&, t]() {
+      for (uint64_t e = lo_of(t); e < lo_of(t + 1); ++e) {
+        const Key ap(app[e], (uint32_t)phase[e]);
+        const u128 v = event_share(dur_ns[e], o->mant.at(ap), o->rho.at(ap));
+        if (v > ((u128)1 << 96)) std::abort(); /* v <= d * r <= 2^96 */
+        GroupAcc &g = groups[t][Key(key[e], (uint32_t)phase[e])];
+        g.count += 1;
+        g.wsum += v;
+        g.raw += (u128)(uint64_t)dur_ns[e];
+      }
+    });
+  for (auto &th : pool) th.join();
+  for (uint64_t t = 0; t < T; ++t)
+    for (const auto &kv : groups[t]) {
+      GroupAcc &g = o->group[kv.first];
+      g.count += kv.second.count;
+      g.wsum += kv.second.wsum;
+      g.raw += kv.second.raw;
+    }
   o->phase_total.assign(o->P, 0);
   for (const auto &kv : o->group) o->phase_total[kv.first.second] += kv.second.wsum;
   o->state = ST_AGGREGATED;

@@ -57,6 +57,16 @@ int atrex_oracle_aggregate_events(atrex_oracle *o, const uint32_t *key,
                                   const int64_t *dur_ns, uint64_t n,
                                   uint64_t *num_groups);
 
+/* The same group-by with the events split into `threads` >= 1 contiguous
+ * ranges, each summed by its own thread into private maps that are then merged
+ * by exact integer addition: the outputs equal the single-threaded ones bit
+ * for bit.  Used to time the oracle on every host core and to evaluate it on
+ * the largest workloads. */
+int atrex_oracle_aggregate_events_sharded(atrex_oracle *o, const uint32_t *key,
+                                          const uint32_t *app, const uint8_t *phase,
+                                          const int64_t *dur_ns, uint64_t n,
+                                          uint32_t threads, uint64_t *num_groups);
+
 /* Groups ascending by (key, phase); arrays sized num_groups (lohi: 2x). */
 int atrex_oracle_phase_normalize(atrex_oracle *o, uint32_t *key, uint8_t *phase,
                                  uint64_t *count, uint64_t *wsum_lohi,

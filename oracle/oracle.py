@@ -29,7 +29,7 @@ def build(force: bool = False) -> str:
     """Compile the oracle with g++ (plain C++17, -O2)."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", "-Wall",
+        subprocess.check_call(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", "-Wall", "-pthread",
                                "-o", tmp, _SRC])
         os.replace(tmp, _LIB)
     return _LIB
@@ -47,6 +47,7 @@ def lib() -> ctypes.CDLL:
         P, U32, U64 = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64
         L.atrex_oracle_init.argtypes = [U32, U32, P, ctypes.POINTER(P)]
         L.atrex_oracle_aggregate_events.argtypes = [P, P, P, P, P, U64, P]
+        L.atrex_oracle_aggregate_events_sharded.argtypes = [P, P, P, P, P, U64, U32, P]
         L.atrex_oracle_phase_normalize.argtypes = [P, P, P, P, P, P, P, P]
         L.atrex_oracle_app_totals.argtypes = [P, P, P, P, P]
         L.atrex_oracle_num_ops.argtypes = [P, P]
@@ -55,7 +56,7 @@ def lib() -> ctypes.CDLL:
         L.atrex_oracle_key_weights.argtypes = [P, P, P, P]
         L.atrex_oracle_weighted_score.argtypes = [P, P, P, U64, P, P, P, P, P]
         L.atrex_oracle_destroy.argtypes = [P]
-        for name in ("init", "aggregate_events", "phase_normalize", "app_totals", "num_ops",
+        for name in ("init", "aggregate_events", "aggregate_events_sharded", "phase_normalize", "app_totals", "num_ops",
                      "op_weights", "num_keys", "key_weights", "weighted_score"):
             getattr(L, "atrex_oracle_" + name).restype = ctypes.c_int
         L.atrex_oracle_destroy.restype = None
@@ -81,8 +82,10 @@ def u128_to_int(lohi: np.ndarray) -> list:
 
 
 def run(key, app, phase, dur_ns, app_weight_q16, num_phases, score_key=None, s=None,
-        want_units: bool = True) -> dict:
-    """Run the oracle end to end.  Raises OracleError on a non-OK status."""
+        want_units: bool = True, threads: int = 1) -> dict:
+    """Run the oracle end to end.  Raises OracleError on a non-OK status.
+    threads > 1 splits the group-by's events over that many threads (the
+    sharded form: identical results)."""
     L = lib()
     key = np.ascontiguousarray(key, dtype=np.uint32)
     app = np.ascontiguousarray(app, dtype=np.uint32)
@@ -98,8 +101,12 @@ def run(key, app, phase, dur_ns, app_weight_q16, num_phases, score_key=None, s=N
         raise OracleError(st, "init")
     try:
         G = ctypes.c_uint64()
-        st = L.atrex_oracle_aggregate_events(ctx, _ptr(key), _ptr(app), _ptr(phase), _ptr(dur_ns),
-                                             n, ctypes.byref(G))
+        if threads > 1:
+            st = L.atrex_oracle_aggregate_events_sharded(ctx, _ptr(key), _ptr(app), _ptr(phase), _ptr(dur_ns),
+                                                         n, int(threads), ctypes.byref(G))
+        else:
+            st = L.atrex_oracle_aggregate_events(ctx, _ptr(key), _ptr(app), _ptr(phase), _ptr(dur_ns),
+                                                 n, ctypes.byref(G))
         if st != OK:
             raise OracleError(st, "aggregate_events")
         g = G.value
