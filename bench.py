@@ -4,12 +4,19 @@
 One step = the whole path over one batch of events already resident in HBM:
 pass A (per-(app, phase) time, Eq. (2)), the Q96 scale (Eq. (3)), pass B
 (per-(key, phase) shares), compaction/ordering, per-phase normalisation and
-Eq. (3) per operator and key, and the importance-weighted score (Eq. (4)-(6)).
-Prints one JSON line: throughput in G events/s, the roofline of the dominant
-kernel (per-kernel hipEvent times from the library, taken on the stream the
-kernels run on) and the CPU oracle timed on a bounded sample.
+Eq. (3) per operator and key, and the importance-weighted score (Eq. (4)-(6)),
+in one library call (atrex_run).  The default workload is the largest: 1B
+events over 64k Zipf(0.9) keys, 3 phases, 100k apps.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1] [--path auto]
+Prints one JSON line: throughput in G events/s; the roofline of the dominant
+kernel (the event bytes the method reads -- 13 per event in pass A, 17 in
+pass B -- over its hipEvent time, taken by the library on the stream the
+kernels run on); a parity self-check of the timed step's outputs against the
+CPU oracle's (digests written by tests/golden/make_digests.py; a mismatch
+makes the run fail); and the CPU oracle timed on bounded samples of the same
+workload, on one core and sharded over the host's cores.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--path auto]
 """
 from __future__ import annotations
 
@@ -17,6 +24,7 @@ import argparse
 import hashlib
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -26,15 +34,21 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E peak, GB/s
 BYTES_PASS_A = 13              # app u32 + phase u8 + dur i64 per event
 BYTES_PASS_B = 17              # key u32 + app u32 + phase u8 + dur i64 per event
-# algorithmic HBM bytes per event of the streaming kernels: the event fields
-# each one must read, plus the 16-byte partition records written and re-read
-KERNEL_BYTES = {"pass_a": BYTES_PASS_A, "pass_a_global": BYTES_PASS_A,
-                "pass_b_lds": BYTES_PASS_B, "pass_b_global": BYTES_PASS_B,
-                "part_hist": 4, "part_scatter": BYTES_PASS_B + 16, "part_aggregate": 16}
+# the event bytes of the method each kernel reads (the kernels that stream
+# the events); the other kernels' traffic is the engine's own
+METHOD_BYTES = {"pass_a": BYTES_PASS_A, "pass_a_range": BYTES_PASS_A, "pass_a_global": BYTES_PASS_A,
+                "pass_b_lds": BYTES_PASS_B, "pass_b_global": BYTES_PASS_B, "part_scatter": BYTES_PASS_B}
+PASS_A_KERNELS = ("pass_a", "pass_a_range", "pass_a_global", "pass_a_reduce", "scale")
+# bytes per event each partition-engine kernel moves besides the method's:
+# histogram (key re-read), scatter (16-byte record written), aggregate (record read)
+ENGINE_BYTES = {"part_hist": 4, "part_scatter": 16, "part_aggregate": 16}
 KERNEL_SOURCES = ["paper_2607_14541_amd/csrc/kernels_aggregate.hip",
                   "paper_2607_14541_amd/csrc/kernels_rows.hip",
                   "paper_2607_14541_amd/csrc/atrex_kernels.h",
                   "paper_2607_14541_amd/csrc/atrex_device.hpp"]
+DEFAULT_STEPS = {0: 200, 1: 200, 2: 40, 3: 20, 4: 30}
+# events of each workload the CPU oracle is timed on: (one thread, all threads)
+CPU_SAMPLE_LOG2 = {0: (20, 20), 1: (24, 26), 2: (20, 22), 3: (21, 23), 4: (24, 26)}
 
 
 def log(*a):
@@ -63,21 +77,41 @@ def traffic_from_profile(slug: str, kernel: str, n: int):
     return k.get("hbm_bytes_per_launch")
 
 
+def host_threads() -> int:
+    """Threads for the sharded CPU oracle: the host's share of cores (the
+    OMP_NUM_THREADS the environment sets, else the CPUs this process may run
+    on), at most 16."""
+    env = os.environ.get("OMP_NUM_THREADS")
+    n = int(env) if env and env.isdigit() else len(os.sched_getaffinity(0))
+    return max(1, min(16, n))
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=1, help="workload index (0..4)")
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=3, help="workload index (0..4); 3 = 1B events")
     ap.add_argument("--path", default="auto", choices=["auto", "lds_hash", "global_hash", "radix_sort"])
-    ap.add_argument("--cpu-sample-log2", type=int, default=26,
-                    help="events of the workload the CPU oracle is timed on (2^k)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-parity", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(--gpus %d requested)" % args.gpus, file=sys.stderr)
         return 2
+    steps = args.steps if args.steps is not None else DEFAULT_STEPS[args.config]
 
     import numpy as np
     import torch
@@ -103,6 +137,8 @@ def main() -> int:
     d_sk = torch.from_numpy(keys.view(np.int32)).to(dev)
     d_s = torch.from_numpy(s).to(dev)
     torch.cuda.synchronize()
+    if args.no_cpu_baseline:
+        del ev
     max_groups = keys.size * P
 
     def make(timing: bool):
@@ -116,80 +152,128 @@ def main() -> int:
                 op_score=torch.empty(keys.size, dtype=torch.float64, device=dev))
     result = {}
 
-    def step(a, times=None):
-        if times is None:  # the whole path in one library call (atrex_run)
-            r = a.run(d_key, d_app, d_ph, d_dur, gbuf, d_sk, d_s, sbuf)
-            result["groups"], result["score"] = r["groups"], r["score"]
-            return
-        # per-kernel times: the calls one by one (times are kept per call)
-        a.reset()
-        a.aggregate(d_key, d_app, d_ph, d_dur)
-        if times is not None:
-            times.extend(a.kernel_times())
-        out = a.normalize(out=gbuf)
-        if times is not None:
-            times.extend(a.kernel_times())
-        result["groups"] = out
-        result["score"] = a.score(d_sk, d_s, out=sbuf)
-        if times is not None:
-            times.extend(a.kernel_times())
+    def step(a):  # the whole path in one library call (atrex_run)
+        r = a.run(d_key, d_app, d_ph, d_dur, gbuf, d_sk, d_s, sbuf)
+        result["groups"], result["score"] = r["groups"], r["score"]
 
     for _ in range(args.warmup):
         step(ag)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(steps):
         step(ag)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     elapsed = t1 - t0
-    ms_step = 1e3 * elapsed / args.steps
-    value = n * args.steps / elapsed / 1e9
-    log("step %.3f ms, %.2f G events/s, path %s" % (ms_step, value, ag.path_used()))
+    ms_step = 1e3 * elapsed / steps
+    value = n * steps / elapsed / 1e9
+    log("step %.3f ms, %.2f G events/s, path %s, one wait %s" % (ms_step, value, ag.path_used(), ag.one_wait))
 
-    # sanity of the timed result: every invocation counted, each phase sums to 1
-    g = result["groups"]
-    assert int(g["count"].sum().item()) == n, "event count mismatch"
-    wsum_phase = torch.zeros(P, dtype=torch.float64, device=dev).index_add_(0, g["phase"].long(), g["weight"])
-    assert torch.allclose(wsum_phase, torch.ones_like(wsum_phase), atol=1e-9), "phase weights"
+    # parity of the timed step's outputs with the CPU oracle's (digests)
+    parity = None
+    if not args.no_parity:
+        sys.path.insert(0, os.path.join(ROOT, "tests", "golden"))
+        import digests as D
+        rec = D.load()["configs"].get(str(args.config)) if os.path.exists(D.DIGEST_FILE) else None
+        if rec is None:
+            parity = {"checked": False, "reason": "no oracle digest for this workload"}
+        else:
+            def h(x):
+                a = x.cpu().numpy()
+                return a
+            out = {k: h(v) for k, v in result["groups"].items()}
+            out.update(score_op=h(result["score"]["op"]), score_op_weight=h(result["score"]["op_weight"]),
+                       score_op_S=h(result["score"]["op_score"]))
+            ow, kw, at = ag.op_weights(), ag.key_weights(), ag.app_totals()
+            out.update(op=h(ow["op"]), op_U=h(ow["U"]), op_w=h(ow["w"]), ukey=h(kw["key"]), key_U=h(kw["U"]),
+                       omega=h(kw["omega"]), app_total=h(at["T"]), mant=h(at["mant"]), rho=h(at["rho"]))
+            bad = D.mismatches(rec, out, s_agg=result["score"]["s_agg"])
+            parity = {"checked": True, "against": "CPU oracle (digests of its outputs on this workload)",
+                      "outputs": len([k for k in rec["digests"] if k in out]) + 1, "ok": not bad,
+                      "mismatch": bad}
+            log("parity", "ok" if not bad else "MISMATCH %s" % bad)
+
+    # aggregate-only time (pass A, scale, pass B, ordering) and the whole step
+    # with a 512 MB write before each repetition (no cache residency), medians
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    reps = max(3, min(10, steps))
+    t_agg, t_flush = [], []
+    for _ in range(reps):
+        flush.fill_(1)
+        torch.cuda.synchronize()
+        ta = time.perf_counter()
+        ag.reset()
+        ag.aggregate(d_key, d_app, d_ph, d_dur)
+        t_agg.append(time.perf_counter() - ta)
+        flush.fill_(2)
+        torch.cuda.synchronize()
+        ta = time.perf_counter()
+        step(ag)
+        t_flush.append(time.perf_counter() - ta)
+    del flush
 
     # per-kernel device times (hipEvents recorded by the library on its stream)
     agt = make(True)
     per = {}
     for _ in range(3):
         times = []
-        step(agt, times)
+        agt.reset()
+        agt.aggregate(d_key, d_app, d_ph, d_dur)
+        times.extend(agt.kernel_times())
+        out_g = agt.normalize(out=gbuf)
+        times.extend(agt.kernel_times())
+        agt.score(d_sk, d_s, out=sbuf)
+        times.extend(agt.kernel_times())
+        del out_g
         for name, ms, items in times:
             per.setdefault(name, []).append((ms, items))
     kernels = {k: dict(avg_ms=sum(m for m, _ in v) / len(v), items=v[0][1]) for k, v in per.items()}
     agt.close()
-    dom = max((k for k in kernels if k in KERNEL_BYTES), key=lambda k: kernels[k]["avg_ms"])
-    alg = KERNEL_BYTES[dom] * n
+    dom = max((k for k in kernels if k in METHOD_BYTES), key=lambda k: kernels[k]["avg_ms"])
+    alg = METHOD_BYTES[dom] * n
     achieved = alg / (kernels[dom]["avg_ms"] * 1e-3) / 1e9
     traffic = traffic_from_profile(cfg["slug"], dom, n)
+    t_a = sum(v["avg_ms"] for k, v in kernels.items() if k in PASS_A_KERNELS)
+    t_b = sum(v["avg_ms"] for k, v in kernels.items() if k in ("pass_b_lds", "pass_b_global", "part_hist",
+                                                              "part_scatter", "part_aggregate"))
+    engine_extra = sum(b for k, b in ENGINE_BYTES.items() if k in kernels)
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "algorithmic_bytes_per_launch": alg, "avg_launch_ms": round(kernels[dom]["avg_ms"], 4)}
+                "algorithmic_bytes_per_launch": alg, "avg_launch_ms": round(kernels[dom]["avg_ms"], 4),
+                "pass_a_frac": round(BYTES_PASS_A * n / (t_a * 1e-3) / 1e9 / HBM_PEAK_GBS, 4) if t_a else None,
+                "pass_b_frac": round(BYTES_PASS_B * n / (t_b * 1e-3) / 1e9 / HBM_PEAK_GBS, 4) if t_b else None,
+                "engine_extra_bytes_per_event": engine_extra}
     log("kernels", json.dumps({k: round(v["avg_ms"], 4) for k, v in kernels.items()}))
 
     cpu = None
     if not args.no_cpu_baseline:
         from oracle import oracle as O  # the CPU baseline leg is the oracle, timed as it stands
-        m = min(n, 1 << args.cpu_sample_log2)
-        log("cpu oracle on the first %d events" % m)
-        tc = time.perf_counter()
-        O.run(ev["key"][:m], ev["app"][:m], ev["phase"][:m], ev["dur_ns"][:m], c, P,
-              score_key=keys, s=s, want_units=True)
-        dt = time.perf_counter() - tc
-        cpu = {"value": round(m / dt / 1e9, 6), "unit": "G events/s", "cores": 1, "kind": "oracle",
-               "sample": "first %d events of the same workload (full path incl. score), %.1f s" % (m, dt)}
+        l1, lt = CPU_SAMPLE_LOG2[args.config]
+        threads = host_threads()
+        res = {}
+        for th, lg in ((1, l1), (threads, lt)):
+            m = min(n, 1 << lg)
+            log("cpu oracle on the first %d events, %d thread(s)" % (m, th))
+            tc = time.perf_counter()
+            O.run(ev["key"][:m], ev["app"][:m], ev["phase"][:m], ev["dur_ns"][:m], c, P,
+                  score_key=keys, s=s, want_units=True, threads=th)
+            dt = time.perf_counter() - tc
+            res[th] = (m, dt)
+        m, dt = res[threads]
+        m1, dt1 = res[1]
+        cpu = {"value": round(m / dt / 1e9, 6), "unit": "G events/s", "cores": threads, "kind": "oracle",
+               "sample": "first %d events of the same workload, full path incl. score, group-by sharded over "
+                         "%d threads (%.1f s)" % (m, threads, dt),
+               "single_thread": {"value": round(m1 / dt1 / 1e9, 6), "cores": 1,
+                                 "sample": "first %d events, one thread (%.1f s)" % (m1, dt1)},
+               "nproc": os.cpu_count(), "cpu_model": cpu_model()}
 
     line = {
         "metric": "trace events aggregated/sec (G ev/s) + % of MI355X peak HBM BW",
         "value": round(value, 3),
         "unit": "G events/s",
         "n_gpus": 1,
-        "steps": args.steps,
+        "steps": steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True,
@@ -202,12 +286,18 @@ def main() -> int:
                    "parallelism": "none", "entry": "atrex_run"},
         "hbm_frac_30B": round(30 * value * 1e9 / (HBM_PEAK_GBS * 1e9), 4),
         "hbm_frac_17B": round(17 * value * 1e9 / (HBM_PEAK_GBS * 1e9), 4),
+        "t_aggregate_ms": round(1e3 * statistics.median(t_agg), 4),
+        "t_pipeline_ms_flushed": round(1e3 * statistics.median(t_flush), 4),
         "kernels_ms": {k: round(v["avg_ms"], 4) for k, v in kernels.items()},
+        "parity": parity,
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
     ag.close()
     print(json.dumps(line), flush=True)
+    if parity is not None and parity.get("checked") and not parity["ok"]:
+        log("parity check FAILED:", parity["mismatch"])
+        return 1
     return 0
 
 

@@ -70,6 +70,8 @@ typedef enum {
 /* Flags for atrex_init_params.flags */
 #define ATREX_FLAG_TIMING 1u /* record per-kernel hipEvent times (atrex_kernel_times) */
 #define ATREX_FLAG_RAW 2u    /* also accumulate the plain device time sum of dur per group */
+#define ATREX_FLAG_APP_COUNT 4u /* also count the invocations n[a,ph] of every (app, phase) in
+                                   pass A (Eq. (2)); read with atrex_get_app_totals */
 
 typedef struct {
   uint64_t lo, hi; /* value = lo + hi * 2^64 */
@@ -161,6 +163,9 @@ typedef struct {
   uint64_t num_keys;
   uint64_t num_scored_ops; /* atrex_weighted_score's num_ops (0 without a score) */
   double s_agg;            /* atrex_weighted_score's s_agg (0 without a score) */
+  uint32_t one_wait;       /* 1: the unit, weight and score kernels enqueued right behind the
+                              group-by were kept, so the host waited once for the whole call;
+                              0: they ran after the group-by's own wait (or not at all) */
 } atrex_run_result;
 
 /* One batch through the whole path in one call: atrex_aggregate_reset,
@@ -182,9 +187,14 @@ atrex_status atrex_run(atrex_ctx *ctx, const atrex_events *ev, const atrex_group
                        uint64_t n_score, uint32_t *op, double *op_weight, double *op_score,
                        atrex_run_result *r);
 
-/* Per (app, phase), index a * P + ph (DEVICE, [A*P]): T = D_a^phi (u128);
- * mant / rho (nullable): the scale m, rho defined above (m = 0: no share). */
-atrex_status atrex_get_app_totals(atrex_ctx *ctx, atrex_u128 *T, uint64_t *mant, int32_t *rho);
+/* Per (app, phase), index a * P + ph (DEVICE, [A*P]): T = D_a^phi (u128),
+ * the device time of Eq. (2) (§3.4); n (nullable) = the number of
+ * invocations of (a, ph), i.e. the sum over kernels of m_{a,phi,r} in Eq. (2),
+ * which needs ATREX_FLAG_APP_COUNT at init (INVALID_ARG otherwise);
+ * mant / rho (nullable): the scale m, rho defined above (m = 0: no share).
+ * Valid after atrex_aggregate_events (STATE before). */
+atrex_status atrex_get_app_totals(atrex_ctx *ctx, atrex_u128 *T, uint64_t *n, uint64_t *mant,
+                                  int32_t *rho);
 
 /* Per-kernel device times of the last aggregate_events / phase_normalize /
  * weighted_score call when ATREX_FLAG_TIMING was set (HOST arrays of cap

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libatrex.so")
 
 OK, E_INVALID_ARG, E_OUT_OF_RANGE, E_STATE, E_CAPACITY, E_DEVICE = 0, -1, -2, -3, -4, -5
 PATHS = {"auto": 0, "lds_hash": 1, "global_hash": 2, "radix_sort": 3}
-FLAG_TIMING, FLAG_RAW = 1, 2
+FLAG_TIMING, FLAG_RAW, FLAG_APP_COUNT = 1, 2, 4
 
 
 class AtrexError(RuntimeError):
@@ -53,7 +53,7 @@ class _Groups(ctypes.Structure):
 
 class _RunResult(ctypes.Structure):
     _fields_ = [("num_groups", ctypes.c_uint64), ("num_ops", ctypes.c_uint64), ("num_keys", ctypes.c_uint64),
-                ("num_scored_ops", ctypes.c_uint64), ("s_agg", ctypes.c_double)]
+                ("num_scored_ops", ctypes.c_uint64), ("s_agg", ctypes.c_double), ("one_wait", ctypes.c_uint32)]
 
 
 _LIB = None
@@ -78,7 +78,7 @@ def _lib() -> ctypes.CDLL:
                                      ctypes.POINTER(ctypes.c_double)],
             "atrex_run": [P, ctypes.POINTER(_Events), ctypes.POINTER(_Groups), U64, P, P, U64, P, P, P,
                           ctypes.POINTER(_RunResult)],
-            "atrex_get_app_totals": [P, P, P, P],
+            "atrex_get_app_totals": [P, P, P, P, P],
             "atrex_kernel_times": [P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float),
                                    ctypes.POINTER(U64), I, ctypes.POINTER(I)],
             "atrex_aggregate_reset": [P],
@@ -134,20 +134,22 @@ class Aggregator:
 
     def __init__(self, num_phases: int, app_weight_q16: torch.Tensor, max_events: int,
                  max_groups: int = 0, max_keys: int = 0, max_score: int = 0, path: str = "auto",
-                 timing: bool = False, raw: bool = False, stream: torch.cuda.Stream | None = None):
+                 timing: bool = False, raw: bool = False, app_count: bool = False,
+                 stream: torch.cuda.Stream | None = None):
         L = _lib()
         c = _dev(_as_i32(app_weight_q16), torch.int32, "app_weight_q16")
         self.device = c.device
         self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
         self.P, self.A = int(num_phases), int(c.numel())
         self.raw = raw
+        self.app_count = app_count
         p = _InitParams()
         p.num_phases, p.num_apps = self.P, self.A
         p.app_weight_q16 = c.data_ptr()
         p.max_events, p.max_groups, p.max_keys, p.max_score = max_events, max_groups, max_keys, max_score
         p.path = PATHS[path]
         p.stream = self.stream.cuda_stream
-        p.flags = (FLAG_TIMING if timing else 0) | (FLAG_RAW if raw else 0)
+        p.flags = (FLAG_TIMING if timing else 0) | (FLAG_RAW if raw else 0) | (FLAG_APP_COUNT if app_count else 0)
         nbytes = ctypes.c_size_t()
         _check(L.atrex_workspace_bytes(ctypes.byref(p), ctypes.byref(nbytes)), "atrex_workspace_bytes")
         self.workspace = torch.empty(max(int(nbytes.value), 256), dtype=torch.uint8, device=self.device)
@@ -158,6 +160,7 @@ class Aggregator:
         self._ctx = ctx
         self.num_groups = None
         self.num_ops = self.num_keys = None
+        self.one_wait = None
         # marshalled arguments of the last normalize()/score() call, reused
         # while the caller passes the same output tensors (and sizes) again
         self._gcache = None
@@ -255,6 +258,7 @@ class Aggregator:
                               nsc, sp[2], sp[3], sp[4], ctypes.byref(r))
         # counts of the stages that completed (as after the separate calls)
         self.num_groups, self.num_ops, self.num_keys = r.num_groups, r.num_ops, r.num_keys
+        self.one_wait = bool(r.one_wait)
         _check(st, "atrex_run")
         G, k = r.num_groups, r.num_scored_ops
         v = self._rviews  # views of the first G groups / k operators, kept while they stay the same
@@ -313,12 +317,18 @@ class Aggregator:
 
     # -- inspection ------------------------------------------------------------------------
     def app_totals(self) -> dict:
+        """D_a^phi, the scale (m, rho) and, with app_count=True at construction,
+        the invocation count n of every (app, phase), index a * P + phase."""
         GA, dev = self.A * self.P, self.device
         T = torch.empty((GA, 2), dtype=torch.int64, device=dev)
+        n = torch.empty(GA, dtype=torch.int64, device=dev) if self.app_count else None
         m = torch.empty(GA, dtype=torch.int64, device=dev)
         r = torch.empty(GA, dtype=torch.int32, device=dev)
-        _check(_lib().atrex_get_app_totals(self._ctx, _ptr(T), _ptr(m), _ptr(r)), "atrex_get_app_totals")
-        return dict(T=T, mant=m, rho=r)
+        _check(_lib().atrex_get_app_totals(self._ctx, _ptr(T), _ptr(n), _ptr(m), _ptr(r)), "atrex_get_app_totals")
+        out = dict(T=T, mant=m, rho=r)
+        if n is not None:
+            out["n"] = n
+        return out
 
     def kernel_times(self) -> list:
         cap = 64
@@ -346,13 +356,14 @@ class Aggregator:
 
 
 def aggregate(key, app, phase, dur_ns, app_weight_q16, num_phases, path="auto", raw=False,
-              score_key=None, s=None, max_groups=0, max_keys=0) -> dict:
+              score_key=None, s=None, max_groups=0, max_keys=0, app_count=False) -> dict:
     """Whole path in one call: returns groups, per-op and per-key weights, and
     the score when (score_key, s) are given."""
     n = key.numel()
     nsc = score_key.numel() if score_key is not None else 0
     ag = Aggregator(num_phases, app_weight_q16, max_events=max(n, 1), max_groups=max_groups,
-                    max_keys=max_keys, max_score=max(nsc, 1) if nsc else 0, path=path, raw=raw)
+                    max_keys=max_keys, max_score=max(nsc, 1) if nsc else 0, path=path, raw=raw,
+                    app_count=app_count)
     try:
         ag.aggregate(key, app, phase, dur_ns)
         out = ag.normalize()

@@ -21,7 +21,7 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr size_t kLdsBytes = 160 * 1024;
-constexpr uint32_t kPassAThreads = 1024;  // two workgroups per CU (32 waves) when the table allows
+constexpr uint32_t kPassAThreads = 1024;  // one workgroup per CU (16 waves), two groups of loads in flight per lane
 constexpr uint64_t kPartialRowsMax = 1024;  // pass-A workgroups with private partial rows
 constexpr uint64_t kMaxWG = 256;            // persistent workgroups of the LDS engines
 constexpr uint32_t kMaxBucketBits = 12;     // radix-partition buckets: at most 4096
@@ -38,7 +38,7 @@ uint64_t next_pow2(uint64_t x) {
 
 // Byte offsets of every workspace region (all 256-byte aligned).
 struct Layout {
-  size_t ctrl, T, carryA, partA, scale, bscale, dict, acc, raw;
+  size_t ctrl, T, carryA, partA, partC, nA, scale, bscale, dict, acc, raw;
   size_t okey, oacc, oraw, ocount, skey, sval, sraw, scount;  // LDS engine outputs
   size_t ol_rk, ol_key, ol_lo, ol_hi, ol_rlo, ol_rhi, ol_count, ol_part;  // per-owner sorted lists
   size_t H, O, rec, rraw, bstart, istart;                     // partition engine
@@ -63,17 +63,25 @@ struct Params {
   uint32_t P, A;
   uint64_t max_events, max_groups, max_keys, max_score;
   bool raw;
+  bool count;  // invocation counts per (app, phase) in pass A
 };
 
-constexpr uint32_t kPassARangeBins = (kLdsBytes - 512) / 4;  // 32-bit LDS counters per range
 constexpr uint32_t kPassARangesMax = 16;
 constexpr uint32_t kPassASlices = 32;
 
-int pass_a_mode(uint64_t G_A) {
-  if (G_A * 8 <= kLdsBytes - 1024) return 0;  // 64-bit LDS table
-  if (G_A * 4 <= kLdsBytes - 512) return 1;   // 32-bit LDS table
-  if ((G_A + kPassARangeBins - 1) / kPassARangeBins <= kPassARangesMax) return 3;  // ranges of the table
-  return 2;                                   // global atomics
+// 32-bit LDS counters per range of the range-split pass A (a u32 count beside
+// each with counting on); 64 per-lane spare counters follow the range
+uint32_t pass_a_range_bins(bool count) { return (uint32_t)((kLdsBytes - 512) / (count ? 8 : 4)); }
+
+// The pass-A variant for G_A = A * P (app, phase) pairs: the LDS entry grows
+// by a 32-bit count with counting on.
+int pass_a_mode(uint64_t G_A, bool count) {
+  const uint64_t cb = count ? 4 : 0;
+  if (G_A * (8 + cb) <= kLdsBytes - 1024) return 0;  // 64-bit LDS table
+  if (G_A * (4 + cb) <= kLdsBytes - 512) return 1;   // 32-bit LDS table
+  const uint64_t bins = pass_a_range_bins(count);
+  if ((G_A + bins - 1) / bins <= kPassARangesMax) return 3;  // ranges of the table
+  return 2;                                                  // global atomics
 }
 
 Layout make_layout(const Params& p) {
@@ -91,7 +99,7 @@ Layout make_layout(const Params& p) {
   L.maxSort = std::max<uint64_t>(std::max<uint64_t>(L.maxG, L.maxS), 1);
   L.capD = next_pow2(std::max<uint64_t>(1024, 2 * L.maxK));
   L.maxOps = std::min<uint64_t>(L.maxG, 65536);
-  L.passA = pass_a_mode(GA);
+  L.passA = pass_a_mode(GA, p.count);
   L.partA_rows = L.passA == 0 ? kPartialRowsMax : L.passA == 1 ? kMaxWG : L.passA == 3 ? kPassASlices : 0;
   L.ldsSlots = pass_b_lds_slots(p.P, p.raw, kLdsBytes);
   L.tabSlots = lds_table_slots(p.P, p.raw, kLdsBytes);
@@ -104,6 +112,8 @@ Layout make_layout(const Params& p) {
   L.T = take(GA * 16);
   L.carryA = take(GA * 8);
   L.partA = take(L.partA_rows * GA * (L.passA == 0 ? 8 : 4));
+  L.partC = take(p.count ? L.partA_rows * GA * 4 : 0);
+  L.nA = take(p.count ? GA * 8 : 0);
   L.scale = take(GA * 8);
   L.bscale = take(GA * 8);
   L.dict = take(L.capD * 8);
@@ -202,6 +212,7 @@ atrex_status check_params(const atrex_init_params* ip, Params* out) {
   if (p.max_groups >= (1ull << 32) || p.max_score >= (1ull << 31) || p.max_keys >= (1ull << 31))
     return ATREX_E_INVALID_ARG;
   p.raw = (ip->flags & ATREX_FLAG_RAW) != 0;
+  p.count = (ip->flags & ATREX_FLAG_APP_COUNT) != 0;
   *out = p;
   return ATREX_OK;
 }
@@ -639,6 +650,9 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
   // pass A, Eq. (2), and the Eq. (3) scale words of every (app, phase)
   uint64_t* T = c->at<uint64_t>(L.T);
   uint64_t* scale = c->at<uint64_t>(L.scale);
+  // invocation counts per (app, phase): per-block partials, then their sums
+  uint32_t* pcount = c->p.count ? c->at<uint32_t>(L.partC) : nullptr;
+  uint64_t* nA = c->p.count ? c->at<uint64_t>(L.nA) : nullptr;
   if (L.passA == 0 && vec_ok) {
     // one workgroup per CU (two groups of loads in flight per lane): two per
     // CU ran as one after the other (the SIMDs favour the older one) and
@@ -647,35 +661,37 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
     nb = std::max<uint64_t>(1, std::min<uint64_t>(nb, (n / 4 + kPassAThreads - 1) / kPassAThreads));
     TIMED(c, "pass_a", n,
           launch_pass_a_lds(s, d, A, P, (uint32_t)nb, c->at<unsigned long long>(L.partA),
-                            c->at<unsigned long long>(L.carryA), c->err()));
+                            c->at<unsigned long long>(L.carryA), pcount, c->err()));
     TIMED(c, "pass_a_reduce", GA,
           launch_pass_a_reduce(s, c->at<unsigned long long>(L.partA), (uint32_t)nb, (uint32_t)GA,
                                c->at<unsigned long long>(L.carryA), T, c->app_weight, c->Csum(), P, scale,
-                               c->at<void>(L.bscale)));
+                               c->at<void>(L.bscale), pcount, nA));
   } else if (L.passA == 3 && vec_ok) {
-    const uint32_t R = (uint32_t)((GA + kPassARangeBins - 1) / kPassARangeBins);
+    const uint32_t bins = pass_a_range_bins(c->p.count);
+    const uint32_t R = (uint32_t)((GA + bins - 1) / bins);
     const uint32_t GR = (uint32_t)((GA + R - 1) / R);
     TIMED(c, "pass_a_range", n,
           launch_pass_a_range(s, d, A, P, GR, R, kPassASlices, c->at<uint32_t>(L.partA),
-                              c->at<unsigned long long>(L.carryA), c->err()));
+                              c->at<unsigned long long>(L.carryA), pcount, c->err()));
     TIMED(c, "pass_a_reduce", GA,
           launch_pass_a_reduce32(s, c->at<uint32_t>(L.partA), kPassASlices, (uint32_t)GA,
                                  c->at<unsigned long long>(L.carryA), T, c->app_weight, c->Csum(), P, scale,
-                                 c->at<void>(L.bscale)));
+                                 c->at<void>(L.bscale), pcount, nA));
   } else if (L.passA == 1 && vec_ok) {
     const uint64_t nb = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)c->cus, kMaxWG));
     TIMED(c, "pass_a", n,
           launch_pass_a_lds32(s, d, A, P, (uint32_t)nb, c->at<uint32_t>(L.partA), c->at<unsigned long long>(L.carryA),
-                              c->err()));
+                              pcount, c->err()));
     TIMED(c, "pass_a_reduce", GA,
           launch_pass_a_reduce32(s, c->at<uint32_t>(L.partA), (uint32_t)nb, (uint32_t)GA,
                                  c->at<unsigned long long>(L.carryA), T, c->app_weight, c->Csum(), P, scale,
-                                 c->at<void>(L.bscale)));
+                                 c->at<void>(L.bscale), pcount, nA));
   } else {
     launch_fill_u64(s, T, GA * 2, 0);
+    if (nA) launch_fill_u64(s, nA, GA, 0);
     TIMED(c, "pass_a_global", n,
           launch_pass_a_global(s, d, A, P, (uint32_t)std::max<uint64_t>(1, (uint64_t)c->cus * 8), (unsigned long long*)T,
-                               c->err()));
+                               (unsigned long long*)nA, c->err()));
     // scale, Eq. (3) (the column-sum kernels of the other modes compute it with T)
     TIMED(c, "scale", GA, launch_scale(s, T, c->app_weight, c->Csum(), A, P, scale, c->at<void>(L.bscale)));
   }
@@ -1162,6 +1178,7 @@ atrex_status atrex_run(atrex_ctx* c, const atrex_events* ev, const atrex_groups*
   r->num_groups = G;
   if (G > out_capacity) return ATREX_E_CAPACITY;
   if (spec && fast && G <= kUnitsSmallMax) {  // the speculation stands (the device took the same decision)
+    r->one_wait = 1;
     st = normalize_finish(c, h, units_err, &r->num_ops, &r->num_keys);
     if (st != ATREX_OK) return st;
     return score_small_finish(w, &r->num_scored_ops, &r->s_agg);
@@ -1194,11 +1211,13 @@ atrex_status atrex_run(atrex_ctx* c, const atrex_events* ev, const atrex_groups*
   return score_small_finish(w, &r->num_scored_ops, &r->s_agg);
 }
 
-atrex_status atrex_get_app_totals(atrex_ctx* c, atrex_u128* T, uint64_t* mant, int32_t* rho) {
+atrex_status atrex_get_app_totals(atrex_ctx* c, atrex_u128* T, uint64_t* n, uint64_t* mant, int32_t* rho) {
   if (!c || !T) return ATREX_E_INVALID_ARG;
+  if (n && !c->p.count) return ATREX_E_INVALID_ARG;
   if (c->state < 1) return ATREX_E_STATE;
   const uint64_t GA = (uint64_t)c->p.A * c->p.P;
   (void)hipMemcpyAsync(T, c->at<void>(c->L.T), GA * 16, hipMemcpyDeviceToDevice, c->s);
+  if (n) (void)hipMemcpyAsync(n, c->at<void>(c->L.nA), GA * 8, hipMemcpyDeviceToDevice, c->s);
   if (mant || rho) launch_unpack_scale(c->s, c->at<uint64_t>(c->L.scale), GA, mant, rho);
   return sync_read(c);
 }

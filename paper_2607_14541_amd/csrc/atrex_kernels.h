@@ -93,22 +93,24 @@ struct SortedGroups {
 
 // kernels_aggregate.hip
 hipError_t set_kernel_smem_limits();
+// pcount / cnt (nullable): per-block invocation counts of each (app, phase)
+// and their sums (the launch with pcount set writes them; the reduce sums them).
 void launch_pass_a_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
-                       unsigned long long* partial, unsigned long long* carry, uint32_t* err);
+                       unsigned long long* partial, unsigned long long* carry, uint32_t* pcount, uint32_t* err);
 // The reduce reads the carry (extension) table and leaves it zero for the
 // next pass A.
 void launch_pass_a_reduce(hipStream_t s, const unsigned long long* partial, uint32_t nb, uint32_t G,
                           unsigned long long* carry, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
-                          uint32_t P, uint64_t* scale, void* bscale);
+                          uint32_t P, uint64_t* scale, void* bscale, const uint32_t* pcount, uint64_t* cnt);
 void launch_pass_a_lds32(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
-                         uint32_t* partial, unsigned long long* ext, uint32_t* err);
+                         uint32_t* partial, unsigned long long* ext, uint32_t* pcount, uint32_t* err);
 void launch_pass_a_reduce32(hipStream_t s, const uint32_t* partial, uint32_t nb, uint32_t G,
                             unsigned long long* ext, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
-                            uint32_t P, uint64_t* scale, void* bscale);
+                            uint32_t P, uint64_t* scale, void* bscale, const uint32_t* pcount, uint64_t* cnt);
 void launch_pass_a_range(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t GR, uint32_t R,
-                         uint32_t slices, uint32_t* partial, unsigned long long* ext, uint32_t* err);
+                         uint32_t slices, uint32_t* partial, unsigned long long* ext, uint32_t* pcount, uint32_t* err);
 void launch_pass_a_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
-                          unsigned long long* T, uint32_t* err);
+                          unsigned long long* T, unsigned long long* cnt, uint32_t* err);
 void launch_unpack_scale(hipStream_t s, const uint64_t* sw, uint64_t G, uint64_t* mant, int32_t* rho);
 // scale words (general form) and the 16-byte pass-B entries
 void launch_scale(hipStream_t s, const uint64_t* T, const uint32_t* c, const uint64_t* Csum, uint32_t A,

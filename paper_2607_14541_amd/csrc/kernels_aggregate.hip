@@ -20,17 +20,35 @@ __device__ __forceinline__ void flag_error(uint32_t* err, bool bad, uint32_t bit
 // Pass A, LDS-privatised dense histogram on g = a * P + ph.  Each workgroup
 // keeps the low 64 bits of its partial sums in LDS; the (rare) wrap-arounds
 // are counted in a global carry table.  Partials go to partial[block][g].
-template <int BLOCK>
+// COUNT: the invocations of each g are counted too (a u32 table after the
+// sums; a workgroup sees fewer than 2^31 events), partial counts to
+// pcount[block][g].
+template <int BLOCK, bool COUNT>
 __global__ __launch_bounds__(BLOCK) void k_pass_a_lds(EventsDev ev, uint32_t A, uint32_t P, uint32_t G,
                                                       unsigned long long* __restrict__ partial,
                                                       unsigned long long* __restrict__ carry,
-                                                      uint32_t* __restrict__ err) {
+                                                      uint32_t* __restrict__ pcount, uint32_t* __restrict__ err) {
   extern __shared__ unsigned long long s_lo[];
-  for (uint32_t g = threadIdx.x; g < G; g += BLOCK) s_lo[g] = 0;
+  uint32_t* s_n = (uint32_t*)(s_lo + G);  // COUNT only
+  for (uint32_t g = threadIdx.x; g < G; g += BLOCK) {
+    s_lo[g] = 0;
+    if (COUNT) s_n[g] = 0;
+  }
   __syncthreads();
   const uint64_t n = ev.n, n4 = n / 4;
   const uint64_t stride = (uint64_t)gridDim.x * BLOCK;
   bool bad = false;
+  auto one = [&](uint32_t a, uint32_t ph, int64_t dd) {
+    const bool ok = a < A && ph < P && dd >= 0;
+    bad |= !ok;
+    if (ok) {
+      const uint32_t g = a * P + ph;
+      const unsigned long long d = (unsigned long long)dd;
+      const unsigned long long old = atomicAdd(&s_lo[g], d);
+      if (old + d < old) atomicAdd(&carry[g], 1ull);
+      if (COUNT) atomicAdd(&s_n[g], 1u);
+    }
+  };
   // the next two groups' loads are issued before the current group is added
   uint64_t q = (uint64_t)blockIdx.x * BLOCK + threadIdx.x;
   Ev4 nxt, nxt2;
@@ -41,48 +59,35 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_lds(EventsDev ev, uint32_t A, 
     nxt = nxt2;
     if (q + 2 * stride < n4) load4<false>(ev.key, ev.app, ev.phase, ev.dur, (q + 2 * stride) * 4, nxt2);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const bool ok = e.app[j] < A && e.ph[j] < P && e.dur[j] >= 0;
-      bad |= !ok;
-      if (ok) {
-        const uint32_t g = e.app[j] * P + e.ph[j];
-        const unsigned long long d = (unsigned long long)e.dur[j];
-        const unsigned long long old = atomicAdd(&s_lo[g], d);
-        if (old + d < old) atomicAdd(&carry[g], 1ull);
-      }
-    }
+    for (int j = 0; j < 4; ++j) one(e.app[j], e.ph[j], e.dur[j]);
   }
-  if (blockIdx.x == 0) {  // tail events
-    for (uint64_t i = n4 * 4 + threadIdx.x; i < n; i += BLOCK) {
-      const uint32_t a = ev.app[i], ph = ev.phase[i];
-      const int64_t dd = ev.dur[i];
-      const bool ok = a < A && ph < P && dd >= 0;
-      bad |= !ok;
-      if (ok) {
-        const uint32_t g = a * P + ph;
-        const unsigned long long old = atomicAdd(&s_lo[g], (unsigned long long)dd);
-        if (old + (unsigned long long)dd < old) atomicAdd(&carry[g], 1ull);
-      }
-    }
-  }
+  if (blockIdx.x == 0)  // tail events
+    for (uint64_t i = n4 * 4 + threadIdx.x; i < n; i += BLOCK) one(ev.app[i], ev.phase[i], ev.dur[i]);
   flag_error(err, bad, ATREX_ERRBIT_RANGE);
   __syncthreads();
   unsigned long long* out = partial + (size_t)blockIdx.x * G;
-  for (uint32_t g = threadIdx.x; g < G; g += BLOCK) out[g] = s_lo[g];
+  for (uint32_t g = threadIdx.x; g < G; g += BLOCK) {
+    out[g] = s_lo[g];
+    if (COUNT) pcount[(size_t)blockIdx.x * G + g] = s_n[g];
+  }
 }
 
 // Pass A with 32-bit LDS accumulators (twice the (app, phase) capacity of the
 // 64-bit table).  A wrap of the 32-bit sum and the high half of a duration
 // are both counted in ext[g] in units of 2^32 (global atomics, rare: only
 // when a workgroup's partial sum of one (app, phase) passes 2^32, or for a
-// duration of 2^32 ns or more).
-template <int BLOCK>
+// duration of 2^32 ns or more).  COUNT as in k_pass_a_lds.
+template <int BLOCK, bool COUNT>
 __global__ __launch_bounds__(BLOCK) void k_pass_a_lds32(EventsDev ev, uint32_t A, uint32_t P, uint32_t G,
                                                         uint32_t* __restrict__ partial,
                                                         unsigned long long* __restrict__ ext,
-                                                        uint32_t* __restrict__ err) {
+                                                        uint32_t* __restrict__ pcount, uint32_t* __restrict__ err) {
   extern __shared__ uint32_t s32[];
-  for (uint32_t g = threadIdx.x; g < G; g += BLOCK) s32[g] = 0;
+  uint32_t* s_n = s32 + G;  // COUNT only
+  for (uint32_t g = threadIdx.x; g < G; g += BLOCK) {
+    s32[g] = 0;
+    if (COUNT) s_n[g] = 0;
+  }
   __syncthreads();
   const uint64_t n = ev.n, n4 = n / 4;
   const uint64_t stride = (uint64_t)gridDim.x * BLOCK;
@@ -97,6 +102,7 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_lds32(EventsDev ev, uint32_t A
     const uint32_t old = atomicAdd(&s32[g], lo);
     const uint64_t up = (d >> 32) + ((old + lo < old) ? 1u : 0u);
     if (up) atomicAdd(&ext[g], (unsigned long long)up);
+    if (COUNT) atomicAdd(&s_n[g], 1u);
   };
   uint64_t q = (uint64_t)blockIdx.x * BLOCK + threadIdx.x;
   Ev4 nxt;
@@ -112,7 +118,10 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_lds32(EventsDev ev, uint32_t A
   flag_error(err, bad, ATREX_ERRBIT_RANGE);
   __syncthreads();
   uint32_t* out = partial + (size_t)blockIdx.x * G;
-  for (uint32_t g = threadIdx.x; g < G; g += BLOCK) out[g] = s32[g];
+  for (uint32_t g = threadIdx.x; g < G; g += BLOCK) {
+    out[g] = s32[g];
+    if (COUNT) pcount[(size_t)blockIdx.x * G + g] = s_n[g];
+  }
 }
 
 // Pass A for more (app, phase) pairs than one LDS holds: the pairs are split
@@ -122,19 +131,24 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_lds32(EventsDev ev, uint32_t A
 // (workgroups go round-robin over the 8 XCDs) and walk the slice in the same
 // order with ordinary (L2-allocating) loads, so the slice comes from HBM about
 // once and from that XCD's L2 for the others.  Each lane keeps three groups of
-// four events in flight (loads issued two iterations ahead).
-template <int BLOCK>
+// four events in flight (loads issued two iterations ahead).  COUNT: a u32
+// count table after the GR counters and their spares.
+template <int BLOCK, bool COUNT>
 __global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A, uint32_t P, uint32_t G,
                                                         uint32_t GR, uint32_t R, uint32_t slices,
                                                         uint32_t* __restrict__ partial,
                                                         unsigned long long* __restrict__ ext,
-                                                        uint32_t* __restrict__ err) {
+                                                        uint32_t* __restrict__ pcount, uint32_t* __restrict__ err) {
   extern __shared__ uint32_t s32[];
+  uint32_t* s_n = s32 + GR + 64;  // COUNT only
   const uint32_t xcd = blockIdx.x % 8, k = blockIdx.x / 8;
   const uint32_t slice = (k / R) * 8 + xcd, range = k % R;
   if (slice >= slices) return;  // whole workgroup
   const uint32_t g0 = range * GR, g1 = min(G, g0 + GR);
-  for (uint32_t g = threadIdx.x; g < g1 - g0; g += BLOCK) s32[g] = 0;
+  for (uint32_t g = threadIdx.x; g < g1 - g0; g += BLOCK) {
+    s32[g] = 0;
+    if (COUNT) s_n[g] = 0;
+  }
   __syncthreads();
   const uint64_t n = ev.n;
   const uint64_t per = ((n + slices - 1) / slices + 3) / 4 * 4;
@@ -150,6 +164,7 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A
     const uint32_t old = atomicAdd(&s32[g - g0], lo);
     const uint64_t up = (d >> 32) + ((old + lo < old) ? 1u : 0u);
     if (up) atomicAdd(&ext[g], (unsigned long long)up);
+    if (COUNT) atomicAdd(&s_n[g - g0], 1u);
   };
   // groups of four events of the slice: iteration `it` covers groups
   // it * BLOCK + [0, BLOCK); the trip count is uniform over the workgroup
@@ -172,13 +187,15 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A
   };
   // Four events without branches.  An event outside the range adds to a
   // per-lane spare counter past the range, so the four LDS atomics issue back
-  // to back and are waited for once.  When every lane's four events are valid
-  // (the usual case, checked for the group at once: largest app, the phase
-  // bytes, the sign of the durations) the counter's byte offset and the range
-  // test need no per-event validity; otherwise the wave takes the per-event
-  // checks.  The high words and wrap-arounds go to ext[g] only when present.
+  // to back and are waited for once (an atomic masked to the lanes in range
+  // would be waited for before the next one is issued).  When every lane's four
+  // events are valid (the usual case, checked for the group at once: largest
+  // app, the phase bytes, the sign of the durations) the counter's byte offset
+  // and the range test need no per-event validity; otherwise the wave takes the
+  // per-event checks.  The high words and wrap-arounds go to ext[g] only when
+  // present.  COUNT: the counts are added with no-return atomics, in range only.
   const uint32_t gn = g1 - g0, lane = threadIdx.x & 63;
-  const uint32_t spare = GR + lane, spare4 = 4 * spare, gn4 = 4 * gn, P4 = 4 * P, g04 = 4 * g0;
+  const uint32_t spare4 = 4 * (GR + lane), gn4 = 4 * gn, P4 = 4 * P, g04 = 4 * g0;
   const uint32_t pbytes = P * 0x01010101u;  // P in every byte (P <= 128)
   auto process = [&](uint64_t it, const G4& x) {
     if (it * BLOCK + threadIdx.x >= ng) return;
@@ -204,9 +221,14 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j) old[j] = atomicAdd((uint32_t*)((char*)s32 + rb[j]), (uint32_t)dv[j]);
+      if (COUNT) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (in[j]) atomicAdd((uint32_t*)((char*)s_n + rb[j]), 1u);
+      }
       bool cy = false;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) cy |= old[j] + (uint32_t)dv[j] < old[j];
+      for (int j = 0; j < 4; ++j) cy |= in[j] & (old[j] + (uint32_t)dv[j] < old[j]);
       if (__any(cy | (hor != 0)))
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -215,24 +237,8 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A
         }
       return;
     }
-    uint32_t r[4], lo[4];
-    bool in[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t ph = (x.p >> (8 * j)) & 0xFFu;
-      const bool ok = (av[j] < A) & (ph < P) & ((int32_t)dhi[j] >= 0);  // bitwise: no branches
-      bad |= !ok;
-      r[j] = av[j] * P + ph - g0;  // position in the range when in[j]
-      in[j] = ok & (r[j] < gn);
-      lo[j] = in[j] ? (uint32_t)dv[j] : 0u;
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) old[j] = atomicAdd(&s32[in[j] ? r[j] : spare], lo[j]);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t up = dhi[j] + ((old[j] + lo[j] < old[j]) ? 1u : 0u);  // d >= 0: high word < 2^31
-      if (in[j] && up) atomicAdd(&ext[g0 + r[j]], (unsigned long long)up);
-    }
+    for (int j = 0; j < 4; ++j) one(av[j], (x.p >> (8 * j)) & 0xFFu, dv[j]);
   };
   G4 x0, x1, x2;
   if (0 < iters) load(0, x0);
@@ -252,13 +258,18 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A
   flag_error(err, bad, ATREX_ERRBIT_RANGE);
   __syncthreads();
   uint32_t* out = partial + (size_t)slice * G;
-  for (uint32_t g = threadIdx.x; g < g1 - g0; g += BLOCK) out[g0 + g] = s32[g];
+  for (uint32_t g = threadIdx.x; g < g1 - g0; g += BLOCK) {
+    out[g0 + g] = s32[g];
+    if (COUNT) pcount[(size_t)slice * G + g0 + g] = s_n[g];
+  }
 }
 
-// Pass A straight into global 128-bit accumulators (any number of (a, ph)).
-template <int BLOCK>
+// Pass A straight into global 128-bit accumulators (any number of (a, ph));
+// COUNT: invocation counts into cnt[g] (u64, global atomics).
+template <int BLOCK, bool COUNT>
 __global__ __launch_bounds__(BLOCK) void k_pass_a_global(EventsDev ev, uint32_t A, uint32_t P,
                                                          unsigned long long* __restrict__ T,
+                                                         unsigned long long* __restrict__ cnt,
                                                          uint32_t* __restrict__ err) {
   const uint64_t n = ev.n;
   bool bad = false;
@@ -270,6 +281,7 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_global(EventsDev ev, uint32_t 
     if (ok) {
       const size_t g = (size_t)a * P + ph;
       acc_add_plain(&T[2 * g], &T[2 * g + 1], (u128)(uint64_t)d);
+      if (COUNT) atomicAdd(&cnt[g], 1ull);
     }
   }
   flag_error(err, bad, ATREX_ERRBIT_RANGE);
@@ -385,31 +397,43 @@ __global__ void k_scale(const uint64_t* __restrict__ T, const uint32_t* __restri
 }
 
 // T[g] = sum over blocks of partial[b][g] + ext[g] * 2^ext_shift, and the
-// scale words of g (Eq. (3)) from it.  Block = 64 consecutive g x 16 strides
-// over the partial rows.
+// scale words of g (Eq. (3)) from it; with pcount, n[g] = sum over blocks of
+// pcount[b][g].  Block = 64 consecutive g x 16 strides over the partial rows.
 template <typename PT>
 __global__ __launch_bounds__(1024) void k_pass_a_reduce(const PT* __restrict__ partial, uint32_t nb, uint32_t G,
                                                         unsigned long long* __restrict__ ext, int ext_shift,
                                                         uint64_t* __restrict__ T, const uint32_t* __restrict__ c,
                                                         const uint64_t* __restrict__ Csum, uint32_t P,
-                                                        uint64_t* __restrict__ scale, uint64_t* __restrict__ bscale) {
-  __shared__ uint64_t s_lo[16][64], s_hi[16][64];
+                                                        uint64_t* __restrict__ scale, uint64_t* __restrict__ bscale,
+                                                        const uint32_t* __restrict__ pcount,
+                                                        uint64_t* __restrict__ cnt) {
+  __shared__ uint64_t s_lo[16][64], s_hi[16][64], s_n[16][64];
   const uint32_t gl = threadIdx.x & 63, r = threadIdx.x >> 6;
   const uint32_t g = blockIdx.x * 64 + gl;
   u128 acc = 0;
+  uint64_t na = 0;
   if (g < G) {
 #pragma unroll 8
     for (uint32_t b = r; b < nb; b += 16) acc += (uint64_t)partial[(size_t)b * G + g];
+    if (pcount)
+#pragma unroll 8
+      for (uint32_t b = r; b < nb; b += 16) na += pcount[(size_t)b * G + g];
   }
   s_lo[r][gl] = (uint64_t)acc;
   s_hi[r][gl] = (uint64_t)(acc >> 64);
+  s_n[r][gl] = na;
   __syncthreads();
   if (r == 0 && g < G) {
     u128 t = (u128)ext[g] << ext_shift;
     ext[g] = 0;  // left clear for the next pass A (the only reader of ext is this kernel)
-    for (int i = 0; i < 16; ++i) t += make_u128(s_lo[i][gl], s_hi[i][gl]);
+    uint64_t nt = 0;
+    for (int i = 0; i < 16; ++i) {
+      t += make_u128(s_lo[i][gl], s_hi[i][gl]);
+      nt += s_n[i][gl];
+    }
     T[2 * g] = (uint64_t)t;
     T[2 * g + 1] = (uint64_t)(t >> 64);
+    if (pcount) cnt[g] = nt;
     write_scale(g, t, c, *Csum, P, scale, bscale);  // Eq. (3) scale of this (app, phase)
   }
 }
@@ -939,44 +963,59 @@ void launch_unpack_scale(hipStream_t s, const uint64_t* sw, uint64_t G, uint64_t
 }
 
 void launch_pass_a_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
-                       unsigned long long* partial, unsigned long long* carry, uint32_t* err) {
+                       unsigned long long* partial, unsigned long long* carry, uint32_t* pcount, uint32_t* err) {
   const uint32_t G = A * P;
-  const size_t smem = (size_t)G * 8;
-  hipLaunchKernelGGL((k_pass_a_lds<1024>), dim3(nblocks), dim3(1024), smem, s, ev, A, P, G, partial, carry, err);
+  if (pcount)
+    hipLaunchKernelGGL((k_pass_a_lds<1024, true>), dim3(nblocks), dim3(1024), (size_t)G * 12, s, ev, A, P, G, partial,
+                       carry, pcount, err);
+  else
+    hipLaunchKernelGGL((k_pass_a_lds<1024, false>), dim3(nblocks), dim3(1024), (size_t)G * 8, s, ev, A, P, G, partial,
+                       carry, pcount, err);
 }
 
 void launch_pass_a_reduce(hipStream_t s, const unsigned long long* partial, uint32_t nb, uint32_t G,
                           unsigned long long* carry, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
-                          uint32_t P, uint64_t* scale, void* bscale) {
+                          uint32_t P, uint64_t* scale, void* bscale, const uint32_t* pcount, uint64_t* cnt) {
   hipLaunchKernelGGL(k_pass_a_reduce<unsigned long long>, dim3((G + 63) / 64), dim3(1024), 0, s, partial, nb, G, carry,
-                     64, T, c, Csum, P, scale, (uint64_t*)bscale);
+                     64, T, c, Csum, P, scale, (uint64_t*)bscale, pcount, cnt);
 }
 
 void launch_pass_a_lds32(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
-                         uint32_t* partial, unsigned long long* ext, uint32_t* err) {
+                         uint32_t* partial, unsigned long long* ext, uint32_t* pcount, uint32_t* err) {
   const uint32_t G = A * P;
-  hipLaunchKernelGGL((k_pass_a_lds32<1024>), dim3(nblocks), dim3(1024), (size_t)G * 4, s, ev, A, P, G, partial, ext,
-                     err);
+  if (pcount)
+    hipLaunchKernelGGL((k_pass_a_lds32<1024, true>), dim3(nblocks), dim3(1024), (size_t)G * 8, s, ev, A, P, G,
+                       partial, ext, pcount, err);
+  else
+    hipLaunchKernelGGL((k_pass_a_lds32<1024, false>), dim3(nblocks), dim3(1024), (size_t)G * 4, s, ev, A, P, G,
+                       partial, ext, pcount, err);
 }
 
 void launch_pass_a_reduce32(hipStream_t s, const uint32_t* partial, uint32_t nb, uint32_t G,
                             unsigned long long* ext, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
-                            uint32_t P, uint64_t* scale, void* bscale) {
+                            uint32_t P, uint64_t* scale, void* bscale, const uint32_t* pcount, uint64_t* cnt) {
   hipLaunchKernelGGL(k_pass_a_reduce<uint32_t>, dim3((G + 63) / 64), dim3(1024), 0, s, partial, nb, G, ext, 32, T, c,
-                     Csum, P, scale, (uint64_t*)bscale);
+                     Csum, P, scale, (uint64_t*)bscale, pcount, cnt);
 }
 
 void launch_pass_a_range(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t GR, uint32_t R,
-                         uint32_t slices, uint32_t* partial, unsigned long long* ext, uint32_t* err) {
+                         uint32_t slices, uint32_t* partial, unsigned long long* ext, uint32_t* pcount, uint32_t* err) {
   const uint32_t G = A * P;
   const uint32_t nblocks = ((slices + 7) / 8) * 8 * R;
-  hipLaunchKernelGGL((k_pass_a_range<1024>), dim3(nblocks), dim3(1024), ((size_t)GR + 64) * 4, s, ev, A, P, G, GR, R, slices,
-                     partial, ext, err);
+  if (pcount)
+    hipLaunchKernelGGL((k_pass_a_range<1024, true>), dim3(nblocks), dim3(1024), ((size_t)2 * GR + 64) * 4, s, ev, A,
+                       P, G, GR, R, slices, partial, ext, pcount, err);
+  else
+    hipLaunchKernelGGL((k_pass_a_range<1024, false>), dim3(nblocks), dim3(1024), ((size_t)GR + 64) * 4, s, ev, A, P,
+                       G, GR, R, slices, partial, ext, pcount, err);
 }
 
 void launch_pass_a_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
-                          unsigned long long* T, uint32_t* err) {
-  hipLaunchKernelGGL((k_pass_a_global<256>), dim3(nblocks), dim3(256), 0, s, ev, A, P, T, err);
+                          unsigned long long* T, unsigned long long* cnt, uint32_t* err) {
+  if (cnt)
+    hipLaunchKernelGGL((k_pass_a_global<256, true>), dim3(nblocks), dim3(256), 0, s, ev, A, P, T, cnt, err);
+  else
+    hipLaunchKernelGGL((k_pass_a_global<256, false>), dim3(nblocks), dim3(256), 0, s, ev, A, P, T, cnt, err);
 }
 
 void launch_scale(hipStream_t s, const uint64_t* T, const uint32_t* c, const uint64_t* Csum, uint32_t A,
@@ -1035,13 +1074,14 @@ void launch_compact_rows(hipStream_t s, const GroupTables& gt, uint32_t P, const
 }
 
 hipError_t set_kernel_smem_limits() {
-  hipError_t e = hipFuncSetAttribute((const void*)k_pass_a_lds<1024>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     160 * 1024);
-  if (e != hipSuccess) return e;
-  e = hipFuncSetAttribute((const void*)k_pass_a_lds32<1024>, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-  if (e != hipSuccess) return e;
-  e = hipFuncSetAttribute((const void*)k_pass_a_range<1024>, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-  if (e != hipSuccess) return e;
+  const void* pass_a[] = {(const void*)k_pass_a_lds<1024, false>,   (const void*)k_pass_a_lds<1024, true>,
+                          (const void*)k_pass_a_lds32<1024, false>, (const void*)k_pass_a_lds32<1024, true>,
+                          (const void*)k_pass_a_range<1024, false>, (const void*)k_pass_a_range<1024, true>};
+  hipError_t e = hipSuccess;
+  for (const void* f : pass_a) {
+    e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+  }
   e = hipFuncSetAttribute((const void*)k_pass_b_lds<1024, true>, hipFuncAttributeMaxDynamicSharedMemorySize,
                           160 * 1024);
   if (e != hipSuccess) return e;

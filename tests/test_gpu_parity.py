@@ -73,9 +73,13 @@ def _config_case(ci, n):
     return cfg, ev, c
 
 
-@pytest.mark.parametrize("path", ENGINES)
+@pytest.mark.parametrize("path,count", [("lds_hash", True), ("global_hash", True), ("radix_sort", True),
+                                        ("lds_hash", False), ("radix_sort", False)])
 @pytest.mark.parametrize("ci,n", [(0, 1 << 20), (1, 1 << 21), (2, 1 << 20), (3, 1 << 21), (4, 1 << 21)])
-def test_config_prefix(path, ci, n):
+def test_config_prefix(path, count, ci, n):
+    """Prefixes of every workload; pass A with and without the per-(app,
+    phase) invocation counts (the counting variants take more LDS per pair, so
+    the 256M- and 1B-event workloads' pair tables split differently)."""
     cfg, ev, c = _config_case(ci, n)
     keys = synth.key_space(cfg)
     if keys.size > 1 << 18:
@@ -83,8 +87,9 @@ def test_config_prefix(path, ci, n):
     s = synth.scores(cfg, keys, nan_frac=0.1)
     H.say("config", ci, "n", n, path)
     g = H.run_gpu(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, cfg["num_phases"], path=path,
-                  score_key=keys, s=s, max_groups=2 * n, max_keys=n)
-    o = O.run(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, cfg["num_phases"], score_key=keys, s=s)
+                  score_key=keys, s=s, max_groups=2 * n, max_keys=n, app_count=count)
+    o = O.run(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, cfg["num_phases"], score_key=keys, s=s,
+              threads=8)
     H.compare(g, o, score=True)
 
 
@@ -137,8 +142,9 @@ def test_group_count_boundaries(path, G):
     H.compare(g, O.run(key, app, ph, dur, c, P))
 
 
+@pytest.mark.parametrize("count", [False, True])
 @pytest.mark.parametrize("seed", [0, 1])
-def test_range_split_pass_a_wraps_and_high_words(seed):
+def test_range_split_pass_a_wraps_and_high_words(seed, count):
     """100000 apps x 3 phases: pass A runs in ranges of the (app, phase)
     table with 32-bit LDS counters.  A third of the events land on one
     (app, phase) with durations near 2^31 (the 32-bit counter wraps every
@@ -156,8 +162,8 @@ def test_range_split_pass_a_wraps_and_high_words(seed):
     big = rng.random(n) < 0.1
     dur[big] = rng.integers(1 << 32, 1 << 40, int(big.sum()))
     c = rng.integers(1, 1000, A).astype(np.uint32)
-    H.say("range-split pass A, wraps and high words, seed", seed)
-    g = H.run_gpu(key, app, ph, dur, c, P, max_groups=2 * n, max_keys=n)
+    H.say("range-split pass A, wraps and high words, seed", seed, "counts", count)
+    g = H.run_gpu(key, app, ph, dur, c, P, max_groups=2 * n, max_keys=n, app_count=count)
     o = O.run(key, app, ph, dur, c, P)
     H.compare(g, o)
 
@@ -184,3 +190,24 @@ def test_weights_are_correctly_rounded_ratios(ci, n):
     for U, w in ((_u(g["op_U"]), g["op_w"]), (_u(g["key_U"]), g["omega"])):
         tot = float(sum(U))
         assert np.array_equal(w, np.array([float(u) / tot for u in U])), "unit weight"
+
+
+@pytest.mark.parametrize("path", ENGINES)
+def test_negative_scale_exponents(path):
+    """(app, phase) pairs whose Q96 factor 2^96 c_a / (C T) is below 2^-8 (one
+    app with c_a = 1 among apps of weight 2^32 - 1, with durations near 2^62):
+    rho < -8 takes the general scale word on every engine, and rho < 0 must
+    come back signed."""
+    rng = np.random.default_rng(17)
+    n, P, A = 20000, 2, 1000
+    key = ((rng.integers(0, 30, n) << 16) | rng.integers(0, 4, n)).astype(np.uint32)
+    app = rng.integers(0, A, n).astype(np.uint32)
+    app[: n // 2] = 0
+    ph = rng.integers(0, P, n).astype(np.uint8)
+    dur = rng.integers(1 << 60, 1 << 62, n).astype(np.int64)
+    c = np.full(A, 2 ** 32 - 1, np.uint32)
+    c[0] = 1
+    o = O.run(key, app, ph, dur, c, P)
+    assert o["rho"].min() < -8
+    H.say("negative scale exponents", path)
+    H.compare(H.run_gpu(key, app, ph, dur, c, P, path=path, max_groups=2 * n, max_keys=n), o)

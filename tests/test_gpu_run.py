@@ -233,3 +233,44 @@ def test_run_when_the_lds_engine_falls_back():
     G, path = _run_vs_separate(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, cfg["num_phases"], keys, s,
                                path="lds_hash", label="fallback")
     assert path == "lds_hash+radix_all"
+
+
+@pytest.mark.parametrize("ci,n", [(1, 1 << 21), (0, 1 << 20), (1, (1 << 21) + 3)])
+def test_one_wait_lds_path_matches_the_oracle(ci, n):
+    """The exact path the benchmark times on the 64M-event workload: atrex_run
+    with the capacities the benchmark gives (max_keys = the 4096-key space,
+    every key scored), so AUTO takes the LDS engine and the unit, weight and
+    score kernels enqueued behind the group-by are kept (one host wait).
+    Every output against the oracle, element by element (§3.4 Eq. (2)-(3),
+    §3.6 Eq. (4)-(6)); the 1M-event workload at its full size."""
+    from oracle import oracle as O
+    cfg = synth.CONFIGS[ci]
+    ev = synth.events(cfg, n=n)
+    c = synth.app_weights(cfg)
+    keys = synth.key_space(cfg)
+    s = synth.scores(cfg, keys)
+    P = cfg["num_phases"]
+    H.say("one-wait LDS path vs oracle, config", ci, "n", n, "keys", keys.size)
+    g, one_wait, path = H.run_one_call(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, P, keys, s,
+                                       max_keys=keys.size, max_groups=keys.size * P)
+    assert path == "lds_hash" and one_wait, (path, one_wait)
+    o = O.run(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, P, score_key=keys, s=s, threads=8)
+    H.compare(g, o, raw=False, score=True)
+
+
+def test_one_wait_path_with_nan_scores_and_app_counts():
+    """The same one-wait path with units marked incorrect (NaN) and the
+    per-(app, phase) invocation counts on."""
+    from oracle import oracle as O
+    cfg = synth.CONFIGS[1]
+    ev = synth.events(cfg, n=1 << 20)
+    c = synth.app_weights(cfg)
+    keys = synth.key_space(cfg)
+    s = synth.scores(cfg, keys, nan_frac=0.3)
+    H.say("one-wait LDS path, NaN scores, app counts")
+    g, one_wait, path = H.run_one_call(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, 2, keys, s,
+                                       max_keys=keys.size, max_groups=2 * keys.size, app_count=True)
+    assert path == "lds_hash" and one_wait
+    assert "app_n" in g
+    H.compare(g, O.run(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, 2, score_key=keys, s=s, threads=8),
+              raw=False, score=True)
