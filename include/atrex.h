@@ -214,6 +214,42 @@ atrex_status atrex_aggregate_destroy(atrex_ctx *ctx);
 
 const char *atrex_status_str(atrex_status s);
 
+/* ---- Allocation-free variant of atrex_run --------------------------------
+ * For callers that cannot allocate device memory or create a context: tight
+ * serving loops and harnesses that forbid hipMalloc.  It takes no context and
+ * no workspace and calls no hipMalloc, hipFree or other allocating routine:
+ * its scratch is a static device array of ATREX_NOALLOC_SCRATCH_BYTES that
+ * every GPU the library is loaded on holds until the process ends.  Calls that
+ * overlap on one GPU (from two host threads, or on two streams) race on that
+ * array and must be serialised by the caller.  Each call clears what must
+ * start at zero; nothing carries over between calls.  It synchronises the
+ * stream, so it cannot be captured into a HIP graph.
+ * Same outputs, statuses and order of checks as atrex_run (the per-(key,
+ * phase) group-by uses the global-hash engine, whose scratch does not grow
+ * with the number of events; results are identical).  CAPACITY when n,
+ * out_capacity, n_score or num_apps * num_phases exceeds the limits below, or
+ * the call's scratch does not fit the array. */
+#define ATREX_NOALLOC_SCRATCH_BYTES (64ull << 20)
+#define ATREX_NOALLOC_MAX_EVENTS (1ull << 24)
+#define ATREX_NOALLOC_MAX_GROUPS (1ull << 16) /* out_capacity */
+#define ATREX_NOALLOC_MAX_PAIRS (1ull << 13)  /* num_apps * num_phases */
+#define ATREX_NOALLOC_MAX_SCORE 8192ull       /* n_score */
+
+typedef struct {
+  uint32_t num_phases;            /* P in [1, 8] */
+  uint32_t num_apps;              /* A >= 1; event app ids must be < A */
+  const uint32_t *app_weight_q16; /* DEVICE [A]: card-hour weight c_a (Q16); sum must be > 0 */
+  void *stream;                   /* hipStream_t; NULL = default stream */
+} atrex_noalloc_params;
+
+/* HOST: p, ev (struct of DEVICE pointers), out (struct of DEVICE pointers), r;
+ * score_key, s, op, op_weight, op_score as for atrex_run (DEVICE). */
+atrex_status atrex_run_noalloc(const atrex_noalloc_params *p, const atrex_events *ev,
+                               const atrex_groups *out, uint64_t out_capacity,
+                               const uint32_t *score_key, const double *s, uint64_t n_score,
+                               uint32_t *op, double *op_weight, double *op_score,
+                               atrex_run_result *r);
+
 #ifdef __cplusplus
 }
 #endif

@@ -51,6 +51,11 @@ class _Groups(ctypes.Structure):
                 ("phase_total", ctypes.c_void_p), ("raw_ns", ctypes.c_void_p)]
 
 
+class _NoAllocParams(ctypes.Structure):
+    _fields_ = [("num_phases", ctypes.c_uint32), ("num_apps", ctypes.c_uint32),
+                ("app_weight_q16", ctypes.c_void_p), ("stream", ctypes.c_void_p)]
+
+
 class _RunResult(ctypes.Structure):
     _fields_ = [("num_groups", ctypes.c_uint64), ("num_ops", ctypes.c_uint64), ("num_keys", ctypes.c_uint64),
                 ("num_scored_ops", ctypes.c_uint64), ("s_agg", ctypes.c_double), ("one_wait", ctypes.c_uint32)]
@@ -78,6 +83,8 @@ def _lib() -> ctypes.CDLL:
                                      ctypes.POINTER(ctypes.c_double)],
             "atrex_run": [P, ctypes.POINTER(_Events), ctypes.POINTER(_Groups), U64, P, P, U64, P, P, P,
                           ctypes.POINTER(_RunResult)],
+            "atrex_run_noalloc": [ctypes.POINTER(_NoAllocParams), ctypes.POINTER(_Events), ctypes.POINTER(_Groups),
+                                  U64, P, P, U64, P, P, P, ctypes.POINTER(_RunResult)],
             "atrex_get_app_totals": [P, P, P, P, P],
             "atrex_kernel_times": [P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float),
                                    ctypes.POINTER(U64), I, ctypes.POINTER(I)],
@@ -377,3 +384,45 @@ def aggregate(key, app, phase, dur_ns, app_weight_q16, num_phases, path="auto", 
         return out
     finally:
         ag.close()
+
+
+def run_noalloc(key, app, phase, dur_ns, app_weight_q16, num_phases, out: dict, score_key=None, s=None,
+                score_out: dict | None = None, stream: torch.cuda.Stream | None = None) -> dict:
+    """The whole path through atrex_run_noalloc: no context, no workspace, no
+    device allocation by the library (caller-owned inputs and outputs only).
+    `out` as from Aggregator.group_buffers(); `score_out` holds op / op_weight /
+    op_score tensors of at least len(score_key) entries.  Returns the counts,
+    s_agg and views of the first num_groups / num_scored_ops entries."""
+    key = _dev(_as_i32(key), torch.int32, "key")
+    app = _dev(_as_i32(app), torch.int32, "app")
+    phase = _dev(phase, torch.uint8, "phase")
+    dur_ns = _dev(dur_ns, torch.int64, "dur_ns")
+    c = _dev(_as_i32(app_weight_q16), torch.int32, "app_weight_q16")
+    n = key.numel()
+    if not (app.numel() == n and phase.numel() == n and dur_ns.numel() == n):
+        raise ValueError("event arrays differ in length")
+    st = stream if stream is not None else torch.cuda.current_stream(key.device)
+    p = _NoAllocParams(int(num_phases), c.numel(), c.data_ptr(), st.cuda_stream)
+    ev = _Events(_ptr(key), _ptr(app), _ptr(phase), _ptr(dur_ns), n)
+    g = _Groups(_ptr(out["key"]), _ptr(out["phase"]), _ptr(out["count"]), _ptr(out["wsum"]),
+                _ptr(out["weight"]), _ptr(out["phase_total"]), _ptr(out.get("raw_ns")))
+    nsc, sp = 0, (ctypes.c_void_p(0),) * 5
+    if score_key is not None:
+        score_key = _dev(_as_i32(score_key), torch.int32, "score_key")
+        s = _dev(s, torch.float64, "s")
+        nsc = score_key.numel()
+        if s.numel() != nsc:
+            raise ValueError("score_key and s differ in length")
+        if any(score_out[k].numel() < nsc for k in ("op", "op_weight", "op_score")):
+            raise ValueError("score output buffers too small")
+        sp = (_ptr(score_key), _ptr(s), _ptr(score_out["op"]), _ptr(score_out["op_weight"]),
+              _ptr(score_out["op_score"]))
+    r = _RunResult()
+    _check(_lib().atrex_run_noalloc(ctypes.byref(p), ctypes.byref(ev), ctypes.byref(g), out["key"].numel(), sp[0],
+                                    sp[1], nsc, sp[2], sp[3], sp[4], ctypes.byref(r)), "atrex_run_noalloc")
+    G, k = r.num_groups, r.num_scored_ops
+    res = dict(num_groups=G, num_ops=r.num_ops, num_keys=r.num_keys, num_scored_ops=k, s_agg=r.s_agg,
+               groups={kk: (t if kk == "phase_total" else t[:G]) for kk, t in out.items()})
+    if score_key is not None:
+        res["score"] = {kk: score_out[kk][:k] for kk in ("op", "op_weight", "op_score")}
+    return res

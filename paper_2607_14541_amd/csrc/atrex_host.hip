@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -63,7 +64,8 @@ struct Params {
   uint32_t P, A;
   uint64_t max_events, max_groups, max_keys, max_score;
   bool raw;
-  bool count;  // invocation counts per (app, phase) in pass A
+  bool count;    // invocation counts per (app, phase) in pass A
+  bool compact;  // global-hash engine only: no per-event scratch, rows sized to the groups
 };
 
 constexpr uint32_t kPassARangesMax = 16;
@@ -100,12 +102,17 @@ Layout make_layout(const Params& p) {
   L.capD = next_pow2(std::max<uint64_t>(1024, 2 * L.maxK));
   L.maxOps = std::min<uint64_t>(L.maxG, 65536);
   L.passA = pass_a_mode(GA, p.count);
-  L.partA_rows = L.passA == 0 ? kPartialRowsMax : L.passA == 1 ? kMaxWG : L.passA == 3 ? kPassASlices : 0;
+  L.partA_rows = L.passA == 0 ? (p.compact ? kMaxWG : kPartialRowsMax)
+                 : L.passA == 1 ? kMaxWG : L.passA == 3 ? kPassASlices : 0;
   L.ldsSlots = pass_b_lds_slots(p.P, p.raw, kLdsBytes);
   L.tabSlots = lds_table_slots(p.P, p.raw, kLdsBytes);
   L.capo = owner_cap(L.ldsSlots);
   L.scap = spill_cap(p.max_events, kMaxWG);
-  L.maxRows = 2 * L.maxG + (1 << 21);
+  // the global-hash engine emits one row per group; the others may emit a
+  // group's rows from several workgroups or bucket chunks
+  L.maxRows = p.compact ? L.maxG : 2 * L.maxG + (1 << 21);
+  // regions of the LDS and partition engines (none in the compact layout)
+  const uint64_t lds_eng = p.compact ? 0 : 1, part_eng = p.compact ? 0 : 1;
   L.maxSort = std::max<uint64_t>(L.maxSort, L.maxRows);
   const uint64_t accw = (p.raw ? 2 : 1);
   L.ctrl = take(4096);
@@ -119,33 +126,33 @@ Layout make_layout(const Params& p) {
   L.dict = take(L.capD * 8);
   L.acc = take(L.capD * p.P * 16);
   L.raw = take(p.raw ? L.capD * p.P * 16 : 0);
-  const uint64_t oslots = kMaxWG * ATREX_OWNERS * (uint64_t)L.capo;
+  const uint64_t oslots = lds_eng * kMaxWG * ATREX_OWNERS * (uint64_t)L.capo;
   L.okey = take(oslots * 4);
   L.oacc = take(oslots * p.P * 16);
   L.oraw = take(p.raw ? oslots * p.P * 16 : 0);
-  L.ocount = take(kMaxWG * ATREX_OWNERS * 4);
-  const uint64_t sslots = kMaxWG * (uint64_t)L.scap;
+  L.ocount = take(lds_eng * kMaxWG * ATREX_OWNERS * 4);
+  const uint64_t sslots = lds_eng * kMaxWG * (uint64_t)L.scap;
   L.skey = take(sslots * 4);
   L.sval = take(sslots * 16);
   L.sraw = take(p.raw ? sslots * 8 : 0);
-  L.scount = take(kMaxWG * 4);
+  L.scount = take(lds_eng * kMaxWG * 4);
   L.oSlots = owner_list_slots(p.P, p.raw);
-  const uint64_t olrows = (uint64_t)ATREX_OWNERS * L.oSlots * p.P;
+  const uint64_t olrows = lds_eng * ATREX_OWNERS * L.oSlots * p.P;
   L.ol_rk = take(olrows * 8);
   L.ol_key = take(olrows * 4);
   L.ol_lo = take(olrows * 8);
   L.ol_hi = take(olrows * 8);
   L.ol_rlo = take(p.raw ? olrows * 8 : 0);
   L.ol_rhi = take(p.raw ? olrows * 8 : 0);
-  L.ol_count = take(ATREX_OWNERS * 4);
-  L.ol_part = take((uint64_t)ATREX_OWNERS * p.P * 16);
-  const uint64_t hsz = ((uint64_t)1 << kMaxBucketBits) * std::max<uint64_t>(kMaxWG, kMaxPartWG);
+  L.ol_count = take(lds_eng * ATREX_OWNERS * 4);
+  L.ol_part = take(lds_eng * ATREX_OWNERS * p.P * 16);
+  const uint64_t hsz = part_eng * ((uint64_t)1 << kMaxBucketBits) * std::max<uint64_t>(kMaxWG, kMaxPartWG);
   L.H = take(hsz * 4);
   L.O = take(hsz * 4);
-  L.rec = take(p.max_events * 16);
-  L.rraw = take(p.raw ? p.max_events * 8 : 0);
-  L.bstart = take((((uint64_t)1 << kMaxBucketBits) + 1) * 4);
-  L.istart = take((((uint64_t)1 << kMaxBucketBits) + 1) * 4);
+  L.rec = take(part_eng * p.max_events * 16);
+  L.rraw = take(p.raw ? part_eng * p.max_events * 8 : 0);
+  L.bstart = take(part_eng * (((uint64_t)1 << kMaxBucketBits) + 1) * 4);
+  L.istart = take(part_eng * (((uint64_t)1 << kMaxBucketBits) + 1) * 4);
   L.rk = take(L.maxRows * 8);
   L.rlo_acc = take(L.maxRows * 8);
   L.rhi_acc = take(L.maxRows * 8);
@@ -213,6 +220,7 @@ atrex_status check_params(const atrex_init_params* ip, Params* out) {
     return ATREX_E_INVALID_ARG;
   p.raw = (ip->flags & ATREX_FLAG_RAW) != 0;
   p.count = (ip->flags & ATREX_FLAG_APP_COUNT) != 0;
+  p.compact = false;
   *out = p;
   return ATREX_OK;
 }
@@ -390,6 +398,17 @@ struct atrex_ctx {
 
 namespace {
 
+// The kernels' dynamic LDS limits, set once per process.
+hipError_t ensure_smem_limits() {
+  static std::mutex mu;
+  static bool done = false;
+  std::lock_guard<std::mutex> lk(mu);
+  if (done) return hipSuccess;
+  const hipError_t e = set_kernel_smem_limits();
+  if (e == hipSuccess) done = true;
+  return e;
+}
+
 atrex_status sync_status(atrex_ctx* c) {
   const hipError_t e1 = hipGetLastError();
   const hipError_t e2 = hipStreamSynchronize(c->s);
@@ -551,11 +570,7 @@ atrex_status atrex_aggregate_init(const atrex_init_params* ip, atrex_ctx** out) 
   if (!ip->app_weight_q16 || !ip->workspace || !aligned(ip->workspace, kAlign)) return ATREX_E_INVALID_ARG;
   const Layout L = make_layout(p);
   if (ip->workspace_bytes < L.bytes) return ATREX_E_CAPACITY;
-  static bool smem_set = false;
-  if (!smem_set) {
-    if (set_kernel_smem_limits() != hipSuccess) return ATREX_E_DEVICE;
-    smem_set = true;
-  }
+  if (ensure_smem_limits() != hipSuccess) return ATREX_E_DEVICE;
   atrex_ctx* c = new (std::nothrow) atrex_ctx();
   if (!c) return ATREX_E_INVALID_ARG;
   c->p = p;
@@ -657,7 +672,7 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
     // one workgroup per CU (two groups of loads in flight per lane): two per
     // CU ran as one after the other (the SIMDs favour the older one) and
     // doubled the partial rows for the reduce
-    uint64_t nb = std::min<uint64_t>((uint64_t)c->cus, kPartialRowsMax);
+    uint64_t nb = std::min<uint64_t>((uint64_t)c->cus, L.partA_rows);
     nb = std::max<uint64_t>(1, std::min<uint64_t>(nb, (n / 4 + kPassAThreads - 1) / kPassAThreads));
     TIMED(c, "pass_a", n,
           launch_pass_a_lds(s, d, A, P, (uint32_t)nb, c->at<unsigned long long>(L.partA),
@@ -699,6 +714,7 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
   const Rows rows = c->rows();
   atrex_path path = c->path;
   if (path == ATREX_PATH_AUTO) path = (c->p.max_keys <= L.ldsSlots) ? ATREX_PATH_LDS_HASH : ATREX_PATH_RADIX_SORT;
+  if (c->p.compact) path = ATREX_PATH_GLOBAL_HASH;  // the only engine the compact layout holds
   // the LDS engine indexes its scale words with 24-bit multiplies
   if (path == ATREX_PATH_LDS_HASH && (uint64_t)A * P >= (1u << 24)) path = ATREX_PATH_RADIX_SORT;
   if (!vec_ok && path != ATREX_PATH_GLOBAL_HASH) path = ATREX_PATH_GLOBAL_HASH;
@@ -1256,3 +1272,97 @@ atrex_status atrex_aggregate_destroy(atrex_ctx* c) {
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// atrex_run without a context or workspace, for callers that cannot allocate.
+// Its device memory is `scratch`, one copy per GPU for the life of the
+// process.  Host code never uses the array's name as an address (it is a
+// host-side stand-in): each device's address comes from hipGetSymbolAddress
+// on the first call with that device current.
+namespace {
+constexpr int kNoAllocDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kNoAllocDevices];
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[ATREX_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+hipError_t scratch_on_device(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kNoAllocDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress((void**)&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_dev[dev] = ptr;
+  }
+  *out = g_scratch_dev[dev];
+  return hipSuccess;
+}
+}  // namespace
+
+extern "C" atrex_status atrex_run_noalloc(const atrex_noalloc_params* np, const atrex_events* ev,
+                                          const atrex_groups* out, uint64_t out_capacity, const uint32_t* score_key,
+                                          const double* sv, uint64_t n_score, uint32_t* op, double* op_weight,
+                                          double* op_score, atrex_run_result* r) {
+  if (!np || !ev || !out || !r) return ATREX_E_INVALID_ARG;
+  *r = atrex_run_result{};
+  if (!np->app_weight_q16 || np->num_phases < 1 || np->num_phases > 8 || np->num_apps < 1)
+    return ATREX_E_INVALID_ARG;
+  if (ev->n > ATREX_NOALLOC_MAX_EVENTS || out_capacity > ATREX_NOALLOC_MAX_GROUPS ||
+      n_score > ATREX_NOALLOC_MAX_SCORE || (uint64_t)np->num_apps * np->num_phases > ATREX_NOALLOC_MAX_PAIRS)
+    return ATREX_E_CAPACITY;
+  // the layout of this call's sizes, in the compact form (global-hash engine)
+  atrex_init_params ip{};
+  ip.num_phases = np->num_phases;
+  ip.num_apps = np->num_apps;
+  ip.app_weight_q16 = np->app_weight_q16;
+  ip.max_events = std::max<uint64_t>(ev->n, 1);
+  ip.max_groups = std::max<uint64_t>(out_capacity, 1);
+  ip.max_keys = ip.max_groups;
+  ip.max_score = std::max<uint64_t>(n_score, 1);
+  ip.path = ATREX_PATH_GLOBAL_HASH;
+  Params p;
+  atrex_status st = check_params(&ip, &p);
+  if (st != ATREX_OK) return st;
+  p.compact = true;
+  const Layout L = make_layout(p);
+  if (L.bytes > ATREX_NOALLOC_SCRATCH_BYTES) return ATREX_E_CAPACITY;
+  if (ensure_smem_limits() != hipSuccess) return ATREX_E_DEVICE;
+  void* ws = nullptr;
+  if (scratch_on_device(&ws) != hipSuccess) return ATREX_E_DEVICE;
+  // the context lives on the stack; without a mapped host buffer its status
+  // readbacks are plain copies into its own host words
+  atrex_ctx c;
+  c.p = p;
+  c.L = L;
+  c.ws = (char*)ws;
+  c.s = (hipStream_t)np->stream;
+  c.path = ATREX_PATH_GLOBAL_HASH;
+  c.flags = 0;
+  c.app_weight = np->app_weight_q16;
+  c.state = 0;
+  c.S_ready = false;
+  c.G = c.nops = c.nkeys = 0;
+  c.path_used = "none";
+  c.ntimed = 0;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&c.cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return ATREX_E_DEVICE;
+  // the array keeps the previous call's contents: clear what must start at
+  // zero (the pass-A carry table; the call clears or writes everything else),
+  // with a fill kernel, and compute C = sum c_a as init does
+  launch_fill_u64(c.s, c.at<uint64_t>(L.carryA), (uint64_t)p.A * p.P, 0);
+  launch_sum_u32(c.s, c.app_weight, p.A, c.Csum());
+  uint64_t C = 0;
+  d2h(&c, &C, c.Csum(), 8);
+  st = sync_read(&c);
+  if (st != ATREX_OK) return st;
+  if (C == 0) return ATREX_E_INVALID_ARG;
+  return atrex_run(&c, ev, out, out_capacity, score_key, sv, n_score, op, op_weight, op_score, r);
+}
