@@ -124,14 +124,16 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_lds32(EventsDev ev, uint32_t A
   }
 }
 
+constexpr int RANGE_DEPTH = 6;  // groups of four events in flight per lane in k_pass_a_range
+
 // Pass A for more (app, phase) pairs than one LDS holds: the pairs are split
 // into R ranges of at most GR, the events into `slices`; each workgroup sums
 // one (slice, range) in 32-bit LDS counters (wraps and high halves into ext[g]
 // as in k_pass_a_lds32).  The R workgroups of a slice are placed on one XCD
 // (workgroups go round-robin over the 8 XCDs) and walk the slice in the same
 // order with ordinary (L2-allocating) loads, so the slice comes from HBM about
-// once and from that XCD's L2 for the others.  Each lane keeps three groups of
-// four events in flight (loads issued two iterations ahead).  COUNT: a u32
+// once and from that XCD's L2 for the others.  Each lane keeps RANGE_DEPTH
+// groups of four events in flight.  COUNT: a u32
 // count table after the GR counters and their spares.
 template <int BLOCK, bool COUNT>
 __global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A, uint32_t P, uint32_t G,
@@ -240,19 +242,20 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A
 #pragma unroll
     for (int j = 0; j < 4; ++j) one(av[j], (x.p >> (8 * j)) & 0xFFu, dv[j]);
   };
-  G4 x0, x1, x2;
-  if (0 < iters) load(0, x0);
-  if (1 < iters) load(1, x1);
-  if (2 < iters) load(2, x2);
-  for (uint64_t it = 0; it < iters; it += 3) {
-    process(it, x0);
-    if (it + 3 < iters) load(it + 3, x0);
-    if (it + 1 >= iters) break;
-    process(it + 1, x1);
-    if (it + 4 < iters) load(it + 4, x1);
-    if (it + 2 >= iters) break;
-    process(it + 2, x2);
-    if (it + 5 < iters) load(it + 5, x2);
+  // a ring of DEPTH groups per lane: group it is processed while the loads of
+  // the next DEPTH - 1 are in flight (the loads come from L2 with a long
+  // latency under the R-fold re-reads; the waves would otherwise wait on them)
+  G4 x[RANGE_DEPTH];
+#pragma unroll
+  for (int k = 0; k < RANGE_DEPTH; ++k)
+    if ((uint64_t)k < iters) load(k, x[k]);
+  for (uint64_t it = 0; it < iters; it += RANGE_DEPTH) {
+#pragma unroll
+    for (int k = 0; k < RANGE_DEPTH; ++k) {
+      if (it + k >= iters) break;
+      process(it + k, x[k]);
+      if (it + k + RANGE_DEPTH < iters) load(it + k + RANGE_DEPTH, x[k]);
+    }
   }
   for (uint64_t i = b + 4 * ng + threadIdx.x; i < e; i += BLOCK) one(ev.app[i], ev.phase[i], ev.dur[i]);
   flag_error(err, bad, ATREX_ERRBIT_RANGE);

@@ -794,12 +794,18 @@ __global__ __launch_bounds__(1024) void k_part_aggregate(const uint64_t* __restr
   extern __shared__ unsigned long long smem[];
   __shared__ uint32_t s_wsum[16];
   __shared__ unsigned long long s_base;
-  const uint32_t SP = S * P, region = 2 * SP + 128;
-  unsigned long long* acc = smem;                        // [S * P] x (lo, hi), then 64 dummies
-  unsigned long long* racc = smem + region;              // RAW only
+  // low and high words of the [S * P] accumulators as two arrays (a wave's
+  // 64-bit atomics then spread over twice the LDS banks of interleaved
+  // pairs), each followed by 64 per-lane dummy entries for lanes with nothing
+  // to add (never read); RAW: the same again
+  const uint32_t SP = S * P, NE = SP + 64, region = 2 * NE;
+  unsigned long long* lo_ = smem;
+  unsigned long long* hi_ = smem + NE;
+  unsigned long long* rlo_ = smem + region;  // RAW only
+  unsigned long long* rhi_ = smem + region + NE;
   uint32_t* tag = (uint32_t*)(smem + (RAW ? 2 : 1) * region);  // [S], 16-byte aligned
   const uint32_t NB = 1u << BB, lowbits = 32 - BB, NBK = S / 4;
-  const uint32_t lane = lane_of(), dummy = 2 * SP + 2 * lane;
+  const uint32_t lane = lane_of(), dummy = SP + lane;
   const uint32_t items = item_start[NB];
   auto bucket_tags = [&](uint32_t bq) -> uint4 { return *(const uint4*)&tag[4 * bq]; };
   auto find_slot = [&](uint32_t k, uint32_t bq, uint4 tv) -> int32_t {
@@ -833,9 +839,10 @@ __global__ __launch_bounds__(1024) void k_part_aggregate(const uint64_t* __restr
     const uint32_t c = it - item_start[bkt];
     const uint32_t r0 = bstart[bkt] + c * CH;
     const uint32_t r1 = min(bstart[bkt + 1], r0 + CH);
-    for (uint32_t i = threadIdx.x; i < 2 * SP; i += blockDim.x) {
-      acc[i] = 0;
-      if (RAW) racc[i] = 0;
+    for (uint32_t i = threadIdx.x; i < SP; i += blockDim.x) {
+      lo_[i] = 0;
+      hi_[i] = 0;
+      if (RAW) { rlo_[i] = 0; rhi_[i] = 0; }
     }
     for (uint32_t i = threadIdx.x; i < S; i += blockDim.x) tag[i] = EMPTY_TAG;
     __syncthreads();
@@ -916,32 +923,32 @@ __global__ __launch_bounds__(1024) void k_part_aggregate(const uint64_t* __restr
         if (hot.take(gi[j], vlo[j], vhi[j], d[j])) gi[j] = 0xFFFFFFFFu;
       uint32_t at[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) at[j] = gi[j] != 0xFFFFFFFFu ? 2 * gi[j] : dummy;
+      for (int j = 0; j < 4; ++j) at[j] = gi[j] != 0xFFFFFFFFu ? gi[j] : dummy;
       unsigned long long old[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) old[j] = atomicAdd(&acc[at[j]], (unsigned long long)vlo[j]);
+      for (int j = 0; j < 4; ++j) old[j] = atomicAdd(&lo_[at[j]], (unsigned long long)vlo[j]);
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        atomicAdd(&acc[at[j] + 1],
+        atomicAdd(&hi_[at[j]],
                   (unsigned long long)vhi[j] + ((old[j] + vlo[j] < old[j]) ? 1ull : 0ull) + (1ull << ATREX_COUNT_SHIFT));
       if (RAW) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) old[j] = atomicAdd(&racc[at[j]], (unsigned long long)d[j]);
+        for (int j = 0; j < 4; ++j) old[j] = atomicAdd(&rlo_[at[j]], (unsigned long long)d[j]);
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          if (old[j] + d[j] < old[j]) atomicAdd(&racc[at[j] + 1], 1ull);
+          if (old[j] + d[j] < old[j]) atomicAdd(&rhi_[at[j]], 1ull);
       }
     }
     hot.flush([&](uint32_t g, u128 tv, uint32_t c, u128 tr) {
-      acc_add_n(&acc[2 * g], &acc[2 * g + 1], tv, c);
-      if (RAW) acc_add_plain(&racc[2 * g], &racc[2 * g + 1], tr);
+      acc_add_n(&lo_[g], &hi_[g], tv, c);
+      if (RAW) acc_add_plain(&rlo_[g], &rhi_[g], tr);
     });
     __syncthreads();
     // the item's rows: each thread takes a contiguous run of (slot, phase)
     // entries; one row-list reservation per workgroup
     const uint32_t per = (SP + blockDim.x - 1) / blockDim.x, e0 = threadIdx.x * per;
     auto present = [&](uint32_t i) {
-      return i < SP && tag[i / P] != EMPTY_TAG && (acc[2 * i + 1] >> ATREX_COUNT_SHIFT) != 0;
+      return i < SP && tag[i / P] != EMPTY_TAG && (hi_[i] >> ATREX_COUNT_SHIFT) != 0;
     };
     uint32_t mine = 0;
     for (uint32_t k = 0; k < per; ++k) mine += present(e0 + k) ? 1u : 0u;
@@ -970,9 +977,9 @@ __global__ __launch_bounds__(1024) void k_part_aggregate(const uint64_t* __restr
       }
       const uint32_t sl = i / P, ph = i - sl * P;
       rows.rk[pos] = ((uint64_t)unmix32((bkt << lowbits) | tag[sl]) << 3) | ph;
-      rows.lo[pos] = acc[2 * i];
-      rows.hi[pos] = acc[2 * i + 1];
-      if (RAW) { rows.rlo[pos] = racc[2 * i]; rows.rhi[pos] = racc[2 * i + 1]; }
+      rows.lo[pos] = lo_[i];
+      rows.hi[pos] = hi_[i];
+      if (RAW) { rows.rlo[pos] = rlo_[i]; rows.rhi[pos] = rhi_[i]; }
       ++pos;
     }
     __syncthreads();
