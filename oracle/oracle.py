@@ -20,22 +20,33 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "atrex_oracle.cpp")
-_LIB = os.path.join(_HERE, "libatrex_oracle.so")
+# ATREX_ORACLE_SANITIZE=1: an AddressSanitizer + UndefinedBehaviorSanitizer
+# build (the process must have the ASan runtime preloaded)
+SANITIZE = os.environ.get("ATREX_ORACLE_SANITIZE") == "1"
+_LIB = os.path.join(_HERE, "libatrex_oracle_san.so" if SANITIZE else "libatrex_oracle.so")
+_SAN_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+              "-fno-sanitize-recover=undefined"]
 
 OK, E_INVALID_ARG, E_OUT_OF_RANGE, E_STATE = 0, -1, -2, -3
 
 
 def build(force: bool = False) -> str:
-    """Compile the oracle with g++ (plain C++17, -O2)."""
+    """Compile the oracle with g++ (plain C++17, -O2; sanitized with
+    ATREX_ORACLE_SANITIZE=1)."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", "-Wall", "-pthread",
+        opt = _SAN_FLAGS if SANITIZE else ["-O2"]
+        subprocess.check_call(["g++", *opt, "-std=c++17", "-fPIC", "-shared", "-Wall", "-pthread",
                                "-o", tmp, _SRC])
         os.replace(tmp, _LIB)
     return _LIB
 
 
 _lib = None
+
+
+def library_path() -> str:
+    return _LIB
 
 
 def lib() -> ctypes.CDLL:

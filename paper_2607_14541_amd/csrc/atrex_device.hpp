@@ -136,9 +136,15 @@ __device__ __forceinline__ void lds_stage(D* dst, const T* __restrict__ src, uin
 }
 
 // --- hashing ----------------------------------------------------------------
-// Multiplicative (Fibonacci) hash; the slot is taken from the high bits.
+// Multiplicative (Fibonacci) hash; the slot is taken from the high bits.  The
+// multiplier is the odd integer nearest 2^32 / phi (golden ratio), Knuth's
+// multiplicative hashing (TAOCP vol. 3, §6.4).
 __device__ __forceinline__ uint32_t hash_mul(uint32_t k) { return k * 0x9E3779B1u; }
 
+// An invertible 32-bit mixer of xorshift-multiply rounds (shifts 16, 15, 16):
+// the "lowbias32" function found by C. Wellons' hash-prospector search
+// (published 2018, public domain).  Every round is a bijection, so the key can
+// be recovered from the hash (the inverse is unmix32 in kernels_rows.hip).
 __device__ __forceinline__ uint32_t hash32(uint32_t k) {
   k ^= k >> 16;
   k *= 0x7feb352dU;

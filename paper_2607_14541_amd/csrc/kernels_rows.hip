@@ -24,7 +24,11 @@ namespace {
 constexpr uint32_t MAXPROBE_R = 32;
 constexpr uint32_t EMPTY_TAG = 0xFFFFFFFFu;
 
-// Invertible 32-bit mix (xorshift-multiply) and its inverse.
+// Inverse of hash32 (atrex_device.hpp, the "lowbias32" mixer of C. Wellons'
+// hash-prospector): its rounds undone in reverse order.  x ^= x >> 16 is its
+// own inverse on 32 bits; x ^= x >> 15 is undone by x ^= (x >> 15) ^ (x >> 30);
+// each multiplier is replaced by its inverse modulo 2^32 (checked: the
+// products 0x846ca68b * 0x43021123 and 0x7feb352d * 0x1d69e2a5 are 1 mod 2^32).
 __device__ __forceinline__ uint32_t unmix32(uint32_t h) {
   h ^= h >> 16;
   h *= 0x43021123u;  // inverse of 0x846ca68b mod 2^32
