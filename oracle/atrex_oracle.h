@@ -97,6 +97,31 @@ int atrex_oracle_weighted_score(atrex_oracle *o, const uint32_t *score_key,
 
 void atrex_oracle_destroy(atrex_oracle *o);
 
+/* ---- Target-DSL device-time share ("adoption", §4.1 Metrics);
+ * atrex_oracle_adoption.cpp.  Events of one profile: key, is_dsl (1 = the
+ * invocation ran inside the target DSL, 0 = not; anything else is
+ * OUT_OF_RANGE), dur >= 0; n < 2^31.
+ *   D_dsl[k], D_tot[k] = sums of dur (u128);  share[k] = RN(D_dsl)/RN(D_tot),
+ *   NaN when D_tot = 0 (the shape did not run);
+ *   op_share[i] = exact mean of share over operator i's running shapes,
+ *   rounded once (NaN when none runs);
+ *   adoption = exact mean of op_share over the operators where it is
+ *   defined, rounded once (NaN when none is). */
+typedef struct atrex_oracle_share atrex_oracle_share;
+int atrex_oracle_share_compute(const uint32_t *key, const uint8_t *is_dsl, const int64_t *dur_ns,
+                               uint64_t n, atrex_oracle_share **out);
+int atrex_oracle_share_sizes(const atrex_oracle_share *s, uint64_t *num_keys, uint64_t *num_ops);
+/* keys ascending; count = invocations; dsl/total (lohi) */
+int atrex_oracle_share_keys(const atrex_oracle_share *s, uint32_t *key, uint64_t *count,
+                            uint64_t *dsl_lohi, uint64_t *total_lohi, double *share);
+/* operators ascending (every operator with an invocation); shapes = running shapes */
+int atrex_oracle_share_ops(const atrex_oracle_share *s, uint32_t *op, uint32_t *shapes, double *op_share,
+                           double *adoption, uint64_t *defined_ops);
+void atrex_oracle_share_destroy(atrex_oracle_share *s);
+/* The exact mean of n >= 1 finite non-negative doubles whose mean is a normal
+ * number, rounded to nearest, ties to even (NaN for n = 0). */
+double atrex_oracle_exact_mean(const double *x, uint64_t n);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,4 +1,4 @@
-"""ctypes binding of the CPU oracle (atrex_oracle.cpp).
+"""ctypes binding of the CPU oracle (atrex_oracle*.cpp, one shared library).
 
 TEST INFRASTRUCTURE ONLY: imported by tests/, by the smoke check and by the
 benchmark's CPU-baseline leg.  The product path (the GPU library and its
@@ -19,7 +19,9 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRC = os.path.join(_HERE, "atrex_oracle.cpp")
+# every oracle source: the weighting path, and the rows built beside it
+SOURCES = [os.path.join(_HERE, f) for f in ("atrex_oracle.cpp", "atrex_oracle_adoption.cpp")]
+_HDR = os.path.join(_HERE, "atrex_oracle.h")
 # ATREX_ORACLE_SANITIZE=1: an AddressSanitizer + UndefinedBehaviorSanitizer
 # build (the process must have the ASan runtime preloaded)
 SANITIZE = os.environ.get("ATREX_ORACLE_SANITIZE") == "1"
@@ -33,11 +35,12 @@ OK, E_INVALID_ARG, E_OUT_OF_RANGE, E_STATE = 0, -1, -2, -3
 def build(force: bool = False) -> str:
     """Compile the oracle with g++ (plain C++17, -O2; sanitized with
     ATREX_ORACLE_SANITIZE=1)."""
-    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+    newest = max(os.path.getmtime(f) for f in SOURCES + [_HDR])
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < newest:
         tmp = _LIB + ".tmp%d" % os.getpid()
         opt = _SAN_FLAGS if SANITIZE else ["-O2"]
         subprocess.check_call(["g++", *opt, "-std=c++17", "-fPIC", "-shared", "-Wall", "-pthread",
-                               "-o", tmp, _SRC])
+                               "-o", tmp, *SOURCES])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -71,6 +74,17 @@ def lib() -> ctypes.CDLL:
                      "op_weights", "num_keys", "key_weights", "weighted_score"):
             getattr(L, "atrex_oracle_" + name).restype = ctypes.c_int
         L.atrex_oracle_destroy.restype = None
+        # target-DSL device-time share (atrex_oracle_adoption.cpp)
+        L.atrex_oracle_share_compute.argtypes = [P, P, P, U64, ctypes.POINTER(P)]
+        L.atrex_oracle_share_sizes.argtypes = [P, P, P]
+        L.atrex_oracle_share_keys.argtypes = [P, P, P, P, P, P]
+        L.atrex_oracle_share_ops.argtypes = [P, P, P, P, P, P]
+        L.atrex_oracle_share_destroy.argtypes = [P]
+        L.atrex_oracle_share_destroy.restype = None
+        for name in ("share_compute", "share_sizes", "share_keys", "share_ops"):
+            getattr(L, "atrex_oracle_" + name).restype = ctypes.c_int
+        L.atrex_oracle_exact_mean.argtypes = [P, U64]
+        L.atrex_oracle_exact_mean.restype = ctypes.c_double
         _lib = L
     return _lib
 
@@ -193,3 +207,48 @@ def status_of(key, app, phase, dur_ns, app_weight_q16, num_phases, score_key=Non
     except OracleError as e:
         return e.status
     return OK
+
+
+def exact_mean(x) -> float:
+    """The oracle's exact mean of finite non-negative doubles, rounded once."""
+    a = np.ascontiguousarray(x, dtype=np.float64)
+    return lib().atrex_oracle_exact_mean(_ptr(a), a.size)
+
+
+def target_share(key, is_dsl, dur_ns) -> dict:
+    """Target-DSL device-time share of one profile (§4.1, Metrics): per key
+    the DSL and total device time and their ratio, per operator the exact mean
+    over its running shapes, and the mean over the operators where defined.
+    Raises OracleError on a non-OK status."""
+    L = lib()
+    key = np.ascontiguousarray(key, dtype=np.uint32)
+    flag = np.ascontiguousarray(is_dsl, dtype=np.uint8)
+    dur_ns = np.ascontiguousarray(dur_ns, dtype=np.int64)
+    n = key.size
+    assert flag.size == n and dur_ns.size == n
+    h = ctypes.c_void_p()
+    st = L.atrex_oracle_share_compute(_ptr(key), _ptr(flag), _ptr(dur_ns), n, ctypes.byref(h))
+    if st != OK:
+        raise OracleError(st, "share_compute")
+    try:
+        nk, no = ctypes.c_uint64(), ctypes.c_uint64()
+        L.atrex_oracle_share_sizes(h, ctypes.byref(nk), ctypes.byref(no))
+        K, I = nk.value, no.value
+        out = {"key": np.zeros(K, np.uint32), "count": np.zeros(K, np.uint64),
+               "dsl_ns": np.zeros((K, 2), np.uint64), "total_ns": np.zeros((K, 2), np.uint64),
+               "share": np.zeros(K, np.float64), "op": np.zeros(I, np.uint32),
+               "op_shapes": np.zeros(I, np.uint32), "op_share": np.zeros(I, np.float64)}
+        st = L.atrex_oracle_share_keys(h, _ptr(out["key"]), _ptr(out["count"]), _ptr(out["dsl_ns"]),
+                                       _ptr(out["total_ns"]), _ptr(out["share"]))
+        if st != OK:
+            raise OracleError(st, "share_keys")
+        adop, nd = ctypes.c_double(), ctypes.c_uint64()
+        st = L.atrex_oracle_share_ops(h, _ptr(out["op"]), _ptr(out["op_shapes"]), _ptr(out["op_share"]),
+                                      ctypes.byref(adop), ctypes.byref(nd))
+        if st != OK:
+            raise OracleError(st, "share_ops")
+        out["adoption"] = adop.value
+        out["defined_ops"] = nd.value
+        return out
+    finally:
+        L.atrex_oracle_share_destroy(h)
