@@ -17,6 +17,11 @@ makes the run fail); and the CPU oracle timed on bounded samples of the same
 workload, on one core and sharded over the host's cores.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--path auto]
+
+--row share measures the target-DSL device-time share instead (§4.1, Metrics:
+the plain device-time group-by of one profile's kernel invocations and the
+per-shape, per-operator and overall shares), on the 64M-invocation profile by
+default (--config picks 0..2 of the profile workloads).
 """
 from __future__ import annotations
 
@@ -45,6 +50,7 @@ PASS_A_KERNELS = ("pass_a", "pass_a_range", "pass_a_global", "pass_a_reduce", "s
 ENGINE_BYTES = {"part_hist": 4, "part_scatter": 16, "part_aggregate": 16}
 KERNEL_SOURCES = ["paper_2607_14541_amd/csrc/kernels_aggregate.hip",
                   "paper_2607_14541_amd/csrc/kernels_rows.hip",
+                  "paper_2607_14541_amd/csrc/kernels_share.hip",
                   "paper_2607_14541_amd/csrc/atrex_kernels.h",
                   "paper_2607_14541_amd/csrc/atrex_device.hpp"]
 DEFAULT_STEPS = {0: 200, 1: 200, 2: 40, 3: 20, 4: 30}
@@ -104,20 +110,155 @@ def cpu_model() -> str:
     return "unknown"
 
 
+def kernel_averages(runs) -> dict:
+    """{name: {avg_ms, items}} from lists of (name, ms, items) per repetition."""
+    per = {}
+    for times in runs:
+        for name, ms, items in times:
+            per.setdefault(name, []).append((ms, items))
+    return {k: dict(avg_ms=sum(m for m, _ in v) / len(v), items=v[0][1]) for k, v in per.items()}
+
+
+# event bytes the target-share kernels read: phase + dur in the per-phase
+# totals, key + phase + dur in the per-(key, phase) group-by
+SHARE_METHOD_BYTES = {"time_totals": 9, "pass_b_lds": 13, "pass_b_global": 13, "part_scatter": 13}
+SHARE_DEFAULT_STEPS = {0: 200, 1: 100, 2: 100}
+
+
+def bench_share(args) -> int:
+    import numpy as np
+    import torch
+    from paper_2607_14541_amd import atrex as X
+    from paper_2607_14541_amd import synth
+
+    ci = 1 if args.config is None else args.config
+    cfg = synth.SHARE_CONFIGS[ci]
+    n = cfg["n"]
+    steps = args.steps if args.steps is not None else SHARE_DEFAULT_STEPS[ci]
+    units = synth.profile_units(cfg)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log("target share, profile", ci, cfg["name"])
+    p = synth.profile(cfg)
+    d_key = torch.from_numpy(p["key"].view(np.int32)).to(dev)
+    d_flag = torch.from_numpy(p["is_dsl"]).to(dev)
+    d_dur = torch.from_numpy(p["dur_ns"]).to(dev)
+    torch.cuda.synchronize()
+    K = units.size
+
+    def make(timing: bool):
+        return X.Aggregator(2, None, max_events=n, max_keys=K, max_groups=2 * K, path=args.path, timing=timing,
+                            device_time=True)
+
+    ag = make(False)
+    sbuf = ag.share_buffers(K, min(K, 65536))
+    res = {}
+
+    def step(a):  # one profile: device-time group-by, then the shares
+        a.reset()
+        a.aggregate(d_key, None, d_flag, d_dur)
+        res["r"] = a.target_share(out=sbuf)
+
+    for _ in range(args.warmup):
+        step(ag)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step(ag)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_step = 1e3 * elapsed / steps
+    value = n * steps / elapsed / 1e9
+    log("step %.3f ms, %.2f G invocations/s, path %s" % (ms_step, value, ag.path_used()))
+
+    parity = None
+    o = None
+    if not args.no_parity or not args.no_cpu_baseline:
+        from oracle import oracle as O  # checker and CPU baseline: the oracle as it stands
+        tc = time.perf_counter()
+        o = O.target_share(p["key"], p["is_dsl"], p["dur_ns"])
+        t_oracle = time.perf_counter() - tc
+    if not args.no_parity:
+        r = res["r"]
+
+        def f64_same(a, b):
+            a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+            return a.shape == b.shape and np.array_equal(np.isnan(a), np.isnan(b)) and np.array_equal(
+                a[~np.isnan(a)].view(np.uint64), b[~np.isnan(b)].view(np.uint64))
+        bad = [k for k, ok in (
+            ("key", np.array_equal(r["key"].cpu().numpy().view(np.uint32), o["key"])),
+            ("count", np.array_equal(r["count"].cpu().numpy().view(np.uint64), o["count"])),
+            ("dsl_ns", np.array_equal(r["dsl_ns"].cpu().numpy().view(np.uint64), o["dsl_ns"])),
+            ("total_ns", np.array_equal(r["total_ns"].cpu().numpy().view(np.uint64), o["total_ns"])),
+            ("share", f64_same(r["share"].cpu().numpy(), o["share"])),
+            ("op", np.array_equal(r["op"].cpu().numpy().view(np.uint32), o["op"])),
+            ("op_shapes", np.array_equal(r["op_shapes"].cpu().numpy().view(np.uint32), o["op_shapes"])),
+            ("op_share", f64_same(r["op_share"].cpu().numpy(), o["op_share"])),
+            ("adoption", f64_same([r["adoption"]], [o["adoption"]]))) if not ok]
+        parity = {"checked": True, "against": "CPU oracle on the same profile, every output", "ok": not bad,
+                  "mismatch": bad}
+        log("parity", "ok" if not bad else "MISMATCH %s" % bad)
+
+    agt = make(True)
+    runs = []
+    for _ in range(5):
+        agt.reset()
+        agt.aggregate(d_key, None, d_flag, d_dur)
+        t = agt.kernel_times()
+        agt.target_share(out=sbuf)
+        runs.append(t + agt.kernel_times())
+    agt.close()
+    kernels = kernel_averages(runs)
+    dom = max((k for k in kernels if k in SHARE_METHOD_BYTES), key=lambda k: kernels[k]["avg_ms"])
+    alg = SHARE_METHOD_BYTES[dom] * n
+    achieved = alg / (kernels[dom]["avg_ms"] * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "algorithmic_bytes_per_launch": alg, "avg_launch_ms": round(kernels[dom]["avg_ms"], 4)}
+    log("kernels", json.dumps({k: round(v["avg_ms"], 4) for k, v in kernels.items()}))
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = {"value": round(n / t_oracle / 1e9, 6), "unit": "G invocations/s", "cores": 1, "kind": "oracle",
+               "sample": "the whole %d-invocation profile, one thread (%.1f s)" % (n, t_oracle),
+               "nproc": os.cpu_count(), "cpu_model": cpu_model()}
+    r = res["r"]
+    line = {
+        "metric": "profile kernel invocations folded into the target-DSL device-time share per second",
+        "value": round(value, 3), "unit": "G invocations/s", "n_gpus": 1, "steps": steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u128+f64", "data": "synthetic",
+        "config": {"workload": cfg["name"], "invocations": n, "units": int(K), "operators": cfg["ops"],
+                   "seed": cfg["seed"], "path": ag.path_used(), "parallelism": "none",
+                   "entry": "atrex_aggregate_events + atrex_target_share"},
+        "adoption": r["adoption"], "defined_ops": r["defined_ops"],
+        "kernels_ms": {k: round(v["avg_ms"], 4) for k, v in kernels.items()},
+        "parity": parity, "roofline": roofline, "cpu_baseline": cpu,
+    }
+    ag.close()
+    print(json.dumps(line), flush=True)
+    return 1 if parity is not None and not parity["ok"] else 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=3, help="workload index (0..4); 3 = 1B events")
+    ap.add_argument("--config", type=int, default=None, help="workload index (0..4); default 3 = 1B events")
+    ap.add_argument("--row", default="weights", choices=["weights", "share"],
+                    help="weights: the importance-weight path (default); share: the target-DSL share")
     ap.add_argument("--path", default="auto", choices=["auto", "lds_hash", "global_hash", "radix_sort"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(--gpus %d requested)" % args.gpus, file=sys.stderr)
         return 2
+    if args.row == "share":
+        return bench_share(args)
+    if args.config is None:
+        args.config = 3
     steps = args.steps if args.steps is not None else DEFAULT_STEPS[args.config]
 
     import numpy as np
@@ -221,7 +362,7 @@ def main() -> int:
 
     # per-kernel device times (hipEvents recorded by the library on its stream)
     agt = make(True)
-    per = {}
+    runs = []
     for _ in range(3):
         times = []
         agt.reset()
@@ -232,9 +373,8 @@ def main() -> int:
         agt.score(d_sk, d_s, out=sbuf)
         times.extend(agt.kernel_times())
         del out_g
-        for name, ms, items in times:
-            per.setdefault(name, []).append((ms, items))
-    kernels = {k: dict(avg_ms=sum(m for m, _ in v) / len(v), items=v[0][1]) for k, v in per.items()}
+        runs.append(times)
+    kernels = kernel_averages(runs)
     agt.close()
     dom = max((k for k in kernels if k in METHOD_BYTES), key=lambda k: kernels[k]["avg_ms"])
     alg = METHOD_BYTES[dom] * n

@@ -72,6 +72,13 @@ typedef enum {
 #define ATREX_FLAG_RAW 2u    /* also accumulate the plain device time sum of dur per group */
 #define ATREX_FLAG_APP_COUNT 4u /* also count the invocations n[a,ph] of every (app, phase) in
                                    pass A (Eq. (2)); read with atrex_get_app_totals */
+#define ATREX_FLAG_DEVICE_TIME 8u /* plain device-time group-by: the events carry no application
+                                     (atrex_events.app must be NULL), num_apps must be 1 and
+                                     app_weight_q16 is ignored; every invocation's share is its
+                                     duration, so W[k,ph] = sum of dur (u128) and
+                                     atrex_get_app_totals gives T[ph] and n[ph] (counts always
+                                     on).  Not with ATREX_FLAG_RAW (W is already the raw time).
+                                     This is the input of atrex_target_share. */
 
 typedef struct {
   uint64_t lo, hi; /* value = lo + hi * 2^64 */
@@ -97,7 +104,7 @@ typedef struct {
 
 typedef struct { /* DEVICE struct-of-arrays, caller-owned, read only, borrowed for the call */
   const uint32_t *key;   /* [n] op << 16 | shape */
-  const uint32_t *app;   /* [n] application id < A */
+  const uint32_t *app;   /* [n] application id < A; NULL with ATREX_FLAG_DEVICE_TIME */
   const uint8_t *phase;  /* [n] serving phase < P */
   const int64_t *dur_ns; /* [n] invocation duration, >= 0 */
   uint64_t n;            /* n <= max_events, n < 2^31 */
@@ -195,6 +202,45 @@ atrex_status atrex_run(atrex_ctx *ctx, const atrex_events *ev, const atrex_group
  * Valid after atrex_aggregate_events (STATE before). */
 atrex_status atrex_get_app_totals(atrex_ctx *ctx, atrex_u128 *T, uint64_t *n, uint64_t *mant,
                                   int32_t *rho);
+
+/* ---- Target-DSL device-time share (§4.1, Metrics: "FlyDSL adoption") -------
+ * Input: a context initialised with ATREX_FLAG_DEVICE_TIME and num_phases = 2
+ * whose atrex_aggregate_events has run on one profile's kernel invocations,
+ * with phase = 1 for an invocation inside the target DSL and 0 otherwise.
+ * Per (operator, shape) key k:
+ *   dsl_ns[k] = sum of dur inside the DSL, total_ns[k] = sum of dur (u128),
+ *   share[k] = RN(dsl) / RN(total), NaN when total = 0 (the shape did not run);
+ * per operator i (every operator with an invocation, ascending):
+ *   op_shapes[i] = its running shapes (total > 0),
+ *   op_share[i] = the exact mean of share over them, rounded once to the
+ *   nearest double (NaN when none runs: the operator is then excluded);
+ * adoption = the exact mean of op_share over the operators where it is
+ *   defined, rounded once (NaN when none is); defined_ops = their number.
+ * The means do not depend on the order of the terms.  Keys ascending. */
+typedef struct {           /* DEVICE outputs, caller-allocated */
+  uint32_t *key;           /* [key_capacity] */
+  uint64_t *count;         /* [key_capacity] invocations */
+  atrex_u128 *dsl_ns;      /* [key_capacity] */
+  atrex_u128 *total_ns;    /* [key_capacity] */
+  double *share;           /* [key_capacity] */
+  uint32_t *op;            /* [op_capacity] */
+  uint32_t *op_shapes;     /* [op_capacity] */
+  double *op_share;        /* [op_capacity] */
+} atrex_share_out;
+
+typedef struct {   /* HOST result */
+  uint64_t num_keys, num_ops, defined_ops;
+  double adoption;
+} atrex_share_result;
+
+/* Valid once atrex_aggregate_events has run (STATE before), any number of
+ * times; leaves the context's state as it is.  INVALID_ARG unless the
+ * context has ATREX_FLAG_DEVICE_TIME and num_phases = 2.  CAPACITY when the
+ * keys exceed key_capacity or the operators op_capacity (r still receives the
+ * counts; the outputs then hold the first entries only).  HOST: out (struct of
+ * DEVICE pointers), r. */
+atrex_status atrex_target_share(atrex_ctx *ctx, const atrex_share_out *out, uint64_t key_capacity,
+                                uint64_t op_capacity, atrex_share_result *r);
 
 /* Per-kernel device times of the last aggregate_events / phase_normalize /
  * weighted_score call when ATREX_FLAG_TIMING was set (HOST arrays of cap

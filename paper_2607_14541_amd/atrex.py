@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libatrex.so")
 
 OK, E_INVALID_ARG, E_OUT_OF_RANGE, E_STATE, E_CAPACITY, E_DEVICE = 0, -1, -2, -3, -4, -5
 PATHS = {"auto": 0, "lds_hash": 1, "global_hash": 2, "radix_sort": 3}
-FLAG_TIMING, FLAG_RAW, FLAG_APP_COUNT = 1, 2, 4
+FLAG_TIMING, FLAG_RAW, FLAG_APP_COUNT, FLAG_DEVICE_TIME = 1, 2, 4, 8
 
 
 class AtrexError(RuntimeError):
@@ -56,6 +56,17 @@ class _NoAllocParams(ctypes.Structure):
                 ("app_weight_q16", ctypes.c_void_p), ("stream", ctypes.c_void_p)]
 
 
+class _ShareOut(ctypes.Structure):
+    _fields_ = [("key", ctypes.c_void_p), ("count", ctypes.c_void_p), ("dsl_ns", ctypes.c_void_p),
+                ("total_ns", ctypes.c_void_p), ("share", ctypes.c_void_p), ("op", ctypes.c_void_p),
+                ("op_shapes", ctypes.c_void_p), ("op_share", ctypes.c_void_p)]
+
+
+class _ShareResult(ctypes.Structure):
+    _fields_ = [("num_keys", ctypes.c_uint64), ("num_ops", ctypes.c_uint64), ("defined_ops", ctypes.c_uint64),
+                ("adoption", ctypes.c_double)]
+
+
 class _RunResult(ctypes.Structure):
     _fields_ = [("num_groups", ctypes.c_uint64), ("num_ops", ctypes.c_uint64), ("num_keys", ctypes.c_uint64),
                 ("num_scored_ops", ctypes.c_uint64), ("s_agg", ctypes.c_double), ("one_wait", ctypes.c_uint32)]
@@ -86,6 +97,7 @@ def _lib() -> ctypes.CDLL:
             "atrex_run_noalloc": [ctypes.POINTER(_NoAllocParams), ctypes.POINTER(_Events), ctypes.POINTER(_Groups),
                                   U64, P, P, U64, P, P, P, ctypes.POINTER(_RunResult)],
             "atrex_get_app_totals": [P, P, P, P, P],
+            "atrex_target_share": [P, ctypes.POINTER(_ShareOut), U64, U64, ctypes.POINTER(_ShareResult)],
             "atrex_kernel_times": [P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float),
                                    ctypes.POINTER(U64), I, ctypes.POINTER(I)],
             "atrex_aggregate_reset": [P],
@@ -137,26 +149,40 @@ def _as_i32(t: torch.Tensor) -> torch.Tensor:
 
 
 class Aggregator:
-    """One aggregation context: init -> aggregate -> normalize -> weights/score."""
+    """One aggregation context: init -> aggregate -> normalize -> weights/score.
 
-    def __init__(self, num_phases: int, app_weight_q16: torch.Tensor, max_events: int,
+    device_time=True: the plain device-time group-by (ATREX_FLAG_DEVICE_TIME):
+    no applications (app_weight_q16 is ignored and may be None; aggregate()
+    takes app=None), W = sum of dur per (key, phase); with num_phases = 2 it
+    feeds target_share()."""
+
+    def __init__(self, num_phases: int, app_weight_q16: torch.Tensor | None, max_events: int,
                  max_groups: int = 0, max_keys: int = 0, max_score: int = 0, path: str = "auto",
                  timing: bool = False, raw: bool = False, app_count: bool = False,
-                 stream: torch.cuda.Stream | None = None):
+                 stream: torch.cuda.Stream | None = None, device_time: bool = False,
+                 device: torch.device | None = None):
         L = _lib()
-        c = _dev(_as_i32(app_weight_q16), torch.int32, "app_weight_q16")
-        self.device = c.device
+        self.device_time = device_time
+        if device_time:
+            c = None
+            self.device = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
+            self.A = 1
+        else:
+            c = _dev(_as_i32(app_weight_q16), torch.int32, "app_weight_q16")
+            self.device = c.device
+            self.A = int(c.numel())
         self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
-        self.P, self.A = int(num_phases), int(c.numel())
+        self.P = int(num_phases)
         self.raw = raw
-        self.app_count = app_count
+        self.app_count = app_count or device_time  # the device-time mode always counts
         p = _InitParams()
         p.num_phases, p.num_apps = self.P, self.A
-        p.app_weight_q16 = c.data_ptr()
+        p.app_weight_q16 = c.data_ptr() if c is not None else None
         p.max_events, p.max_groups, p.max_keys, p.max_score = max_events, max_groups, max_keys, max_score
         p.path = PATHS[path]
         p.stream = self.stream.cuda_stream
-        p.flags = (FLAG_TIMING if timing else 0) | (FLAG_RAW if raw else 0) | (FLAG_APP_COUNT if app_count else 0)
+        p.flags = ((FLAG_TIMING if timing else 0) | (FLAG_RAW if raw else 0) | (FLAG_APP_COUNT if app_count else 0)
+                   | (FLAG_DEVICE_TIME if device_time else 0))
         nbytes = ctypes.c_size_t()
         _check(L.atrex_workspace_bytes(ctypes.byref(p), ctypes.byref(nbytes)), "atrex_workspace_bytes")
         self.workspace = torch.empty(max(int(nbytes.value), 256), dtype=torch.uint8, device=self.device)
@@ -175,14 +201,14 @@ class Aggregator:
         self._rviews = self._sviews = None
 
     # -- Eq. (2)-(3) group-by ---------------------------------------------------------
-    def aggregate(self, key: torch.Tensor, app: torch.Tensor, phase: torch.Tensor,
+    def aggregate(self, key: torch.Tensor, app: torch.Tensor | None, phase: torch.Tensor,
                   dur_ns: torch.Tensor) -> int:
         key = _dev(_as_i32(key), torch.int32, "key")
-        app = _dev(_as_i32(app), torch.int32, "app")
+        app = _dev(_as_i32(app), torch.int32, "app") if app is not None else None
         phase = _dev(phase, torch.uint8, "phase")
         dur_ns = _dev(dur_ns, torch.int64, "dur_ns")
         n = key.numel()
-        if not (app.numel() == n and phase.numel() == n and dur_ns.numel() == n):
+        if not ((app is None or app.numel() == n) and phase.numel() == n and dur_ns.numel() == n):
             raise ValueError("event arrays differ in length")
         self._events = (key, app, phase, dur_ns)  # keep alive for the call
         ev = _Events(_ptr(key), _ptr(app), _ptr(phase), _ptr(dur_ns), n)
@@ -337,6 +363,44 @@ class Aggregator:
             out["n"] = n
         return out
 
+    # -- target-DSL device-time share (§4.1, Metrics) ----------------------------------
+    def share_buffers(self, key_capacity: int, op_capacity: int) -> dict:
+        """Output tensors for target_share()."""
+        dev, kc, oc = self.device, max(int(key_capacity), 1), max(int(op_capacity), 1)
+        return dict(key=torch.empty(kc, dtype=torch.int32, device=dev),
+                    count=torch.empty(kc, dtype=torch.int64, device=dev),
+                    dsl_ns=torch.empty((kc, 2), dtype=torch.int64, device=dev),
+                    total_ns=torch.empty((kc, 2), dtype=torch.int64, device=dev),
+                    share=torch.empty(kc, dtype=torch.float64, device=dev),
+                    op=torch.empty(oc, dtype=torch.int32, device=dev),
+                    op_shapes=torch.empty(oc, dtype=torch.int32, device=dev),
+                    op_share=torch.empty(oc, dtype=torch.float64, device=dev))
+
+    def target_share(self, key_capacity: int | None = None, op_capacity: int | None = None,
+                     out: dict | None = None) -> dict:
+        """Per key the DSL (phase 1) and total device time and their ratio, per
+        operator the exact mean over its running shapes, and the mean over the
+        operators where it is defined (device_time=True, num_phases=2, after
+        aggregate()).  Capacities default to the group count, or to the sizes
+        of `out` (from share_buffers())."""
+        G = self.num_groups or 0
+        if out is not None:
+            kc = out["key"].numel() if key_capacity is None else int(key_capacity)
+            oc = out["op"].numel() if op_capacity is None else int(op_capacity)
+        else:
+            kc = G if key_capacity is None else int(key_capacity)
+            oc = min(G, 65536) if op_capacity is None else int(op_capacity)
+            out = self.share_buffers(kc, oc)
+        so = _ShareOut(*(_ptr(out[k]) for k in ("key", "count", "dsl_ns", "total_ns", "share", "op", "op_shapes",
+                                                 "op_share")))
+        r = _ShareResult()
+        _check(_lib().atrex_target_share(self._ctx, ctypes.byref(so), kc, oc, ctypes.byref(r)), "atrex_target_share")
+        K, I = r.num_keys, r.num_ops
+        res = {k: v[:K] for k, v in out.items() if not k.startswith("op")}
+        res.update({k: v[:I] for k, v in out.items() if k.startswith("op")})
+        res.update(adoption=r.adoption, defined_ops=r.defined_ops, num_keys=K, num_ops=I)
+        return res
+
     def kernel_times(self) -> list:
         cap = 64
         names = (ctypes.c_char_p * cap)()
@@ -381,6 +445,22 @@ def aggregate(key, app, phase, dur_ns, app_weight_q16, num_phases, path="auto", 
         out["path"] = ag.path_used()
         if score_key is not None:
             out.update({"score_" + k if k != "s_agg" else k: v for k, v in ag.score(score_key, s).items()})
+        return out
+    finally:
+        ag.close()
+
+
+def target_share(key, is_dsl, dur_ns, path="auto", max_keys=0) -> dict:
+    """The target-DSL device-time share of one profile (§4.1, Metrics) in one
+    call: the device-time group-by with phase = is_dsl (1 inside the target
+    DSL, 0 outside), then atrex_target_share."""
+    n = key.numel()
+    ag = Aggregator(2, None, max_events=max(n, 1), max_keys=max_keys, path=path, device_time=True,
+                    device=key.device)
+    try:
+        ag.aggregate(key, None, is_dsl, dur_ns)
+        out = ag.target_share()
+        out["path"] = ag.path_used()
         return out
     finally:
         ag.close()

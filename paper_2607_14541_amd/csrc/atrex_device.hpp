@@ -286,7 +286,9 @@ struct Ev4 {
   int64_t dur[4];
 };
 
-template <bool WITH_KEY>
+// NO_APP: the events carry no application (plain device-time group-by);
+// every event belongs to application 0 and the app array is not read.
+template <bool WITH_KEY, bool NO_APP = false>
 __device__ __forceinline__ void load4(const uint32_t* __restrict__ key, const uint32_t* __restrict__ app,
                                       const uint8_t* __restrict__ phase, const int64_t* __restrict__ dur,
                                       uint64_t i, Ev4& e) {
@@ -294,7 +296,7 @@ __device__ __forceinline__ void load4(const uint32_t* __restrict__ key, const ui
     const v4u k = __builtin_nontemporal_load((const v4u*)(key + i));
     e.key[0] = k.x; e.key[1] = k.y; e.key[2] = k.z; e.key[3] = k.w;
   }
-  const v4u a = __builtin_nontemporal_load((const v4u*)(app + i));
+  const v4u a = NO_APP ? v4u{0u, 0u, 0u, 0u} : __builtin_nontemporal_load((const v4u*)(app + i));
   const uint32_t p = __builtin_nontemporal_load((const uint32_t*)(phase + i));
   const v2l d0 = __builtin_nontemporal_load((const v2l*)(dur + i));
   const v2l d1 = __builtin_nontemporal_load((const v2l*)(dur + i + 2));
@@ -306,11 +308,12 @@ __device__ __forceinline__ void load4(const uint32_t* __restrict__ key, const ui
 // The same for a wave whose 64 groups of four all exist: event index e0 of
 // lane 0 is wave-uniform, so each load takes a scalar base address and a
 // 32-bit lane offset.
+template <bool NO_APP = false>
 __device__ __forceinline__ void load4_lane(const uint32_t* __restrict__ key, const uint32_t* __restrict__ app,
                                            const uint8_t* __restrict__ phase, const int64_t* __restrict__ dur,
                                            uint64_t e0, uint32_t lane, Ev4& e) {
   const v4u k = __builtin_nontemporal_load((const v4u*)(key + e0) + lane);
-  const v4u a = __builtin_nontemporal_load((const v4u*)(app + e0) + lane);
+  const v4u a = NO_APP ? v4u{0u, 0u, 0u, 0u} : __builtin_nontemporal_load((const v4u*)(app + e0) + lane);
   const uint32_t p = __builtin_nontemporal_load((const uint32_t*)(phase + e0) + lane);
   const v2l d0 = __builtin_nontemporal_load((const v2l*)(dur + e0) + 2 * lane);
   const v2l d1 = __builtin_nontemporal_load((const v2l*)(dur + e0) + 2 * lane + 1);
@@ -318,6 +321,12 @@ __device__ __forceinline__ void load4_lane(const uint32_t* __restrict__ key, con
   e.app[0] = a.x; e.app[1] = a.y; e.app[2] = a.z; e.app[3] = a.w;
   e.ph[0] = p & 0xFF; e.ph[1] = (p >> 8) & 0xFF; e.ph[2] = (p >> 16) & 0xFF; e.ph[3] = p >> 24;
   e.dur[0] = d0.x; e.dur[1] = d0.y; e.dur[2] = d1.x; e.dur[3] = d1.y;
+}
+
+// Application of event i (0 for events that carry none).
+template <bool NO_APP>
+__device__ __forceinline__ uint32_t app_at(const uint32_t* __restrict__ app, uint64_t i) {
+  return NO_APP ? 0u : app[i];
 }
 
 // Error bits of the device error word.

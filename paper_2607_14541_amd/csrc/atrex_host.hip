@@ -66,6 +66,7 @@ struct Params {
   bool raw;
   bool count;    // invocation counts per (app, phase) in pass A
   bool compact;  // global-hash engine only: no per-event scratch, rows sized to the groups
+  bool time;     // plain device-time group-by: no applications, identity scale (counts always on)
 };
 
 constexpr uint32_t kPassARangesMax = 16;
@@ -120,7 +121,7 @@ Layout make_layout(const Params& p) {
   L.carryA = take(GA * 8);
   L.partA = take(L.partA_rows * GA * (L.passA == 0 ? 8 : 4));
   L.partC = take(p.count ? L.partA_rows * GA * 4 : 0);
-  L.nA = take(p.count ? GA * 8 : 0);
+  L.nA = take(p.count || p.time ? GA * 8 : 0);
   L.scale = take(GA * 8);
   L.bscale = take(GA * 8);
   L.dict = take(L.capD * 8);
@@ -221,6 +222,8 @@ atrex_status check_params(const atrex_init_params* ip, Params* out) {
   p.raw = (ip->flags & ATREX_FLAG_RAW) != 0;
   p.count = (ip->flags & ATREX_FLAG_APP_COUNT) != 0;
   p.compact = false;
+  p.time = (ip->flags & ATREX_FLAG_DEVICE_TIME) != 0;
+  if (p.time && (p.A != 1 || p.raw)) return ATREX_E_INVALID_ARG;
   *out = p;
   return ATREX_OK;
 }
@@ -567,7 +570,8 @@ atrex_status atrex_aggregate_init(const atrex_init_params* ip, atrex_ctx** out) 
   Params p;
   atrex_status st = check_params(ip, &p);
   if (st != ATREX_OK) return st;
-  if (!ip->app_weight_q16 || !ip->workspace || !aligned(ip->workspace, kAlign)) return ATREX_E_INVALID_ARG;
+  if ((!ip->app_weight_q16 && !p.time) || !ip->workspace || !aligned(ip->workspace, kAlign))
+    return ATREX_E_INVALID_ARG;
   const Layout L = make_layout(p);
   if (ip->workspace_bytes < L.bytes) return ATREX_E_CAPACITY;
   if (ensure_smem_limits() != hipSuccess) return ATREX_E_DEVICE;
@@ -579,7 +583,7 @@ atrex_status atrex_aggregate_init(const atrex_init_params* ip, atrex_ctx** out) 
   c->s = (hipStream_t)ip->stream;
   c->path = ip->path;
   c->flags = ip->flags;
-  c->app_weight = ip->app_weight_q16;
+  c->app_weight = p.time ? nullptr : ip->app_weight_q16;
   c->state = 0;
   c->S_ready = false;
   c->G = c->nops = c->nkeys = 0;
@@ -611,6 +615,15 @@ atrex_status atrex_aggregate_init(const atrex_init_params* ip, atrex_ctx** out) 
   }
   // the pass-A carry table starts clear (each pass-A reduce clears it again)
   launch_fill_u64(c->s, c->at<uint64_t>(c->L.carryA), (uint64_t)p.A * p.P, 0);
+  if (p.time) {  // no applications, no card-hour weights
+    st = sync_status(c);
+    if (st != ATREX_OK) {
+      atrex_aggregate_destroy(c);
+      return st;
+    }
+    *out = c;
+    return ATREX_OK;
+  }
   // C = sum_a c_a, checked > 0 (p_a = c_a / C must exist)
   launch_sum_u32(c->s, c->app_weight, p.A, c->Csum());
   uint64_t C = 0;
@@ -644,7 +657,8 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
   if (c->state != 0) return ATREX_E_STATE;
   const uint64_t n = ev->n;
   if (n > c->p.max_events) return ATREX_E_CAPACITY;
-  if (n > 0 && (!ev->key || !ev->app || !ev->phase || !ev->dur_ns)) return ATREX_E_INVALID_ARG;
+  if (c->p.time ? ev->app != nullptr : (n > 0 && !ev->app)) return ATREX_E_INVALID_ARG;
+  if (n > 0 && (!ev->key || !ev->phase || !ev->dur_ns)) return ATREX_E_INVALID_ARG;
   const uint32_t P = c->p.P, A = c->p.A;
   const uint64_t GA = (uint64_t)A * P;
   const Layout& L = c->L;
@@ -667,8 +681,19 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
   uint64_t* scale = c->at<uint64_t>(L.scale);
   // invocation counts per (app, phase): per-block partials, then their sums
   uint32_t* pcount = c->p.count ? c->at<uint32_t>(L.partC) : nullptr;
-  uint64_t* nA = c->p.count ? c->at<uint64_t>(L.nA) : nullptr;
-  if (L.passA == 0 && vec_ok) {
+  uint64_t* nA = c->p.count || c->p.time ? c->at<uint64_t>(L.nA) : nullptr;
+  if (c->p.time) {
+    // no applications: per-phase device time and counts with the range
+    // checks, and the identity scale (m = 2^55, rho = 0: each share is the
+    // duration itself) in both word forms
+    launch_fill_u64(s, T, 2 * (uint64_t)P, 0);
+    launch_fill_u64(s, nA, P, 0);
+    TIMED(c, "time_totals", n,
+          launch_time_totals(s, d, P, (uint32_t)c->cus, vec_ok, (unsigned long long*)T, (unsigned long long*)nA,
+                             c->err()));
+    launch_fill_u64(s, scale, P, (uint64_t)64 << 56);
+    launch_fill_u64(s, c->at<uint64_t>(L.bscale), P, ((uint64_t)63 << 56) | ((uint64_t)1 << 55));
+  } else if (L.passA == 0 && vec_ok) {
     // one workgroup per CU (two groups of loads in flight per lane): two per
     // CU ran as one after the other (the SIMDs favour the older one) and
     // doubled the partial rows for the reduce
@@ -1229,13 +1254,50 @@ atrex_status atrex_run(atrex_ctx* c, const atrex_events* ev, const atrex_groups*
 
 atrex_status atrex_get_app_totals(atrex_ctx* c, atrex_u128* T, uint64_t* n, uint64_t* mant, int32_t* rho) {
   if (!c || !T) return ATREX_E_INVALID_ARG;
-  if (n && !c->p.count) return ATREX_E_INVALID_ARG;
+  if (n && !c->p.count && !c->p.time) return ATREX_E_INVALID_ARG;
   if (c->state < 1) return ATREX_E_STATE;
   const uint64_t GA = (uint64_t)c->p.A * c->p.P;
   (void)hipMemcpyAsync(T, c->at<void>(c->L.T), GA * 16, hipMemcpyDeviceToDevice, c->s);
   if (n) (void)hipMemcpyAsync(n, c->at<void>(c->L.nA), GA * 8, hipMemcpyDeviceToDevice, c->s);
   if (mant || rho) launch_unpack_scale(c->s, c->at<uint64_t>(c->L.scale), GA, mant, rho);
   return sync_read(c);
+}
+
+atrex_status atrex_target_share(atrex_ctx* c, const atrex_share_out* out, uint64_t key_capacity,
+                                uint64_t op_capacity, atrex_share_result* r) {
+  if (!c || !out || !r) return ATREX_E_INVALID_ARG;
+  if (!c->p.time || c->p.P != 2) return ATREX_E_INVALID_ARG;
+  if (c->state < 1) return ATREX_E_STATE;
+  if (key_capacity && (!out->key || !out->count || !out->dsl_ns || !out->total_ns || !out->share))
+    return ATREX_E_INVALID_ARG;
+  if (op_capacity && (!out->op || !out->op_shapes || !out->op_share)) return ATREX_E_INVALID_ARG;
+  const Layout& L = c->L;
+  ShareOut so;
+  so.key = out->key;
+  so.count = out->count;
+  so.dsl = (uint64_t*)out->dsl_ns;
+  so.total = (uint64_t*)out->total_ns;
+  so.share = out->share;
+  so.op = out->op;
+  so.op_shapes = out->op_shapes;
+  so.op_share = out->op_share;
+  unsigned long long* words = c->at<unsigned long long>(L.ctrl + 2048);
+  c->begin_call();
+  TIMED(c, "target_share", c->G,
+        launch_target_share(c->s, c->groups(), c->G, c->at<uint32_t>(L.flags), c->at<uint32_t>(L.scan),
+                            c->at<uint32_t>(L.sv[0]), c->at<uint32_t>(L.sv[1]), c->at<void>(L.scan_tmp), so,
+                            key_capacity, op_capacity, c->at<double>(L.sk[0]), c->at<uint32_t>(L.starts), words));
+  uint64_t w[4] = {0, 0, 0, 0};
+  d2h(c, w, words, sizeof(w));
+  const atrex_status st = sync_read(c);
+  c->end_call();
+  if (st != ATREX_OK) return st;
+  r->num_keys = w[0];
+  r->num_ops = w[1];
+  r->defined_ops = w[2];
+  memcpy(&r->adoption, &w[3], sizeof(double));
+  if (w[0] > key_capacity || w[1] > op_capacity) return ATREX_E_CAPACITY;
+  return ATREX_OK;
 }
 
 atrex_status atrex_kernel_times(atrex_ctx* c, const char** names, float* ms, uint64_t* items, int cap, int* count) {

@@ -91,6 +91,31 @@ struct SortedGroups {
   uint64_t* raw;   // [G][2] or null
 };
 
+// Outputs of the target-DSL share (DEVICE arrays of the caller).
+struct ShareOut {
+  uint32_t* key;       // [K]
+  uint64_t* count;     // [K]
+  uint64_t* dsl;       // [K][2]
+  uint64_t* total;     // [K][2]
+  double* share;       // [K]
+  uint32_t* op;        // [I]
+  uint32_t* op_shapes; // [I]
+  double* op_share;    // [I]
+};
+
+// kernels_share.hip
+hipError_t set_share_smem_limits();
+// per-phase device time and counts of events without applications (global
+// accumulators cleared by the caller), with the range checks
+void launch_time_totals(hipStream_t s, const EventsDev& ev, uint32_t P, uint32_t nblocks, bool vec,
+                        unsigned long long* T, unsigned long long* cnt, uint32_t* err);
+// The target-DSL share from groups of phase 0 (outside) and 1 (inside the
+// DSL); words[8]: key count, operator count, defined operators, the overall
+// mean (as double bits), and its exact-sum chunks.
+void launch_target_share(hipStream_t s, const SortedGroups& g, uint64_t G, uint32_t* hk, uint32_t* kidx,
+                         uint32_t* ho, uint32_t* oidx, void* scan_tmp, const ShareOut& out, uint64_t kcap,
+                         uint64_t ocap, double* share_all, uint32_t* op_first, unsigned long long* words);
+
 // kernels_aggregate.hip
 hipError_t set_kernel_smem_limits();
 // pcount / cnt (nullable): per-block invocation counts of each (app, phase)

@@ -471,15 +471,16 @@ __device__ __forceinline__ void global_accumulate(const GroupTables& gt, uint32_
   if (RAW) acc_add_plain(&gt.raw[2 * gi], &gt.raw[2 * gi + 1], (u128)d);
 }
 
-// Pass B through the global dictionary and global atomics only.
-template <int BLOCK, bool RAW>
+// Pass B through the global dictionary and global atomics only.  NO_APP:
+// the events carry no application (every event is application 0).
+template <int BLOCK, bool RAW, bool NO_APP = false>
 __global__ __launch_bounds__(BLOCK) void k_pass_b_global(EventsDev ev, uint32_t A, uint32_t P,
                                                          const uint64_t* __restrict__ scale, GroupTables gt,
                                                          uint32_t* __restrict__ err) {
   const uint64_t n = ev.n;
   bool bad = false;
   for (uint64_t i = (uint64_t)blockIdx.x * BLOCK + threadIdx.x; i < n; i += (uint64_t)gridDim.x * BLOCK) {
-    const uint32_t k = ev.key[i], a = ev.app[i], ph = ev.phase[i];
+    const uint32_t k = ev.key[i], a = app_at<NO_APP>(ev.app, i), ph = ev.phase[i];
     const int64_t d = ev.dur[i];
     const bool ok = a < A && ph < P && d >= 0;
     bad |= !ok;
@@ -577,7 +578,7 @@ struct StagedEv4 {
   uint64_t sw[4];      // pass-B scale words
 };
 
-template <int BLOCK, bool RAW>
+template <int BLOCK, bool RAW, bool NO_APP = false>
 __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, const uint64_t* __restrict__ scale,
                                                       const uint64_t* __restrict__ bscale, uint32_t S,
                                                       OwnerRegions orr, SpillList sp, Rows rows,
@@ -729,7 +730,7 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
       for (int j = 0; j < 4; ++j) {
         const bool valid = (uint32_t)j < nvalid;
         const uint64_t i = valid ? first + j : 0;
-        const u128 v = event_share((uint64_t)g.dur[j], valid ? scale[ev.app[i] * P + ph[j]] : 0);
+        const u128 v = event_share((uint64_t)g.dur[j], valid ? scale[app_at<NO_APP>(ev.app, i) * P + ph[j]] : 0);
         vlo[j] = (uint64_t)v;
         vhi[j] = (uint64_t)(v >> 64);
       }
@@ -837,10 +838,10 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
     auto load_blk = [&](uint32_t bk, Ev4& e) {
       const uint64_t g0 = 64 * (uint64_t)bk;
       if (bk < FULLBLK) {
-        load4_lane(ev.key, ev.app, ev.phase, ev.dur, g0 * 4, lane, e);
+        load4_lane<NO_APP>(ev.key, ev.app, ev.phase, ev.dur, g0 * 4, lane, e);
       } else {
         const uint64_t q = g0 + lane;
-        load4<true>(ev.key, ev.app, ev.phase, ev.dur, min(q, n4 - 1) * 4, e);
+        load4<true, NO_APP>(ev.key, ev.app, ev.phase, ev.dur, min(q, n4 - 1) * 4, e);
         if (q >= n4) {
 #pragma unroll
           for (int j = 0; j < 4; ++j) e.key[j] = ATREX_EMPTY_KEY;
@@ -882,7 +883,9 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
     Ev4 e;
 #pragma unroll
     for (int j = 0; j < 4; ++j) { e.key[j] = ATREX_EMPTY_KEY; e.app[j] = 0; e.ph[j] = 0; e.dur[j] = 0; }
-    if (i < n) { e.key[0] = ev.key[i]; e.app[0] = ev.app[i]; e.ph[0] = ev.phase[i]; e.dur[0] = ev.dur[i]; }
+    if (i < n) {
+      e.key[0] = ev.key[i]; e.app[0] = app_at<NO_APP>(ev.app, i); e.ph[0] = ev.phase[i]; e.dur[0] = ev.dur[i];
+    }
     StagedEv4 g;
     stage(e, g);
     process(g, TAIL);
@@ -1029,7 +1032,9 @@ void launch_scale(hipStream_t s, const uint64_t* T, const uint32_t* c, const uin
 
 void launch_pass_b_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, const uint64_t* scale,
                           const GroupTables& gt, bool raw, uint32_t nblocks, uint32_t* err) {
-  if (raw)
+  if (!ev.app)  // events without applications (the host takes no raw time then)
+    hipLaunchKernelGGL((k_pass_b_global<256, false, true>), dim3(nblocks), dim3(256), 0, s, ev, A, P, scale, gt, err);
+  else if (raw)
     hipLaunchKernelGGL((k_pass_b_global<256, true>), dim3(nblocks), dim3(256), 0, s, ev, A, P, scale, gt, err);
   else
     hipLaunchKernelGGL((k_pass_b_global<256, false>), dim3(nblocks), dim3(256), 0, s, ev, A, P, scale, gt, err);
@@ -1061,7 +1066,10 @@ void launch_pass_b_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t 
   SpillList sp{spill_key, spill_val, spill_raw, spill_count, scap};
   const uint64_t* bscale = (const uint64_t*)bscale_v;
   (void)A;
-  if (raw)
+  if (!ev.app)  // events without applications (the host takes no raw time then)
+    hipLaunchKernelGGL((k_pass_b_lds<1024, false, true>), dim3(nblocks), dim3(1024), smem, s, ev, P, scale, bscale, S,
+                       orr, sp, rows, err);
+  else if (raw)
     hipLaunchKernelGGL((k_pass_b_lds<1024, true>), dim3(nblocks), dim3(1024), smem, s, ev, P, scale, bscale, S, orr,
                        sp, rows, err);
   else
@@ -1091,7 +1099,12 @@ hipError_t set_kernel_smem_limits() {
   e = hipFuncSetAttribute((const void*)k_pass_b_lds<1024, false>, hipFuncAttributeMaxDynamicSharedMemorySize,
                           160 * 1024);
   if (e != hipSuccess) return e;
+  e = hipFuncSetAttribute((const void*)k_pass_b_lds<1024, false, true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                          160 * 1024);
+  if (e != hipSuccess) return e;
   e = set_score_smem_limits();
+  if (e != hipSuccess) return e;
+  e = set_share_smem_limits();
   if (e != hipSuccess) return e;
   e = set_units_smem_limits();
   if (e != hipSuccess) return e;

@@ -553,22 +553,24 @@ __global__ __launch_bounds__(1024) void k_part_hist(PartSource src, uint32_t BB,
 // as runs, consecutive lanes writing consecutive records of a bucket, while
 // the next tile's events are loaded.
 
+template <bool NO_APP>
 __device__ __forceinline__ void load_group(const EventsDev& ev, uint64_t q, uint64_t e, Ev4& x) {
   if (q + 3 < e) {  // q is a multiple of 4: a whole, 16-byte aligned group
-    load4<true>(ev.key, ev.app, ev.phase, ev.dur, q, x);
+    load4<true, NO_APP>(ev.key, ev.app, ev.phase, ev.dur, q, x);
   } else {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const bool in = q + j < e;
       x.key[j] = in ? ev.key[q + j] : 0;
-      x.app[j] = in ? ev.app[q + j] : 0;
+      x.app[j] = in ? app_at<NO_APP>(ev.app, q + j) : 0;
       x.ph[j] = in ? ev.phase[q + j] : 0;
       x.dur[j] = in ? ev.dur[q + j] : 0;
     }
   }
 }
 
-template <bool RAW, bool SPILL, uint32_t SC_EPT, uint32_t SC_BLOCK>
+// NO_APP: the events carry no application (every event is application 0).
+template <bool RAW, bool SPILL, uint32_t SC_EPT, uint32_t SC_BLOCK, bool NO_APP = false>
 __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint32_t A, uint32_t P,
                                                            const uint64_t* __restrict__ scale,
                                                            const uint64_t* __restrict__ bscale, uint32_t BB,
@@ -602,7 +604,7 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint3
   Ev4 nxt[G4];
   if (!SPILL) {
 #pragma unroll
-    for (uint32_t g = 0; g < G4; ++g) load_group(src.ev, b + 4 * ((uint64_t)g * SC_BLOCK + tid), e, nxt[g]);
+    for (uint32_t g = 0; g < G4; ++g) load_group<NO_APP>(src.ev, b + 4 * ((uint64_t)g * SC_BLOCK + tid), e, nxt[g]);
   }
   // Four barriers per tile: the counters are double-buffered (the next
   // tile's are cleared during this tile's scan) and each bucket's position
@@ -707,7 +709,7 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint3
           }
         } else {  // rho outside [-8, 63] (rare): the general scale word, found again from the event
           const uint64_t i = t0 + 4 * ((uint64_t)(j / 4) * SC_BLOCK + tid) + (j % 4);
-          const u128 x = event_share(d, scale[src.ev.app[i] * P + ph]);
+          const u128 x = event_share(d, scale[app_at<NO_APP>(src.ev.app, i) * P + ph]);
           vl = (uint64_t)x;
           vh = (uint64_t)(x >> 64);
         }
@@ -721,7 +723,7 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint3
     if (!SPILL && t0 + SC_TILE < e) {
 #pragma unroll
       for (uint32_t g = 0; g < G4; ++g)
-        load_group(src.ev, t0 + SC_TILE + 4 * ((uint64_t)g * SC_BLOCK + tid), e, nxt[g]);
+        load_group<NO_APP>(src.ev, t0 + SC_TILE + 4 * ((uint64_t)g * SC_BLOCK + tid), e, nxt[g]);
     }
     __syncthreads();
     const uint32_t nt = (uint32_t)min((uint64_t)SC_TILE, e - t0);
@@ -1057,7 +1059,10 @@ void launch_part_scatter(hipStream_t s, const PartSource& src, uint32_t nwg, uin
 #define ATREX_SCATTER(R, S)                                                                                     \
   hipLaunchKernelGGL((k_part_scatter<R, S, kScatterEpt, kScatterBlock>), dim3(nwg), dim3(kScatterBlock), smem, s, \
                      src, A, P, scale, bscale, BB, O, rec, rraw, err)
-  if (rraw) {
+  if (!src.spill && !src.ev.app) {  // events without applications (the host takes no raw time then)
+    hipLaunchKernelGGL((k_part_scatter<false, false, kScatterEpt, kScatterBlock, true>), dim3(nwg),
+                       dim3(kScatterBlock), smem, s, src, A, P, scale, bscale, BB, O, rec, rraw, err);
+  } else if (rraw) {
     if (src.spill) ATREX_SCATTER(true, true); else ATREX_SCATTER(true, false);
   } else {
     if (src.spill) ATREX_SCATTER(false, true); else ATREX_SCATTER(false, false);
@@ -1142,7 +1147,8 @@ hipError_t set_rows_smem_limits() {
                        (const void*)k_part_scatter<true, false, kScatterEpt, kScatterBlock>,
                        (const void*)k_part_scatter<true, true, kScatterEpt, kScatterBlock>,
                        (const void*)k_part_scatter<false, false, kScatterEpt, kScatterBlock>,
-                       (const void*)k_part_scatter<false, true, kScatterEpt, kScatterBlock>};
+                       (const void*)k_part_scatter<false, true, kScatterEpt, kScatterBlock>,
+                       (const void*)k_part_scatter<false, false, kScatterEpt, kScatterBlock, true>};
   for (const void* f : fns) {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 2048);
     if (e != hipSuccess) return e;

@@ -222,3 +222,57 @@ def scores(cfg: dict, keys: np.ndarray, nan_frac: float = 0.0) -> np.ndarray:
         v = (u64_stream(cfg["seed"], 301, n) >> np.uint64(11)).astype(np.float64) * 2.0 ** -53
         s[v < nan_frac] = np.nan
     return s
+
+
+# ---------------------------------------------------------------------------
+# Profiles for the target-DSL device-time share (§4.1, Metrics): the kernel
+# invocations of one candidate's forward passes, labelled by (operator,
+# shape) unit and by whether the kernel ran inside the target DSL.  The units
+# follow the benchmark's release size (30 operators, 440 shapes) or a wide
+# table; each unit has its own chance of running inside the DSL (a quarter
+# never do -- delegated to library or framework kernels -- a quarter always
+# do, the rest mixed), a few units record only zero-length invocations (they
+# do not run), and the last operator has no running shape at all.
+SHARE_CONFIGS = {
+    0: dict(name="1M invocations, 440 units of 30 operators", slug="share_1M_440", n=1 << 20, seed=10,
+            ops=30, shapes=440, mu=math.log(2e4), sigma=1.5),
+    1: dict(name="64M invocations, 440 units of 30 operators", slug="share_64M_440", n=1 << 26, seed=11,
+            ops=30, shapes=440, mu=math.log(2e4), sigma=1.5),
+    2: dict(name="16M invocations, 64k units of 256 operators", slug="share_16M_64k", n=1 << 24, seed=12,
+            ops=256, shapes=65536, mu=math.log(2e4), sigma=2.0),
+}
+
+
+def _unif(seed: int, stream: int, n: int) -> np.ndarray:
+    return (u64_stream(seed, stream, n) >> np.uint64(11)).astype(np.float64) * 2.0 ** -53
+
+
+def profile_units(cfg: dict) -> np.ndarray:
+    """The workload's (operator, shape) keys, ascending: the shapes split as
+    evenly as possible over the operators."""
+    I, K = cfg["ops"], cfg["shapes"]
+    per = np.full(I, K // I, np.int64)
+    per[: K % I] += 1
+    op = np.repeat(np.arange(I, dtype=np.uint32), per)
+    sh = np.concatenate([np.arange(p, dtype=np.uint32) for p in per])
+    return ((op << np.uint32(16)) | sh).astype(np.uint32)
+
+
+def profile(cfg: dict, n: int | None = None) -> dict:
+    """Invocations [0, n) of a profile: key, is_dsl (uint8 0/1), dur_ns."""
+    n = cfg["n"] if n is None else n
+    seed = cfg["seed"]
+    units = profile_units(cfg)
+    K = units.size
+    r = _unif(seed, 400, K)
+    p_dsl = np.where(r < 0.25, 0.0, np.where(r < 0.5, 1.0, _unif(seed, 401, K)))
+    idle = _unif(seed, 402, K) < 0.03                 # units with zero-length invocations only
+    idle |= (units >> np.uint32(16)) == cfg["ops"] - 1  # the last operator never runs
+    u = u64_stream(seed, 403, n)
+    idx = (u % np.uint64(K)).astype(np.int64)
+    key = units[idx]
+    is_dsl = (_unif(seed, 404, n) < p_dsl[idx]).astype(np.uint8)
+    dur = np.rint(np.exp(cfg["mu"] + cfg["sigma"] * normals(seed, 405, n)))
+    dur = np.clip(dur, 0, 2.0 ** 62).astype(np.int64)
+    dur[idle[idx]] = 0
+    return dict(key=key, is_dsl=is_dsl, dur_ns=dur)

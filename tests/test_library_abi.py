@@ -59,3 +59,17 @@ def test_init_rejects_bad_arguments_before_touching_the_device(lib):
     assert lib.atrex_aggregate_init(ctypes.byref(p), ctypes.byref(ctx)) == X.E_INVALID_ARG  # no weights
     assert ctx.value is None
     assert lib.atrex_aggregate_events(None, None, None) == X.E_INVALID_ARG
+
+
+def test_device_time_flag_validation(lib):
+    """The plain device-time mode takes one application and no raw-time flag."""
+    from paper_2607_14541_amd import atrex as X
+    p = X._InitParams()
+    b = ctypes.c_size_t()
+    p.max_events = 1000
+    for A, flags, ok in ((1, X.FLAG_DEVICE_TIME, True), (2, X.FLAG_DEVICE_TIME, False),
+                         (1, X.FLAG_DEVICE_TIME | X.FLAG_RAW, False),
+                         (1, X.FLAG_DEVICE_TIME | X.FLAG_APP_COUNT | X.FLAG_TIMING, True)):
+        p.num_phases, p.num_apps, p.flags = 2, A, flags
+        assert (lib.atrex_workspace_bytes(ctypes.byref(p), ctypes.byref(b)) == 0) == ok, (A, flags)
+    assert lib.atrex_target_share(None, None, 0, 0, None) == X.E_INVALID_ARG
