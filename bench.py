@@ -21,7 +21,9 @@ workload, on one core and sharded over the host's cores.
 --row share measures the target-DSL device-time share instead (§4.1, Metrics:
 the plain device-time group-by of one profile's kernel invocations and the
 per-shape, per-operator and overall shares), on the 64M-invocation profile by
-default (--config picks 0..2 of the profile workloads).
+default (--config picks 0..2 of the profile workloads).  --row refresh
+measures an incremental refresh of the weights over an append-only log (the
+workload's events, the last eighth new), beside a from-scratch run.
 """
 from __future__ import annotations
 
@@ -239,14 +241,152 @@ def bench_share(args) -> int:
     return 1 if parity is not None and not parity["ok"] else 0
 
 
+def bench_refresh(args) -> int:
+    """Incremental refresh: the workload's events are an append-only log whose
+    last eighth is new; a step restores the folded totals of the first seven
+    eighths (a checkpoint), folds the new events (pass A over them only),
+    re-runs pass B over the whole log, orders, normalises and scores.  The
+    same log re-weighted from scratch (atrex_run) is timed beside it."""
+    import numpy as np
+    import torch
+    from paper_2607_14541_amd import atrex as X
+    from paper_2607_14541_amd import synth
+
+    ci = 3 if args.config is None else args.config
+    cfg = synth.CONFIGS[ci]
+    n, P = cfg["n"], cfg["num_phases"]
+    n_new = n // 8
+    n_old = n - n_new
+    steps = args.steps if args.steps is not None else max(5, DEFAULT_STEPS[ci] // 2)
+    keys = synth.key_space(cfg)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log("refresh, config", ci, cfg["name"], "log", n, "new", n_new)
+    ev = synth.events(cfg)
+    c = synth.app_weights(cfg)
+    s = synth.scores(cfg, keys)
+    d = {k: torch.from_numpy(ev[k].view(dt)).to(dev) for k, dt in (("key", np.int32), ("app", np.int32),
+                                                                     ("phase", np.uint8), ("dur_ns", np.int64))}
+    d_c = torch.from_numpy(c.view(np.int32)).to(dev)
+    d_sk = torch.from_numpy(keys.view(np.int32)).to(dev)
+    d_s = torch.from_numpy(s).to(dev)
+    torch.cuda.synchronize()
+    if args.no_cpu_baseline:
+        del ev
+    G = keys.size * P
+    kw = dict(max_events=n, max_groups=G, max_keys=keys.size, max_score=keys.size, path=args.path)
+    ag = X.Aggregator(P, d_c, incremental=True, **kw)
+    old = {k: v[:n_old] for k, v in d.items()}
+    ag.refresh(old["key"], old["app"], old["phase"], old["dur_ns"], n_old)
+    state = ag.refresh_state()
+    gbuf = ag.group_buffers(G)
+    sbuf = dict(op=torch.empty(keys.size, dtype=torch.int32, device=dev),
+                op_weight=torch.empty(keys.size, dtype=torch.float64, device=dev),
+                op_score=torch.empty(keys.size, dtype=torch.float64, device=dev))
+    res = {}
+
+    def step(a):
+        a.reset()
+        a.refresh_restore(state)
+        a.refresh(d["key"], d["app"], d["phase"], d["dur_ns"], n_new)
+        res["groups"] = a.normalize(out=gbuf)
+        res["score"] = a.score(d_sk, d_s, out=sbuf)
+
+    def timed(fn, k):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(k):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / k
+
+    t_refresh = timed(lambda: step(ag), steps)
+    full = X.Aggregator(P, d_c, **kw)
+    fb = full.group_buffers(G)
+    t_full = timed(lambda: full.run(d["key"], d["app"], d["phase"], d["dur_ns"], fb, d_sk, d_s, sbuf), steps)
+    full.close()
+    log("refresh %.3f ms, whole log from scratch %.3f ms" % (1e3 * t_refresh, 1e3 * t_full))
+
+    parity = None
+    if not args.no_parity:
+        sys.path.insert(0, os.path.join(ROOT, "tests", "golden"))
+        import digests as D
+        rec = D.load()["configs"].get(str(ci)) if os.path.exists(D.DIGEST_FILE) else None
+        if rec is None:
+            parity = {"checked": False, "reason": "no oracle digest for this workload"}
+        else:
+            out = {k: v.cpu().numpy() for k, v in res["groups"].items()}
+            out.update(score_op=res["score"]["op"].cpu().numpy(),
+                       score_op_weight=res["score"]["op_weight"].cpu().numpy(),
+                       score_op_S=res["score"]["op_score"].cpu().numpy())
+            ow, kwt, at = ag.op_weights(), ag.key_weights(), ag.app_totals()
+            out.update(op=ow["op"].cpu().numpy(), op_U=ow["U"].cpu().numpy(), op_w=ow["w"].cpu().numpy(),
+                       ukey=kwt["key"].cpu().numpy(), key_U=kwt["U"].cpu().numpy(), omega=kwt["omega"].cpu().numpy(),
+                       app_total=at["T"].cpu().numpy(), mant=at["mant"].cpu().numpy(), rho=at["rho"].cpu().numpy())
+            bad = D.mismatches(rec, out, s_agg=res["score"]["s_agg"])
+            parity = {"checked": True, "against": "CPU oracle over the whole log (digests of its outputs)",
+                      "ok": not bad, "mismatch": bad}
+            log("parity", "ok" if not bad else "MISMATCH %s" % bad)
+
+    agt = X.Aggregator(P, d_c, incremental=True, timing=True, **kw)
+    runs = []
+    for _ in range(3):
+        agt.reset()
+        agt.refresh_restore(state)
+        agt.refresh(d["key"], d["app"], d["phase"], d["dur_ns"], n_new)
+        runs.append(agt.kernel_times())
+    agt.close()
+    kernels = kernel_averages(runs)
+    dom = max((k for k in kernels if k in METHOD_BYTES), key=lambda k: kernels[k]["avg_ms"])
+    # pass-A kernels read the new events only
+    units = n_new if dom in ("pass_a", "pass_a_range", "pass_a_global") else n
+    alg = METHOD_BYTES[dom] * units
+    achieved = alg / (kernels[dom]["avg_ms"] * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "algorithmic_bytes_per_launch": alg, "avg_launch_ms": round(kernels[dom]["avg_ms"], 4)}
+    log("kernels", json.dumps({k: round(v["avg_ms"], 4) for k, v in kernels.items()}))
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import oracle as O  # a refresh's result is the oracle over the whole log
+        l1, lt = CPU_SAMPLE_LOG2[ci]
+        threads = host_threads()
+        m = min(n, 1 << lt)
+        tc = time.perf_counter()
+        O.run(ev["key"][:m], ev["app"][:m], ev["phase"][:m], ev["dur_ns"][:m], c, P, score_key=keys, s=s,
+              threads=threads)
+        dt = time.perf_counter() - tc
+        cpu = {"value": round(m / dt / 1e9, 6), "unit": "G events/s", "cores": threads, "kind": "oracle",
+               "sample": "first %d events of the log, whole path incl. score, group-by sharded over %d threads "
+                         "(%.1f s)" % (m, threads, dt), "nproc": os.cpu_count(), "cpu_model": cpu_model()}
+    line = {
+        "metric": "log events re-weighted per second by an incremental refresh (1/8 of the log new)",
+        "value": round(n / t_refresh / 1e9, 3), "unit": "G events/s", "n_gpus": 1, "steps": steps,
+        "warmup": args.warmup, "ms_per_step": round(1e3 * t_refresh, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u128", "data": "synthetic",
+        "config": {"workload": cfg["name"], "log_events": n, "new_events": n_new, "seed": cfg["seed"],
+                   "path": ag.path_used(), "parallelism": "none",
+                   "entry": "atrex_refresh_restore + atrex_refresh + atrex_phase_normalize + atrex_weighted_score"},
+        "ms_whole_log_from_scratch": round(1e3 * t_full, 4), "speedup_vs_from_scratch": round(t_full / t_refresh, 3),
+        "kernels_ms": {k: round(v["avg_ms"], 4) for k, v in kernels.items()},
+        "parity": parity, "roofline": roofline, "cpu_baseline": cpu,
+    }
+    ag.close()
+    print(json.dumps(line), flush=True)
+    return 1 if parity is not None and parity.get("checked") and not parity["ok"] else 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=None, help="workload index (0..4); default 3 = 1B events")
-    ap.add_argument("--row", default="weights", choices=["weights", "share"],
-                    help="weights: the importance-weight path (default); share: the target-DSL share")
+    ap.add_argument("--row", default="weights", choices=["weights", "share", "refresh"],
+                    help="weights: the importance-weight path (default); share: the target-DSL share; "
+                         "refresh: an incremental refresh of an append-only log")
     ap.add_argument("--path", default="auto", choices=["auto", "lds_hash", "global_hash", "radix_sort"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true")
@@ -257,6 +397,8 @@ def main() -> int:
         return 2
     if args.row == "share":
         return bench_share(args)
+    if args.row == "refresh":
+        return bench_refresh(args)
     if args.config is None:
         args.config = 3
     steps = args.steps if args.steps is not None else DEFAULT_STEPS[args.config]

@@ -79,6 +79,11 @@ typedef enum {
                                      atrex_get_app_totals gives T[ph] and n[ph] (counts always
                                      on).  Not with ATREX_FLAG_RAW (W is already the raw time).
                                      This is the input of atrex_target_share. */
+#define ATREX_FLAG_INCREMENTAL 16u /* the events are an append-only log that grows between calls:
+                                      the context keeps the per-(app, phase) totals (and counts) of
+                                      the events folded so far, and each group-by runs pass A over
+                                      the new events only (see atrex_refresh).  Implies
+                                      ATREX_FLAG_APP_COUNT; not with ATREX_FLAG_DEVICE_TIME. */
 
 typedef struct {
   uint64_t lo, hi; /* value = lo + hi * 2^64 */
@@ -202,6 +207,35 @@ atrex_status atrex_run(atrex_ctx *ctx, const atrex_events *ev, const atrex_group
  * Valid after atrex_aggregate_events (STATE before). */
 atrex_status atrex_get_app_totals(atrex_ctx *ctx, atrex_u128 *T, uint64_t *n, uint64_t *mant,
                                   int32_t *rho);
+
+/* ---- Incremental refresh of the weights (§3.4: the weights are recomputed
+ * when the trace distribution is refreshed) -------------------------------
+ * With ATREX_FLAG_INCREMENTAL the caller keeps the trace as an append-only
+ * log of events in device memory (n < 2^31, at most max_events) and the
+ * context keeps the per-(app, phase) totals of the first n_folded events.  A
+ * refresh folds the new events log[n_folded, n) into those totals (pass A
+ * over the new events only: D_a^phi is a plain sum), forms the Eq. (3) scale
+ * from the totals of the whole log, runs pass B over the whole log (every
+ * event's share depends on the new totals) and orders the groups, exactly as
+ * atrex_aggregate_events over the whole log would: the results are identical
+ * bit for bit.  The first n_folded events must not have changed since they
+ * were folded (the library cannot check it).  On success n_folded becomes n;
+ * after an error the totals and n_folded are as before.  Then
+ * atrex_phase_normalize / atrex_weighted_score as usual; atrex_aggregate_reset
+ * keeps the totals.  atrex_aggregate_events and atrex_run on such a context
+ * fold log[n_folded, ev->n) the same way (INVALID_ARG when ev->n < n_folded).
+ * Errors: INVALID_ARG unless the context has ATREX_FLAG_INCREMENTAL and
+ * log->n = n_folded + n_new; as atrex_aggregate_events otherwise.
+ * HOST: log (struct of DEVICE pointers), num_groups. */
+atrex_status atrex_refresh(atrex_ctx *ctx, const atrex_events *log, uint64_t n_new, uint64_t *num_groups);
+
+/* The incremental state, to checkpoint a context or to resume in another one
+ * (same num_phases, num_apps and app weights): T (u128) and n (u64) per
+ * (app, phase), index a * P + ph (DEVICE, [A*P]), and n_folded (HOST).
+ * atrex_refresh_restore needs the initialised state (after init or reset);
+ * INVALID_ARG without ATREX_FLAG_INCREMENTAL or with n_folded > max_events. */
+atrex_status atrex_refresh_state(atrex_ctx *ctx, atrex_u128 *T, uint64_t *n, uint64_t *n_folded);
+atrex_status atrex_refresh_restore(atrex_ctx *ctx, const atrex_u128 *T, const uint64_t *n, uint64_t n_folded);
 
 /* ---- Target-DSL device-time share (§4.1, Metrics: "FlyDSL adoption") -------
  * Input: a context initialised with ATREX_FLAG_DEVICE_TIME and num_phases = 2

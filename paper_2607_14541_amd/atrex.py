@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libatrex.so")
 
 OK, E_INVALID_ARG, E_OUT_OF_RANGE, E_STATE, E_CAPACITY, E_DEVICE = 0, -1, -2, -3, -4, -5
 PATHS = {"auto": 0, "lds_hash": 1, "global_hash": 2, "radix_sort": 3}
-FLAG_TIMING, FLAG_RAW, FLAG_APP_COUNT, FLAG_DEVICE_TIME = 1, 2, 4, 8
+FLAG_TIMING, FLAG_RAW, FLAG_APP_COUNT, FLAG_DEVICE_TIME, FLAG_INCREMENTAL = 1, 2, 4, 8, 16
 
 
 class AtrexError(RuntimeError):
@@ -98,6 +98,9 @@ def _lib() -> ctypes.CDLL:
                                   U64, P, P, U64, P, P, P, ctypes.POINTER(_RunResult)],
             "atrex_get_app_totals": [P, P, P, P, P],
             "atrex_target_share": [P, ctypes.POINTER(_ShareOut), U64, U64, ctypes.POINTER(_ShareResult)],
+            "atrex_refresh": [P, ctypes.POINTER(_Events), U64, ctypes.POINTER(U64)],
+            "atrex_refresh_state": [P, P, P, ctypes.POINTER(U64)],
+            "atrex_refresh_restore": [P, P, P, U64],
             "atrex_kernel_times": [P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float),
                                    ctypes.POINTER(U64), I, ctypes.POINTER(I)],
             "atrex_aggregate_reset": [P],
@@ -154,13 +157,16 @@ class Aggregator:
     device_time=True: the plain device-time group-by (ATREX_FLAG_DEVICE_TIME):
     no applications (app_weight_q16 is ignored and may be None; aggregate()
     takes app=None), W = sum of dur per (key, phase); with num_phases = 2 it
-    feeds target_share()."""
+    feeds target_share().
+
+    incremental=True: the events form an append-only log (ATREX_FLAG_INCREMENTAL);
+    refresh() folds the events added since the last one."""
 
     def __init__(self, num_phases: int, app_weight_q16: torch.Tensor | None, max_events: int,
                  max_groups: int = 0, max_keys: int = 0, max_score: int = 0, path: str = "auto",
                  timing: bool = False, raw: bool = False, app_count: bool = False,
                  stream: torch.cuda.Stream | None = None, device_time: bool = False,
-                 device: torch.device | None = None):
+                 device: torch.device | None = None, incremental: bool = False):
         L = _lib()
         self.device_time = device_time
         if device_time:
@@ -174,7 +180,7 @@ class Aggregator:
         self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
         self.P = int(num_phases)
         self.raw = raw
-        self.app_count = app_count or device_time  # the device-time mode always counts
+        self.app_count = app_count or device_time or incremental  # these modes always count
         p = _InitParams()
         p.num_phases, p.num_apps = self.P, self.A
         p.app_weight_q16 = c.data_ptr() if c is not None else None
@@ -182,7 +188,7 @@ class Aggregator:
         p.path = PATHS[path]
         p.stream = self.stream.cuda_stream
         p.flags = ((FLAG_TIMING if timing else 0) | (FLAG_RAW if raw else 0) | (FLAG_APP_COUNT if app_count else 0)
-                   | (FLAG_DEVICE_TIME if device_time else 0))
+                   | (FLAG_DEVICE_TIME if device_time else 0) | (FLAG_INCREMENTAL if incremental else 0))
         nbytes = ctypes.c_size_t()
         _check(L.atrex_workspace_bytes(ctypes.byref(p), ctypes.byref(nbytes)), "atrex_workspace_bytes")
         self.workspace = torch.empty(max(int(nbytes.value), 256), dtype=torch.uint8, device=self.device)
@@ -218,6 +224,40 @@ class Aggregator:
         self._events = None
         self.num_groups = G.value
         return self.num_groups
+
+    def refresh(self, key: torch.Tensor, app: torch.Tensor, phase: torch.Tensor, dur_ns: torch.Tensor,
+                n_new: int) -> int:
+        """Incremental refresh (incremental=True): the tensors hold the whole
+        log, whose last n_new events are new since the last refresh; the
+        results equal a group-by of the whole log.  Returns the group count."""
+        key = _dev(_as_i32(key), torch.int32, "key")
+        app = _dev(_as_i32(app), torch.int32, "app")
+        phase = _dev(phase, torch.uint8, "phase")
+        dur_ns = _dev(dur_ns, torch.int64, "dur_ns")
+        n = key.numel()
+        if not (app.numel() == n and phase.numel() == n and dur_ns.numel() == n):
+            raise ValueError("event arrays differ in length")
+        self._events = (key, app, phase, dur_ns)
+        ev = _Events(_ptr(key), _ptr(app), _ptr(phase), _ptr(dur_ns), n)
+        G = ctypes.c_uint64()
+        _check(_lib().atrex_refresh(self._ctx, ctypes.byref(ev), int(n_new), ctypes.byref(G)), "atrex_refresh")
+        self._events = None
+        self.num_groups = G.value
+        return self.num_groups
+
+    def refresh_state(self) -> dict:
+        """The folded per-(app, phase) totals T, counts n and n_folded."""
+        GA, dev = self.A * self.P, self.device
+        T = torch.empty((GA, 2), dtype=torch.int64, device=dev)
+        n = torch.empty(GA, dtype=torch.int64, device=dev)
+        nf = ctypes.c_uint64()
+        _check(_lib().atrex_refresh_state(self._ctx, _ptr(T), _ptr(n), ctypes.byref(nf)), "atrex_refresh_state")
+        return dict(T=T, n=n, n_folded=nf.value)
+
+    def refresh_restore(self, state: dict) -> None:
+        """Resume from refresh_state() of a context with the same parameters."""
+        _check(_lib().atrex_refresh_restore(self._ctx, _ptr(state["T"].contiguous()), _ptr(state["n"].contiguous()),
+                                            int(state["n_folded"])), "atrex_refresh_restore")
 
     def reset(self) -> None:
         """Back to the initialised state: the next batch reuses the workspace."""

@@ -40,6 +40,7 @@ uint64_t next_pow2(uint64_t x) {
 // Byte offsets of every workspace region (all 256-byte aligned).
 struct Layout {
   size_t ctrl, T, carryA, partA, partC, nA, scale, bscale, dict, acc, raw;
+  size_t T_run, n_run;  // incremental refresh: totals of the events folded so far
   size_t okey, oacc, oraw, ocount, skey, sval, sraw, scount;  // LDS engine outputs
   size_t ol_rk, ol_key, ol_lo, ol_hi, ol_rlo, ol_rhi, ol_count, ol_part;  // per-owner sorted lists
   size_t H, O, rec, rraw, bstart, istart;                     // partition engine
@@ -67,6 +68,7 @@ struct Params {
   bool count;    // invocation counts per (app, phase) in pass A
   bool compact;  // global-hash engine only: no per-event scratch, rows sized to the groups
   bool time;     // plain device-time group-by: no applications, identity scale (counts always on)
+  bool incr;     // incremental refresh of an append-only log (counts always on)
 };
 
 constexpr uint32_t kPassARangesMax = 16;
@@ -124,6 +126,8 @@ Layout make_layout(const Params& p) {
   L.nA = take(p.count || p.time ? GA * 8 : 0);
   L.scale = take(GA * 8);
   L.bscale = take(GA * 8);
+  L.T_run = take(p.incr ? GA * 16 : 0);
+  L.n_run = take(p.incr ? GA * 8 : 0);
   L.dict = take(L.capD * 8);
   L.acc = take(L.capD * p.P * 16);
   L.raw = take(p.raw ? L.capD * p.P * 16 : 0);
@@ -224,6 +228,9 @@ atrex_status check_params(const atrex_init_params* ip, Params* out) {
   p.compact = false;
   p.time = (ip->flags & ATREX_FLAG_DEVICE_TIME) != 0;
   if (p.time && (p.A != 1 || p.raw)) return ATREX_E_INVALID_ARG;
+  p.incr = (ip->flags & ATREX_FLAG_INCREMENTAL) != 0;
+  if (p.incr && p.time) return ATREX_E_INVALID_ARG;
+  if (p.incr) p.count = true;  // the counts of the whole log are kept too
   *out = p;
   return ATREX_OK;
 }
@@ -261,6 +268,7 @@ struct atrex_ctx {
   int state;  // 0 initialised, 1 aggregated, 2 normalised
   bool S_ready;  // the per-phase totals S were written by the ordering step
   uint64_t G, nops, nkeys;
+  uint64_t n_folded;  // incremental refresh: events whose totals are in T_run / n_run
   int cus;
   const char* path_used;
   std::vector<Timed> timed;
@@ -587,6 +595,7 @@ atrex_status atrex_aggregate_init(const atrex_init_params* ip, atrex_ctx** out) 
   c->state = 0;
   c->S_ready = false;
   c->G = c->nops = c->nkeys = 0;
+  c->n_folded = 0;
   c->path_used = "none";
   c->ntimed = 0;
   if (hipHostMalloc((void**)&c->pinned, kPinnedBytes, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) {
@@ -615,6 +624,10 @@ atrex_status atrex_aggregate_init(const atrex_init_params* ip, atrex_ctx** out) 
   }
   // the pass-A carry table starts clear (each pass-A reduce clears it again)
   launch_fill_u64(c->s, c->at<uint64_t>(c->L.carryA), (uint64_t)p.A * p.P, 0);
+  if (p.incr) {  // nothing folded yet
+    launch_fill_u64(c->s, c->at<uint64_t>(c->L.T_run), 2 * (uint64_t)p.A * p.P, 0);
+    launch_fill_u64(c->s, c->at<uint64_t>(c->L.n_run), (uint64_t)p.A * p.P, 0);
+  }
   if (p.time) {  // no applications, no card-hour weights
     st = sync_status(c);
     if (st != ATREX_OK) {
@@ -658,6 +671,7 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
   const uint64_t n = ev->n;
   if (n > c->p.max_events) return ATREX_E_CAPACITY;
   if (c->p.time ? ev->app != nullptr : (n > 0 && !ev->app)) return ATREX_E_INVALID_ARG;
+  if (c->p.incr && n < c->n_folded) return ATREX_E_INVALID_ARG;  // the log only grows
   if (n > 0 && (!ev->key || !ev->phase || !ev->dur_ns)) return ATREX_E_INVALID_ARG;
   const uint32_t P = c->p.P, A = c->p.A;
   const uint64_t GA = (uint64_t)A * P;
@@ -672,6 +686,19 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
   d.n = n;
   const bool vec_ok = aligned(ev->key, 16) && aligned(ev->app, 16) && aligned(ev->phase, 4) &&
                       aligned(ev->dur_ns, 16);
+  // pass A reads the events it folds: all of them, or with an incremental
+  // context the ones past those folded before
+  const uint64_t from = c->p.incr ? c->n_folded : 0;
+  EventsDev dA = d;
+  if (from) {
+    dA.key = ev->key + from;
+    dA.app = ev->app + from;
+    dA.phase = ev->phase + from;
+    dA.dur = ev->dur_ns + from;
+    dA.n = n - from;
+  }
+  const uint64_t na = dA.n;
+  const bool vecA = aligned(dA.key, 16) && aligned(dA.app, 16) && aligned(dA.phase, 4) && aligned(dA.dur, 16);
   GroupTables gt = c->tables();
   // clear the control words (the pass-A carry table is clear: init clears
   // it and every pass-A reduce leaves it so)
@@ -688,39 +715,39 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
     // duration itself) in both word forms
     launch_fill_u64(s, T, 2 * (uint64_t)P, 0);
     launch_fill_u64(s, nA, P, 0);
-    TIMED(c, "time_totals", n,
-          launch_time_totals(s, d, P, (uint32_t)c->cus, vec_ok, (unsigned long long*)T, (unsigned long long*)nA,
+    TIMED(c, "time_totals", na,
+          launch_time_totals(s, dA, P, (uint32_t)c->cus, vecA, (unsigned long long*)T, (unsigned long long*)nA,
                              c->err()));
     launch_fill_u64(s, scale, P, (uint64_t)64 << 56);
     launch_fill_u64(s, c->at<uint64_t>(L.bscale), P, ((uint64_t)63 << 56) | ((uint64_t)1 << 55));
-  } else if (L.passA == 0 && vec_ok) {
+  } else if (L.passA == 0 && vecA) {
     // one workgroup per CU (two groups of loads in flight per lane): two per
     // CU ran as one after the other (the SIMDs favour the older one) and
     // doubled the partial rows for the reduce
     uint64_t nb = std::min<uint64_t>((uint64_t)c->cus, L.partA_rows);
-    nb = std::max<uint64_t>(1, std::min<uint64_t>(nb, (n / 4 + kPassAThreads - 1) / kPassAThreads));
-    TIMED(c, "pass_a", n,
-          launch_pass_a_lds(s, d, A, P, (uint32_t)nb, c->at<unsigned long long>(L.partA),
+    nb = std::max<uint64_t>(1, std::min<uint64_t>(nb, (na / 4 + kPassAThreads - 1) / kPassAThreads));
+    TIMED(c, "pass_a", na,
+          launch_pass_a_lds(s, dA, A, P, (uint32_t)nb, c->at<unsigned long long>(L.partA),
                             c->at<unsigned long long>(L.carryA), pcount, c->err()));
     TIMED(c, "pass_a_reduce", GA,
           launch_pass_a_reduce(s, c->at<unsigned long long>(L.partA), (uint32_t)nb, (uint32_t)GA,
                                c->at<unsigned long long>(L.carryA), T, c->app_weight, c->Csum(), P, scale,
                                c->at<void>(L.bscale), pcount, nA));
-  } else if (L.passA == 3 && vec_ok) {
+  } else if (L.passA == 3 && vecA) {
     const uint32_t bins = pass_a_range_bins(c->p.count);
     const uint32_t R = (uint32_t)((GA + bins - 1) / bins);
     const uint32_t GR = (uint32_t)((GA + R - 1) / R);
-    TIMED(c, "pass_a_range", n,
-          launch_pass_a_range(s, d, A, P, GR, R, kPassASlices, c->at<uint32_t>(L.partA),
+    TIMED(c, "pass_a_range", na,
+          launch_pass_a_range(s, dA, A, P, GR, R, kPassASlices, c->at<uint32_t>(L.partA),
                               c->at<unsigned long long>(L.carryA), pcount, c->err()));
     TIMED(c, "pass_a_reduce", GA,
           launch_pass_a_reduce32(s, c->at<uint32_t>(L.partA), kPassASlices, (uint32_t)GA,
                                  c->at<unsigned long long>(L.carryA), T, c->app_weight, c->Csum(), P, scale,
                                  c->at<void>(L.bscale), pcount, nA));
-  } else if (L.passA == 1 && vec_ok) {
+  } else if (L.passA == 1 && vecA) {
     const uint64_t nb = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)c->cus, kMaxWG));
-    TIMED(c, "pass_a", n,
-          launch_pass_a_lds32(s, d, A, P, (uint32_t)nb, c->at<uint32_t>(L.partA), c->at<unsigned long long>(L.carryA),
+    TIMED(c, "pass_a", na,
+          launch_pass_a_lds32(s, dA, A, P, (uint32_t)nb, c->at<uint32_t>(L.partA), c->at<unsigned long long>(L.carryA),
                               pcount, c->err()));
     TIMED(c, "pass_a_reduce", GA,
           launch_pass_a_reduce32(s, c->at<uint32_t>(L.partA), (uint32_t)nb, (uint32_t)GA,
@@ -729,10 +756,16 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
   } else {
     launch_fill_u64(s, T, GA * 2, 0);
     if (nA) launch_fill_u64(s, nA, GA, 0);
-    TIMED(c, "pass_a_global", n,
-          launch_pass_a_global(s, d, A, P, (uint32_t)std::max<uint64_t>(1, (uint64_t)c->cus * 8), (unsigned long long*)T,
+    TIMED(c, "pass_a_global", na,
+          launch_pass_a_global(s, dA, A, P, (uint32_t)std::max<uint64_t>(1, (uint64_t)c->cus * 8), (unsigned long long*)T,
                                (unsigned long long*)nA, c->err()));
     // scale, Eq. (3) (the column-sum kernels of the other modes compute it with T)
+    TIMED(c, "scale", GA, launch_scale(s, T, c->app_weight, c->Csum(), A, P, scale, c->at<void>(L.bscale)));
+  }
+  if (c->p.incr) {
+    // the totals of the whole log: those folded before plus the new events'
+    // (skipped on the device after a range error), and the scale from them
+    launch_fold_totals(s, T, nA, c->at<uint64_t>(L.T_run), c->at<uint64_t>(L.n_run), GA, c->err());
     TIMED(c, "scale", GA, launch_scale(s, T, c->app_weight, c->Csum(), A, P, scale, c->at<void>(L.bscale)));
   }
   // pass B, Eq. (2)-(3): every engine emits rows (key << 3 | phase, Q96 sum)
@@ -863,6 +896,12 @@ atrex_status aggregate_complete(atrex_ctx* c, AggRun* a, uint64_t* num_groups, b
     if (st != ATREX_OK) return st;
   }
   if (G > L.maxG) return ATREX_E_CAPACITY;
+  if (c->p.incr) {  // the refresh stands: the totals of the whole log become the folded ones
+    const uint64_t GA = (uint64_t)c->p.A * c->p.P;
+    launch_copy_u64(s, c->at<uint64_t>(L.T_run), c->at<uint64_t>(L.T), 2 * GA);
+    launch_copy_u64(s, c->at<uint64_t>(L.n_run), c->at<uint64_t>(L.nA), GA);
+    c->n_folded = n;
+  }
   c->end_call();
   c->G = G;
   c->S_ready = ranked;
@@ -1261,6 +1300,33 @@ atrex_status atrex_get_app_totals(atrex_ctx* c, atrex_u128* T, uint64_t* n, uint
   if (n) (void)hipMemcpyAsync(n, c->at<void>(c->L.nA), GA * 8, hipMemcpyDeviceToDevice, c->s);
   if (mant || rho) launch_unpack_scale(c->s, c->at<uint64_t>(c->L.scale), GA, mant, rho);
   return sync_read(c);
+}
+
+atrex_status atrex_refresh(atrex_ctx* c, const atrex_events* log, uint64_t n_new, uint64_t* num_groups) {
+  if (!c || !log || !num_groups) return ATREX_E_INVALID_ARG;
+  if (!c->p.incr || log->n < n_new || log->n - n_new != c->n_folded) return ATREX_E_INVALID_ARG;
+  return atrex_aggregate_events(c, log, num_groups);
+}
+
+atrex_status atrex_refresh_state(atrex_ctx* c, atrex_u128* T, uint64_t* n, uint64_t* n_folded) {
+  if (!c || !T || !n || !n_folded || !c->p.incr) return ATREX_E_INVALID_ARG;
+  const uint64_t GA = (uint64_t)c->p.A * c->p.P;
+  launch_copy_u64(c->s, (uint64_t*)T, c->at<uint64_t>(c->L.T_run), 2 * GA);
+  launch_copy_u64(c->s, n, c->at<uint64_t>(c->L.n_run), GA);
+  const atrex_status st = sync_read(c);
+  if (st == ATREX_OK) *n_folded = c->n_folded;
+  return st;
+}
+
+atrex_status atrex_refresh_restore(atrex_ctx* c, const atrex_u128* T, const uint64_t* n, uint64_t n_folded) {
+  if (!c || !T || !n || !c->p.incr || n_folded > c->p.max_events) return ATREX_E_INVALID_ARG;
+  if (c->state != 0) return ATREX_E_STATE;
+  const uint64_t GA = (uint64_t)c->p.A * c->p.P;
+  launch_copy_u64(c->s, c->at<uint64_t>(c->L.T_run), (const uint64_t*)T, 2 * GA);
+  launch_copy_u64(c->s, c->at<uint64_t>(c->L.n_run), n, GA);
+  const atrex_status st = sync_read(c);
+  if (st == ATREX_OK) c->n_folded = n_folded;
+  return st;
 }
 
 atrex_status atrex_target_share(atrex_ctx* c, const atrex_share_out* out, uint64_t key_capacity,

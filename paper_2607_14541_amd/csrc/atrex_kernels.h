@@ -137,6 +137,11 @@ void launch_pass_a_range(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_
 void launch_pass_a_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
                           unsigned long long* T, unsigned long long* cnt, uint32_t* err);
 void launch_unpack_scale(hipStream_t s, const uint64_t* sw, uint64_t G, uint64_t* mant, int32_t* rho);
+// incremental refresh: T += T_run, cnt += n_run over G (app, phase) pairs,
+// unless err has the range bit; and a plain device copy
+void launch_fold_totals(hipStream_t s, uint64_t* T, uint64_t* cnt, const uint64_t* T_run, const uint64_t* n_run,
+                        uint64_t G, const uint32_t* err);
+void launch_copy_u64(hipStream_t s, uint64_t* dst, const uint64_t* src, uint64_t n);
 // scale words (general form) and the 16-byte pass-B entries
 void launch_scale(hipStream_t s, const uint64_t* T, const uint32_t* c, const uint64_t* Csum, uint32_t A,
                   uint32_t P, uint64_t* scale, void* bscale);

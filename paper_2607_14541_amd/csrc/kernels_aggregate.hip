@@ -5,6 +5,8 @@
 //   compaction of the distinct (key, phase) groups.
 // Events are a struct of arrays (key u32, app u32, phase u8, dur i64) read
 // with 16-byte nontemporal vector loads, four events per thread per step.
+#include <algorithm>
+
 #include "atrex_device.hpp"
 #include "atrex_kernels.h"
 
@@ -960,10 +962,43 @@ __global__ void k_unpack_scale(const uint64_t* __restrict__ sw, uint64_t G, uint
   if (rho) rho[g] = w ? (int32_t)(w >> 56) - 64 : 0;
 }
 
+// ---------------------------------------------------------------------------
+// Incremental refresh (an append-only event log): the per-(app, phase) totals
+// of the events folded so far (run) plus those of the new events (T, n, as
+// pass A left them) become the totals of the whole log, in T and n.  Skipped
+// after a range error in the new events, so that a failed refresh leaves
+// every total as it was.
+__global__ void k_fold_totals(uint64_t* __restrict__ T, uint64_t* __restrict__ cnt,
+                              const uint64_t* __restrict__ T_run, const uint64_t* __restrict__ n_run, uint64_t G,
+                              const uint32_t* __restrict__ err) {
+  const uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= G || (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & ATREX_ERRBIT_RANGE)) return;
+  const u128 t = make_u128(T[2 * g], T[2 * g + 1]) + make_u128(T_run[2 * g], T_run[2 * g + 1]);
+  T[2 * g] = (uint64_t)t;
+  T[2 * g + 1] = (uint64_t)(t >> 64);
+  cnt[g] += n_run[g];
+}
+
+__global__ void k_copy_u64(uint64_t* __restrict__ dst, const uint64_t* __restrict__ src, uint64_t n) {
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (uint64_t)gridDim.x * blockDim.x)
+    dst[i] = src[i];
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
 // Host launchers
+void launch_fold_totals(hipStream_t s, uint64_t* T, uint64_t* cnt, const uint64_t* T_run, const uint64_t* n_run,
+                        uint64_t G, const uint32_t* err) {
+  if (G) hipLaunchKernelGGL(k_fold_totals, dim3((uint32_t)((G + 255) / 256)), dim3(256), 0, s, T, cnt, T_run, n_run, G, err);
+}
+
+void launch_copy_u64(hipStream_t s, uint64_t* dst, const uint64_t* src, uint64_t n) {
+  if (!n) return;
+  const uint64_t nb = std::min<uint64_t>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(k_copy_u64, dim3((uint32_t)nb), dim3(256), 0, s, dst, src, n);
+}
+
 void launch_unpack_scale(hipStream_t s, const uint64_t* sw, uint64_t G, uint64_t* mant, int32_t* rho) {
   if (G) hipLaunchKernelGGL(k_unpack_scale, dim3((uint32_t)((G + 255) / 256)), dim3(256), 0, s, sw, G, mant, rho);
 }

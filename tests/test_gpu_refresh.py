@@ -1,0 +1,154 @@
+"""Incremental refresh of the weights on the GPU (§3.4: the weights are
+recomputed whenever the trace distribution is refreshed) against the oracle
+over the whole log.  The trace is an append-only log in device memory; each
+refresh folds the new events into the context's per-(app, phase) totals
+(pass A over the new events only) and re-runs pass B over the log.  After
+every refresh all outputs must equal the oracle's on the log so far: every
+integer bit for bit (groups, counts, W, S, T, n, m, rho, U), the fp64
+weights and S_agg within 1e-12."""
+import numpy as np
+import pytest
+import torch
+
+import gpu_helpers as H
+from oracle import oracle as O
+from paper_2607_14541_amd import atrex as X
+from paper_2607_14541_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _outputs(ag, sk, sv):
+    out = {k: H._np_out(k, v) for k, v in ag.normalize().items()}
+    out.update({("op_" + k if k != "op" else k): H._np_out(k, v) for k, v in ag.op_weights().items()})
+    kw = ag.key_weights()
+    out.update(ukey=H._np_out("key", kw["key"]), key_U=H._np_out("U", kw["U"]), omega=H._np_out("omega", kw["omega"]))
+    out.update({"app_" + k: H._np_out("app_" + k, v) for k, v in ag.app_totals().items()})
+    sc = ag.score(sk, sv)
+    out.update(score_op=H._np_out("op", sc["op"]), score_op_weight=H._np_out("w", sc["op_weight"]),
+               score_op_score=H._np_out("s", sc["op_score"]), s_agg=sc["s_agg"])
+    out["num_groups"] = out["key"].size
+    return out
+
+
+def _log(ci, n):
+    cfg = synth.CONFIGS[ci]
+    ev = synth.events(cfg, n=n)
+    keys = synth.key_space(cfg)
+    return cfg, ev, synth.app_weights(cfg), keys, synth.scores(cfg, keys, nan_frac=0.1)
+
+
+@pytest.mark.parametrize("path", ["auto", "lds_hash", "radix_sort", "global_hash"])
+@pytest.mark.parametrize("ci", [1, 3])
+def test_refresh_equals_the_whole_log(ci, path):
+    # batch ends: unaligned (pass A over the new events takes the global
+    # kernel), aligned, and the whole log
+    n = (1 << 21) + 37
+    ends = [1000003, 1572864, n]
+    cfg, ev, c, keys, s = _log(ci, n)
+    P = cfg["num_phases"]
+    d = {k: H.dev(ev[k], dt) for k, dt in (("key", np.int32), ("app", np.int32), ("phase", np.uint8),
+                                             ("dur_ns", np.int64))}
+    sk, sv = H.dev(keys, np.int32), H.dev(s, np.float64)
+    ag = X.Aggregator(P, H.dev(c, np.int32), max_events=n, max_keys=keys.size, max_groups=keys.size * P,
+                      max_score=keys.size, path=path, raw=True, incremental=True)
+    try:
+        prev = 0
+        for end in ends:
+            H.say("refresh, config", ci, path, "log", end, "new", end - prev)
+            ag.reset()
+            ag.refresh(d["key"][:end], d["app"][:end], d["phase"][:end], d["dur_ns"][:end], end - prev)
+            g = _outputs(ag, sk, sv)
+            o = O.run(ev["key"][:end], ev["app"][:end], ev["phase"][:end], ev["dur_ns"][:end], c, P,
+                      score_key=keys, s=s)
+            H.compare(g, o, raw=True, score=True)
+            st = ag.refresh_state()
+            assert st["n_folded"] == end
+            assert np.array_equal(H._np_out("T", st["T"]), o["app_total"])
+            assert np.array_equal(H._np_out("n", st["n"]), o["app_count"])
+            prev = end
+    finally:
+        ag.close()
+
+
+def test_refresh_through_the_one_call_path():
+    """atrex_run on an incremental context folds the events past those folded."""
+    n = (1 << 20) + 5
+    cfg, ev, c, keys, s = _log(1, n)
+    P = cfg["num_phases"]
+    d = {k: H.dev(ev[k], dt) for k, dt in (("key", np.int32), ("app", np.int32), ("phase", np.uint8),
+                                             ("dur_ns", np.int64))}
+    ag = X.Aggregator(P, H.dev(c, np.int32), max_events=n, max_keys=keys.size, max_groups=keys.size * P,
+                      max_score=keys.size, incremental=True)
+    try:
+        gb = ag.group_buffers(keys.size * P)
+        sb = dict(op=torch.empty(keys.size, dtype=torch.int32, device="cuda"),
+                  op_weight=torch.empty(keys.size, dtype=torch.float64, device="cuda"),
+                  op_score=torch.empty(keys.size, dtype=torch.float64, device="cuda"))
+        for end in (300001, n):
+            r = ag.run(d["key"][:end], d["app"][:end], d["phase"][:end], d["dur_ns"][:end], gb,
+                       H.dev(keys, np.int32), H.dev(s, np.float64), sb)
+            o = O.run(ev["key"][:end], ev["app"][:end], ev["phase"][:end], ev["dur_ns"][:end], c, P,
+                      score_key=keys, s=s)
+            gr = {k: H._np_out(k, v) for k, v in r["groups"].items()}
+            assert np.array_equal(gr["wsum"], o["wsum"]) and np.array_equal(gr["count"], o["count"])
+            assert abs(r["score"]["s_agg"] - o["s_agg"]) <= H.REL_TOL * abs(o["s_agg"])
+    finally:
+        ag.close()
+
+
+def test_checkpoint_and_resume_in_another_context():
+    n = (1 << 20) + 11
+    cut = 600000
+    cfg, ev, c, keys, s = _log(3, n)
+    P = cfg["num_phases"]
+    d = {k: H.dev(ev[k], dt) for k, dt in (("key", np.int32), ("app", np.int32), ("phase", np.uint8),
+                                             ("dur_ns", np.int64))}
+    dc = H.dev(c, np.int32)
+    kw = dict(max_events=n, max_keys=keys.size, max_groups=keys.size * P, max_score=keys.size, incremental=True)
+    a = X.Aggregator(P, dc, **kw)
+    b = X.Aggregator(P, dc, **kw)
+    try:
+        a.refresh(d["key"][:cut], d["app"][:cut], d["phase"][:cut], d["dur_ns"][:cut], cut)
+        state = a.refresh_state()
+        b.refresh_restore(state)
+        b.refresh(d["key"], d["app"], d["phase"], d["dur_ns"], n - cut)
+        g = b.normalize()
+        o = O.run(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, P)
+        assert np.array_equal(H._np_out("wsum", g["wsum"]), o["wsum"])
+        assert np.array_equal(H._np_out("key", g["key"]), o["key"])
+        assert np.array_equal(H._np_out("T", b.app_totals()["T"]), o["app_total"])
+    finally:
+        a.close()
+        b.close()
+
+
+def test_a_failed_refresh_changes_nothing():
+    n = 200000
+    cfg, ev, c, keys, s = _log(1, n)
+    P = cfg["num_phases"]
+    bad = {k: v.copy() for k, v in ev.items()}
+    bad["app"][150000] = cfg["num_apps"]  # out of range, in the new events
+    dc = H.dev(c, np.int32)
+    ag = X.Aggregator(P, dc, max_events=n, max_keys=keys.size, max_groups=keys.size * P, incremental=True)
+    try:
+        d = {k: H.dev(ev[k], dt) for k, dt in (("key", np.int32), ("app", np.int32), ("phase", np.uint8),
+                                                 ("dur_ns", np.int64))}
+        db = {k: H.dev(bad[k], dt) for k, dt in (("key", np.int32), ("app", np.int32), ("phase", np.uint8),
+                                                   ("dur_ns", np.int64))}
+        ag.refresh(d["key"][:100000], d["app"][:100000], d["phase"][:100000], d["dur_ns"][:100000], 100000)
+        ag.reset()
+        with pytest.raises(X.AtrexError) as e:
+            ag.refresh(db["key"], db["app"], db["phase"], db["dur_ns"], n - 100000)
+        assert e.value.status == X.E_OUT_OF_RANGE
+        assert ag.refresh_state()["n_folded"] == 100000
+        with pytest.raises(X.AtrexError) as e:  # n_new that does not continue the log
+            ag.refresh(d["key"], d["app"], d["phase"], d["dur_ns"], 5)
+        assert e.value.status == X.E_INVALID_ARG
+        ag.refresh(d["key"], d["app"], d["phase"], d["dur_ns"], n - 100000)
+        g = ag.normalize()
+        o = O.run(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, P)
+        assert np.array_equal(H._np_out("wsum", g["wsum"]), o["wsum"])
+        assert np.array_equal(H._np_out("n", ag.refresh_state()["n"]), o["app_count"])
+    finally:
+        ag.close()

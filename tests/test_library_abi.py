@@ -73,3 +73,18 @@ def test_device_time_flag_validation(lib):
         p.num_phases, p.num_apps, p.flags = 2, A, flags
         assert (lib.atrex_workspace_bytes(ctypes.byref(p), ctypes.byref(b)) == 0) == ok, (A, flags)
     assert lib.atrex_target_share(None, None, 0, 0, None) == X.E_INVALID_ARG
+
+
+def test_incremental_flag_validation(lib):
+    """An incremental context cannot also be a device-time one."""
+    from paper_2607_14541_amd import atrex as X
+    p = X._InitParams()
+    b = ctypes.c_size_t()
+    p.max_events, p.num_phases, p.num_apps = 1000, 2, 4
+    p.flags = X.FLAG_INCREMENTAL
+    assert lib.atrex_workspace_bytes(ctypes.byref(p), ctypes.byref(b)) == 0
+    p.num_apps, p.flags = 1, X.FLAG_INCREMENTAL | X.FLAG_DEVICE_TIME
+    assert lib.atrex_workspace_bytes(ctypes.byref(p), ctypes.byref(b)) == X.E_INVALID_ARG
+    assert lib.atrex_refresh(None, None, 0, None) == X.E_INVALID_ARG
+    assert lib.atrex_refresh_state(None, None, None, None) == X.E_INVALID_ARG
+    assert lib.atrex_refresh_restore(None, None, None, 0) == X.E_INVALID_ARG
