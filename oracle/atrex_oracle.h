@@ -122,6 +122,23 @@ void atrex_oracle_share_destroy(atrex_oracle_share *s);
  * number, rounded to nearest, ties to even (NaN for n = 0). */
 double atrex_oracle_exact_mean(const double *x, uint64_t n);
 
+/* ---- Observed runtime of each unit, the deployment baseline (§3.1,
+ * "Baselines and weights"); atrex_oracle_stats.cpp.  Units: keys
+ * (by_phase = 0) or (key, phase) pairs (by_phase = 1), ascending.  Per unit:
+ * count, total (u128, lohi), mean = RN(total)/RN(count), min, max, and for
+ * each of nq <= 8 quantiles q_1e5[j] in [1, 100000] (q = q_1e5 / 1e5) the
+ * nearest-rank value: rank ceil(q count) of the ascending durations.
+ * OUT_OF_RANGE for phase >= num_phases or dur < 0; INVALID_ARG for a bad q. */
+typedef struct atrex_oracle_stats atrex_oracle_stats;
+int atrex_oracle_unit_stats(const uint32_t *key, const uint8_t *phase, const int64_t *dur_ns, uint64_t n,
+                            uint32_t num_phases, int by_phase, const uint32_t *q_1e5, uint32_t nq,
+                            atrex_oracle_stats **out);
+int atrex_oracle_stats_size(const atrex_oracle_stats *s, uint64_t *num_units);
+/* quant: [num_units][nq] */
+int atrex_oracle_stats_get(const atrex_oracle_stats *s, uint32_t *key, uint8_t *phase, uint64_t *count,
+                           uint64_t *total_lohi, double *mean, int64_t *mn, int64_t *mx, int64_t *quant);
+void atrex_oracle_stats_destroy(atrex_oracle_stats *s);
+
 #ifdef __cplusplus
 }
 #endif

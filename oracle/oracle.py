@@ -20,7 +20,8 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 # every oracle source: the weighting path, and the rows built beside it
-SOURCES = [os.path.join(_HERE, f) for f in ("atrex_oracle.cpp", "atrex_oracle_adoption.cpp")]
+SOURCES = [os.path.join(_HERE, f) for f in ("atrex_oracle.cpp", "atrex_oracle_adoption.cpp",
+                                             "atrex_oracle_stats.cpp")]
 _HDR = os.path.join(_HERE, "atrex_oracle.h")
 # ATREX_ORACLE_SANITIZE=1: an AddressSanitizer + UndefinedBehaviorSanitizer
 # build (the process must have the ASan runtime preloaded)
@@ -85,6 +86,14 @@ def lib() -> ctypes.CDLL:
             getattr(L, "atrex_oracle_" + name).restype = ctypes.c_int
         L.atrex_oracle_exact_mean.argtypes = [P, U64]
         L.atrex_oracle_exact_mean.restype = ctypes.c_double
+        # observed runtime per unit (atrex_oracle_stats.cpp)
+        L.atrex_oracle_unit_stats.argtypes = [P, P, P, U64, U32, ctypes.c_int, P, U32, ctypes.POINTER(P)]
+        L.atrex_oracle_stats_size.argtypes = [P, P]
+        L.atrex_oracle_stats_get.argtypes = [P, P, P, P, P, P, P, P, P]
+        L.atrex_oracle_stats_destroy.argtypes = [P]
+        L.atrex_oracle_stats_destroy.restype = None
+        for name in ("unit_stats", "stats_size", "stats_get"):
+            getattr(L, "atrex_oracle_" + name).restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -252,3 +261,36 @@ def target_share(key, is_dsl, dur_ns) -> dict:
         return out
     finally:
         L.atrex_oracle_share_destroy(h)
+
+
+def unit_stats(key, phase, dur_ns, num_phases, q_1e5=(50000, 99000), by_phase=True) -> dict:
+    """Observed runtime per unit (§3.1, the deployment baseline): count,
+    total, mean, min, max and nearest-rank quantiles (q_1e5: q in 1e-5
+    steps).  Raises OracleError on a non-OK status."""
+    L = lib()
+    key = np.ascontiguousarray(key, dtype=np.uint32)
+    phase = np.ascontiguousarray(phase, dtype=np.uint8)
+    dur_ns = np.ascontiguousarray(dur_ns, dtype=np.int64)
+    q = np.ascontiguousarray(q_1e5, dtype=np.uint32)
+    n = key.size
+    assert phase.size == n and dur_ns.size == n
+    h = ctypes.c_void_p()
+    st = L.atrex_oracle_unit_stats(_ptr(key), _ptr(phase), _ptr(dur_ns), n, int(num_phases), int(bool(by_phase)),
+                                   _ptr(q), q.size, ctypes.byref(h))
+    if st != OK:
+        raise OracleError(st, "unit_stats")
+    try:
+        nu = ctypes.c_uint64()
+        L.atrex_oracle_stats_size(h, ctypes.byref(nu))
+        U = nu.value
+        out = {"key": np.zeros(U, np.uint32), "phase": np.zeros(U, np.uint8), "count": np.zeros(U, np.uint64),
+               "total_ns": np.zeros((U, 2), np.uint64), "mean_ns": np.zeros(U, np.float64),
+               "min_ns": np.zeros(U, np.int64), "max_ns": np.zeros(U, np.int64),
+               "quantile_ns": np.zeros((U, q.size), np.int64)}
+        st = L.atrex_oracle_stats_get(h, *(_ptr(out[k]) for k in ("key", "phase", "count", "total_ns", "mean_ns",
+                                                                   "min_ns", "max_ns", "quantile_ns")))
+        if st != OK:
+            raise OracleError(st, "stats_get")
+        return out
+    finally:
+        L.atrex_oracle_stats_destroy(h)
