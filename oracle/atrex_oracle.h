@@ -139,6 +139,29 @@ int atrex_oracle_stats_get(const atrex_oracle_stats *s, uint32_t *key, uint8_t *
                            uint64_t *total_lohi, double *mean, int64_t *mn, int64_t *mx, int64_t *quant);
 void atrex_oracle_stats_destroy(atrex_oracle_stats *s);
 
+/* ---- Host/device correlation join (§3.1); atrex_oracle_join.cpp.
+ * Kernel records: corr, anchor (0 = none), stream, start, end (end < start:
+ * OUT_OF_RANGE).  Host records: kind (0 launch, keyed by correlation id; 1
+ * graph anchor), id (nonzero, unique per kind: INVALID_ARG otherwise), label
+ * key/app/phase.  Interval records: stream, begin, end, label; ascending by
+ * (stream, begin), begin <= end, not overlapping on a stream (INVALID_ARG
+ * otherwise).  A kernel takes the label of its correlation id, else of its
+ * anchor, else of the interval on its stream containing its start, else
+ * none (source 0, 1, 2, 3).  Labelled kernels become events (key, app, phase,
+ * dur = end - start) in kernel order.  n, m, mi < 2^31. */
+typedef struct atrex_oracle_join atrex_oracle_join;
+int atrex_oracle_correlate(const uint64_t *k_corr, const uint64_t *k_anchor, const uint32_t *k_stream,
+                           const int64_t *k_start, const int64_t *k_end, uint64_t n,
+                           const uint8_t *h_kind, const uint64_t *h_id, const uint32_t *h_key,
+                           const uint32_t *h_app, const uint8_t *h_phase, uint64_t m,
+                           const uint32_t *i_stream, const int64_t *i_begin, const int64_t *i_end,
+                           const uint32_t *i_key, const uint32_t *i_app, const uint8_t *i_phase, uint64_t mi,
+                           atrex_oracle_join **out);
+int atrex_oracle_join_counts(const atrex_oracle_join *j, uint64_t *labelled, uint64_t *by /* [4] */);
+int atrex_oracle_join_get(const atrex_oracle_join *j, uint32_t *key, uint32_t *app, uint8_t *phase, int64_t *dur,
+                          uint8_t *source);
+void atrex_oracle_join_destroy(atrex_oracle_join *j);
+
 #ifdef __cplusplus
 }
 #endif

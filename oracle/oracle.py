@@ -21,7 +21,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 # every oracle source: the weighting path, and the rows built beside it
 SOURCES = [os.path.join(_HERE, f) for f in ("atrex_oracle.cpp", "atrex_oracle_adoption.cpp",
-                                             "atrex_oracle_stats.cpp")]
+                                             "atrex_oracle_stats.cpp", "atrex_oracle_join.cpp")]
 _HDR = os.path.join(_HERE, "atrex_oracle.h")
 # ATREX_ORACLE_SANITIZE=1: an AddressSanitizer + UndefinedBehaviorSanitizer
 # build (the process must have the ASan runtime preloaded)
@@ -93,6 +93,14 @@ def lib() -> ctypes.CDLL:
         L.atrex_oracle_stats_destroy.argtypes = [P]
         L.atrex_oracle_stats_destroy.restype = None
         for name in ("unit_stats", "stats_size", "stats_get"):
+            getattr(L, "atrex_oracle_" + name).restype = ctypes.c_int
+        # host/device correlation join (atrex_oracle_join.cpp)
+        L.atrex_oracle_correlate.argtypes = [P] * 5 + [U64] + [P] * 5 + [U64] + [P] * 6 + [U64, ctypes.POINTER(P)]
+        L.atrex_oracle_join_counts.argtypes = [P, P, P]
+        L.atrex_oracle_join_get.argtypes = [P, P, P, P, P, P]
+        L.atrex_oracle_join_destroy.argtypes = [P]
+        L.atrex_oracle_join_destroy.restype = None
+        for name in ("correlate", "join_counts", "join_get"):
             getattr(L, "atrex_oracle_" + name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -294,3 +302,44 @@ def unit_stats(key, phase, dur_ns, num_phases, q_1e5=(50000, 99000), by_phase=Tr
         return out
     finally:
         L.atrex_oracle_stats_destroy(h)
+
+
+def correlate(kernels: dict, host: dict, intervals: dict | None = None) -> dict:
+    """Host/device correlation join (§3.1).  kernels: corr, anchor, stream,
+    start_ns, end_ns; host: kind, id, key, app, phase; intervals: stream,
+    begin_ns, end_ns, key, app, phase.  Returns the labelled events (kernel
+    order), the per-kernel source (0 corr, 1 anchor, 2 interval, 3 none) and
+    the counts.  Raises OracleError on a non-OK status."""
+    L = lib()
+    K = {k: np.ascontiguousarray(kernels[k], dt) for k, dt in
+         (("corr", np.uint64), ("anchor", np.uint64), ("stream", np.uint32), ("start_ns", np.int64),
+          ("end_ns", np.int64))}
+    H = {k: np.ascontiguousarray(host[k], dt) for k, dt in
+         (("kind", np.uint8), ("id", np.uint64), ("key", np.uint32), ("app", np.uint32), ("phase", np.uint8))}
+    iv = intervals or {k: [] for k in ("stream", "begin_ns", "end_ns", "key", "app", "phase")}
+    I = {k: np.ascontiguousarray(iv[k], dt) for k, dt in
+         (("stream", np.uint32), ("begin_ns", np.int64), ("end_ns", np.int64), ("key", np.uint32),
+          ("app", np.uint32), ("phase", np.uint8))}
+    n, m, mi = K["corr"].size, H["kind"].size, I["stream"].size
+    h = ctypes.c_void_p()
+    st = L.atrex_oracle_correlate(*(_ptr(K[k]) for k in ("corr", "anchor", "stream", "start_ns", "end_ns")), n,
+                                  *(_ptr(H[k]) for k in ("kind", "id", "key", "app", "phase")), m,
+                                  *(_ptr(I[k]) for k in ("stream", "begin_ns", "end_ns", "key", "app", "phase")), mi,
+                                  ctypes.byref(h))
+    if st != OK:
+        raise OracleError(st, "correlate")
+    try:
+        lab = ctypes.c_uint64()
+        by = np.zeros(4, np.uint64)
+        L.atrex_oracle_join_counts(h, ctypes.byref(lab), _ptr(by))
+        nl = lab.value
+        out = {"key": np.zeros(nl, np.uint32), "app": np.zeros(nl, np.uint32), "phase": np.zeros(nl, np.uint8),
+               "dur_ns": np.zeros(nl, np.int64), "source": np.zeros(n, np.uint8)}
+        st = L.atrex_oracle_join_get(h, *(_ptr(out[k]) for k in ("key", "app", "phase", "dur_ns", "source")))
+        if st != OK:
+            raise OracleError(st, "join_get")
+        out["by_source"] = by
+        out["labelled"] = nl
+        return out
+    finally:
+        L.atrex_oracle_join_destroy(h)

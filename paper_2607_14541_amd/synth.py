@@ -276,3 +276,71 @@ def profile(cfg: dict, n: int | None = None) -> dict:
     dur = np.clip(dur, 0, 2.0 ** 62).astype(np.int64)
     dur[idle[idx]] = 0
     return dict(key=key, is_dsl=is_dsl, dur_ns=dur)
+
+
+# ---------------------------------------------------------------------------
+# Raw trace records for the host/device correlation join (§3.1): device
+# kernel records (correlation id, graph anchor, stream, start, end) and the
+# host records that label them -- launch records by correlation id, graph
+# records by anchor, and per-stream operator intervals for kernels that carry
+# neither.  Built from a labelled workload (the labels of its events are the
+# ground truth): most kernels carry their launch's correlation id, some run
+# inside a captured graph (anchor only), some carry no id and fall inside
+# their operator's interval, and a few match nothing.
+JOIN_CONFIGS = {
+    0: dict(name="1M kernel records labelled from the 1M-event workload", slug="join_1M", base=0, n=1 << 20,
+            seed=20, streams=8, p_corr=0.80, p_anchor=0.10, p_time=0.08),
+    1: dict(name="64M kernel records labelled from the 64M-event workload", slug="join_64M", base=1, n=1 << 26,
+            seed=21, streams=32, p_corr=0.80, p_anchor=0.10, p_time=0.08),
+}
+
+
+def join_trace(jc: dict, n: int | None = None) -> dict:
+    """kernels / host / intervals record sets and the ground-truth events."""
+    n = jc["n"] if n is None else n
+    seed = jc["seed"]
+    ev = events(CONFIGS[jc["base"]], n=n)
+    S = jc["streams"]
+    u = _unif(seed, 500, n)
+    c1, c2, c3 = jc["p_corr"], jc["p_corr"] + jc["p_anchor"], jc["p_corr"] + jc["p_anchor"] + jc["p_time"]
+    kind = (u >= c1).astype(np.uint8) + (u >= c2) + (u >= c3)
+    stream = (u64_stream(seed, 501, n) % np.uint64(S)).astype(np.uint32)
+    # device timeline: each stream runs its kernels back to back with gaps of
+    # 1..1000 ns (a segmented prefix sum over the kernels of each stream)
+    gap = (u64_stream(seed, 502, n) % np.uint64(1000)).astype(np.int64) + 1
+    order = np.argsort(stream, kind="stable")
+    sp = ev["dur_ns"][order] + gap[order]
+    cs = np.cumsum(sp)
+    first = np.searchsorted(stream[order], np.arange(S, dtype=np.uint32))
+    base = np.where(first > 0, cs[np.maximum(first - 1, 0)], 0)
+    start = np.empty(n, np.int64)
+    start[order] = cs - sp - base[stream[order]]
+    del sp, cs, order
+    end = start + ev["dur_ns"]
+    # correlation ids: distinct pseudo-random values (a bijection of the index)
+    corr_all = u64_stream(seed, 503, n)
+    assert not np.any(corr_all == 0)
+    corr = np.where(kind == 0, corr_all, np.uint64(0))
+    # graph anchors, one per anchored kernel
+    anchored = np.nonzero(kind == 1)[0]
+    anchor = np.zeros(n, np.uint64)
+    anchor[anchored] = np.arange(anchored.size, dtype=np.uint64) + np.uint64(1)
+    # host records in launch order: launches of the correlated kernels, a few
+    # launches whose kernels were not traced (ids that no kernel carries:
+    # u64_stream of another stream), then the graph records
+    hk = np.nonzero(kind == 0)[0]
+    extra = hk[: max(1, hk.size // 50)]
+    ex_id = u64_stream(seed, 506, extra.size) | np.uint64(1)
+    h_id = np.concatenate([corr[hk], ex_id, anchor[anchored]])
+    h_src = np.concatenate([hk, extra, anchored])
+    h_kind = np.concatenate([np.zeros(hk.size + extra.size, np.uint8), np.ones(anchored.size, np.uint8)])
+    host = dict(kind=h_kind, id=h_id, key=ev["key"][h_src], app=ev["app"][h_src], phase=ev["phase"][h_src])
+    # operator intervals of the kernels matched by time: [start, end + 1), inside
+    # the gap before the stream's next kernel; ascending per stream
+    ti = np.nonzero(kind == 2)[0]
+    ib, ie = start[ti], end[ti] + 1
+    o = np.lexsort((ib, stream[ti]))
+    intervals = dict(stream=stream[ti][o], begin_ns=ib[o], end_ns=ie[o], key=ev["key"][ti][o], app=ev["app"][ti][o],
+                     phase=ev["phase"][ti][o])
+    kernels = dict(corr=corr, anchor=anchor, stream=stream, start_ns=start, end_ns=end)
+    return dict(kernels=kernels, host=host, intervals=intervals, truth=ev, kind=kind)

@@ -12,7 +12,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 ORACLE_TESTS = ["test_oracle_golden.py", "test_oracle_bruteforce.py", "test_oracle_invariants.py",
                 "test_oracle_special.py", "test_oracle_paper_table.py", "test_oracle_sharded.py",
-                "test_oracle_adoption.py", "test_oracle_stats.py"]
+                "test_oracle_adoption.py", "test_oracle_stats.py", "test_oracle_join.py"]
 
 
 def _runtime():
