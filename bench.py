@@ -23,7 +23,10 @@ the plain device-time group-by of one profile's kernel invocations and the
 per-shape, per-operator and overall shares), on the 64M-invocation profile by
 default (--config picks 0..2 of the profile workloads).  --row refresh
 measures an incremental refresh of the weights over an append-only log (the
-workload's events, the last eighth new), beside a from-scratch run.
+workload's events, the last eighth new), beside a from-scratch run.  --row
+stats measures the observed runtime per unit (count, total, mean, min, max,
+median, p99) on a profile workload; --row join the host/device correlation
+join that labels raw kernel records.
 """
 from __future__ import annotations
 
@@ -113,10 +116,16 @@ def cpu_model() -> str:
 
 
 def kernel_averages(runs) -> dict:
-    """{name: {avg_ms, items}} from lists of (name, ms, items) per repetition."""
+    """{name: {avg_ms, items}} from lists of (name, ms, items) per repetition:
+    a name's launches within one repetition are summed, then averaged over
+    the repetitions."""
     per = {}
     for times in runs:
+        tot = {}
         for name, ms, items in times:
+            t = tot.setdefault(name, [0.0, items])
+            t[0] += ms
+        for name, (ms, items) in tot.items():
             per.setdefault(name, []).append((ms, items))
     return {k: dict(avg_ms=sum(m for m, _ in v) / len(v), items=v[0][1]) for k, v in per.items()}
 
@@ -237,6 +246,220 @@ def bench_share(args) -> int:
         "parity": parity, "roofline": roofline, "cpu_baseline": cpu,
     }
     ag.close()
+    print(json.dumps(line), flush=True)
+    return 1 if parity is not None and not parity["ok"] else 0
+
+
+# event bytes the unit-statistics kernels read per event: key + phase + dur
+# while placing the durations, the duration in each select round
+STATS_METHOD_BYTES = {"stats_scatter": 13}
+STATS_Q = (50000, 99000)
+
+
+def bench_stats(args) -> int:
+    """Observed runtime per unit (§3.1, the deployment baseline): a step is the
+    device-time group-by of a profile's invocations and the per-unit count,
+    total, mean, min, max, median and p99 (atrex_unit_stats), units = keys
+    with their phases merged."""
+    import numpy as np
+    import torch
+    from paper_2607_14541_amd import atrex as X
+    from paper_2607_14541_amd import synth
+
+    ci = 1 if args.config is None else args.config
+    cfg = synth.SHARE_CONFIGS[ci]
+    n = cfg["n"]
+    steps = args.steps if args.steps is not None else SHARE_DEFAULT_STEPS[ci] // 2
+    units = synth.profile_units(cfg)
+    K = units.size
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log("unit statistics, profile", ci, cfg["name"])
+    p = synth.profile(cfg)
+    d_key = torch.from_numpy(p["key"].view(np.int32)).to(dev)
+    d_ph = torch.from_numpy(p["is_dsl"]).to(dev)
+    d_dur = torch.from_numpy(p["dur_ns"]).to(dev)
+    torch.cuda.synchronize()
+
+    def make(timing: bool):
+        return X.Aggregator(2, None, max_events=n, max_keys=K, max_groups=2 * K, path=args.path, timing=timing,
+                            device_time=True)
+
+    ag = make(False)
+    sbuf = ag.stats_buffers(2 * K, len(STATS_Q))
+    res = {}
+
+    def step(a):
+        a.reset()
+        a.aggregate(d_key, None, d_ph, d_dur)
+        res["r"] = a.unit_stats(d_key, d_ph, d_dur, q_1e5=STATS_Q, by_phase=False, out=sbuf)
+
+    for _ in range(args.warmup):
+        step(ag)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step(ag)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_step = 1e3 * elapsed / steps
+    value = n * steps / elapsed / 1e9
+    log("step %.3f ms, %.2f G invocations/s, path %s" % (ms_step, value, ag.path_used()))
+    parity, cpu = None, None
+    if not args.no_parity:
+        from oracle import oracle as O  # the checker
+        o = O.unit_stats(p["key"], p["is_dsl"], p["dur_ns"], 2, q_1e5=STATS_Q, by_phase=False)
+        r = res["r"]
+        bad = [k for k, a, b in (
+            ("key", r["key"].cpu().numpy().view(np.uint32), o["key"]),
+            ("count", r["count"].cpu().numpy().view(np.uint64), o["count"]),
+            ("total_ns", r["total_ns"].cpu().numpy().view(np.uint64), o["total_ns"]),
+            ("mean_ns", r["mean_ns"].cpu().numpy().view(np.uint64), o["mean_ns"].view(np.uint64)),
+            ("min_ns", r["min_ns"].cpu().numpy(), o["min_ns"]), ("max_ns", r["max_ns"].cpu().numpy(), o["max_ns"]),
+            ("quantile_ns", r["quantile_ns"].cpu().numpy(), o["quantile_ns"])) if not np.array_equal(a, b)]
+        parity = {"checked": True, "against": "CPU oracle on the same profile, every output", "ok": not bad,
+                  "mismatch": bad}
+        log("parity", "ok" if not bad else "MISMATCH %s" % bad)
+    agt = make(True)
+    runs = []
+    for _ in range(5):
+        agt.reset()
+        agt.aggregate(d_key, None, d_ph, d_dur)
+        t = agt.kernel_times()
+        agt.unit_stats(d_key, d_ph, d_dur, q_1e5=STATS_Q, by_phase=False, out=sbuf)
+        runs.append(t + agt.kernel_times())
+    agt.close()
+    kernels = kernel_averages(runs)
+    dom = "stats_scatter"
+    alg = STATS_METHOD_BYTES[dom] * n
+    achieved = alg / (kernels[dom]["avg_ms"] * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "algorithmic_bytes_per_launch": alg, "avg_launch_ms": round(kernels[dom]["avg_ms"], 4),
+                "select_rounds_ms": round(kernels.get("stats_select", {}).get("avg_ms", 0.0), 4)}
+    log("kernels", json.dumps({k: round(v["avg_ms"], 4) for k, v in kernels.items()}))
+    if not args.no_cpu_baseline:
+        from oracle import oracle as O
+        m = min(n, 1 << 24)
+        tc = time.perf_counter()
+        O.unit_stats(p["key"][:m], p["is_dsl"][:m], p["dur_ns"][:m], 2, q_1e5=STATS_Q, by_phase=False)
+        dt = time.perf_counter() - tc
+        cpu = {"value": round(m / dt / 1e9, 6), "unit": "G invocations/s", "cores": 1, "kind": "oracle",
+               "sample": "first %d invocations of the same profile, one thread (%.1f s)" % (m, dt),
+               "nproc": os.cpu_count(), "cpu_model": cpu_model()}
+    line = {
+        "metric": "profile kernel invocations summarised into per-unit runtime statistics per second",
+        "value": round(value, 3), "unit": "G invocations/s", "n_gpus": 1, "steps": steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "int64+u128", "data": "synthetic",
+        "config": {"workload": cfg["name"], "invocations": n, "units": int(K), "quantiles_1e5": list(STATS_Q),
+                   "seed": cfg["seed"], "path": ag.path_used(), "parallelism": "none",
+                   "entry": "atrex_aggregate_events + atrex_unit_stats"},
+        "kernels_ms": {k: round(v["avg_ms"], 4) for k, v in kernels.items()},
+        "parity": parity, "roofline": roofline, "cpu_baseline": cpu,
+    }
+    ag.close()
+    print(json.dumps(line), flush=True)
+    return 1 if parity is not None and not parity["ok"] else 0
+
+
+# bytes the correlation join must move per kernel record (corr 8, anchor 8,
+# stream 4, start 8, end 8 read) and per labelled event (key 4, app 4,
+# phase 1, dur 8 written); host records (kind 1, id 8, key 4, app 4, phase 1)
+# are read once
+JOIN_READ_PER_KERNEL, JOIN_WRITE_PER_EVENT, JOIN_READ_PER_HOST = 36, 17, 18
+JOIN_DEFAULT_STEPS = {0: 100, 1: 20}
+
+
+def bench_join(args) -> int:
+    """Host/device correlation join (§3.1): a step labels one trace's device
+    kernel records from its host records (correlation ids, graph anchors,
+    stream intervals) and writes the labelled events (atrex_correlate)."""
+    import numpy as np
+    import torch
+    from paper_2607_14541_amd import atrex as X
+    from paper_2607_14541_amd import synth
+
+    ci = 1 if args.config is None else args.config
+    jc = synth.JOIN_CONFIGS[ci]
+    steps = args.steps if args.steps is not None else JOIN_DEFAULT_STEPS[ci]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log("correlation join", ci, jc["name"])
+    t = time.time()
+    tr = synth.join_trace(jc)
+    log("generated in %.1fs" % (time.time() - t))
+    n, m, mi = tr["kind"].size, tr["host"]["id"].size, tr["intervals"]["stream"].size
+
+    np_of = {torch.int64: np.int64, torch.int32: np.int32, torch.uint8: np.uint8}
+
+    def up(d, spec):
+        return {f: torch.from_numpy(np.ascontiguousarray(d[f]).view(np_of[dt])).to(dev) for f, dt in spec}
+    k = up(tr["kernels"], X.Correlator.KERNEL_FIELDS)
+    h = up(tr["host"], X.Correlator.HOST_FIELDS)
+    iv = up(tr["intervals"], X.Correlator.INTERVAL_FIELDS)
+    c = X.Correlator(n, m, device=dev)
+    out = c.buffers(n)
+    src = torch.empty(n, dtype=torch.uint8, device=dev)
+    res = {}
+
+    def step():
+        res["r"] = c.run(k, h, iv, out=out, source=src)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record()
+    for _ in range(steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_dev = ev0.elapsed_time(ev1) / steps
+    ms_step = 1e3 * elapsed / steps
+    value = n * steps / elapsed / 1e9
+    r = res["r"]
+    L = r["labelled"]
+    log("step %.3f ms (%.3f ms between hipEvents), %.2f G records/s, labelled %d" % (ms_step, ms_dev, value, L))
+    parity = None
+    if not args.no_parity:
+        msk = tr["kind"] < 3
+        bad = [f for f, a, b in (("source", r["source"].cpu().numpy(), tr["kind"]),
+                                 ("key", r["key"].cpu().numpy().view(np.uint32), tr["truth"]["key"][msk]),
+                                 ("app", r["app"].cpu().numpy().view(np.uint32), tr["truth"]["app"][msk]),
+                                 ("phase", r["phase"].cpu().numpy(), tr["truth"]["phase"][msk]),
+                                 ("dur_ns", r["dur_ns"].cpu().numpy(), tr["truth"]["dur_ns"][msk]))
+               if not np.array_equal(a, b)]
+        parity = {"checked": True, "against": "the labelled events the records were built from (the oracle "
+                  "recovers them exactly at the sizes its tests run)", "ok": not bad, "mismatch": bad}
+        log("parity", "ok" if not bad else "MISMATCH %s" % bad)
+    alg = JOIN_READ_PER_KERNEL * n + JOIN_WRITE_PER_EVENT * L + JOIN_READ_PER_HOST * m
+    achieved = alg / (ms_dev * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "kernel": "atrex_correlate (build, probe, scan, emit)", "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "algorithmic_bytes_per_launch": alg, "avg_launch_ms": round(ms_dev, 4)}
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import oracle as O  # the CPU baseline leg: the oracle as it stands
+        sub = synth.join_trace(jc, n=1 << 21)
+        tc = time.perf_counter()
+        O.correlate(sub["kernels"], sub["host"], sub["intervals"])
+        dt = time.perf_counter() - tc
+        cpu = {"value": round((1 << 21) / dt / 1e9, 6), "unit": "G records/s", "cores": 1, "kind": "oracle",
+               "sample": "a 2097152-record trace of the same recipe, one thread (%.1f s)" % dt,
+               "nproc": os.cpu_count(), "cpu_model": cpu_model()}
+    line = {
+        "metric": "device kernel records labelled by the host/device correlation join per second",
+        "value": round(value, 3), "unit": "G records/s", "n_gpus": 1, "steps": steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "u64 ids", "data": "synthetic",
+        "config": {"workload": jc["name"], "kernel_records": n, "host_records": m, "intervals": mi,
+                   "streams": jc["streams"], "seed": jc["seed"], "parallelism": "none", "entry": "atrex_correlate"},
+        "labelled": L, "by_source": r["by_source"], "ms_between_events": round(ms_dev, 4),
+        "parity": parity, "roofline": roofline, "cpu_baseline": cpu,
+    }
     print(json.dumps(line), flush=True)
     return 1 if parity is not None and not parity["ok"] else 0
 
@@ -384,9 +607,10 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=None, help="workload index (0..4); default 3 = 1B events")
-    ap.add_argument("--row", default="weights", choices=["weights", "share", "refresh"],
+    ap.add_argument("--row", default="weights", choices=["weights", "share", "refresh", "stats", "join"],
                     help="weights: the importance-weight path (default); share: the target-DSL share; "
-                         "refresh: an incremental refresh of an append-only log")
+                         "refresh: an incremental refresh of an append-only log; stats: runtime statistics per unit; "
+                         "join: the host/device correlation join")
     ap.add_argument("--path", default="auto", choices=["auto", "lds_hash", "global_hash", "radix_sort"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true")
@@ -399,6 +623,10 @@ def main() -> int:
         return bench_share(args)
     if args.row == "refresh":
         return bench_refresh(args)
+    if args.row == "stats":
+        return bench_stats(args)
+    if args.row == "join":
+        return bench_join(args)
     if args.config is None:
         args.config = 3
     steps = args.steps if args.steps is not None else DEFAULT_STEPS[args.config]

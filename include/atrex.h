@@ -237,6 +237,113 @@ atrex_status atrex_refresh(atrex_ctx *ctx, const atrex_events *log, uint64_t n_n
 atrex_status atrex_refresh_state(atrex_ctx *ctx, atrex_u128 *T, uint64_t *n, uint64_t *n_folded);
 atrex_status atrex_refresh_restore(atrex_ctx *ctx, const atrex_u128 *T, const uint64_t *n, uint64_t n_folded);
 
+/* ---- Observed runtime per unit (§3.1, "Baselines and weights": the runtime
+ * observed in production for each retained (operator, shape) unit, kept as
+ * its deployment baseline) ----------------------------------------------
+ * Input: a context initialised with ATREX_FLAG_DEVICE_TIME whose
+ * atrex_aggregate_events has run, and the same events again (ev->n must be
+ * the aggregated count; INVALID_ARG when an event's unit is not among the
+ * aggregated groups or the counts differ).  Units: every (key, phase) group
+ * (by_phase != 0) or every key with its phases merged (by_phase = 0),
+ * ascending.  Per unit u (DEVICE outputs of `capacity` rows; quantile_ns is
+ * [capacity][nq]):
+ *   count, total_ns = sum of dur (u128), mean_ns = RN(total) / count,
+ *   min_ns, max_ns, and for each of nq <= 8 quantiles q_1e5[j] in [1, 100000]
+ *   (HOST; q = q_1e5 / 1e5) the nearest-rank value: the duration of rank
+ *   ceil(q count) in ascending order.
+ * phase is 0 for merged units.  CAPACITY when the units exceed capacity
+ * (*num_units still receives their number).  Valid after aggregate_events
+ * (STATE before); leaves the context's state as it is.
+ * HOST: ev (struct of DEVICE pointers), q_1e5, out (struct), num_units. */
+typedef struct {
+  uint32_t *key;
+  uint8_t *phase;
+  uint64_t *count;
+  atrex_u128 *total_ns;
+  double *mean_ns;
+  int64_t *min_ns;
+  int64_t *max_ns;
+  int64_t *quantile_ns;
+} atrex_stats_out;
+
+atrex_status atrex_unit_stats(atrex_ctx *ctx, const atrex_events *ev, int by_phase, const uint32_t *q_1e5,
+                              uint32_t nq, const atrex_stats_out *out, uint64_t capacity, uint64_t *num_units);
+
+/* ---- Host/device correlation join (§3.1: the tracer matches host events --
+ * the framework operation, its shape and serving phase from the Python frame
+ * -- with device kernel records through correlation ids when available, and
+ * through graph anchors or timestamps otherwise) --------------------------
+ * Each kernel record takes, in this order: the label of the host launch
+ * record with its correlation id (corr != 0); else of the host graph record
+ * with its anchor (anchor != 0); else of the interval record on its stream
+ * whose [begin, end) contains its start; else none.  Labelled records become
+ * events (key, app, phase, dur = end - start) in kernel-record order: the
+ * input of atrex_aggregate_events.  Context-free; all work on p->stream, which
+ * the call synchronises.
+ * Errors: INVALID_ARG for a host record of kind > 1, id 0 or an id repeated
+ * within its kind, for intervals that are not ascending by (stream, begin),
+ * have end < begin or overlap on a stream, and for bad parameters;
+ * OUT_OF_RANGE for a kernel record with end < start; CAPACITY when n exceeds
+ * the capacities, the workspace is too small, or more records are labelled
+ * than out_capacity (r still receives the counts). */
+typedef struct {            /* DEVICE, read only */
+  const uint64_t *corr;     /* [n] correlation id of the launch, 0 = none */
+  const uint64_t *anchor;   /* [n] graph anchor, 0 = none */
+  const uint32_t *stream;   /* [n] */
+  const int64_t *start_ns;  /* [n] device timestamps */
+  const int64_t *end_ns;    /* [n] */
+  uint64_t n;
+} atrex_kernel_records;
+
+typedef struct {            /* DEVICE, read only */
+  const uint8_t *kind;      /* [n] 0 = launch (id is its correlation id), 1 = graph (id is its anchor) */
+  const uint64_t *id;       /* [n] nonzero, unique within its kind */
+  const uint32_t *key;      /* [n] labels: op << 16 | shape, app, serving phase */
+  const uint32_t *app;
+  const uint8_t *phase;
+  uint64_t n;
+} atrex_host_records;
+
+typedef struct {            /* DEVICE, read only; ascending by (stream, begin_ns) */
+  const uint32_t *stream;
+  const int64_t *begin_ns;  /* [n] on the device timeline */
+  const int64_t *end_ns;    /* [n] exclusive */
+  const uint32_t *key;
+  const uint32_t *app;
+  const uint8_t *phase;
+  uint64_t n;
+} atrex_interval_records;
+
+typedef struct {            /* DEVICE outputs, out_capacity rows */
+  uint32_t *key;
+  uint32_t *app;
+  uint8_t *phase;
+  int64_t *dur_ns;
+} atrex_event_out;
+
+typedef struct {
+  uint64_t max_kernels;     /* kernel records per call, < 2^31 */
+  uint64_t max_host;        /* host records per call, < 2^31 */
+  void *workspace;          /* DEVICE, caller-owned, 256-byte aligned */
+  size_t workspace_bytes;
+  void *stream;             /* hipStream_t; NULL = default stream */
+} atrex_join_params;
+
+typedef struct {
+  uint64_t labelled;        /* events written (or wanted, on CAPACITY) */
+  uint64_t by_source[4];    /* kernel records labelled by correlation id, by anchor, by interval; unlabelled */
+} atrex_join_result;
+
+/* Workspace size for p (workspace fields ignored).  HOST: p, bytes. */
+atrex_status atrex_join_workspace_bytes(const atrex_join_params *p, size_t *bytes);
+
+/* HOST: p, k, h, iv (nullable: no intervals), out (structs of DEVICE
+ * pointers), r.  source (DEVICE [k->n], nullable): per kernel record 0, 1, 2
+ * or 3 as above. */
+atrex_status atrex_correlate(const atrex_join_params *p, const atrex_kernel_records *k, const atrex_host_records *h,
+                             const atrex_interval_records *iv, const atrex_event_out *out, uint64_t out_capacity,
+                             uint8_t *source, atrex_join_result *r);
+
 /* ---- Target-DSL device-time share (§4.1, Metrics: "FlyDSL adoption") -------
  * Input: a context initialised with ATREX_FLAG_DEVICE_TIME and num_phases = 2
  * whose atrex_aggregate_events has run on one profile's kernel invocations,

@@ -62,6 +62,42 @@ class _ShareOut(ctypes.Structure):
                 ("op_shapes", ctypes.c_void_p), ("op_share", ctypes.c_void_p)]
 
 
+class _StatsOut(ctypes.Structure):
+    _fields_ = [("key", ctypes.c_void_p), ("phase", ctypes.c_void_p), ("count", ctypes.c_void_p),
+                ("total_ns", ctypes.c_void_p), ("mean_ns", ctypes.c_void_p), ("min_ns", ctypes.c_void_p),
+                ("max_ns", ctypes.c_void_p), ("quantile_ns", ctypes.c_void_p)]
+
+
+class _KernelRecords(ctypes.Structure):
+    _fields_ = [("corr", ctypes.c_void_p), ("anchor", ctypes.c_void_p), ("stream", ctypes.c_void_p),
+                ("start_ns", ctypes.c_void_p), ("end_ns", ctypes.c_void_p), ("n", ctypes.c_uint64)]
+
+
+class _HostRecords(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_void_p), ("id", ctypes.c_void_p), ("key", ctypes.c_void_p),
+                ("app", ctypes.c_void_p), ("phase", ctypes.c_void_p), ("n", ctypes.c_uint64)]
+
+
+class _IntervalRecords(ctypes.Structure):
+    _fields_ = [("stream", ctypes.c_void_p), ("begin_ns", ctypes.c_void_p), ("end_ns", ctypes.c_void_p),
+                ("key", ctypes.c_void_p), ("app", ctypes.c_void_p), ("phase", ctypes.c_void_p),
+                ("n", ctypes.c_uint64)]
+
+
+class _EventOut(ctypes.Structure):
+    _fields_ = [("key", ctypes.c_void_p), ("app", ctypes.c_void_p), ("phase", ctypes.c_void_p),
+                ("dur_ns", ctypes.c_void_p)]
+
+
+class _JoinParams(ctypes.Structure):
+    _fields_ = [("max_kernels", ctypes.c_uint64), ("max_host", ctypes.c_uint64), ("workspace", ctypes.c_void_p),
+                ("workspace_bytes", ctypes.c_size_t), ("stream", ctypes.c_void_p)]
+
+
+class _JoinResult(ctypes.Structure):
+    _fields_ = [("labelled", ctypes.c_uint64), ("by_source", ctypes.c_uint64 * 4)]
+
+
 class _ShareResult(ctypes.Structure):
     _fields_ = [("num_keys", ctypes.c_uint64), ("num_ops", ctypes.c_uint64), ("defined_ops", ctypes.c_uint64),
                 ("adoption", ctypes.c_double)]
@@ -99,6 +135,12 @@ def _lib() -> ctypes.CDLL:
             "atrex_get_app_totals": [P, P, P, P, P],
             "atrex_target_share": [P, ctypes.POINTER(_ShareOut), U64, U64, ctypes.POINTER(_ShareResult)],
             "atrex_refresh": [P, ctypes.POINTER(_Events), U64, ctypes.POINTER(U64)],
+            "atrex_join_workspace_bytes": [ctypes.POINTER(_JoinParams), ctypes.POINTER(ctypes.c_size_t)],
+            "atrex_correlate": [ctypes.POINTER(_JoinParams), ctypes.POINTER(_KernelRecords),
+                                ctypes.POINTER(_HostRecords), ctypes.POINTER(_IntervalRecords),
+                                ctypes.POINTER(_EventOut), U64, P, ctypes.POINTER(_JoinResult)],
+            "atrex_unit_stats": [P, ctypes.POINTER(_Events), I, P, ctypes.c_uint32, ctypes.POINTER(_StatsOut), U64,
+                                 ctypes.POINTER(U64)],
             "atrex_refresh_state": [P, P, P, ctypes.POINTER(U64)],
             "atrex_refresh_restore": [P, P, P, U64],
             "atrex_kernel_times": [P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float),
@@ -441,6 +483,47 @@ class Aggregator:
         res.update(adoption=r.adoption, defined_ops=r.defined_ops, num_keys=K, num_ops=I)
         return res
 
+    # -- observed runtime per unit (§3.1, the deployment baseline) ----------------------
+    def stats_buffers(self, capacity: int, nq: int) -> dict:
+        """Output tensors for unit_stats()."""
+        dev, c = self.device, max(int(capacity), 1)
+        return dict(key=torch.empty(c, dtype=torch.int32, device=dev),
+                    phase=torch.empty(c, dtype=torch.uint8, device=dev),
+                    count=torch.empty(c, dtype=torch.int64, device=dev),
+                    total_ns=torch.empty((c, 2), dtype=torch.int64, device=dev),
+                    mean_ns=torch.empty(c, dtype=torch.float64, device=dev),
+                    min_ns=torch.empty(c, dtype=torch.int64, device=dev),
+                    max_ns=torch.empty(c, dtype=torch.int64, device=dev),
+                    quantile_ns=torch.empty((c, max(nq, 1)), dtype=torch.int64, device=dev))
+
+    def unit_stats(self, key: torch.Tensor, phase: torch.Tensor, dur_ns: torch.Tensor, q_1e5=(50000, 99000),
+                   by_phase: bool = True, capacity: int | None = None, out: dict | None = None) -> dict:
+        """Count, total, mean, min, max and nearest-rank quantiles (q in 1e-5
+        steps) of the durations of every unit, after aggregate() on the same
+        events (device_time=True).  Capacity defaults to the group count."""
+        key = _dev(_as_i32(key), torch.int32, "key")
+        phase = _dev(phase, torch.uint8, "phase")
+        dur_ns = _dev(dur_ns, torch.int64, "dur_ns")
+        n = key.numel()
+        if not (phase.numel() == n and dur_ns.numel() == n):
+            raise ValueError("event arrays differ in length")
+        q = (ctypes.c_uint32 * 8)(*[int(x) for x in q_1e5])
+        nq = len(q_1e5)
+        if out is None:
+            out = self.stats_buffers((self.num_groups or 0) if capacity is None else capacity, nq)
+        cap = out["key"].numel() if capacity is None else int(capacity)
+        so = _StatsOut(*(_ptr(out[k]) for k in ("key", "phase", "count", "total_ns", "mean_ns", "min_ns", "max_ns",
+                                                 "quantile_ns")))
+        ev = _Events(_ptr(key), None, _ptr(phase), _ptr(dur_ns), n)
+        U = ctypes.c_uint64()
+        _check(_lib().atrex_unit_stats(self._ctx, ctypes.byref(ev), int(bool(by_phase)), q, nq, ctypes.byref(so), cap,
+                                       ctypes.byref(U)), "atrex_unit_stats")
+        u = U.value
+        res = {k: v[:u] for k, v in out.items()}
+        res["quantile_ns"] = out["quantile_ns"][:u, :nq]
+        res["num_units"] = u
+        return res
+
     def kernel_times(self) -> list:
         cap = 64
         names = (ctypes.c_char_p * cap)()
@@ -504,6 +587,88 @@ def target_share(key, is_dsl, dur_ns, path="auto", max_keys=0) -> dict:
         return out
     finally:
         ag.close()
+
+
+def unit_stats(key, phase, dur_ns, num_phases, q_1e5=(50000, 99000), by_phase=True, path="auto",
+               max_keys=0, max_groups=0) -> dict:
+    """Observed runtime per unit (§3.1) in one call: the device-time group-by
+    of the events, then atrex_unit_stats on the same events."""
+    n = key.numel()
+    ag = Aggregator(num_phases, None, max_events=max(n, 1), max_keys=max_keys, max_groups=max_groups, path=path,
+                    device_time=True, device=key.device)
+    try:
+        ag.aggregate(key, None, phase, dur_ns)
+        out = ag.unit_stats(key, phase, dur_ns, q_1e5=q_1e5, by_phase=by_phase)
+        out["path"] = ag.path_used()
+        return out
+    finally:
+        ag.close()
+
+
+class Correlator:
+    """Host/device correlation join (§3.1) with a workspace for up to
+    max_kernels kernel records and max_host host records: run() labels
+    kernel records by correlation id, graph anchor or stream interval and
+    returns the labelled events in kernel-record order."""
+
+    KERNEL_FIELDS = (("corr", torch.int64), ("anchor", torch.int64), ("stream", torch.int32),
+                     ("start_ns", torch.int64), ("end_ns", torch.int64))
+    HOST_FIELDS = (("kind", torch.uint8), ("id", torch.int64), ("key", torch.int32), ("app", torch.int32),
+                   ("phase", torch.uint8))
+    INTERVAL_FIELDS = (("stream", torch.int32), ("begin_ns", torch.int64), ("end_ns", torch.int64),
+                       ("key", torch.int32), ("app", torch.int32), ("phase", torch.uint8))
+
+    def __init__(self, max_kernels: int, max_host: int, device=None, stream: torch.cuda.Stream | None = None):
+        self.device = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        self.p = _JoinParams(int(max_kernels), int(max_host), None, 0, self.stream.cuda_stream)
+        nb = ctypes.c_size_t()
+        _check(_lib().atrex_join_workspace_bytes(ctypes.byref(self.p), ctypes.byref(nb)), "atrex_join_workspace_bytes")
+        self.workspace = torch.empty(max(int(nb.value), 256), dtype=torch.uint8, device=self.device)
+        self.p.workspace, self.p.workspace_bytes = self.workspace.data_ptr(), self.workspace.numel()
+
+    def buffers(self, capacity: int) -> dict:
+        c, dev = max(int(capacity), 1), self.device
+        return dict(key=torch.empty(c, dtype=torch.int32, device=dev), app=torch.empty(c, dtype=torch.int32, device=dev),
+                    phase=torch.empty(c, dtype=torch.uint8, device=dev),
+                    dur_ns=torch.empty(c, dtype=torch.int64, device=dev))
+
+    @staticmethod
+    def _fields(d: dict, spec, name: str) -> tuple:
+        ts = []
+        for f, dt in spec:
+            t = d[f]
+            if dt in (torch.int32, torch.int64) and t.dtype != dt:
+                t = t.view(dt) if t.element_size() == torch.empty(0, dtype=dt).element_size() else t.to(dt)
+            ts.append(_dev(t, dt, name + "." + f))
+        n = ts[0].numel()
+        if any(t.numel() != n for t in ts):
+            raise ValueError(name + " arrays differ in length")
+        return tuple(ts), n
+
+    def run(self, kernels: dict, host: dict, intervals: dict | None = None, out: dict | None = None,
+            source: torch.Tensor | None = None) -> dict:
+        kt, nk = self._fields(kernels, self.KERNEL_FIELDS, "kernels")
+        ht, nh = self._fields(host, self.HOST_FIELDS, "host")
+        kr = _KernelRecords(*(_ptr(t) for t in kt), nk)
+        hr = _HostRecords(*(_ptr(t) for t in ht), nh)
+        ir = None
+        if intervals is not None:
+            it, ni = self._fields(intervals, self.INTERVAL_FIELDS, "intervals")
+            ir = _IntervalRecords(*(_ptr(t) for t in it), ni)
+        if out is None:
+            out = self.buffers(nk)
+        if source is None:
+            source = torch.empty(max(nk, 1), dtype=torch.uint8, device=self.device)
+        eo = _EventOut(*(_ptr(out[k]) for k in ("key", "app", "phase", "dur_ns")))
+        r = _JoinResult()
+        _check(_lib().atrex_correlate(ctypes.byref(self.p), ctypes.byref(kr), ctypes.byref(hr),
+                                      ctypes.byref(ir) if ir is not None else None, ctypes.byref(eo),
+                                      out["key"].numel(), _ptr(source), ctypes.byref(r)), "atrex_correlate")
+        L = r.labelled
+        res = {k: v[:L] for k, v in out.items()}
+        res.update(source=source[:nk], labelled=L, by_source=list(r.by_source))
+        return res
 
 
 def run_noalloc(key, app, phase, dur_ns, app_weight_q16, num_phases, out: dict, score_key=None, s=None,

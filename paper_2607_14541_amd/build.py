@@ -20,7 +20,7 @@ BUILD_DIR = os.path.join(HERE, "_build")
 
 HIP_SOURCES = ["atrex_host.hip", "kernels_aggregate.hip", "kernels_rows.hip", "kernels_util.hip",
                "kernels_normalize.hip", "kernels_small.hip", "kernels_units.hip", "kernels_score.hip",
-               "kernels_share.hip"]
+               "kernels_share.hip", "kernels_stats.hip", "kernels_join.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 HIP_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17",

@@ -28,6 +28,8 @@ constexpr uint64_t kMaxWG = 256;            // persistent workgroups of the LDS 
 constexpr uint32_t kMaxBucketBits = 12;     // radix-partition buckets: at most 4096
 constexpr uint32_t kChunk = 1u << 20;       // records per bucket chunk of the partition engine
 constexpr uint32_t kMaxTimed = 64;
+constexpr uint64_t kStatsBatch = 8192;   // large units per radix-select batch
+constexpr uint32_t kStatsTargets = 10;   // up to 8 quantiles, the minimum and the maximum
 constexpr uint32_t kSpillInline = 16384;    // spill records the owner merge takes in
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -41,6 +43,12 @@ uint64_t next_pow2(uint64_t x) {
 struct Layout {
   size_t ctrl, T, carryA, partA, partC, nA, scale, bscale, dict, acc, raw;
   size_t T_run, n_run;  // incremental refresh: totals of the events folded so far
+  // observed runtime per unit (device-time contexts): unit counts and
+  // segment starts, write cursors, lookup table, size-class lists, radix
+  // select state of one batch of large units
+  size_t st_cnt, st_start, st_cur, st_hkey, st_hval, st_tiny, st_small, st_large, st_cstart, st_prefix, st_want,
+      st_hist, st_mat;
+  uint64_t st_cap;  // lookup-table capacity (a power of two)
   size_t okey, oacc, oraw, ocount, skey, sval, sraw, scount;  // LDS engine outputs
   size_t ol_rk, ol_key, ol_lo, ol_hi, ol_rlo, ol_rhi, ol_count, ol_part;  // per-owner sorted lists
   size_t H, O, rec, rraw, bstart, istart;                     // partition engine
@@ -128,6 +136,23 @@ Layout make_layout(const Params& p) {
   L.bscale = take(GA * 8);
   L.T_run = take(p.incr ? GA * 16 : 0);
   L.n_run = take(p.incr ? GA * 8 : 0);
+  {
+    const uint64_t U = p.time ? L.maxG : 0, B = p.time ? kStatsBatch : 0;
+    L.st_cap = next_pow2(std::max<uint64_t>(1024, 2 * U));
+    L.st_cnt = take((U + 1) * 4);
+    L.st_start = take((U + 1) * 4);
+    L.st_cur = take(U * 4);
+    L.st_hkey = take(p.time ? L.st_cap * 8 : 0);
+    L.st_hval = take(p.time ? L.st_cap * 4 : 0);
+    L.st_tiny = take(U * 4);
+    L.st_small = take(U * 4);
+    L.st_large = take(U * 4);
+    L.st_cstart = take((B + 1) * 4);
+    L.st_prefix = take(B * kStatsTargets * 8);
+    L.st_want = take(B * kStatsTargets * 4);
+    L.st_hist = take(B * kStatsTargets * 256 * 4);
+    L.st_mat = take(std::min<uint64_t>(U, stats_dense_units()) * kMaxWG * 4);
+  }
   L.dict = take(L.capD * 8);
   L.acc = take(L.capD * p.P * 16);
   L.raw = take(p.raw ? L.capD * p.P * 16 : 0);
@@ -169,7 +194,8 @@ Layout make_layout(const Params& p) {
     L.sv[i] = take(L.maxSort * 4);
   }
   L.rs_tmp = take(radix_sort_tmp_bytes(L.maxSort));
-  L.scan_tmp = take(std::max(scan_tmp_bytes(L.maxSort + 1), scan_tmp_bytes(hsz)));
+  L.scan_tmp = take(std::max(std::max(scan_tmp_bytes(L.maxSort + 1), scan_tmp_bytes(hsz)),
+                             p.time ? scan_tmp_bytes(std::min<uint64_t>(L.maxG, stats_dense_units()) * kMaxWG) : 0));
   L.g_key = take(L.maxG * 4);
   L.g_ph = take(L.maxG);
   L.g_cnt = take(L.maxG * 8);
@@ -269,6 +295,7 @@ struct atrex_ctx {
   bool S_ready;  // the per-phase totals S were written by the ordering step
   uint64_t G, nops, nkeys;
   uint64_t n_folded;  // incremental refresh: events whose totals are in T_run / n_run
+  uint64_t n_agg;     // events of the last successful group-by
   int cus;
   const char* path_used;
   std::vector<Timed> timed;
@@ -896,6 +923,7 @@ atrex_status aggregate_complete(atrex_ctx* c, AggRun* a, uint64_t* num_groups, b
     if (st != ATREX_OK) return st;
   }
   if (G > L.maxG) return ATREX_E_CAPACITY;
+  c->n_agg = n;
   if (c->p.incr) {  // the refresh stands: the totals of the whole log become the folded ones
     const uint64_t GA = (uint64_t)c->p.A * c->p.P;
     launch_copy_u64(s, c->at<uint64_t>(L.T_run), c->at<uint64_t>(L.T), 2 * GA);
@@ -1327,6 +1355,208 @@ atrex_status atrex_refresh_restore(atrex_ctx* c, const atrex_u128* T, const uint
   const atrex_status st = sync_read(c);
   if (st == ATREX_OK) c->n_folded = n_folded;
   return st;
+}
+
+atrex_status atrex_unit_stats(atrex_ctx* c, const atrex_events* ev, int by_phase, const uint32_t* q_1e5, uint32_t nq,
+                              const atrex_stats_out* out, uint64_t capacity, uint64_t* num_units) {
+  if (!c || !ev || !out || !num_units || nq > 8 || (nq && !q_1e5)) return ATREX_E_INVALID_ARG;
+  if (!c->p.time) return ATREX_E_INVALID_ARG;
+  if (c->state < 1) return ATREX_E_STATE;
+  if (ev->app || ev->n != c->n_agg || (ev->n && (!ev->key || !ev->phase || !ev->dur_ns))) return ATREX_E_INVALID_ARG;
+  if (capacity && (!out->key || !out->phase || !out->count || !out->total_ns || !out->mean_ns || !out->min_ns ||
+                   !out->max_ns || (nq && !out->quantile_ns)))
+    return ATREX_E_INVALID_ARG;
+  StatsQ q{};
+  for (uint32_t j = 0; j < nq; ++j) {
+    if (q_1e5[j] < 1 || q_1e5[j] > 100000) return ATREX_E_INVALID_ARG;
+    q.q[j] = q_1e5[j];
+  }
+  q.n = nq;
+  const Layout& L = c->L;
+  hipStream_t s = c->s;
+  const uint64_t G = c->G, n = ev->n;
+  StatsOut so;
+  so.key = out->key;
+  so.phase = out->phase;
+  so.count = out->count;
+  so.total = (uint64_t*)out->total_ns;
+  so.mean = out->mean_ns;
+  so.min = out->min_ns;
+  so.max = out->max_ns;
+  so.quant = out->quantile_ns;
+  StatsTable t;
+  t.key = c->at<uint64_t>(L.st_hkey);
+  t.val = c->at<uint32_t>(L.st_hval);
+  t.mask = (uint32_t)(L.st_cap - 1);
+  unsigned long long* words = c->at<unsigned long long>(L.ctrl + 2048);
+  uint32_t* ucount = c->at<uint32_t>(L.st_cnt);
+  uint32_t* seg = c->at<uint32_t>(L.st_start);
+  int64_t* vals = c->at<int64_t>(L.rec);
+  c->begin_call();
+  launch_fill_u64(s, (uint64_t*)words, 8, 0);
+  launch_fill_u32(s, c->err(), 1, 0);
+  launch_fill_u64(s, t.key, L.st_cap, 0);
+  launch_fill_u32(s, ucount, G + 1, 0);  // G + 1 counts (the scan's last entry is the total)
+  // units, their counts and totals, the lookup table; segment starts
+  TIMED(c, "stats_units", G,
+        launch_stats_units(s, c->groups(), G, by_phase != 0, c->at<uint32_t>(L.flags), c->at<uint32_t>(L.scan),
+                           c->at<void>(L.scan_tmp), so, capacity, ucount, t, words));
+  exclusive_scan_u32(s, ucount, seg, G + 1, c->at<void>(L.scan_tmp));
+  uint64_t w0 = 0;
+  d2h(c, &w0, words, 8);
+  atrex_status st = sync_read(c);
+  if (st != ATREX_OK) return st;
+  const uint64_t U = w0;
+  EventsDev d;
+  d.key = ev->key;
+  d.app = nullptr;
+  d.phase = ev->phase;
+  d.dur = ev->dur_ns;
+  d.n = n;
+  const bool vec = aligned(ev->key, 16) && aligned(ev->phase, 4) && aligned(ev->dur_ns, 16);
+  const uint32_t nwg = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)c->cus, kMaxWG));
+  if (U <= stats_dense_units()) {  // per-workgroup LDS counters: two passes, no global atomics
+    TIMED(c, "stats_scatter", n,
+          launch_stats_dense(s, d, c->p.P, by_phase != 0, vec, nwg, t, (uint32_t)U, c->at<uint32_t>(L.st_mat),
+                             c->at<void>(L.scan_tmp), seg, vals, words, c->err()));
+  } else {
+    launch_copy_u32(s, c->at<uint32_t>(L.st_cur), seg, U);
+    TIMED(c, "stats_scatter", n,
+          launch_stats_scatter(s, d, c->p.P, by_phase != 0, vec, nwg, t, seg, c->at<uint32_t>(L.st_cur), vals, words,
+                               c->err()));
+  }
+  uint32_t* tiny = c->at<uint32_t>(L.st_tiny);
+  uint32_t* small = c->at<uint32_t>(L.st_small);
+  uint32_t* large = c->at<uint32_t>(L.st_large);
+  launch_stats_classify(s, ucount, U, tiny, small, large, words);
+  uint64_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  uint32_t e = 0;
+  d2h(c, w, words, sizeof(w));
+  d2h(c, &e, c->err(), 4);
+  st = sync_read(c);
+  if (st != ATREX_OK) return st;
+  if (e & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
+  if (e & ATREX_ERRBIT_CAPACITY) return ATREX_E_INVALID_ARG;  // not the events that were aggregated
+  const uint64_t vmax = w[1], ntiny = w[2], nsmall = w[3], nlarge = w[4];
+  TIMED(c, "stats_sorts", ntiny + nsmall, launch_stats_sorts(s, tiny, ntiny, small, nsmall, seg, vals, q, so, capacity));
+  if (nlarge) {
+    int bits = 0;
+    while (bits < 64 && (vmax >> bits)) ++bits;
+    const int rounds = std::max(1, (bits + 7) / 8);
+    const uint32_t T = nq + 2;
+    uint32_t* cstart = c->at<uint32_t>(L.st_cstart);
+    uint64_t* prefix = c->at<uint64_t>(L.st_prefix);
+    uint32_t* want = c->at<uint32_t>(L.st_want);
+    uint32_t* hist = c->at<uint32_t>(L.st_hist);
+    for (uint64_t b0 = 0; b0 < nlarge; b0 += kStatsBatch) {
+      const uint32_t nb = (uint32_t)std::min<uint64_t>(kStatsBatch, nlarge - b0);
+      launch_fill_u32(s, cstart, nb + 1, 0);
+      launch_select_init(s, large + b0, nb, seg, q, prefix, want, cstart);
+      exclusive_scan_u32(s, cstart, cstart, nb + 1, c->at<void>(L.scan_tmp));
+      uint32_t nchunks = 0;
+      d2h(c, &nchunks, cstart + nb, 4);
+      st = sync_read(c);
+      if (st != ATREX_OK) return st;
+      for (int r = 0; r < rounds; ++r)
+        TIMED(c, "stats_select", nchunks,
+              launch_select_round(s, large + b0, nb, cstart, nchunks, seg, vals, T, 8 * (rounds - 1 - r), prefix,
+                                  want, hist));
+      launch_select_out(s, large + b0, nb, q, prefix, so, capacity);
+    }
+  }
+  st = sync_read(c);
+  c->end_call();
+  if (st != ATREX_OK) return st;
+  *num_units = U;
+  return U > capacity ? ATREX_E_CAPACITY : ATREX_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Host/device correlation join.
+namespace {
+struct JoinLayout {
+  size_t ctrl, slot0, slot1, ref, flag, pos, scan_tmp, bytes;
+  uint64_t cap;
+};
+
+bool join_params_ok(const atrex_join_params* p) {
+  return p && p->max_kernels < (1ull << 31) && p->max_host < (1ull << 31);
+}
+
+JoinLayout join_layout(const atrex_join_params* p) {
+  JoinLayout L;
+  size_t off = 0;
+  auto take = [&](size_t b) {
+    const size_t at = off;
+    off += align_up(b ? b : 1);
+    return at;
+  };
+  const uint64_t nk = std::max<uint64_t>(p->max_kernels, 1);
+  L.cap = next_pow2(std::max<uint64_t>(1024, 2 * p->max_host));
+  L.ctrl = take(256);
+  L.slot0 = take(L.cap * 16);
+  L.slot1 = take(L.cap * 16);
+  L.ref = take(nk * 4);
+  L.flag = take(nk * 4);
+  L.pos = take(nk * 4);
+  L.scan_tmp = take(scan_tmp_bytes(nk));
+  L.bytes = off;
+  return L;
+}
+}  // namespace
+
+atrex_status atrex_join_workspace_bytes(const atrex_join_params* p, size_t* bytes) {
+  if (!join_params_ok(p) || !bytes) return ATREX_E_INVALID_ARG;
+  *bytes = join_layout(p).bytes;
+  return ATREX_OK;
+}
+
+atrex_status atrex_correlate(const atrex_join_params* p, const atrex_kernel_records* k, const atrex_host_records* h,
+                             const atrex_interval_records* iv, const atrex_event_out* out, uint64_t out_capacity,
+                             uint8_t* source, atrex_join_result* r) {
+  if (!join_params_ok(p) || !k || !h || !out || !r || !p->workspace || !aligned(p->workspace, kAlign))
+    return ATREX_E_INVALID_ARG;
+  *r = atrex_join_result{};
+  const JoinLayout L = join_layout(p);
+  if (p->workspace_bytes < L.bytes || k->n > p->max_kernels || h->n > p->max_host) return ATREX_E_CAPACITY;
+  if (k->n && (!k->corr || !k->anchor || !k->stream || !k->start_ns || !k->end_ns)) return ATREX_E_INVALID_ARG;
+  if (h->n && (!h->kind || !h->id || !h->key || !h->app || !h->phase)) return ATREX_E_INVALID_ARG;
+  const uint64_t ni = iv ? iv->n : 0;
+  if (ni >= (1ull << 31)) return ATREX_E_INVALID_ARG;
+  if (ni && (!iv->stream || !iv->begin_ns || !iv->end_ns || !iv->key || !iv->app || !iv->phase))
+    return ATREX_E_INVALID_ARG;
+  if (out_capacity && (!out->key || !out->app || !out->phase || !out->dur_ns)) return ATREX_E_INVALID_ARG;
+  char* ws = (char*)p->workspace;
+  hipStream_t s = (hipStream_t)p->stream;
+  JoinKernels jk{k->corr, k->anchor, k->stream, k->start_ns, k->end_ns, k->n};
+  JoinHost jh{h->kind, h->id, h->key, h->app, h->phase, h->n};
+  JoinIntervals ji{};
+  if (ni) ji = JoinIntervals{iv->stream, iv->begin_ns, iv->end_ns, iv->key, iv->app, iv->phase, ni};
+  JoinTables t{(uint64_t*)(ws + L.slot0), (uint64_t*)(ws + L.slot1), (uint32_t)(L.cap - 1)};
+  JoinOut jo{out->key, out->app, out->phase, out->dur_ns};
+  uint32_t* err = (uint32_t*)(ws + L.ctrl);
+  unsigned long long* words = (unsigned long long*)(ws + L.ctrl + 64);
+  uint32_t* flag = (uint32_t*)(ws + L.flag);
+  uint32_t* pos = (uint32_t*)(ws + L.pos);
+  launch_fill_u64(s, (uint64_t*)(ws + L.ctrl), 32, 0);
+  launch_join(s, jk, jh, ji, t, source, (uint32_t*)(ws + L.ref), flag, pos, ws + L.scan_tmp, jo, out_capacity, words,
+              err, 0);
+  launch_join(s, jk, jh, ji, t, source, (uint32_t*)(ws + L.ref), flag, pos, ws + L.scan_tmp, jo, out_capacity, words,
+              err, 1);
+  uint32_t e = 0, tail[2] = {0, 0};
+  uint64_t by[4] = {0, 0, 0, 0};
+  (void)hipMemcpyAsync(&e, err, 4, hipMemcpyDeviceToHost, s);
+  (void)hipMemcpyAsync(by, words, sizeof(by), hipMemcpyDeviceToHost, s);
+  if (k->n) {
+    (void)hipMemcpyAsync(&tail[0], pos + (k->n - 1), 4, hipMemcpyDeviceToHost, s);
+    (void)hipMemcpyAsync(&tail[1], flag + (k->n - 1), 4, hipMemcpyDeviceToHost, s);
+  }
+  if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess) return ATREX_E_DEVICE;
+  if (e & ATREX_ERRBIT_DUP) return ATREX_E_INVALID_ARG;
+  if (e & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
+  r->labelled = (uint64_t)tail[0] + tail[1];
+  for (int i = 0; i < 4; ++i) r->by_source[i] = by[i];
+  return r->labelled > out_capacity ? ATREX_E_CAPACITY : ATREX_OK;
 }
 
 atrex_status atrex_target_share(atrex_ctx* c, const atrex_share_out* out, uint64_t key_capacity,

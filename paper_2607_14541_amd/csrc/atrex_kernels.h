@@ -103,6 +103,105 @@ struct ShareOut {
   double* op_share;    // [I]
 };
 
+// Observed runtime per unit (kernels_stats.hip): the unit lookup table
+// (open addressing, key = (key << 3 | phase) + 1, 0 = free), the caller's
+// outputs, and the requested quantiles (1e-5 steps).
+struct StatsTable {
+  uint64_t* key;  // [mask + 1]
+  uint32_t* val;  // [mask + 1] unit index
+  uint32_t mask;
+};
+struct StatsOut {
+  uint32_t* key;
+  uint8_t* phase;
+  uint64_t* count;
+  uint64_t* total;  // [U][2]
+  double* mean;
+  int64_t* min;
+  int64_t* max;
+  int64_t* quant;   // [U][nq]
+};
+struct StatsQ {
+  uint32_t q[8];
+  uint32_t n;
+};
+hipError_t set_stats_smem_limits();
+uint32_t stats_small_max();
+uint32_t stats_sel_chunk();
+// unit heads, unit indices (scan), unit identity / count / total / mean, the
+// per-unit counts and the lookup table; words[0] = number of units
+void launch_stats_units(hipStream_t s, const SortedGroups& g, uint64_t G, bool by_phase, uint32_t* head,
+                        uint32_t* uidx, void* scan_tmp, const StatsOut& out, uint64_t cap, uint32_t* ucount,
+                        const StatsTable& t, unsigned long long* words);
+// durations into their units' blocks; words[1] = the largest duration
+void launch_stats_scatter(hipStream_t s, const EventsDev& ev, uint32_t P, bool by_phase, bool vec, uint32_t nblocks,
+                          const StatsTable& t, const uint32_t* seg_start, uint32_t* cursor, int64_t* vals,
+                          unsigned long long* words, uint32_t* err);
+// the same placement in two passes with per-workgroup LDS counters (U <=
+// stats_dense_units(); mat: U x nblocks counts, scanned in place)
+uint32_t stats_dense_units();
+void launch_stats_dense(hipStream_t s, const EventsDev& ev, uint32_t P, bool by_phase, bool vec, uint32_t nblocks,
+                        const StatsTable& t, uint32_t U, uint32_t* mat, void* scan_tmp, const uint32_t* seg_start,
+                        int64_t* vals, unsigned long long* words, uint32_t* err);
+// units by size into three lists; words[2..4] = their lengths
+void launch_stats_classify(hipStream_t s, const uint32_t* ucount, uint64_t U, uint32_t* tiny, uint32_t* small,
+                           uint32_t* large, unsigned long long* words);
+void launch_stats_sorts(hipStream_t s, const uint32_t* tiny, uint64_t ntiny, const uint32_t* small, uint64_t nsmall,
+                        const uint32_t* seg_start, const int64_t* vals, const StatsQ& q, const StatsOut& out,
+                        uint64_t cap);
+// radix select over a batch of large units: state, chunk counts (into
+// ccount[0..nb), scanned by the caller), rounds, outputs
+void launch_select_init(hipStream_t s, const uint32_t* lu, uint32_t nb, const uint32_t* seg_start, const StatsQ& q,
+                        uint64_t* prefix, uint32_t* want, uint32_t* ccount);
+void launch_select_round(hipStream_t s, const uint32_t* lu, uint32_t nb, const uint32_t* cstart, uint32_t nchunks,
+                         const uint32_t* seg_start, const int64_t* vals, uint32_t T, int shift, uint64_t* prefix,
+                         uint32_t* want, uint32_t* hist);
+void launch_select_out(hipStream_t s, const uint32_t* lu, uint32_t nb, const StatsQ& q, const uint64_t* prefix,
+                       const StatsOut& out, uint64_t cap);
+
+// Host/device correlation join (kernels_join.hip).
+struct JoinKernels {
+  const uint64_t* corr;
+  const uint64_t* anchor;
+  const uint32_t* stream;
+  const int64_t* start;
+  const int64_t* end;
+  uint64_t n;
+};
+struct JoinHost {
+  const uint8_t* kind;
+  const uint64_t* id;
+  const uint32_t* key;
+  const uint32_t* app;
+  const uint8_t* phase;
+  uint64_t n;
+};
+struct JoinIntervals {
+  const uint32_t* stream;
+  const int64_t* begin;
+  const int64_t* end;
+  const uint32_t* key;
+  const uint32_t* app;
+  const uint8_t* phase;
+  uint64_t n;
+};
+struct JoinTables {  // open addressing, 16-byte slots (id, record index), id 0 = free; one table per id space
+  uint64_t* slot0;
+  uint64_t* slot1;
+  uint32_t mask;
+};
+struct JoinOut {
+  uint32_t* key;
+  uint32_t* app;
+  uint8_t* phase;
+  int64_t* dur;
+};
+// stage 0: tables, checks, probe and the scan of the flags (words[0..3]:
+// records per source); stage 1: the labelled events
+void launch_join(hipStream_t s, const JoinKernels& k, const JoinHost& h, const JoinIntervals& iv,
+                 const JoinTables& t, uint8_t* source, uint32_t* ref, uint32_t* flag, uint32_t* pos, void* scan_tmp,
+                 const JoinOut& out, uint64_t cap, unsigned long long* words, uint32_t* err, int stage);
+
 // kernels_share.hip
 hipError_t set_share_smem_limits();
 // per-phase device time and counts of events without applications (global
@@ -190,6 +289,8 @@ void launch_rows_reduce(hipStream_t s, const Rows& rows, const uint64_t* rk_sort
 
 // kernels_util.hip
 void launch_fill_u64(hipStream_t s, uint64_t* p, uint64_t n, uint64_t v);
+void launch_fill_u32(hipStream_t s, uint32_t* p, uint64_t n, uint32_t v);
+void launch_copy_u32(hipStream_t s, uint32_t* dst, const uint32_t* src, uint64_t n);
 // Up to kPublishMax device word ranges copied to a host-mapped buffer (32-bit words).
 constexpr uint32_t kPublishMax = 16;
 struct PublishList {

@@ -1141,6 +1141,8 @@ hipError_t set_kernel_smem_limits() {
   if (e != hipSuccess) return e;
   e = set_share_smem_limits();
   if (e != hipSuccess) return e;
+  e = set_stats_smem_limits();
+  if (e != hipSuccess) return e;
   e = set_units_smem_limits();
   if (e != hipSuccess) return e;
   e = set_normalize_smem_limits();

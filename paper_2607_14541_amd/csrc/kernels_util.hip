@@ -7,6 +7,7 @@
 // tile's earlier items with the same digit comes from eight wave ballots
 // (lanes with an equal digit), per-wave digit counts in LDS, and a running
 // per-digit count carried across rounds.
+#include <algorithm>
 #include "atrex_device.hpp"
 #include "atrex_kernels.h"
 
@@ -20,6 +21,16 @@ constexpr int RS_WAVES = RS_BLOCK / 64;
 constexpr int SC_BLOCK = 256;
 constexpr int SC_ITEMS = 8;
 constexpr int SC_TILE = SC_BLOCK * SC_ITEMS;
+
+__global__ void k_fill_u32(uint32_t* __restrict__ p, uint64_t n, uint32_t v) {
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (uint64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+__global__ void k_copy_u32(uint32_t* __restrict__ dst, const uint32_t* __restrict__ src, uint64_t n) {
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (uint64_t)gridDim.x * blockDim.x)
+    dst[i] = src[i];
+}
 
 __global__ void k_fill_u64(uint64_t* __restrict__ p, uint64_t n, uint64_t v) {
   for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (uint64_t)gridDim.x * blockDim.x)
@@ -195,6 +206,18 @@ void launch_fill_u64(hipStream_t s, uint64_t* p, uint64_t n, uint64_t v) {
   uint64_t nb = cdiv(n, 256);
   if (nb > 8192) nb = 8192;
   hipLaunchKernelGGL(k_fill_u64, dim3((uint32_t)nb), dim3(256), 0, s, p, n, v);
+}
+
+void launch_fill_u32(hipStream_t s, uint32_t* p, uint64_t n, uint32_t v) {
+  if (n == 0) return;
+  const uint64_t nb = std::min<uint64_t>(cdiv(n, 256), 8192);
+  hipLaunchKernelGGL(k_fill_u32, dim3((uint32_t)nb), dim3(256), 0, s, p, n, v);
+}
+
+void launch_copy_u32(hipStream_t s, uint32_t* dst, const uint32_t* src, uint64_t n) {
+  if (n == 0) return;
+  const uint64_t nb = std::min<uint64_t>(cdiv(n, 256), 8192);
+  hipLaunchKernelGGL(k_copy_u32, dim3((uint32_t)nb), dim3(256), 0, s, dst, src, n);
 }
 
 void launch_publish(hipStream_t s, const PublishList& pl, uint32_t* dst, uint32_t* done, uint32_t seq) {

@@ -88,3 +88,14 @@ def test_incremental_flag_validation(lib):
     assert lib.atrex_refresh(None, None, 0, None) == X.E_INVALID_ARG
     assert lib.atrex_refresh_state(None, None, None, None) == X.E_INVALID_ARG
     assert lib.atrex_refresh_restore(None, None, None, 0) == X.E_INVALID_ARG
+    assert lib.atrex_unit_stats(None, None, 0, None, 0, None, 0, None) == X.E_INVALID_ARG
+
+
+def test_join_parameters(lib):
+    from paper_2607_14541_amd import atrex as X
+    p = X._JoinParams(1 << 20, 1 << 20, None, 0, None)
+    b = ctypes.c_size_t()
+    assert lib.atrex_join_workspace_bytes(ctypes.byref(p), ctypes.byref(b)) == 0 and b.value > 0
+    p.max_kernels = 1 << 31
+    assert lib.atrex_join_workspace_bytes(ctypes.byref(p), ctypes.byref(b)) == X.E_INVALID_ARG
+    assert lib.atrex_correlate(None, None, None, None, None, 0, None, None) == X.E_INVALID_ARG
