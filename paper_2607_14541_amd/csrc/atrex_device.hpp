@@ -141,6 +141,13 @@ __device__ __forceinline__ void lds_stage(D* dst, const T* __restrict__ src, uin
 // multiplicative hashing (TAOCP vol. 3, §6.4).
 __device__ __forceinline__ uint32_t hash_mul(uint32_t k) { return k * 0x9E3779B1u; }
 
+// Home bucket of key k in an LDS table of NB buckets of four slots (NB <
+// 2^16): floor((hash >> 8) * (NB - 1) / 2^24), always below NB - 1, so the
+// key's window (its home bucket and the next) lies inside the table.
+__device__ __forceinline__ uint32_t lds_home_bucket(uint32_t k, uint32_t NB) {
+  return (uint32_t)(((uint64_t)(hash_mul(k) >> 8) * ((NB - 1) << 8)) >> 32);
+}
+
 // An invertible 32-bit mixer of xorshift-multiply rounds (shifts 16, 15, 16):
 // the "lowbias32" function found by C. Wellons' hash-prospector search
 // (published 2018, public domain).  Every round is a bijection, so the key can

@@ -28,6 +28,8 @@ constexpr uint64_t kMaxWG = 256;            // persistent workgroups of the LDS 
 constexpr uint32_t kMaxBucketBits = 12;     // radix-partition buckets: at most 4096
 constexpr uint32_t kChunk = 1u << 20;       // records per bucket chunk of the partition engine
 constexpr uint32_t kMaxTimed = 64;
+constexpr uint64_t kSeedMinEvents = 1ull << 22;  // events from which the LDS engine may be seeded
+constexpr uint32_t kSeedSamples = 1u << 18;      // sampled events (the sample table has twice the slots)
 constexpr uint64_t kStatsBatch = 8192;   // large units per radix-select batch
 constexpr uint32_t kStatsTargets = 10;   // up to 8 quantiles, the minimum and the maximum
 constexpr uint32_t kSpillInline = 16384;    // spill records the owner merge takes in
@@ -43,6 +45,7 @@ uint64_t next_pow2(uint64_t x) {
 struct Layout {
   size_t ctrl, T, carryA, partA, partC, nA, scale, bscale, dict, acc, raw;
   size_t T_run, n_run;  // incremental refresh: totals of the events folded so far
+  size_t seed;          // tag table image of the LDS engine seeded with the hottest keys
   // observed runtime per unit (device-time contexts): unit counts and
   // segment starts, write cursors, lookup table, size-class lists, radix
   // select state of one batch of large units
@@ -134,6 +137,7 @@ Layout make_layout(const Params& p) {
   L.nA = take(p.count || p.time ? GA * 8 : 0);
   L.scale = take(GA * 8);
   L.bscale = take(GA * 8);
+  L.seed = take(lds_eng * (size_t)L.ldsSlots * 4);
   L.T_run = take(p.incr ? GA * 16 : 0);
   L.n_run = take(p.incr ? GA * 8 : 0);
   {
@@ -805,13 +809,37 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
   if (!vec_ok && path != ATREX_PATH_GLOBAL_HASH) path = ATREX_PATH_GLOBAL_HASH;
   const uint32_t nwg = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)c->cus, kMaxWG));
   atrex_status st = ATREX_OK;
+  // More keys than one LDS table holds: when the hottest keys that fit the
+  // table cover at least half of a sample of the events, the LDS engine
+  // starts from those keys and spills the rest (the partition engine then
+  // sees only the spilled events); otherwise the partition engine takes all.
+  // (Events without applications take the partition engine as before.)
+  const uint32_t* seed = nullptr;
+  if (c->path == ATREX_PATH_AUTO && path == ATREX_PATH_RADIX_SORT && !c->p.compact && vec_ok && ev->app &&
+      n >= kSeedMinEvents &&
+      (uint64_t)A * P < (1u << 24)) {
+    unsigned long long* covered = c->at<unsigned long long>(L.ctrl + 3072);
+    TIMED(c, "seed", kSeedSamples,
+          launch_seed(s, ev->key, n, kSeedSamples, c->at<uint64_t>(L.rk), 2 * kSeedSamples,
+                      c->at<uint32_t>(L.rlo_acc), c->at<uint64_t>(L.sk[0]), c->at<uint32_t>(L.sv[0]),
+                      c->at<uint64_t>(L.sk[1]), c->at<uint32_t>(L.sv[1]), c->at<void>(L.rs_tmp), L.ldsSlots,
+                      c->at<uint32_t>(L.seed), covered));
+    uint64_t cov = 0;
+    d2h(c, &cov, covered, 8);
+    st = sync_read(c);
+    if (st != ATREX_OK) return st;
+    if (2 * cov >= kSeedSamples) {
+      path = ATREX_PATH_LDS_HASH;
+      seed = c->at<uint32_t>(L.seed);
+    }
+  }
   if (path == ATREX_PATH_LDS_HASH) {
-    c->path_used = "lds_hash";
+    c->path_used = seed ? "lds_hash_seeded" : "lds_hash";
     const uint32_t scap = spill_cap(n, nwg);
     TIMED(c, "pass_b_lds", n,
           launch_pass_b_lds(s, d, A, P, scale, c->at<void>(L.bscale), c->p.raw, L.ldsSlots, nwg, c->owners(), c->at<uint32_t>(L.skey),
                             c->at<uint64_t>(L.sval), c->p.raw ? c->at<uint64_t>(L.sraw) : nullptr,
-                            c->at<uint32_t>(L.scount), scap, rows, c->err()));
+                            c->at<uint32_t>(L.scount), scap, rows, seed, c->err()));
     TIMED(c, "owner_finish", (uint64_t)nwg * ATREX_OWNERS,
           launch_owner_finish(s, c->owners(), nwg, P, c->p.raw, L.oSlots, c->spills(nwg), c->lists(), rows,
                               c->err()));

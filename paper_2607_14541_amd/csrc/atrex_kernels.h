@@ -254,7 +254,13 @@ uint32_t owner_cap(uint32_t S);
 void launch_pass_b_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, const uint64_t* scale,
                        const void* bscale, bool raw, uint32_t S, uint32_t nblocks, const OwnerRegions& orr, uint32_t* spill_key,
                        uint64_t* spill_val, uint64_t* spill_raw, uint32_t* spill_count, uint32_t scap,
-                       const Rows& rows, uint32_t* err);
+                       const Rows& rows, const uint32_t* seed, uint32_t* err);
+// A tag table image of S slots holding the hottest keys of a sample of NS
+// events (tab_cap >= 2 NS, a power of two; list/idx and list2/idx2 hold
+// tab_cap entries); *covered = sampled events of the placed keys.
+void launch_seed(hipStream_t s, const uint32_t* key, uint64_t n, uint32_t NS, uint64_t* tab, uint32_t tab_cap,
+                 uint32_t* cnt, uint64_t* list, uint32_t* idx, uint64_t* list2, uint32_t* idx2, void* sort_tmp,
+                 uint32_t S, uint32_t* seed, unsigned long long* covered);
 void launch_compact_rows(hipStream_t s, const GroupTables& gt, uint32_t P, const Rows& rows, uint32_t* err);
 
 // kernels_rows.hip

@@ -580,11 +580,14 @@ struct StagedEv4 {
   uint64_t sw[4];      // pass-B scale words
 };
 
-template <int BLOCK, bool RAW, bool NO_APP = false>
+// seed (nullable): a tag table image of S slots that every workgroup starts
+// from (the workload's hottest keys, each inside its window); the table is
+// then closed: an event whose key is not in its window is spilled at once.
+template <int BLOCK, bool RAW, bool NO_APP = false, bool SEEDED = false>
 __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, const uint64_t* __restrict__ scale,
                                                       const uint64_t* __restrict__ bscale, uint32_t S,
                                                       OwnerRegions orr, SpillList sp, Rows rows,
-                                                      uint32_t* __restrict__ err) {
+                                                      const uint32_t* __restrict__ seed, uint32_t* __restrict__ err) {
   extern __shared__ unsigned long long smem[];
   const uint32_t SP = S * P;
   // low and high words of the [S * P] accumulators as two arrays (8-byte
@@ -626,7 +629,7 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
     if (RAW) { s_rlo[i] = 0; s_rhi[i] = 0; }
   }
   const uint32_t dummy = SP + (threadIdx.x & 63);  // this lane's dummy entry
-  for (uint32_t i = threadIdx.x; i < S; i += BLOCK) s_tag[i] = ATREX_EMPTY_KEY;
+  for (uint32_t i = threadIdx.x; i < S; i += BLOCK) s_tag[i] = SEEDED ? seed[i] : ATREX_EMPTY_KEY;
   for (uint32_t i = threadIdx.x; i < ATREX_OWNERS; i += BLOCK) s_ocnt[i] = 0;
   __syncthreads();
   const uint32_t lane = lane_id();
@@ -665,7 +668,7 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
   // first, gives the first slot holding the key).  The host takes this engine
   // only when A * P < 2^24, so the scale word index is one 24-bit multiply-add.
   auto home_bucket = [&](uint32_t k) -> uint32_t {
-    return (uint32_t)(((uint64_t)(hash_mul(k) >> 8) * (NH8 & 0xFFFFFFu)) >> 32);
+    return (uint32_t)(((uint64_t)(hash_mul(k) >> 8) * (NH8 & 0xFFFFFFu)) >> 32);  // = lds_home_bucket(k, NB)
   };
   auto stage = [&](const Ev4& e, StagedEv4& g) {
 #pragma unroll
@@ -757,12 +760,13 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
     }
     if (__builtin_expect(__any(miss), 0)) {
       // first occurrence of a key, a key placed past its window, the reserved
-      // key, or events past the end: probe on, then spill what is unplaced
+      // key, or events past the end: probe on (not in a seeded table), then
+      // spill what is unplaced
       const uint32_t nvalid = nvalid_of(bk);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const bool valid = (uint32_t)j < nvalid;
-        if (valid && gi[j] == INVALID_GI && g.key[j] != ATREX_EMPTY_KEY) {
+        if (!SEEDED && valid && gi[j] == INVALID_GI && g.key[j] != ATREX_EMPTY_KEY) {
           const uint32_t b = home_bucket(g.key[j]);
           const uint32_t sl = find_slot(g.key[j], b, bucket_tags(b));
           if (sl != INVALID_GI) gi[j] = __umul24(sl, P) + ph[j];
@@ -963,6 +967,82 @@ __global__ void k_unpack_scale(const uint64_t* __restrict__ sw, uint64_t G, uint
 }
 
 // ---------------------------------------------------------------------------
+// Seeding the LDS engine with the hottest keys.  A sample of NS events at a
+// fixed stride counts its keys in a global table (open addressing, key + 1,
+// 0 = free); the occupied entries become sort keys (~count << 32 | key:
+// ascending = hottest first, ties by key); one workgroup then places the
+// hottest 2S keys, 1024 at a time in that order, into a tag image of S slots,
+// each in the first free slot of its window (home bucket and the next; a key
+// whose window is full is left out), and counts the sampled events the placed
+// keys cover.  Which keys are seeded changes only which events spill, never a
+// result.
+__global__ void k_seed_count(const uint32_t* __restrict__ key, uint64_t n, uint32_t NS,
+                             unsigned long long* __restrict__ tab, uint32_t mask, uint32_t* __restrict__ cnt) {
+  const uint32_t s = blockIdx.x * blockDim.x + threadIdx.x;
+  const bool in = s < NS;
+  const uint32_t k = in ? key[(uint64_t)s * n / NS] : ATREX_EMPTY_KEY;
+  const bool live = in && k != ATREX_EMPTY_KEY;  // the reserved tag is never seeded
+  // the lanes sharing the wave's first key count it with one atomic (a key
+  // that dominates the events would otherwise serialise the wave on one slot)
+  const uint64_t act = __ballot(live);
+  if (act == 0) return;
+  const uint32_t lead = (uint32_t)__ffsll((unsigned long long)act) - 1;
+  const uint32_t k0 = __builtin_amdgcn_readlane(k, lead);
+  const uint64_t same = __ballot(live && k == k0);
+  const bool first = (threadIdx.x & 63) == lead;
+  if (!live || (k == k0 && !first)) return;
+  const uint32_t add = k == k0 ? (uint32_t)__popcll(same) : 1u;
+  uint32_t h = hash32(k) & mask;
+  for (uint32_t probe = 0; probe <= mask; ++probe) {  // the table has at least twice NS slots
+    const unsigned long long prev = atomicCAS(&tab[h], 0ull, (unsigned long long)k + 1);
+    if (prev == 0 || prev == (unsigned long long)k + 1) {
+      atomicAdd(&cnt[h], add);
+      return;
+    }
+    h = (h + 1) & mask;
+  }
+}
+
+__global__ void k_seed_list(const unsigned long long* __restrict__ tab, const uint32_t* __restrict__ cnt,
+                            uint32_t cap, uint64_t* __restrict__ list, uint32_t* __restrict__ idx) {
+  const uint32_t h = blockIdx.x * blockDim.x + threadIdx.x;
+  if (h >= cap) return;
+  // free slots sort after every key
+  list[h] = tab[h] ? ((uint64_t)(0xFFFFFFFFu - cnt[h]) << 32) | (uint32_t)(tab[h] - 1) : ~(uint64_t)0;
+  idx[h] = h;
+}
+
+__global__ __launch_bounds__(1024) void k_seed_build(const uint64_t* __restrict__ list, uint32_t L, uint32_t S,
+                                                     uint32_t* __restrict__ seed,
+                                                     unsigned long long* __restrict__ covered) {
+  extern __shared__ uint32_t s_img[];  // [S]
+  __shared__ unsigned long long s_cov;
+  for (uint32_t i = threadIdx.x; i < S; i += blockDim.x) s_img[i] = ATREX_EMPTY_KEY;
+  if (threadIdx.x == 0) s_cov = 0;
+  __syncthreads();
+  // candidates in chunks of 1024, hottest chunk first; within a chunk each
+  // thread claims the first free slot of its key's window
+  const uint32_t NB = S / 4;
+  for (uint32_t c0 = 0; c0 < L; c0 += 1024) {
+    const uint32_t c = c0 + threadIdx.x;
+    const uint64_t e = c < L ? list[c] : ~(uint64_t)0;
+    if (e != ~(uint64_t)0) {
+      const uint32_t k = (uint32_t)e, count = 0xFFFFFFFFu - (uint32_t)(e >> 32);
+      const uint32_t b = lds_home_bucket(k, NB);
+      for (uint32_t t = 4 * b; t < 4 * b + 8; ++t) {
+        if (atomicCAS(&s_img[t], ATREX_EMPTY_KEY, k) == ATREX_EMPTY_KEY) {
+          atomicAdd(&s_cov, (unsigned long long)count);
+          break;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *covered = s_cov;
+  for (uint32_t i = threadIdx.x; i < S; i += blockDim.x) seed[i] = s_img[i];
+}
+
+// ---------------------------------------------------------------------------
 // Incremental refresh (an append-only event log): the per-(app, phase) totals
 // of the events folded so far (run) plus those of the new events (T, n, as
 // pass A left them) become the totals of the whole log, in T and n.  Skipped
@@ -988,6 +1068,21 @@ __global__ void k_copy_u64(uint64_t* __restrict__ dst, const uint64_t* __restric
 
 // ---------------------------------------------------------------------------
 // Host launchers
+void launch_seed(hipStream_t s, const uint32_t* key, uint64_t n, uint32_t NS, uint64_t* tab, uint32_t tab_cap,
+                 uint32_t* cnt, uint64_t* list, uint32_t* idx, uint64_t* list2, uint32_t* idx2, void* sort_tmp,
+                 uint32_t S, uint32_t* seed, unsigned long long* covered) {
+  launch_fill_u64(s, tab, tab_cap, 0);
+  launch_fill_u32(s, cnt, tab_cap, 0);
+  hipLaunchKernelGGL(k_seed_count, dim3((NS + 255) / 256), dim3(256), 0, s, key, n, NS, (unsigned long long*)tab,
+                     tab_cap - 1, cnt);
+  hipLaunchKernelGGL(k_seed_list, dim3((tab_cap + 255) / 256), dim3(256), 0, s, (const unsigned long long*)tab, cnt,
+                     tab_cap, list, idx);
+  radix_sort_pairs(s, list, idx, list2, idx2, tab_cap, 64, sort_tmp);  // hottest first, free slots last
+  // candidates: the hottest 2S keys (colder ones rarely find a free slot in their window)
+  hipLaunchKernelGGL(k_seed_build, dim3(1), dim3(1024), (size_t)S * 4, s, list, std::min<uint32_t>(tab_cap, 2 * S), S,
+                     seed, covered);
+}
+
 void launch_fold_totals(hipStream_t s, uint64_t* T, uint64_t* cnt, const uint64_t* T_run, const uint64_t* n_run,
                         uint64_t G, const uint32_t* err) {
   if (G) hipLaunchKernelGGL(k_fold_totals, dim3((uint32_t)((G + 255) / 256)), dim3(256), 0, s, T, cnt, T_run, n_run, G, err);
@@ -1087,29 +1182,36 @@ size_t pass_b_lds_smem(uint32_t P, bool raw, uint32_t S) {
   return ((size_t)S * P * 16 + 64 * 16) * (raw ? 2 : 1) + (size_t)S * 4 + ATREX_OWNERS * 4 + 8;
 }
 
-// a workgroup sees at most n / nwg + 4 * 64 + 3 events (its share of the
-// 64-group blocks, and the tail); its spill region holds half of that
-uint32_t spill_cap(uint64_t n, uint32_t nwg) { return (uint32_t)((n + nwg - 1) / nwg / 2 + 8 * 1024); }
+// a workgroup sees about n / nwg events (its share of the 64-group blocks,
+// and the tail); its spill region holds five eighths of that (a table seeded
+// with the hottest keys is taken when they cover at least half of a sample)
+uint32_t spill_cap(uint64_t n, uint32_t nwg) { return (uint32_t)((n + nwg - 1) / nwg * 5 / 8 + 8 * 1024); }
 
 uint32_t owner_cap(uint32_t S) { return 2 * ((S + ATREX_OWNERS - 1) / ATREX_OWNERS) + 32; }
 
 void launch_pass_b_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, const uint64_t* scale,
                        const void* bscale_v, bool raw, uint32_t S, uint32_t nblocks, const OwnerRegions& orr, uint32_t* spill_key,
                        uint64_t* spill_val, uint64_t* spill_raw, uint32_t* spill_count, uint32_t scap,
-                       const Rows& rows, uint32_t* err) {
+                       const Rows& rows, const uint32_t* seed, uint32_t* err) {
   const size_t smem = pass_b_lds_smem(P, raw, S);
   SpillList sp{spill_key, spill_val, spill_raw, spill_count, scap};
   const uint64_t* bscale = (const uint64_t*)bscale_v;
   (void)A;
-  if (!ev.app)  // events without applications (the host takes no raw time then)
+  if (!ev.app)  // events without applications (the host takes no raw time then, nor seeds)
     hipLaunchKernelGGL((k_pass_b_lds<1024, false, true>), dim3(nblocks), dim3(1024), smem, s, ev, P, scale, bscale, S,
-                       orr, sp, rows, err);
+                       orr, sp, rows, seed, err);
+  else if (seed && raw)
+    hipLaunchKernelGGL((k_pass_b_lds<1024, true, false, true>), dim3(nblocks), dim3(1024), smem, s, ev, P, scale,
+                       bscale, S, orr, sp, rows, seed, err);
+  else if (seed)
+    hipLaunchKernelGGL((k_pass_b_lds<1024, false, false, true>), dim3(nblocks), dim3(1024), smem, s, ev, P, scale,
+                       bscale, S, orr, sp, rows, seed, err);
   else if (raw)
     hipLaunchKernelGGL((k_pass_b_lds<1024, true>), dim3(nblocks), dim3(1024), smem, s, ev, P, scale, bscale, S, orr,
-                       sp, rows, err);
+                       sp, rows, seed, err);
   else
     hipLaunchKernelGGL((k_pass_b_lds<1024, false>), dim3(nblocks), dim3(1024), smem, s, ev, P, scale, bscale, S, orr,
-                       sp, rows, err);
+                       sp, rows, seed, err);
 }
 
 void launch_compact_rows(hipStream_t s, const GroupTables& gt, uint32_t P, const Rows& rows, uint32_t* err) {
@@ -1136,6 +1238,12 @@ hipError_t set_kernel_smem_limits() {
   if (e != hipSuccess) return e;
   e = hipFuncSetAttribute((const void*)k_pass_b_lds<1024, false, true>, hipFuncAttributeMaxDynamicSharedMemorySize,
                           160 * 1024);
+  if (e != hipSuccess) return e;
+  e = hipFuncSetAttribute((const void*)k_pass_b_lds<1024, true, false, true>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  if (e != hipSuccess) return e;
+  e = hipFuncSetAttribute((const void*)k_pass_b_lds<1024, false, false, true>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
   if (e != hipSuccess) return e;
   e = set_score_smem_limits();
   if (e != hipSuccess) return e;
