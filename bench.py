@@ -48,11 +48,19 @@ BYTES_PASS_B = 17              # key u32 + app u32 + phase u8 + dur i64 per even
 # the event bytes of the method each kernel reads (the kernels that stream
 # the events); the other kernels' traffic is the engine's own
 METHOD_BYTES = {"pass_a": BYTES_PASS_A, "pass_a_range": BYTES_PASS_A, "pass_a_global": BYTES_PASS_A,
-                "pass_b_lds": BYTES_PASS_B, "pass_b_global": BYTES_PASS_B, "part_scatter": BYTES_PASS_B}
+                "pass_b_lds": BYTES_PASS_B, "pass_b_global": BYTES_PASS_B, "part_scatter": BYTES_PASS_B,
+                "hot_scatter": BYTES_PASS_B}
 PASS_A_KERNELS = ("pass_a", "pass_a_range", "pass_a_global", "pass_a_reduce", "scale")
+# pass B: every kernel from the scale words to the (key, phase) rows
+PASS_B_KERNELS = ("seed", "seed_image", "pass_b_lds", "pass_b_global", "compact_rows", "owner_finish",
+                  "part_hist", "part_scatter", "part_aggregate", "part_hist_spill", "part_scatter_spill",
+                  "part_aggregate_spill", "part_hist_cold", "hot_scatter", "part_aggregate_cold")
 # bytes per event each partition-engine kernel moves besides the method's:
-# histogram (key re-read), scatter (16-byte record written), aggregate (record read)
-ENGINE_BYTES = {"part_hist": 4, "part_scatter": 16, "part_aggregate": 16}
+# histogram (key re-read), scatter (16-byte record written), aggregate (record
+# read); the hot scatter writes records only for the events of keys outside
+# its table, so its figures are upper bounds
+ENGINE_BYTES = {"part_hist": 4, "part_scatter": 16, "part_aggregate": 16,
+                "part_hist_cold": 4, "hot_scatter": 16, "part_aggregate_cold": 16}
 KERNEL_SOURCES = ["paper_2607_14541_amd/csrc/kernels_aggregate.hip",
                   "paper_2607_14541_amd/csrc/kernels_rows.hip",
                   "paper_2607_14541_amd/csrc/kernels_share.hip",
@@ -751,8 +759,7 @@ def main() -> int:
     achieved = alg / (kernels[dom]["avg_ms"] * 1e-3) / 1e9
     traffic = traffic_from_profile(cfg["slug"], dom, n)
     t_a = sum(v["avg_ms"] for k, v in kernels.items() if k in PASS_A_KERNELS)
-    t_b = sum(v["avg_ms"] for k, v in kernels.items() if k in ("pass_b_lds", "pass_b_global", "part_hist",
-                                                              "part_scatter", "part_aggregate"))
+    t_b = sum(v["avg_ms"] for k, v in kernels.items() if k in PASS_B_KERNELS)
     engine_extra = sum(b for k, b in ENGINE_BYTES.items() if k in kernels)
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,

@@ -540,19 +540,24 @@ namespace {
 // The radix-partition engine over all events (spill = false) or over the LDS
 // engine's spill regions: bucket histograms, scan, scatter of 16-byte records,
 // work items, per-bucket-chunk LDS group-by -> rows.
+// Radix-partition buckets: at least 256 (work for every CU even with one
+// chunk per bucket; few buckets keep the scatter's runs long) and about half
+// an LDS table of keys per bucket (with raw time the scatter's LDS tile
+// leaves room for 2^11 buckets).
+uint32_t bucket_bits(const atrex_ctx* c, uint64_t keys_est) {
+  const uint32_t maxBB = c->p.raw ? kMaxBucketBits - 1 : kMaxBucketBits;
+  uint32_t BB = 8;
+  while (BB < maxBB && ((keys_est + (1ull << BB) - 1) >> BB) > c->L.tabSlots / 2) ++BB;
+  return BB;
+}
+
 atrex_status run_partition(atrex_ctx* c, const EventsDev& d, const uint64_t* scale, bool spill, uint32_t nwg,
                            uint64_t nrec, uint64_t keys_est) {
   if (!spill) nwg = part_scatter_wgs((uint32_t)c->cus);  // event ranges: several workgroups per CU
   const Layout& L = c->L;
   hipStream_t s = c->s;
   const uint32_t P = c->p.P;
-  // buckets: at least 256 (work for every CU even with one chunk per bucket;
-  // few buckets keep the scatter's runs long) and about half an LDS table of
-  // keys per bucket
-  // (with raw time the scatter's LDS tile leaves room for 2^11 buckets)
-  const uint32_t maxBB = c->p.raw ? kMaxBucketBits - 1 : kMaxBucketBits;
-  uint32_t BB = 8;
-  while (BB < maxBB && ((keys_est + (1ull << BB) - 1) >> BB) > L.tabSlots / 2) ++BB;
+  const uint32_t BB = bucket_bits(c, keys_est);
   PartSource src;
   src.ev = d;
   src.per = ((d.n + nwg - 1) / nwg + 3) / 4 * 4;
@@ -814,7 +819,13 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
   // starts from those keys and spills the rest (the partition engine then
   // sees only the spilled events); otherwise the partition engine takes all.
   // (Events without applications take the partition engine as before.)
+  // When the image leaves more than 1/16 of the sample to spill (and without
+  // raw time), a smaller table beside the partition engine's tile takes the
+  // hottest keys instead and the other events are partitioned in the same
+  // pass (k_part_scatter_hot): no spill records are written and read again.
   const uint32_t* seed = nullptr;
+  bool hot = false;
+  uint32_t hotS = 0, hotBB = 0;
   if (c->path == ATREX_PATH_AUTO && path == ATREX_PATH_RADIX_SORT && !c->p.compact && vec_ok && ev->app &&
       n >= kSeedMinEvents &&
       (uint64_t)A * P < (1u << 24)) {
@@ -831,9 +842,41 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
     if (2 * cov >= kSeedSamples) {
       path = ATREX_PATH_LDS_HASH;
       seed = c->at<uint32_t>(L.seed);
+      if (!c->p.raw && 16 * cov < 15 * (uint64_t)kSeedSamples) {
+        hotBB = bucket_bits(c, c->p.max_keys);
+        hotS = std::min(hot_scatter_slots(P, hotBB), L.ldsSlots);
+        if (hotS) {
+          TIMED(c, "seed_image", hotS,
+                launch_seed_image(s, c->at<uint64_t>(L.sk[0]), 2 * kSeedSamples, hotS, c->at<uint32_t>(L.seed),
+                                  covered));
+          hot = true;
+        }
+      }
     }
   }
-  if (path == ATREX_PATH_LDS_HASH) {
+  if (hot) {
+    c->path_used = "hot_scatter";
+    PartSource src{};
+    src.ev = d;
+    src.per = ((n + nwg - 1) / nwg + 3) / 4 * 4;
+    src.spill = false;
+    uint32_t* H = c->at<uint32_t>(L.H);
+    uint32_t* O = c->at<uint32_t>(L.O);
+    TIMED(c, "part_hist_cold", n, launch_part_hist_cold(s, src, nwg, hotBB, H, seed, hotS));
+    exclusive_scan_u32(s, H, O, ((uint64_t)1 << hotBB) * nwg, c->at<void>(L.scan_tmp));
+    TIMED(c, "hot_scatter", n,
+          launch_hot_scatter(s, src, nwg, A, P, scale, c->at<uint64_t>(L.bscale), hotBB, O, c->at<uint64_t>(L.rec),
+                             seed, hotS, c->owners(), rows, c->err()));
+    launch_fill_u32(s, c->at<uint32_t>(L.scount), nwg, 0);  // the owner merge finds no spill records
+    TIMED(c, "owner_finish", (uint64_t)nwg * ATREX_OWNERS,
+          launch_owner_finish(s, c->owners(), nwg, P, false, L.oSlots, c->spills(nwg), c->lists(), rows, c->err()));
+    launch_lists_to_rows(s, c->lists(), rows, c->err());
+    launch_part_items(s, O, H, nwg, hotBB, kChunk, c->at<uint32_t>(L.bstart), c->at<uint32_t>(L.istart));
+    TIMED(c, "part_aggregate_cold", n,
+          launch_part_aggregate(s, c->at<uint64_t>(L.rec), nullptr, hotBB, kChunk, c->at<uint32_t>(L.bstart),
+                                c->at<uint32_t>(L.istart), P, L.tabSlots, (uint32_t)c->cus, rows, c->err()));
+    path = ATREX_PATH_RADIX_SORT;  // rows from here on as from the partition engine
+  } else if (path == ATREX_PATH_LDS_HASH) {
     c->path_used = seed ? "lds_hash_seeded" : "lds_hash";
     const uint32_t scap = spill_cap(n, nwg);
     TIMED(c, "pass_b_lds", n,

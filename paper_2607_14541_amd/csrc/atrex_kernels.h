@@ -255,12 +255,15 @@ void launch_pass_b_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t 
                        const void* bscale, bool raw, uint32_t S, uint32_t nblocks, const OwnerRegions& orr, uint32_t* spill_key,
                        uint64_t* spill_val, uint64_t* spill_raw, uint32_t* spill_count, uint32_t scap,
                        const Rows& rows, const uint32_t* seed, uint32_t* err);
-// A tag table image of S slots holding the hottest keys of a sample of NS
-// events (tab_cap >= 2 NS, a power of two; list/idx and list2/idx2 hold
+// A tag table image of S slots holding the hottest keys of a sample of NS <=
+// 2^18 events (tab_cap >= 2 NS, a power of two; list/idx and list2/idx2 hold
 // tab_cap entries); *covered = sampled events of the placed keys.
 void launch_seed(hipStream_t s, const uint32_t* key, uint64_t n, uint32_t NS, uint64_t* tab, uint32_t tab_cap,
                  uint32_t* cnt, uint64_t* list, uint32_t* idx, uint64_t* list2, uint32_t* idx2, void* sort_tmp,
                  uint32_t S, uint32_t* seed, unsigned long long* covered);
+// Another image, of S slots, from the sorted list launch_seed left in `list`.
+void launch_seed_image(hipStream_t s, const uint64_t* list, uint32_t tab_cap, uint32_t S, uint32_t* seed,
+                       unsigned long long* covered);
 void launch_compact_rows(hipStream_t s, const GroupTables& gt, uint32_t P, const Rows& rows, uint32_t* err);
 
 // kernels_rows.hip
@@ -281,6 +284,17 @@ void launch_lists_to_rows(hipStream_t s, const OwnerLists& ol, const Rows& rows,
 constexpr uint32_t kMaxPartWG = 1024;  // partition workgroups over the events
 uint32_t part_scatter_wgs(uint32_t cus);
 void launch_part_hist(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t BB, uint32_t* H);
+// the histogram of the events whose key is not in the seeded image (S slots)
+void launch_part_hist_cold(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t BB, uint32_t* H,
+                           const uint32_t* seed, uint32_t S);
+// Slots of k_part_scatter_hot's table at P phases and 2^BB buckets (0: none fit).
+uint32_t hot_scatter_slots(uint32_t P, uint32_t BB);
+// Pass B with a seeded LDS table for the image's keys and the partition
+// scatter for the other events (positions O from launch_part_hist_cold); the
+// table goes to the owner regions [nwg][ATREX_OWNERS].
+void launch_hot_scatter(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t A, uint32_t P,
+                        const uint64_t* scale, const uint64_t* bscale, uint32_t BB, const uint32_t* O, uint64_t* rec,
+                        const uint32_t* seed, uint32_t S, const OwnerRegions& orr, const Rows& rows, uint32_t* err);
 void launch_part_scatter(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t A, uint32_t P,
                          const uint64_t* scale, const uint64_t* bscale, uint32_t BB, const uint32_t* O, uint64_t* rec,
                          uint64_t* rraw, uint32_t* err);

@@ -969,13 +969,15 @@ __global__ void k_unpack_scale(const uint64_t* __restrict__ sw, uint64_t G, uint
 // ---------------------------------------------------------------------------
 // Seeding the LDS engine with the hottest keys.  A sample of NS events at a
 // fixed stride counts its keys in a global table (open addressing, key + 1,
-// 0 = free); the occupied entries become sort keys (~count << 32 | key:
-// ascending = hottest first, ties by key); one workgroup then places the
+// 0 = free); the occupied entries become sort keys (the inverted count:
+// ascending = hottest first, ties in table order); one workgroup then places the
 // hottest 2S keys, 1024 at a time in that order, into a tag image of S slots,
 // each in the first free slot of its window (home bucket and the next; a key
 // whose window is full is left out), and counts the sampled events the placed
 // keys cover.  Which keys are seeded changes only which events spill, never a
 // result.
+constexpr uint32_t kSeedCountBits = 19, kSeedCountMask = (1u << kSeedCountBits) - 1;
+
 __global__ void k_seed_count(const uint32_t* __restrict__ key, uint64_t n, uint32_t NS,
                              unsigned long long* __restrict__ tab, uint32_t mask, uint32_t* __restrict__ cnt) {
   const uint32_t s = blockIdx.x * blockDim.x + threadIdx.x;
@@ -1007,8 +1009,9 @@ __global__ void k_seed_list(const unsigned long long* __restrict__ tab, const ui
                             uint32_t cap, uint64_t* __restrict__ list, uint32_t* __restrict__ idx) {
   const uint32_t h = blockIdx.x * blockDim.x + threadIdx.x;
   if (h >= cap) return;
-  // free slots sort after every key
-  list[h] = tab[h] ? ((uint64_t)(0xFFFFFFFFu - cnt[h]) << 32) | (uint32_t)(tab[h] - 1) : ~(uint64_t)0;
+  // (key << 32 | 2^19 - 1 - count): the sort takes the low 19 bits only
+  // (counts are at most NS <= 2^18; free slots, with count 0, sort last)
+  list[h] = tab[h] ? ((uint64_t)(uint32_t)(tab[h] - 1) << 32) | (kSeedCountMask - cnt[h]) : kSeedCountMask;
   idx[h] = h;
 }
 
@@ -1025,9 +1028,10 @@ __global__ __launch_bounds__(1024) void k_seed_build(const uint64_t* __restrict_
   const uint32_t NB = S / 4;
   for (uint32_t c0 = 0; c0 < L; c0 += 1024) {
     const uint32_t c = c0 + threadIdx.x;
-    const uint64_t e = c < L ? list[c] : ~(uint64_t)0;
-    if (e != ~(uint64_t)0) {
-      const uint32_t k = (uint32_t)e, count = 0xFFFFFFFFu - (uint32_t)(e >> 32);
+    const uint64_t e = c < L ? list[c] : kSeedCountMask;
+    const uint32_t count = kSeedCountMask - (uint32_t)(e & kSeedCountMask);
+    if (count) {
+      const uint32_t k = (uint32_t)(e >> 32);
       const uint32_t b = lds_home_bucket(k, NB);
       for (uint32_t t = 4 * b; t < 4 * b + 8; ++t) {
         if (atomicCAS(&s_img[t], ATREX_EMPTY_KEY, k) == ATREX_EMPTY_KEY) {
@@ -1077,7 +1081,12 @@ void launch_seed(hipStream_t s, const uint32_t* key, uint64_t n, uint32_t NS, ui
                      tab_cap - 1, cnt);
   hipLaunchKernelGGL(k_seed_list, dim3((tab_cap + 255) / 256), dim3(256), 0, s, (const unsigned long long*)tab, cnt,
                      tab_cap, list, idx);
-  radix_sort_pairs(s, list, idx, list2, idx2, tab_cap, 64, sort_tmp);  // hottest first, free slots last
+  radix_sort_pairs(s, list, idx, list2, idx2, tab_cap, kSeedCountBits, sort_tmp);  // hottest first, free last
+  launch_seed_image(s, list, tab_cap, S, seed, covered);
+}
+
+void launch_seed_image(hipStream_t s, const uint64_t* list, uint32_t tab_cap, uint32_t S, uint32_t* seed,
+                       unsigned long long* covered) {
   // candidates: the hottest 2S keys (colder ones rarely find a free slot in their window)
   hipLaunchKernelGGL(k_seed_build, dim3(1), dim3(1024), (size_t)S * 4, s, list, std::min<uint32_t>(tab_cap, 2 * S), S,
                      seed, covered);

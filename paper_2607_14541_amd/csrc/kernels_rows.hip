@@ -512,11 +512,41 @@ __device__ __forceinline__ uint32_t count_in(uint32_t* cnt, uint32_t b, bool act
   return active ? atomicAdd(&cnt[b], 1u) : 0u;
 }
 
-__global__ __launch_bounds__(1024) void k_part_hist(PartSource src, uint32_t BB, uint32_t* __restrict__ H) {
+constexpr uint32_t kNoSlot = 0xFFFFFFFFu;
+
+// Key `k` is in a seeded table image of S slots (four-slot buckets; a key
+// sits in its home bucket or the next): its slot, else kNoSlot.  The
+// reserved key is never in the image (it marks free slots).
+__device__ __forceinline__ uint32_t image_slot(const uint32_t* s_img, uint32_t S, uint32_t k) {
+  const uint32_t b = lds_home_bucket(k, S / 4);
+  const uint4 t0 = *(const uint4*)&s_img[4 * b], t1 = *(const uint4*)&s_img[4 * b + 4];
+  uint32_t x = kNoSlot;
+  x = t1.w == k ? 4 * b + 7 : x;
+  x = t1.z == k ? 4 * b + 6 : x;
+  x = t1.y == k ? 4 * b + 5 : x;
+  x = t1.x == k ? 4 * b + 4 : x;
+  x = t0.w == k ? 4 * b + 3 : x;
+  x = t0.z == k ? 4 * b + 2 : x;
+  x = t0.y == k ? 4 * b + 1 : x;
+  x = t0.x == k ? 4 * b : x;
+  return k == ATREX_EMPTY_KEY ? kNoSlot : x;
+}
+
+constexpr int HIST_DEPTH = 4;  // groups of four keys in flight per lane in k_part_hist
+
+// HOT: only the events whose key is not in the seeded image `seed` of S
+// slots are counted (those k_part_scatter_hot turns into records).
+template <bool HOT>
+__global__ __launch_bounds__(1024) void k_part_hist(PartSource src, uint32_t BB, uint32_t* __restrict__ H,
+                                                    const uint32_t* __restrict__ seed, uint32_t S) {
   extern __shared__ uint32_t s_h[];
   const uint32_t NB = 1u << BB, w = blockIdx.x, nw = gridDim.x, sh = 32 - BB;
+  uint32_t* s_img = s_h + NB;  // [S], HOT only (16-byte aligned: NB >= 4)
   for (uint32_t i = threadIdx.x; i < NB; i += blockDim.x) s_h[i] = 0;
+  if (HOT)
+    for (uint32_t i = threadIdx.x; i < S; i += blockDim.x) s_img[i] = seed[i];
   __syncthreads();
+  auto cold = [&](uint32_t k) { return !HOT || image_slot(s_img, S, k) == kNoSlot; };
   uint64_t b, e;
   part_range(src, w, b, e);
   if (src.spill) {
@@ -527,17 +557,34 @@ __global__ __launch_bounds__(1024) void k_part_hist(PartSource src, uint32_t BB,
     }
   } else {  // b is a multiple of 4: four keys per lane with one 16-byte load
     const uint64_t e4 = b + (e - b) / 4 * 4;
-    for (uint64_t q0 = b; q0 < e4; q0 += 4 * (uint64_t)blockDim.x) {
-      const uint64_t q = q0 + 4 * (uint64_t)threadIdx.x;
-      const bool v = q < e4;
-      v4u k = {0, 0, 0, 0};
-      if (v) k = __builtin_nontemporal_load((const v4u*)(src.ev.key + q));
-      (void)count_in(s_h, hash32(k.x) >> sh, v);
-      (void)count_in(s_h, hash32(k.y) >> sh, v);
-      (void)count_in(s_h, hash32(k.z) >> sh, v);
-      (void)count_in(s_h, hash32(k.w) >> sh, v);
+    // groups of four keys, iteration `it` covering groups it * blockDim.x +
+    // [0, blockDim.x) (uniform trip count); a ring of HIST_DEPTH groups per
+    // lane keeps that many loads in flight while one is counted
+    const uint64_t ng = (e4 - b) / 4, iters = (ng + blockDim.x - 1) / blockDim.x;
+    auto load = [&](uint64_t it, v4u& k) {
+      const uint64_t gi = it * blockDim.x + threadIdx.x;
+      if (gi < ng) k = __builtin_nontemporal_load((const v4u*)(src.ev.key + b + 4 * gi));
+    };
+    v4u ring[HIST_DEPTH];
+#pragma unroll
+    for (int d = 0; d < HIST_DEPTH; ++d) load(d, ring[d]);
+    for (uint64_t it = 0; it < iters; it += HIST_DEPTH) {
+#pragma unroll
+      for (int d = 0; d < HIST_DEPTH; ++d) {
+        if (it + d >= iters) break;
+        const bool v = (it + d) * blockDim.x + threadIdx.x < ng;
+        const v4u k = ring[d];
+        if (it + d + HIST_DEPTH < iters) load(it + d + HIST_DEPTH, ring[d]);
+        (void)count_in(s_h, hash32(k.x) >> sh, v && cold(k.x));
+        (void)count_in(s_h, hash32(k.y) >> sh, v && cold(k.y));
+        (void)count_in(s_h, hash32(k.z) >> sh, v && cold(k.z));
+        (void)count_in(s_h, hash32(k.w) >> sh, v && cold(k.w));
+      }
     }
-    for (uint64_t i = e4 + threadIdx.x; i < e; i += blockDim.x) atomicAdd(&s_h[hash32(src.ev.key[i]) >> sh], 1u);
+    for (uint64_t i = e4 + threadIdx.x; i < e; i += blockDim.x) {
+      const uint32_t k = src.ev.key[i];
+      if (cold(k)) atomicAdd(&s_h[hash32(k) >> sh], 1u);
+    }
   }
   __syncthreads();
   for (uint32_t i = threadIdx.x; i < NB; i += blockDim.x) H[(size_t)i * nw + w] = s_h[i];
@@ -738,6 +785,242 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint3
     }
   }
   if (__any(bad) && (tid & 63) == 0) atomicOr(err, ATREX_ERRBIT_RANGE);
+}
+
+// Pass B of a seeded table and the partition scatter in one pass over the
+// events.  An event whose key is in the image `seed` (the sample's hottest
+// keys, each in its two-bucket window; the same image in every workgroup) is
+// added to this workgroup's LDS table of S slots x P two-word accumulators;
+// every other event becomes a partition record, ranked, placed and written
+// out in tiles as in k_part_scatter (k_part_hist<true> with the same image
+// counts exactly these).  At the end the table goes to the owner regions as
+// the LDS engine's does.  The table takes what LDS leaves beside the tile's
+// staging, which holds 1 / STAGE_DIV (1 or 2) of a tile's records: a tile
+// with more records is placed and written out in two rounds.
+template <uint32_t SC_EPT, uint32_t SC_BLOCK, uint32_t STAGE_DIV>
+__global__ __launch_bounds__(SC_BLOCK) void k_part_scatter_hot(PartSource src, uint32_t A, uint32_t P,
+                                                               const uint64_t* __restrict__ scale,
+                                                               const uint64_t* __restrict__ bscale, uint32_t BB,
+                                                               const uint32_t* __restrict__ O,
+                                                               uint64_t* __restrict__ rec,
+                                                               const uint32_t* __restrict__ seed, uint32_t S,
+                                                               OwnerRegions orr, Rows rows,
+                                                               uint32_t* __restrict__ err) {
+  extern __shared__ uint64_t sm64[];
+  constexpr uint32_t NWV = SC_BLOCK / 64;
+  constexpr uint32_t SC_TILE = SC_EPT * SC_BLOCK, CAP = SC_TILE / STAGE_DIV;
+  const uint32_t NB = 1u << BB, w = blockIdx.x, nw = gridDim.x, tid = threadIdx.x, lane = tid & 63;
+  const uint32_t SP = S * P, NE = SP + 64;
+  uint64_t* s_rec = sm64;                                             // [CAP][2]
+  unsigned long long* s_lo = (unsigned long long*)(s_rec + 2 * CAP);  // [SP + 64 per-lane dummies]
+  unsigned long long* s_hi = s_lo + NE;                                   // [SP + 64]
+  uint32_t* s_tag = (uint32_t*)(s_hi + NE);                               // [S], 16-byte aligned
+  uint16_t* s_bkt = (uint16_t*)(s_tag + S);                               // [CAP]
+  uint32_t* s_cur = (uint32_t*)(s_bkt + CAP);      // [NB] this workgroup's next record per bucket
+  uint32_t* s_cnt = s_cur + NB;                    // [2][NB] records of the tile per bucket (by tile parity)
+  uint32_t* s_off = s_cnt + 2 * NB;                // [NB] tile offsets
+  uint32_t* s_ocnt = s_off + NB;                   // [ATREX_OWNERS]
+  __shared__ uint32_t s_w[NWV];
+  for (uint32_t i = tid; i < NB; i += SC_BLOCK) {
+    s_cur[i] = O[(size_t)i * nw + w];
+    s_cnt[i] = 0;
+    s_cnt[NB + i] = 0;
+  }
+  for (uint32_t i = tid; i < NE; i += SC_BLOCK) {
+    s_lo[i] = 0;
+    s_hi[i] = 0;
+  }
+  for (uint32_t i = tid; i < S; i += SC_BLOCK) s_tag[i] = seed[i];
+  for (uint32_t i = tid; i < ATREX_OWNERS; i += SC_BLOCK) s_ocnt[i] = 0;
+  const uint32_t dummy = SP + lane;  // this lane's dummy entry
+  uint64_t b, e;
+  part_range(src, w, b, e);
+  const uint32_t lowbits = 32 - BB;
+  const uint64_t lowmask = ((uint64_t)1 << lowbits) - 1;
+  bool bad = false;
+  constexpr uint32_t G4 = SC_EPT / 4;
+  Ev4 nxt[G4];
+#pragma unroll
+  for (uint32_t g = 0; g < G4; ++g) load_group<false>(src.ev, b + 4 * ((uint64_t)g * SC_BLOCK + tid), e, nxt[g]);
+  constexpr uint32_t PERMAX = 4;  // buckets per thread in the scan (NB <= 4 * SC_BLOCK)
+  const uint32_t per = (NB + SC_BLOCK - 1) / SC_BLOCK, b0 = tid * per;
+  uint32_t prevcnt[PERMAX] = {0, 0, 0, 0};
+  uint32_t parity = 0;
+  __syncthreads();
+  for (uint64_t t0 = b; t0 < e; t0 += SC_TILE, parity ^= 1u) {  // uniform trip count
+    Ev4 evg[G4];
+#pragma unroll
+    for (uint32_t g = 0; g < G4; ++g) evg[g] = nxt[g];
+    uint32_t* cnt = s_cnt + parity * NB;
+    uint32_t* cnt_next = s_cnt + (parity ^ 1u) * NB;
+    // phase 1: the table slot (hot) or the bucket and rank (cold) of every
+    // event; the scale words are requested here and used after the scan
+    uint32_t hh[SC_EPT], rk[SC_EPT], hs[SC_EPT];  // hash; rank << 4 | record << 3 | phase; slot
+    uint64_t dv[SC_EPT], sw[SC_EPT];
+#pragma unroll
+    for (uint32_t j = 0; j < SC_EPT; ++j) {
+      const uint64_t i = t0 + 4 * ((uint64_t)(j / 4) * SC_BLOCK + tid) + (j % 4);
+      const bool vj = i < e;
+      const Ev4& ev = evg[j / 4];
+      const uint32_t jj = j % 4;
+      const uint32_t a = ev.app[jj], ph = ev.ph[jj], key = ev.key[jj];
+      const int64_t dd = ev.dur[jj];
+      const bool ok = a < A && ph < P && dd >= 0;
+      bad |= vj && !ok;
+      sw[j] = ok ? bscale[a * P + ph] : 0;
+      dv[j] = ok ? (uint64_t)dd : 0;
+      rk[j] = ok ? ph : 0u;
+      hs[j] = vj ? image_slot(s_tag, S, key) : kNoSlot;
+      if (vj && hs[j] == kNoSlot) rk[j] |= 8u;
+      if (!ok) hs[j] = kNoSlot;  // an invalid event adds nothing (the call fails on it)
+      hh[j] = hash32(key);
+    }
+#pragma unroll
+    for (uint32_t j = 0; j < SC_EPT; ++j) rk[j] |= count_in(cnt, hh[j] >> lowbits, (rk[j] >> 3) & 1u) << 4;
+    __syncthreads();
+    // exclusive scan of the tile's bucket counts; the previous tile's counts
+    // advance the positions, and the next tile's counters are cleared
+    uint32_t tot = 0;  // records of the tile
+    {
+      uint32_t sum = 0;
+#pragma unroll
+      for (uint32_t k = 0; k < PERMAX; ++k) {
+        if (k < per && b0 + k < NB) {
+          const uint32_t c = cnt[b0 + k];
+          s_cur[b0 + k] += prevcnt[k];
+          prevcnt[k] = c;
+          cnt_next[b0 + k] = 0;
+          sum += c;
+        }
+      }
+      const uint32_t wave = tid >> 6;
+      uint32_t inc = sum;
+      for (int dd = 1; dd < 64; dd <<= 1) {
+        const uint32_t y = __shfl_up(inc, dd, 64);
+        if (lane >= (uint32_t)dd) inc += y;
+      }
+      if (lane == 63) s_w[wave] = inc;
+      __syncthreads();
+      uint32_t off = 0;
+      for (uint32_t x = 0; x < NWV; ++x) {
+        const uint32_t v = s_w[x];
+        if (x < wave) off += v;
+        tot += v;
+      }
+      uint32_t run = off + inc - sum;
+#pragma unroll
+      for (uint32_t k = 0; k < PERMAX; ++k)
+        if (k < per && b0 + k < NB) { s_off[b0 + k] = run; run += prevcnt[k]; }
+    }
+    __syncthreads();
+    // phase 2: the Q96 share of every event; the records of the first round
+    // (tile positions below CAP) placed in LDS in bucket order, then the hot
+    // events added to the table without branches (a lane with nothing to add
+    // adds into its own dummy entry): the low words first, their returned
+    // values giving the carries, then the high words with the count
+    auto place = [&](uint32_t j, uint32_t r0, const uint64_t* vlj, const uint64_t* vhj) {
+      if ((rk[j] >> 3) & 1u) {
+        const uint32_t bk = hh[j] >> lowbits;
+        const uint32_t at = s_off[bk] + (rk[j] >> 4) - r0;
+        if (at < CAP) {
+          s_rec[2 * at] = vlj[j];
+          s_rec[2 * at + 1] = vhj[j] | ((uint64_t)(rk[j] & 7u) << 33) | (((uint64_t)hh[j] & lowmask) << 36);
+          s_bkt[at] = (uint16_t)bk;
+        }
+      }
+    };
+    auto write_out = [&](uint32_t r0) {
+      const uint32_t m = min(CAP, tot - r0);
+      for (uint32_t k = tid; k < m; k += SC_BLOCK) {
+        const uint32_t bb = s_bkt[k];
+        const size_t pos = (size_t)s_cur[bb] + (k + r0 - s_off[bb]);
+        v2l r;
+        r.x = (long long)s_rec[2 * k];
+        r.y = (long long)s_rec[2 * k + 1];
+        *(v2l*)(rec + 2 * pos) = r;
+      }
+    };
+    uint64_t vl[SC_EPT], vh[SC_EPT];
+#pragma unroll
+    for (uint32_t j = 0; j < SC_EPT; ++j) {
+      const uint64_t wv = sw[j], d = dv[j];
+      const uint32_t ph = rk[j] & 7u;
+      if ((uint32_t)(wv >> 56) <= 127u) {
+        if ((d >> 32) == 0) {
+          uint32_t h32;
+          bscale_share32((uint32_t)d, (uint32_t)wv, (uint32_t)(wv >> 32), vl[j], h32);
+          vh[j] = h32;
+        } else {
+          bscale_share64(d, (uint32_t)wv, (uint32_t)(wv >> 32), vl[j], vh[j]);
+        }
+      } else {  // rho outside [-8, 63] (rare): the general scale word, found again from the event
+        const uint64_t i = t0 + 4 * ((uint64_t)(j / 4) * SC_BLOCK + tid) + (j % 4);
+        const u128 x = event_share(d, scale[app_at<false>(src.ev.app, i) * P + ph]);
+        vl[j] = (uint64_t)x;
+        vh[j] = (uint64_t)(x >> 64);
+      }
+      place(j, 0, vl, vh);
+    }
+    {
+      uint32_t at[SC_EPT];
+#pragma unroll
+      for (uint32_t j = 0; j < SC_EPT; ++j) at[j] = hs[j] != kNoSlot ? hs[j] * P + (rk[j] & 7u) : dummy;
+      unsigned long long old[SC_EPT];
+#pragma unroll
+      for (uint32_t j = 0; j < SC_EPT; ++j) old[j] = atomicAdd(&s_lo[at[j]], (unsigned long long)vl[j]);
+#pragma unroll
+      for (uint32_t j = 0; j < SC_EPT; ++j) {
+        const unsigned long long carry = (old[j] + vl[j] < old[j]) ? 1ull : 0ull;
+        atomicAdd(&s_hi[at[j]], (unsigned long long)vh[j] + carry + (1ull << ATREX_COUNT_SHIFT));
+      }
+    }
+    if (t0 + SC_TILE < e) {
+#pragma unroll
+      for (uint32_t g = 0; g < G4; ++g)
+        load_group<false>(src.ev, t0 + SC_TILE + 4 * ((uint64_t)g * SC_BLOCK + tid), e, nxt[g]);
+    }
+    __syncthreads();
+    write_out(0);
+    if (STAGE_DIV > 1 && tot > CAP) {  // uniform: the second round
+      __syncthreads();
+#pragma unroll
+      for (uint32_t j = 0; j < SC_EPT; ++j) place(j, CAP, vl, vh);
+      __syncthreads();
+      write_out(CAP);
+    }
+  }
+  if (__any(bad) && lane == 0) atomicOr(err, ATREX_ERRBIT_RANGE);
+  __syncthreads();
+  // the table -> owner regions (owner = top byte of the key hash); a region
+  // that is full sends its rows straight to the row list
+  for (uint32_t s0 = 0; s0 < S; s0 += SC_BLOCK) {
+    const uint32_t sl = s0 + tid;
+    const uint32_t t = sl < S ? s_tag[sl] : ATREX_EMPTY_KEY;
+    bool spill_rows = false;
+    if (t != ATREX_EMPTY_KEY) {
+      const uint32_t o = hash32(t) >> 24;
+      const uint32_t r = atomicAdd(&s_ocnt[o], 1u);
+      if (r < orr.capo) {
+        const size_t ri = ((size_t)w * ATREX_OWNERS + o) * orr.capo + r;
+        orr.key[ri] = t;
+        for (uint32_t ph = 0; ph < P; ++ph) {
+          orr.acc[(ri * P + ph) * 2] = s_lo[sl * P + ph];
+          orr.acc[(ri * P + ph) * 2 + 1] = s_hi[sl * P + ph];
+        }
+      } else {
+        spill_rows = true;
+      }
+    }
+    for (uint32_t ph = 0; ph < P; ++ph) {
+      const size_t gi = (size_t)sl * P + ph;
+      const uint64_t hi = spill_rows ? s_hi[gi] : 0;
+      const bool want = spill_rows && (hi >> ATREX_COUNT_SHIFT) != 0;
+      row_append(rows, want, ((uint64_t)t << 3) | ph, want ? s_lo[gi] : 0, hi, 0, 0, err);
+    }
+  }
+  __syncthreads();
+  for (uint32_t o = tid; o < ATREX_OWNERS; o += SC_BLOCK)
+    orr.count[(size_t)w * ATREX_OWNERS + o] = min(s_ocnt[o], orr.capo);
 }
 
 // Work items = (bucket, chunk of at most CH records); item_start[b] = first
@@ -1040,6 +1323,10 @@ size_t lds_table_bytes(uint32_t P, bool raw, uint32_t S) {
 }
 
 constexpr uint32_t kScatterEpt = 4, kScatterBlock = 1024;
+// k_part_scatter_hot: events per thread per tile, and the dynamic LDS it may
+// take (static LDS beside it: the scan's wave sums)
+constexpr uint32_t kHotEpt = 4, kHotStageDiv = 1;
+constexpr size_t kHotLds = 160 * 1024 - 256;
 
 static size_t scatter_smem(uint32_t BB, bool raw) {
   return (size_t)kScatterEpt * kScatterBlock * (16 + (raw ? 8 : 0) + 2) + ((size_t)4 << BB) * 4;
@@ -1049,7 +1336,34 @@ uint32_t part_scatter_wgs(uint32_t cus) { return std::min<uint32_t>(kMaxPartWG, 
 
 
 void launch_part_hist(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t BB, uint32_t* H) {
-  hipLaunchKernelGGL(k_part_hist, dim3(nwg), dim3(1024), (size_t)4 << BB, s, src, BB, H);
+  hipLaunchKernelGGL(k_part_hist<false>, dim3(nwg), dim3(1024), (size_t)4 << BB, s, src, BB, H, nullptr, 0u);
+}
+
+void launch_part_hist_cold(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t BB, uint32_t* H,
+                           const uint32_t* seed, uint32_t S) {
+  hipLaunchKernelGGL(k_part_hist<true>, dim3(nwg), dim3(1024), ((size_t)4 << BB) + (size_t)4 * S, s, src, BB, H,
+                     seed, S);
+}
+
+// LDS of k_part_scatter_hot: the staged records and their buckets, the
+// bucket counters, the owner counters and the table of S slots.
+static size_t hot_scatter_smem(uint32_t P, uint32_t BB, uint32_t S) {
+  return (size_t)kHotEpt * kScatterBlock / kHotStageDiv * (16 + 2) + ((size_t)4 << BB) * 4 + (size_t)ATREX_OWNERS * 4 +
+         ((size_t)S * P + 64) * 16 + (size_t)S * 4;
+}
+
+uint32_t hot_scatter_slots(uint32_t P, uint32_t BB) {
+  const size_t fixed = hot_scatter_smem(P, BB, 0);
+  if (fixed >= kHotLds) return 0;
+  const uint32_t S = (uint32_t)((kHotLds - fixed) / (16 * (size_t)P + 4)) & ~3u;
+  return S >= 8 ? S : 0;
+}
+
+void launch_hot_scatter(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t A, uint32_t P,
+                        const uint64_t* scale, const uint64_t* bscale, uint32_t BB, const uint32_t* O, uint64_t* rec,
+                        const uint32_t* seed, uint32_t S, const OwnerRegions& orr, const Rows& rows, uint32_t* err) {
+  hipLaunchKernelGGL((k_part_scatter_hot<kHotEpt, kScatterBlock, kHotStageDiv>), dim3(nwg), dim3(kScatterBlock),
+                     hot_scatter_smem(P, BB, S), s, src, A, P, scale, bscale, BB, O, rec, seed, S, orr, rows, err);
 }
 
 void launch_part_scatter(hipStream_t s, const PartSource& src, uint32_t nwg, uint32_t A, uint32_t P,
@@ -1143,7 +1457,7 @@ void launch_lists_to_rows(hipStream_t s, const OwnerLists& ol, const Rows& rows,
 // Dynamic LDS limits: 160 KB less a margin that covers each kernel's static LDS.
 hipError_t set_rows_smem_limits() {
   const void* fns[] = {(const void*)k_part_aggregate<true>, (const void*)k_part_aggregate<false>,
-                       (const void*)k_part_hist,
+                       (const void*)k_part_hist<false>, (const void*)k_part_hist<true>,
                        (const void*)k_part_scatter<true, false, kScatterEpt, kScatterBlock>,
                        (const void*)k_part_scatter<true, true, kScatterEpt, kScatterBlock>,
                        (const void*)k_part_scatter<false, false, kScatterEpt, kScatterBlock>,
@@ -1151,6 +1465,11 @@ hipError_t set_rows_smem_limits() {
                        (const void*)k_part_scatter<false, false, kScatterEpt, kScatterBlock, true>};
   for (const void* f : fns) {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 2048);
+    if (e != hipSuccess) return e;
+  }
+  {
+    const hipError_t e = hipFuncSetAttribute((const void*)k_part_scatter_hot<kHotEpt, kScatterBlock, kHotStageDiv>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)kHotLds);
     if (e != hipSuccess) return e;
   }
   const void* fo[] = {(const void*)k_owner_finish<true>, (const void*)k_owner_finish<false>,

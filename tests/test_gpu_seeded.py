@@ -1,19 +1,25 @@
 """The LDS engine seeded with a sample's hottest keys (more keys than one
 LDS table holds, most events on a few thousand of them): every output equals
 the oracle's, on prefixes of the skewed workloads large enough for the
-seeding (at least 2^22 events), through the separate calls and atrex_run."""
+seeding (at least 2^22 events), through the separate calls and atrex_run.
+With raw time, or when the image covers at least 15/16 of the sample, pass B
+runs on the seeded table and spills the rest (lds_hash_seeded); otherwise a
+smaller seeded table sits beside the partition scatter in one pass
+(hot_scatter)."""
 import numpy as np
 import pytest
 
 import gpu_helpers as H
 from oracle import oracle as O
+from paper_2607_14541_amd import atrex as X
 from paper_2607_14541_amd import synth
 
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("ci,n", [(3, (1 << 22) + 5), (4, (1 << 22) + 1)])
-def test_seeded_lds_engine_matches_the_oracle(ci, n):
+@pytest.mark.parametrize("ci,n,one_call_path", [(3, (1 << 22) + 5, "hot_scatter"),
+                                                (4, (1 << 22) + 1, "lds_hash_seeded")])
+def test_seeded_lds_engine_matches_the_oracle(ci, n, one_call_path):
     cfg = synth.CONFIGS[ci]
     ev = synth.events(cfg, n=n)
     c = synth.app_weights(cfg)
@@ -28,7 +34,7 @@ def test_seeded_lds_engine_matches_the_oracle(ci, n):
     H.compare(g, o, raw=True, score=True)
     g1, _, path = H.run_one_call(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, P, keys, s,
                                  max_keys=keys.size, max_groups=keys.size * P)
-    assert path == "lds_hash_seeded"
+    assert path == one_call_path
     H.compare(g1, o, raw=False, score=True)
 
 
@@ -63,3 +69,55 @@ def test_cold_stretch_overflows_the_spill_regions():
     assert g["path"] == "lds_hash+radix_all", g["path"]
     o = O.run(key, ev["app"], ev["phase"], ev["dur_ns"], c, P, threads=8)
     H.compare(g, o, raw=True)
+
+
+@pytest.mark.parametrize("n", [(1 << 22) + 3, (1 << 23) + 1001])
+def test_hot_scatter_matches_the_oracle(n):
+    """The seeded table beside the partition scatter, without raw time, on
+    two ragged prefixes of the 1B-event workload (64k Zipf(0.9) keys, 3
+    phases, 100k apps)."""
+    cfg = synth.CONFIGS[3]
+    ev = synth.events(cfg, n=n)
+    c = synth.app_weights(cfg)
+    keys = synth.key_space(cfg)
+    P = cfg["num_phases"]
+    H.say("hot scatter, n", n)
+    g = H.run_gpu(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, P, raw=False, max_keys=keys.size,
+                  max_groups=keys.size * P)
+    assert g["path"] == "hot_scatter", g["path"]
+    o = O.run(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, P, threads=8)
+    H.compare(g, o, raw=False)
+
+
+def test_hot_scatter_reserved_key_and_range_error():
+    """The reserved key (never in an image) goes to the partition records;
+    an invalid event fails the call with OUT_OF_RANGE and the context stays
+    usable."""
+    cfg = synth.CONFIGS[3]
+    n = (1 << 22) + 9
+    ev = synth.events(cfg, n=n)
+    c = synth.app_weights(cfg)
+    keys = synth.key_space(cfg)
+    P = cfg["num_phases"]
+    key = ev["key"].copy()
+    key[::1000] = 0xFFFFFFFF
+    H.say("hot scatter, reserved key")
+    g = H.run_gpu(key, ev["app"], ev["phase"], ev["dur_ns"], c, P, raw=False, max_keys=keys.size + 1,
+                  max_groups=(keys.size + 1) * P)
+    assert g["path"] == "hot_scatter", g["path"]
+    H.compare(g, O.run(key, ev["app"], ev["phase"], ev["dur_ns"], c, P, threads=8), raw=False)
+    app = ev["app"].copy()
+    app[n // 2] = cfg["num_apps"]  # one application past the table
+    ag = X.Aggregator(P, H.dev(c, np.int32), max_events=n, max_keys=keys.size, max_groups=keys.size * P)
+    try:
+        kt = H.dev(ev["key"], np.int32)
+        pt, dt = H.dev(ev["phase"], np.uint8), H.dev(ev["dur_ns"], np.int64)
+        with pytest.raises(X.AtrexError) as e:
+            ag.aggregate(kt, H.dev(app, np.int32), pt, dt)
+        assert e.value.status == X.E_OUT_OF_RANGE
+        G = ag.aggregate(kt, H.dev(ev["app"], np.int32), pt, dt)
+        assert ag.path_used() == "hot_scatter"
+        o = O.run(ev["key"], ev["app"], ev["phase"], ev["dur_ns"], c, P, threads=8)
+        assert G == o["key"].size
+    finally:
+        ag.close()
