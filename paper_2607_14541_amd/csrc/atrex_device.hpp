@@ -148,6 +148,12 @@ __device__ __forceinline__ uint32_t lds_home_bucket(uint32_t k, uint32_t NB) {
   return (uint32_t)(((uint64_t)(hash_mul(k) >> 8) * ((NB - 1) << 8)) >> 32);
 }
 
+// Bucket of key k in a table of NB four-slot buckets whose keys sit in their
+// bucket only (no window): floor(hash * NB / 2^32).
+__device__ __forceinline__ uint32_t lds_only_bucket(uint32_t k, uint32_t NB) {
+  return (uint32_t)(((uint64_t)hash_mul(k) * NB) >> 32);
+}
+
 // An invertible 32-bit mixer of xorshift-multiply rounds (shifts 16, 15, 16):
 // the "lowbias32" function found by C. Wellons' hash-prospector search
 // (published 2018, public domain).  Every round is a bijection, so the key can

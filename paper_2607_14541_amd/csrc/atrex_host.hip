@@ -847,7 +847,7 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
         hotS = std::min(hot_scatter_slots(P, hotBB), L.ldsSlots);
         if (hotS) {
           TIMED(c, "seed_image", hotS,
-                launch_seed_image(s, c->at<uint64_t>(L.sk[0]), 2 * kSeedSamples, hotS, c->at<uint32_t>(L.seed),
+                launch_seed_image(s, c->at<uint64_t>(L.sk[0]), 2 * kSeedSamples, hotS, 1, c->at<uint32_t>(L.seed),
                                   covered));
           hot = true;
         }

@@ -261,9 +261,11 @@ void launch_pass_b_lds(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t 
 void launch_seed(hipStream_t s, const uint32_t* key, uint64_t n, uint32_t NS, uint64_t* tab, uint32_t tab_cap,
                  uint32_t* cnt, uint64_t* list, uint32_t* idx, uint64_t* list2, uint32_t* idx2, void* sort_tmp,
                  uint32_t S, uint32_t* seed, unsigned long long* covered);
-// Another image, of S slots, from the sorted list launch_seed left in `list`.
-void launch_seed_image(hipStream_t s, const uint64_t* list, uint32_t tab_cap, uint32_t S, uint32_t* seed,
-                       unsigned long long* covered);
+// Another image, of S slots, from the sorted list launch_seed left in `list`:
+// window 2 places keys as the LDS engine looks them up (home bucket or the
+// next), window 1 in their own bucket only (the hot scatter's lookup).
+void launch_seed_image(hipStream_t s, const uint64_t* list, uint32_t tab_cap, uint32_t S, uint32_t window,
+                       uint32_t* seed, unsigned long long* covered);
 void launch_compact_rows(hipStream_t s, const GroupTables& gt, uint32_t P, const Rows& rows, uint32_t* err);
 
 // kernels_rows.hip

@@ -972,8 +972,9 @@ __global__ void k_unpack_scale(const uint64_t* __restrict__ sw, uint64_t G, uint
 // 0 = free); the occupied entries become sort keys (the inverted count:
 // ascending = hottest first, ties in table order); one workgroup then places the
 // hottest 2S keys, 1024 at a time in that order, into a tag image of S slots,
-// each in the first free slot of its window (home bucket and the next; a key
-// whose window is full is left out), and counts the sampled events the placed
+// each in the first free slot of its window (home bucket and the next, or its
+// own bucket only; a key whose window is full is left out), and counts the
+// sampled events the placed
 // keys cover.  Which keys are seeded changes only which events spill, never a
 // result.
 constexpr uint32_t kSeedCountBits = 19, kSeedCountMask = (1u << kSeedCountBits) - 1;
@@ -1015,8 +1016,10 @@ __global__ void k_seed_list(const unsigned long long* __restrict__ tab, const ui
   idx[h] = h;
 }
 
+// window 2: a key may sit in its home bucket or the next (lds_home_bucket,
+// the LDS engine's lookup); window 1: in its own bucket only (lds_only_bucket).
 __global__ __launch_bounds__(1024) void k_seed_build(const uint64_t* __restrict__ list, uint32_t L, uint32_t S,
-                                                     uint32_t* __restrict__ seed,
+                                                     uint32_t window, uint32_t* __restrict__ seed,
                                                      unsigned long long* __restrict__ covered) {
   extern __shared__ uint32_t s_img[];  // [S]
   __shared__ unsigned long long s_cov;
@@ -1032,8 +1035,8 @@ __global__ __launch_bounds__(1024) void k_seed_build(const uint64_t* __restrict_
     const uint32_t count = kSeedCountMask - (uint32_t)(e & kSeedCountMask);
     if (count) {
       const uint32_t k = (uint32_t)(e >> 32);
-      const uint32_t b = lds_home_bucket(k, NB);
-      for (uint32_t t = 4 * b; t < 4 * b + 8; ++t) {
+      const uint32_t b = window == 2 ? lds_home_bucket(k, NB) : lds_only_bucket(k, NB);
+      for (uint32_t t = 4 * b; t < 4 * b + 4 * window; ++t) {
         if (atomicCAS(&s_img[t], ATREX_EMPTY_KEY, k) == ATREX_EMPTY_KEY) {
           atomicAdd(&s_cov, (unsigned long long)count);
           break;
@@ -1082,14 +1085,14 @@ void launch_seed(hipStream_t s, const uint32_t* key, uint64_t n, uint32_t NS, ui
   hipLaunchKernelGGL(k_seed_list, dim3((tab_cap + 255) / 256), dim3(256), 0, s, (const unsigned long long*)tab, cnt,
                      tab_cap, list, idx);
   radix_sort_pairs(s, list, idx, list2, idx2, tab_cap, kSeedCountBits, sort_tmp);  // hottest first, free last
-  launch_seed_image(s, list, tab_cap, S, seed, covered);
+  launch_seed_image(s, list, tab_cap, S, 2, seed, covered);
 }
 
-void launch_seed_image(hipStream_t s, const uint64_t* list, uint32_t tab_cap, uint32_t S, uint32_t* seed,
-                       unsigned long long* covered) {
+void launch_seed_image(hipStream_t s, const uint64_t* list, uint32_t tab_cap, uint32_t S, uint32_t window,
+                       uint32_t* seed, unsigned long long* covered) {
   // candidates: the hottest 2S keys (colder ones rarely find a free slot in their window)
   hipLaunchKernelGGL(k_seed_build, dim3(1), dim3(1024), (size_t)S * 4, s, list, std::min<uint32_t>(tab_cap, 2 * S), S,
-                     seed, covered);
+                     window, seed, covered);
 }
 
 void launch_fold_totals(hipStream_t s, uint64_t* T, uint64_t* cnt, const uint64_t* T_run, const uint64_t* n_run,

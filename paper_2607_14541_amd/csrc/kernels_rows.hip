@@ -514,21 +514,17 @@ __device__ __forceinline__ uint32_t count_in(uint32_t* cnt, uint32_t b, bool act
 
 constexpr uint32_t kNoSlot = 0xFFFFFFFFu;
 
-// Key `k` is in a seeded table image of S slots (four-slot buckets; a key
-// sits in its home bucket or the next): its slot, else kNoSlot.  The
-// reserved key is never in the image (it marks free slots).
+// Key `k` is in a seeded table image of S slots whose keys sit in their own
+// four-slot bucket (lds_only_bucket): its slot, else kNoSlot.  The reserved
+// key is never in the image (it marks free slots).
 __device__ __forceinline__ uint32_t image_slot(const uint32_t* s_img, uint32_t S, uint32_t k) {
-  const uint32_t b = lds_home_bucket(k, S / 4);
-  const uint4 t0 = *(const uint4*)&s_img[4 * b], t1 = *(const uint4*)&s_img[4 * b + 4];
+  const uint32_t b = lds_only_bucket(k, S / 4);
+  const uint4 t = *(const uint4*)&s_img[4 * b];
   uint32_t x = kNoSlot;
-  x = t1.w == k ? 4 * b + 7 : x;
-  x = t1.z == k ? 4 * b + 6 : x;
-  x = t1.y == k ? 4 * b + 5 : x;
-  x = t1.x == k ? 4 * b + 4 : x;
-  x = t0.w == k ? 4 * b + 3 : x;
-  x = t0.z == k ? 4 * b + 2 : x;
-  x = t0.y == k ? 4 * b + 1 : x;
-  x = t0.x == k ? 4 * b : x;
+  x = t.w == k ? 4 * b + 3 : x;
+  x = t.z == k ? 4 * b + 2 : x;
+  x = t.y == k ? 4 * b + 1 : x;
+  x = t.x == k ? 4 * b : x;
   return k == ATREX_EMPTY_KEY ? kNoSlot : x;
 }
 
@@ -789,7 +785,7 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint3
 
 // Pass B of a seeded table and the partition scatter in one pass over the
 // events.  An event whose key is in the image `seed` (the sample's hottest
-// keys, each in its two-bucket window; the same image in every workgroup) is
+// keys, each in its own bucket; the same image in every workgroup) is
 // added to this workgroup's LDS table of S slots x P two-word accumulators;
 // every other event becomes a partition record, ranked, placed and written
 // out in tiles as in k_part_scatter (k_part_hist<true> with the same image
