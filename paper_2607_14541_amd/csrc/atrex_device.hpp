@@ -154,6 +154,38 @@ __device__ __forceinline__ uint32_t lds_only_bucket(uint32_t k, uint32_t NB) {
   return (uint32_t)(((uint64_t)hash_mul(k) * NB) >> 32);
 }
 
+// Wave-aggregated LDS counter increment: lanes whose bucket equals the first
+// active lane's add once together (a hot bucket costs one atomic per wave);
+// returns each lane's rank among the increments of its counter.
+__device__ __forceinline__ uint32_t count_in(uint32_t* cnt, uint32_t b, bool active) {
+  const uint64_t act = __ballot(active);
+  if (act == 0) return 0;
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t lead = __builtin_amdgcn_readlane(b, __ffsll((unsigned long long)act) - 1);
+  const uint64_t same = __ballot(active && b == lead);
+  uint32_t base = 0;
+  if (lane == (uint32_t)(__ffsll((unsigned long long)act) - 1)) base = atomicAdd(&cnt[lead], (uint32_t)__popcll(same));
+  base = __builtin_amdgcn_readlane(base, __ffsll((unsigned long long)act) - 1);
+  if (active && b == lead) return base + (uint32_t)__popcll(same & ((1ull << lane) - 1ull));
+  return active ? atomicAdd(&cnt[b], 1u) : 0u;
+}
+
+#define ATREX_NO_SLOT 0xFFFFFFFFu
+
+// Key `k` is in a seeded table image of S slots whose keys sit in their own
+// four-slot bucket (lds_only_bucket): its slot, else ATREX_NO_SLOT.  The
+// reserved key is never in the image (it marks free slots).
+__device__ __forceinline__ uint32_t image_slot(const uint32_t* s_img, uint32_t S, uint32_t k) {
+  const uint32_t b = lds_only_bucket(k, S / 4);
+  const uint4 t = *(const uint4*)&s_img[4 * b];
+  uint32_t x = ATREX_NO_SLOT;
+  x = t.w == k ? 4 * b + 3 : x;
+  x = t.z == k ? 4 * b + 2 : x;
+  x = t.y == k ? 4 * b + 1 : x;
+  x = t.x == k ? 4 * b : x;
+  return k == ATREX_EMPTY_KEY ? ATREX_NO_SLOT : x;
+}
+
 // An invertible 32-bit mixer of xorshift-multiply rounds (shifts 16, 15, 16):
 // the "lowbias32" function found by C. Wellons' hash-prospector search
 // (published 2018, public domain).  Every round is a bijection, so the key can

@@ -739,73 +739,8 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
   // clear the control words (the pass-A carry table is clear: init clears
   // it and every pass-A reduce leaves it so)
   launch_fill_u64(s, c->at<uint64_t>(L.ctrl), 64, 0);
-  // pass A, Eq. (2), and the Eq. (3) scale words of every (app, phase)
-  uint64_t* T = c->at<uint64_t>(L.T);
-  uint64_t* scale = c->at<uint64_t>(L.scale);
-  // invocation counts per (app, phase): per-block partials, then their sums
-  uint32_t* pcount = c->p.count ? c->at<uint32_t>(L.partC) : nullptr;
-  uint64_t* nA = c->p.count || c->p.time ? c->at<uint64_t>(L.nA) : nullptr;
-  if (c->p.time) {
-    // no applications: per-phase device time and counts with the range
-    // checks, and the identity scale (m = 2^55, rho = 0: each share is the
-    // duration itself) in both word forms
-    launch_fill_u64(s, T, 2 * (uint64_t)P, 0);
-    launch_fill_u64(s, nA, P, 0);
-    TIMED(c, "time_totals", na,
-          launch_time_totals(s, dA, P, (uint32_t)c->cus, vecA, (unsigned long long*)T, (unsigned long long*)nA,
-                             c->err()));
-    launch_fill_u64(s, scale, P, (uint64_t)64 << 56);
-    launch_fill_u64(s, c->at<uint64_t>(L.bscale), P, ((uint64_t)63 << 56) | ((uint64_t)1 << 55));
-  } else if (L.passA == 0 && vecA) {
-    // one workgroup per CU (two groups of loads in flight per lane): two per
-    // CU ran as one after the other (the SIMDs favour the older one) and
-    // doubled the partial rows for the reduce
-    uint64_t nb = std::min<uint64_t>((uint64_t)c->cus, L.partA_rows);
-    nb = std::max<uint64_t>(1, std::min<uint64_t>(nb, (na / 4 + kPassAThreads - 1) / kPassAThreads));
-    TIMED(c, "pass_a", na,
-          launch_pass_a_lds(s, dA, A, P, (uint32_t)nb, c->at<unsigned long long>(L.partA),
-                            c->at<unsigned long long>(L.carryA), pcount, c->err()));
-    TIMED(c, "pass_a_reduce", GA,
-          launch_pass_a_reduce(s, c->at<unsigned long long>(L.partA), (uint32_t)nb, (uint32_t)GA,
-                               c->at<unsigned long long>(L.carryA), T, c->app_weight, c->Csum(), P, scale,
-                               c->at<void>(L.bscale), pcount, nA));
-  } else if (L.passA == 3 && vecA) {
-    const uint32_t bins = pass_a_range_bins(c->p.count);
-    const uint32_t R = (uint32_t)((GA + bins - 1) / bins);
-    const uint32_t GR = (uint32_t)((GA + R - 1) / R);
-    TIMED(c, "pass_a_range", na,
-          launch_pass_a_range(s, dA, A, P, GR, R, kPassASlices, c->at<uint32_t>(L.partA),
-                              c->at<unsigned long long>(L.carryA), pcount, c->err()));
-    TIMED(c, "pass_a_reduce", GA,
-          launch_pass_a_reduce32(s, c->at<uint32_t>(L.partA), kPassASlices, (uint32_t)GA,
-                                 c->at<unsigned long long>(L.carryA), T, c->app_weight, c->Csum(), P, scale,
-                                 c->at<void>(L.bscale), pcount, nA));
-  } else if (L.passA == 1 && vecA) {
-    const uint64_t nb = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)c->cus, kMaxWG));
-    TIMED(c, "pass_a", na,
-          launch_pass_a_lds32(s, dA, A, P, (uint32_t)nb, c->at<uint32_t>(L.partA), c->at<unsigned long long>(L.carryA),
-                              pcount, c->err()));
-    TIMED(c, "pass_a_reduce", GA,
-          launch_pass_a_reduce32(s, c->at<uint32_t>(L.partA), (uint32_t)nb, (uint32_t)GA,
-                                 c->at<unsigned long long>(L.carryA), T, c->app_weight, c->Csum(), P, scale,
-                                 c->at<void>(L.bscale), pcount, nA));
-  } else {
-    launch_fill_u64(s, T, GA * 2, 0);
-    if (nA) launch_fill_u64(s, nA, GA, 0);
-    TIMED(c, "pass_a_global", na,
-          launch_pass_a_global(s, dA, A, P, (uint32_t)std::max<uint64_t>(1, (uint64_t)c->cus * 8), (unsigned long long*)T,
-                               (unsigned long long*)nA, c->err()));
-    // scale, Eq. (3) (the column-sum kernels of the other modes compute it with T)
-    TIMED(c, "scale", GA, launch_scale(s, T, c->app_weight, c->Csum(), A, P, scale, c->at<void>(L.bscale)));
-  }
-  if (c->p.incr) {
-    // the totals of the whole log: those folded before plus the new events'
-    // (skipped on the device after a range error), and the scale from them
-    launch_fold_totals(s, T, nA, c->at<uint64_t>(L.T_run), c->at<uint64_t>(L.n_run), GA, c->err());
-    TIMED(c, "scale", GA, launch_scale(s, T, c->app_weight, c->Csum(), A, P, scale, c->at<void>(L.bscale)));
-  }
-  // pass B, Eq. (2)-(3): every engine emits rows (key << 3 | phase, Q96 sum)
-  const Rows rows = c->rows();
+  // The engine of pass B, chosen before pass A: the seed step below only
+  // reads keys, and the hot scatter's histogram can then ride in pass A.
   atrex_path path = c->path;
   if (path == ATREX_PATH_AUTO) path = (c->p.max_keys <= L.ldsSlots) ? ATREX_PATH_LDS_HASH : ATREX_PATH_RADIX_SORT;
   if (c->p.compact) path = ATREX_PATH_GLOBAL_HASH;  // the only engine the compact layout holds
@@ -854,15 +789,101 @@ atrex_status aggregate_enqueue(atrex_ctx* c, const atrex_events* ev, AggRun* a) 
       }
     }
   }
+  // the hot scatter's partition: ranges of the whole event array (pass A may
+  // see only the new events of a log), counted inside the range-split pass A
+  // when that is pass A's engine
+  HistJob hj{};
+  bool hist_in_a = false;
+  if (hot) {
+    hj.key = d.key;
+    hj.n = n;
+    hj.per = ((n + nwg - 1) / nwg + 3) / 4 * 4;
+    hj.nwg = nwg;
+    hj.BB = hotBB;
+    hj.S = hotS;
+    hj.seed = seed;
+    hj.H = c->at<uint32_t>(L.H);
+    hist_in_a = !c->p.time && L.passA == 3 && vecA;
+  }
+  // pass A, Eq. (2), and the Eq. (3) scale words of every (app, phase)
+  uint64_t* T = c->at<uint64_t>(L.T);
+  uint64_t* scale = c->at<uint64_t>(L.scale);
+  // invocation counts per (app, phase): per-block partials, then their sums
+  uint32_t* pcount = c->p.count ? c->at<uint32_t>(L.partC) : nullptr;
+  uint64_t* nA = c->p.count || c->p.time ? c->at<uint64_t>(L.nA) : nullptr;
+  if (c->p.time) {
+    // no applications: per-phase device time and counts with the range
+    // checks, and the identity scale (m = 2^55, rho = 0: each share is the
+    // duration itself) in both word forms
+    launch_fill_u64(s, T, 2 * (uint64_t)P, 0);
+    launch_fill_u64(s, nA, P, 0);
+    TIMED(c, "time_totals", na,
+          launch_time_totals(s, dA, P, (uint32_t)c->cus, vecA, (unsigned long long*)T, (unsigned long long*)nA,
+                             c->err()));
+    launch_fill_u64(s, scale, P, (uint64_t)64 << 56);
+    launch_fill_u64(s, c->at<uint64_t>(L.bscale), P, ((uint64_t)63 << 56) | ((uint64_t)1 << 55));
+  } else if (L.passA == 0 && vecA) {
+    // one workgroup per CU (two groups of loads in flight per lane): two per
+    // CU ran as one after the other (the SIMDs favour the older one) and
+    // doubled the partial rows for the reduce
+    uint64_t nb = std::min<uint64_t>((uint64_t)c->cus, L.partA_rows);
+    nb = std::max<uint64_t>(1, std::min<uint64_t>(nb, (na / 4 + kPassAThreads - 1) / kPassAThreads));
+    TIMED(c, "pass_a", na,
+          launch_pass_a_lds(s, dA, A, P, (uint32_t)nb, c->at<unsigned long long>(L.partA),
+                            c->at<unsigned long long>(L.carryA), pcount, c->err()));
+    TIMED(c, "pass_a_reduce", GA,
+          launch_pass_a_reduce(s, c->at<unsigned long long>(L.partA), (uint32_t)nb, (uint32_t)GA,
+                               c->at<unsigned long long>(L.carryA), T, c->app_weight, c->Csum(), P, scale,
+                               c->at<void>(L.bscale), pcount, nA));
+  } else if (L.passA == 3 && vecA) {
+    // with the histogram inside, its counters and image take LDS from the bins
+    const uint32_t hist_bins =
+        hist_in_a ? (uint32_t)((pass_a_hist_bytes(hj) + 16 + (c->p.count ? 7 : 3)) / (c->p.count ? 8 : 4)) : 0;
+    const uint32_t bins = pass_a_range_bins(c->p.count) - hist_bins;
+    const uint32_t R = (uint32_t)((GA + bins - 1) / bins);
+    const uint32_t GR = (uint32_t)((GA + R - 1) / R);
+    TIMED(c, "pass_a_range", na,
+          launch_pass_a_range(s, dA, A, P, GR, R, kPassASlices, c->at<uint32_t>(L.partA),
+                              c->at<unsigned long long>(L.carryA), pcount, hist_in_a ? &hj : nullptr, c->err()));
+    TIMED(c, "pass_a_reduce", GA,
+          launch_pass_a_reduce32(s, c->at<uint32_t>(L.partA), kPassASlices, (uint32_t)GA,
+                                 c->at<unsigned long long>(L.carryA), T, c->app_weight, c->Csum(), P, scale,
+                                 c->at<void>(L.bscale), pcount, nA));
+  } else if (L.passA == 1 && vecA) {
+    const uint64_t nb = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)c->cus, kMaxWG));
+    TIMED(c, "pass_a", na,
+          launch_pass_a_lds32(s, dA, A, P, (uint32_t)nb, c->at<uint32_t>(L.partA), c->at<unsigned long long>(L.carryA),
+                              pcount, c->err()));
+    TIMED(c, "pass_a_reduce", GA,
+          launch_pass_a_reduce32(s, c->at<uint32_t>(L.partA), (uint32_t)nb, (uint32_t)GA,
+                                 c->at<unsigned long long>(L.carryA), T, c->app_weight, c->Csum(), P, scale,
+                                 c->at<void>(L.bscale), pcount, nA));
+  } else {
+    launch_fill_u64(s, T, GA * 2, 0);
+    if (nA) launch_fill_u64(s, nA, GA, 0);
+    TIMED(c, "pass_a_global", na,
+          launch_pass_a_global(s, dA, A, P, (uint32_t)std::max<uint64_t>(1, (uint64_t)c->cus * 8), (unsigned long long*)T,
+                               (unsigned long long*)nA, c->err()));
+    // scale, Eq. (3) (the column-sum kernels of the other modes compute it with T)
+    TIMED(c, "scale", GA, launch_scale(s, T, c->app_weight, c->Csum(), A, P, scale, c->at<void>(L.bscale)));
+  }
+  if (c->p.incr) {
+    // the totals of the whole log: those folded before plus the new events'
+    // (skipped on the device after a range error), and the scale from them
+    launch_fold_totals(s, T, nA, c->at<uint64_t>(L.T_run), c->at<uint64_t>(L.n_run), GA, c->err());
+    TIMED(c, "scale", GA, launch_scale(s, T, c->app_weight, c->Csum(), A, P, scale, c->at<void>(L.bscale)));
+  }
+  // pass B, Eq. (2)-(3): every engine emits rows (key << 3 | phase, Q96 sum)
+  const Rows rows = c->rows();
   if (hot) {
     c->path_used = "hot_scatter";
     PartSource src{};
     src.ev = d;
-    src.per = ((n + nwg - 1) / nwg + 3) / 4 * 4;
+    src.per = hj.per;
     src.spill = false;
     uint32_t* H = c->at<uint32_t>(L.H);
     uint32_t* O = c->at<uint32_t>(L.O);
-    TIMED(c, "part_hist_cold", n, launch_part_hist_cold(s, src, nwg, hotBB, H, seed, hotS));
+    if (!hist_in_a) TIMED(c, "part_hist_cold", n, launch_part_hist_cold(s, src, nwg, hotBB, H, seed, hotS));
     exclusive_scan_u32(s, H, O, ((uint64_t)1 << hotBB) * nwg, c->at<void>(L.scan_tmp));
     TIMED(c, "hot_scatter", n,
           launch_hot_scatter(s, src, nwg, A, P, scale, c->at<uint64_t>(L.bscale), hotBB, O, c->at<uint64_t>(L.rec),

@@ -57,6 +57,18 @@ struct PartSource {
   bool spill;
 };
 
+// The hot scatter's partition histogram as a side job of another kernel:
+// range w = [w per, (w + 1) per) of key[0, n) (per a multiple of 4), its keys
+// not in the seeded image (S slots, one bucket per key) counted per bucket
+// (top BB bits of hash32) into H[bucket * nwg + w].
+struct HistJob {
+  const uint32_t* key;
+  uint64_t n, per;
+  uint32_t nwg, BB, S;
+  const uint32_t* seed;
+  uint32_t* H;
+};
+
 // Per-owner sorted group lists written by the owner merge of the LDS engine.
 struct OwnerLists {
   uint64_t* rk;      // [ATREX_OWNERS][cap] sort keys key << 3 | phase, ascending within an owner
@@ -231,8 +243,13 @@ void launch_pass_a_lds32(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_
 void launch_pass_a_reduce32(hipStream_t s, const uint32_t* partial, uint32_t nb, uint32_t G,
                             unsigned long long* ext, uint64_t* T, const uint32_t* c, const uint64_t* Csum,
                             uint32_t P, uint64_t* scale, void* bscale, const uint32_t* pcount, uint64_t* cnt);
+// hj (nullable): the hot scatter's partition histogram taken inside the
+// range-split pass A (workgroup w < hj->nwg counts range w's cold keys); the
+// launch then needs pass_a_hist_bytes(*hj) more LDS per workgroup.
 void launch_pass_a_range(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t GR, uint32_t R,
-                         uint32_t slices, uint32_t* partial, unsigned long long* ext, uint32_t* pcount, uint32_t* err);
+                         uint32_t slices, uint32_t* partial, unsigned long long* ext, uint32_t* pcount,
+                         const HistJob* hj, uint32_t* err);
+size_t pass_a_hist_bytes(const HistJob& hj);
 void launch_pass_a_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
                           unsigned long long* T, unsigned long long* cnt, uint32_t* err);
 void launch_unpack_scale(hipStream_t s, const uint64_t* sw, uint64_t G, uint64_t* mant, int32_t* rho);

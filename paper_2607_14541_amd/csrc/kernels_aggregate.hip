@@ -137,26 +137,63 @@ constexpr int RANGE_DEPTH = 6;  // groups of four events in flight per lane in k
 // once and from that XCD's L2 for the others.  Each lane keeps RANGE_DEPTH
 // groups of four events in flight.  COUNT: a u32
 // count table after the GR counters and their spares.
-template <int BLOCK, bool COUNT>
+//
+// HIST: workgroup w < hj.nwg also takes the partition histogram of the hot
+// scatter's range w (as k_part_hist<true>: the keys outside the seeded image,
+// per bucket), one group of four keys per lane after every RANGE_DEPTH groups
+// of events, in the time this pass spends waiting on L2.
+template <int BLOCK, bool COUNT, bool HIST>
 __global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A, uint32_t P, uint32_t G,
                                                         uint32_t GR, uint32_t R, uint32_t slices,
                                                         uint32_t* __restrict__ partial,
                                                         unsigned long long* __restrict__ ext,
-                                                        uint32_t* __restrict__ pcount, uint32_t* __restrict__ err) {
+                                                        uint32_t* __restrict__ pcount, HistJob hj,
+                                                        uint32_t* __restrict__ err) {
   extern __shared__ uint32_t s32[];
   uint32_t* s_n = s32 + GR + 64;  // COUNT only
+  // HIST: bucket counters and the image, 16-byte aligned after the tables
+  uint32_t* s_h = s32 + (((COUNT ? 2 * GR : GR) + 64 + 3) & ~3u);
+  uint32_t* s_img = s_h + (HIST ? (1u << hj.BB) : 0u);
   const uint32_t xcd = blockIdx.x % 8, k = blockIdx.x / 8;
   const uint32_t slice = (k / R) * 8 + xcd, range = k % R;
-  if (slice >= slices) return;  // whole workgroup
-  const uint32_t g0 = range * GR, g1 = min(G, g0 + GR);
+  const bool sums = slice < slices;                 // uniform over the workgroup
+  const bool hist = HIST && blockIdx.x < hj.nwg;    // uniform
+  if (!sums && !hist) return;
+  const uint32_t g0 = range * GR, g1 = sums ? min(G, g0 + GR) : g0;
   for (uint32_t g = threadIdx.x; g < g1 - g0; g += BLOCK) {
     s32[g] = 0;
     if (COUNT) s_n[g] = 0;
   }
+  if (hist) {
+    for (uint32_t i = threadIdx.x; i < (1u << hj.BB); i += BLOCK) s_h[i] = 0;
+    for (uint32_t i = threadIdx.x; i < hj.S; i += BLOCK) s_img[i] = hj.seed[i];
+  }
   __syncthreads();
+  // the histogram's range [hb, he) and its groups of four keys
+  const uint64_t hb = hist ? min(hj.n, (uint64_t)blockIdx.x * hj.per) : 0;
+  const uint64_t he = hist ? min(hj.n, hb + hj.per) : 0;
+  const uint64_t hng = (he - hb) / 4, hiters = (hng + BLOCK - 1) / BLOCK;
+  const uint32_t hsh = 32 - hj.BB;
+  uint64_t hi = 0;
+  v4u hk = {0, 0, 0, 0};
+  auto hload = [&](uint64_t j) {
+    const uint64_t gi = j * BLOCK + threadIdx.x;
+    if (gi < hng) hk = __builtin_nontemporal_load((const v4u*)(hj.key + hb + 4 * gi));
+  };
+  auto hstep = [&]() {  // uniform: every lane of the workgroup calls it
+    const bool v = hi * BLOCK + threadIdx.x < hng;
+    const v4u kk = hk;
+    if (hi + 1 < hiters) hload(hi + 1);
+    (void)count_in(s_h, hash32(kk.x) >> hsh, v && image_slot(s_img, hj.S, kk.x) == ATREX_NO_SLOT);
+    (void)count_in(s_h, hash32(kk.y) >> hsh, v && image_slot(s_img, hj.S, kk.y) == ATREX_NO_SLOT);
+    (void)count_in(s_h, hash32(kk.z) >> hsh, v && image_slot(s_img, hj.S, kk.z) == ATREX_NO_SLOT);
+    (void)count_in(s_h, hash32(kk.w) >> hsh, v && image_slot(s_img, hj.S, kk.w) == ATREX_NO_SLOT);
+    ++hi;
+  };
+  if (HIST && hiters) hload(0);
   const uint64_t n = ev.n;
   const uint64_t per = ((n + slices - 1) / slices + 3) / 4 * 4;
-  const uint64_t b = min(n, (uint64_t)slice * per), e = min(n, b + per);
+  const uint64_t b = sums ? min(n, (uint64_t)slice * per) : 0, e = sums ? min(n, b + per) : 0;
   bool bad = false;
   auto one = [&](uint32_t a, uint32_t ph, int64_t dd) {
     const bool ok = a < A && ph < P && dd >= 0;
@@ -258,15 +295,27 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A
       process(it + k, x[k]);
       if (it + k + RANGE_DEPTH < iters) load(it + k + RANGE_DEPTH, x[k]);
     }
+    if (HIST && hi < hiters) hstep();
   }
   for (uint64_t i = b + 4 * ng + threadIdx.x; i < e; i += BLOCK) one(ev.app[i], ev.phase[i], ev.dur[i]);
   flag_error(err, bad, ATREX_ERRBIT_RANGE);
-  __syncthreads();
-  uint32_t* out = partial + (size_t)slice * G;
-  for (uint32_t g = threadIdx.x; g < g1 - g0; g += BLOCK) {
-    out[g0 + g] = s32[g];
-    if (COUNT) pcount[(size_t)slice * G + g0 + g] = s_n[g];
+  if (HIST) {
+    while (hi < hiters) hstep();
+    for (uint64_t i = hb + 4 * hng + threadIdx.x; i < he; i += BLOCK) {  // the range's last keys
+      const uint32_t kk = hj.key[i];
+      if (image_slot(s_img, hj.S, kk) == ATREX_NO_SLOT) atomicAdd(&s_h[hash32(kk) >> hsh], 1u);
+    }
   }
+  __syncthreads();
+  if (sums) {
+    uint32_t* out = partial + (size_t)slice * G;
+    for (uint32_t g = threadIdx.x; g < g1 - g0; g += BLOCK) {
+      out[g0 + g] = s32[g];
+      if (COUNT) pcount[(size_t)slice * G + g0 + g] = s_n[g];
+    }
+  }
+  if (hist)
+    for (uint32_t i = threadIdx.x; i < (1u << hj.BB); i += BLOCK) hj.H[(size_t)i * hj.nwg + blockIdx.x] = s_h[i];
 }
 
 // Pass A straight into global 128-bit accumulators (any number of (a, ph));
@@ -1147,16 +1196,25 @@ void launch_pass_a_reduce32(hipStream_t s, const uint32_t* partial, uint32_t nb,
 }
 
 void launch_pass_a_range(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t GR, uint32_t R,
-                         uint32_t slices, uint32_t* partial, unsigned long long* ext, uint32_t* pcount, uint32_t* err) {
+                         uint32_t slices, uint32_t* partial, unsigned long long* ext, uint32_t* pcount,
+                         const HistJob* hj, uint32_t* err) {
   const uint32_t G = A * P;
   const uint32_t nblocks = ((slices + 7) / 8) * 8 * R;
-  if (pcount)
-    hipLaunchKernelGGL((k_pass_a_range<1024, true>), dim3(nblocks), dim3(1024), ((size_t)2 * GR + 64) * 4, s, ev, A,
-                       P, G, GR, R, slices, partial, ext, pcount, err);
-  else
-    hipLaunchKernelGGL((k_pass_a_range<1024, false>), dim3(nblocks), dim3(1024), ((size_t)GR + 64) * 4, s, ev, A, P,
-                       G, GR, R, slices, partial, ext, pcount, err);
+  const size_t tables = ((((size_t)(pcount ? 2 * GR : GR) + 64 + 3) & ~(size_t)3)) * 4;
+  const HistJob none{};
+#define ATREX_RANGE(C, H)                                                                                    \
+  hipLaunchKernelGGL((k_pass_a_range<1024, C, H>), dim3(std::max(nblocks, H ? hj->nwg : 0u)), dim3(1024),  \
+                     tables + (H ? pass_a_hist_bytes(*hj) : 0), s, ev, A, P, G, GR, R, slices, partial, ext,  \
+                     pcount, H ? *hj : none, err)
+  if (hj) {
+    if (pcount) ATREX_RANGE(true, true); else ATREX_RANGE(false, true);
+  } else {
+    if (pcount) ATREX_RANGE(true, false); else ATREX_RANGE(false, false);
+  }
+#undef ATREX_RANGE
 }
+
+size_t pass_a_hist_bytes(const HistJob& hj) { return ((size_t)4 << hj.BB) + (size_t)4 * hj.S; }
 
 void launch_pass_a_global(hipStream_t s, const EventsDev& ev, uint32_t A, uint32_t P, uint32_t nblocks,
                           unsigned long long* T, unsigned long long* cnt, uint32_t* err) {
@@ -1236,7 +1294,8 @@ void launch_compact_rows(hipStream_t s, const GroupTables& gt, uint32_t P, const
 hipError_t set_kernel_smem_limits() {
   const void* pass_a[] = {(const void*)k_pass_a_lds<1024, false>,   (const void*)k_pass_a_lds<1024, true>,
                           (const void*)k_pass_a_lds32<1024, false>, (const void*)k_pass_a_lds32<1024, true>,
-                          (const void*)k_pass_a_range<1024, false>, (const void*)k_pass_a_range<1024, true>};
+                          (const void*)k_pass_a_range<1024, false, false>, (const void*)k_pass_a_range<1024, true, false>,
+                          (const void*)k_pass_a_range<1024, false, true>, (const void*)k_pass_a_range<1024, true, true>};
   hipError_t e = hipSuccess;
   for (const void* f : pass_a) {
     e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);

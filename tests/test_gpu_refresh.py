@@ -71,6 +71,35 @@ def test_refresh_equals_the_whole_log(ci, path):
         ag.close()
 
 
+def test_refresh_on_the_hot_scatter():
+    """A log long enough for the seeding (at least 2^22 events) with the 1B
+    workload's keys and no raw time: pass B over the whole log takes the hot
+    scatter; every refresh still equals the oracle over the log so far."""
+    n = (1 << 22) + 4099
+    ends = [(1 << 22) + 1, n]
+    cfg, ev, c, keys, s = _log(3, n)
+    P = cfg["num_phases"]
+    d = {k: H.dev(ev[k], dt) for k, dt in (("key", np.int32), ("app", np.int32), ("phase", np.uint8),
+                                             ("dur_ns", np.int64))}
+    sk, sv = H.dev(keys, np.int32), H.dev(s, np.float64)
+    ag = X.Aggregator(P, H.dev(c, np.int32), max_events=n, max_keys=keys.size, max_groups=keys.size * P,
+                      max_score=keys.size, incremental=True)
+    try:
+        prev = 0
+        for end in ends:
+            H.say("refresh on the hot scatter, log", end, "new", end - prev)
+            ag.reset()
+            ag.refresh(d["key"][:end], d["app"][:end], d["phase"][:end], d["dur_ns"][:end], end - prev)
+            assert ag.path_used() == "hot_scatter", ag.path_used()
+            g = _outputs(ag, sk, sv)
+            o = O.run(ev["key"][:end], ev["app"][:end], ev["phase"][:end], ev["dur_ns"][:end], c, P,
+                      score_key=keys, s=s, threads=8)
+            H.compare(g, o, raw=False, score=True)
+            prev = end
+    finally:
+        ag.close()
+
+
 def test_refresh_through_the_one_call_path():
     """atrex_run on an incremental context folds the events past those folded."""
     n = (1 << 20) + 5
