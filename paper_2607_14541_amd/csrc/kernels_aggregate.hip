@@ -180,14 +180,19 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_range(EventsDev ev, uint32_t A
     const uint64_t gi = j * BLOCK + threadIdx.x;
     if (gi < hng) hk = __builtin_nontemporal_load((const v4u*)(hj.key + hb + 4 * gi));
   };
+  // plain no-return LDS atomics: the keys outside the image are the colder
+  // ones, spread over the buckets (the hot keys are the image's)
   auto hstep = [&]() {  // uniform: every lane of the workgroup calls it
     const bool v = hi * BLOCK + threadIdx.x < hng;
     const v4u kk = hk;
     if (hi + 1 < hiters) hload(hi + 1);
-    (void)count_in(s_h, hash32(kk.x) >> hsh, v && image_slot(s_img, hj.S, kk.x) == ATREX_NO_SLOT);
-    (void)count_in(s_h, hash32(kk.y) >> hsh, v && image_slot(s_img, hj.S, kk.y) == ATREX_NO_SLOT);
-    (void)count_in(s_h, hash32(kk.z) >> hsh, v && image_slot(s_img, hj.S, kk.z) == ATREX_NO_SLOT);
-    (void)count_in(s_h, hash32(kk.w) >> hsh, v && image_slot(s_img, hj.S, kk.w) == ATREX_NO_SLOT);
+    const uint32_t kv[4] = {kk.x, kk.y, kk.z, kk.w};
+    bool cold[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cold[j] = v && image_slot(s_img, hj.S, kv[j]) == ATREX_NO_SLOT;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (cold[j]) atomicAdd(&s_h[hash32(kv[j]) >> hsh], 1u);
     ++hi;
   };
   if (HIST && hiters) hload(0);
