@@ -541,10 +541,20 @@ __global__ __launch_bounds__(1024) void k_part_hist(PartSource src, uint32_t BB,
         const bool v = (it + d) * blockDim.x + threadIdx.x < ng;
         const v4u k = ring[d];
         if (it + d + HIST_DEPTH < iters) load(it + d + HIST_DEPTH, ring[d]);
-        (void)count_in(s_h, hash32(k.x) >> sh, v && cold(k.x));
-        (void)count_in(s_h, hash32(k.y) >> sh, v && cold(k.y));
-        (void)count_in(s_h, hash32(k.z) >> sh, v && cold(k.z));
-        (void)count_in(s_h, hash32(k.w) >> sh, v && cold(k.w));
+        if (HOT) {  // the keys outside the image are spread over the buckets: plain atomics
+          const uint32_t kv[4] = {k.x, k.y, k.z, k.w};
+          bool c[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) c[j] = v && cold(kv[j]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (c[j]) atomicAdd(&s_h[hash32(kv[j]) >> sh], 1u);
+        } else {
+          (void)count_in(s_h, hash32(k.x) >> sh, v);
+          (void)count_in(s_h, hash32(k.y) >> sh, v);
+          (void)count_in(s_h, hash32(k.z) >> sh, v);
+          (void)count_in(s_h, hash32(k.w) >> sh, v);
+        }
       }
     }
     for (uint64_t i = e4 + threadIdx.x; i < e; i += blockDim.x) {
@@ -841,8 +851,11 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter_hot(PartSource src, u
       if (!ok) hs[j] = kNoSlot;  // an invalid event adds nothing (the call fails on it)
       hh[j] = hash32(key);
     }
+    // ranks from plain LDS atomics: the records' keys are the colder ones,
+    // spread over the buckets
 #pragma unroll
-    for (uint32_t j = 0; j < SC_EPT; ++j) rk[j] |= count_in(cnt, hh[j] >> lowbits, (rk[j] >> 3) & 1u) << 4;
+    for (uint32_t j = 0; j < SC_EPT; ++j)
+      if ((rk[j] >> 3) & 1u) rk[j] |= atomicAdd(&cnt[hh[j] >> lowbits], 1u) << 4;
     __syncthreads();
     // exclusive scan of the tile's bucket counts; the previous tile's counts
     // advance the positions, and the next tile's counters are cleared
