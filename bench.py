@@ -430,7 +430,28 @@ def bench_join(args) -> int:
     value = n * steps / elapsed / 1e9
     r = res["r"]
     L = r["labelled"]
-    log("step %.3f ms (%.3f ms between hipEvents), %.2f G records/s, labelled %d" % (ms_step, ms_dev, value, L))
+    log("step %.3f ms (%.3f ms between hipEvents), %.2f G records/s, labelled %d, method %s" % (
+        ms_step, ms_dev, value, L, r["method"]))
+    # the other method on the same trace, for comparison (not the metric)
+    other = "hash" if r["method"] == "partition" else None
+    ms_other = None
+    if other:
+        c2 = X.Correlator(n, m, device=dev, method=other)
+        c2.run(k, h, iv, out=out, source=src)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        reps = max(3, steps // 4)
+        for _ in range(reps):
+            c2.run(k, h, iv, out=out, source=src)
+        e1.record()
+        torch.cuda.synchronize()
+        ms_other = e0.elapsed_time(e1) / reps
+        del c2
+        log("the %s join on the same trace: %.3f ms" % (other, ms_other))
+        step()  # the timed method's outputs again, for the parity check
+        torch.cuda.synchronize()
+        r = res["r"]
     parity = None
     if not args.no_parity:
         msk = tr["kind"] < 3
@@ -445,7 +466,8 @@ def bench_join(args) -> int:
         log("parity", "ok" if not bad else "MISMATCH %s" % bad)
     alg = JOIN_READ_PER_KERNEL * n + JOIN_WRITE_PER_EVENT * L + JOIN_READ_PER_HOST * m
     achieved = alg / (ms_dev * 1e-3) / 1e9
-    roofline = {"bound": "hbm", "kernel": "atrex_correlate (build, probe, scan, emit)", "achieved": round(achieved, 1),
+    roofline = {"bound": "hbm", "kernel": "atrex_correlate (%s join: every kernel of the call)" % r["method"],
+                "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
                 "algorithmic_bytes_per_launch": alg, "avg_launch_ms": round(ms_dev, 4)}
     cpu = None
@@ -466,6 +488,7 @@ def bench_join(args) -> int:
         "config": {"workload": jc["name"], "kernel_records": n, "host_records": m, "intervals": mi,
                    "streams": jc["streams"], "seed": jc["seed"], "parallelism": "none", "entry": "atrex_correlate"},
         "labelled": L, "by_source": r["by_source"], "ms_between_events": round(ms_dev, 4),
+        "method": r["method"], "ms_hash_join": round(ms_other, 4) if ms_other else None,
         "parity": parity, "roofline": roofline, "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -321,17 +321,32 @@ typedef struct {            /* DEVICE outputs, out_capacity rows */
   int64_t *dur_ns;
 } atrex_event_out;
 
+/* Join methods (same results; they differ in how the host record of an id
+ * is found):
+ * HASH: the host records go into two open-addressing tables in device
+ *   memory (one per id space), probed once per id of a kernel record;
+ * PARTITION: host records and probes are scattered by the id's hash into
+ *   buckets of about 2048 host records, each joined in LDS by one workgroup;
+ *   for at most 2048 * 2^15 host records; it falls back to HASH when a
+ *   bucket's table fills up (ids that crowd one bucket);
+ * AUTO: PARTITION when max_host allows it, else HASH. */
+#define ATREX_JOIN_AUTO 0u
+#define ATREX_JOIN_HASH 1u
+#define ATREX_JOIN_PARTITION 2u
+
 typedef struct {
   uint64_t max_kernels;     /* kernel records per call, < 2^31 */
   uint64_t max_host;        /* host records per call, < 2^31 */
   void *workspace;          /* DEVICE, caller-owned, 256-byte aligned */
   size_t workspace_bytes;
   void *stream;             /* hipStream_t; NULL = default stream */
+  uint32_t method;          /* ATREX_JOIN_*; PARTITION with max_host above its limit is INVALID_ARG */
 } atrex_join_params;
 
 typedef struct {
   uint64_t labelled;        /* events written (or wanted, on CAPACITY) */
   uint64_t by_source[4];    /* kernel records labelled by correlation id, by anchor, by interval; unlabelled */
+  uint32_t method_used;     /* ATREX_JOIN_HASH or ATREX_JOIN_PARTITION */
 } atrex_join_result;
 
 /* Workspace size for p (workspace fields ignored).  HOST: p, bytes. */

@@ -91,11 +91,14 @@ class _EventOut(ctypes.Structure):
 
 class _JoinParams(ctypes.Structure):
     _fields_ = [("max_kernels", ctypes.c_uint64), ("max_host", ctypes.c_uint64), ("workspace", ctypes.c_void_p),
-                ("workspace_bytes", ctypes.c_size_t), ("stream", ctypes.c_void_p)]
+                ("workspace_bytes", ctypes.c_size_t), ("stream", ctypes.c_void_p), ("method", ctypes.c_uint32)]
 
 
 class _JoinResult(ctypes.Structure):
-    _fields_ = [("labelled", ctypes.c_uint64), ("by_source", ctypes.c_uint64 * 4)]
+    _fields_ = [("labelled", ctypes.c_uint64), ("by_source", ctypes.c_uint64 * 4), ("method_used", ctypes.c_uint32)]
+
+
+JOIN_METHODS = {"auto": 0, "hash": 1, "partition": 2}
 
 
 class _ShareResult(ctypes.Structure):
@@ -609,7 +612,9 @@ class Correlator:
     """Host/device correlation join (§3.1) with a workspace for up to
     max_kernels kernel records and max_host host records: run() labels
     kernel records by correlation id, graph anchor or stream interval and
-    returns the labelled events in kernel-record order."""
+    returns the labelled events in kernel-record order.  method: "auto",
+    "hash" or "partition" (include/atrex.h, ATREX_JOIN_*); run() reports the
+    one used."""
 
     KERNEL_FIELDS = (("corr", torch.int64), ("anchor", torch.int64), ("stream", torch.int32),
                      ("start_ns", torch.int64), ("end_ns", torch.int64))
@@ -618,10 +623,11 @@ class Correlator:
     INTERVAL_FIELDS = (("stream", torch.int32), ("begin_ns", torch.int64), ("end_ns", torch.int64),
                        ("key", torch.int32), ("app", torch.int32), ("phase", torch.uint8))
 
-    def __init__(self, max_kernels: int, max_host: int, device=None, stream: torch.cuda.Stream | None = None):
+    def __init__(self, max_kernels: int, max_host: int, device=None, stream: torch.cuda.Stream | None = None,
+                 method: str = "auto"):
         self.device = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
         self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
-        self.p = _JoinParams(int(max_kernels), int(max_host), None, 0, self.stream.cuda_stream)
+        self.p = _JoinParams(int(max_kernels), int(max_host), None, 0, self.stream.cuda_stream, JOIN_METHODS[method])
         nb = ctypes.c_size_t()
         _check(_lib().atrex_join_workspace_bytes(ctypes.byref(self.p), ctypes.byref(nb)), "atrex_join_workspace_bytes")
         self.workspace = torch.empty(max(int(nb.value), 256), dtype=torch.uint8, device=self.device)
@@ -667,7 +673,8 @@ class Correlator:
                                       out["key"].numel(), _ptr(source), ctypes.byref(r)), "atrex_correlate")
         L = r.labelled
         res = {k: v[:L] for k, v in out.items()}
-        res.update(source=source[:nk], labelled=L, by_source=list(r.by_source))
+        res.update(source=source[:nk], labelled=L, by_source=list(r.by_source),
+                   method={v: k for k, v in JOIN_METHODS.items()}[r.method_used])
         return res
 
 

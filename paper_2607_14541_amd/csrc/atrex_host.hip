@@ -1569,10 +1569,13 @@ namespace {
 struct JoinLayout {
   size_t ctrl, slot0, slot1, ref, flag, pos, scan_tmp, bytes;
   uint64_t cap;
+  bool part;    // the partitioned join (its buffers share the hash tables' space)
+  uint32_t bb;  // its bucket bits for max_host
 };
 
 bool join_params_ok(const atrex_join_params* p) {
-  return p && p->max_kernels < (1ull << 31) && p->max_host < (1ull << 31);
+  return p && p->max_kernels < (1ull << 31) && p->max_host < (1ull << 31) && p->method <= ATREX_JOIN_PARTITION &&
+         !(p->method == ATREX_JOIN_PARTITION && p->max_host > kJoinPartMaxHost);
 }
 
 JoinLayout join_layout(const atrex_join_params* p) {
@@ -1584,14 +1587,22 @@ JoinLayout join_layout(const atrex_join_params* p) {
     return at;
   };
   const uint64_t nk = std::max<uint64_t>(p->max_kernels, 1);
+  L.part = p->method != ATREX_JOIN_HASH && p->max_host <= kJoinPartMaxHost;
+  L.bb = join_part_bucket_bits(p->max_host);
   L.cap = next_pow2(std::max<uint64_t>(1024, 2 * p->max_host));
   L.ctrl = take(256);
-  L.slot0 = take(L.cap * 16);
-  L.slot1 = take(L.cap * 16);
   L.ref = take(nk * 4);
   L.flag = take(nk * 4);
   L.pos = take(nk * 4);
-  L.scan_tmp = take(scan_tmp_bytes(nk));
+  const uint64_t scan_n = L.part ? std::max<uint64_t>(nk, ((uint64_t)1 << L.bb) * kJoinPartWG) : nk;
+  L.scan_tmp = take(scan_tmp_bytes(scan_n));
+  // the hash tables, or in the same space the partitioned join's buffers
+  // (the hash join runs after it only when it gave up)
+  const size_t tables = align_up(L.cap * 16) * 2;
+  const size_t shared = L.part ? std::max(tables, join_part_bytes(nk, p->max_host, L.bb)) : tables;
+  const size_t at = take(shared);
+  L.slot0 = at;
+  L.slot1 = at + align_up(L.cap * 16);
   L.bytes = off;
   return L;
 }
@@ -1618,6 +1629,7 @@ atrex_status atrex_correlate(const atrex_join_params* p, const atrex_kernel_reco
   if (ni && (!iv->stream || !iv->begin_ns || !iv->end_ns || !iv->key || !iv->app || !iv->phase))
     return ATREX_E_INVALID_ARG;
   if (out_capacity && (!out->key || !out->app || !out->phase || !out->dur_ns)) return ATREX_E_INVALID_ARG;
+  if (L.part && ensure_smem_limits() != hipSuccess) return ATREX_E_DEVICE;
   char* ws = (char*)p->workspace;
   hipStream_t s = (hipStream_t)p->stream;
   JoinKernels jk{k->corr, k->anchor, k->stream, k->start_ns, k->end_ns, k->n};
@@ -1629,13 +1641,24 @@ atrex_status atrex_correlate(const atrex_join_params* p, const atrex_kernel_reco
   uint32_t* err = (uint32_t*)(ws + L.ctrl);
   unsigned long long* words = (unsigned long long*)(ws + L.ctrl + 64);
   uint32_t* flag = (uint32_t*)(ws + L.flag);
+  uint32_t* ref = (uint32_t*)(ws + L.ref);
   uint32_t* pos = (uint32_t*)(ws + L.pos);
-  launch_fill_u64(s, (uint64_t*)(ws + L.ctrl), 32, 0);
-  launch_join(s, jk, jh, ji, t, source, (uint32_t*)(ws + L.ref), flag, pos, ws + L.scan_tmp, jo, out_capacity, words,
-              err, 0);
-  launch_join(s, jk, jh, ji, t, source, (uint32_t*)(ws + L.ref), flag, pos, ws + L.scan_tmp, jo, out_capacity, words,
-              err, 1);
-  uint32_t e = 0, tail[2] = {0, 0};
+  uint32_t e = 0;
+  bool hash = !L.part;
+  if (L.part) {
+    launch_fill_u64(s, (uint64_t*)(ws + L.ctrl), 32, 0);
+    launch_join_part(s, jk, jh, ji, join_part_bucket_bits(h->n), ws + L.slot0, source, ref, flag, pos,
+                     ws + L.scan_tmp, words, err);
+    (void)hipMemcpyAsync(&e, err, 4, hipMemcpyDeviceToHost, s);
+    if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess) return ATREX_E_DEVICE;
+    hash = (e & ATREX_ERRBIT_SPILL) != 0;  // a bucket's ids did not fit its LDS tables
+  }
+  if (hash) {
+    launch_fill_u64(s, (uint64_t*)(ws + L.ctrl), 32, 0);
+    launch_join(s, jk, jh, ji, t, source, ref, flag, pos, ws + L.scan_tmp, jo, out_capacity, words, err, 0);
+  }
+  launch_join(s, jk, jh, ji, t, source, ref, flag, pos, ws + L.scan_tmp, jo, out_capacity, words, err, 1);
+  uint32_t tail[2] = {0, 0};
   uint64_t by[4] = {0, 0, 0, 0};
   (void)hipMemcpyAsync(&e, err, 4, hipMemcpyDeviceToHost, s);
   (void)hipMemcpyAsync(by, words, sizeof(by), hipMemcpyDeviceToHost, s);
@@ -1644,6 +1667,7 @@ atrex_status atrex_correlate(const atrex_join_params* p, const atrex_kernel_reco
     (void)hipMemcpyAsync(&tail[1], flag + (k->n - 1), 4, hipMemcpyDeviceToHost, s);
   }
   if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess) return ATREX_E_DEVICE;
+  r->method_used = hash ? ATREX_JOIN_HASH : ATREX_JOIN_PARTITION;
   if (e & ATREX_ERRBIT_DUP) return ATREX_E_INVALID_ARG;
   if (e & ATREX_ERRBIT_RANGE) return ATREX_E_OUT_OF_RANGE;
   r->labelled = (uint64_t)tail[0] + tail[1];

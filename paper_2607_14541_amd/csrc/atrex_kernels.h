@@ -208,11 +208,26 @@ struct JoinOut {
   uint8_t* phase;
   int64_t* dur;
 };
-// stage 0: tables, checks, probe and the scan of the flags (words[0..3]:
-// records per source); stage 1: the labelled events
+// The hash join.  stage 0: tables, checks, probe and the scan of the flags
+// (words[0..3]: records per source); stage 1: the labelled events
 void launch_join(hipStream_t s, const JoinKernels& k, const JoinHost& h, const JoinIntervals& iv,
                  const JoinTables& t, uint8_t* source, uint32_t* ref, uint32_t* flag, uint32_t* pos, void* scan_tmp,
                  const JoinOut& out, uint64_t cap, unsigned long long* words, uint32_t* err, int stage);
+// The partitioned join: 2^bb buckets of at most about kJoinBucketHost host
+// records on average (join_part_bucket_bits), so that a bucket's ids fit two
+// LDS tables; kJoinPartWG workgroups take the partition passes.  Its stage 0
+// (launch_join_part, in `part` of join_part_bytes(...) bytes; scan_tmp for
+// max(n kernel records, 2^bb * kJoinPartWG)) replaces the hash join's; a table
+// that fills up flags ATREX_ERRBIT_SPILL, and the host then runs the hash
+// join's stage 0 instead.  Stage 1 is the same.
+constexpr uint32_t kJoinPartWG = 256, kJoinBucketHost = 2048, kJoinMinBucketBits = 4, kJoinMaxBucketBits = 15;
+constexpr uint64_t kJoinPartMaxHost = (uint64_t)kJoinBucketHost << kJoinMaxBucketBits;
+uint32_t join_part_bucket_bits(uint64_t n_host);
+size_t join_part_bytes(uint64_t n_kernels, uint64_t n_host, uint32_t bb);
+void launch_join_part(hipStream_t s, const JoinKernels& k, const JoinHost& h, const JoinIntervals& iv, uint32_t bb,
+                      void* part, uint8_t* source, uint32_t* ref, uint32_t* flag, uint32_t* pos, void* scan_tmp,
+                      unsigned long long* words, uint32_t* err);
+hipError_t set_join_smem_limits();
 
 // kernels_share.hip
 hipError_t set_share_smem_limits();

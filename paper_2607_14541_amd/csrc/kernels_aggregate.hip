@@ -1331,5 +1331,7 @@ hipError_t set_kernel_smem_limits() {
   if (e != hipSuccess) return e;
   e = set_normalize_smem_limits();
   if (e != hipSuccess) return e;
+  e = set_join_smem_limits();
+  if (e != hipSuccess) return e;
   return set_rows_smem_limits();
 }

@@ -5,14 +5,21 @@
 // stream that contains their start; labelled records become the events of
 // the weighting path.
 //
-// A hash join: the host records go into two open-addressing tables in device
-// memory (one per id space, keyed by the nonzero 64-bit id, linear probing;
-// a slot is 16 bytes -- the id and the record index -- so that a probe reads
-// one 16-byte piece of one cache line),
-// one thread per kernel record probes them, and an interval is found by a
-// binary search of the intervals (ascending by (stream, begin)).  The
-// labelled records are then written in kernel-record order at positions from
-// an exclusive scan of their flags.
+// Two methods find the host record of an id:
+// - the hash join: the host records go into two open-addressing tables in
+//   device memory (one per id space, keyed by the nonzero 64-bit id, linear
+//   probing; a slot is 16 bytes -- the id and the record index -- so that a
+//   probe reads one 16-byte piece of one cache line), and one thread per
+//   kernel record probes them;
+// - the partitioned join: the host records and the probes (a kernel record's
+//   nonzero correlation id and anchor) are scattered by the top bits of the
+//   id's hash into buckets small enough for two LDS tables, and one workgroup
+//   per bucket builds its tables in LDS and answers its probes, writing the
+//   host record's index beside each kernel record.  The random global
+//   atomics and probes of the hash join become streaming passes.
+// An interval is then found by a binary search of the intervals (ascending by
+// (stream, begin)), and the labelled records are written in kernel-record
+// order at positions from an exclusive scan of their flags.
 #include "atrex_device.hpp"
 #include "atrex_kernels.h"
 
@@ -21,9 +28,8 @@ namespace {
 constexpr uint32_t kNoRef = 0xFFFFFFFFu;
 constexpr uint32_t kRefInterval = 0x80000000u;  // ref bit: the label is an interval's (indices < 2^31)
 
-__device__ __forceinline__ uint32_t id_slot(uint64_t id, uint32_t mask) {
-  return hash32((uint32_t)id ^ hash32((uint32_t)(id >> 32))) & mask;
-}
+__device__ __forceinline__ uint32_t id_hash(uint64_t id) { return hash32((uint32_t)id ^ hash32((uint32_t)(id >> 32))); }
+__device__ __forceinline__ uint32_t id_slot(uint64_t id, uint32_t mask) { return id_hash(id) & mask; }
 
 // Host records into the tables (kind 0: correlation ids, kind 1: anchors).
 // A kind above 1, an id of 0 or an id met twice in one kind flags
@@ -81,7 +87,11 @@ __device__ __forceinline__ uint32_t table_find(const uint64_t* __restrict__ slot
 // 2 interval, 3 none), the record that labels it (ref: a host record's index,
 // or an interval's index with kRefInterval), and its flag for the
 // compaction.  end < start flags ATREX_ERRBIT_RANGE.
-__global__ void k_join_probe(JoinKernels k, JoinTables t, JoinIntervals iv, uint8_t* __restrict__ source,
+// PART: the host record of each id was found by the partitioned join and
+// stands in ref0 (correlation id) and ref1 (anchor); kNoRef where none.
+template <bool PART>
+__global__ void k_join_probe(JoinKernels k, JoinTables t, const uint32_t* __restrict__ ref0,
+                             const uint32_t* __restrict__ ref1, JoinIntervals iv, uint8_t* __restrict__ source,
                              uint32_t* __restrict__ ref, uint32_t* __restrict__ flag,
                              unsigned long long* __restrict__ by, uint32_t* __restrict__ err) {
   __shared__ uint32_t s_by[4];
@@ -95,11 +105,11 @@ __global__ void k_join_probe(JoinKernels k, JoinTables t, JoinIntervals iv, uint
       atomicOr(err, ATREX_ERRBIT_RANGE);
     } else {
       const uint64_t c = k.corr[e], a = k.anchor[e];
-      if (c != 0) r = table_find(t.slot0, t.mask, c);
+      if (c != 0) r = PART ? ref0[e] : table_find(t.slot0, t.mask, c);
       if (r != kNoRef) {
         src = 0;
       } else {
-        if (a != 0) r = table_find(t.slot1, t.mask, a);
+        if (a != 0) r = PART ? ref1[e] : table_find(t.slot1, t.mask, a);
         if (r != kNoRef) {
           src = 1;
         } else if (iv.n) {
@@ -125,6 +135,169 @@ __global__ void k_join_probe(JoinKernels k, JoinTables t, JoinIntervals iv, uint
   }
   __syncthreads();
   if (threadIdx.x < 4 && s_by[threadIdx.x]) atomicAdd(&by[threadIdx.x], (unsigned long long)s_by[threadIdx.x]);
+}
+
+// ---------------------------------------------------------------------------
+// The partitioned join.  The passes over host and kernel records split them
+// into gridDim.x contiguous ranges; bucket of an id = the top bb bits of its
+// hash, slot in the bucket's LDS table = the next kJoinSlotBits bits.
+constexpr uint32_t kJoinSlotBits = 12, kJoinSlots = 1u << kJoinSlotBits;  // per id space per bucket
+
+__device__ __forceinline__ void join_range(uint64_t n, uint64_t& b, uint64_t& e) {
+  const uint64_t per = (n + gridDim.x - 1) / gridDim.x;
+  b = min(n, (uint64_t)blockIdx.x * per);
+  e = min(n, b + per);
+}
+
+// Host records per bucket (records of kind > 1 or id 0 are not counted and
+// flag ATREX_ERRBIT_DUP); H[bucket * gridDim.x + w].
+__global__ __launch_bounds__(1024) void k_jp_hist_host(JoinHost h, uint32_t bb, uint32_t* __restrict__ H,
+                                                       uint32_t* __restrict__ err) {
+  extern __shared__ uint32_t s_c[];  // [2^bb]
+  const uint32_t NB = 1u << bb, sh = 32 - bb;
+  for (uint32_t i = threadIdx.x; i < NB; i += blockDim.x) s_c[i] = 0;
+  __syncthreads();
+  uint64_t b, e;
+  join_range(h.n, b, e);
+  bool bad = false;
+  for (uint64_t j = b + threadIdx.x; j < e; j += blockDim.x) {
+    const uint32_t kind = h.kind[j];
+    const uint64_t id = h.id[j];
+    if (kind > 1 || id == 0) {
+      bad = true;
+      continue;
+    }
+    atomicAdd(&s_c[id_hash(id) >> sh], 1u);
+  }
+  if (bad) atomicOr(err, ATREX_ERRBIT_DUP);
+  __syncthreads();
+  for (uint32_t i = threadIdx.x; i < NB; i += blockDim.x) H[(size_t)i * gridDim.x + blockIdx.x] = s_c[i];
+}
+
+// The counted host records as (id, index << 1 | kind) at their bucket's
+// positions O (exclusive scan of H).
+__global__ __launch_bounds__(1024) void k_jp_scatter_host(JoinHost h, uint32_t bb, const uint32_t* __restrict__ O,
+                                                          uint64_t* __restrict__ rec) {
+  extern __shared__ uint32_t s_cur[];  // [2^bb]
+  const uint32_t NB = 1u << bb, sh = 32 - bb;
+  for (uint32_t i = threadIdx.x; i < NB; i += blockDim.x) s_cur[i] = O[(size_t)i * gridDim.x + blockIdx.x];
+  __syncthreads();
+  uint64_t b, e;
+  join_range(h.n, b, e);
+  for (uint64_t j = b + threadIdx.x; j < e; j += blockDim.x) {
+    const uint32_t kind = h.kind[j];
+    const uint64_t id = h.id[j];
+    if (kind > 1 || id == 0) continue;
+    const uint32_t pos = atomicAdd(&s_cur[id_hash(id) >> sh], 1u);
+    v2l r;
+    r.x = (long long)id;
+    r.y = (long long)(((uint64_t)j << 1) | kind);
+    *(v2l*)(rec + 2 * (size_t)pos) = r;
+  }
+}
+
+// Probes per bucket: a kernel record's nonzero correlation id (kind 0) and
+// nonzero anchor (kind 1).  end < start flags ATREX_ERRBIT_RANGE.
+__global__ __launch_bounds__(1024) void k_jp_hist_probe(JoinKernels k, uint32_t bb, uint32_t* __restrict__ H,
+                                                        uint32_t* __restrict__ err) {
+  extern __shared__ uint32_t s_c[];
+  const uint32_t NB = 1u << bb, sh = 32 - bb;
+  for (uint32_t i = threadIdx.x; i < NB; i += blockDim.x) s_c[i] = 0;
+  __syncthreads();
+  uint64_t b, e;
+  join_range(k.n, b, e);
+  bool bad = false;
+  for (uint64_t j = b + threadIdx.x; j < e; j += blockDim.x) {
+    bad |= k.end[j] < k.start[j];
+    const uint64_t c = k.corr[j], a = k.anchor[j];
+    if (c) atomicAdd(&s_c[id_hash(c) >> sh], 1u);
+    if (a) atomicAdd(&s_c[id_hash(a) >> sh], 1u);
+  }
+  if (bad) atomicOr(err, ATREX_ERRBIT_RANGE);
+  __syncthreads();
+  for (uint32_t i = threadIdx.x; i < NB; i += blockDim.x) H[(size_t)i * gridDim.x + blockIdx.x] = s_c[i];
+}
+
+__global__ __launch_bounds__(1024) void k_jp_scatter_probe(JoinKernels k, uint32_t bb, const uint32_t* __restrict__ O,
+                                                           uint64_t* __restrict__ rec) {
+  extern __shared__ uint32_t s_cur[];
+  const uint32_t NB = 1u << bb, sh = 32 - bb;
+  for (uint32_t i = threadIdx.x; i < NB; i += blockDim.x) s_cur[i] = O[(size_t)i * gridDim.x + blockIdx.x];
+  __syncthreads();
+  uint64_t b, e;
+  join_range(k.n, b, e);
+  for (uint64_t j = b + threadIdx.x; j < e; j += blockDim.x) {
+    const uint64_t ids[2] = {k.corr[j], k.anchor[j]};
+#pragma unroll
+    for (uint32_t kind = 0; kind < 2; ++kind) {
+      if (!ids[kind]) continue;
+      const uint32_t pos = atomicAdd(&s_cur[id_hash(ids[kind]) >> sh], 1u);
+      v2l r;
+      r.x = (long long)ids[kind];
+      r.y = (long long)((j << 1) | kind);
+      *(v2l*)(rec + 2 * (size_t)pos) = r;
+    }
+  }
+}
+
+// One workgroup per bucket: its host records into two LDS tables (one per id
+// space; open addressing over kJoinSlots slots, id 0 = free), then its probes
+// answered: ref0[e] / ref1[e] = the host record's index.  An id met twice in
+// a space flags ATREX_ERRBIT_DUP; a table that fills up flags
+// ATREX_ERRBIT_SPILL (the host then runs the hash join instead).  Hh/Oh and
+// Hp/Op: counts and positions of the host records and probes, [bucket][nw].
+__global__ __launch_bounds__(1024) void k_jp_bucket(const uint64_t* __restrict__ hrec, const uint32_t* __restrict__ Hh,
+                                                    const uint32_t* __restrict__ Oh, const uint64_t* __restrict__ prec,
+                                                    const uint32_t* __restrict__ Hp, const uint32_t* __restrict__ Op,
+                                                    uint32_t nw, uint32_t bb, uint32_t* __restrict__ ref0,
+                                                    uint32_t* __restrict__ ref1, uint32_t* __restrict__ err) {
+  extern __shared__ unsigned long long s_id[];                  // [2][kJoinSlots]
+  uint32_t* s_ix = (uint32_t*)(s_id + 2 * kJoinSlots);          // [2][kJoinSlots]
+  const uint32_t bk = blockIdx.x, sh = 32 - bb - kJoinSlotBits;
+  for (uint32_t i = threadIdx.x; i < 2 * kJoinSlots; i += blockDim.x) s_id[i] = 0;
+  __syncthreads();
+  const size_t c0 = (size_t)bk * nw, c1 = c0 + nw - 1;
+  const uint32_t hs = Oh[c0], he = Oh[c1] + Hh[c1];
+  bool dup = false, full = false;
+  for (uint32_t i = hs + threadIdx.x; i < he; i += blockDim.x) {
+    const uint64_t id = hrec[2 * (size_t)i], v = hrec[2 * (size_t)i + 1];
+    const uint32_t kind = (uint32_t)v & 1u;
+    unsigned long long* tid_ = s_id + kind * kJoinSlots;
+    uint32_t sl = (id_hash(id) >> sh) & (kJoinSlots - 1);
+    uint32_t probe = 0;
+    for (; probe < kJoinSlots; ++probe) {
+      const unsigned long long prev = atomicCAS(&tid_[sl], 0ull, (unsigned long long)id);
+      if (prev == 0) {
+        s_ix[kind * kJoinSlots + sl] = (uint32_t)(v >> 1);
+        break;
+      }
+      if (prev == id) {
+        dup = true;
+        break;
+      }
+      sl = (sl + 1) & (kJoinSlots - 1);
+    }
+    full |= probe == kJoinSlots;
+  }
+  if (dup) atomicOr(err, ATREX_ERRBIT_DUP);
+  if (full) atomicOr(err, ATREX_ERRBIT_SPILL);
+  __syncthreads();
+  const uint32_t ps = Op[c0], pe = Op[c1] + Hp[c1];
+  for (uint32_t i = ps + threadIdx.x; i < pe; i += blockDim.x) {
+    const uint64_t id = prec[2 * (size_t)i], v = prec[2 * (size_t)i + 1];
+    const uint32_t kind = (uint32_t)v & 1u;
+    const unsigned long long* tid_ = s_id + kind * kJoinSlots;
+    uint32_t sl = (id_hash(id) >> sh) & (kJoinSlots - 1);
+    for (uint32_t probe = 0; probe < kJoinSlots; ++probe) {
+      const unsigned long long x = tid_[sl];
+      if (x == id) {
+        (kind ? ref1 : ref0)[v >> 1] = s_ix[kind * kJoinSlots + sl];
+        break;
+      }
+      if (x == 0) break;
+      sl = (sl + 1) & (kJoinSlots - 1);
+    }
+  }
 }
 
 // The labelled records as events, in kernel-record order.
@@ -159,12 +332,72 @@ void launch_join(hipStream_t s, const JoinKernels& k, const JoinHost& h, const J
     if (iv.n)
       hipLaunchKernelGGL(k_join_check_intervals, dim3((uint32_t)((iv.n + 255) / 256)), dim3(256), 0, s, iv, err);
     if (k.n) {
-      hipLaunchKernelGGL(k_join_probe, dim3((uint32_t)((k.n + 255) / 256)), dim3(256), 0, s, k, t, iv, source, ref,
-                         flag, words, err);
+      hipLaunchKernelGGL(k_join_probe<false>, dim3((uint32_t)((k.n + 255) / 256)), dim3(256), 0, s, k, t, nullptr,
+                         nullptr, iv, source, ref, flag, words, err);
       exclusive_scan_u32(s, flag, pos, k.n, scan_tmp);
     }
   } else if (k.n) {  // the events
     hipLaunchKernelGGL(k_join_emit, dim3((uint32_t)((k.n + 255) / 256)), dim3(256), 0, s, k, h, iv, ref, flag, pos,
                        out, cap);
   }
+}
+
+uint32_t join_part_bucket_bits(uint64_t nh) {
+  uint32_t bb = kJoinMinBucketBits;
+  while (bb < kJoinMaxBucketBits && ((nh + (1ull << bb) - 1) >> bb) > kJoinBucketHost) ++bb;
+  return bb;
+}
+
+size_t join_part_bytes(uint64_t nk, uint64_t nh, uint32_t bb) {
+  const size_t m = ((size_t)1 << bb) * kJoinPartWG * 4;
+  return nh * 16 + 2 * nk * 16 + 2 * nk * 4 + 4 * m + 8 * 256;  // eight pieces, each 256-byte aligned
+}
+
+void launch_join_part(hipStream_t s, const JoinKernels& k, const JoinHost& h, const JoinIntervals& iv, uint32_t bb,
+                      void* part, uint8_t* source, uint32_t* ref, uint32_t* flag, uint32_t* pos, void* scan_tmp,
+                      unsigned long long* words, uint32_t* err) {
+  const size_t m = ((size_t)1 << bb) * kJoinPartWG;
+  char* p = (char*)part;
+  auto take = [&](size_t bytes) {
+    char* at = p;
+    p += (bytes + 255) / 256 * 256;
+    return at;
+  };
+  uint64_t* hrec = (uint64_t*)take(h.n * 16);
+  uint64_t* prec = (uint64_t*)take(2 * k.n * 16);
+  uint32_t* ref0 = (uint32_t*)take(k.n * 4);
+  uint32_t* ref1 = (uint32_t*)take(k.n * 4);
+  uint32_t* Hh = (uint32_t*)take(m * 4);
+  uint32_t* Oh = (uint32_t*)take(m * 4);
+  uint32_t* Hp = (uint32_t*)take(m * 4);
+  uint32_t* Op = (uint32_t*)take(m * 4);
+  const size_t cnt_smem = (size_t)4 << bb;
+  launch_fill_u32(s, ref0, k.n, kNoRef);
+  launch_fill_u32(s, ref1, k.n, kNoRef);
+  hipLaunchKernelGGL(k_jp_hist_host, dim3(kJoinPartWG), dim3(1024), cnt_smem, s, h, bb, Hh, err);
+  exclusive_scan_u32(s, Hh, Oh, m, scan_tmp);
+  hipLaunchKernelGGL(k_jp_scatter_host, dim3(kJoinPartWG), dim3(1024), cnt_smem, s, h, bb, Oh, hrec);
+  hipLaunchKernelGGL(k_jp_hist_probe, dim3(kJoinPartWG), dim3(1024), cnt_smem, s, k, bb, Hp, err);
+  exclusive_scan_u32(s, Hp, Op, m, scan_tmp);
+  hipLaunchKernelGGL(k_jp_scatter_probe, dim3(kJoinPartWG), dim3(1024), cnt_smem, s, k, bb, Op, prec);
+  hipLaunchKernelGGL(k_jp_bucket, dim3(1u << bb), dim3(1024), (size_t)2 * kJoinSlots * 12, s, hrec, Hh, Oh, prec, Hp,
+                     Op, kJoinPartWG, bb, ref0, ref1, err);
+  if (iv.n)
+    hipLaunchKernelGGL(k_join_check_intervals, dim3((uint32_t)((iv.n + 255) / 256)), dim3(256), 0, s, iv, err);
+  if (k.n) {
+    const JoinTables none{};
+    hipLaunchKernelGGL(k_join_probe<true>, dim3((uint32_t)((k.n + 255) / 256)), dim3(256), 0, s, k, none, ref0, ref1,
+                       iv, source, ref, flag, words, err);
+    exclusive_scan_u32(s, flag, pos, k.n, scan_tmp);
+  }
+}
+
+hipError_t set_join_smem_limits() {
+  const void* fns[] = {(const void*)k_jp_hist_host, (const void*)k_jp_scatter_host, (const void*)k_jp_hist_probe,
+                       (const void*)k_jp_scatter_probe, (const void*)k_jp_bucket};
+  for (const void* f : fns) {
+    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 128 * 1024);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }

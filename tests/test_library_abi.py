@@ -96,6 +96,21 @@ def test_join_parameters(lib):
     p = X._JoinParams(1 << 20, 1 << 20, None, 0, None)
     b = ctypes.c_size_t()
     assert lib.atrex_join_workspace_bytes(ctypes.byref(p), ctypes.byref(b)) == 0 and b.value > 0
+    sizes = {}
+    for name, m in X.JOIN_METHODS.items():
+        p.method = m
+        assert lib.atrex_join_workspace_bytes(ctypes.byref(p), ctypes.byref(b)) == 0
+        sizes[name] = b.value
+    assert sizes["auto"] == sizes["partition"] >= sizes["hash"]
+    p.method = 3  # no such method
+    assert lib.atrex_join_workspace_bytes(ctypes.byref(p), ctypes.byref(b)) == X.E_INVALID_ARG
+    p.method, p.max_host = X.JOIN_METHODS["partition"], (2048 << 15) + 1  # beyond the partitioned join's buckets
+    assert lib.atrex_join_workspace_bytes(ctypes.byref(p), ctypes.byref(b)) == X.E_INVALID_ARG
+    p.method = X.JOIN_METHODS["auto"]  # takes the hash join there: the hash join's workspace
+    assert lib.atrex_join_workspace_bytes(ctypes.byref(p), ctypes.byref(b)) == 0
+    auto_big = b.value
+    p.method = X.JOIN_METHODS["hash"]
+    assert lib.atrex_join_workspace_bytes(ctypes.byref(p), ctypes.byref(b)) == 0 and b.value == auto_big
     p.max_kernels = 1 << 31
     assert lib.atrex_join_workspace_bytes(ctypes.byref(p), ctypes.byref(b)) == X.E_INVALID_ARG
     assert lib.atrex_correlate(None, None, None, None, None, 0, None, None) == X.E_INVALID_ARG
