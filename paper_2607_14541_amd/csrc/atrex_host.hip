@@ -451,10 +451,19 @@ hipError_t ensure_smem_limits() {
   return e;
 }
 
+// ATREX_E_DEVICE, with the HIP error and where it was met on stderr (device
+// errors are rare and otherwise carry no detail through the status code).
+atrex_status device_error(hipError_t e, const char* where) {
+  fprintf(stderr, "atrex: HIP error %d (%s) at %s\n", (int)e, hipGetErrorString(e), where);
+  return ATREX_E_DEVICE;
+}
+
 atrex_status sync_status(atrex_ctx* c) {
   const hipError_t e1 = hipGetLastError();
   const hipError_t e2 = hipStreamSynchronize(c->s);
-  return (e1 == hipSuccess && e2 == hipSuccess) ? ATREX_OK : ATREX_E_DEVICE;
+  if (e1 != hipSuccess) return device_error(e1, "a launch or call before the synchronisation");
+  if (e2 != hipSuccess) return device_error(e2, "stream synchronisation");
+  return ATREX_OK;
 }
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
@@ -486,8 +495,14 @@ atrex_status wait_published(atrex_ctx* c, uint32_t seq) {
     if (__atomic_load_n(done, __ATOMIC_ACQUIRE) == seq) return ATREX_OK;
     if (spin % 256 == 0) {
       const hipError_t q = hipStreamQuery(c->s);
-      if (q == hipSuccess) return __atomic_load_n(done, __ATOMIC_ACQUIRE) == seq ? ATREX_OK : ATREX_E_DEVICE;
-      if (q != hipErrorNotReady) return ATREX_E_DEVICE;
+      if (q == hipSuccess) {
+        // the stream has finished: the completion word is written; read it
+        // again after a synchronisation before calling its absence an error
+        const hipError_t e = hipStreamSynchronize(c->s);
+        if (e == hipSuccess && __atomic_load_n(done, __ATOMIC_ACQUIRE) == seq) return ATREX_OK;
+        return device_error(e != hipSuccess ? e : hipErrorUnknown, "completion word of the status readback");
+      }
+      if (q != hipErrorNotReady) return device_error(q, "stream query while waiting for the status readback");
     }
     __builtin_ia32_pause();
   }
@@ -510,9 +525,10 @@ atrex_status sync_read(atrex_ctx* c) {
     if (++c->publish_seq == 0) c->publish_seq = 1;  // 0 is the buffer's initial value
     launch_publish(c->s, pl, c->pinned_dev, c->pinned_dev + kDoneOff / 4, c->publish_seq);
     const bool poll = !c->plain_copies && !(c->flags & ATREX_FLAG_TIMING);
-    if (hipGetLastError() != hipSuccess) {
+    const hipError_t le = hipGetLastError();
+    if (le != hipSuccess) {
       (void)hipStreamSynchronize(c->s);
-      st = ATREX_E_DEVICE;
+      st = device_error(le, "a launch or call before the status readback");
     } else {
       st = poll ? wait_published(c, c->publish_seq) : sync_status(c);
     }

@@ -121,3 +121,34 @@ def test_hot_scatter_reserved_key_and_range_error():
         assert G == o["key"].size
     finally:
         ag.close()
+
+
+@pytest.mark.parametrize("P", [1, 8])
+def test_hot_scatter_phases_wide_durations_and_general_scale_words(P):
+    """The hot scatter at 1 and 8 phases (Zipf(1.0) over 64k keys: the
+    seeded image covers between half and 15/16 of the sample), with a tenth
+    of the durations at 2^32 or more (the 64-bit share) and one application
+    of weight 1 among weights 2^32 - 1 with durations near 2^62, whose scale
+    exponent falls below -8 (the general scale word)."""
+    import math
+    rng = np.random.default_rng(40 + P)
+    n, A = (1 << 22) + 13, 1000
+    w = np.arange(1, 65537, dtype=float) ** -1.0
+    cdf = np.cumsum(w) / w.sum()
+    ids = rng.permutation(1 << 24)[:65536].astype(np.uint32) * np.uint32(131) + np.uint32(7)
+    key = ids[np.minimum(np.searchsorted(cdf, rng.random(n)), 65535)]
+    app = rng.integers(0, A, n).astype(np.uint32)
+    ph = rng.integers(0, P, n).astype(np.uint8)
+    dur = rng.lognormal(math.log(3e4), 2.0, n).astype(np.int64)
+    big = rng.random(n) < 0.1
+    dur[big] = rng.integers(1 << 32, 1 << 40, int(big.sum()))
+    c = np.full(A, 2 ** 32 - 1, np.uint32)
+    c[0] = 1
+    z = app == 0
+    dur[z] = rng.integers(1 << 60, 1 << 62, int(z.sum()))
+    H.say("hot scatter, P", P)
+    o = O.run(key, app, ph, dur, c, P, threads=8)
+    assert o["rho"].min() < -8
+    g = H.run_gpu(key, app, ph, dur, c, P, raw=False, max_keys=65536, max_groups=65536 * P)
+    assert g["path"] == "hot_scatter", g["path"]
+    H.compare(g, o, raw=False)
