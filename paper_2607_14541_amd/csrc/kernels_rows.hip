@@ -843,8 +843,11 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter_hot(PartSource src, u
       const int64_t dd = ev.dur[jj];
       const bool ok = a < A && ph < P && dd >= 0;
       bad |= vj && !ok;
-      sw[j] = ok ? bscale[a * P + ph] : 0;
-      dv[j] = ok ? (uint64_t)dd : 0;
+      // a lane past the range (its event zero-filled) and an invalid event
+      // take the zero scale word (no share): every share below, hot or not,
+      // is formed, and the general scale word's path re-reads the event
+      sw[j] = (vj && ok) ? bscale[a * P + ph] : 0;
+      dv[j] = (vj && ok) ? (uint64_t)dd : 0;
       rk[j] = ok ? ph : 0u;
       hs[j] = vj ? image_slot(s_tag, S, key) : kNoSlot;
       if (vj && hs[j] == kNoSlot) rk[j] |= 8u;
@@ -933,8 +936,8 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter_hot(PartSource src, u
           bscale_share64(d, (uint32_t)wv, (uint32_t)(wv >> 32), vl[j], vh[j]);
         }
       } else {  // rho outside [-8, 63] (rare): the general scale word, found again from the event
-        const uint64_t i = t0 + 4 * ((uint64_t)(j / 4) * SC_BLOCK + tid) + (j % 4);
-        const u128 x = event_share(d, scale[app_at<false>(src.ev.app, i) * P + ph]);
+        const uint64_t i = t0 + 4 * ((uint64_t)(j / 4) * SC_BLOCK + tid) + (j % 4);  // < e: sw != 0 above
+        const u128 x = i < e ? event_share(d, scale[app_at<false>(src.ev.app, i) * P + ph]) : (u128)0;
         vl[j] = (uint64_t)x;
         vh[j] = (uint64_t)(x >> 64);
       }
