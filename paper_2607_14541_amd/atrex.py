@@ -576,6 +576,14 @@ def aggregate(key, app, phase, dur_ns, app_weight_q16, num_phases, path="auto", 
         ag.close()
 
 
+def score(ctx: "Aggregator", score_key, s) -> float:
+    """S_agg of Eq. (6) (§3.6) for an Aggregator whose group-by and
+    normalisation have run: score_key (u32 keys) and s (fp64 S_j, NaN = not
+    correct) as device tensors.  Repeatable; ctx.score() also returns the
+    per-operator weights and medians."""
+    return ctx.score(score_key, s)["s_agg"]
+
+
 def target_share(key, is_dsl, dur_ns, path="auto", max_keys=0) -> dict:
     """The target-DSL device-time share of one profile (§4.1, Metrics) in one
     call: the device-time group-by with phase = is_dsl (1 inside the target

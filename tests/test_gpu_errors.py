@@ -75,6 +75,9 @@ def test_call_order():
     ag.normalize()
     r = ag.score(k, torch.tensor([0.5, 0.25], dtype=torch.float64, device="cuda"))
     assert r["op"].numel() == 1
+    # the module-level form returns the same S_agg (keys 1 and 2 are one
+    # operator: the median of 0.5 and 0.25, weight 1)
+    assert X.score(ag, k, torch.tensor([0.5, 0.25], dtype=torch.float64, device="cuda")) == r["s_agg"] == 0.375
     ag.close()
 
 
