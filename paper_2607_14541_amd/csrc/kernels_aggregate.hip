@@ -829,9 +829,12 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
                      (uint64_t)g.dur[j], err);
       }
     }
-    // hot group: when at least half the lanes share the first lane's (slot,
-    // phase) in the first event slot, lanes sharing a group are summed with
-    // shuffles first (a milder skew costs less as LDS atomic conflicts)
+    // hot groups: when at least half the lanes share the first lane's (slot,
+    // phase) in the first event slot, up to two groups are taken off the
+    // atomics: each lane sums its own events of the group, the wave sums the
+    // lanes, and one lane adds the total once (a hot key split over two
+    // phases would otherwise put half the wave on one LDS address).  A
+    // milder skew costs less as LDS atomic conflicts.
     bool hot = false;
     {
       const uint64_t act = __ballot(gi[0] != INVALID_GI);
@@ -842,30 +845,36 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
       }
     }
     if (hot) {
+#pragma unroll 1
+      for (int r = 0; r < 2; ++r) {
+        // the group of the first lane's first remaining event (in the first
+        // round, the one that made the wave hot)
+        const uint32_t first = gi[0] != INVALID_GI ? gi[0]
+                             : gi[1] != INVALID_GI ? gi[1]
+                             : gi[2] != INVALID_GI ? gi[2] : gi[3];
+        const uint64_t act = __ballot(first != INVALID_GI);
+        if (act == 0) break;
+        const uint32_t lead = __builtin_amdgcn_readlane(first, __ffsll((unsigned long long)act) - 1);
+        uint32_t cnt = 0;
+        u128 sv = 0, sr = 0;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint64_t act = __ballot(gi[j] != INVALID_GI);
-        if (act == 0) continue;
-        const uint32_t fl = __ffsll((unsigned long long)act) - 1;
-        const uint32_t lead = __builtin_amdgcn_readlane(gi[j], fl);
-        const uint64_t same = __ballot(gi[j] == lead);
-        if (__popcll(same) < 16) continue;
-        const bool mine = gi[j] == lead;
-        const u128 tot = wave_sum_u128(mine ? make_u128(vlo[j], vhi[j]) : (u128)0);
+        for (int j = 0; j < 4; ++j) {
+          const bool m = gi[j] == lead;
+          cnt += (uint32_t)__popcll(__ballot(m));
+          sv += m ? make_u128(vlo[j], vhi[j]) : (u128)0;
+          if (RAW) sr += m ? (u128)(uint64_t)g.dur[j] : (u128)0;
+        }
+        if (cnt < 32) break;  // wave-uniform
+        const u128 tot = wave_sum_u128(sv);  // lane 0
         u128 rtot = 0;
-        if (RAW) rtot = wave_sum_u128(mine ? (u128)(uint64_t)g.dur[j] : (u128)0);
-        const uint64_t tlo = __shfl((unsigned long long)(uint64_t)tot, 0, 64);
-        const uint64_t thi = __shfl((unsigned long long)(uint64_t)(tot >> 64), 0, 64);
-        uint64_t rlo = 0, rhi = 0;
-        if (RAW) {
-          rlo = __shfl((unsigned long long)(uint64_t)rtot, 0, 64);
-          rhi = __shfl((unsigned long long)(uint64_t)(rtot >> 64), 0, 64);
+        if (RAW) rtot = wave_sum_u128(sr);
+        if (lane == 0) {
+          acc_add_n(&s_lo[lead], &s_hi[lead], tot, cnt);
+          if (RAW) acc_add_plain(&s_rlo[lead], &s_rhi[lead], rtot);
         }
-        if (lane == fl) {
-          acc_add_n(&s_lo[lead], &s_hi[lead], make_u128(tlo, thi), __popcll(same));
-          if (RAW) acc_add_plain(&s_rlo[lead], &s_rhi[lead], make_u128(rlo, rhi));
-        }
-        if (mine) gi[j] = INVALID_GI;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (gi[j] == lead) gi[j] = INVALID_GI;
       }
     }
     // accumulate without branches: a lane with nothing to add for an event
