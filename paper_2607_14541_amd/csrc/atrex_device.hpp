@@ -223,6 +223,33 @@ __device__ __forceinline__ u128 wave_sum_u128(u128 v) {
   return v;  // valid in lane 0
 }
 
+// Sum over the 64 lanes of a wave, returned in every lane, of a u32 whose
+// total fits in 32 bits: an inclusive scan by DPP (row shifts by 1, 2, 4 and
+// 8 lanes within each row of 16, then the broadcasts of lanes 15 and 31 into
+// the rows after them) leaves the total in lane 63.  Every lane of the wave
+// must be active.
+__device__ __forceinline__ uint32_t wave_total_u32(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15 into rows 1, 3
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31 into rows 2, 3
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+}
+
+// Wave total of a u128 below 2^98 per lane, in every lane: four 26-bit limbs,
+// whose sums over 64 lanes stay below 2^32, summed with wave_total_u32.
+__device__ __forceinline__ u128 wave_total_u98(u128 v) {
+  const uint32_t M = (1u << 26) - 1;
+  const uint64_t lo = (uint64_t)v, hi = (uint64_t)(v >> 64);
+  const uint32_t l0 = wave_total_u32((uint32_t)lo & M);
+  const uint32_t l1 = wave_total_u32((uint32_t)(lo >> 26) & M);
+  const uint32_t l2 = wave_total_u32((uint32_t)((lo >> 52) | (hi << 12)) & M);
+  const uint32_t l3 = wave_total_u32((uint32_t)(hi >> 14));
+  return (u128)l0 + ((u128)l1 << 26) + ((u128)l2 << 52) + ((u128)l3 << 78);
+}
+
 // Accumulate a share into a two-word accumulator (global or LDS) with
 // 64-bit atomics: the low word's carry is detected from the returned value.
 template <typename Ptr>

@@ -865,7 +865,7 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
           if (RAW) sr += m ? (u128)(uint64_t)g.dur[j] : (u128)0;
         }
         if (cnt < 32) break;  // wave-uniform
-        const u128 tot = wave_sum_u128(sv);  // lane 0
+        const u128 tot = wave_total_u98(sv);  // sv < 2^98: four shares of at most 2^96
         u128 rtot = 0;
         if (RAW) rtot = wave_sum_u128(sr);
         if (lane == 0) {
