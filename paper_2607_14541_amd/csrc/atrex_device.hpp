@@ -223,19 +223,24 @@ __device__ __forceinline__ u128 wave_sum_u128(u128 v) {
   return v;  // valid in lane 0
 }
 
-// Sum over the 64 lanes of a wave, returned in every lane, of a u32 whose
-// total fits in 32 bits: an inclusive scan by DPP (row shifts by 1, 2, 4 and
-// 8 lanes within each row of 16, then the broadcasts of lanes 15 and 31 into
-// the rows after them) leaves the total in lane 63.  Every lane of the wave
-// must be active.
-__device__ __forceinline__ uint32_t wave_total_u32(uint32_t x) {
+// Inclusive scan over the 64 lanes of a wave (lane i gets x_0 + ... + x_i)
+// by DPP: row shifts by 1, 2, 4 and 8 lanes within each row of 16, then the
+// broadcasts of lane 15 into rows 1 and 3 and of lane 31 into rows 2 and 3.
+// Every lane of the wave must be active.
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t x) {
   x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false);  // row_shr:1
   x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false);  // row_shr:2
   x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false);  // row_shr:4
   x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false);  // row_shr:8
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15 into rows 1, 3
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31 into rows 2, 3
-  return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return x;
+}
+
+// Sum over the 64 lanes of a wave of a u32 whose total fits in 32 bits,
+// returned in every lane (lane 63 of the inclusive scan).
+__device__ __forceinline__ uint32_t wave_total_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan_u32(x), 63);
 }
 
 // Wave total of a u128 below 2^98 per lane, in every lane: four 26-bit limbs,

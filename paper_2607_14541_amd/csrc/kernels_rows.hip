@@ -691,11 +691,7 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint3
         }
       }
       const uint32_t lane = tid & 63, wave = tid >> 6;
-      uint32_t inc = sum;
-      for (int dd = 1; dd < 64; dd <<= 1) {
-        const uint32_t y = __shfl_up(inc, dd, 64);
-        if (lane >= (uint32_t)dd) inc += y;
-      }
+      const uint32_t inc = wave_incl_scan_u32(sum);
       if (lane == 63) s_w[wave] = inc;
       __syncthreads();
       uint32_t off = 0;
@@ -876,11 +872,7 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter_hot(PartSource src, u
         }
       }
       const uint32_t wave = tid >> 6;
-      uint32_t inc = sum;
-      for (int dd = 1; dd < 64; dd <<= 1) {
-        const uint32_t y = __shfl_up(inc, dd, 64);
-        if (lane >= (uint32_t)dd) inc += y;
-      }
+      const uint32_t inc = wave_incl_scan_u32(sum);
       if (lane == 63) s_w[wave] = inc;
       __syncthreads();
       uint32_t off = 0;
