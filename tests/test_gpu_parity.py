@@ -211,3 +211,49 @@ def test_negative_scale_exponents(path):
     assert o["rho"].min() < -8
     H.say("negative scale exponents", path)
     H.compare(H.run_gpu(key, app, ph, dur, c, P, path=path, max_groups=2 * n, max_keys=n), o)
+
+
+@pytest.mark.parametrize("raw", [False, True])
+@pytest.mark.parametrize("case", ["two_phases", "two_keys_two_phases", "one_phase", "hot_then_cold"])
+def test_hot_groups_summed_across_the_wave(case, raw):
+    """The LDS engine's hot groups: when at least half of a wave's lanes share
+    the (key, phase) of the first lane's first event, up to two groups are
+    summed per lane and then across the wave, the rest go to LDS atomics.
+    two_phases: one key in two phases (70/30), both groups summed;
+    two_keys_two_phases: four hot groups, two summed, two by atomics;
+    one_phase: P = 1; hot_then_cold: the second group is a cold key, which
+    ends the rounds.  1% of the durations are 2^32 ns or more (the wide share
+    path)."""
+    rng = np.random.default_rng({"two_phases": 1, "two_keys_two_phases": 2, "one_phase": 3,
+                                 "hot_then_cold": 4}[case])
+    n = (1 << 21) + 37
+    u = rng.random(n)
+    cold = 100 + rng.integers(0, 1000, n)
+    if case == "two_phases":
+        P = 2
+        key = np.where(u < 0.95, 7, cold)
+        ph = (rng.random(n) < 0.3).astype(np.int64)
+    elif case == "two_keys_two_phases":
+        P = 2
+        key = np.select([u < 0.70, u < 0.95], [7, 9], cold)
+        ph = np.select([u < 0.55, u < 0.70, u < 0.85, u < 0.95], [0, 1, 0, 1], rng.integers(0, P, n))
+    elif case == "one_phase":
+        P = 1
+        key = np.where(u < 0.9, 7, cold)
+        ph = np.zeros(n, np.int64)
+    else:
+        P = 3
+        key = np.where(u < 0.7, 7, cold)
+        ph = np.where(u < 0.7, 1, rng.integers(0, P, n))
+    A = 16
+    app = rng.integers(0, A, n)
+    dur = rng.integers(1, 1 << 20, n)
+    wide = rng.random(n) < 0.01
+    dur[wide] = rng.integers(1 << 32, 1 << 40, int(wide.sum()))
+    c = rng.integers(1, 1 << 20, A)
+    H.say("hot groups", case, "raw", raw, "n", n)
+    g = H.run_gpu(key, app, ph, dur, c, P, path="lds_hash", raw=raw, max_keys=1002, max_groups=1002 * P)
+    assert g["path"] == "lds_hash", g["path"]
+    o = O.run(key.astype(np.uint32), app.astype(np.uint32), ph.astype(np.uint8), dur.astype(np.int64), c, P,
+              threads=8)
+    H.compare(g, o, raw=raw)
