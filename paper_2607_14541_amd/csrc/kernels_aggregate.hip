@@ -1032,7 +1032,7 @@ __global__ void k_unpack_scale(const uint64_t* __restrict__ sw, uint64_t G, uint
 // ---------------------------------------------------------------------------
 // Seeding the LDS engine with the hottest keys.  A sample of NS events at a
 // fixed stride counts its keys in a global table (open addressing, key + 1,
-// 0 = free); the occupied entries become sort keys (the inverted count:
+// 0 = free; each workgroup's share counted in LDS first); the occupied entries become sort keys (the inverted count:
 // ascending = hottest first, ties in table order); one workgroup then places the
 // hottest 2S keys, 1024 at a time in that order, into a tag image of S slots,
 // each in the first free slot of its window (home bucket and the next, or its
@@ -1042,30 +1042,65 @@ __global__ void k_unpack_scale(const uint64_t* __restrict__ sw, uint64_t G, uint
 // result.
 constexpr uint32_t kSeedCountBits = 19, kSeedCountMask = (1u << kSeedCountBits) - 1;
 
-__global__ void k_seed_count(const uint32_t* __restrict__ key, uint64_t n, uint32_t NS,
-                             unsigned long long* __restrict__ tab, uint32_t mask, uint32_t* __restrict__ cnt) {
-  const uint32_t s = blockIdx.x * blockDim.x + threadIdx.x;
-  const bool in = s < NS;
-  const uint32_t k = in ? key[(uint64_t)s * n / NS] : ATREX_EMPTY_KEY;
-  const bool live = in && k != ATREX_EMPTY_KEY;  // the reserved tag is never seeded
-  // the lanes sharing the wave's first key count it with one atomic (a key
-  // that dominates the events would otherwise serialise the wave on one slot)
-  const uint64_t act = __ballot(live);
-  if (act == 0) return;
-  const uint32_t lead = (uint32_t)__ffsll((unsigned long long)act) - 1;
-  const uint32_t k0 = __builtin_amdgcn_readlane(k, lead);
-  const uint64_t same = __ballot(live && k == k0);
-  const bool first = (threadIdx.x & 63) == lead;
-  if (!live || (k == k0 && !first)) return;
-  const uint32_t add = k == k0 ? (uint32_t)__popcll(same) : 1u;
-  uint32_t h = hash32(k) & mask;
-  for (uint32_t probe = 0; probe <= mask; ++probe) {  // the table has at least twice NS slots
-    const unsigned long long prev = atomicCAS(&tab[h], 0ull, (unsigned long long)k + 1);
-    if (prev == 0 || prev == (unsigned long long)k + 1) {
-      atomicAdd(&cnt[h], add);
-      return;
+// Each workgroup counts kSeedPerWG sampled events in an LDS table (the lanes
+// of a wave sharing the wave's first key add once), then adds each distinct
+// key to the global table once, with its count: a key that dominates the
+// events costs one global atomic per workgroup instead of one per sample
+// (atomics on one address serialise).
+constexpr uint32_t kSeedPerWG = 2048, kSeedLdsSlots = 4096;
+
+__global__ __launch_bounds__(1024) void k_seed_count(const uint32_t* __restrict__ key, uint64_t n, uint32_t NS,
+                                                     unsigned long long* __restrict__ tab, uint32_t mask,
+                                                     uint32_t* __restrict__ cnt) {
+  __shared__ uint32_t s_key[kSeedLdsSlots], s_cnt[kSeedLdsSlots];
+  const uint32_t tid = threadIdx.x, lane = tid & 63;
+  for (uint32_t i = tid; i < kSeedLdsSlots; i += 1024) {
+    s_key[i] = ATREX_EMPTY_KEY;
+    s_cnt[i] = 0;
+  }
+  constexpr uint32_t PER = kSeedPerWG / 1024;
+  uint32_t kk[PER];
+#pragma unroll
+  for (uint32_t j = 0; j < PER; ++j) {
+    const uint32_t s = blockIdx.x * kSeedPerWG + j * 1024 + tid;
+    kk[j] = s < NS ? key[(uint64_t)s * n / NS] : ATREX_EMPTY_KEY;
+  }
+  __syncthreads();
+#pragma unroll
+  for (uint32_t j = 0; j < PER; ++j) {
+    const uint32_t k = kk[j];
+    const bool live = k != ATREX_EMPTY_KEY;  // the reserved tag is never seeded
+    const uint64_t act = __ballot(live);
+    if (act == 0) continue;  // wave-uniform
+    const uint32_t lead = (uint32_t)__ffsll((unsigned long long)act) - 1;
+    const uint32_t k0 = __builtin_amdgcn_readlane(k, lead);
+    const uint64_t same = __ballot(live && k == k0);
+    if (live && (k != k0 || lane == lead)) {
+      const uint32_t add = k == k0 ? (uint32_t)__popcll(same) : 1u;
+      uint32_t h = hash32(k) & (kSeedLdsSlots - 1);
+      for (uint32_t probe = 0; probe < kSeedLdsSlots; ++probe) {  // at most kSeedPerWG of the slots are taken
+        const uint32_t prev = atomicCAS(&s_key[h], ATREX_EMPTY_KEY, k);
+        if (prev == ATREX_EMPTY_KEY || prev == k) {
+          atomicAdd(&s_cnt[h], add);
+          break;
+        }
+        h = (h + 1) & (kSeedLdsSlots - 1);
+      }
     }
-    h = (h + 1) & mask;
+  }
+  __syncthreads();
+  for (uint32_t i = tid; i < kSeedLdsSlots; i += 1024) {
+    const uint32_t k = s_key[i];
+    if (k == ATREX_EMPTY_KEY) continue;
+    uint32_t h = hash32(k) & mask;
+    for (uint32_t probe = 0; probe <= mask; ++probe) {  // the table has at least twice NS slots
+      const unsigned long long prev = atomicCAS(&tab[h], 0ull, (unsigned long long)k + 1);
+      if (prev == 0 || prev == (unsigned long long)k + 1) {
+        atomicAdd(&cnt[h], s_cnt[i]);
+        break;
+      }
+      h = (h + 1) & mask;
+    }
   }
 }
 
@@ -1143,8 +1178,8 @@ void launch_seed(hipStream_t s, const uint32_t* key, uint64_t n, uint32_t NS, ui
                  uint32_t S, uint32_t* seed, unsigned long long* covered) {
   launch_fill_u64(s, tab, tab_cap, 0);
   launch_fill_u32(s, cnt, tab_cap, 0);
-  hipLaunchKernelGGL(k_seed_count, dim3((NS + 255) / 256), dim3(256), 0, s, key, n, NS, (unsigned long long*)tab,
-                     tab_cap - 1, cnt);
+  hipLaunchKernelGGL(k_seed_count, dim3((NS + kSeedPerWG - 1) / kSeedPerWG), dim3(1024), 0, s, key, n, NS,
+                     (unsigned long long*)tab, tab_cap - 1, cnt);
   hipLaunchKernelGGL(k_seed_list, dim3((tab_cap + 255) / 256), dim3(256), 0, s, (const unsigned long long*)tab, cnt,
                      tab_cap, list, idx);
   radix_sort_pairs(s, list, idx, list2, idx2, tab_cap, kSeedCountBits, sort_tmp);  // hottest first, free last
