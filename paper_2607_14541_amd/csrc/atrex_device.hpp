@@ -357,10 +357,14 @@ typedef long long v2l __attribute__((ext_vector_type(2)));
 
 // Four consecutive events starting at a multiple of 4 (16-byte aligned SoA),
 // with 16-byte non-temporal vector loads.
+// The four phases stay packed, one byte each, until used: unpacking them
+// right after the load would wait for it, and (loads completing in order)
+// for every load issued before it.
 struct Ev4 {
   uint32_t key[4], app[4];
-  uint32_t ph[4];
+  uint32_t ph4;
   int64_t dur[4];
+  __device__ __forceinline__ uint32_t ph(int j) const { return (ph4 >> (8 * j)) & 0xFFu; }
 };
 
 // NO_APP: the events carry no application (plain device-time group-by);
@@ -378,7 +382,7 @@ __device__ __forceinline__ void load4(const uint32_t* __restrict__ key, const ui
   const v2l d0 = __builtin_nontemporal_load((const v2l*)(dur + i));
   const v2l d1 = __builtin_nontemporal_load((const v2l*)(dur + i + 2));
   e.app[0] = a.x; e.app[1] = a.y; e.app[2] = a.z; e.app[3] = a.w;
-  e.ph[0] = p & 0xFF; e.ph[1] = (p >> 8) & 0xFF; e.ph[2] = (p >> 16) & 0xFF; e.ph[3] = p >> 24;
+  e.ph4 = p;
   e.dur[0] = d0.x; e.dur[1] = d0.y; e.dur[2] = d1.x; e.dur[3] = d1.y;
 }
 
@@ -396,7 +400,7 @@ __device__ __forceinline__ void load4_lane(const uint32_t* __restrict__ key, con
   const v2l d1 = __builtin_nontemporal_load((const v2l*)(dur + e0) + 2 * lane + 1);
   e.key[0] = k.x; e.key[1] = k.y; e.key[2] = k.z; e.key[3] = k.w;
   e.app[0] = a.x; e.app[1] = a.y; e.app[2] = a.z; e.app[3] = a.w;
-  e.ph[0] = p & 0xFF; e.ph[1] = (p >> 8) & 0xFF; e.ph[2] = (p >> 16) & 0xFF; e.ph[3] = p >> 24;
+  e.ph4 = p;
   e.dur[0] = d0.x; e.dur[1] = d0.y; e.dur[2] = d1.x; e.dur[3] = d1.y;
 }
 

@@ -61,7 +61,7 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_lds(EventsDev ev, uint32_t A, 
     nxt = nxt2;
     if (q + 2 * stride < n4) load4<false>(ev.key, ev.app, ev.phase, ev.dur, (q + 2 * stride) * 4, nxt2);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) one(e.app[j], e.ph[j], e.dur[j]);
+    for (int j = 0; j < 4; ++j) one(e.app[j], e.ph(j), e.dur[j]);
   }
   if (blockIdx.x == 0)  // tail events
     for (uint64_t i = n4 * 4 + threadIdx.x; i < n; i += BLOCK) one(ev.app[i], ev.phase[i], ev.dur[i]);
@@ -113,7 +113,7 @@ __global__ __launch_bounds__(BLOCK) void k_pass_a_lds32(EventsDev ev, uint32_t A
     const Ev4 e = nxt;
     if (q + stride < n4) load4<false>(ev.key, ev.app, ev.phase, ev.dur, (q + stride) * 4, nxt);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) one(e.app[j], e.ph[j], e.dur[j]);
+    for (int j = 0; j < 4; ++j) one(e.app[j], e.ph(j), e.dur[j]);
   }
   if (blockIdx.x == 0)
     for (uint64_t i = n4 * 4 + threadIdx.x; i < n; i += BLOCK) one(ev.app[i], ev.phase[i], ev.dur[i]);
@@ -727,11 +727,11 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
   auto stage = [&](const Ev4& e, StagedEv4& g) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      g.sw[j] = bscale[__umul24(e.app[j], P) + e.ph[j]];
+      g.sw[j] = bscale[__umul24(e.app[j], P) + e.ph(j)];
       g.key[j] = e.key[j];
       g.dur[j] = e.dur[j];
     }
-    g.ph4 = e.ph[0] | (e.ph[1] << 8) | (e.ph[2] << 16) | (e.ph[3] << 24);
+    g.ph4 = e.ph4;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const uint32_t k = e.key[j], b = home_bucket(k);
@@ -746,7 +746,7 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
       w = t0.y == k ? 1u : w;
       w = t0.x == k ? 0u : w;
       const bool hit = w != INVALID_GI && k != ATREX_EMPTY_KEY;
-      g.gi[j] = hit ? __umul24(4 * b + w, P) + e.ph[j] : INVALID_GI;
+      g.gi[j] = hit ? __umul24(4 * b + w, P) + e.ph(j) : INVALID_GI;
     }
   };
   // The waves of the workgroup claim the blocks of its share one at a time
@@ -951,9 +951,10 @@ __global__ __launch_bounds__(BLOCK) void k_pass_b_lds(EventsDev ev, uint32_t P, 
     const uint64_t i = n4 * 4 + lane;
     Ev4 e;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) { e.key[j] = ATREX_EMPTY_KEY; e.app[j] = 0; e.ph[j] = 0; e.dur[j] = 0; }
+    for (int j = 0; j < 4; ++j) { e.key[j] = ATREX_EMPTY_KEY; e.app[j] = 0; e.dur[j] = 0; }
+    e.ph4 = 0;
     if (i < n) {
-      e.key[0] = ev.key[i]; e.app[0] = app_at<NO_APP>(ev.app, i); e.ph[0] = ev.phase[i]; e.dur[0] = ev.dur[i];
+      e.key[0] = ev.key[i]; e.app[0] = app_at<NO_APP>(ev.app, i); e.ph4 = ev.phase[i]; e.dur[0] = ev.dur[i];
     }
     StagedEv4 g;
     stage(e, g);

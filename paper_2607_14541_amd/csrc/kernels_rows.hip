@@ -581,12 +581,13 @@ __device__ __forceinline__ void load_group(const EventsDev& ev, uint64_t q, uint
   if (q + 3 < e) {  // q is a multiple of 4: a whole, 16-byte aligned group
     load4<true, NO_APP>(ev.key, ev.app, ev.phase, ev.dur, q, x);
   } else {
+    x.ph4 = 0;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const bool in = q + j < e;
       x.key[j] = in ? ev.key[q + j] : 0;
       x.app[j] = in ? app_at<NO_APP>(ev.app, q + j) : 0;
-      x.ph[j] = in ? ev.phase[q + j] : 0;
+      x.ph4 |= (in ? (uint32_t)ev.phase[q + j] : 0u) << (8 * j);
       x.dur[j] = in ? ev.dur[q + j] : 0;
     }
   }
@@ -661,7 +662,7 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter(PartSource src, uint3
       } else {
         const Ev4& ev = evg[j / 4];
         const uint32_t jj = j % 4;
-        const uint32_t a = ev.app[jj], ph = ev.ph[jj];
+        const uint32_t a = ev.app[jj], ph = ev.ph(jj);
         const int64_t dd = ev.dur[jj];
         const bool ok = a < A && ph < P && dd >= 0;
         bad |= vj && !ok;
@@ -835,7 +836,7 @@ __global__ __launch_bounds__(SC_BLOCK) void k_part_scatter_hot(PartSource src, u
       const bool vj = i < e;
       const Ev4& ev = evg[j / 4];
       const uint32_t jj = j % 4;
-      const uint32_t a = ev.app[jj], ph = ev.ph[jj], key = ev.key[jj];
+      const uint32_t a = ev.app[jj], ph = ev.ph(jj), key = ev.key[jj];
       const int64_t dd = ev.dur[jj];
       const bool ok = a < A && ph < P && dd >= 0;
       bad |= vj && !ok;
