@@ -89,15 +89,33 @@ __device__ __forceinline__ uint32_t table_find(const uint64_t* __restrict__ slot
 // compaction.  end < start flags ATREX_ERRBIT_RANGE.
 // PART: the host record of each id was found by the partitioned join and
 // stands in ref0 (correlation id) and ref1 (anchor); kNoRef where none.
+// The records that need an interval (about a tenth) are gathered in LDS and
+// searched by the workgroup's first waves, all lanes busy, instead of by a
+// few lanes of every wave.
+constexpr uint32_t kProbeBlock = 1024;
+
 template <bool PART>
-__global__ void k_join_probe(JoinKernels k, JoinTables t, const uint32_t* __restrict__ ref0,
-                             const uint32_t* __restrict__ ref1, JoinIntervals iv, uint8_t* __restrict__ source,
-                             uint32_t* __restrict__ ref, uint32_t* __restrict__ flag,
-                             unsigned long long* __restrict__ by, uint32_t* __restrict__ err) {
-  __shared__ uint32_t s_by[4];
+__global__ __launch_bounds__(kProbeBlock) void k_join_probe(JoinKernels k, JoinTables t,
+                                                            const uint32_t* __restrict__ ref0,
+                                                            const uint32_t* __restrict__ ref1, JoinIntervals iv,
+                                                            uint8_t* __restrict__ source, uint32_t* __restrict__ ref,
+                                                            uint32_t* __restrict__ flag,
+                                                            unsigned long long* __restrict__ by,
+                                                            uint32_t* __restrict__ err) {
+  __shared__ uint32_t s_by[4], s_nt;
+  __shared__ uint32_t s_task[kProbeBlock];  // the block's records that need an interval search
   if (threadIdx.x < 4) s_by[threadIdx.x] = 0;
+  if (threadIdx.x == 0) s_nt = 0;
   __syncthreads();
-  const uint64_t e = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const uint64_t e0 = (uint64_t)blockIdx.x * kProbeBlock;
+  const uint64_t e = e0 + threadIdx.x;
+  auto label = [&](uint64_t i, uint32_t src, uint32_t r) {
+    if (source) source[i] = (uint8_t)src;
+    ref[i] = r;
+    flag[i] = src < 3 ? 1u : 0u;
+    atomicAdd(&s_by[src], 1u);
+  };
+  bool search = false;
   if (e < k.n) {
     const int64_t st = k.start[e], en = k.end[e];
     uint32_t src = 3, r = kNoRef;
@@ -110,28 +128,37 @@ __global__ void k_join_probe(JoinKernels k, JoinTables t, const uint32_t* __rest
         src = 0;
       } else {
         if (a != 0) r = PART ? ref1[e] : table_find(t.slot1, t.mask, a);
-        if (r != kNoRef) {
-          src = 1;
-        } else if (iv.n) {
-          // the last interval with (stream, begin) <= (stream, start)
-          const uint32_t sm = k.stream[e];
-          uint64_t lo = 0, hi = iv.n;  // answer in [lo - 1, hi - 1]
-          while (lo < hi) {
-            const uint64_t mid = (lo + hi) / 2;
-            const uint32_t ms = iv.stream[mid];
-            if (ms < sm || (ms == sm && iv.begin[mid] <= st)) lo = mid + 1; else hi = mid;
-          }
-          if (lo > 0 && iv.stream[lo - 1] == sm && st < iv.end[lo - 1]) {
-            src = 2;
-            r = (uint32_t)(lo - 1) | kRefInterval;
-          }
-        }
+        if (r != kNoRef) src = 1;
+        else search = iv.n != 0;
       }
     }
-    if (source) source[e] = (uint8_t)src;
-    ref[e] = r;
-    flag[e] = src < 3 ? 1u : 0u;
-    atomicAdd(&s_by[src], 1u);
+    if (!search) label(e, src, r);
+  }
+  {  // wave-aggregated append to the block's search list
+    const uint64_t bm = __ballot(search);
+    if (bm) {
+      const uint32_t lane = threadIdx.x & 63, leader = __ffsll((unsigned long long)bm) - 1;
+      uint32_t base = 0;
+      if (lane == leader) base = atomicAdd(&s_nt, (uint32_t)__popcll(bm));
+      base = __shfl(base, leader, 64);
+      if (search) s_task[base + __popcll(bm & ((1ull << lane) - 1ull))] = threadIdx.x;
+    }
+  }
+  __syncthreads();
+  const uint32_t nt = s_nt;
+  for (uint32_t q = threadIdx.x; q < nt; q += kProbeBlock) {
+    const uint64_t i = e0 + s_task[q];
+    const int64_t st = k.start[i];
+    const uint32_t sm = k.stream[i];
+    // the last interval with (stream, begin) <= (stream, start)
+    uint64_t lo = 0, hi = iv.n;  // answer in [lo - 1, hi - 1]
+    while (lo < hi) {
+      const uint64_t mid = (lo + hi) / 2;
+      const uint32_t ms = iv.stream[mid];
+      if (ms < sm || (ms == sm && iv.begin[mid] <= st)) lo = mid + 1; else hi = mid;
+    }
+    const bool in = lo > 0 && iv.stream[lo - 1] == sm && st < iv.end[lo - 1];
+    label(i, in ? 2u : 3u, in ? ((uint32_t)(lo - 1) | kRefInterval) : kNoRef);
   }
   __syncthreads();
   if (threadIdx.x < 4 && s_by[threadIdx.x]) atomicAdd(&by[threadIdx.x], (unsigned long long)s_by[threadIdx.x]);
@@ -332,8 +359,8 @@ void launch_join(hipStream_t s, const JoinKernels& k, const JoinHost& h, const J
     if (iv.n)
       hipLaunchKernelGGL(k_join_check_intervals, dim3((uint32_t)((iv.n + 255) / 256)), dim3(256), 0, s, iv, err);
     if (k.n) {
-      hipLaunchKernelGGL(k_join_probe<false>, dim3((uint32_t)((k.n + 255) / 256)), dim3(256), 0, s, k, t, nullptr,
-                         nullptr, iv, source, ref, flag, words, err);
+      hipLaunchKernelGGL(k_join_probe<false>, dim3((uint32_t)((k.n + kProbeBlock - 1) / kProbeBlock)),
+                         dim3(kProbeBlock), 0, s, k, t, nullptr, nullptr, iv, source, ref, flag, words, err);
       exclusive_scan_u32(s, flag, pos, k.n, scan_tmp);
     }
   } else if (k.n) {  // the events
@@ -386,8 +413,8 @@ void launch_join_part(hipStream_t s, const JoinKernels& k, const JoinHost& h, co
     hipLaunchKernelGGL(k_join_check_intervals, dim3((uint32_t)((iv.n + 255) / 256)), dim3(256), 0, s, iv, err);
   if (k.n) {
     const JoinTables none{};
-    hipLaunchKernelGGL(k_join_probe<true>, dim3((uint32_t)((k.n + 255) / 256)), dim3(256), 0, s, k, none, ref0, ref1,
-                       iv, source, ref, flag, words, err);
+    hipLaunchKernelGGL(k_join_probe<true>, dim3((uint32_t)((k.n + kProbeBlock - 1) / kProbeBlock)),
+                       dim3(kProbeBlock), 0, s, k, none, ref0, ref1, iv, source, ref, flag, words, err);
     exclusive_scan_u32(s, flag, pos, k.n, scan_tmp);
   }
 }
