@@ -508,22 +508,33 @@ __global__ __launch_bounds__(1024) void k_select_hist(const uint32_t* __restrict
   __syncthreads();
   const uint32_t nd = s_nd, lane = threadIdx.x & 63;
   const int top = shift + 8;  // bits at and above `top` must equal the prefix
-  const uint32_t steps = (ce - cb + 1023) / 1024;  // uniform over the workgroup: wave ballots below
+  // four values per thread and step, loaded before the first is counted
+  const uint32_t steps = (ce - cb + 4095) / 4096;  // uniform over the workgroup: wave ballots below
   for (uint32_t st = 0; st < steps; ++st) {
-    const uint32_t x = cb + st * 1024 + threadIdx.x;
-    const bool in = x < ce;
-    const uint64_t v = in ? (uint64_t)vals[x] : 0;
-    const uint64_t above = top >= 64 ? 0 : v >> top;
-    const uint32_t dg = (uint32_t)(v >> shift) & 255u;
-    for (uint32_t k = 0; k < nd; ++k) {
-      const bool m = in && above == s_p[k];
-      const uint64_t act = __ballot(m);
-      if (act == 0) continue;  // wave-uniform
-      const uint32_t lead = (uint32_t)__ffsll((unsigned long long)act) - 1;
-      const uint32_t d0 = __builtin_amdgcn_readlane(dg, lead);
-      const uint64_t same = __ballot(m && dg == d0);
-      if (lane == lead) atomicAdd(&s_h[k * 256 + d0], (uint32_t)__popcll(same));
-      else if (m && dg != d0) atomicAdd(&s_h[k * 256 + dg], 1u);
+    uint64_t vv[4];
+    bool inv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t x = cb + st * 4096 + (uint32_t)u * 1024 + threadIdx.x;
+      inv[u] = x < ce;
+      vv[u] = inv[u] ? (uint64_t)vals[x] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const bool in = inv[u];
+      const uint64_t v = vv[u];
+      const uint64_t above = top >= 64 ? 0 : v >> top;
+      const uint32_t dg = (uint32_t)(v >> shift) & 255u;
+      for (uint32_t k = 0; k < nd; ++k) {
+        const bool m = in && above == s_p[k];
+        const uint64_t act = __ballot(m);
+        if (act == 0) continue;  // wave-uniform
+        const uint32_t lead = (uint32_t)__ffsll((unsigned long long)act) - 1;
+        const uint32_t d0 = __builtin_amdgcn_readlane(dg, lead);
+        const uint64_t same = __ballot(m && dg == d0);
+        if (lane == lead) atomicAdd(&s_h[k * 256 + d0], (uint32_t)__popcll(same));
+        else if (m && dg != d0) atomicAdd(&s_h[k * 256 + dg], 1u);
+      }
     }
   }
   __syncthreads();
