@@ -1033,14 +1033,14 @@ __global__ void k_unpack_scale(const uint64_t* __restrict__ sw, uint64_t G, uint
 // ---------------------------------------------------------------------------
 // Seeding the LDS engine with the hottest keys.  A sample of NS events at a
 // fixed stride counts its keys in a global table (open addressing, key + 1,
-// 0 = free; each workgroup's share counted in LDS first); the occupied entries become sort keys (the inverted count:
-// ascending = hottest first, ties in table order); one workgroup then places the
-// hottest 2S keys, 1024 at a time in that order, into a tag image of S slots,
-// each in the first free slot of its window (home bucket and the next, or its
-// own bucket only; a key whose window is full is left out), and counts the
-// sampled events the placed
-// keys cover.  Which keys are seeded changes only which events spill, never a
-// result.
+// 0 = free; each workgroup's share counted in LDS first); the occupied
+// entries become sort keys (the inverted count: ascending = hottest first,
+// ties in table order); one workgroup then places the hottest 2S keys, 1024
+// at a time in that order, into a tag image of S slots, each in the first
+// free slot of its window (home bucket and the next, or its own bucket only;
+// a key whose window is full is left out), and counts the sampled events the
+// placed keys cover.  Which keys are seeded changes only which events spill,
+// never a result.
 constexpr uint32_t kSeedCountBits = 19, kSeedCountMask = (1u << kSeedCountBits) - 1;
 
 // Each workgroup counts kSeedPerWG sampled events in an LDS table (the lanes
